@@ -1,0 +1,112 @@
+"""Seeded synthetic inputs for the selective diagonal SSM layer.
+
+This module only draws random tensors with the shapes and value distributions
+of the layer workloads; it holds none of the gradient arithmetic, and both the
+HIP path and the oracle read the very tensors it returns (the oracle after an
+exact upcast to fp64).
+
+Workloads (b batch, T length, D channels, N state, d_model, window Tbar):
+
+=======  ====  =========  =====  ==  =======  =====  =====  ========
+name     b     T          D      N   d_model  Tbar   proj   dtype
+=======  ====  =========  =====  ==  =======  =====  =====  ========
+small    1     256        64     16  64       32     no     fp32
+layer    2     4,096      1536   16  768      --     yes    bf16
+long     2     65,536     1536   16  768      2048   yes    bf16
+slice    1     262,144    4096   16  2048     4096   yes    bf16
+vlong    1     1,048,576  3072   16  --       8192   no     bf16
+=======  ====  =========  =====  ==  =======  =====  =====  ========
+
+Distributions: x ~ N(0,1); Delta = softplus(N(0,1)) (drawn as Delta_pre ~ N(0,1)
+when the layer applies the softplus itself); A_log ~ U(log 1, log 16) per (d, n);
+upstream gradient ~ N(0,1); B, C ~ N(0, 1/N) without projections and N(0,1) with
+them (the marginals of x W_B with W_B ~ N(0, 1/fan_in)).  With projections the
+stored activations x, z, Delta_pre, B, C are drawn directly from those marginals
+(rather than computed from u and the weights), u ~ N(0,1), and
+W ~ N(0, 1/fan_in).  ``delta_scale`` < 1 gives the slow-decay variants in which
+the truncation window is visible (Delta / 32 for "small", Delta / 2048 for "long").
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import torch
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    b: int
+    T: int
+    D: int
+    N: int
+    d_model: int
+    tbar: int           # 0: full gradient only
+    proj: bool          # input projections and SiLU gate
+    bf16: bool          # bf16 inputs (else fp32)
+    seed: int
+    delta_scale: float = 1.0
+
+    @property
+    def M(self) -> int:
+        return self.b * self.T
+
+    def with_(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+WORKLOADS = {
+    "small": Workload("small", 1, 256, 64, 16, 64, 32, False, False, 692000),
+    "layer": Workload("layer", 2, 4096, 1536, 16, 768, 0, True, True, 692001),
+    "long": Workload("long", 2, 65536, 1536, 16, 768, 2048, True, True, 692002),
+    "slice": Workload("slice", 1, 262144, 4096, 16, 2048, 4096, True, True, 692003),
+    "vlong": Workload("vlong", 1, 1048576, 3072, 16, 1536, 8192, False, True, 692004),
+}
+WORKLOADS["small_slow"] = WORKLOADS["small"].with_(name="small_slow", delta_scale=1.0 / 32)
+WORKLOADS["long_slow"] = WORKLOADS["long"].with_(name="long_slow", proj=False, delta_scale=1.0 / 2048)
+
+
+def make_inputs(w: Workload, device="cpu", seed: int | None = None, h0: bool = False):
+    """Draw the inputs of one gradient call.
+
+    Returns a dict of tensors on ``device``: ``x, delta, A_log, B, C, dy`` and, with
+    projections, ``z, u, W_x, W_in``; ``h0`` when asked.  ``delta`` holds Delta_pre
+    (the layer applies softplus) when ``w.proj`` and Delta itself otherwise.
+    Activations are bf16 (round-to-nearest-even from fp32) or fp32; ``A_log`` and
+    ``h0`` are fp32.
+    """
+    g = torch.Generator(device=device)
+    g.manual_seed(w.seed if seed is None else seed)
+    dt = torch.bfloat16 if w.bf16 else torch.float32
+    b, T, D, N = w.b, w.T, w.D, w.N
+
+    def randn(*shape, std=1.0):
+        t = torch.randn(*shape, generator=g, device=device, dtype=torch.float32)
+        return t.mul_(std) if std != 1.0 else t
+
+    out = {}
+    out["x"] = randn(b, T, D).to(dt)
+    pre = randn(b, T, D)
+    if w.proj:
+        out["delta"] = pre.to(dt)
+    else:
+        d = torch.nn.functional.softplus(pre)
+        if w.delta_scale != 1.0:
+            d.mul_(w.delta_scale)
+        out["delta"] = d.to(dt)
+    del pre
+    out["A_log"] = (torch.rand(D, N, generator=g, device=device, dtype=torch.float32)
+                    .mul_(math.log(16.0)))
+    bc_std = 1.0 if w.proj else 1.0 / math.sqrt(N)
+    out["B"] = randn(b, T, N, std=bc_std).to(dt)
+    out["C"] = randn(b, T, N, std=bc_std).to(dt)
+    out["dy"] = randn(b, T, D).to(dt)
+    if w.proj:
+        out["z"] = randn(b, T, D).to(dt)
+        out["u"] = randn(b, T, w.d_model).to(dt)
+        out["W_x"] = randn(D, D + 2 * N, std=1.0 / math.sqrt(D)).to(dt)
+        out["W_in"] = randn(w.d_model, 2 * D, std=1.0 / math.sqrt(w.d_model)).to(dt)
+    if h0:
+        out["h0"] = randn(b, D, N)
+    return out
