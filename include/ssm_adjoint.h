@@ -1,0 +1,168 @@
+/*
+ * ssm_adjoint.h -- C ABI of the MI355X (gfx950) per-layer adjoint-gradient
+ * library for a selective diagonal state-space layer.
+ *
+ * The operation ("Adjoint sharding for very long context training of state
+ * space models", arXiv 2501.00692):
+ *   Sec. 3.1 (the five SSM steps), specialised to a diagonal, input-dependent
+ *   decay with D channels of N states each:
+ *     a_t[d,n] = exp(-Delta_t[d] * exp(A_log[d,n]))
+ *     h_t[d,n] = a_t[d,n] * h_{t-1}[d,n] + B_t[n] * x_t[d]      (h_{-1} = h0, or 0)
+ *     y_t[d]   = sum_n C_t[n] * h_t[d,n]
+ *   optional: Delta = softplus(Delta_pre) (SSM_DELTA_SOFTPLUS) and a SiLU output
+ *   gate out_t = y_t * silu(z_t) (SSM_GATE_SILU).
+ *   Prop. 2 (one layer): the gradient of L = sum_{b,t,d} dy_t[d] * out_t[d]
+ *   splits into vector-Jacobian products of the A, B and C maps weighted by the
+ *   adjoint states lambda^{t,i} = C^t A^t ... A^{i+1}; summed over the loss terms
+ *   t these are the adjoint mu_i = sum_{t>=i} g_t lambda^{t,i}.
+ *   Eq. "capped" (Sec. 4.3): the truncated form keeps, for every t, only the
+ *   steps i in [t+1-Tbar, t] in the A and B terms; the C term is never truncated.
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE pointers owned by the caller.  The library
+ *     never allocates or frees device memory; scratch comes from the caller's
+ *     `workspace` (size from the matching *_workspace_size query, 256-byte
+ *     aligned pointer).
+ *   - Layouts are row-major and contiguous: x, delta, z, dy, y, dx, ddelta, dz
+ *     are [batch][seqlen][channels]; B, C, dB, dC are [batch][seqlen][dstate];
+ *     A_log and dA_log are [channels][dstate]; h0, h_last, dh0 are
+ *     [batch][channels][dstate].
+ *   - "in_dtype" tensors are fp32 or bf16 (bit pattern of the upper 16 bits of
+ *     an fp32); every gradient output is fp32 and is overwritten.
+ *   - Every call validates its arguments on the host first; on any error it
+ *     returns a non-zero status, enqueues nothing and leaves the outputs
+ *     untouched.  On success the work is enqueued on `stream` (a hipStream_t;
+ *     NULL is the default stream) and the call returns without synchronising;
+ *     asynchronous faults surface at the caller's next synchronisation.
+ *   - Results are deterministic: fixed-order reductions, no float atomics.
+ *   - ssm_last_error() returns a thread-local description of the last failure.
+ */
+#ifndef SSM_ADJOINT_H
+#define SSM_ADJOINT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SSM_OK = 0,
+    SSM_ERR_NULL = 1,        /* a required pointer is NULL                      */
+    SSM_ERR_SHAPE = 2,       /* a size is out of range or inconsistent           */
+    SSM_ERR_DTYPE = 3,       /* unknown dtype code                               */
+    SSM_ERR_UNSUPPORTED = 4, /* valid request this build does not implement      */
+    SSM_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the query says    */
+    SSM_ERR_ALIGN = 6,       /* a pointer is not aligned as documented           */
+    SSM_ERR_HIP = 7          /* the HIP runtime reported an error at launch       */
+} ssm_status;
+
+typedef enum { SSM_F32 = 0, SSM_BF16 = 1 } ssm_dtype;
+typedef enum { SSM_FULL = 0, SSM_TRUNCATED = 1 } ssm_mode;
+
+/* ssm_desc.flags */
+#define SSM_DELTA_SOFTPLUS 1u /* `delta` holds Delta_pre; Delta = softplus(Delta_pre),
+                                 and `ddelta` is the gradient w.r.t. Delta_pre          */
+#define SSM_GATE_SILU 2u      /* `z` present: out = y * silu(z); `dy` is dL/dout        */
+
+/* ssm_proj_grad flags */
+#define SSM_ACCUM_DW 1u       /* dW += X^T dZ instead of dW = X^T dZ                   */
+#define SSM_ACCUM_DX 2u       /* dX += dZ W^T instead of dX = dZ W^T                   */
+
+typedef struct {
+    int64_t batch;    /* b >= 1                                                     */
+    int64_t seqlen;   /* T >= 1                                                     */
+    int64_t channels; /* D >= 1 (the paper's P for a diagonal layer)                */
+    int64_t dstate;   /* N, 1..16                                                   */
+    int64_t chunk;    /* L, time steps per carry chunk: 0 (default 128), or one of
+                         16, 32, 64, 128, 256.  Results do not depend on it beyond
+                         rounding.                                                  */
+    int32_t in_dtype; /* ssm_dtype of x, delta, B, C, z, dy (and of y)              */
+    uint32_t flags;   /* SSM_DELTA_SOFTPLUS | SSM_GATE_SILU                         */
+} ssm_desc;
+
+/* Workspace bytes needed by ssm_adjoint_forward / ssm_adjoint_grad for `desc`
+ * (and `mode`, `tbar`).  Returns SSM_OK and writes *bytes, or an error status. */
+ssm_status ssm_adjoint_forward_workspace_size(const ssm_desc* desc, size_t* bytes);
+ssm_status ssm_adjoint_grad_workspace_size(const ssm_desc* desc, int32_t mode, int64_t tbar,
+                                           size_t* bytes);
+
+/* Forward pass (Sec. 3.1 steps 4-5, with the state recomputed chunk by chunk and
+ * never stored per step).
+ *   x, delta, B, C : in_dtype inputs;  A_log : fp32 [D][N];
+ *   h0     : fp32 [b][D][N] initial state, or NULL for zero;
+ *   z      : in_dtype gate input, required iff SSM_GATE_SILU;
+ *   y      : in_dtype output [b][T][D] (y, or y * silu(z) with the gate);
+ *   h_last : fp32 [b][D][N] final state, or NULL. */
+ssm_status ssm_adjoint_forward(const ssm_desc* desc, const void* x, const void* delta,
+                               const float* A_log, const void* B, const void* C, const float* h0,
+                               const void* z, void* y, float* h_last, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* Per-layer adjoint gradient (Prop. 2; with mode SSM_TRUNCATED the estimator of
+ * Eq. "capped" with window `tbar` >= 1, where tbar >= T is the full gradient).
+ * Inputs as for the forward, plus dy (in_dtype [b][T][D]) = dL/dout.
+ * Outputs (fp32, overwritten):
+ *   dx     [b][T][D]  B-path cotangent summed over the state, sum_n mubar B_t[n]
+ *   ddelta [b][T][D]  dL/dDelta, or dL/dDelta_pre with SSM_DELTA_SOFTPLUS
+ *   dA_log [D][N]
+ *   dB, dC [b][T][N]  (dC is never truncated)
+ *   dz     [b][T][D]  required iff SSM_GATE_SILU, else must be NULL
+ *   dh0    [b][D][N]  dL/dh0, full mode only (must be NULL when truncating), or NULL.
+ * Truncation reuses the full adjoint: mubar_i = mu_i - P(i, i+tbar) mu_{i+tbar}
+ * with P(i, j) = prod_{k=i+1}^{j} a_k. */
+ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
+                            const void* delta, const float* A_log, const void* B, const void* C,
+                            const float* h0, const void* z, const void* dy, float* dx,
+                            float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
+                            float* dh0, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Projection gradients of a linear map Z = X W (Sec. 4.5: the A, B, C networks
+ * are single-layer maps; the per-step vjps summed over t give these products):
+ *   dW [K][Nout] (fp32)  = X^T dZ      (skipped if dW == NULL)
+ *   dX [M][K]    (fp32)  = dZ W^T      (skipped if dX == NULL; needs W)
+ * X: bf16 [M][K] with row stride ldx >= K; dZ: bf16 [M][Nout], stride lddz >= Nout;
+ * W: bf16 [K][Nout], stride ldw >= Nout.  flags: SSM_ACCUM_DW / SSM_ACCUM_DX.
+ * bf16 operands, fp32 accumulation (MFMA).  Strides are in elements and must be
+ * multiples of 8; pointers 16-byte aligned. */
+ssm_status ssm_proj_grad_workspace_size(int64_t M, int64_t K, int64_t Nout, uint32_t flags,
+                                        size_t* bytes);
+ssm_status ssm_proj_grad(int64_t M, int64_t K, int64_t Nout, const void* X, int64_t ldx,
+                         const void* dZ, int64_t lddz, const void* W, int64_t ldw, float* dW,
+                         float* dX, uint32_t flags, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/* Whole-layer gradient for a layer with input projections (bf16 activations):
+ *   [x | z] = u W_in,   [Delta_pre | B | C] = x W_x,   Delta = softplus(Delta_pre),
+ *   out = y * silu(z).
+ * Given the stored activations u [M][d_model], x, z, delta_pre [M][D], B, C [M][N]
+ * (M = b*T rows), the weights W_x [D][D+2N] and W_in [d_model][2D] (bf16), A_log and
+ * the upstream dy = dL/dout, it computes the scan gradient (as ssm_adjoint_grad with
+ * SSM_DELTA_SOFTPLUS | SSM_GATE_SILU; desc->flags is ignored), then
+ *   dZx = [dDelta_pre | dB | dC]            (bf16, internal)
+ *   dW_x = x^T dZx                           fp32 [D][D+2N]
+ *   dx_total = dx + dZx W_x^T                fp32 [M][D] (optional output)
+ *   dW_in = u^T [dx_total | dz]              fp32 [d_model][2D]
+ *   du = [dx_total | dz] W_in^T              fp32 [M][d_model] (optional; needs W_in)
+ * The per-token scan gradients dx, ddelta, dB, dC, dz may be given (fp32 outputs)
+ * or NULL (kept in the workspace).  dA_log, dW_x and dW_in are required. */
+ssm_status ssm_layer_grad_workspace_size(const ssm_desc* desc, int32_t mode, int64_t tbar,
+                                         int64_t d_model, size_t* bytes);
+ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int64_t d_model,
+                          const void* u, const void* x, const void* z, const void* delta_pre,
+                          const void* B, const void* C, const void* W_x, const void* W_in,
+                          const float* A_log, const void* dy, float* dW_in, float* dW_x,
+                          float* dA_log, float* du, float* dx, float* ddelta, float* dB,
+                          float* dC, float* dz, float* dx_total, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/* Thread-local, NUL-terminated description of the last non-OK status returned on
+ * the calling thread ("" if none).  Owned by the library. */
+const char* ssm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSM_ADJOINT_H */

@@ -1,0 +1,284 @@
+"""MI355X (gfx950) per-layer adjoint gradient of a selective diagonal SSM layer.
+
+Thin ctypes binding over the C ABI in ``include/ssm_adjoint.h`` (library
+``libssm_adjoint.so`` in this package directory).  The functions here only
+marshal arguments: they check tensors, allocate outputs and workspace with
+torch, and call the C entry point of the same name on torch's current stream.
+Every step of the computation runs in the library's HIP kernels; there is no
+other implementation behind this module, and it raises if the library is not
+built.
+
+Entry points (names as in the C ABI): :func:`ssm_adjoint_forward`,
+:func:`ssm_adjoint_grad`, :func:`ssm_proj_grad`, :func:`ssm_layer_grad`.
+"""
+from __future__ import annotations
+
+import ctypes
+from pathlib import Path
+
+import torch
+
+_PKG = Path(__file__).resolve().parent
+LIB_PATH = _PKG / "libssm_adjoint.so"
+
+SSM_F32, SSM_BF16 = 0, 1
+SSM_FULL, SSM_TRUNCATED = 0, 1
+SSM_DELTA_SOFTPLUS, SSM_GATE_SILU = 1, 2
+SSM_ACCUM_DW, SSM_ACCUM_DX = 1, 2
+
+STATUS = {0: "SSM_OK", 1: "SSM_ERR_NULL", 2: "SSM_ERR_SHAPE", 3: "SSM_ERR_DTYPE",
+          4: "SSM_ERR_UNSUPPORTED", 5: "SSM_ERR_WORKSPACE", 6: "SSM_ERR_ALIGN", 7: "SSM_ERR_HIP"}
+
+EXPORTED = (
+    "ssm_adjoint_forward_workspace_size", "ssm_adjoint_grad_workspace_size", "ssm_adjoint_forward",
+    "ssm_adjoint_grad", "ssm_proj_grad_workspace_size", "ssm_proj_grad",
+    "ssm_layer_grad_workspace_size", "ssm_layer_grad", "ssm_last_error",
+)
+
+
+class SsmError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class SsmDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64), ("channels", ctypes.c_int64),
+                ("dstate", ctypes.c_int64), ("chunk", ctypes.c_int64), ("in_dtype", ctypes.c_int32),
+                ("flags", ctypes.c_uint32)]
+
+
+_lib = None
+
+
+def load_library():
+    """Load ``libssm_adjoint.so``; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not LIB_PATH.exists():
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2501_00692_amd.build` "
+                           "(there is no fallback implementation)")
+    lib = ctypes.CDLL(str(LIB_PATH))
+    vp, i64, i32, u32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_size_t
+    dp = ctypes.POINTER(SsmDesc)
+    szp = ctypes.POINTER(ctypes.c_size_t)
+    sig = {
+        "ssm_adjoint_forward_workspace_size": [dp, szp],
+        "ssm_adjoint_grad_workspace_size": [dp, i32, i64, szp],
+        "ssm_adjoint_forward": [dp] + [vp] * 9 + [vp, sz, vp],
+        "ssm_adjoint_grad": [dp, i32, i64] + [vp] * 15 + [vp, sz, vp],
+        "ssm_proj_grad_workspace_size": [i64, i64, i64, u32, szp],
+        "ssm_proj_grad": [i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, vp, u32, vp, sz, vp],
+        "ssm_layer_grad_workspace_size": [dp, i32, i64, i64, szp],
+        "ssm_layer_grad": [dp, i32, i64, i64] + [vp] * 20 + [vp, sz, vp],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = ctypes.c_int
+    lib.ssm_last_error.argtypes = []
+    lib.ssm_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load_library().ssm_last_error().decode()
+
+
+def _check(rc: int, where: str):
+    if rc != 0:
+        raise SsmError(rc, where, last_error())
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return SSM_F32
+    if t.dtype == torch.bfloat16:
+        return SSM_BF16
+    raise TypeError(f"activations must be float32 or bfloat16, got {t.dtype}")
+
+
+def _need(t, name, dtype=None, shape=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def make_desc(x: torch.Tensor, N: int, softplus=False, gate=False, chunk=0) -> SsmDesc:
+    b, T, D = x.shape
+    flags = (SSM_DELTA_SOFTPLUS if softplus else 0) | (SSM_GATE_SILU if gate else 0)
+    return SsmDesc(b, T, D, N, chunk, _dtype_code(x), flags)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns blocks aligned to at least 512 bytes
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def grad_workspace_size(desc: SsmDesc, tbar: int = 0) -> int:
+    n = ctypes.c_size_t()
+    mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
+    _check(load_library().ssm_adjoint_grad_workspace_size(ctypes.byref(desc), mode, int(tbar), ctypes.byref(n)),
+           "ssm_adjoint_grad_workspace_size")
+    return n.value
+
+
+def ssm_adjoint_forward(x, delta, A_log, B, C, h0=None, z=None, softplus=False, chunk=0, want_h_last=False,
+                        workspace=None):
+    """Forward pass; returns ``y`` (and ``h_last`` if asked).  ``y`` has x's dtype."""
+    lib = load_library()
+    dt = x.dtype
+    b, T, D = x.shape
+    N = A_log.shape[1]
+    _need(x, "x", dt)
+    _need(delta, "delta", dt, (b, T, D))
+    _need(A_log, "A_log", torch.float32, (D, N))
+    _need(B, "B", dt, (b, T, N))
+    _need(C, "C", dt, (b, T, N))
+    _need(h0, "h0", torch.float32, (b, D, N))
+    _need(z, "z", dt, (b, T, D))
+    desc = make_desc(x, N, softplus, z is not None, chunk)
+    n = ctypes.c_size_t()
+    _check(lib.ssm_adjoint_forward_workspace_size(ctypes.byref(desc), ctypes.byref(n)),
+           "ssm_adjoint_forward_workspace_size")
+    ws = workspace if workspace is not None else _workspace(n.value, x.device)
+    y = torch.empty_like(x)
+    h_last = torch.empty(b, D, N, dtype=torch.float32, device=x.device) if want_h_last else None
+    _check(lib.ssm_adjoint_forward(ctypes.byref(desc), _p(x), _p(delta), _p(A_log), _p(B), _p(C), _p(h0), _p(z),
+                                   _p(y), _p(h_last), _p(ws), ws.numel(), _stream()), "ssm_adjoint_forward")
+    return (y, h_last) if want_h_last else y
+
+
+def ssm_adjoint_grad(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False, tbar=0, chunk=0,
+                     want_dh0=False, out=None, workspace=None):
+    """Per-layer adjoint gradient.  ``tbar > 0`` selects the truncated form.
+
+    Returns a dict with fp32 ``dx, ddelta, dA_log, dB, dC`` (+ ``dz`` with a gate,
+    ``dh0`` if asked).  ``out`` may hold preallocated outputs under the same keys."""
+    lib = load_library()
+    dt = x.dtype
+    b, T, D = x.shape
+    N = A_log.shape[1]
+    _need(x, "x", dt)
+    _need(delta, "delta", dt, (b, T, D))
+    _need(A_log, "A_log", torch.float32, (D, N))
+    _need(B, "B", dt, (b, T, N))
+    _need(C, "C", dt, (b, T, N))
+    _need(dy, "dy", dt, (b, T, D))
+    _need(h0, "h0", torch.float32, (b, D, N))
+    _need(z, "z", dt, (b, T, D))
+    desc = make_desc(x, N, softplus, z is not None, chunk)
+    mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
+    dev = x.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    o = dict(out) if out else {}
+    o.setdefault("dx", torch.empty(b, T, D, **f32))
+    o.setdefault("ddelta", torch.empty(b, T, D, **f32))
+    o.setdefault("dA_log", torch.empty(D, N, **f32))
+    o.setdefault("dB", torch.empty(b, T, N, **f32))
+    o.setdefault("dC", torch.empty(b, T, N, **f32))
+    if z is not None:
+        o.setdefault("dz", torch.empty(b, T, D, **f32))
+    if want_dh0:
+        o.setdefault("dh0", torch.empty(b, D, N, **f32))
+    ws = workspace if workspace is not None else _workspace(grad_workspace_size(desc, tbar), dev)
+    _check(lib.ssm_adjoint_grad(ctypes.byref(desc), mode, int(tbar), _p(x), _p(delta), _p(A_log), _p(B), _p(C),
+                                _p(h0), _p(z), _p(dy), _p(o["dx"]), _p(o["ddelta"]), _p(o["dA_log"]), _p(o["dB"]),
+                                _p(o["dC"]), _p(o.get("dz")), _p(o.get("dh0")), _p(ws), ws.numel(), _stream()),
+           "ssm_adjoint_grad")
+    return o
+
+
+def ssm_proj_grad(X, dZ, W=None, want_dW=True, want_dX=False, dW=None, dX=None, accum_dW=False,
+                  accum_dX=False):
+    """``dW = X^T dZ`` and/or ``dX = dZ W^T`` (bf16 operands, fp32 results)."""
+    lib = load_library()
+    M, Nout = dZ.shape
+    _need(dZ, "dZ", torch.bfloat16)
+    K = (X.shape[1] if X is not None else W.shape[0])
+    if want_dW:
+        _need(X, "X", torch.bfloat16, (M, K))
+        dW = dW if dW is not None else torch.empty(K, Nout, dtype=torch.float32, device=dZ.device)
+    if want_dX:
+        _need(W, "W", torch.bfloat16, (K, Nout))
+        dX = dX if dX is not None else torch.empty(M, K, dtype=torch.float32, device=dZ.device)
+    flags = (SSM_ACCUM_DW if accum_dW else 0) | (SSM_ACCUM_DX if accum_dX else 0)
+    n = ctypes.c_size_t()
+    _check(lib.ssm_proj_grad_workspace_size(M, K, Nout, flags, ctypes.byref(n)), "ssm_proj_grad_workspace_size")
+    ws = _workspace(n.value, dZ.device)
+    _check(lib.ssm_proj_grad(M, K, Nout, _p(X if want_dW else None), K, _p(dZ), Nout, _p(W if want_dX else None),
+                             Nout, _p(dW if want_dW else None), _p(dX if want_dX else None), flags, _p(ws),
+                             ws.numel(), _stream()), "ssm_proj_grad")
+    return (dW if want_dW else None), (dX if want_dX else None)
+
+
+def layer_workspace_size(desc: SsmDesc, tbar: int, d_model: int) -> int:
+    n = ctypes.c_size_t()
+    mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
+    _check(load_library().ssm_layer_grad_workspace_size(ctypes.byref(desc), mode, int(tbar), int(d_model),
+                                                        ctypes.byref(n)), "ssm_layer_grad_workspace_size")
+    return n.value
+
+
+def ssm_layer_grad(u, x, z, delta_pre, B, C, W_x, W_in, A_log, dy, tbar=0, chunk=0, want_du=False,
+                   want_scan=False, out=None, workspace=None):
+    """Whole-layer gradient with input projections (bf16 activations).
+
+    Returns a dict with fp32 ``dW_in, dW_x, dA_log`` (+ ``du`` if asked; + the scan
+    gradients ``dx, ddelta, dB, dC, dz`` and ``dx_total`` if ``want_scan``)."""
+    lib = load_library()
+    b, T, D = x.shape
+    N = A_log.shape[1]
+    dm = u.shape[-1]
+    bf = torch.bfloat16
+    _need(u, "u", bf, (b, T, dm))
+    _need(x, "x", bf)
+    _need(z, "z", bf, (b, T, D))
+    _need(delta_pre, "delta_pre", bf, (b, T, D))
+    _need(B, "B", bf, (b, T, N))
+    _need(C, "C", bf, (b, T, N))
+    _need(W_x, "W_x", bf, (D, D + 2 * N))
+    _need(W_in, "W_in", bf, (dm, 2 * D))
+    _need(A_log, "A_log", torch.float32, (D, N))
+    _need(dy, "dy", bf, (b, T, D))
+    desc = make_desc(x, N, True, True, chunk)
+    mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
+    dev = x.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    o = dict(out) if out else {}
+    o.setdefault("dW_in", torch.empty(dm, 2 * D, **f32))
+    o.setdefault("dW_x", torch.empty(D, D + 2 * N, **f32))
+    o.setdefault("dA_log", torch.empty(D, N, **f32))
+    if want_du:
+        o.setdefault("du", torch.empty(b, T, dm, **f32))
+    if want_scan:
+        for k, shp in (("dx", (b, T, D)), ("ddelta", (b, T, D)), ("dB", (b, T, N)), ("dC", (b, T, N)),
+                       ("dz", (b, T, D)), ("dx_total", (b, T, D))):
+            o.setdefault(k, torch.empty(*shp, **f32))
+    ws = workspace if workspace is not None else _workspace(layer_workspace_size(desc, tbar, dm), dev)
+    _check(lib.ssm_layer_grad(ctypes.byref(desc), mode, int(tbar), dm, _p(u), _p(x), _p(z), _p(delta_pre), _p(B),
+                              _p(C), _p(W_x), _p(W_in), _p(A_log), _p(dy), _p(o["dW_in"]), _p(o["dW_x"]),
+                              _p(o["dA_log"]), _p(o.get("du")), _p(o.get("dx")), _p(o.get("ddelta")), _p(o.get("dB")),
+                              _p(o.get("dC")), _p(o.get("dz")), _p(o.get("dx_total")), _p(ws), ws.numel(),
+                              _stream()), "ssm_layer_grad")
+    return o

@@ -1,0 +1,453 @@
+// abi.cpp -- the extern "C" entry points declared in include/ssm_adjoint.h:
+// argument validation (before anything is enqueued), workspace layout and
+// dispatch to the HIP kernels.
+#include "ssm_adjoint.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ssm_status fail(ssm_status st, const char* fmt, ...) {
+    char msg[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(msg, sizeof msg, fmt, ap);
+    va_end(ap);
+    g_last_error = msg;
+    return st;
+}
+
+ssm_status hip_fail(hipError_t e, const char* where) {
+    return fail(SSM_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+
+constexpr int64_t kMaxGridYZ = 65535;
+
+// Shape checks shared by forward and gradient.  Fills L (chunk) and nc.
+ssm_status check_desc(const ssm_desc* d, int64_t* L, int64_t* nc) {
+    if (!d) return fail(SSM_ERR_NULL, "desc is NULL");
+    if (d->batch < 1 || d->seqlen < 1 || d->channels < 1 || d->dstate < 1)
+        return fail(SSM_ERR_SHAPE, "batch, seqlen, channels and dstate must be >= 1 (got %lld, %lld, %lld, %lld)",
+                    (long long)d->batch, (long long)d->seqlen, (long long)d->channels,
+                    (long long)d->dstate);
+    if (d->dstate > 16) return fail(SSM_ERR_UNSUPPORTED, "dstate %lld > 16", (long long)d->dstate);
+    if (d->in_dtype != SSM_F32 && d->in_dtype != SSM_BF16)
+        return fail(SSM_ERR_DTYPE, "unknown in_dtype %d", (int)d->in_dtype);
+    if (d->flags & ~(SSM_DELTA_SOFTPLUS | SSM_GATE_SILU))
+        return fail(SSM_ERR_SHAPE, "unknown flag bits 0x%x", (unsigned)d->flags);
+    const int64_t l = d->chunk == 0 ? ssmk::default_chunk() : d->chunk;
+    if (!ssmk::chunk_supported(l))
+        return fail(SSM_ERR_UNSUPPORTED, "chunk %lld not in {16, 32, 64, 128, 256}", (long long)d->chunk);
+    const int64_t n = (d->seqlen + l - 1) / l;
+    if (n > kMaxGridYZ || d->batch > kMaxGridYZ / 2)
+        return fail(SSM_ERR_UNSUPPORTED, "seqlen/chunk (%lld) or batch (%lld) exceeds the launch grid",
+                    (long long)n, (long long)d->batch);
+    // All index arithmetic is 64-bit; element counts must fit comfortably.
+    if (d->batch * d->seqlen > (int64_t(1) << 40) || d->channels > (int64_t(1) << 24))
+        return fail(SSM_ERR_SHAPE, "problem too large");
+    *L = l;
+    *nc = n;
+    return SSM_OK;
+}
+
+ssm_status check_mode(const ssm_desc* d, int32_t mode, int64_t tbar, bool* trunc) {
+    if (mode != SSM_FULL && mode != SSM_TRUNCATED)
+        return fail(SSM_ERR_SHAPE, "unknown mode %d", (int)mode);
+    *trunc = false;
+    if (mode == SSM_TRUNCATED) {
+        if (tbar < 1) return fail(SSM_ERR_SHAPE, "truncated mode needs tbar >= 1 (got %lld)", (long long)tbar);
+        *trunc = tbar < d->seqlen;  // tbar >= T is the full gradient
+    }
+    return SSM_OK;
+}
+
+#define REQUIRE_PTR(p, name)                                                         \
+    do {                                                                             \
+        if (!(p)) return fail(SSM_ERR_NULL, "%s is NULL", name);                     \
+        if (!aligned16(p)) return fail(SSM_ERR_ALIGN, "%s is not 16-byte aligned", name); \
+    } while (0)
+#define OPTIONAL_PTR(p, name)                                                        \
+    do {                                                                             \
+        if ((p) && !aligned16(p)) return fail(SSM_ERR_ALIGN, "%s is not 16-byte aligned", name); \
+    } while (0)
+
+ssm_status check_workspace(void* ws, size_t have, size_t need) {
+    if (need == 0) return SSM_OK;
+    if (!ws) return fail(SSM_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+    if (!aligned256(ws)) return fail(SSM_ERR_ALIGN, "workspace is not 256-byte aligned");
+    if (have < need) return fail(SSM_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+    return SSM_OK;
+}
+
+ssmk::ScanProblem make_problem(const ssm_desc* d, int64_t L, int64_t nc) {
+    ssmk::ScanProblem p{};
+    p.nb = d->batch;
+    p.T = d->seqlen;
+    p.D = d->channels;
+    p.N = d->dstate;
+    p.L = L;
+    p.nc = nc;
+    p.bf16 = d->in_dtype == SSM_BF16;
+    p.softplus = (d->flags & SSM_DELTA_SOFTPLUS) != 0;
+    p.gate = (d->flags & SSM_GATE_SILU) != 0;
+    return p;
+}
+
+// Workspace of the whole-layer call: the scan workspace, then bf16 packing
+// buffers, fp32 scan outputs that the caller did not supply, and the GEMM
+// workspace.
+struct LayerWs {
+    size_t scan_off, dzx_off, dxz_off, f32_off, gemm_off, total;
+    size_t scan_total;
+};
+
+size_t up256(size_t v) { return (v + 255) & ~size_t(255); }
+
+LayerWs layer_ws(const ssm_desc* d, int64_t L, bool trunc, int64_t d_model) {
+    LayerWs w{};
+    const int64_t M = d->batch * d->seqlen, D = d->channels, N = d->dstate;
+    ssmk::ScanWorkspace sw = ssmk::scan_workspace(d->batch, d->seqlen, D, N, L, true, trunc);
+    w.scan_total = sw.total;
+    size_t off = 0;
+    w.scan_off = off;
+    off = up256(off + sw.total);
+    w.dzx_off = off;  // bf16 [M][D+2N]
+    off = up256(off + size_t(M) * (D + 2 * N) * 2);
+    w.dxz_off = off;  // bf16 [M][2D]
+    off = up256(off + size_t(M) * 2 * D * 2);
+    w.f32_off = off;  // fp32 dx, ddelta, dz [M][D] and dB, dC [M][N], dx_total [M][D]
+    off = up256(off + size_t(M) * (4 * D + 2 * N) * 4);
+    w.gemm_off = off;
+    size_t g1 = ssmk::gemm_dw_workspace(M, D, D + 2 * N);
+    size_t g2 = ssmk::gemm_dw_workspace(M, d_model, 2 * D);
+    off = up256(off + (g1 > g2 ? g1 : g2));
+    w.total = off;
+    return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ssm_last_error(void) { return g_last_error.c_str(); }
+
+ssm_status ssm_adjoint_forward_workspace_size(const ssm_desc* desc, size_t* bytes) {
+    int64_t L, nc;
+    ssm_status st = check_desc(desc, &L, &nc);
+    if (st) return st;
+    if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");
+    *bytes = ssmk::scan_workspace(desc->batch, desc->seqlen, desc->channels, desc->dstate, L,
+                                  false, false)
+                 .total;
+    return SSM_OK;
+}
+
+ssm_status ssm_adjoint_grad_workspace_size(const ssm_desc* desc, int32_t mode, int64_t tbar,
+                                           size_t* bytes) {
+    int64_t L, nc;
+    ssm_status st = check_desc(desc, &L, &nc);
+    if (st) return st;
+    bool trunc;
+    st = check_mode(desc, mode, tbar, &trunc);
+    if (st) return st;
+    if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");
+    *bytes = ssmk::scan_workspace(desc->batch, desc->seqlen, desc->channels, desc->dstate, L,
+                                  true, trunc)
+                 .total;
+    return SSM_OK;
+}
+
+ssm_status ssm_adjoint_forward(const ssm_desc* desc, const void* x, const void* delta,
+                               const float* A_log, const void* B, const void* C, const float* h0,
+                               const void* z, void* y, float* h_last, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    int64_t L, nc;
+    ssm_status st = check_desc(desc, &L, &nc);
+    if (st) return st;
+    REQUIRE_PTR(x, "x");
+    REQUIRE_PTR(delta, "delta");
+    REQUIRE_PTR(A_log, "A_log");
+    REQUIRE_PTR(B, "B");
+    REQUIRE_PTR(C, "C");
+    REQUIRE_PTR(y, "y");
+    OPTIONAL_PTR(h0, "h0");
+    OPTIONAL_PTR(h_last, "h_last");
+    const bool gate = (desc->flags & SSM_GATE_SILU) != 0;
+    if (gate) REQUIRE_PTR(z, "z");
+    else if (z) return fail(SSM_ERR_SHAPE, "z given without SSM_GATE_SILU");
+    ssmk::ScanWorkspace w = ssmk::scan_workspace(desc->batch, desc->seqlen, desc->channels,
+                                                 desc->dstate, L, false, false);
+    st = check_workspace(workspace, workspace_bytes, w.total);
+    if (st) return st;
+    ssmk::ScanProblem p = make_problem(desc, L, nc);
+    p.x = x;
+    p.delta = delta;
+    p.A_log = A_log;
+    p.B = B;
+    p.C = C;
+    p.h0 = h0;
+    p.z = z;
+    p.y = y;
+    p.h_last = h_last;
+    ssmk::bind_workspace(p, workspace, w);
+    p.mbuf = nullptr;
+    hipError_t e = ssmk::launch_forward(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "ssm_adjoint_forward launch");
+    return SSM_OK;
+}
+
+static ssm_status grad_validate(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
+                                const void* delta, const float* A_log, const void* B,
+                                const void* C, const float* h0, const void* z, const void* dy,
+                                float* dx, float* ddelta, float* dA_log, float* dB, float* dC,
+                                float* dz, float* dh0, int64_t* L, int64_t* nc, bool* trunc) {
+    ssm_status st = check_desc(desc, L, nc);
+    if (st) return st;
+    st = check_mode(desc, mode, tbar, trunc);
+    if (st) return st;
+    REQUIRE_PTR(x, "x");
+    REQUIRE_PTR(delta, "delta");
+    REQUIRE_PTR(A_log, "A_log");
+    REQUIRE_PTR(B, "B");
+    REQUIRE_PTR(C, "C");
+    REQUIRE_PTR(dy, "dy");
+    REQUIRE_PTR(dx, "dx");
+    REQUIRE_PTR(ddelta, "ddelta");
+    REQUIRE_PTR(dA_log, "dA_log");
+    REQUIRE_PTR(dB, "dB");
+    REQUIRE_PTR(dC, "dC");
+    OPTIONAL_PTR(h0, "h0");
+    const bool gate = (desc->flags & SSM_GATE_SILU) != 0;
+    if (gate) {
+        REQUIRE_PTR(z, "z");
+        REQUIRE_PTR(dz, "dz");
+    } else if (z || dz) {
+        return fail(SSM_ERR_SHAPE, "z/dz given without SSM_GATE_SILU");
+    }
+    OPTIONAL_PTR(dh0, "dh0");
+    if (dh0 && mode == SSM_TRUNCATED && *trunc)
+        return fail(SSM_ERR_UNSUPPORTED, "dh0 is defined for the full gradient only");
+    return SSM_OK;
+}
+
+static void grad_bind(ssmk::ScanProblem& p, const void* x, const void* delta, const float* A_log,
+                      const void* B, const void* C, const float* h0, const void* z, const void* dy,
+                      float* dx, float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
+                      float* dh0) {
+    p.x = x;
+    p.delta = delta;
+    p.A_log = A_log;
+    p.B = B;
+    p.C = C;
+    p.h0 = h0;
+    p.z = z;
+    p.dy = dy;
+    p.dx = dx;
+    p.ddelta = ddelta;
+    p.dA_log = dA_log;
+    p.dB = dB;
+    p.dC = dC;
+    p.dz = dz;
+    p.dh0 = dh0;
+}
+
+ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
+                            const void* delta, const float* A_log, const void* B, const void* C,
+                            const float* h0, const void* z, const void* dy, float* dx,
+                            float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
+                            float* dh0, void* workspace, size_t workspace_bytes, void* stream) {
+    int64_t L, nc;
+    bool trunc;
+    ssm_status st = grad_validate(desc, mode, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta,
+                                  dA_log, dB, dC, dz, dh0, &L, &nc, &trunc);
+    if (st) return st;
+    ssmk::ScanWorkspace w = ssmk::scan_workspace(desc->batch, desc->seqlen, desc->channels,
+                                                 desc->dstate, L, true, trunc);
+    st = check_workspace(workspace, workspace_bytes, w.total);
+    if (st) return st;
+    ssmk::ScanProblem p = make_problem(desc, L, nc);
+    p.trunc = trunc;
+    p.tbar = trunc ? tbar : 0;
+    p.nsplit = ssmk::choose_nsplit(p.nb, p.D, nc);
+    p.nslice = ssmk::choose_nslice(p.nb, nc);
+    grad_bind(p, x, delta, A_log, B, C, h0, z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0);
+    ssmk::bind_workspace(p, workspace, w);
+    hipError_t e = ssmk::launch_grad(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "ssm_adjoint_grad launch");
+    return SSM_OK;
+}
+
+ssm_status ssm_proj_grad_workspace_size(int64_t M, int64_t K, int64_t Nout, uint32_t flags,
+                                        size_t* bytes) {
+    if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");
+    if (M < 1 || K < 1 || Nout < 1) return fail(SSM_ERR_SHAPE, "M, K, Nout must be >= 1");
+    if (flags & ~(SSM_ACCUM_DW | SSM_ACCUM_DX)) return fail(SSM_ERR_SHAPE, "unknown flag bits");
+    *bytes = ssmk::gemm_dw_workspace(M, K, Nout);
+    return SSM_OK;
+}
+
+static ssm_status check_gemm_shape(int64_t M, int64_t K, int64_t Nout, int64_t ldx, int64_t lddz,
+                                   int64_t ldw, bool need_w) {
+    if (M < 1 || K < 1 || Nout < 1)
+        return fail(SSM_ERR_SHAPE, "M, K, Nout must be >= 1 (got %lld, %lld, %lld)", (long long)M,
+                    (long long)K, (long long)Nout);
+    if (K % 8 || Nout % 8)
+        return fail(SSM_ERR_UNSUPPORTED, "K and Nout must be multiples of 8 (got %lld, %lld)",
+                    (long long)K, (long long)Nout);
+    if (ldx < K || lddz < Nout || (need_w && ldw < Nout))
+        return fail(SSM_ERR_SHAPE, "leading dimension smaller than the row length");
+    if (ldx % 8 || lddz % 8 || (need_w && ldw % 8))
+        return fail(SSM_ERR_ALIGN, "leading dimensions must be multiples of 8 elements");
+    if (M > (int64_t(1) << 31) || K > (int64_t(1) << 20) || Nout > (int64_t(1) << 20))
+        return fail(SSM_ERR_SHAPE, "GEMM too large");
+    return SSM_OK;
+}
+
+ssm_status ssm_proj_grad(int64_t M, int64_t K, int64_t Nout, const void* X, int64_t ldx,
+                         const void* dZ, int64_t lddz, const void* W, int64_t ldw, float* dW,
+                         float* dX, uint32_t flags, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+    if (flags & ~(SSM_ACCUM_DW | SSM_ACCUM_DX)) return fail(SSM_ERR_SHAPE, "unknown flag bits");
+    ssm_status st = check_gemm_shape(M, K, Nout, dW ? ldx : K, lddz, ldw, dX != nullptr);
+    if (st) return st;
+    REQUIRE_PTR(dZ, "dZ");
+    if (dW) REQUIRE_PTR(X, "X");
+    if (dX) REQUIRE_PTR(W, "W");
+    OPTIONAL_PTR(dW, "dW");
+    OPTIONAL_PTR(dX, "dX");
+    if (dW) {
+        st = check_workspace(workspace, workspace_bytes, ssmk::gemm_dw_workspace(M, K, Nout));
+        if (st) return st;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (dW) {
+        hipError_t e = ssmk::launch_gemm_dw(M, K, Nout, static_cast<const uint16_t*>(X), ldx,
+                                            static_cast<const uint16_t*>(dZ), lddz, dW,
+                                            (flags & SSM_ACCUM_DW) != 0, workspace, s);
+        if (e != hipSuccess) return hip_fail(e, "ssm_proj_grad dW launch");
+    }
+    if (dX) {
+        hipError_t e = ssmk::launch_gemm_dx(M, K, Nout, static_cast<const uint16_t*>(dZ), lddz,
+                                            static_cast<const uint16_t*>(W), ldw, dX,
+                                            (flags & SSM_ACCUM_DX) != 0, nullptr, nullptr, 0, s);
+        if (e != hipSuccess) return hip_fail(e, "ssm_proj_grad dX launch");
+    }
+    return SSM_OK;
+}
+
+ssm_status ssm_layer_grad_workspace_size(const ssm_desc* desc, int32_t mode, int64_t tbar,
+                                         int64_t d_model, size_t* bytes) {
+    int64_t L, nc;
+    ssm_status st = check_desc(desc, &L, &nc);
+    if (st) return st;
+    bool trunc;
+    st = check_mode(desc, mode, tbar, &trunc);
+    if (st) return st;
+    if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");
+    if (d_model < 1) return fail(SSM_ERR_SHAPE, "d_model must be >= 1");
+    *bytes = layer_ws(desc, L, trunc, d_model).total;
+    return SSM_OK;
+}
+
+ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int64_t d_model,
+                          const void* u, const void* x, const void* z, const void* delta_pre,
+                          const void* B, const void* C, const void* W_x, const void* W_in,
+                          const float* A_log, const void* dy, float* dW_in, float* dW_x,
+                          float* dA_log, float* du, float* dx, float* ddelta, float* dB,
+                          float* dC, float* dz, float* dx_total, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    int64_t L, nc;
+    ssm_status st = check_desc(desc, &L, &nc);
+    if (st) return st;
+    if (desc->in_dtype != SSM_BF16)
+        return fail(SSM_ERR_UNSUPPORTED, "the layer gradient takes bf16 activations");
+    bool trunc;
+    st = check_mode(desc, mode, tbar, &trunc);
+    if (st) return st;
+    if (d_model < 1) return fail(SSM_ERR_SHAPE, "d_model must be >= 1");
+    const int64_t M = desc->batch * desc->seqlen, D = desc->channels, N = desc->dstate;
+    st = check_gemm_shape(M, D, D + 2 * N, D, D + 2 * N, D + 2 * N, true);
+    if (st) return st;
+    st = check_gemm_shape(M, d_model, 2 * D, d_model, 2 * D, 2 * D, du != nullptr);
+    if (st) return st;
+    REQUIRE_PTR(u, "u");
+    REQUIRE_PTR(W_x, "W_x");
+    REQUIRE_PTR(dW_in, "dW_in");
+    REQUIRE_PTR(dW_x, "dW_x");
+    if (du) {
+        REQUIRE_PTR(W_in, "W_in");
+        OPTIONAL_PTR(du, "du");
+    }
+    OPTIONAL_PTR(dx_total, "dx_total");
+    LayerWs w = layer_ws(desc, L, trunc, d_model);
+    st = check_workspace(workspace, workspace_bytes, w.total);
+    if (st) return st;
+    char* ws = static_cast<char*>(workspace);
+    float* f32 = reinterpret_cast<float*>(ws + w.f32_off);
+    float* dx_ = dx ? dx : f32;
+    float* dd_ = ddelta ? ddelta : f32 + M * D;
+    float* dz_ = dz ? dz : f32 + 2 * M * D;
+    float* dxt_ = dx_total ? dx_total : f32 + 3 * M * D;
+    float* dB_ = dB ? dB : f32 + 4 * M * D;
+    float* dC_ = dC ? dC : f32 + 4 * M * D + M * N;
+
+    ssm_desc sd = *desc;
+    sd.flags = SSM_DELTA_SOFTPLUS | SSM_GATE_SILU;
+    bool trunc2;
+    st = grad_validate(&sd, mode, tbar, x, delta_pre, A_log, B, C, nullptr, z, dy, dx_, dd_, dA_log,
+                       dB_, dC_, dz_, nullptr, &L, &nc, &trunc2);
+    if (st) return st;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ssmk::ScanWorkspace sw = ssmk::scan_workspace(sd.batch, sd.seqlen, D, N, L, true, trunc);
+    ssmk::ScanProblem p = make_problem(&sd, L, nc);
+    p.trunc = trunc;
+    p.tbar = trunc ? tbar : 0;
+    p.nsplit = ssmk::choose_nsplit(p.nb, p.D, nc);
+    p.nslice = ssmk::choose_nslice(p.nb, nc);
+    grad_bind(p, x, delta_pre, A_log, B, C, nullptr, z, dy, dx_, dd_, dA_log, dB_, dC_, dz_, nullptr);
+    ssmk::bind_workspace(p, ws + w.scan_off, sw);
+    hipError_t e = ssmk::launch_grad(p, s);
+    if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad scan launch");
+
+    // dZx = [dDelta_pre | dB | dC] (bf16), [dx_total | dz] (bf16)
+    uint16_t* dzx = reinterpret_cast<uint16_t*>(ws + w.dzx_off);
+    uint16_t* dxz = reinterpret_cast<uint16_t*>(ws + w.dxz_off);
+    const int64_t nx = D + 2 * N;
+    if ((e = ssmk::launch_pack_bf16(M, D, dd_, D, dzx, nx, 0, s)) != hipSuccess ||
+        (e = ssmk::launch_pack_bf16(M, N, dB_, N, dzx, nx, D, s)) != hipSuccess ||
+        (e = ssmk::launch_pack_bf16(M, N, dC_, N, dzx, nx, D + N, s)) != hipSuccess ||
+        (e = ssmk::launch_pack_bf16(M, D, dz_, D, dxz, 2 * D, D, s)) != hipSuccess)
+        return hip_fail(e, "ssm_layer_grad pack launch");
+    void* gws = ws + w.gemm_off;
+    // dW_x = x^T dZx
+    e = ssmk::launch_gemm_dw(M, D, nx, static_cast<const uint16_t*>(x), D, dzx, nx, dW_x, false, gws, s);
+    if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_x launch");
+    // dx_total = dx + dZx W_x^T, also packed into [dx_total | dz]
+    e = ssmk::launch_gemm_dx(M, D, nx, dzx, nx, static_cast<const uint16_t*>(W_x), nx, dxt_, false,
+                             dx_, dxz, 2 * D, s);
+    if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dx_total launch");
+    // dW_in = u^T [dx_total | dz]
+    e = ssmk::launch_gemm_dw(M, d_model, 2 * D, static_cast<const uint16_t*>(u), d_model, dxz, 2 * D,
+                             dW_in, false, gws, s);
+    if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_in launch");
+    if (du) {
+        e = ssmk::launch_gemm_dx(M, d_model, 2 * D, dxz, 2 * D, static_cast<const uint16_t*>(W_in),
+                                 2 * D, du, false, nullptr, nullptr, 0, s);
+        if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad du launch");
+    }
+    return SSM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,84 @@
+// internal.h -- launch interface between the C ABI (abi.cpp) and the HIP kernels.
+// Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ssmk {
+
+// One scan problem: the selective diagonal layer of shape [b][T][D] x N states,
+// split into nc = ceil(T / L) carry chunks of L steps.
+struct ScanProblem {
+    int64_t nb, T, D, N, L, nc;
+    bool bf16;       // inputs are bf16 (else fp32)
+    bool softplus;   // delta holds Delta_pre
+    bool gate;       // SiLU output gate with z
+    bool trunc;      // truncated estimator with window tbar (< T)
+    int64_t tbar;
+    int nsplit;      // channel splits of the fused kernel (dB/dC partials when > 1)
+    int nslice;      // slices of the dA_log reduction
+    // inputs
+    const void* x;
+    const void* delta;
+    const float* A_log;
+    const void* B;
+    const void* C;
+    const float* h0;
+    const void* z;
+    const void* dy;
+    // outputs
+    void* y;
+    float* h_last;
+    float* dx;
+    float* ddelta;
+    float* dA_log;
+    float* dB;
+    float* dC;
+    float* dz;
+    float* dh0;
+    // workspace regions
+    float* hbuf;    // [b][nc][N][D]
+    float* mbuf;    // [b][nc][N][D]
+    double* sdel;   // [b][nc][D]
+    double* psum;   // [b][nc+1][D]
+    float* pB;      // [nsplit][b][T][N]
+    float* pC;      // [nsplit][b][T][N]
+    float* dAtmp;   // [nslice][N][D]
+};
+
+// Workspace layout shared by the size query and the launch.
+struct ScanWorkspace {
+    size_t off_hbuf, off_mbuf, off_sdel, off_psum, off_pB, off_pC, off_dAtmp, total;
+};
+
+int64_t default_chunk();
+bool chunk_supported(int64_t L);
+int choose_nsplit(int64_t nb, int64_t D, int64_t nc);
+int choose_nslice(int64_t nb, int64_t nc);
+ScanWorkspace scan_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t L, bool grad,
+                             bool trunc);
+void bind_workspace(ScanProblem& p, void* ws, const ScanWorkspace& w);
+
+hipError_t launch_forward(const ScanProblem& p, hipStream_t s);
+hipError_t launch_grad(const ScanProblem& p, hipStream_t s);
+
+// bf16 MFMA GEMMs (gemm.hip).
+// dW[K][N] (+)= X^T dZ with X [M][K] (ldx), dZ [M][N] (lddz).
+size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N);
+hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, int64_t ldx,
+                          const uint16_t* dZ, int64_t lddz, float* dW, bool accum, void* ws,
+                          hipStream_t s);
+// dX[M][K] (+)= dZ W^T with dZ [M][N] (lddz), W [K][N] (ldw); optional fp32 addend
+// add[M][K] (ld = K) and optional bf16 copy of the result into out16 (ld16).
+hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, int64_t lddz,
+                          const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
+                          uint16_t* out16, int64_t ld16, hipStream_t s);
+
+// fp32 -> bf16 (round to nearest even) copy of a [rows][cols] block into a strided
+// destination: dst[r*ldd + col0 + c] = bf16(src[r*lds + c]).
+hipError_t launch_pack_bf16(int64_t rows, int64_t cols, const float* src, int64_t lds,
+                            uint16_t* dst, int64_t ldd, int64_t col0, hipStream_t s);
+
+}  // namespace ssmk

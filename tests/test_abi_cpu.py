@@ -1,0 +1,118 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every
+function the header declares, and rejects bad arguments on the host (before
+any HIP call) with the documented status codes."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2501_00692_amd as ssm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ssm_adjoint.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not ssm.LIB_PATH.exists():
+        pytest.fail("libssm_adjoint.so is not built (run __graft_entry__.build())")
+    return ssm.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ssm_[a-z_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert sorted(ssm.EXPORTED) == declared_functions()
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def desc(**kw):
+    d = dict(batch=1, seqlen=256, channels=64, dstate=16, chunk=0, in_dtype=ssm.SSM_F32, flags=0)
+    d.update(kw)
+    return ssm.SsmDesc(**d)
+
+
+FAKE = ctypes.c_void_p(0x100000)  # never dereferenced: every call below fails validation
+MISALIGNED = ctypes.c_void_p(0x100004)
+
+
+def grad_call(lib, dsc, mode=ssm.SSM_FULL, tbar=0, x=FAKE, dh0=None, z=None, dz=None, ws=FAKE,
+              ws_bytes=1 << 40):
+    return lib.ssm_adjoint_grad(ctypes.byref(dsc) if dsc is not None else None, mode, tbar, x, FAKE, FAKE, FAKE,
+                                FAKE, None, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, dz, dh0, ws, ws_bytes, None)
+
+
+def test_null_and_shape_errors(lib):
+    assert grad_call(lib, None) == 1
+    assert "desc" in ssm.last_error()
+    assert grad_call(lib, desc(batch=0)) == 2
+    assert grad_call(lib, desc(seqlen=0)) == 2
+    assert grad_call(lib, desc(dstate=17)) == 4
+    assert grad_call(lib, desc(in_dtype=7)) == 3
+    assert grad_call(lib, desc(chunk=100)) == 4
+    assert grad_call(lib, desc(flags=8)) == 2
+    assert grad_call(lib, desc(), x=None) == 1
+    assert "x is NULL" in ssm.last_error()
+    assert grad_call(lib, desc(), x=MISALIGNED) == 6
+
+
+def test_mode_errors(lib):
+    assert grad_call(lib, desc(), mode=5) == 2
+    assert grad_call(lib, desc(), mode=ssm.SSM_TRUNCATED, tbar=0) == 2
+    # dh0 exists for the full gradient only
+    assert grad_call(lib, desc(), mode=ssm.SSM_TRUNCATED, tbar=32, dh0=FAKE) == 4
+    # gate flag and z must agree
+    assert grad_call(lib, desc(flags=ssm.SSM_GATE_SILU)) == 1
+    assert grad_call(lib, desc(), z=FAKE, dz=FAKE) == 2
+
+
+def test_workspace_errors(lib):
+    d = desc()
+    assert grad_call(lib, d, ws=None) == 5
+    assert grad_call(lib, d, ws_bytes=16) == 5
+    assert grad_call(lib, d, ws=ctypes.c_void_p(0x100010)) == 6
+
+
+def test_workspace_queries(lib):
+    n = ctypes.c_size_t()
+    d = desc()
+    assert lib.ssm_adjoint_grad_workspace_size(ctypes.byref(d), ssm.SSM_FULL, 0, ctypes.byref(n)) == 0
+    full = n.value
+    assert full > 0
+    assert lib.ssm_adjoint_grad_workspace_size(ctypes.byref(d), ssm.SSM_TRUNCATED, 32, ctypes.byref(n)) == 0
+    assert n.value >= full
+    # tbar >= T is the full gradient
+    assert lib.ssm_adjoint_grad_workspace_size(ctypes.byref(d), ssm.SSM_TRUNCATED, 256, ctypes.byref(n)) == 0
+    assert n.value == full
+    assert lib.ssm_adjoint_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    assert 0 < n.value <= full
+    assert lib.ssm_proj_grad_workspace_size(8192, 1536, 1568, 0, ctypes.byref(n)) == 0
+    assert lib.ssm_proj_grad_workspace_size(0, 1, 1, 0, ctypes.byref(n)) == 2
+    ld = desc(batch=2, seqlen=4096, channels=1536, in_dtype=ssm.SSM_BF16)
+    assert lib.ssm_layer_grad_workspace_size(ctypes.byref(ld), ssm.SSM_FULL, 0, 768, ctypes.byref(n)) == 0
+    assert n.value > 0
+
+
+def test_proj_errors(lib):
+    call = lambda M, K, N, X=FAKE, dZ=FAKE, W=None, dW=FAKE, dX=None, ldx=None: lib.ssm_proj_grad(
+        M, K, N, X, ldx if ldx is not None else K, dZ, N, W, N, dW, dX, 0, FAKE, 1 << 40, None)
+    assert call(0, 8, 8) == 2
+    assert call(16, 12, 8) == 4          # K must be a multiple of 8
+    assert call(16, 8, 8, dZ=None) == 1
+    assert call(16, 8, 8, dX=FAKE) == 1  # dX needs W
+    assert call(16, 8, 8, ldx=4) == 2
+
+
+def test_layer_rejects_fp32(lib):
+    d = desc()
+    rc = lib.ssm_layer_grad(ctypes.byref(d), 0, 0, 64, *([FAKE] * 13), *([None] * 7), FAKE, 1 << 40, None)
+    assert rc == 4

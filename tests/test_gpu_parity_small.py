@@ -1,0 +1,150 @@
+"""GPU parity against the fp64 oracle at sizes the oracle finishes in seconds:
+several chunks and 16-channel tiles, ragged tails, every chunk size, full and
+truncated forms, gate and softplus, fp32 and bf16 inputs."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2501_00692_amd as ssm
+from paper_2501_00692_amd.synth import WORKLOADS, Workload, make_inputs
+
+from gpu_helpers import TOL_BF16, TOL_F32, check, say, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(w: Workload, h0=False):
+    inp = make_inputs(w, device="cuda", h0=h0)
+    torch.cuda.synchronize()
+    return inp
+
+
+def _oracle_grad(inp, w, tbar, literal=False, want_dh0=False):
+    args = [to_np(inp[k]) for k in ("x", "delta", "A_log", "B", "C", "dy")]
+    kw = dict(h0=to_np(inp["h0"]) if "h0" in inp else None,
+              z=to_np(inp["z"]) if "z" in inp else None, delta_softplus=w.proj)
+    if tbar <= 0 or tbar >= w.T:
+        return oracle.bptt(*args, want_dh0=want_dh0, **kw)
+    fn = oracle.adjoint_sum if literal else oracle.trunc_tail
+    return fn(*args, tbar=tbar, want_dh0=False, **kw)
+
+
+def _gpu_grad(inp, w, tbar, chunk, want_dh0=False):
+    g = ssm.ssm_adjoint_grad(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"],
+                             h0=inp.get("h0"), z=inp.get("z"), softplus=w.proj, tbar=tbar, chunk=chunk,
+                             want_dh0=want_dh0)
+    torch.cuda.synchronize()
+    return g
+
+
+def _compare(g, ref, tol, gate, dh0=False):
+    rep = {}
+    for k in ("dx", "ddelta", "dA_log", "dB", "dC") + (("dz",) if gate else ()) + (("dh0",) if dh0 else ()):
+        check(k, to_np(g[k]), ref[k], tol, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
+SMALL = WORKLOADS["small"]
+SLOW = WORKLOADS["small_slow"]
+
+
+@pytest.mark.parametrize("chunk", [16, 32, 64, 128, 256])
+def test_forward_small(chunk):
+    w = SMALL
+    say(f"[forward] workload={w.name} chunk={chunk}")
+    inp = _inputs(w, h0=True)
+    y, hl = ssm.ssm_adjoint_forward(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], h0=inp["h0"],
+                                    chunk=chunk, want_h_last=True)
+    torch.cuda.synchronize()
+    ry, rh = oracle.forward(*(to_np(inp[k]) for k in ("x", "delta", "A_log", "B", "C")), h0=to_np(inp["h0"]))
+    check("y", to_np(y), ry, TOL_F32)
+    check("h_last", to_np(hl), rh, TOL_F32)
+
+
+@pytest.mark.parametrize("chunk", [16, 64, 128, 256])
+def test_grad_small_full(chunk):
+    w = SMALL
+    say(f"[grad full] workload={w.name} chunk={chunk}")
+    inp = _inputs(w, h0=True)
+    g = _gpu_grad(inp, w, 0, chunk, want_dh0=True)
+    _compare(g, _oracle_grad(inp, w, 0, want_dh0=True), TOL_F32, False, dh0=True)
+
+
+@pytest.mark.parametrize("chunk", [16, 64, 128, 256])
+def test_grad_small_truncated_literal(chunk):
+    w = SMALL
+    say(f"[grad trunc] workload={w.name} tbar={w.tbar} chunk={chunk}")
+    inp = _inputs(w)
+    g = _gpu_grad(inp, w, w.tbar, chunk)
+    _compare(g, _oracle_grad(inp, w, w.tbar, literal=True), TOL_F32, False)
+
+
+@pytest.mark.parametrize("tbar", [1, 2, 31, 32, 33, 255, 256, 300])
+@pytest.mark.parametrize("chunk", [16, 128])
+def test_grad_slow_decay_truncated(tbar, chunk):
+    w = SLOW
+    say(f"[grad trunc slow] workload={w.name} tbar={tbar} chunk={chunk}")
+    inp = _inputs(w)
+    g = _gpu_grad(inp, w, tbar, chunk)
+    ref = _oracle_grad(inp, w, tbar, literal=True)
+    _compare(g, ref, TOL_F32, False)
+    if 1 < tbar <= w.T // 4:
+        full = _oracle_grad(inp, w, 0)
+        assert np.linalg.norm(ref["dx"] - full["dx"]) > 1e-3 * np.linalg.norm(full["dx"])  # window visible
+
+
+RAGGED = Workload("ragged", 2, 250, 50, 5, 50, 0, False, False, 692100, delta_scale=0.25)
+
+
+@pytest.mark.parametrize("chunk,tbar", [(64, 0), (16, 0), (64, 37), (32, 100), (16, 249), (128, 250)])
+def test_grad_ragged_shapes(chunk, tbar):
+    """T not a multiple of the chunk, D not a multiple of 16, N < 16, batch 2, h0."""
+    w = RAGGED
+    say(f"[grad ragged] T={w.T} D={w.D} N={w.N} b={w.b} chunk={chunk} tbar={tbar}")
+    inp = _inputs(w, h0=True)
+    full = tbar == 0 or tbar >= w.T
+    g = _gpu_grad(inp, w, tbar, chunk, want_dh0=full)
+    _compare(g, _oracle_grad(inp, w, tbar, literal=True, want_dh0=full), TOL_F32, False, dh0=full)
+
+
+GATED32 = Workload("gated32", 2, 300, 40, 16, 40, 0, True, False, 692101)
+
+
+@pytest.mark.parametrize("chunk,tbar", [(64, 0), (128, 20), (256, 0)])
+def test_grad_gate_softplus_fp32(chunk, tbar):
+    w = GATED32
+    say(f"[grad gate fp32] chunk={chunk} tbar={tbar}")
+    inp = _inputs(w)
+    g = _gpu_grad(inp, w, tbar, chunk)
+    _compare(g, _oracle_grad(inp, w, tbar, literal=True), TOL_F32, True)
+    y = ssm.ssm_adjoint_forward(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], z=inp["z"],
+                                softplus=True, chunk=chunk)
+    torch.cuda.synchronize()
+    ry, _ = oracle.forward(*(to_np(inp[k]) for k in ("x", "delta", "A_log", "B", "C")), z=to_np(inp["z"]),
+                           delta_softplus=True)
+    check("y", to_np(y), ry, TOL_F32)
+
+
+BF16MID = Workload("bf16mid", 2, 1000, 256, 16, 128, 0, True, True, 692102)
+
+
+@pytest.mark.parametrize("tbar", [0, 64])
+def test_grad_bf16_gate(tbar):
+    w = BF16MID
+    say(f"[grad bf16 gate] T={w.T} D={w.D} tbar={tbar}")
+    inp = _inputs(w)
+    g = _gpu_grad(inp, w, tbar, 0)
+    _compare(g, _oracle_grad(inp, w, tbar), TOL_BF16, True)
+
+
+def test_grad_deterministic():
+    w = BF16MID
+    say("[determinism] two identical calls")
+    inp = _inputs(w)
+    a = _gpu_grad(inp, w, 64, 0)
+    b = _gpu_grad(inp, w, 64, 0)
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
