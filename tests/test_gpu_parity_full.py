@@ -1,0 +1,229 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times.  Where the fp64 oracle cannot run over the whole problem in
+seconds, it checks sampled outputs it can compute exactly:
+
+* per-channel outputs (dx, ddelta, dz, the dA_log row) of sampled channels, with
+  the oracle run over the full sequence for those channels only (channels are
+  independent except through dB and dC);
+* all-channel outputs (dB, dC and every per-channel output) on sampled time
+  windows, with the oracle run on a slice that starts PRE steps before the
+  window from a zero state and ends POST steps after it.  The states' decay makes
+  the slice exact to far below the tolerance: each step multiplies the carried
+  state by a <= exp(-Delta) with Delta = softplus(N(0,1)), so PRE = POST = 512
+  steps leave a factor of about exp(-400); the truncated adjoint only reaches
+  tbar steps ahead, which POST covers;
+* projection-gradient columns whose upstream factor is per-channel (dW_x
+  columns of dDelta_pre, dW_in columns of dz), and dx_total / du rows on the
+  sampled windows.
+The whole-layer chain is compared on every entry at the "layer" workload."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2501_00692_amd as ssm
+from paper_2501_00692_amd.synth import WORKLOADS, make_inputs
+
+from gpu_helpers import TOL_BF16, check, say, to_np
+
+pytestmark = pytest.mark.gpu
+
+PRE = 512
+POST = 512
+
+
+def _sel_channels(D, k=16, seed=5):
+    rng = np.random.default_rng(seed)
+    return np.sort(rng.choice(D, size=min(k, D), replace=False))
+
+
+def _windows(T, tbar, k=2, width=256, seed=7):
+    rng = np.random.default_rng(seed)
+    starts = [0, T - width]  # the sequence edges
+    for _ in range(k):
+        starts.append(int(rng.integers(PRE, max(PRE + 1, T - width - POST - tbar))))
+    return sorted(set(starts))
+
+
+def _scan_fn(tbar, T):
+    return oracle.bptt if tbar <= 0 or tbar >= T else oracle.trunc_tail
+
+
+def _oracle_channels(inp, w, tbar, sel):
+    """Per-channel oracle outputs for channels `sel` over the full sequence."""
+    s = torch.as_tensor(sel, device="cuda")
+    host = {k: to_np(inp[k].index_select(-1, s)) for k in ("x", "delta", "dy")}
+    if "z" in inp:
+        host["z"] = to_np(inp["z"].index_select(-1, s))
+    A = to_np(inp["A_log"])[sel]
+    B, C = to_np(inp["B"]), to_np(inp["C"])
+    fn = _scan_fn(tbar, w.T)
+    kw = dict(z=host.get("z"), delta_softplus=w.proj)
+    if fn is oracle.bptt:
+        return fn(host["x"], host["delta"], A, B, C, host["dy"], want_dh0=False, **kw)
+    return fn(host["x"], host["delta"], A, B, C, host["dy"], tbar=tbar, **kw)
+
+
+def _oracle_window(inp, w, tbar, t0, t1):
+    """All-channel oracle on the slice [t0-PRE, t1+POST+tbar) (clipped), zero state
+    at its start; returns outputs restricted to [t0, t1)."""
+    post = POST + (tbar if 0 < tbar < w.T else 0)
+    a, e = max(0, t0 - PRE), min(w.T, t1 + post)
+    sl = slice(a, e)
+    h = {k: to_np(inp[k][:, sl]) for k in ("x", "delta", "dy", "B", "C")}
+    z = to_np(inp["z"][:, sl]) if "z" in inp else None
+    A = to_np(inp["A_log"])
+    fn = _scan_fn(tbar, w.T)
+    kw = dict(z=z, delta_softplus=w.proj)
+    if fn is oracle.bptt:
+        r = fn(h["x"], h["delta"], A, h["B"], h["C"], h["dy"], want_dh0=False, **kw)
+    else:
+        r = fn(h["x"], h["delta"], A, h["B"], h["C"], h["dy"], tbar=tbar, **kw)
+    cut = slice(t0 - a, t1 - a)
+    return {k: (v[:, cut] if v is not None and v.ndim == 3 else v) for k, v in r.items()}
+
+
+def _check_scan_sampled(g, inp, w, tbar, rep):
+    sel = _sel_channels(w.D)
+    say(f"   oracle on {len(sel)} sampled channels, full sequence")
+    rc = _oracle_channels(inp, w, tbar, sel)
+    s = torch.as_tensor(sel, device="cuda")
+    for k in ("dx", "ddelta") + (("dz",) if w.proj else ()):
+        check(f"{k}[ch]", to_np(g[k].index_select(-1, s)), rc[k], TOL_BF16, rep)
+    check("dA_log[ch]", to_np(g["dA_log"])[sel], rc["dA_log"], TOL_BF16, rep)
+    wins = _windows(w.T, tbar if 0 < tbar < w.T else 0)
+    for t0 in wins:
+        t1 = t0 + 256
+        say(f"   oracle on window [{t0}, {t1}) over all channels")
+        rw = _oracle_window(inp, w, tbar, t0, t1)
+        for k in ("dB", "dC", "dx", "ddelta") + (("dz",) if w.proj else ()):
+            check(f"{k}[t{t0}]", to_np(g[k][:, t0:t1]), rw[k], TOL_BF16, rep)
+    return sel, wins
+
+
+@pytest.mark.parametrize("tbar", [0])
+def test_layer_workload_every_entry(tbar):
+    """b=2, T=4096, D=1536, d_model=768, N=16, full gradient with projections."""
+    w = WORKLOADS["layer"]
+    say(f"[layer full-size] {w}")
+    inp = make_inputs(w, device="cuda")
+    o = ssm.ssm_layer_grad(inp["u"], inp["x"], inp["z"], inp["delta"], inp["B"], inp["C"], inp["W_x"],
+                           inp["W_in"], inp["A_log"], inp["dy"], tbar=tbar, want_du=True, want_scan=True)
+    torch.cuda.synchronize()
+    h = {k: to_np(v) for k, v in inp.items()}
+    ref = oracle.layer_grad(h["u"], h["x"], h["z"], h["delta"], h["B"], h["C"], h["W_x"], h["A_log"], h["dy"],
+                            W_in=h["W_in"])
+    M = w.M
+    rep = {}
+    for k in ("dx", "ddelta", "dB", "dC", "dz", "dA_log"):
+        check(k, to_np(o[k]), ref[k], TOL_BF16, rep)
+    check("dx_total", to_np(o["dx_total"]).reshape(M, -1), ref["dx_total"], TOL_BF16, rep)
+    for k in ("dW_x", "dW_in"):
+        check(k, to_np(o[k]), ref[k], TOL_BF16, rep)
+    check("du", to_np(o["du"]).reshape(M, -1), ref["du"], TOL_BF16, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
+def _layer_sampled(name, tbar):
+    w = WORKLOADS[name]
+    say(f"[layer sampled] {w} tbar={tbar}")
+    inp = make_inputs(w, device="cuda")
+    o = ssm.ssm_layer_grad(inp["u"], inp["x"], inp["z"], inp["delta"], inp["B"], inp["C"], inp["W_x"],
+                           inp["W_in"], inp["A_log"], inp["dy"], tbar=tbar, want_du=True, want_scan=True)
+    torch.cuda.synchronize()
+    rep = {}
+    sel, wins = _check_scan_sampled(o, inp, w, tbar, rep)
+    # dW_x columns of dDelta_pre for the sampled channels; dW_in columns of dz
+    rc = _oracle_channels(inp, w, tbar, sel)
+    M, D, N = w.M, w.D, w.N
+    x = to_np(inp["x"]).reshape(M, D)
+    u = to_np(inp["u"]).reshape(M, -1)
+    check("dW_x[:,ch]", to_np(o["dW_x"])[:, sel], x.T @ rc["ddelta"].reshape(M, -1), TOL_BF16, rep)
+    check("dW_in[:,D+ch]", to_np(o["dW_in"])[:, D + sel], u.T @ rc["dz"].reshape(M, -1), TOL_BF16, rep)
+    del x, u
+    Wx, Win = to_np(inp["W_x"]), to_np(inp["W_in"])
+    for t0 in wins:
+        t1 = t0 + 256
+        rw = _oracle_window(inp, w, tbar, t0, t1)
+        dzx = np.concatenate([rw["ddelta"], rw["dB"], rw["dC"]], axis=-1)
+        dxt = rw["dx"] + dzx @ Wx.T
+        check(f"dx_total[t{t0}]", to_np(o["dx_total"][:, t0:t1]), dxt, TOL_BF16, rep)
+        du = np.concatenate([dxt, rw["dz"]], axis=-1) @ Win.T
+        check(f"du[t{t0}]", to_np(o["du"][:, t0:t1]), du, TOL_BF16, rep)
+    say("   rel-L2 max:", f"{max(rep.values()):.2e}", "over", len(rep), "checks")
+
+
+def test_long_workload_truncated_sampled():
+    """b=2, T=65536, D=1536, d_model=768, truncated tbar=2048 with projections."""
+    _layer_sampled("long", WORKLOADS["long"].tbar)
+
+
+@pytest.mark.parametrize("tbar", [0, 4096])
+def test_slice_workload_sampled(tbar):
+    """b=1, T=262144, D=4096, d_model=2048: full and truncated (tbar=4096)."""
+    _layer_sampled("slice", tbar)
+
+
+def test_vlong_workload_truncated_sampled():
+    """b=1, T=1,048,576, D=3072, truncated tbar=8192, scan only."""
+    w = WORKLOADS["vlong"]
+    say(f"[vlong sampled] {w}")
+    inp = make_inputs(w, device="cuda")
+    g = ssm.ssm_adjoint_grad(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], tbar=w.tbar)
+    torch.cuda.synchronize()
+    rep = {}
+    _check_scan_sampled(g, inp, w, w.tbar, rep)
+    say("   rel-L2 max:", f"{max(rep.values()):.2e}", "over", len(rep), "checks")
+
+
+def test_long_slow_decay_truncated():
+    """Slow decay (Delta / 2048) so that the 2048-step window is visible: full
+    shape on sampled channels, and every output on a reduced shape."""
+    w = WORKLOADS["long_slow"]
+    say(f"[long_slow] {w}")
+    inp = make_inputs(w, device="cuda")
+    g = ssm.ssm_adjoint_grad(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], tbar=w.tbar)
+    torch.cuda.synchronize()
+    rep = {}
+    sel = _sel_channels(w.D)
+    rc = _oracle_channels(inp, w, w.tbar, sel)
+    s = torch.as_tensor(sel, device="cuda")
+    for k in ("dx", "ddelta"):
+        check(f"{k}[ch]", to_np(g[k].index_select(-1, s)), rc[k], TOL_BF16, rep)
+    check("dA_log[ch]", to_np(g["dA_log"])[sel], rc["dA_log"], TOL_BF16, rep)
+    full = _oracle_channels(inp, w, 0, sel)
+    assert np.linalg.norm(rc["dx"] - full["dx"]) > 1e-2 * np.linalg.norm(full["dx"])  # window visible
+    del g, inp
+    small = w.with_(name="long_slow_small", b=1, T=8192, D=512)
+    inp = make_inputs(small, device="cuda")
+    g = ssm.ssm_adjoint_grad(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], tbar=w.tbar)
+    torch.cuda.synchronize()
+    h = {k: to_np(v) for k, v in inp.items()}
+    ref = oracle.trunc_tail(h["x"], h["delta"], h["A_log"], h["B"], h["C"], h["dy"], tbar=w.tbar)
+    for k in ("dx", "ddelta", "dA_log", "dB", "dC"):
+        check(k, to_np(g[k]), ref[k], TOL_BF16, rep)
+    say("   rel-L2 max:", f"{max(rep.values()):.2e}", "over", len(rep), "checks")
+
+
+def test_proj_grad_slice_shapes_sampled():
+    """The projection GEMMs at the slice workload's shapes (M = 262,144 rows):
+    sampled dW entries and dX rows against the oracle's plain loops."""
+    M, D, N, dm = 262144, 4096, 16, 2048
+    say(f"[proj sampled] M={M} K={D} N={D + 2 * N}")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4242)
+    X = torch.randn(M, D, generator=g, device="cuda").to(torch.bfloat16)
+    dZ = torch.randn(M, D + 2 * N, generator=g, device="cuda").to(torch.bfloat16)
+    W = (torch.randn(D, D + 2 * N, generator=g, device="cuda") / 64).to(torch.bfloat16)
+    dW, dX = ssm.ssm_proj_grad(X, dZ, W, want_dW=True, want_dX=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    kk = rng.integers(0, D, 4096)
+    jj = rng.integers(0, D + 2 * N, 4096)
+    rows = np.sort(rng.choice(M, 256, replace=False))
+    bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)
+    Xb, Zb, Wb = bits(X), bits(dZ), bits(W)
+    rep = {}
+    check("dW[sampled]", to_np(dW)[kk, jj], oracle.proj_dw(Xb, Zb, kk, jj), TOL_BF16, rep)
+    check("dX[rows]", to_np(dX[torch.as_tensor(rows, device="cuda")]), oracle.proj_dx(Zb, Wb, rows), TOL_BF16, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
