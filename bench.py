@@ -1,0 +1,248 @@
+"""Benchmark of the per-layer adjoint gradient on one MI355X.
+
+One step = one whole-layer gradient call (``ssm_layer_grad``): the chunked
+forward recomputation, the reverse adjoint scan with its vjp epilogue, and the
+projection-gradient GEMMs, on the "layer" workload (b=2, T=4096, d_model=768,
+D=1536, N=16, full gradient; bf16 activations, fp32 accumulation).  Inputs are
+seeded synthetic tensors already resident in HBM.  The other workloads are
+reported under "extra".
+
+Prints ONE JSON line.  ``--gpus`` above 1 is not supported (one GPU).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA
+
+
+def scan_bytes_per_token(D, N, s, gate):
+    """Compulsory HBM bytes per token of the scan gradient: every input read once
+    and every output written once at the ABI's dtypes (outputs fp32)."""
+    if gate:  # reads x, Delta_pre, dy, z; writes dx, dDelta_pre, dz
+        per_ch = 4 * s + 12
+    else:     # reads x, Delta, dy; writes dx, dDelta
+        per_ch = 3 * s + 8
+    return D * per_ch + N * (2 * s + 8)  # reads B, C; writes dB, dC
+
+
+def layer_gemm_flops(M, D, N, dm, with_du=False):
+    f = 2 * M * D * (D + 2 * N)        # dW_x = x^T dZx
+    f += 2 * M * (D + 2 * N) * D       # dx_total = dx + dZx W_x^T
+    f += 2 * M * dm * 2 * D            # dW_in = u^T [dx_total | dz]
+    if with_du:
+        f += 2 * M * 2 * D * dm
+    return f
+
+
+def _timed(fn, steps, warmup, torch):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        fn()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) / steps
+
+
+def _kernel_times(fn, steps, ssm, torch):
+    """Per-kernel average launch duration (ms) from hipEvents recorded on the
+    launch stream around every kernel of `steps` calls."""
+    torch.cuda.synchronize()
+    ssm.timing_summary()
+    ssm.timing_enable(True)
+    for _ in range(steps):
+        fn()
+    ssm.timing_enable(False)
+    torch.cuda.synchronize()
+    out = {}
+    for name, (n, ms) in ssm.timing_summary().items():
+        out[name] = {"launches": n, "total_ms": ms, "avg_ms": ms / n, "launches_per_step": n / steps}
+    return out
+
+
+def layer_step(w, inp, ssm, torch, tbar=0):
+    b, T, D, N, dm = w.b, w.T, w.D, w.N, w.d_model
+    f32 = dict(dtype=torch.float32, device="cuda")
+    out = {"dW_in": torch.empty(dm, 2 * D, **f32), "dW_x": torch.empty(D, D + 2 * N, **f32),
+           "dA_log": torch.empty(D, N, **f32)}
+    desc = ssm.make_desc(inp["x"], N, True, True, 0)
+    ws = torch.empty(ssm.layer_workspace_size(desc, tbar, dm), dtype=torch.uint8, device="cuda")
+
+    def step():
+        ssm.ssm_layer_grad(inp["u"], inp["x"], inp["z"], inp["delta"], inp["B"], inp["C"], inp["W_x"],
+                           inp["W_in"], inp["A_log"], inp["dy"], tbar=tbar, out=out, workspace=ws)
+    return step
+
+
+def scan_step(w, inp, ssm, torch, tbar=0):
+    b, T, D, N = w.b, w.T, w.D, w.N
+    f32 = dict(dtype=torch.float32, device="cuda")
+    out = {"dx": torch.empty(b, T, D, **f32), "ddelta": torch.empty(b, T, D, **f32),
+           "dA_log": torch.empty(D, N, **f32), "dB": torch.empty(b, T, N, **f32), "dC": torch.empty(b, T, N, **f32)}
+    z = inp.get("z") if w.proj else None
+    if z is not None:
+        out["dz"] = torch.empty(b, T, D, **f32)
+    desc = ssm.make_desc(inp["x"], N, w.proj, z is not None, 0)
+    ws = torch.empty(ssm.grad_workspace_size(desc, tbar), dtype=torch.uint8, device="cuda")
+
+    def step():
+        ssm.ssm_adjoint_grad(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], z=z,
+                             softplus=w.proj, tbar=tbar, out=out, workspace=ws)
+    return step
+
+
+def roofline_for(kern, ktimes, w, kind):
+    """Roofline entry for kernel `kern` (algorithmic work per launch / average
+    launch duration)."""
+    kt = ktimes[kern]
+    s = 2 if w.bf16 else 4
+    if kern == "grad_fused":
+        per_launch = scan_bytes_per_token(w.D, w.N, s, w.proj) * w.M  # bytes
+        ach = per_launch / (kt["avg_ms"] * 1e-3) / 1e9
+        return {"kernel": kern, "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": ach / HBM_PEAK_GBS, "traffic": None, "avg_ms": kt["avg_ms"],
+                "algorithmic_bytes_per_launch": per_launch}
+    if kern in ("gemm_dw", "gemm_dx"):
+        M, D, N, dm = w.M, w.D, w.N, w.d_model
+        if kern == "gemm_dw":
+            flops = 2 * M * D * (D + 2 * N) + 2 * M * dm * 2 * D
+        else:
+            flops = 2 * M * (D + 2 * N) * D
+        per_launch = flops / kt["launches_per_step"]
+        ach = per_launch / (kt["avg_ms"] * 1e-3) / 1e12
+        return {"kernel": kern, "bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": ach / MFMA_BF16_PEAK_TFS, "traffic": None, "avg_ms": kt["avg_ms"],
+                "algorithmic_flops_per_launch": per_launch}
+    return None
+
+
+def cpu_baseline(w, T_sample=256):
+    """The fp64 oracle (layer gradient incl. projections) on the first T_sample
+    tokens of every batch row of the workload, all channels."""
+    import numpy as np
+
+    import oracle
+    from paper_2501_00692_amd.synth import make_inputs
+
+    ws = w.with_(T=T_sample)
+    inp = make_inputs(ws, device="cpu")
+    h = {k: v.float().double().numpy() for k, v in inp.items()}
+    nthreads = oracle.max_threads()
+    t0 = time.perf_counter()
+    if w.proj:
+        oracle.layer_grad(h["u"], h["x"], h["z"], h["delta"], h["B"], h["C"], h["W_x"], h["A_log"], h["dy"],
+                          tbar=w.tbar, scan=oracle.trunc_tail if w.tbar else None)
+    else:
+        oracle.trunc_tail(h["x"], h["delta"], h["A_log"], h["B"], h["C"], h["dy"], tbar=w.tbar)
+    dt = time.perf_counter() - t0
+    del np
+    return {"value": ws.b * T_sample / dt, "unit": "tokens/s", "cores": nthreads, "kind": "oracle",
+            "sample": f"fp64 oracle layer gradient (BPTT scan + projection chain) on b={ws.b} x T={T_sample} "
+                      f"tokens of the {w.name} workload, all {w.D} channels; {dt:.2f} s wall on {nthreads} "
+                      f"OpenMP threads (numpy BLAS for the projection products)"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-tokens", type=int, default=4096)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one GPU only "
+              f"(the multi-GPU sharding is a design, not an implementation)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2501_00692_amd as ssm
+    from paper_2501_00692_amd.synth import WORKLOADS, make_inputs
+
+    torch.cuda.set_device(0)
+    w = WORKLOADS["layer"]
+    inp = make_inputs(w, device="cuda")
+    step = layer_step(w, inp, ssm, torch, tbar=0)
+    ms = _timed(step, args.steps, args.warmup, torch)
+    ktimes = _kernel_times(step, args.steps, ssm, torch)
+    dom = max(ktimes, key=lambda k: ktimes[k]["total_ms"])
+    roof = roofline_for(dom, ktimes, w, "layer")
+    value = w.M / (ms * 1e-3)
+
+    extra = {"kernels_layer": ktimes,
+             "roofline_other": {k: roofline_for(k, ktimes, w, "layer") for k in ("grad_fused", "gemm_dw", "gemm_dx")
+                                if k in ktimes and k != dom},
+             "gemm_tflops_layer": layer_gemm_flops(w.M, w.D, w.N, w.d_model) / 1e12}
+    del inp, step
+    torch.cuda.empty_cache()
+
+    if not args.no_extra:
+        runs = [("small", "scan", 0), ("small", "scan", 32), ("long", "layer", 2048), ("long", "scan", 2048),
+                ("long_slow", "scan", 2048), ("slice", "layer", 0), ("slice", "layer", 4096),
+                ("vlong", "scan", 8192)]
+        res = {}
+        for name, kind, tbar in runs:
+            wl = WORKLOADS[name]
+            x = make_inputs(wl, device="cuda")
+            st = (layer_step if kind == "layer" else scan_step)(wl, x, ssm, torch, tbar=tbar)
+            steps = 5 if wl.M >= 262144 else 10
+            m = _timed(st, steps, 2, torch)
+            kt = _kernel_times(st, 2, ssm, torch)
+            entry = {"ms_per_step": m, "tokens_per_s": wl.M / (m * 1e-3), "tbar": tbar,
+                     "grad_fused_avg_ms": kt.get("grad_fused", {}).get("avg_ms")}
+            r = roofline_for("grad_fused", kt, wl, kind)
+            if r:
+                entry["grad_fused_GBps"] = r["achieved"]
+                entry["grad_fused_hbm_frac"] = r["frac"]
+            for g in ("gemm_dw", "gemm_dx"):
+                if g in kt:
+                    rg = roofline_for(g, kt, wl, kind)
+                    entry[f"{g}_TFLOPs"] = rg["achieved"]
+            res[f"{name}/{kind}/tbar={tbar}"] = entry
+            del x, st
+            torch.cuda.empty_cache()
+        extra["workloads"] = res
+
+    line = {
+        "metric": "SSM-layer adjoint-gradient tokens/sec (full & truncated Tbar); % HBM/MFMA peak",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp32",
+        "data": "synthetic",
+        "config": {"workload": "layer: one selective diagonal SSM layer with input projections and SiLU gate, "
+                               "b=2, T=4096, d_model=768, D=1536, N=16, full adjoint gradient",
+                   "batch": w.b, "seq_len": w.T, "d_model": w.d_model, "channels": w.D, "dstate": w.N,
+                   "inputs": "bf16", "accumulate": "fp32", "chunk": 128},
+        "roofline": roof,
+    }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_tokens)
+    line["extra"] = extra
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

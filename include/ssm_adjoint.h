@@ -157,6 +157,16 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
                           float* dC, float* dz, float* dx_total, void* workspace,
                           size_t workspace_bytes, void* stream);
 
+/* Measurement support (not part of the method).  While enabled, every kernel the
+ * library launches is bracketed by two hipEvents recorded on its stream;
+ * ssm_timing_summary waits for the recorded events, writes one line
+ * "<kernel> <launches> <total_ms>" per kernel name into buf (NUL-terminated,
+ * truncated to len; SSM_ERR_SHAPE if truncated, SSM_ERR_HIP if an event failed)
+ * and clears the records.  Timing adds an event pair per launch and is meant for
+ * profiling runs only.  Not thread-safe across concurrent profiling sessions. */
+ssm_status ssm_timing_enable(int32_t on);
+ssm_status ssm_timing_summary(char* buf, size_t len);
+
 /* Thread-local, NUL-terminated description of the last non-OK status returned on
  * the calling thread ("" if none).  Owned by the library. */
 const char* ssm_last_error(void);

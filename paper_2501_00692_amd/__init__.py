@@ -32,7 +32,8 @@ STATUS = {0: "SSM_OK", 1: "SSM_ERR_NULL", 2: "SSM_ERR_SHAPE", 3: "SSM_ERR_DTYPE"
 EXPORTED = (
     "ssm_adjoint_forward_workspace_size", "ssm_adjoint_grad_workspace_size", "ssm_adjoint_forward",
     "ssm_adjoint_grad", "ssm_proj_grad_workspace_size", "ssm_proj_grad",
-    "ssm_layer_grad_workspace_size", "ssm_layer_grad", "ssm_last_error",
+    "ssm_layer_grad_workspace_size", "ssm_layer_grad", "ssm_timing_enable", "ssm_timing_summary",
+    "ssm_last_error",
 )
 
 
@@ -77,6 +78,10 @@ def load_library():
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
+    lib.ssm_timing_enable.argtypes = [i32]
+    lib.ssm_timing_enable.restype = ctypes.c_int
+    lib.ssm_timing_summary.argtypes = [ctypes.c_char_p, sz]
+    lib.ssm_timing_summary.restype = ctypes.c_int
     lib.ssm_last_error.argtypes = []
     lib.ssm_last_error.restype = ctypes.c_char_p
     _lib = lib
@@ -85,6 +90,25 @@ def load_library():
 
 def last_error() -> str:
     return load_library().ssm_last_error().decode()
+
+
+def timing_enable(on: bool = True):
+    """Bracket every library kernel launch with hipEvents on its stream (profiling)."""
+    load_library().ssm_timing_enable(1 if on else 0)
+
+
+def timing_summary() -> dict:
+    """Per-kernel ``{name: (launches, total_ms)}`` of the launches recorded since the
+    last summary (waits for their events)."""
+    buf = ctypes.create_string_buffer(1 << 16)
+    rc = load_library().ssm_timing_summary(buf, len(buf))
+    if rc != 0:
+        raise SsmError(rc, "ssm_timing_summary", "event timing failed")
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, n, ms = line.split()
+        out[name] = (int(n), float(ms))
+    return out
 
 
 def _check(rc: int, where: str):

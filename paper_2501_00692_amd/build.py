@@ -11,7 +11,11 @@ from pathlib import Path
 
 PKG = Path(__file__).resolve().parent
 ROOT = PKG.parent
-SRC = [PKG / "csrc" / "scan.hip", PKG / "csrc" / "gemm.hip", PKG / "csrc" / "abi.cpp"]
+CSRC = PKG / "csrc"
+SRC = [CSRC / "scan.hip", CSRC / "scan_grad_f32_full.hip", CSRC / "scan_grad_f32_trunc.hip",
+       CSRC / "scan_grad_bf16_full.hip", CSRC / "scan_grad_bf16_trunc.hip", CSRC / "gemm.hip",
+       CSRC / "abi.cpp", CSRC / "timing.cpp"]
+OBJ = PKG / "_build"
 LIB = PKG / "libssm_adjoint.so"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -20,7 +24,6 @@ FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     "-Wall",
     # no packed fp32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -29,9 +32,25 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> Path:
+def _compile(src: Path, verbose: bool) -> Path:
+    obj = OBJ / (src.name + ".o")
+    cmd = [HIPCC, *FLAGS, "-c", "-o", str(obj), str(src)]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return obj
+
+
+def build(verbose: bool = False, jobs: int | None = None) -> Path:
+    """Compile every source (in parallel) and link the shared library."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    OBJ.mkdir(exist_ok=True)
+    jobs = jobs or min(len(SRC), os.cpu_count() or 1)
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), SRC))
     tmp = LIB.with_suffix(".so.tmp")
-    cmd = [HIPCC, *FLAGS, "-o", str(tmp), *map(str, SRC)]
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", str(tmp), *map(str, objs)]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

@@ -296,6 +296,7 @@ hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, in
     dim3 grid(cdiv(N, BN), cdiv(K, BM), static_cast<unsigned>(splits));
     const bool direct = splits == 1;
     float* out = direct ? dW : static_cast<float*>(ws);
+    SSMK_TIMED("gemm_dw", s);
     hipLaunchKernelGGL(k_gemm_dw, grid, dim3(256), 0, s, M, K, N, X, ldx, dZ, lddz, out, per,
                        direct ? 1 : 0, accum ? 1 : 0);
     if (!direct)
@@ -308,6 +309,7 @@ hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, i
                           const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
                           uint16_t* out16, int64_t ld16, hipStream_t s) {
     dim3 grid(cdiv(K, BN), cdiv(M, BM));
+    SSMK_TIMED("gemm_dx", s);
     hipLaunchKernelGGL(k_gemm_dx, grid, dim3(256), 0, s, M, K, N, dZ, lddz, W, ldw, dX,
                        accum ? 1 : 0, add, out16, ld16);
     return hipGetLastError();
@@ -315,6 +317,7 @@ hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, i
 
 hipError_t launch_pack_bf16(int64_t rows, int64_t cols, const float* src, int64_t lds,
                             uint16_t* dst, int64_t ldd, int64_t col0, hipStream_t s) {
+    SSMK_TIMED("pack", s);
     hipLaunchKernelGGL(k_pack, dim3(cdiv(rows * cols, 256)), dim3(256), 0, s, rows, cols, src, lds,
                        dst, ldd, col0);
     return hipGetLastError();

@@ -8,6 +8,25 @@
 
 namespace ssmk {
 
+// Opt-in per-kernel timing (timing.cpp): while enabled, a TimedScope records a
+// hipEvent on the launch stream before and after the kernel launched inside it.
+bool timing_enabled();
+class TimedScope {
+  public:
+    TimedScope(const char* name, hipStream_t s);
+    ~TimedScope();
+    TimedScope(const TimedScope&) = delete;
+    TimedScope& operator=(const TimedScope&) = delete;
+
+  private:
+    bool on_;
+    hipStream_t s_;
+    size_t idx_ = 0;
+};
+#define SSMK_CAT2(a, b) a##b
+#define SSMK_CAT(a, b) SSMK_CAT2(a, b)
+#define SSMK_TIMED(name, s) ::ssmk::TimedScope SSMK_CAT(ssmk_timed_, __LINE__)(name, s)
+
 // One scan problem: the selective diagonal layer of shape [b][T][D] x N states,
 // split into nc = ceil(T / L) carry chunks of L steps.
 struct ScanProblem {
