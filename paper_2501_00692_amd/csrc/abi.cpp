@@ -279,7 +279,7 @@ ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, co
     ssmk::ScanProblem p = make_problem(desc, L, nc);
     p.trunc = trunc;
     p.tbar = trunc ? tbar : 0;
-    p.nsplit = ssmk::choose_nsplit(p.nb, p.D, nc);
+    ssmk::choose_split(p.nb, p.D, nc, &p.nsplit, &p.tps);
     p.nslice = ssmk::choose_nslice(p.nb, nc);
     grad_bind(p, x, delta, A_log, B, C, h0, z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0);
     ssmk::bind_workspace(p, workspace, w);
@@ -414,7 +414,7 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     ssmk::ScanProblem p = make_problem(&sd, L, nc);
     p.trunc = trunc;
     p.tbar = trunc ? tbar : 0;
-    p.nsplit = ssmk::choose_nsplit(p.nb, p.D, nc);
+    ssmk::choose_split(p.nb, p.D, nc, &p.nsplit, &p.tps);
     p.nslice = ssmk::choose_nslice(p.nb, nc);
     grad_bind(p, x, delta_pre, A_log, B, C, nullptr, z, dy, dx_, dd_, dA_log, dB_, dC_, dz_, nullptr);
     ssmk::bind_workspace(p, ws + w.scan_off, sw);

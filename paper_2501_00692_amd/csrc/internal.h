@@ -37,6 +37,7 @@ struct ScanProblem {
     bool trunc;      // truncated estimator with window tbar (< T)
     int64_t tbar;
     int nsplit;      // channel splits of the fused kernel (dB/dC partials when > 1)
+    int tps;         // 16-channel tiles per split (every split has at least one)
     int nslice;      // slices of the dA_log reduction
     // inputs
     const void* x;
@@ -74,7 +75,7 @@ struct ScanWorkspace {
 
 int64_t default_chunk();
 bool chunk_supported(int64_t L);
-int choose_nsplit(int64_t nb, int64_t D, int64_t nc);
+void choose_split(int64_t nb, int64_t D, int64_t nc, int* nsplit, int* tiles_per_split);
 int choose_nslice(int64_t nb, int64_t nc);
 ScanWorkspace scan_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t L, bool grad,
                              bool trunc);

@@ -7,9 +7,8 @@ namespace {
 
 template <typename TI>
 hipError_t forward_dispatch(const ScanProblem& p, hipStream_t s) {
-    const bool n16 = p.N == 16;
 #define SSMK_FWD(SP, GT) \
-    return n16 ? forward_impl<TI, SP, GT, true>(p, s) : forward_impl<TI, SP, GT, false>(p, s)
+    return forward_impl<TI, SP, GT>(p, s)
     if (p.softplus) {
         if (p.gate) SSMK_FWD(true, true);
         SSMK_FWD(true, false);
@@ -27,15 +26,17 @@ int64_t default_chunk() { return 128; }
 
 bool chunk_supported(int64_t L) { return L == 16 || L == 32 || L == 64 || L == 128 || L == 256; }
 
-int choose_nsplit(int64_t nb, int64_t D, int64_t nc) {
-    // Enough single-wave workgroups to fill 256 CUs several times over, but
-    // no more splits than 16-channel tiles.
-    const int64_t target = 4096;
+void choose_split(int64_t nb, int64_t D, int64_t nc, int* nsplit, int* tiles_per_split) {
+    // Enough single-wave workgroups to fill 256 CUs several times over; every
+    // split gets at least one 16-channel tile.
+    const int64_t target = 2048;
     const int64_t ntile = (D + 15) / 16;
     int64_t ns = (target + nb * nc - 1) / (nb * nc);
     if (ns < 1) ns = 1;
     if (ns > ntile) ns = ntile;
-    return static_cast<int>(ns);
+    const int64_t tps = (ntile + ns - 1) / ns;
+    *tiles_per_split = static_cast<int>(tps);
+    *nsplit = static_cast<int>((ntile + tps - 1) / tps);
 }
 
 int choose_nslice(int64_t nb, int64_t nc) {
@@ -62,7 +63,8 @@ ScanWorkspace scan_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_
     if (grad && trunc) off = align_up(off + static_cast<size_t>(nb * (nc + 1) * D) * sizeof(double));
     w.off_pB = w.off_pC = w.off_dAtmp = off;
     if (grad) {
-        const int ns = choose_nsplit(nb, D, nc);
+        int ns, tps;
+        choose_split(nb, D, nc, &ns, &tps);
         if (ns > 1) {
             const size_t part = static_cast<size_t>(ns) * nb * T * N * sizeof(float);
             w.off_pB = off;

@@ -8,11 +8,12 @@
 //                  and the truncated window of Eq. "capped";
 //   k_reduce_*   : deterministic reductions of the dB/dC and dA_log partials.
 //
-// Thread layout of the per-step kernels: one wave of 64 lanes covers 16
-// channels; the 4 lanes of a quad share a channel and hold 4 of its 16 states
-// each, so per-channel sums over the state are two DPP quad swaps.  Loads of
-// x, Delta, dy, z are coalesced along the contiguous channel dimension; B_t and
-// C_t are the same for every channel and are vector-loaded per lane.
+// Thread layouts: the chunk-aggregate and forward kernels give each lane one
+// channel with all of its states in registers; the fused gradient kernel gives a
+// wave 16 channels, the 4 lanes of a quad sharing a channel and holding 4 of its
+// 16 states each, so per-channel sums over the state are two DPP quad swaps.
+// Loads of x, Delta, dy, z are coalesced along the contiguous channel
+// dimension; B_t and C_t are the same for every channel.
 #pragma once
 
 #include "internal.h"
@@ -101,17 +102,25 @@ __device__ __forceinline__ void lane_consts(const float* A_log, int64_t d, int r
     }
 }
 
+// Uniform loads of the (up to) 16 states of row `row` of a [rows][N] tensor:
+// the same for every lane of the wave.
+template <typename TI>
+__device__ __forceinline__ void ld_row16(const TI* p, int64_t row, int64_t N, float v[16]) {
+#pragma unroll
+    for (int n = 0; n < 16; ++n) v[n] = n < N ? ldf(p, row * N + n) : 0.f;
+}
+
 // ---------------------------------------------------------------------------
-// k_chunk_aggr: grid (ceil(D/64), nc, b), 256 threads (64 channels).
-// For chunk c = [s, e]: hloc = state at e from a zero carry-in,
-// mloc = sum_{t in c} g_t C_t prod_{j=s}^{t} a_j  (the adjoint that the chunk
-// hands to h_{s-1} from a zero carry at its end), sdel = sum_t Delta_t.
+// k_chunk_aggr: grid (ceil(D/256), nc, b), 256 threads, one lane per channel
+// holding all 16 states.  For chunk c = [s, e]:
+//   hloc = state at e from a zero carry-in,
+//   mloc = sum_{t in c} g_t C_t prod_{j=s}^{t} a_j  (the adjoint that the chunk
+//          hands to h_{s-1} from a zero carry at its end),
+//   sdel = sum_{t in c} Delta_t (fp64).
 // ---------------------------------------------------------------------------
-template <typename TI, bool SP, bool GATE, bool WANT_M, bool N16>
+template <typename TI, bool SP, bool GATE, bool WANT_M>
 __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
-    const int lane = threadIdx.x;
-    const int r = lane & 3;
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (lane >> 2);
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const bool dv = d < p.D;
     const TI* X = static_cast<const TI*>(p.x);
@@ -120,13 +129,18 @@ __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
     const TI* Cp = static_cast<const TI*>(p.C);
     const TI* DY = static_cast<const TI*>(p.dy);
     const TI* Z = static_cast<const TI*>(p.z);
-
-    float cn[4], wn[4];
-    lane_consts(p.A_log, d, r, p.N, dv, cn, wn);
-    float h[4] = {0.f, 0.f, 0.f, 0.f}, m[4] = {0.f, 0.f, 0.f, 0.f}, P[4] = {1.f, 1.f, 1.f, 1.f};
+    float cn[16], h[16], m[16], P[16];
+#pragma unroll
+    for (int n = 0; n < 16; ++n) {
+        cn[n] = (dv && n < p.N) ? -__expf(p.A_log[d * p.N + n]) * kLog2e : 0.f;
+        h[n] = 0.f;
+        m[n] = 0.f;
+        P[n] = 1.f;
+    }
     double sd = 0.0;
     const int64_t t0 = c * p.L;
     const int64_t t1 = min(t0 + p.L, p.T);
+#pragma unroll 2
     for (int64_t t = t0; t < t1; ++t) {
         const int64_t td = (bb * p.T + t) * p.D + d;
         float xv = 0.f, dl = 0.f, g = 0.f;
@@ -144,31 +158,30 @@ __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
                 }
             }
         }
-        float Bv[4], Cv[4];
-        ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, true, Bv);
-        if constexpr (WANT_M) ld4<TI, N16>(Cp, bb * p.T + t, r, p.N, true, Cv);
+        float Bv[16], Cv[16];
+        ld_row16(Bp, bb * p.T + t, p.N, Bv);
+        if constexpr (WANT_M) ld_row16(Cp, bb * p.T + t, p.N, Cv);
         sd += static_cast<double>(dl);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const float av = fexp2(cn[k] * dl);
-            h[k] = fmaf(av, h[k], Bv[k] * xv);
+        for (int n = 0; n < 16; ++n) {
+            const float av = fexp2(cn[n] * dl);
+            h[n] = fmaf(av, h[n], Bv[n] * xv);
             if constexpr (WANT_M) {
-                P[k] *= av;
-                m[k] = fmaf(g * Cv[k], P[k], m[k]);
+                P[n] *= av;
+                m[n] = fmaf(g * Cv[n], P[n], m[n]);
             }
         }
     }
     if (!dv) return;
     const int64_t cb = ((bb * p.nc + c) * p.N) * p.D + d;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int n = r * 4 + k;
+    for (int n = 0; n < 16; ++n) {
         if (n < p.N) {
-            p.hbuf[cb + n * p.D] = h[k];
-            if constexpr (WANT_M) p.mbuf[cb + n * p.D] = m[k];
+            p.hbuf[cb + n * p.D] = h[n];
+            if constexpr (WANT_M) p.mbuf[cb + n * p.D] = m[n];
         }
     }
-    if (r == 0) p.sdel[(bb * p.nc + c) * p.D + d] = sd;
+    p.sdel[(bb * p.nc + c) * p.D + d] = sd;
 }
 
 // ---------------------------------------------------------------------------
@@ -249,55 +262,50 @@ __global__ __launch_bounds__(256) void k_carry(const ScanProblem p) {
 }
 
 // ---------------------------------------------------------------------------
-// k_forward: grid (ceil(D/64), nc, b), 256 threads.  y_t = sum_n C_t h_t
-// (times silu(z_t) with the gate), state recomputed from the chunk carry-in.
+// k_forward: grid (ceil(D/256), nc, b), 256 threads, one lane per channel.
+// y_t = sum_n C_t h_t (times silu(z_t) with the gate), the state recomputed from
+// the chunk carry-in.
 // ---------------------------------------------------------------------------
-template <typename TI, bool SP, bool GATE, bool N16>
+template <typename TI, bool SP, bool GATE>
 __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
-    const int lane = threadIdx.x;
-    const int r = lane & 3;
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (lane >> 2);
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     const int64_t c = blockIdx.y, bb = blockIdx.z;
-    const bool dv = d < p.D;
+    if (d >= p.D) return;
     const TI* X = static_cast<const TI*>(p.x);
     const TI* DL = static_cast<const TI*>(p.delta);
     const TI* Bp = static_cast<const TI*>(p.B);
     const TI* Cp = static_cast<const TI*>(p.C);
     const TI* Z = static_cast<const TI*>(p.z);
     TI* Y = static_cast<TI*>(p.y);
-    float cn[4], wn[4];
-    lane_consts(p.A_log, d, r, p.N, dv, cn, wn);
-    float h[4];
     const int64_t cb = ((bb * p.nc + c) * p.N) * p.D + d;
+    float cn[16], h[16];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) h[k] = (dv && r * 4 + k < p.N) ? p.hbuf[cb + (r * 4 + k) * p.D] : 0.f;
+    for (int n = 0; n < 16; ++n) {
+        cn[n] = n < p.N ? -__expf(p.A_log[d * p.N + n]) * kLog2e : 0.f;
+        h[n] = n < p.N ? p.hbuf[cb + n * p.D] : 0.f;
+    }
     const int64_t t0 = c * p.L;
     const int64_t t1 = min(t0 + p.L, p.T);
+#pragma unroll 2
     for (int64_t t = t0; t < t1; ++t) {
         const int64_t td = (bb * p.T + t) * p.D + d;
-        float xv = 0.f, dl = 0.f;
-        if (dv) {
-            xv = ldf(X, td);
-            const float pv = ldf(DL, td);
-            dl = SP ? softplus_f(pv) : pv;
-        }
-        float Bv[4], Cv[4];
-        ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, true, Bv);
-        ld4<TI, N16>(Cp, bb * p.T + t, r, p.N, true, Cv);
-        float yp = 0.f;
+        const float xv = ldf(X, td);
+        const float pv = ldf(DL, td);
+        const float dl = SP ? softplus_f(pv) : pv;
+        float Bv[16], Cv[16];
+        ld_row16(Bp, bb * p.T + t, p.N, Bv);
+        ld_row16(Cp, bb * p.T + t, p.N, Cv);
+        float y = 0.f;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
-            yp = fmaf(Cv[k], h[k], yp);
+        for (int n = 0; n < 16; ++n) {
+            h[n] = fmaf(fexp2(cn[n] * dl), h[n], Bv[n] * xv);
+            y = fmaf(Cv[n], h[n], y);
         }
-        float y = quad_sum(yp);
-        if (r == 0 && dv) {
-            if constexpr (GATE) {
-                const float zv = ldf(Z, td);
-                y *= zv * sigmoid_f(zv);
-            }
-            stf(Y, td, y);
+        if constexpr (GATE) {
+            const float zv = ldf(Z, td);
+            y *= zv * sigmoid_f(zv);
         }
+        stf(Y, td, y);
     }
 }
 
@@ -325,68 +333,109 @@ __device__ __forceinline__ void ck_get(const float (&ck)[NCK][4], int q, float (
     }
 }
 
-// Sum over the 16 channels of the wave of a per-(channel, state) value, for one
-// time step, and add it into acc_row[off + n].  Fixed summation order.
-__device__ __forceinline__ void channel_sum_add(float (*buf)[17], const float v[4], int lane,
-                                                float* acc_row, int off) {
-    const int ch = lane >> 2, r = lane & 3;
+// Broadcast lane `src` (0..3, a compile-time constant after unrolling) of each
+// quad to the whole quad.
+__device__ __forceinline__ float quad_bcast(float v, int src) {
+    const int iv = __float_as_int(v);
+    switch (src & 3) {
+        case 0: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0x00, 0xF, 0xF, true));
+        case 1: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0x55, 0xF, 0xF, true));
+        case 2: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0xAA, 0xF, 0xF, true));
+        default: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0xFF, 0xF, 0xF, true));
+    }
+}
+
+// Raw per-(step, channel) inputs of the steps a lane prepares for its quad.
+template <int SPL>
+struct RawIn {
+    float x[SPL], p[SPL], dy[SPL], z[SPL];
+};
+
+// Load the raw inputs of the steps j = r + 4*jj of segment [ts, ts+S) (zero where
+// t >= T or the channel is padding).  `full` also loads dy and z.
+template <typename TI, bool GATE, int SPL>
+__device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64_t ts, int64_t d,
+                                         bool dv, int r, bool full, RawIn<SPL>& o) {
+    const TI* X = static_cast<const TI*>(p.x);
+    const TI* DL = static_cast<const TI*>(p.delta);
+    const TI* DY = static_cast<const TI*>(p.dy);
+    const TI* Z = static_cast<const TI*>(p.z);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) buf[r * 4 + k][ch] = v[k];
-    __syncthreads();
-    const int n = lane >> 2, part = lane & 3;
-    float s = ((buf[n][part * 4 + 0] + buf[n][part * 4 + 1]) + buf[n][part * 4 + 2]) +
-              buf[n][part * 4 + 3];
-    s = quad_sum(s);
-    if (part == 0) acc_row[off + n] += s;
-    __syncthreads();
+    for (int jj = 0; jj < SPL; ++jj) {
+        const int64_t t = ts + r + 4 * jj;
+        const bool v = dv && t < p.T;
+        const int64_t td = (bb * p.T + t) * p.D + d;
+        o.x[jj] = v ? ldf(X, td) : 0.f;
+        o.p[jj] = v ? ldf(DL, td) : 0.f;
+        if (full) {
+            o.dy[jj] = v ? ldf(DY, td) : 0.f;
+            o.z[jj] = (GATE && v) ? ldf(Z, td) : 0.f;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
 // k_grad: grid (nsplit, nc, b), one wave (64 lanes) per workgroup.  The
 // workgroup owns carry chunk c (L = S*NCK steps) and a range of 16-channel
-// tiles.  Per tile:
+// tiles; lanes of a quad share a channel and hold 4 of its states.  Per tile:
 //   1. checkpoint sweep: from the carry-in state H_c, the state at the start of
-//      each S-step segment (registers, NCK x 4 per lane);
+//      each S-step segment;
 //   2. segments in reverse order: recompute the segment's states forward
-//      (keeping h_{t-1} and a_t), write dz and the dC partial; then run the
-//      adjoint backwards, mu_t = g_t C_t + a_{t+1} mu_{t+1}, starting from the
+//      (keeping h_{t-1} and a_t), write dz, sum g_t h_t over the channels (dC);
+//      then run the adjoint backwards, mu_t = g_t C_t + a_{t+1} mu_{t+1}, from the
 //      chunk's reverse carry M_c, and apply the vjp epilogue:
-//        s = mubar * a_t * h_{t-1};  ddelta = sum_n s wn;  dA_log += s Delta wn;
-//        dx = sum_n mubar B_t;  dB_t[n] += mubar x_t  (over channels).
+//        s = mubar a_t h_{t-1};  ddelta = sum_n s wn;  dA_log += s Delta wn;
+//        dx = sum_n mubar B_t;  dB_t[n] += mubar x_t (over channels).
 //      Truncated mode: mubar_t = mu_t - P(t, t+tbar) mu_{t+tbar}; mu at the
-//      shifted position t+tbar comes from a second reverse sweep run in lockstep
-//      from the carry of its own chunk, and P(t, t+tbar) = 2^{cn W_t} with the
-//      window sum W_t = sum_{j=t+1}^{t+tbar} Delta_j kept in fp64.
-// dB/dC are summed over channels per step in LDS, accumulated over the tiles,
-// and written once per chunk (partials per split when nsplit > 1).  The dA_log
-// partial of (chunk, channel, state) is written into that chunk's hbuf slot.
+//      shifted position comes from a second reverse sweep run in lockstep from
+//      the carry of its own chunk, and P(t, t+tbar) = 2^{cn W_t} with the window
+//      sum W_t = sum_{j=t+1}^{t+tbar} Delta_j kept in fp64.
+// Per-channel quantities (softplus, the gate, the load of x) are computed once
+// per step: lane r of a quad prepares steps r, r+4, ... of the segment and DPP
+// broadcasts them; the next segment's raw inputs are loaded ahead.  Sums over
+// channels of dB/dC go through LDS once per segment and accumulate across tiles
+// in the output (nsplit == 1) or in per-split partials.
 // ---------------------------------------------------------------------------
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK>
 __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
     constexpr int L = S * NCK;
-    __shared__ float acc[L][32];  // [t][0..15] dB, [t][16..31] dC
-    __shared__ float buf[16][17];
+    constexpr int SPL = S / 4;  // steps each lane prepares per segment
+    __shared__ float red[S][16][17];  // [step][state][channel]
     const int lane = threadIdx.x;
     const int r = lane & 3, chl = lane >> 2;
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const int split = blockIdx.x;
     const int64_t t0 = c * L;
-    const TI* X = static_cast<const TI*>(p.x);
-    const TI* DL = static_cast<const TI*>(p.delta);
     const TI* Bp = static_cast<const TI*>(p.B);
     const TI* Cp = static_cast<const TI*>(p.C);
-    const TI* DY = static_cast<const TI*>(p.dy);
-    const TI* Z = static_cast<const TI*>(p.z);
-
-    for (int i = lane; i < L * 32; i += 64) (&acc[0][0])[i] = 0.f;
-    __syncthreads();
+    const int64_t btn = p.nb * p.T * p.N;
+    float* dBo = p.nsplit == 1 ? p.dB : p.pB + static_cast<int64_t>(split) * btn;
+    float* dCo = p.nsplit == 1 ? p.dC : p.pC + static_cast<int64_t>(split) * btn;
 
     const int64_t ntile = (p.D + 15) / 16;
-    const int64_t per = (ntile + p.nsplit - 1) / p.nsplit;
-    const int64_t tile_lo = split * per;
-    const int64_t tile_hi = min(ntile, tile_lo + per);
+    const int64_t tile_lo = static_cast<int64_t>(split) * p.tps;
+    const int64_t tile_hi = min(ntile, tile_lo + p.tps);
+
+    // Sum red[j][n][0..15] for the S*16 (step, state) pairs of segment q and add
+    // the result into dst (or store it, for the first tile of the split).
+    auto flush = [&](float* dst, int q, bool first) {
+#pragma unroll
+        for (int i = 0; i < S * 16 / 64; ++i) {
+            const int o = lane + 64 * i;
+            const int j = o >> 4, n = o & 15;
+            float s = 0.f;
+#pragma unroll
+            for (int ch = 0; ch < 16; ++ch) s += red[j][n][ch];
+            const int64_t t = t0 + q * S + j;
+            if (t < p.T && n < p.N) {
+                const int64_t idx = (bb * p.T + t) * p.N + n;
+                dst[idx] = first ? s : dst[idx] + s;
+            }
+        }
+    };
 
     for (int64_t tile = tile_lo; tile < tile_hi; ++tile) {
+        const bool first = tile == tile_lo;
         const int64_t d = tile * 16 + chl;
         const bool dv = d < p.D;
         float cn[4], wn[4];
@@ -401,21 +450,26 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) h[k] = nv[k] ? p.hbuf[cb + k * p.D] : 0.f;
         float ck[NCK][4];
+        RawIn<SPL> nxt;
+        load_raw<TI, GATE, SPL>(p, bb, t0, d, dv, r, false, nxt);
         for (int q = 0; q < NCK; ++q) {
             ck_put<NCK>(ck, q, h);
-#pragma unroll 4
+            const RawIn<SPL> cur = nxt;
+            if (q + 1 < NCK) load_raw<TI, GATE, SPL>(p, bb, t0 + (q + 1) * S, d, dv, r, false, nxt);
+            float dls[SPL];
+#pragma unroll
+            for (int jj = 0; jj < SPL; ++jj) {
+                // padding steps (t >= T) and channels keep Delta = 0, i.e. a = 1
+                const bool v = dv && t0 + q * S + r + 4 * jj < p.T;
+                dls[jj] = (SP && v) ? softplus_f(cur.p[jj]) : cur.p[jj];
+            }
+#pragma unroll
             for (int j = 0; j < S; ++j) {
                 const int64_t t = t0 + q * S + j;
-                const bool tv = t < p.T;
-                float xv = 0.f, dl = 0.f;
-                if (tv && dv) {
-                    const int64_t td = (bb * p.T + t) * p.D + d;
-                    xv = ldf(X, td);
-                    const float pv = ldf(DL, td);
-                    dl = SP ? softplus_f(pv) : pv;
-                }
+                const float xv = quad_bcast(cur.x[j >> 2], j & 3);
+                const float dl = quad_bcast(dls[j >> 2], j & 3);
                 float Bv[4];
-                ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, tv, Bv);
+                ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, t < p.T, Bv);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
             }
@@ -431,6 +485,9 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
         float Msh[4] = {0.f, 0.f, 0.f, 0.f};
         double W = 0.0;
         if constexpr (TRUNC) {
+            const TI* DL = static_cast<const TI*>(p.delta);
+            const TI* DY = static_cast<const TI*>(p.dy);
+            const TI* Z = static_cast<const TI*>(p.z);
             const int64_t tb = p.tbar;
             const int64_t pstart = t0 + L - 1 + tb;
             const int64_t pb = bb * (p.nc + 1) * p.D + d;
@@ -471,31 +528,58 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
             }
         }
 
+        RawIn<SPL> nxs;  // raw inputs at the shifted positions (truncated mode)
+        load_raw<TI, GATE, SPL>(p, bb, t0 + (NCK - 1) * S, d, dv, r, true, nxt);
+        if constexpr (TRUNC)
+            load_raw<TI, GATE, SPL>(p, bb, t0 + (NCK - 1) * S + p.tbar, d, dv, r, true, nxs);
         for (int q = NCK - 1; q >= 0; --q) {
             ck_get<NCK>(ck, q, h);
+            const RawIn<SPL> cur = nxt;
+            RawIn<SPL> cus;
+            if constexpr (TRUNC) cus = nxs;
+            if (q > 0) {
+                load_raw<TI, GATE, SPL>(p, bb, t0 + (q - 1) * S, d, dv, r, true, nxt);
+                if constexpr (TRUNC)
+                    load_raw<TI, GATE, SPL>(p, bb, t0 + (q - 1) * S + p.tbar, d, dv, r, true, nxs);
+            }
+            // per-channel quantities of the steps this lane prepares
+            float dls[SPL], gs[SPL], gfs[SPL], sgs[SPL], dlps[SPL], gps[SPL];
+#pragma unroll
+            for (int jj = 0; jj < SPL; ++jj) {
+                // padding steps (t >= T) and channels keep Delta = 0, i.e. a = 1
+                const bool v = dv && t0 + q * S + r + 4 * jj < p.T;
+                dls[jj] = (SP && v) ? softplus_f(cur.p[jj]) : cur.p[jj];
+                sgs[jj] = SP ? 1.f - __expf(-dls[jj]) : 1.f;  // d softplus / d Delta_pre
+                if constexpr (GATE) {
+                    const float sg = sigmoid_f(cur.z[jj]);
+                    gs[jj] = cur.dy[jj] * cur.z[jj] * sg;
+                    gfs[jj] = cur.dy[jj] * sg * (1.f + cur.z[jj] * (1.f - sg));
+                } else {
+                    gs[jj] = cur.dy[jj];
+                    gfs[jj] = 0.f;
+                }
+                if constexpr (TRUNC) {
+                    const bool vs = dv && t0 + q * S + p.tbar + r + 4 * jj < p.T;
+                    dlps[jj] = (SP && vs) ? softplus_f(cus.p[jj]) : cus.p[jj];
+                    if constexpr (GATE)
+                        gps[jj] = cus.dy[jj] * cus.z[jj] * sigmoid_f(cus.z[jj]);
+                    else
+                        gps[jj] = cus.dy[jj];
+                }
+            }
+
             float hp[S][4], ah[S][4], gh[S], dlh[S], xh[S];
 #pragma unroll
             for (int j = 0; j < S; ++j) {
                 const int64_t t = t0 + q * S + j;
                 const bool tv = t < p.T;
-                const int64_t td = (bb * p.T + t) * p.D + d;
-                float xv = 0.f, dl = 0.f, g = 0.f, gy = 0.f, zv = 0.f;
-                if (tv && dv) {
-                    xv = ldf(X, td);
-                    const float pv = ldf(DL, td);
-                    dl = SP ? softplus_f(pv) : pv;
-                    gy = ldf(DY, td);
-                    if constexpr (GATE) {
-                        zv = ldf(Z, td);
-                        g = gy * zv * sigmoid_f(zv);
-                    } else {
-                        g = gy;
-                    }
-                }
+                const float xv = quad_bcast(cur.x[j >> 2], j & 3);
+                const float dl = quad_bcast(dls[j >> 2], j & 3);
+                const float g = quad_bcast(gs[j >> 2], j & 3);
                 float Bv[4], Cv[4];
                 ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, tv, Bv);
                 ld4<TI, N16>(Cp, bb * p.T + t, r, p.N, tv, Cv);
-                float yp = 0.f, gv[4];
+                float yp = 0.f;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     hp[j][k] = h[k];
@@ -503,25 +587,23 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
                     ah[j][k] = av;
                     h[k] = fmaf(av, h[k], Bv[k] * xv);
                     yp = fmaf(Cv[k], h[k], yp);
-                    gv[k] = g * h[k];
+                    red[j][r * 4 + k][chl] = g * h[k];
                 }
-                channel_sum_add(buf, gv, lane, acc[q * S + j], 16);
                 if constexpr (GATE) {
                     const float y = quad_sum(yp);
-                    if (r == 0 && tv && dv) {
-                        const float sg = sigmoid_f(zv);
-                        p.dz[td] = gy * y * sg * (1.f + zv * (1.f - sg));
-                    }
+                    if (r == (j & 3) && tv && dv) p.dz[(bb * p.T + t) * p.D + d] = gfs[j >> 2] * y;
                 }
                 gh[j] = g;
                 dlh[j] = dl;
                 xh[j] = xv;
             }
+            __syncthreads();
+            flush(dCo, q, first);
+            __syncthreads();
 #pragma unroll
             for (int j = S - 1; j >= 0; --j) {
                 const int64_t t = t0 + q * S + j;
                 const bool tv = t < p.T;
-                const int64_t td = (bb * p.T + t) * p.D + d;
                 float Bv[4], Cv[4];
                 ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, tv, Bv);
                 ld4<TI, N16>(Cp, bb * p.T + t, r, p.N, tv, Cv);
@@ -534,19 +616,8 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
                 if constexpr (TRUNC) {
                     const int64_t ps = t + p.tbar;
                     const bool pv = ps < p.T;
-                    float dlp = 0.f, gp = 0.f;
-                    if (pv && dv) {
-                        const int64_t tdp = (bb * p.T + ps) * p.D + d;
-                        const float pr = ldf(DL, tdp);
-                        dlp = SP ? softplus_f(pr) : pr;
-                        const float gy = ldf(DY, tdp);
-                        if constexpr (GATE) {
-                            const float zv = ldf(Z, tdp);
-                            gp = gy * zv * sigmoid_f(zv);
-                        } else {
-                            gp = gy;
-                        }
-                    }
+                    const float dlp = quad_bcast(dlps[j >> 2], j & 3);
+                    const float gp = quad_bcast(gps[j >> 2], j & 3);
                     float Cs[4];
                     ld4<TI, N16>(Cp, bb * p.T + ps, r, p.N, pv, Cs);
                     const float wf = static_cast<float>(W);
@@ -558,47 +629,36 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
                     }
                     W += static_cast<double>(dlh[j]) - static_cast<double>(dlp);
                 }
-                float dxp = 0.f, ddp = 0.f, bv[4];
+                float dxp = 0.f, ddp = 0.f;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     dxp = fmaf(mb[k], Bv[k], dxp);
                     const float s = mb[k] * ah[j][k] * hp[j][k];
                     ddp = fmaf(s, wn[k], ddp);
                     dA[k] = fmaf(s, dlh[j], dA[k]);
-                    bv[k] = mb[k] * xh[j];
+                    red[j][r * 4 + k][chl] = mb[k] * xh[j];
                     Mp[k] = ah[j][k] * mu[k];
                 }
-                channel_sum_add(buf, bv, lane, acc[q * S + j], 0);
                 const float dxv = quad_sum(dxp);
                 const float ddv = quad_sum(ddp);
-                if (r == 0 && tv && dv) {
+                if (r == (j & 3) && tv && dv) {
+                    const int64_t td = (bb * p.T + t) * p.D + d;
                     p.dx[td] = dxv;
-                    // softplus'(Delta_pre) = sigmoid(Delta_pre) = 1 - e^{-Delta}
-                    p.ddelta[td] = SP ? ddv * (1.f - __expf(-dlh[j])) : ddv;
+                    p.ddelta[td] = ddv * sgs[j >> 2];
                 }
             }
+            __syncthreads();
+            flush(dBo, q, first);
+            __syncthreads();
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k)
             if (nv[k]) p.hbuf[cb + k * p.D] = dA[k] * wn[k];
     }
-    __syncthreads();
-    float* dBo = p.nsplit == 1 ? p.dB : p.pB + static_cast<int64_t>(split) * p.nb * p.T * p.N;
-    float* dCo = p.nsplit == 1 ? p.dC : p.pC + static_cast<int64_t>(split) * p.nb * p.T * p.N;
-    for (int i = lane; i < L * 32; i += 64) {
-        const int tl = i >> 5, col = i & 31, n = col & 15;
-        const int64_t t = t0 + tl;
-        if (t >= p.T || n >= p.N) continue;
-        const int64_t o = (bb * p.T + t) * p.N + n;
-        if (col < 16)
-            dBo[o] = acc[tl][col];
-        else
-            dCo[o] = acc[tl][col];
-    }
 }
 
 // dB, dC = sum over splits of the partials (fixed order).
-__global__ __launch_bounds__(256) void k_reduce_bc(const ScanProblem p) {
+[[maybe_unused]] __global__ __launch_bounds__(256) void k_reduce_bc(const ScanProblem p) {
     const int64_t total = p.nb * p.T * p.N;
     const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     if (i >= total) return;
@@ -613,7 +673,7 @@ __global__ __launch_bounds__(256) void k_reduce_bc(const ScanProblem p) {
 
 // dA_log, stage 1: grid (ceil(D/256), N, nslice); slice s sums the (b, chunk)
 // partials q in its contiguous range, in order.
-__global__ __launch_bounds__(256) void k_reduce_da1(const ScanProblem p) {
+[[maybe_unused]] __global__ __launch_bounds__(256) void k_reduce_da1(const ScanProblem p) {
     const int64_t d = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     if (d >= p.D) return;
     const int64_t n = blockIdx.y, s = blockIdx.z;
@@ -626,7 +686,7 @@ __global__ __launch_bounds__(256) void k_reduce_da1(const ScanProblem p) {
 }
 
 // dA_log, stage 2: sum of the slices, transposed to [D][N].
-__global__ __launch_bounds__(256) void k_reduce_da2(const ScanProblem p) {
+[[maybe_unused]] __global__ __launch_bounds__(256) void k_reduce_da2(const ScanProblem p) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     if (i >= p.D * p.N) return;
     const int64_t d = i / p.N, n = i % p.N;
@@ -637,19 +697,19 @@ __global__ __launch_bounds__(256) void k_reduce_da2(const ScanProblem p) {
 
 inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b - 1) / b); }
 
-template <typename TI, bool SP, bool GATE, bool N16>
+template <typename TI, bool SP, bool GATE>
 hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
-    dim3 g1(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
+    dim3 g1(cdiv(p.D, 256), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
-        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, N16>), g1, dim3(256), 0, s, p);
+        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false>), g1, dim3(256), 0, s, p);
     }
     SSMK_TIMED("carry", s);
     hipLaunchKernelGGL(k_carry, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N),
                                      static_cast<unsigned>(2 * p.nb)),
                        dim3(256), 0, s, p);
     SSMK_TIMED("forward", s);
-    hipLaunchKernelGGL((k_forward<TI, SP, GATE, N16>), g1, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((k_forward<TI, SP, GATE>), g1, dim3(256), 0, s, p);
     return hipGetLastError();
 }
 
@@ -663,10 +723,10 @@ void grad_main(const ScanProblem& p, hipStream_t s) {
 
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16>
 hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
-    dim3 g1(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
+    dim3 g1(cdiv(p.D, 256), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
-        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16>), g1, dim3(256), 0, s, p);
+        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true>), g1, dim3(256), 0, s, p);
     }
     {
         SSMK_TIMED("carry", s);
