@@ -54,7 +54,7 @@ ssm_status check_desc(const ssm_desc* d, int64_t* L, int64_t* nc) {
         return fail(SSM_ERR_UNSUPPORTED, "seqlen/chunk (%lld) or batch (%lld) exceeds the launch grid",
                     (long long)n, (long long)d->batch);
     // All index arithmetic is 64-bit; element counts must fit comfortably.
-    if (d->batch * d->seqlen > (int64_t(1) << 40) || d->channels > (int64_t(1) << 24))
+    if (d->batch * d->seqlen > (int64_t(1) << 40) || d->channels > (int64_t(1) << 22))
         return fail(SSM_ERR_SHAPE, "problem too large");
     *L = l;
     *nc = n;

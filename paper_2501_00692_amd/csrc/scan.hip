@@ -7,8 +7,9 @@ namespace {
 
 template <typename TI>
 hipError_t forward_dispatch(const ScanProblem& p, hipStream_t s) {
+    const bool n16 = p.N == 16;
 #define SSMK_FWD(SP, GT) \
-    return forward_impl<TI, SP, GT>(p, s)
+    return n16 ? forward_impl<TI, SP, GT, true>(p, s) : forward_impl<TI, SP, GT, false>(p, s)
     if (p.softplus) {
         if (p.gate) SSMK_FWD(true, true);
         SSMK_FWD(true, false);

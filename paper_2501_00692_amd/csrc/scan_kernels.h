@@ -42,10 +42,19 @@ __device__ __forceinline__ void stf(uint16_t* p, int64_t i, float v) {
     p[i] = r;
 }
 
-__device__ __forceinline__ float softplus_f(float p) {
-    return fmaxf(p, 0.f) + log1pf(__expf(-fabsf(p)));
+// log(1 + e) for e in [0, 1] from the hardware logarithm; the factor
+// e / ((1 + e) - 1) cancels the rounding of 1 + e (Goldberg's log1p).
+__device__ __forceinline__ float log1p_small(float e) {
+    const float u = 1.f + e;
+    const float d = u - 1.f;
+    return d == 0.f ? e : __logf(u) * (e * __builtin_amdgcn_rcpf(d));
 }
-__device__ __forceinline__ float sigmoid_f(float z) { return 1.f / (1.f + __expf(-z)); }
+__device__ __forceinline__ float softplus_f(float p) {
+    return fmaxf(p, 0.f) + log1p_small(__expf(-fabsf(p)));
+}
+__device__ __forceinline__ float sigmoid_f(float z) {
+    return __builtin_amdgcn_rcpf(1.f + __expf(-z));
+}
 
 // DPP quad permutations: [1,0,3,2] and [2,3,0,1].
 __device__ __forceinline__ float dpp_swap1(float v) {
@@ -110,78 +119,122 @@ __device__ __forceinline__ void ld_row16(const TI* p, int64_t row, int64_t N, fl
     for (int n = 0; n < 16; ++n) v[n] = n < N ? ldf(p, row * N + n) : 0.f;
 }
 
+// Broadcast lane `src` (0..3, a compile-time constant after unrolling) of each
+// quad to the whole quad.
+__device__ __forceinline__ float quad_bcast(float v, int src) {
+    const int iv = __float_as_int(v);
+    switch (src & 3) {
+        case 0: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0x00, 0xF, 0xF, true));
+        case 1: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0x55, 0xF, 0xF, true));
+        case 2: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0xAA, 0xF, 0xF, true));
+        default: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0xFF, 0xF, 0xF, true));
+    }
+}
+
+// Raw per-(step, channel) inputs of the steps a lane prepares for its quad.
+template <int SPL>
+struct RawIn {
+    float x[SPL], p[SPL], dy[SPL], z[SPL];
+};
+
+// Load the raw inputs of the steps j = r + 4*jj of segment [ts, ts+S) (zero where
+// t >= T or the channel is padding).  `full` also loads dy and z.
+template <typename TI, bool GATE, int SPL>
+__device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64_t ts, int64_t d,
+                                         bool dv, int r, bool full, RawIn<SPL>& o) {
+    const TI* X = static_cast<const TI*>(p.x);
+    const TI* DL = static_cast<const TI*>(p.delta);
+    const TI* DY = static_cast<const TI*>(p.dy);
+    const TI* Z = static_cast<const TI*>(p.z);
+#pragma unroll
+    for (int jj = 0; jj < SPL; ++jj) {
+        const int64_t t = ts + r + 4 * jj;
+        const bool v = dv && t < p.T;
+        const int64_t td = (bb * p.T + t) * p.D + d;
+        o.x[jj] = v ? ldf(X, td) : 0.f;
+        o.p[jj] = v ? ldf(DL, td) : 0.f;
+        if (full) {
+            o.dy[jj] = v ? ldf(DY, td) : 0.f;
+            o.z[jj] = (GATE && v) ? ldf(Z, td) : 0.f;
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
-// k_chunk_aggr: grid (ceil(D/256), nc, b), 256 threads, one lane per channel
-// holding all 16 states.  For chunk c = [s, e]:
+// k_chunk_aggr: grid (ceil(D/64), nc, b), 256 threads; the 4 lanes of a quad
+// share a channel and hold 4 states each.  For chunk c = [s, e]:
 //   hloc = state at e from a zero carry-in,
 //   mloc = sum_{t in c} g_t C_t prod_{j=s}^{t} a_j  (the adjoint that the chunk
 //          hands to h_{s-1} from a zero carry at its end),
 //   sdel = sum_{t in c} Delta_t (fp64).
+// Lane r prepares the per-channel quantities of steps s+r, s+r+4, ... and
+// broadcasts them to its quad; its raw inputs are loaded one group ahead.
 // ---------------------------------------------------------------------------
-template <typename TI, bool SP, bool GATE, bool WANT_M>
+template <typename TI, bool SP, bool GATE, bool WANT_M, bool N16>
 __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int lane = threadIdx.x;
+    const int r = lane & 3;
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (lane >> 2);
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const bool dv = d < p.D;
-    const TI* X = static_cast<const TI*>(p.x);
-    const TI* DL = static_cast<const TI*>(p.delta);
     const TI* Bp = static_cast<const TI*>(p.B);
     const TI* Cp = static_cast<const TI*>(p.C);
-    const TI* DY = static_cast<const TI*>(p.dy);
-    const TI* Z = static_cast<const TI*>(p.z);
-    float cn[16], h[16], m[16], P[16];
-#pragma unroll
-    for (int n = 0; n < 16; ++n) {
-        cn[n] = (dv && n < p.N) ? -__expf(p.A_log[d * p.N + n]) * kLog2e : 0.f;
-        h[n] = 0.f;
-        m[n] = 0.f;
-        P[n] = 1.f;
-    }
+    float cn[4], wn[4];
+    lane_consts(p.A_log, d, r, p.N, dv, cn, wn);
+    float h[4] = {0.f, 0.f, 0.f, 0.f}, m[4] = {0.f, 0.f, 0.f, 0.f}, P[4] = {1.f, 1.f, 1.f, 1.f};
     double sd = 0.0;
     const int64_t t0 = c * p.L;
     const int64_t t1 = min(t0 + p.L, p.T);
-#pragma unroll 2
-    for (int64_t t = t0; t < t1; ++t) {
-        const int64_t td = (bb * p.T + t) * p.D + d;
-        float xv = 0.f, dl = 0.f, g = 0.f;
-        if (dv) {
-            xv = ldf(X, td);
-            const float pv = ldf(DL, td);
-            dl = SP ? softplus_f(pv) : pv;
-            if constexpr (WANT_M) {
-                const float gy = ldf(DY, td);
-                if constexpr (GATE) {
-                    const float zv = ldf(Z, td);
-                    g = gy * zv * sigmoid_f(zv);
-                } else {
-                    g = gy;
+    RawIn<1> nxt;
+    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, WANT_M, nxt);
+    for (int64_t s0 = t0; s0 < t1; s0 += 4) {
+        const RawIn<1> cur = nxt;
+        if (s0 + 4 < t1) load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, WANT_M, nxt);
+        const bool v = dv && s0 + r < t1;
+        const float dlr = (SP && v) ? softplus_f(cur.p[0]) : cur.p[0];
+        float gr = 0.f;
+        if constexpr (WANT_M) {
+            if constexpr (GATE)
+                gr = cur.dy[0] * cur.z[0] * sigmoid_f(cur.z[0]);
+            else
+                gr = cur.dy[0];
+        }
+        sd += static_cast<double>(dlr);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t t = s0 + j;
+            const bool tv = t < t1;
+            const float xv = quad_bcast(cur.x[0], j);
+            const float dl = quad_bcast(dlr, j);
+            float Bv[4], Cv[4];
+            ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, tv, Bv);
+            if constexpr (WANT_M) ld4<TI, N16>(Cp, bb * p.T + t, r, p.N, tv, Cv);
+            const float g = WANT_M ? quad_bcast(gr, j) : 0.f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float av = fexp2(cn[k] * dl);
+                h[k] = fmaf(av, h[k], Bv[k] * xv);
+                if constexpr (WANT_M) {
+                    P[k] *= av;
+                    m[k] = fmaf(g * Cv[k], P[k], m[k]);
                 }
             }
         }
-        float Bv[16], Cv[16];
-        ld_row16(Bp, bb * p.T + t, p.N, Bv);
-        if constexpr (WANT_M) ld_row16(Cp, bb * p.T + t, p.N, Cv);
-        sd += static_cast<double>(dl);
-#pragma unroll
-        for (int n = 0; n < 16; ++n) {
-            const float av = fexp2(cn[n] * dl);
-            h[n] = fmaf(av, h[n], Bv[n] * xv);
-            if constexpr (WANT_M) {
-                P[n] *= av;
-                m[n] = fmaf(g * Cv[n], P[n], m[n]);
-            }
-        }
     }
+    // sum of Delta over the quad's prepared steps, in a fixed order
+    const double s1 = __shfl_xor(sd, 1);
+    const double s2 = __shfl_xor(sd, 2);
+    const double s3 = __shfl_xor(sd, 3);
     if (!dv) return;
-    const int64_t cb = ((bb * p.nc + c) * p.N) * p.D + d;
+    const int64_t cb = ((bb * p.nc + c) * p.N + r * 4) * p.D + d;
 #pragma unroll
-    for (int n = 0; n < 16; ++n) {
-        if (n < p.N) {
-            p.hbuf[cb + n * p.D] = h[n];
-            if constexpr (WANT_M) p.mbuf[cb + n * p.D] = m[n];
+    for (int k = 0; k < 4; ++k) {
+        if (r * 4 + k < p.N) {
+            p.hbuf[cb + k * p.D] = h[k];
+            if constexpr (WANT_M) p.mbuf[cb + k * p.D] = m[k];
         }
     }
-    p.sdel[(bb * p.nc + c) * p.D + d] = sd;
+    if (r == 0) p.sdel[(bb * p.nc + c) * p.D + d] = ((sd + s1) + s2) + s3;
 }
 
 // ---------------------------------------------------------------------------
@@ -333,43 +386,101 @@ __device__ __forceinline__ void ck_get(const float (&ck)[NCK][4], int q, float (
     }
 }
 
-// Broadcast lane `src` (0..3, a compile-time constant after unrolling) of each
-// quad to the whole quad.
-__device__ __forceinline__ float quad_bcast(float v, int src) {
-    const int iv = __float_as_int(v);
-    switch (src & 3) {
-        case 0: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0x00, 0xF, 0xF, true));
-        case 1: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0x55, 0xF, 0xF, true));
-        case 2: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0xAA, 0xF, 0xF, true));
-        default: return __int_as_float(__builtin_amdgcn_mov_dpp(iv, 0xFF, 0xF, 0xF, true));
-    }
-}
+// ---------------------------------------------------------------------------
+// B_t and C_t of one chunk, staged in LDS once per workgroup: bf16 inputs keep
+// their bit patterns (two states per 32-bit word), fp32 inputs stay fp32.
+// Row t holds B (states 0..15) then C.
+// ---------------------------------------------------------------------------
+template <typename TI, int L>
+struct BCStage {
+    static constexpr int W = sizeof(TI) == 2 ? 16 : 32;  // 32-bit words per row
+    uint32_t w[L][W];
 
-// Raw per-(step, channel) inputs of the steps a lane prepares for its quad.
-template <int SPL>
-struct RawIn {
-    float x[SPL], p[SPL], dy[SPL], z[SPL];
+    __device__ __forceinline__ void load(const ScanProblem& p, int64_t bb, int64_t t0, int lane) {
+        const TI* Bp = static_cast<const TI*>(p.B);
+        const TI* Cp = static_cast<const TI*>(p.C);
+        for (int i = lane; i < L * W; i += 64) {
+            const int t = i / W, c = i % W;
+            const int64_t tg = t0 + t;
+            const bool tv = tg < p.T;
+            const int64_t row = (bb * p.T + tg) * p.N;
+            if constexpr (sizeof(TI) == 2) {
+                const TI* src = c < 8 ? Bp : Cp;
+                const int n0 = 2 * (c & 7);
+                const uint32_t lo = (tv && n0 < p.N) ? static_cast<uint32_t>(src[row + n0]) : 0u;
+                const uint32_t hi = (tv && n0 + 1 < p.N) ? static_cast<uint32_t>(src[row + n0 + 1]) : 0u;
+                w[t][c] = lo | (hi << 16);
+            } else {
+                const TI* src = c < 16 ? Bp : Cp;
+                const int n = c & 15;
+                const float v = (tv && n < p.N) ? ldf(src, row + n) : 0.f;
+                w[t][c] = __float_as_uint(v);
+            }
+        }
+    }
+    // States 4r..4r+3 of B and C at in-chunk step t.
+    __device__ __forceinline__ void get(int t, int r, float Bv[4], float Cv[4]) const {
+        if constexpr (sizeof(TI) == 2) {
+            const uint2 b = *reinterpret_cast<const uint2*>(&w[t][2 * r]);
+            const uint2 c = *reinterpret_cast<const uint2*>(&w[t][8 + 2 * r]);
+            Bv[0] = __uint_as_float(b.x << 16); Bv[1] = __uint_as_float(b.x & 0xffff0000u);
+            Bv[2] = __uint_as_float(b.y << 16); Bv[3] = __uint_as_float(b.y & 0xffff0000u);
+            Cv[0] = __uint_as_float(c.x << 16); Cv[1] = __uint_as_float(c.x & 0xffff0000u);
+            Cv[2] = __uint_as_float(c.y << 16); Cv[3] = __uint_as_float(c.y & 0xffff0000u);
+        } else {
+            const uint4 b = *reinterpret_cast<const uint4*>(&w[t][4 * r]);
+            const uint4 c = *reinterpret_cast<const uint4*>(&w[t][16 + 4 * r]);
+            Bv[0] = __uint_as_float(b.x); Bv[1] = __uint_as_float(b.y);
+            Bv[2] = __uint_as_float(b.z); Bv[3] = __uint_as_float(b.w);
+            Cv[0] = __uint_as_float(c.x); Cv[1] = __uint_as_float(c.y);
+            Cv[2] = __uint_as_float(c.z); Cv[3] = __uint_as_float(c.w);
+        }
+    }
+    __device__ __forceinline__ void getB(int t, int r, float Bv[4]) const {
+        if constexpr (sizeof(TI) == 2) {
+            const uint2 b = *reinterpret_cast<const uint2*>(&w[t][2 * r]);
+            Bv[0] = __uint_as_float(b.x << 16); Bv[1] = __uint_as_float(b.x & 0xffff0000u);
+            Bv[2] = __uint_as_float(b.y << 16); Bv[3] = __uint_as_float(b.y & 0xffff0000u);
+        } else {
+            const uint4 b = *reinterpret_cast<const uint4*>(&w[t][4 * r]);
+            Bv[0] = __uint_as_float(b.x); Bv[1] = __uint_as_float(b.y);
+            Bv[2] = __uint_as_float(b.z); Bv[3] = __uint_as_float(b.w);
+        }
+    }
 };
 
-// Load the raw inputs of the steps j = r + 4*jj of segment [ts, ts+S) (zero where
-// t >= T or the channel is padding).  `full` also loads dy and z.
+// Wave-uniform pointers to the chunk-start row of the [b][T][D] tensors; a lane
+// addresses its element with the 32-bit offset tl*D + d.
+template <typename TI>
+struct ChunkPtrs {
+    const TI* x;
+    const TI* p;
+    const TI* dy;
+    const TI* z;
+    __device__ __forceinline__ void set(const ScanProblem& q, int64_t row) {
+        const int64_t base = row * q.D;
+        x = static_cast<const TI*>(q.x) + base;
+        p = static_cast<const TI*>(q.delta) + base;
+        dy = static_cast<const TI*>(q.dy) + base;
+        z = static_cast<const TI*>(q.z) + base;
+    }
+};
+
+// Raw inputs of the steps tl = tq + r + 4*jj (in-chunk index) that lane r prepares,
+// zero where the step or the channel is padding (steps tl >= lim are padding).
 template <typename TI, bool GATE, int SPL>
-__device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64_t ts, int64_t d,
-                                         bool dv, int r, bool full, RawIn<SPL>& o) {
-    const TI* X = static_cast<const TI*>(p.x);
-    const TI* DL = static_cast<const TI*>(p.delta);
-    const TI* DY = static_cast<const TI*>(p.dy);
-    const TI* Z = static_cast<const TI*>(p.z);
+__device__ __forceinline__ void load_raw2(const ChunkPtrs<TI>& c, uint32_t D, uint32_t d, int tq,
+                                          int r, int64_t lim, bool dv, bool full, RawIn<SPL>& o) {
 #pragma unroll
     for (int jj = 0; jj < SPL; ++jj) {
-        const int64_t t = ts + r + 4 * jj;
-        const bool v = dv && t < p.T;
-        const int64_t td = (bb * p.T + t) * p.D + d;
-        o.x[jj] = v ? ldf(X, td) : 0.f;
-        o.p[jj] = v ? ldf(DL, td) : 0.f;
+        const int tl = tq + r + 4 * jj;
+        const bool v = dv && tl < lim;
+        const uint32_t off = static_cast<uint32_t>(tl) * D + d;
+        o.x[jj] = v ? ldf(c.x, off) : 0.f;
+        o.p[jj] = v ? ldf(c.p, off) : 0.f;
         if (full) {
-            o.dy[jj] = v ? ldf(DY, td) : 0.f;
-            o.z[jj] = (GATE && v) ? ldf(Z, td) : 0.f;
+            o.dy[jj] = v ? ldf(c.dy, off) : 0.f;
+            o.z[jj] = (GATE && v) ? ldf(c.z, off) : 0.f;
         }
     }
 }
@@ -377,44 +488,54 @@ __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64
 // ---------------------------------------------------------------------------
 // k_grad: grid (nsplit, nc, b), one wave (64 lanes) per workgroup.  The
 // workgroup owns carry chunk c (L = S*NCK steps) and a range of 16-channel
-// tiles; lanes of a quad share a channel and hold 4 of its states.  Per tile:
+// tiles; lanes of a quad share a channel and hold 4 of its states.  B and C of
+// the chunk are staged in LDS once.  Per tile:
 //   1. checkpoint sweep: from the carry-in state H_c, the state at the start of
 //      each S-step segment;
 //   2. segments in reverse order: recompute the segment's states forward
-//      (keeping h_{t-1} and a_t), write dz, sum g_t h_t over the channels (dC);
-//      then run the adjoint backwards, mu_t = g_t C_t + a_{t+1} mu_{t+1}, from the
-//      chunk's reverse carry M_c, and apply the vjp epilogue:
+//      (keeping a_t and a_t h_{t-1}), write dz, sum g_t h_t over the channels
+//      (dC); then run the adjoint backwards, mu_t = g_t C_t + a_{t+1} mu_{t+1},
+//      from the chunk's reverse carry M_c, and apply the vjp epilogue:
 //        s = mubar a_t h_{t-1};  ddelta = sum_n s wn;  dA_log += s Delta wn;
 //        dx = sum_n mubar B_t;  dB_t[n] += mubar x_t (over channels).
 //      Truncated mode: mubar_t = mu_t - P(t, t+tbar) mu_{t+tbar}; mu at the
 //      shifted position comes from a second reverse sweep run in lockstep from
 //      the carry of its own chunk, and P(t, t+tbar) = 2^{cn W_t} with the window
 //      sum W_t = sum_{j=t+1}^{t+tbar} Delta_j kept in fp64.
-// Per-channel quantities (softplus, the gate, the load of x) are computed once
-// per step: lane r of a quad prepares steps r, r+4, ... of the segment and DPP
-// broadcasts them; the next segment's raw inputs are loaded ahead.  Sums over
-// channels of dB/dC go through LDS once per segment and accumulate across tiles
-// in the output (nsplit == 1) or in per-split partials.
+// Per-channel quantities (softplus, the gate) are computed once per step: lane
+// r of a quad prepares steps r, r+4, ... of the segment and DPP-broadcasts
+// them; the next segment's raw inputs are loaded ahead.  Sums over channels of
+// dB/dC go through LDS once per segment and accumulate across tiles in the
+// output (nsplit == 1) or in per-split partials.
 // ---------------------------------------------------------------------------
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK>
-__global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_grad(const ScanProblem p) {
     constexpr int L = S * NCK;
     constexpr int SPL = S / 4;  // steps each lane prepares per segment
-    __shared__ float red[S][16][17];  // [step][state][channel]
+    __shared__ float red[S][16][20];  // [step][state][channel], 16-byte aligned rows
+    __shared__ BCStage<TI, L> bc;
     const int lane = threadIdx.x;
     const int r = lane & 3, chl = lane >> 2;
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const int split = blockIdx.x;
     const int64_t t0 = c * L;
-    const TI* Bp = static_cast<const TI*>(p.B);
-    const TI* Cp = static_cast<const TI*>(p.C);
+    const int64_t lim = p.T - t0;  // in-chunk steps tl < lim are real
+    const uint32_t D32 = static_cast<uint32_t>(p.D);
     const int64_t btn = p.nb * p.T * p.N;
+    ChunkPtrs<TI> cp;
+    cp.set(p, bb * p.T + t0);
+    float* dxo = p.dx + (bb * p.T + t0) * p.D;
+    float* ddo = p.ddelta + (bb * p.T + t0) * p.D;
+    float* dzo = GATE ? p.dz + (bb * p.T + t0) * p.D : nullptr;
     float* dBo = p.nsplit == 1 ? p.dB : p.pB + static_cast<int64_t>(split) * btn;
     float* dCo = p.nsplit == 1 ? p.dC : p.pC + static_cast<int64_t>(split) * btn;
 
     const int64_t ntile = (p.D + 15) / 16;
     const int64_t tile_lo = static_cast<int64_t>(split) * p.tps;
     const int64_t tile_hi = min(ntile, tile_lo + p.tps);
+
+    bc.load(p, bb, t0, lane);
+    __syncthreads();
 
     // Sum red[j][n][0..15] for the S*16 (step, state) pairs of segment q and add
     // the result into dst (or store it, for the first tile of the split).
@@ -423,9 +544,12 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
         for (int i = 0; i < S * 16 / 64; ++i) {
             const int o = lane + 64 * i;
             const int j = o >> 4, n = o & 15;
-            float s = 0.f;
-#pragma unroll
-            for (int ch = 0; ch < 16; ++ch) s += red[j][n][ch];
+            const float4 a0 = *reinterpret_cast<const float4*>(&red[j][n][0]);
+            const float4 a1 = *reinterpret_cast<const float4*>(&red[j][n][4]);
+            const float4 a2 = *reinterpret_cast<const float4*>(&red[j][n][8]);
+            const float4 a3 = *reinterpret_cast<const float4*>(&red[j][n][12]);
+            const float s = (((a0.x + a0.y) + (a0.z + a0.w)) + ((a1.x + a1.y) + (a1.z + a1.w))) +
+                            (((a2.x + a2.y) + (a2.z + a2.w)) + ((a3.x + a3.y) + (a3.z + a3.w)));
             const int64_t t = t0 + q * S + j;
             if (t < p.T && n < p.N) {
                 const int64_t idx = (bb * p.T + t) * p.N + n;
@@ -444,6 +568,7 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) nv[k] = dv && (r * 4 + k < p.N);
         const int64_t cb = ((bb * p.nc + c) * p.N + r * 4) * p.D + d;
+        const uint32_t d32 = dv ? static_cast<uint32_t>(d) : 0u;
 
         // 1. checkpoint sweep
         float h[4];
@@ -451,25 +576,24 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
         for (int k = 0; k < 4; ++k) h[k] = nv[k] ? p.hbuf[cb + k * p.D] : 0.f;
         float ck[NCK][4];
         RawIn<SPL> nxt;
-        load_raw<TI, GATE, SPL>(p, bb, t0, d, dv, r, false, nxt);
+        load_raw2<TI, GATE, SPL>(cp, D32, d32, 0, r, lim, dv, false, nxt);
         for (int q = 0; q < NCK; ++q) {
             ck_put<NCK>(ck, q, h);
             const RawIn<SPL> cur = nxt;
-            if (q + 1 < NCK) load_raw<TI, GATE, SPL>(p, bb, t0 + (q + 1) * S, d, dv, r, false, nxt);
+            if (q + 1 < NCK) load_raw2<TI, GATE, SPL>(cp, D32, d32, (q + 1) * S, r, lim, dv, false, nxt);
             float dls[SPL];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) {
-                // padding steps (t >= T) and channels keep Delta = 0, i.e. a = 1
-                const bool v = dv && t0 + q * S + r + 4 * jj < p.T;
+                // padding steps and channels keep Delta = 0, i.e. a = 1
+                const bool v = dv && q * S + r + 4 * jj < lim;
                 dls[jj] = (SP && v) ? softplus_f(cur.p[jj]) : cur.p[jj];
             }
 #pragma unroll
             for (int j = 0; j < S; ++j) {
-                const int64_t t = t0 + q * S + j;
                 const float xv = quad_bcast(cur.x[j >> 2], j & 3);
                 const float dl = quad_bcast(dls[j >> 2], j & 3);
                 float Bv[4];
-                ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, t < p.T, Bv);
+                bc.getB(q * S + j, r, Bv);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
             }
@@ -484,17 +608,19 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
         // truncated-mode state: shifted adjoint carry and the window sum
         float Msh[4] = {0.f, 0.f, 0.f, 0.f};
         double W = 0.0;
+        ChunkPtrs<TI> cps;
+        int64_t lims = 0;
         if constexpr (TRUNC) {
-            const TI* DL = static_cast<const TI*>(p.delta);
-            const TI* DY = static_cast<const TI*>(p.dy);
-            const TI* Z = static_cast<const TI*>(p.z);
+            const TI* Cp = static_cast<const TI*>(p.C);
             const int64_t tb = p.tbar;
+            cps.set(p, bb * p.T + min(t0 + tb, p.T - 1));
+            lims = p.T - (t0 + tb);
             const int64_t pstart = t0 + L - 1 + tb;
             const int64_t pb = bb * (p.nc + 1) * p.D + d;
             if (pstart < p.T) {
-                const int64_t cp = pstart / L;
-                const int64_t cpend = (cp + 1) * L - 1;
-                const int64_t mb = ((bb * p.nc + cp) * p.N + r * 4) * p.D + d;
+                const int64_t cpk = pstart / L;
+                const int64_t cpend = (cpk + 1) * L - 1;
+                const int64_t mb = ((bb * p.nc + cpk) * p.N + r * 4) * p.D + d;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) Msh[k] = nv[k] ? p.mbuf[mb + k * p.D] : 0.f;
                 double pre = 0.0;
@@ -502,6 +628,9 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
                     const bool pv = ps < p.T;
                     float dlp = 0.f, gp = 0.f;
                     if (pv && dv) {
+                        const TI* DL = static_cast<const TI*>(p.delta);
+                        const TI* DY = static_cast<const TI*>(p.dy);
+                        const TI* Z = static_cast<const TI*>(p.z);
                         const int64_t td = (bb * p.T + ps) * p.D + d;
                         const float pr = ldf(DL, td);
                         dlp = SP ? softplus_f(pr) : pr;
@@ -521,33 +650,30 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
                     pre += static_cast<double>(dlp);
                 }
                 if (dv)
-                    W = (p.psum[pb + cp * p.D] - p.psum[pb + (c + 1) * p.D]) +
-                        (p.sdel[(bb * p.nc + cp) * p.D + d] - pre);
+                    W = (p.psum[pb + cpk * p.D] - p.psum[pb + (c + 1) * p.D]) +
+                        (p.sdel[(bb * p.nc + cpk) * p.D + d] - pre);
             } else if (dv) {
                 W = p.psum[pb + p.nc * p.D] - p.psum[pb + (c + 1) * p.D];
             }
         }
 
         RawIn<SPL> nxs;  // raw inputs at the shifted positions (truncated mode)
-        load_raw<TI, GATE, SPL>(p, bb, t0 + (NCK - 1) * S, d, dv, r, true, nxt);
-        if constexpr (TRUNC)
-            load_raw<TI, GATE, SPL>(p, bb, t0 + (NCK - 1) * S + p.tbar, d, dv, r, true, nxs);
+        load_raw2<TI, GATE, SPL>(cp, D32, d32, (NCK - 1) * S, r, lim, dv, true, nxt);
+        if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (NCK - 1) * S, r, lims, dv, true, nxs);
         for (int q = NCK - 1; q >= 0; --q) {
             ck_get<NCK>(ck, q, h);
             const RawIn<SPL> cur = nxt;
             RawIn<SPL> cus;
             if constexpr (TRUNC) cus = nxs;
             if (q > 0) {
-                load_raw<TI, GATE, SPL>(p, bb, t0 + (q - 1) * S, d, dv, r, true, nxt);
-                if constexpr (TRUNC)
-                    load_raw<TI, GATE, SPL>(p, bb, t0 + (q - 1) * S + p.tbar, d, dv, r, true, nxs);
+                load_raw2<TI, GATE, SPL>(cp, D32, d32, (q - 1) * S, r, lim, dv, true, nxt);
+                if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (q - 1) * S, r, lims, dv, true, nxs);
             }
             // per-channel quantities of the steps this lane prepares
             float dls[SPL], gs[SPL], gfs[SPL], sgs[SPL], dlps[SPL], gps[SPL];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) {
-                // padding steps (t >= T) and channels keep Delta = 0, i.e. a = 1
-                const bool v = dv && t0 + q * S + r + 4 * jj < p.T;
+                const bool v = dv && q * S + r + 4 * jj < lim;
                 dls[jj] = (SP && v) ? softplus_f(cur.p[jj]) : cur.p[jj];
                 sgs[jj] = SP ? 1.f - __expf(-dls[jj]) : 1.f;  // d softplus / d Delta_pre
                 if constexpr (GATE) {
@@ -559,7 +685,7 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
                     gfs[jj] = 0.f;
                 }
                 if constexpr (TRUNC) {
-                    const bool vs = dv && t0 + q * S + p.tbar + r + 4 * jj < p.T;
+                    const bool vs = dv && q * S + r + 4 * jj < lims;
                     dlps[jj] = (SP && vs) ? softplus_f(cus.p[jj]) : cus.p[jj];
                     if constexpr (GATE)
                         gps[jj] = cus.dy[jj] * cus.z[jj] * sigmoid_f(cus.z[jj]);
@@ -568,30 +694,28 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
                 }
             }
 
-            float hp[S][4], ah[S][4], gh[S], dlh[S], xh[S];
+            float ahp[S][4], ah[S][4], gh[S], dlh[S], xh[S];
 #pragma unroll
             for (int j = 0; j < S; ++j) {
-                const int64_t t = t0 + q * S + j;
-                const bool tv = t < p.T;
+                const int tl = q * S + j;
                 const float xv = quad_bcast(cur.x[j >> 2], j & 3);
                 const float dl = quad_bcast(dls[j >> 2], j & 3);
                 const float g = quad_bcast(gs[j >> 2], j & 3);
                 float Bv[4], Cv[4];
-                ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, tv, Bv);
-                ld4<TI, N16>(Cp, bb * p.T + t, r, p.N, tv, Cv);
+                bc.get(tl, r, Bv, Cv);
                 float yp = 0.f;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    hp[j][k] = h[k];
                     const float av = fexp2(cn[k] * dl);
                     ah[j][k] = av;
-                    h[k] = fmaf(av, h[k], Bv[k] * xv);
+                    ahp[j][k] = av * h[k];
+                    h[k] = fmaf(Bv[k], xv, ahp[j][k]);
                     yp = fmaf(Cv[k], h[k], yp);
                     red[j][r * 4 + k][chl] = g * h[k];
                 }
                 if constexpr (GATE) {
                     const float y = quad_sum(yp);
-                    if (r == (j & 3) && tv && dv) p.dz[(bb * p.T + t) * p.D + d] = gfs[j >> 2] * y;
+                    if (r == (j & 3) && tl < lim && dv) dzo[static_cast<uint32_t>(tl) * D32 + d32] = gfs[j >> 2] * y;
                 }
                 gh[j] = g;
                 dlh[j] = dl;
@@ -602,11 +726,9 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
             __syncthreads();
 #pragma unroll
             for (int j = S - 1; j >= 0; --j) {
-                const int64_t t = t0 + q * S + j;
-                const bool tv = t < p.T;
+                const int tl = q * S + j;
                 float Bv[4], Cv[4];
-                ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, tv, Bv);
-                ld4<TI, N16>(Cp, bb * p.T + t, r, p.N, tv, Cv);
+                bc.get(tl, r, Bv, Cv);
                 float mu[4], mb[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
@@ -614,12 +736,12 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
                     mb[k] = mu[k];
                 }
                 if constexpr (TRUNC) {
-                    const int64_t ps = t + p.tbar;
+                    const int64_t ps = t0 + tl + p.tbar;
                     const bool pv = ps < p.T;
                     const float dlp = quad_bcast(dlps[j >> 2], j & 3);
                     const float gp = quad_bcast(gps[j >> 2], j & 3);
                     float Cs[4];
-                    ld4<TI, N16>(Cp, bb * p.T + ps, r, p.N, pv, Cs);
+                    ld4<TI, N16>(static_cast<const TI*>(p.C), bb * p.T + ps, r, p.N, pv, Cs);
                     const float wf = static_cast<float>(W);
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
@@ -633,7 +755,7 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     dxp = fmaf(mb[k], Bv[k], dxp);
-                    const float s = mb[k] * ah[j][k] * hp[j][k];
+                    const float s = mb[k] * ahp[j][k];
                     ddp = fmaf(s, wn[k], ddp);
                     dA[k] = fmaf(s, dlh[j], dA[k]);
                     red[j][r * 4 + k][chl] = mb[k] * xh[j];
@@ -641,10 +763,10 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
                 }
                 const float dxv = quad_sum(dxp);
                 const float ddv = quad_sum(ddp);
-                if (r == (j & 3) && tv && dv) {
-                    const int64_t td = (bb * p.T + t) * p.D + d;
-                    p.dx[td] = dxv;
-                    p.ddelta[td] = ddv * sgs[j >> 2];
+                if (r == (j & 3) && tl < lim && dv) {
+                    const uint32_t off = static_cast<uint32_t>(tl) * D32 + d32;
+                    dxo[off] = dxv;
+                    ddo[off] = ddv * sgs[j >> 2];
                 }
             }
             __syncthreads();
@@ -697,12 +819,13 @@ __global__ __launch_bounds__(64) void k_grad(const ScanProblem p) {
 
 inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b - 1) / b); }
 
-template <typename TI, bool SP, bool GATE>
+template <typename TI, bool SP, bool GATE, bool N16>
 hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
     dim3 g1(cdiv(p.D, 256), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
+    dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
-        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false>), g1, dim3(256), 0, s, p);
+        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, N16>), g4, dim3(256), 0, s, p);
     }
     SSMK_TIMED("carry", s);
     hipLaunchKernelGGL(k_carry, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N),
@@ -723,10 +846,10 @@ void grad_main(const ScanProblem& p, hipStream_t s) {
 
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16>
 hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
-    dim3 g1(cdiv(p.D, 256), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
+    dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
-        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true>), g1, dim3(256), 0, s, p);
+        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16>), g4, dim3(256), 0, s, p);
     }
     {
         SSMK_TIMED("carry", s);
