@@ -23,6 +23,17 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA
+FP32_VECTOR_PEAK_TFS = 157.3  # MI355X fp32 vector (256 CUs x 2.4 GHz, packed FMA)
+
+
+def scan_flops_per_state_step(trunc):
+    """Algorithmic fp32 operations per (state, token) of the fused gradient (an FMA
+    counts 2, exp counts 1): forward recompute a = exp(Delta c) (2), h = a h + B x (3),
+    y += C h (2), dC contribution and channel sum (2); reverse mu = g C + a mu (3),
+    dx += mu B (2), s = mu (a h) (2), ddelta += s w (2), dA += s Delta (2), dB
+    contribution and sum (2) -> 22.  The truncated window adds the shifted adjoint
+    (g C + a mu, its decay: 6), the window product (2) and mubar = mu - P mu' (2)."""
+    return 22 + (10 if trunc else 0)
 
 
 def scan_bytes_per_token(D, N, s, gate):
@@ -105,6 +116,31 @@ def scan_step(w, inp, ssm, torch, tbar=0):
     return step
 
 
+def measured_traffic(kern, workload):
+    """HBM-side bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source (else None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"traffic_{kern}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if line.strip() and not line.startswith("#"):
+            k, v = line.split(None, 1)
+            rec[k] = v.strip()
+    src = os.path.join(ROOT, "paper_2501_00692_amd", "csrc", rec.get("source", ""))
+    if not os.path.exists(src):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("source_sha256"):
+        return None
+    return int(rec["bytes_per_launch"])
+
+
+def tbar_of(kind):
+    """`kind` is "layer"/"scan" (full) or a (kind, tbar) tuple."""
+    return kind[1] if isinstance(kind, tuple) else 0
+
+
 def roofline_for(kern, ktimes, w, kind):
     """Roofline entry for kernel `kern` (algorithmic work per launch / average
     launch duration)."""
@@ -112,10 +148,13 @@ def roofline_for(kern, ktimes, w, kind):
     s = 2 if w.bf16 else 4
     if kern == "grad_fused":
         per_launch = scan_bytes_per_token(w.D, w.N, s, w.proj) * w.M  # bytes
-        ach = per_launch / (kt["avg_ms"] * 1e-3) / 1e9
-        return {"kernel": kern, "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": ach / HBM_PEAK_GBS, "traffic": None, "avg_ms": kt["avg_ms"],
-                "algorithmic_bytes_per_launch": per_launch}
+        gbs = per_launch / (kt["avg_ms"] * 1e-3) / 1e9
+        flops = scan_flops_per_state_step(0 < tbar_of(kind) < w.T) * w.M * w.D * w.N
+        tfs = flops / (kt["avg_ms"] * 1e-3) / 1e12
+        return {"kernel": kern, "bound": "alu", "achieved": tfs, "peak": FP32_VECTOR_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": tfs / FP32_VECTOR_PEAK_TFS, "traffic": None, "avg_ms": kt["avg_ms"],
+                "algorithmic_flops_per_launch": flops, "algorithmic_bytes_per_launch": per_launch,
+                "hbm_GBps_algorithmic": gbs, "hbm_frac_algorithmic": gbs / HBM_PEAK_GBS}
     if kern in ("gemm_dw", "gemm_dx"):
         M, D, N, dm = w.M, w.D, w.N, w.d_model
         if kern == "gemm_dw":
@@ -164,6 +203,9 @@ def main():
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-tokens", type=int, default=4096)
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="first run a plain 256 MiB device copy (torch copy_) three times, as the known-size "
+                         "reference for HBM traffic counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one GPU only "
@@ -176,6 +218,13 @@ def main():
     from paper_2501_00692_amd.synth import WORKLOADS, make_inputs
 
     torch.cuda.set_device(0)
+    if args.copy_calib:
+        src = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     w = WORKLOADS["layer"]
     inp = make_inputs(w, device="cuda")
     step = layer_step(w, inp, ssm, torch, tbar=0)
@@ -183,6 +232,8 @@ def main():
     ktimes = _kernel_times(step, args.steps, ssm, torch)
     dom = max(ktimes, key=lambda k: ktimes[k]["total_ms"])
     roof = roofline_for(dom, ktimes, w, "layer")
+    if roof is not None:
+        roof["traffic"] = measured_traffic(dom, "layer-b2-T4096-D1536")
     value = w.M / (ms * 1e-3)
 
     extra = {"kernels_layer": ktimes,
@@ -206,10 +257,12 @@ def main():
             kt = _kernel_times(st, 2, ssm, torch)
             entry = {"ms_per_step": m, "tokens_per_s": wl.M / (m * 1e-3), "tbar": tbar,
                      "grad_fused_avg_ms": kt.get("grad_fused", {}).get("avg_ms")}
-            r = roofline_for("grad_fused", kt, wl, kind)
+            r = roofline_for("grad_fused", kt, wl, (kind, tbar))
             if r:
-                entry["grad_fused_GBps"] = r["achieved"]
-                entry["grad_fused_hbm_frac"] = r["frac"]
+                entry["grad_fused_TFLOPs"] = r["achieved"]
+                entry["grad_fused_alu_frac"] = r["frac"]
+                entry["grad_fused_GBps"] = r["hbm_GBps_algorithmic"]
+                entry["grad_fused_hbm_frac"] = r["hbm_frac_algorithmic"]
             for g in ("gemm_dw", "gemm_dx"):
                 if g in kt:
                     rg = roofline_for(g, kt, wl, kind)
