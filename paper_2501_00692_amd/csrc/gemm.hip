@@ -1,14 +1,18 @@
 // gemm.hip -- bf16 MFMA GEMMs for the projection gradients (gfx950,
-// v_mfma_f32_32x32x16_bf16, fp32 accumulation):
-//   k_gemm_dw : dW[K][N] = X^T dZ,  X [M][K], dZ [M][N]; the reduction runs over
-//               the row index M of both operands, so 8x8 blocks are transposed
-//               in registers on their way into LDS (LDS holds [k][m] and [n][m]);
-//               split over M with a deterministic second-stage reduction.
-//   k_gemm_dx : dX[M][K] = dZ W^T,  dZ [M][N], W [K][N]; both operands are
-//               contiguous along the reduction, staged through LDS as is;
-//               epilogue adds an optional fp32 addend, accumulates, and can
-//               write a bf16 copy into a strided buffer.
-//   k_pack    : fp32 -> bf16 (round to nearest even) strided copy.
+// v_mfma_f32_32x32x16_bf16, fp32 accumulation), one templated kernel:
+//   dW[K][N] = X^T dZ  (X [M][K], dZ [M][N]): the reduction runs over the row
+//       index of both operands, so 8x8 blocks are transposed in registers on
+//       their way into LDS; split over M when the output has few tiles, with a
+//       fixed-order second-stage reduction;
+//   dX[M][K] = dZ W^T  (dZ [M][N], W [K][N]): both operands are contiguous along
+//       the reduction and are staged as they are; the epilogue adds an optional
+//       fp32 addend, accumulates, and can write a bf16 copy into a strided buffer.
+// Workgroup: 512 threads = 4x2 waves (two per SIMD); tile BM x BN with BM = 256
+// and BN in {128, 192, 256}; each wave owns a (BM/4) x (BN/2) block of 32x32 MFMA
+// tiles.  Interior tiles run a loop without bounds checks.
+// LDS is double-buffered over 64-deep reduction steps (one barrier per step);
+// the next step's global loads are in flight while the MFMAs run.
+//   k_pack : fp32 -> bf16 (round to nearest even) strided copy.
 #include "internal.h"
 
 namespace ssmk {
@@ -17,10 +21,13 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128;   // output rows per workgroup
-constexpr int BN = 128;   // output cols per workgroup
-constexpr int BK = 64;    // reduction depth per iteration
-constexpr int LDK = BK + 8;  // LDS row length (bf16), padded
+constexpr int BK = 64;   // reduction depth per step
+constexpr int LDK = BK;  // LDS row length (bf16): 8 blocks of 16 bytes, XOR-swizzled
+
+// Physical 16-byte block of logical block `blk` in LDS row `row`: the XOR keeps
+// fragment reads (8 consecutive rows), row-wise staging writes (8 blocks of one
+// row) and transposed staging writes (rows 8 apart) free of bank conflicts.
+__device__ __forceinline__ int swz(int row, int blk) { return (blk ^ (row ^ (row >> 3))) & 7; }
 
 __device__ __forceinline__ uint16_t f2bf(float v) {
     uint32_t u = __float_as_uint(v);
@@ -56,104 +63,196 @@ __device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[
     }
 }
 
-// ---------------------------------------------------------------------------
-// dW partial: grid (ceil(N/BN), ceil(K/BM), splits), 256 threads.
-// Workgroup tile: rows k0..k0+127 of dW, cols n0..n0+127, reduction rows
-// m in [m_lo, m_hi).  Threads 0..127 stage the X block, 128..255 the dZ block:
-// each thread loads an 8(m) x 8 block and writes it transposed.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_gemm_dw(int64_t M, int64_t K, int64_t N,
-                                                 const uint16_t* __restrict__ X, int64_t ldx,
-                                                 const uint16_t* __restrict__ dZ, int64_t lddz,
-                                                 float* __restrict__ out, int64_t m_per_split,
-                                                 int direct, int accum) {
-    __shared__ __attribute__((aligned(16))) uint16_t At[BM][LDK];  // [k][m]
-    __shared__ __attribute__((aligned(16))) uint16_t Bt[BN][LDK];  // [n][m]
+struct GemmArgs {
+    int64_t R, Cc, Kr;    // output rows, output cols, reduction length
+    const uint16_t* A;    // TR: [Kr][R] (reduction-major); else [R][Kr]
+    int64_t lda;
+    const uint16_t* B;    // TR: [Kr][Cc];                  else [Cc][Kr]
+    int64_t ldb;
+    float* C;             // output [R][Cc] (ldc = Cc), or split partials
+    int64_t kper;         // reduction range per split (multiple of BK)
+    int direct;           // write C (else the partial of split blockIdx.z)
+    int accum;            // C += result
+    const float* add;     // optional fp32 addend [R][Cc]
+    uint16_t* out16;      // optional bf16 copy of the result
+    int64_t ld16;
+};
+
+constexpr int NT = 512;  // threads per workgroup (8 waves: 4 rows x 2 cols)
+
+// Staging of both operand tiles (BM and BN rows x BK reduction) into LDS rows of
+// LDK bf16.  TR (reduction-major sources): 8x8 blocks, threads [0, BM) take the A
+// blocks and [BM, BM+BN) the B blocks, one each, transposed in registers.
+// Otherwise: 16-byte pieces spread over all threads.  FULL: the tiles and the
+// reduction step are entirely in bounds (no checks).
+template <bool TR, int BM, int BN>
+struct Stager {
+    static constexpr int PA = TR ? BM : BM * 8;
+    static constexpr int PB = TR ? BN : BN * 8;
+    static constexpr int PER = TR ? 1 : (PA + PB) / NT;
+    static constexpr int REGS = TR ? 8 : 1;
+    static_assert(!TR || BM + BN <= NT, "one block per thread");
+    static_assert(TR || (PA % NT == 0 && PB % NT == 0), "pieces divide evenly");
+    uint4 v[PER][REGS];
+
+    template <bool FULL>
+    __device__ __forceinline__ void load(const GemmArgs& g, int64_t r0, int64_t c0, int64_t k,
+                                         int64_t k_hi, int tid) {
+        if constexpr (TR) {
+            const bool isA = tid < BM;
+            const int pc = isA ? tid : tid - BM;
+            if (!isA && pc >= BN) return;
+            const int rows8 = (isA ? BM : BN) / 8;
+            const int rb = pc / rows8, cb = pc % rows8;  // reduction block, row block
+            const uint16_t* src = isA ? g.A : g.B;
+            const int64_t ld = isA ? g.lda : g.ldb;
+            const int64_t col = (isA ? r0 : c0) + cb * 8;
+            const int64_t ncol = isA ? g.R : g.Cc;
+            const uint16_t* p0 = src + (k + rb * 8) * ld + col;
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                if (FULL || (col < ncol && k + rb * 8 + r < k_hi))
+                    v[0][r] = *reinterpret_cast<const uint4*>(p0 + r * ld);
+                else
+                    v[0][r] = make_uint4(0u, 0u, 0u, 0u);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < PER; ++e) {
+                constexpr int EA = PA / NT;  // pieces of A per thread; the rest are B
+                const bool isA = e < EA;
+                const int q = tid + NT * (isA ? e : e - EA);
+                const int row = q >> 3, seg = q & 7;
+                const int64_t gr = (isA ? r0 : c0) + row, kk = k + seg * 8;
+                const uint16_t* src = isA ? g.A : g.B;
+                const int64_t ld = isA ? g.lda : g.ldb;
+                if (FULL || (gr < (isA ? g.R : g.Cc) && kk < k_hi))
+                    v[e][0] = *reinterpret_cast<const uint4*>(src + gr * ld + kk);
+                else
+                    v[e][0] = make_uint4(0u, 0u, 0u, 0u);
+            }
+        }
+    }
+    __device__ __forceinline__ void store(uint16_t (*As)[LDK], uint16_t (*Bs)[LDK], int tid) const {
+        if constexpr (TR) {
+            const bool isA = tid < BM;
+            const int pc = isA ? tid : tid - BM;
+            if (!isA && pc >= BN) return;
+            const int rows8 = (isA ? BM : BN) / 8;
+            const int rb = pc / rows8, cb = pc % rows8;
+            uint16_t(*dst)[LDK] = isA ? As : Bs;
+            uint4 tr[8];
+            transpose8x8(v[0], tr);
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const int row = cb * 8 + c;
+                *reinterpret_cast<uint4*>(&dst[row][swz(row, rb) * 8]) = tr[c];
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < PER; ++e) {
+                constexpr int EA = PA / NT;
+                const bool isA = e < EA;
+                const int q = tid + NT * (isA ? e : e - EA);
+                const int row = q >> 3, seg = q & 7;
+                uint16_t(*dst)[LDK] = isA ? As : Bs;
+                *reinterpret_cast<uint4*>(&dst[row][swz(row, seg) * 8]) = v[e][0];
+            }
+        }
+    }
+};
+
+// Main loop over the workgroup's reduction range; FULL drops every bounds check.
+template <bool TR, int BM, int BN, bool FULL, int MI, int NJ>
+__device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, uint16_t (*As)[BM][LDK],
+                                              uint16_t (*Bs)[BN][LDK], int64_t r0, int64_t c0,
+                                              int64_t k_lo, int64_t k_hi, int tid, int wr, int wc,
+                                              f32x16 (&acc)[MI][NJ]) {
+    const int lane = tid & 63;
+    const int li = lane & 31;
+    const int lk = (lane >> 5) * 8;
+    Stager<TR, BM, BN> st;
+    if (k_lo < k_hi) {
+        st.template load<FULL>(g, r0, c0, k_lo, k_hi, tid);
+        st.store(As[0], Bs[0], tid);
+    }
+    __syncthreads();
+    int cur = 0;
+    for (int64_t k = k_lo; k < k_hi; k += BK) {
+        const bool more = k + BK < k_hi;
+        if (more) st.template load<FULL>(g, r0, c0, k + BK, k_hi, tid);
+#pragma unroll
+        for (int ks = 0; ks < BK; ks += 16) {
+            bf16x8 a[MI], b[NJ];
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                const int row = wr + i * 32 + li;
+                a[i] = lds_frag(&As[cur][row][swz(row, (ks + lk) >> 3) * 8]);
+            }
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const int row = wc + j * 32 + li;
+                b[j] = lds_frag(&Bs[cur][row][swz(row, (ks + lk) >> 3) * 8]);
+            }
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        if (more) st.store(As[cur ^ 1], Bs[cur ^ 1], tid);
+        __syncthreads();
+        cur ^= 1;
+    }
+}
+
+template <bool TR, int BM, int BN>
+__global__ __launch_bounds__(NT) void k_gemm(const GemmArgs g) {
+    constexpr int MI = BM / 128, NJ = BN / 64;  // 32x32 MFMA tiles per wave (4x2 waves)
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDK];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][LDK];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int64_t n0 = static_cast<int64_t>(blockIdx.x) * BN;
-    const int64_t k0 = static_cast<int64_t>(blockIdx.y) * BM;
-    const int64_t m_lo = static_cast<int64_t>(blockIdx.z) * m_per_split;
-    const int64_t m_hi = min(M, m_lo + m_per_split);
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * BN;
+    const int64_t r0 = static_cast<int64_t>(blockIdx.y) * BM;
+    const int64_t k_lo = static_cast<int64_t>(blockIdx.z) * g.kper;
+    const int64_t k_hi = min(g.Kr, k_lo + g.kper);
+    const int wr = (wave >> 1) * (BM / 4);
+    const int wc = (wave & 1) * (BN / 2);
 
-    // staging role
-    const bool isA = tid < 128;
-    const int st = tid & 127;
-    const int bcol = st & 15;   // 8-wide column block within the 128 columns
-    const int brow = st >> 4;   // 8-row block within BK = 64
-    const uint16_t* src = isA ? X : dZ;
-    const int64_t ld = isA ? ldx : lddz;
-    const int64_t colg = (isA ? k0 : n0) + bcol * 8;
-    const int64_t ncol = isA ? K : N;
-    const bool colv = colg < ncol;  // K, N are multiples of 8
-
-    uint4 regs[8];
-    auto load_tile = [&](int64_t m0) {
+    f32x16 acc[MI][NJ];
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-            const int64_t m = m0 + brow * 8 + r;
-            if (colv && m < m_hi)
-                regs[r] = *reinterpret_cast<const uint4*>(src + m * ld + colg);
-            else
-                regs[r] = make_uint4(0u, 0u, 0u, 0u);
-        }
-    };
-
-    f32x16 acc[2][2];
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    const int wr = (wave >> 1) * 64;  // wave's row offset within the tile
-    const int wc = (wave & 1) * 64;   // wave's col offset
-    const int li = lane & 31;
-    const int lk = (lane >> 5) * 8;
+    const bool full = r0 + BM <= g.R && c0 + BN <= g.Cc && (k_hi - k_lo) % BK == 0;
+    if (full)
+        gemm_mainloop<TR, BM, BN, true, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
+    else
+        gemm_mainloop<TR, BM, BN, false, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
 
-    load_tile(m_lo);
-    for (int64_t m0 = m_lo; m0 < m_hi; m0 += BK) {
-        uint4 tr[8];
-        transpose8x8(regs, tr);
-        __syncthreads();  // previous iteration's fragment reads are done
-        uint16_t(*dst)[LDK] = isA ? At : Bt;
+    // acc element v of lane l is row 8*(v/4) + 4*(l/32) + v%4, col l%32 of its tile
+    float* dst = g.C + (g.direct ? 0 : static_cast<int64_t>(blockIdx.z) * g.R * g.Cc);
 #pragma unroll
-        for (int c = 0; c < 8; ++c)
-            *reinterpret_cast<uint4*>(&dst[bcol * 8 + c][brow * 8]) = tr[c];
-        __syncthreads();
-        if (m0 + BK < m_hi) load_tile(m0 + BK);
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int ks = 0; ks < BK; ks += 16) {
-            bf16x8 a[2], b[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) a[i] = lds_frag(&At[wr + i * 32 + li][ks + lk]);
-#pragma unroll
-            for (int j = 0; j < 2; ++j) b[j] = lds_frag(&Bt[wc + j * 32 + li][ks + lk]);
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
-    }
-
-    // write: acc element v of lane l is row 8*(v/4) + 4*(l/32) + v%4, col l%32
-    float* dst = out + (direct ? 0 : static_cast<int64_t>(blockIdx.z) * K * N);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int64_t row = k0 + wr + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                const int64_t col = n0 + wc + j * 32 + (lane & 31);
-                if (row < K && col < N) {
-                    const int64_t o = row * N + col;
-                    if (direct && accum)
-                        dst[o] += acc[i][j][v];
-                    else
-                        dst[o] = acc[i][j][v];
+                const int64_t row = r0 + wr + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                const int64_t col = c0 + wc + j * 32 + (lane & 31);
+                if (row < g.R && col < g.Cc) {
+                    const int64_t o = row * g.Cc + col;
+                    float val = acc[i][j][v];
+                    if (g.direct) {
+                        if (g.add) val += g.add[o];
+                        if (g.accum) val += dst[o];
+                        if (g.out16) g.out16[row * g.ld16 + col] = f2bf(val);
+                    }
+                    dst[o] = val;
                 }
             }
 }
@@ -168,98 +267,6 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(int64_t KN, int splits, c
     dW[i] = accum ? dW[i] + s : s;
 }
 
-// ---------------------------------------------------------------------------
-// dX: grid (ceil(K/BN), ceil(M/BM)), 256 threads.  Tile rows m0.., cols k0..
-// A = dZ rows (m, reduction n contiguous), B = W rows (k, reduction n contiguous).
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_gemm_dx(int64_t M, int64_t K, int64_t N,
-                                                 const uint16_t* __restrict__ dZ, int64_t lddz,
-                                                 const uint16_t* __restrict__ W, int64_t ldw,
-                                                 float* __restrict__ dX, int accum,
-                                                 const float* __restrict__ add,
-                                                 uint16_t* __restrict__ out16, int64_t ld16) {
-    __shared__ __attribute__((aligned(16))) uint16_t As[BM][LDK];  // [m][n]
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[BN][LDK];  // [k][n]
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int64_t k0 = static_cast<int64_t>(blockIdx.x) * BN;
-    const int64_t m0 = static_cast<int64_t>(blockIdx.y) * BM;
-
-    // staging: each operand tile is 128 rows x 64 values = 1024 16-byte pieces;
-    // thread tid loads pieces tid + 256*e, e = 0..3, for each operand.
-    uint4 ra[4], rb[4];
-    auto load_tile = [&](int64_t n0) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int piece = tid + 256 * e;
-            const int row = piece >> 3, cb = (piece & 7) * 8;
-            const int64_t n = n0 + cb;
-            const int64_t m = m0 + row, k = k0 + row;
-            ra[e] = (m < M && n < N) ? *reinterpret_cast<const uint4*>(dZ + m * lddz + n)
-                                     : make_uint4(0u, 0u, 0u, 0u);
-            rb[e] = (k < K && n < N) ? *reinterpret_cast<const uint4*>(W + k * ldw + n)
-                                     : make_uint4(0u, 0u, 0u, 0u);
-        }
-    };
-
-    f32x16 acc[2][2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-    const int wr = (wave >> 1) * 64;
-    const int wc = (wave & 1) * 64;
-    const int li = lane & 31;
-    const int lk = (lane >> 5) * 8;
-
-    load_tile(0);
-    for (int64_t n0 = 0; n0 < N; n0 += BK) {
-        __syncthreads();
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int piece = tid + 256 * e;
-            const int row = piece >> 3, cb = (piece & 7) * 8;
-            *reinterpret_cast<uint4*>(&As[row][cb]) = ra[e];
-            *reinterpret_cast<uint4*>(&Bs[row][cb]) = rb[e];
-        }
-        __syncthreads();
-        if (n0 + BK < N) load_tile(n0 + BK);
-#pragma unroll
-        for (int ks = 0; ks < BK; ks += 16) {
-            bf16x8 a[2], b[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) a[i] = lds_frag(&As[wr + i * 32 + li][ks + lk]);
-#pragma unroll
-            for (int j = 0; j < 2; ++j) b[j] = lds_frag(&Bs[wc + j * 32 + li][ks + lk]);
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
-    }
-
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t m = m0 + wr + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                const int64_t k = k0 + wc + j * 32 + (lane & 31);
-                if (m < M && k < K) {
-                    const int64_t o = m * K + k;
-                    float val = acc[i][j][v];
-                    if (add) val += add[o];
-                    if (accum) val += dX[o];
-                    dX[o] = val;
-                    if (out16) out16[m * ld16 + k] = f2bf(val);
-                }
-            }
-}
-
 __global__ __launch_bounds__(256) void k_pack(int64_t rows, int64_t cols, const float* src,
                                               int64_t lds, uint16_t* dst, int64_t ldd, int64_t col0) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -268,50 +275,91 @@ __global__ __launch_bounds__(256) void k_pack(int64_t rows, int64_t cols, const 
     dst[r * ldd + col0 + c] = f2bf(src[r * lds + c]);
 }
 
-int dw_splits(int64_t M, int64_t K, int64_t N) {
-    const int64_t tiles = ((K + BM - 1) / BM) * ((N + BN - 1) / BN);
-    const int64_t iters = (M + BK - 1) / BK;
-    int64_t s = (512 + tiles - 1) / tiles;  // aim for >= 2 workgroups per CU
-    if (s > iters / 8) s = iters / 8;        // keep >= 8 iterations per split
-    if (s < 1) s = 1;
-    if (s > 64) s = 64;
-    return static_cast<int>(s);
+inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b - 1) / b); }
+
+constexpr int kCUs = 256;
+
+// Output-tile width and reduction splits for an R x Cc output with reduction Kr,
+// from a simple time model: rounds of 256 workgroups x the MFMA time of one
+// workgroup's share (about 1.2 us per 256x256x64 step), plus the HBM time of
+// writing and re-reading the split partials (4 TB/s).
+struct Plan {
+    int bn;
+    int splits;
+};
+
+Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split) {
+    Plan best{256, 1};
+    double best_us = 1e300;
+    const int bns[3] = {256, 192, 128};
+    for (int bn : bns) {
+        const int64_t tiles = ((R + 255) / 256) * ((Cc + bn - 1) / bn);
+        const int64_t iters = (Kr + BK - 1) / BK;
+        for (int s = 1; s <= (allow_split ? 32 : 1); ++s) {
+            if (s > 1 && iters / s < 8) break;
+            const int64_t wgs = tiles * s;
+            const double rounds = static_cast<double>((wgs + kCUs - 1) / kCUs);
+            double us = rounds * 1.2 * (bn / 256.0) * (static_cast<double>(Kr) / s / BK);
+            if (s > 1) us += static_cast<double>(s) * R * Cc * 8.0 / 4e12 * 1e6;
+            if (us < best_us * 0.999) {
+                best_us = us;
+                best = Plan{bn, s};
+            }
+        }
+    }
+    return best;
 }
 
-inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b - 1) / b); }
+template <bool TR, int BN>
+void launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
+    dim3 grid(cdiv(g.Cc, BN), cdiv(g.R, 256), static_cast<unsigned>(splits));
+    hipLaunchKernelGGL((k_gemm<TR, 256, BN>), grid, dim3(NT), 0, s, g);
+}
+
+template <bool TR>
+void launch_plan(const GemmArgs& g, const Plan& pl, hipStream_t s) {
+    switch (pl.bn) {
+        case 128: launch_tile<TR, 128>(g, pl.splits, s); break;
+        case 192: launch_tile<TR, 192>(g, pl.splits, s); break;
+        default: launch_tile<TR, 256>(g, pl.splits, s); break;
+    }
+}
 
 }  // namespace
 
 size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N) {
-    const int s = dw_splits(M, K, N);
-    return s > 1 ? static_cast<size_t>(s) * K * N * sizeof(float) : 0;
+    const Plan pl = plan_gemm(K, N, M, true);
+    return pl.splits > 1 ? static_cast<size_t>(pl.splits) * K * N * sizeof(float) : 0;
 }
 
 hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, int64_t ldx,
                           const uint16_t* dZ, int64_t lddz, float* dW, bool accum, void* ws,
                           hipStream_t s) {
-    const int splits = dw_splits(M, K, N);
-    int64_t per = (M + splits - 1) / splits;
+    const Plan pl = plan_gemm(K, N, M, true);
+    int64_t per = (M + pl.splits - 1) / pl.splits;
     per = (per + BK - 1) / BK * BK;
-    dim3 grid(cdiv(N, BN), cdiv(K, BM), static_cast<unsigned>(splits));
-    const bool direct = splits == 1;
-    float* out = direct ? dW : static_cast<float*>(ws);
-    SSMK_TIMED("gemm_dw", s);
-    hipLaunchKernelGGL(k_gemm_dw, grid, dim3(256), 0, s, M, K, N, X, ldx, dZ, lddz, out, per,
-                       direct ? 1 : 0, accum ? 1 : 0);
-    if (!direct)
-        hipLaunchKernelGGL(k_splitk_reduce, dim3(cdiv(K * N, 256)), dim3(256), 0, s, K * N, splits,
+    const bool direct = pl.splits == 1;
+    GemmArgs g{K, N, M, X, ldx, dZ, lddz, direct ? dW : static_cast<float*>(ws), per,
+               direct ? 1 : 0, accum ? 1 : 0, nullptr, nullptr, 0};
+    {
+        SSMK_TIMED("gemm_dw", s);
+        launch_plan<true>(g, pl, s);
+    }
+    if (!direct) {
+        SSMK_TIMED("splitk_reduce", s);
+        hipLaunchKernelGGL(k_splitk_reduce, dim3(cdiv(K * N, 256)), dim3(256), 0, s, K * N, pl.splits,
                            static_cast<const float*>(ws), dW, accum ? 1 : 0);
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, int64_t lddz,
                           const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
                           uint16_t* out16, int64_t ld16, hipStream_t s) {
-    dim3 grid(cdiv(K, BN), cdiv(M, BM));
+    const Plan pl = plan_gemm(M, K, N, false);
+    GemmArgs g{M, K, N, dZ, lddz, W, ldw, dX, (N + BK - 1) / BK * BK, 1, accum ? 1 : 0, add, out16, ld16};
     SSMK_TIMED("gemm_dx", s);
-    hipLaunchKernelGGL(k_gemm_dx, grid, dim3(256), 0, s, M, K, N, dZ, lddz, W, ldw, dX,
-                       accum ? 1 : 0, add, out16, ld16);
+    launch_plan<false>(g, pl, s);
     return hipGetLastError();
 }
 
