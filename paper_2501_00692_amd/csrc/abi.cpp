@@ -418,18 +418,19 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     p.nslice = ssmk::choose_nslice(p.nb, nc);
     grad_bind(p, x, delta_pre, A_log, B, C, nullptr, z, dy, dx_, dd_, dA_log, dB_, dC_, dz_, nullptr);
     ssmk::bind_workspace(p, ws + w.scan_off, sw);
-    hipError_t e = ssmk::launch_grad(p, s);
-    if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad scan launch");
-
-    // dZx = [dDelta_pre | dB | dC] (bf16), [dx_total | dz] (bf16)
+    // the scan kernels also write dZx = [dDelta_pre | dB | dC] and the dz half of
+    // [dx_total | dz] in bf16
     uint16_t* dzx = reinterpret_cast<uint16_t*>(ws + w.dzx_off);
     uint16_t* dxz = reinterpret_cast<uint16_t*>(ws + w.dxz_off);
     const int64_t nx = D + 2 * N;
-    if ((e = ssmk::launch_pack_bf16(M, D, dd_, D, dzx, nx, 0, s)) != hipSuccess ||
-        (e = ssmk::launch_pack_bf16(M, N, dB_, N, dzx, nx, D, s)) != hipSuccess ||
-        (e = ssmk::launch_pack_bf16(M, N, dC_, N, dzx, nx, D + N, s)) != hipSuccess ||
-        (e = ssmk::launch_pack_bf16(M, D, dz_, D, dxz, 2 * D, D, s)) != hipSuccess)
-        return hip_fail(e, "ssm_layer_grad pack launch");
+    p.dd16 = dzx;
+    p.ld_dd16 = nx;
+    p.bc16 = dzx + D;
+    p.ld_bc16 = nx;
+    p.dz16 = dxz + D;
+    p.ld_dz16 = 2 * D;
+    hipError_t e = ssmk::launch_grad(p, s);
+    if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad scan launch");
     void* gws = ws + w.gemm_off;
     // dW_x = x^T dZx
     e = ssmk::launch_gemm_dw(M, D, nx, static_cast<const uint16_t*>(x), D, dzx, nx, dW_x, false, gws, s);

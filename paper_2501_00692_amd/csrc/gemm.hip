@@ -12,7 +12,6 @@
 // tiles.  Interior tiles run a loop without bounds checks.
 // LDS is double-buffered over 64-deep reduction steps (one barrier per step);
 // the next step's global loads are in flight while the MFMAs run.
-//   k_pack : fp32 -> bf16 (round to nearest even) strided copy.
 #include "internal.h"
 
 namespace ssmk {
@@ -235,26 +234,38 @@ __global__ __launch_bounds__(NT) void k_gemm(const GemmArgs g) {
         gemm_mainloop<TR, BM, BN, false, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
 
     // acc element v of lane l is row 8*(v/4) + 4*(l/32) + v%4, col l%32 of its tile
-    float* dst = g.C + (g.direct ? 0 : static_cast<int64_t>(blockIdx.z) * g.R * g.Cc);
+    float* __restrict__ dst = g.C + (g.direct ? 0 : static_cast<int64_t>(blockIdx.z) * g.R * g.Cc);
+    const float* __restrict__ addp = g.direct ? g.add : nullptr;
+    const bool accum = g.direct && g.accum;
+    uint16_t* __restrict__ o16 = g.direct ? g.out16 : nullptr;
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < NJ; ++j)
+        for (int j = 0; j < NJ; ++j) {
+            const int64_t col = c0 + wc + j * 32 + (lane & 31);
+            const int64_t rb = r0 + wr + i * 32 + 4 * (lane >> 5);
+            // the tile's addends first, so that their loads overlap
+            float extra[16];
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int64_t row = r0 + wr + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                const int64_t col = c0 + wc + j * 32 + (lane & 31);
+                const int64_t row = rb + 8 * (v >> 2) + (v & 3);
+                const bool in = row < g.R && col < g.Cc;
+                const int64_t o = row * g.Cc + col;
+                float e = 0.f;
+                if (addp && in) e = addp[o];
+                if (accum && in) e += dst[o];
+                extra[v] = e;
+            }
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t row = rb + 8 * (v >> 2) + (v & 3);
                 if (row < g.R && col < g.Cc) {
-                    const int64_t o = row * g.Cc + col;
-                    float val = acc[i][j][v];
-                    if (g.direct) {
-                        if (g.add) val += g.add[o];
-                        if (g.accum) val += dst[o];
-                        if (g.out16) g.out16[row * g.ld16 + col] = f2bf(val);
-                    }
-                    dst[o] = val;
+                    const float val = acc[i][j][v] + extra[v];
+                    dst[row * g.Cc + col] = val;
+                    if (o16) o16[row * g.ld16 + col] = f2bf(val);
                 }
             }
+        }
 }
 
 // dW = (dW +) sum over splits, in split order.
@@ -265,14 +276,6 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(int64_t KN, int splits, c
     float s = 0.f;
     for (int q = 0; q < splits; ++q) s += part[q * KN + i];
     dW[i] = accum ? dW[i] + s : s;
-}
-
-__global__ __launch_bounds__(256) void k_pack(int64_t rows, int64_t cols, const float* src,
-                                              int64_t lds, uint16_t* dst, int64_t ldd, int64_t col0) {
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    if (i >= rows * cols) return;
-    const int64_t r = i / cols, c = i % cols;
-    dst[r * ldd + col0 + c] = f2bf(src[r * lds + c]);
 }
 
 inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b - 1) / b); }
@@ -360,14 +363,6 @@ hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, i
     GemmArgs g{M, K, N, dZ, lddz, W, ldw, dX, (N + BK - 1) / BK * BK, 1, accum ? 1 : 0, add, out16, ld16};
     SSMK_TIMED("gemm_dx", s);
     launch_plan<false>(g, pl, s);
-    return hipGetLastError();
-}
-
-hipError_t launch_pack_bf16(int64_t rows, int64_t cols, const float* src, int64_t lds,
-                            uint16_t* dst, int64_t ldd, int64_t col0, hipStream_t s) {
-    SSMK_TIMED("pack", s);
-    hipLaunchKernelGGL(k_pack, dim3(cdiv(rows * cols, 256)), dim3(256), 0, s, rows, cols, src, lds,
-                       dst, ldd, col0);
     return hipGetLastError();
 }
 

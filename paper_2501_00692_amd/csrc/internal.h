@@ -27,6 +27,10 @@ class TimedScope {
 #define SSMK_CAT(a, b) SSMK_CAT2(a, b)
 #define SSMK_TIMED(name, s) ::ssmk::TimedScope SSMK_CAT(ssmk_timed_, __LINE__)(name, s)
 
+// Waves per workgroup of the fused gradient kernel; each wave works on one
+// 16-channel tile at a time.
+constexpr int kGradWaves = 4;
+
 // One scan problem: the selective diagonal layer of shape [b][T][D] x N states,
 // split into nc = ceil(T / L) carry chunks of L steps.
 struct ScanProblem {
@@ -37,7 +41,7 @@ struct ScanProblem {
     bool trunc;      // truncated estimator with window tbar (< T)
     int64_t tbar;
     int nsplit;      // channel splits of the fused kernel (dB/dC partials when > 1)
-    int tps;         // 16-channel tiles per split (every split has at least one)
+    int tps;         // 16-channel tiles per split (a multiple of kGradWaves unless one split)
     int nslice;      // slices of the dA_log reduction
     // inputs
     const void* x;
@@ -58,6 +62,15 @@ struct ScanProblem {
     float* dC;
     float* dz;
     float* dh0;
+    // optional bf16 (round to nearest even) copies for the projection GEMMs:
+    // ddelta -> dd16[row * ld_dd16 + d], dz -> dz16[row * ld_dz16 + d],
+    // dB -> bc16[row * ld_bc16 + n], dC -> bc16[row * ld_bc16 + N + n], row = b*T + t
+    uint16_t* dd16;
+    int64_t ld_dd16;
+    uint16_t* dz16;
+    int64_t ld_dz16;
+    uint16_t* bc16;
+    int64_t ld_bc16;
     // workspace regions
     float* hbuf;    // [b][nc][N][D]
     float* mbuf;    // [b][nc][N][D]
@@ -98,7 +111,5 @@ hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, i
 
 // fp32 -> bf16 (round to nearest even) copy of a [rows][cols] block into a strided
 // destination: dst[r*ldd + col0 + c] = bf16(src[r*lds + c]).
-hipError_t launch_pack_bf16(int64_t rows, int64_t cols, const float* src, int64_t lds,
-                            uint16_t* dst, int64_t ldd, int64_t col0, hipStream_t s);
 
 }  // namespace ssmk

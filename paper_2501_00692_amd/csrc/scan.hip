@@ -28,16 +28,18 @@ int64_t default_chunk() { return 128; }
 bool chunk_supported(int64_t L) { return L == 16 || L == 32 || L == 64 || L == 128 || L == 256; }
 
 void choose_split(int64_t nb, int64_t D, int64_t nc, int* nsplit, int* tiles_per_split) {
-    // Enough single-wave workgroups to fill 256 CUs several times over; every
-    // split gets at least one 16-channel tile.
-    const int64_t target = 2048;
+    // Workgroups of kGradWaves waves take tiles in groups of kGradWaves; aim at
+    // one round of two workgroups per CU (256 CUs), every split with at least
+    // one group.
+    const int64_t target = 512;
     const int64_t ntile = (D + 15) / 16;
+    const int64_t groups = (ntile + kGradWaves - 1) / kGradWaves;
     int64_t ns = (target + nb * nc - 1) / (nb * nc);
     if (ns < 1) ns = 1;
-    if (ns > ntile) ns = ntile;
-    const int64_t tps = (ntile + ns - 1) / ns;
-    *tiles_per_split = static_cast<int>(tps);
-    *nsplit = static_cast<int>((ntile + tps - 1) / tps);
+    if (ns > groups) ns = groups;
+    const int64_t gps = (groups + ns - 1) / ns;
+    *tiles_per_split = static_cast<int>(gps * kGradWaves);
+    *nsplit = static_cast<int>((groups + gps - 1) / gps);
 }
 
 int choose_nslice(int64_t nb, int64_t nc) {

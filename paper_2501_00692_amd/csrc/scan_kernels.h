@@ -167,14 +167,17 @@ __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64
 //   mloc = sum_{t in c} g_t C_t prod_{j=s}^{t} a_j  (the adjoint that the chunk
 //          hands to h_{s-1} from a zero carry at its end),
 //   sdel = sum_{t in c} Delta_t (fp64).
-// Lane r prepares the per-channel quantities of steps s+r, s+r+4, ... and
-// broadcasts them to its quad; its raw inputs are loaded one group ahead.
+// B and C are staged in LDS as fp32, 64 steps at a time, for the whole
+// workgroup.  Lane r prepares the per-channel quantities of steps s+r, s+r+4,
+// ... and broadcasts them to its quad; its raw inputs are loaded one group ahead.
 // ---------------------------------------------------------------------------
 template <typename TI, bool SP, bool GATE, bool WANT_M, bool N16>
 __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
-    const int lane = threadIdx.x;
-    const int r = lane & 3;
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (lane >> 2);
+    constexpr int SB = 64;  // steps per staged block
+    __shared__ float bcs[SB][32];
+    const int tid = threadIdx.x;
+    const int r = tid & 3;
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const bool dv = d < p.D;
     const TI* Bp = static_cast<const TI*>(p.B);
@@ -187,36 +190,51 @@ __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
     const int64_t t1 = min(t0 + p.L, p.T);
     RawIn<1> nxt;
     load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, WANT_M, nxt);
-    for (int64_t s0 = t0; s0 < t1; s0 += 4) {
-        const RawIn<1> cur = nxt;
-        if (s0 + 4 < t1) load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, WANT_M, nxt);
-        const bool v = dv && s0 + r < t1;
-        const float dlr = (SP && v) ? softplus_f(cur.p[0]) : cur.p[0];
-        float gr = 0.f;
-        if constexpr (WANT_M) {
-            if constexpr (GATE)
-                gr = cur.dy[0] * cur.z[0] * sigmoid_f(cur.z[0]);
-            else
-                gr = cur.dy[0];
+    for (int64_t sb = t0; sb < t1; sb += SB) {
+        __syncthreads();  // the previous block has been consumed
+        for (int i = tid; i < SB * 32; i += 256) {
+            const int t = i >> 5, cc = i & 31, n = cc & 15;
+            const int64_t tg = sb + t;
+            const bool want = cc < 16 || WANT_M;
+            bcs[t][cc] = (want && tg < t1 && n < p.N) ? ldf(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n) : 0.f;
         }
-        sd += static_cast<double>(dlr);
+        __syncthreads();
+        const int64_t se = min(sb + SB, t1);
+        for (int64_t s0 = sb; s0 < se; s0 += 4) {
+            const RawIn<1> cur = nxt;
+            if (s0 + 4 < t1) load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, WANT_M, nxt);
+            const bool v = dv && s0 + r < t1;
+            const float dlr = (SP && v) ? softplus_f(cur.p[0]) : cur.p[0];
+            float gr = 0.f;
+            if constexpr (WANT_M) {
+                if constexpr (GATE)
+                    gr = cur.dy[0] * cur.z[0] * sigmoid_f(cur.z[0]);
+                else
+                    gr = cur.dy[0];
+            }
+            sd += static_cast<double>(dlr);
+            const int tb = static_cast<int>(s0 - sb);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t t = s0 + j;
-            const bool tv = t < t1;
-            const float xv = quad_bcast(cur.x[0], j);
-            const float dl = quad_bcast(dlr, j);
-            float Bv[4], Cv[4];
-            ld4<TI, N16>(Bp, bb * p.T + t, r, p.N, tv, Bv);
-            if constexpr (WANT_M) ld4<TI, N16>(Cp, bb * p.T + t, r, p.N, tv, Cv);
-            const float g = WANT_M ? quad_bcast(gr, j) : 0.f;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const float av = fexp2(cn[k] * dl);
-                h[k] = fmaf(av, h[k], Bv[k] * xv);
+            for (int j = 0; j < 4; ++j) {
+                // steps past the end have zero B, C, Delta and x: a = 1 and no input
+                const float xv = quad_bcast(cur.x[0], j);
+                const float dl = quad_bcast(dlr, j);
+                const float4 b4 = *reinterpret_cast<const float4*>(&bcs[tb + j][4 * r]);
+                const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
+                float Cv[4] = {0.f, 0.f, 0.f, 0.f};
                 if constexpr (WANT_M) {
-                    P[k] *= av;
-                    m[k] = fmaf(g * Cv[k], P[k], m[k]);
+                    const float4 c4 = *reinterpret_cast<const float4*>(&bcs[tb + j][16 + 4 * r]);
+                    Cv[0] = c4.x; Cv[1] = c4.y; Cv[2] = c4.z; Cv[3] = c4.w;
+                }
+                const float g = WANT_M ? quad_bcast(gr, j) : 0.f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float av = fexp2(cn[k] * dl);
+                    h[k] = fmaf(av, h[k], Bv[k] * xv);
+                    if constexpr (WANT_M) {
+                        P[k] *= av;
+                        m[k] = fmaf(g * Cv[k], P[k], m[k]);
+                    }
                 }
             }
         }
@@ -362,90 +380,35 @@ __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
     }
 }
 
-// Checkpoint storage indexed by a wave-uniform segment number (scalar branches).
-template <int NCK, int I = 0>
-__device__ __forceinline__ void ck_put(float (&ck)[NCK][4], int q, const float (&h)[4]) {
-    if constexpr (I < NCK) {
-        if (q == I) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) ck[I][k] = h[k];
-        } else {
-            ck_put<NCK, I + 1>(ck, q, h);
-        }
-    }
-}
-template <int NCK, int I = 0>
-__device__ __forceinline__ void ck_get(const float (&ck)[NCK][4], int q, float (&h)[4]) {
-    if constexpr (I < NCK) {
-        if (q == I) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) h[k] = ck[I][k];
-        } else {
-            ck_get<NCK, I + 1>(ck, q, h);
-        }
-    }
-}
-
 // ---------------------------------------------------------------------------
-// B_t and C_t of one chunk, staged in LDS once per workgroup: bf16 inputs keep
-// their bit patterns (two states per 32-bit word), fp32 inputs stay fp32.
-// Row t holds B (states 0..15) then C.
+// B_t and C_t of one chunk, staged in LDS as fp32 once per workgroup and read
+// by all of its waves.  Row t holds B (states 0..15) then C; padding is zero.
 // ---------------------------------------------------------------------------
 template <typename TI, int L>
 struct BCStage {
-    static constexpr int W = sizeof(TI) == 2 ? 16 : 32;  // 32-bit words per row
-    uint32_t w[L][W];
+    float w[L][32];
 
-    __device__ __forceinline__ void load(const ScanProblem& p, int64_t bb, int64_t t0, int lane) {
+    __device__ __forceinline__ void load(const ScanProblem& p, int64_t bb, int64_t t0, int tid,
+                                         int nthr) {
         const TI* Bp = static_cast<const TI*>(p.B);
         const TI* Cp = static_cast<const TI*>(p.C);
-        for (int i = lane; i < L * W; i += 64) {
-            const int t = i / W, c = i % W;
+        for (int i = tid; i < L * 32; i += nthr) {
+            const int t = i >> 5, c = i & 31, n = c & 15;
             const int64_t tg = t0 + t;
-            const bool tv = tg < p.T;
-            const int64_t row = (bb * p.T + tg) * p.N;
-            if constexpr (sizeof(TI) == 2) {
-                const TI* src = c < 8 ? Bp : Cp;
-                const int n0 = 2 * (c & 7);
-                const uint32_t lo = (tv && n0 < p.N) ? static_cast<uint32_t>(src[row + n0]) : 0u;
-                const uint32_t hi = (tv && n0 + 1 < p.N) ? static_cast<uint32_t>(src[row + n0 + 1]) : 0u;
-                w[t][c] = lo | (hi << 16);
-            } else {
-                const TI* src = c < 16 ? Bp : Cp;
-                const int n = c & 15;
-                const float v = (tv && n < p.N) ? ldf(src, row + n) : 0.f;
-                w[t][c] = __float_as_uint(v);
-            }
+            const TI* src = c < 16 ? Bp : Cp;
+            w[t][c] = (tg < p.T && n < p.N) ? ldf(src, (bb * p.T + tg) * p.N + n) : 0.f;
         }
     }
     // States 4r..4r+3 of B and C at in-chunk step t.
     __device__ __forceinline__ void get(int t, int r, float Bv[4], float Cv[4]) const {
-        if constexpr (sizeof(TI) == 2) {
-            const uint2 b = *reinterpret_cast<const uint2*>(&w[t][2 * r]);
-            const uint2 c = *reinterpret_cast<const uint2*>(&w[t][8 + 2 * r]);
-            Bv[0] = __uint_as_float(b.x << 16); Bv[1] = __uint_as_float(b.x & 0xffff0000u);
-            Bv[2] = __uint_as_float(b.y << 16); Bv[3] = __uint_as_float(b.y & 0xffff0000u);
-            Cv[0] = __uint_as_float(c.x << 16); Cv[1] = __uint_as_float(c.x & 0xffff0000u);
-            Cv[2] = __uint_as_float(c.y << 16); Cv[3] = __uint_as_float(c.y & 0xffff0000u);
-        } else {
-            const uint4 b = *reinterpret_cast<const uint4*>(&w[t][4 * r]);
-            const uint4 c = *reinterpret_cast<const uint4*>(&w[t][16 + 4 * r]);
-            Bv[0] = __uint_as_float(b.x); Bv[1] = __uint_as_float(b.y);
-            Bv[2] = __uint_as_float(b.z); Bv[3] = __uint_as_float(b.w);
-            Cv[0] = __uint_as_float(c.x); Cv[1] = __uint_as_float(c.y);
-            Cv[2] = __uint_as_float(c.z); Cv[3] = __uint_as_float(c.w);
-        }
+        const float4 b = *reinterpret_cast<const float4*>(&w[t][4 * r]);
+        const float4 c = *reinterpret_cast<const float4*>(&w[t][16 + 4 * r]);
+        Bv[0] = b.x; Bv[1] = b.y; Bv[2] = b.z; Bv[3] = b.w;
+        Cv[0] = c.x; Cv[1] = c.y; Cv[2] = c.z; Cv[3] = c.w;
     }
     __device__ __forceinline__ void getB(int t, int r, float Bv[4]) const {
-        if constexpr (sizeof(TI) == 2) {
-            const uint2 b = *reinterpret_cast<const uint2*>(&w[t][2 * r]);
-            Bv[0] = __uint_as_float(b.x << 16); Bv[1] = __uint_as_float(b.x & 0xffff0000u);
-            Bv[2] = __uint_as_float(b.y << 16); Bv[3] = __uint_as_float(b.y & 0xffff0000u);
-        } else {
-            const uint4 b = *reinterpret_cast<const uint4*>(&w[t][4 * r]);
-            Bv[0] = __uint_as_float(b.x); Bv[1] = __uint_as_float(b.y);
-            Bv[2] = __uint_as_float(b.z); Bv[3] = __uint_as_float(b.w);
-        }
+        const float4 b = *reinterpret_cast<const float4*>(&w[t][4 * r]);
+        Bv[0] = b.x; Bv[1] = b.y; Bv[2] = b.z; Bv[3] = b.w;
     }
 };
 
@@ -485,15 +448,21 @@ __device__ __forceinline__ void load_raw2(const ChunkPtrs<TI>& c, uint32_t D, ui
     }
 }
 
+// Orders one wave's LDS writes before its own later LDS reads of other lanes'
+// data (LDS executes a wave's operations in order; this only stops the compiler
+// from moving them).
+__device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
+
 // ---------------------------------------------------------------------------
-// k_grad: grid (nsplit, nc, b), one wave (64 lanes) per workgroup.  The
-// workgroup owns carry chunk c (L = S*NCK steps) and a range of 16-channel
-// tiles; lanes of a quad share a channel and hold 4 of its states.  B and C of
-// the chunk are staged in LDS once.  Per tile:
+// k_grad: grid (nsplit, nc, b), kGradWaves waves per workgroup.  The workgroup
+// owns carry chunk c (L = S*NCK steps) and the 16-channel tiles of its split;
+// wave w takes tiles tile_lo + w, tile_lo + w + kGradWaves, ..., so the waves
+// read adjacent channels together.  Lanes of a quad share a channel and hold 4
+// of its states.  B and C of the chunk are staged in LDS once.  Per tile:
 //   1. checkpoint sweep: from the carry-in state H_c, the state at the start of
 //      each S-step segment;
 //   2. segments in reverse order: recompute the segment's states forward
-//      (keeping a_t and a_t h_{t-1}), write dz, sum g_t h_t over the channels
+//      (keeping a_t and a_t h_{t-1}), form dz, sum g_t h_t over the channels
 //      (dC); then run the adjoint backwards, mu_t = g_t C_t + a_{t+1} mu_{t+1},
 //      from the chunk's reverse carry M_c, and apply the vjp epilogue:
 //        s = mubar a_t h_{t-1};  ddelta = sum_n s wn;  dA_log += s Delta wn;
@@ -503,65 +472,82 @@ __device__ __forceinline__ void load_raw2(const ChunkPtrs<TI>& c, uint32_t D, ui
 //      the carry of its own chunk, and P(t, t+tbar) = 2^{cn W_t} with the window
 //      sum W_t = sum_{j=t+1}^{t+tbar} Delta_j kept in fp64.
 // Per-channel quantities (softplus, the gate) are computed once per step: lane
-// r of a quad prepares steps r, r+4, ... of the segment and DPP-broadcasts
-// them; the next segment's raw inputs are loaded ahead.  Sums over channels of
-// dB/dC go through LDS once per segment and accumulate across tiles in the
-// output (nsplit == 1) or in per-split partials.
+// r of a quad prepares steps r, r+4, ... of the segment, DPP-broadcasts them,
+// keeps that step's per-channel outputs and stores them after the segment; the
+// next segment's raw inputs are loaded ahead.
+// Sums over channels of dB/dC: each wave sums its 16 channels per (step, state)
+// through LDS, the wave sums are added in wave order into a chunk accumulator
+// in LDS, and the workgroup writes the accumulator once at the end (into dB/dC,
+// or into its split's partial when nsplit > 1).  All orders are fixed.
 // ---------------------------------------------------------------------------
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_grad(const ScanProblem p) {
+__global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_grad(const ScanProblem p) {
+    constexpr int NW = kGradWaves;
+    constexpr int NTH = 64 * NW;
     constexpr int L = S * NCK;
     constexpr int SPL = S / 4;  // steps each lane prepares per segment
-    __shared__ float red[S][16][20];  // [step][state][channel], 16-byte aligned rows
+    constexpr int NP = S * 16;  // (step, state) pairs of a segment
+    static_assert(NP % 64 == 0 && NP <= NTH, "pair layout");
     __shared__ BCStage<TI, L> bc;
-    const int lane = threadIdx.x;
+    __shared__ float red[NW][S][16][20];  // per wave [step][state][channel], 16-byte aligned rows
+    __shared__ float wsum[2][NW][NP];     // per-wave channel sums, alternating buffers
+    __shared__ float acc[L][32];          // chunk totals: dB in columns 0..15, dC in 16..31
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
     const int r = lane & 3, chl = lane >> 2;
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const int split = blockIdx.x;
     const int64_t t0 = c * L;
     const int64_t lim = p.T - t0;  // in-chunk steps tl < lim are real
     const uint32_t D32 = static_cast<uint32_t>(p.D);
-    const int64_t btn = p.nb * p.T * p.N;
     ChunkPtrs<TI> cp;
     cp.set(p, bb * p.T + t0);
     float* dxo = p.dx + (bb * p.T + t0) * p.D;
     float* ddo = p.ddelta + (bb * p.T + t0) * p.D;
     float* dzo = GATE ? p.dz + (bb * p.T + t0) * p.D : nullptr;
-    float* dBo = p.nsplit == 1 ? p.dB : p.pB + static_cast<int64_t>(split) * btn;
-    float* dCo = p.nsplit == 1 ? p.dC : p.pC + static_cast<int64_t>(split) * btn;
+    uint16_t* dd16o = p.dd16 ? p.dd16 + (bb * p.T + t0) * p.ld_dd16 : nullptr;
+    uint16_t* dz16o = (GATE && p.dz16) ? p.dz16 + (bb * p.T + t0) * p.ld_dz16 : nullptr;
+    const uint32_t ldd16 = static_cast<uint32_t>(p.ld_dd16), ldz16 = static_cast<uint32_t>(p.ld_dz16);
 
     const int64_t ntile = (p.D + 15) / 16;
     const int64_t tile_lo = static_cast<int64_t>(split) * p.tps;
     const int64_t tile_hi = min(ntile, tile_lo + p.tps);
+    const int64_t nit = (tile_hi - tile_lo + NW - 1) / NW;  // the same for every wave
 
-    bc.load(p, bb, t0, lane);
+    for (int i = tid; i < L * 32; i += NTH) (&acc[0][0])[i] = 0.f;
+    bc.load(p, bb, t0, tid, NTH);
     __syncthreads();
 
-    // Sum red[j][n][0..15] for the S*16 (step, state) pairs of segment q and add
-    // the result into dst (or store it, for the first tile of the split).
-    auto flush = [&](float* dst, int q, bool first) {
+    int fb = 0;
+    // Channel sums of red[wave] for the pairs of segment q, added over the waves
+    // (in wave order) into acc columns col..col+15.  Every wave calls it.
+    auto flush = [&](int q, int col) {
+        wave_lds_sync();
 #pragma unroll
-        for (int i = 0; i < S * 16 / 64; ++i) {
+        for (int i = 0; i < NP / 64; ++i) {
             const int o = lane + 64 * i;
             const int j = o >> 4, n = o & 15;
-            const float4 a0 = *reinterpret_cast<const float4*>(&red[j][n][0]);
-            const float4 a1 = *reinterpret_cast<const float4*>(&red[j][n][4]);
-            const float4 a2 = *reinterpret_cast<const float4*>(&red[j][n][8]);
-            const float4 a3 = *reinterpret_cast<const float4*>(&red[j][n][12]);
-            const float s = (((a0.x + a0.y) + (a0.z + a0.w)) + ((a1.x + a1.y) + (a1.z + a1.w))) +
-                            (((a2.x + a2.y) + (a2.z + a2.w)) + ((a3.x + a3.y) + (a3.z + a3.w)));
-            const int64_t t = t0 + q * S + j;
-            if (t < p.T && n < p.N) {
-                const int64_t idx = (bb * p.T + t) * p.N + n;
-                dst[idx] = first ? s : dst[idx] + s;
-            }
+            const float4 a0 = *reinterpret_cast<const float4*>(&red[wave][j][n][0]);
+            const float4 a1 = *reinterpret_cast<const float4*>(&red[wave][j][n][4]);
+            const float4 a2 = *reinterpret_cast<const float4*>(&red[wave][j][n][8]);
+            const float4 a3 = *reinterpret_cast<const float4*>(&red[wave][j][n][12]);
+            wsum[fb][wave][o] = (((a0.x + a0.y) + (a0.z + a0.w)) + ((a1.x + a1.y) + (a1.z + a1.w))) +
+                                (((a2.x + a2.y) + (a2.z + a2.w)) + ((a3.x + a3.y) + (a3.z + a3.w)));
         }
+        __syncthreads();
+        if (tid < NP) {
+            float s = wsum[fb][0][tid];
+#pragma unroll
+            for (int w = 1; w < NW; ++w) s += wsum[fb][w][tid];
+            acc[q * S + (tid >> 4)][col + (tid & 15)] += s;
+        }
+        fb ^= 1;
     };
 
-    for (int64_t tile = tile_lo; tile < tile_hi; ++tile) {
-        const bool first = tile == tile_lo;
+    for (int64_t it = 0; it < nit; ++it) {
+        const int64_t tile = tile_lo + it * NW + wave;
         const int64_t d = tile * 16 + chl;
-        const bool dv = d < p.D;
+        const bool dv = tile < tile_hi && d < p.D;
         float cn[4], wn[4];
         lane_consts(p.A_log, d, r, p.N, dv, cn, wn);
         bool nv[4];
@@ -574,11 +560,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
         float h[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) h[k] = nv[k] ? p.hbuf[cb + k * p.D] : 0.f;
-        float ck[NCK][4];
+        // segment-start states, in private memory (indexed by the segment)
+        float4 ck[NCK];
         RawIn<SPL> nxt;
         load_raw2<TI, GATE, SPL>(cp, D32, d32, 0, r, lim, dv, false, nxt);
+#pragma unroll 1
         for (int q = 0; q < NCK; ++q) {
-            ck_put<NCK>(ck, q, h);
+            ck[q] = make_float4(h[0], h[1], h[2], h[3]);
             const RawIn<SPL> cur = nxt;
             if (q + 1 < NCK) load_raw2<TI, GATE, SPL>(cp, D32, d32, (q + 1) * S, r, lim, dv, false, nxt);
             float dls[SPL];
@@ -660,8 +648,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
         RawIn<SPL> nxs;  // raw inputs at the shifted positions (truncated mode)
         load_raw2<TI, GATE, SPL>(cp, D32, d32, (NCK - 1) * S, r, lim, dv, true, nxt);
         if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (NCK - 1) * S, r, lims, dv, true, nxs);
+        float4 hq = ck[NCK - 1];
+#pragma unroll 1
         for (int q = NCK - 1; q >= 0; --q) {
-            ck_get<NCK>(ck, q, h);
+            h[0] = hq.x; h[1] = hq.y; h[2] = hq.z; h[3] = hq.w;
+            if (q > 0) hq = ck[q - 1];
             const RawIn<SPL> cur = nxt;
             RawIn<SPL> cus;
             if constexpr (TRUNC) cus = nxs;
@@ -670,12 +661,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
                 if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (q - 1) * S, r, lims, dv, true, nxs);
             }
             // per-channel quantities of the steps this lane prepares
-            float dls[SPL], gs[SPL], gfs[SPL], sgs[SPL], dlps[SPL], gps[SPL];
+            float dls[SPL], gs[SPL], gfs[SPL], dlps[SPL], gps[SPL];
+            bool sv[SPL];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) {
-                const bool v = dv && q * S + r + 4 * jj < lim;
-                dls[jj] = (SP && v) ? softplus_f(cur.p[jj]) : cur.p[jj];
-                sgs[jj] = SP ? 1.f - __expf(-dls[jj]) : 1.f;  // d softplus / d Delta_pre
+                sv[jj] = dv && q * S + r + 4 * jj < lim;
+                dls[jj] = (SP && sv[jj]) ? softplus_f(cur.p[jj]) : cur.p[jj];
                 if constexpr (GATE) {
                     const float sg = sigmoid_f(cur.z[jj]);
                     gs[jj] = cur.dy[jj] * cur.z[jj] * sg;
@@ -695,6 +686,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
             }
 
             float ahp[S][4], ah[S][4], gh[S], dlh[S], xh[S];
+            float yk[SPL];
+#pragma unroll
+            for (int jj = 0; jj < SPL; ++jj) yk[jj] = 0.f;
 #pragma unroll
             for (int j = 0; j < S; ++j) {
                 const int tl = q * S + j;
@@ -710,20 +704,33 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
                     ah[j][k] = av;
                     ahp[j][k] = av * h[k];
                     h[k] = fmaf(Bv[k], xv, ahp[j][k]);
-                    yp = fmaf(Cv[k], h[k], yp);
-                    red[j][r * 4 + k][chl] = g * h[k];
+                    if constexpr (GATE) yp = fmaf(Cv[k], h[k], yp);
+                    red[wave][j][r * 4 + k][chl] = g * h[k];
                 }
                 if constexpr (GATE) {
                     const float y = quad_sum(yp);
-                    if (r == (j & 3) && tl < lim && dv) dzo[static_cast<uint32_t>(tl) * D32 + d32] = gfs[j >> 2] * y;
+                    if ((j & 3) == r) yk[j >> 2] = y;
                 }
                 gh[j] = g;
                 dlh[j] = dl;
                 xh[j] = xv;
             }
-            __syncthreads();
-            flush(dCo, q, first);
-            __syncthreads();
+            if constexpr (GATE) {
+#pragma unroll
+                for (int jj = 0; jj < SPL; ++jj) {
+                    if (sv[jj]) {
+                        const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
+                        const float v = gfs[jj] * yk[jj];
+                        dzo[tl * D32 + d32] = v;
+                        if (dz16o) stf(dz16o, tl * ldz16 + d32, v);
+                    }
+                }
+            }
+            flush(q, 16);
+
+            float dxk[SPL], ddk[SPL];
+#pragma unroll
+            for (int jj = 0; jj < SPL; ++jj) dxk[jj] = ddk[jj] = 0.f;
 #pragma unroll
             for (int j = S - 1; j >= 0; --j) {
                 const int tl = q * S + j;
@@ -758,24 +765,46 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
                     const float s = mb[k] * ahp[j][k];
                     ddp = fmaf(s, wn[k], ddp);
                     dA[k] = fmaf(s, dlh[j], dA[k]);
-                    red[j][r * 4 + k][chl] = mb[k] * xh[j];
+                    red[wave][j][r * 4 + k][chl] = mb[k] * xh[j];
                     Mp[k] = ah[j][k] * mu[k];
                 }
                 const float dxv = quad_sum(dxp);
                 const float ddv = quad_sum(ddp);
-                if (r == (j & 3) && tl < lim && dv) {
-                    const uint32_t off = static_cast<uint32_t>(tl) * D32 + d32;
-                    dxo[off] = dxv;
-                    ddo[off] = ddv * sgs[j >> 2];
+                if ((j & 3) == r) {
+                    dxk[j >> 2] = dxv;
+                    ddk[j >> 2] = ddv;
                 }
             }
-            __syncthreads();
-            flush(dBo, q, first);
-            __syncthreads();
+#pragma unroll
+            for (int jj = 0; jj < SPL; ++jj) {
+                if (sv[jj]) {
+                    const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
+                    const uint32_t off = tl * D32 + d32;
+                    const float ddv = SP ? ddk[jj] * (1.f - __expf(-dls[jj])) : ddk[jj];  // d softplus / d Delta_pre
+                    dxo[off] = dxk[jj];
+                    ddo[off] = ddv;
+                    if (dd16o) stf(dd16o, tl * ldd16 + d32, ddv);
+                }
+            }
+            flush(q, 0);
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k)
             if (nv[k]) p.hbuf[cb + k * p.D] = dA[k] * wn[k];
+    }
+
+    __syncthreads();
+    const int64_t btn = p.nb * p.T * p.N;
+    float* dBo = p.nsplit == 1 ? p.dB : p.pB + static_cast<int64_t>(split) * btn;
+    float* dCo = p.nsplit == 1 ? p.dC : p.pC + static_cast<int64_t>(split) * btn;
+    for (int i = tid; i < L * 32; i += NTH) {
+        const int t = i >> 5, cc = i & 31, n = cc & 15;
+        if (t < lim && n < p.N) {
+            const int64_t row = bb * p.T + t0 + t;
+            float* dst = cc < 16 ? dBo : dCo;
+            dst[row * p.N + n] = acc[t][cc];
+            if (p.nsplit == 1 && p.bc16) stf(p.bc16, row * p.ld_bc16 + (cc < 16 ? 0 : p.N) + n, acc[t][cc]);
+        }
     }
 }
 
@@ -791,6 +820,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 8))) void
     }
     p.dB[i] = sb;
     p.dC[i] = sc;
+    if (p.bc16) {
+        const int64_t row = i / p.N, n = i % p.N;
+        stf(p.bc16, row * p.ld_bc16 + n, sb);
+        stf(p.bc16, row * p.ld_bc16 + p.N + n, sc);
+    }
 }
 
 // dA_log, stage 1: grid (ceil(D/256), N, nslice); slice s sums the (b, chunk)
@@ -841,7 +875,7 @@ void grad_main(const ScanProblem& p, hipStream_t s) {
     dim3 g(static_cast<unsigned>(p.nsplit), static_cast<unsigned>(p.nc),
            static_cast<unsigned>(p.nb));
     SSMK_TIMED("grad_fused", s);
-    hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK>), g, dim3(64), 0, s, p);
+    hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK>), g, dim3(64 * kGradWaves), 0, s, p);
 }
 
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16>
