@@ -79,11 +79,12 @@ struct ScanProblem {
     float* pB;      // [nsplit][b][T][N]
     float* pC;      // [nsplit][b][T][N]
     float* dAtmp;   // [nslice][N][D]
+    float* sink;    // 1 KB that padding lanes store into (gradient only)
 };
 
 // Workspace layout shared by the size query and the launch.
 struct ScanWorkspace {
-    size_t off_hbuf, off_mbuf, off_sdel, off_psum, off_pB, off_pC, off_dAtmp, total;
+    size_t off_hbuf, off_mbuf, off_sdel, off_psum, off_pB, off_pC, off_dAtmp, off_sink, total;
 };
 
 int64_t default_chunk();

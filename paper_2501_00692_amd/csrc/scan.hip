@@ -78,6 +78,8 @@ ScanWorkspace scan_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_
         w.off_dAtmp = off;
         off = align_up(off + static_cast<size_t>(choose_nslice(nb, nc)) * N * D * sizeof(float));
     }
+    w.off_sink = off;
+    if (grad) off = align_up(off + 1024);
     w.total = off;
     return w;
 }
@@ -90,7 +92,8 @@ void bind_workspace(ScanProblem& p, void* ws, const ScanWorkspace& w) {
     p.psum = w.off_psum != w.off_pB ? reinterpret_cast<double*>(b + w.off_psum) : nullptr;
     p.pB = w.off_pB != w.off_pC ? reinterpret_cast<float*>(b + w.off_pB) : nullptr;
     p.pC = p.pB ? reinterpret_cast<float*>(b + w.off_pC) : nullptr;
-    p.dAtmp = w.off_dAtmp != w.total ? reinterpret_cast<float*>(b + w.off_dAtmp) : nullptr;
+    p.dAtmp = w.off_dAtmp != w.off_sink ? reinterpret_cast<float*>(b + w.off_dAtmp) : nullptr;
+    p.sink = w.off_sink != w.total ? reinterpret_cast<float*>(b + w.off_sink) : nullptr;
 }
 
 hipError_t launch_forward(const ScanProblem& p, hipStream_t s) {

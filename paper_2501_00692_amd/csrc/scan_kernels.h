@@ -30,6 +30,16 @@ __device__ __forceinline__ float ldf(const uint16_t* p, int64_t i) {
     return __uint_as_float(static_cast<uint32_t>(p[i]) << 16);
 }
 __device__ __forceinline__ void stf(float* p, int64_t i, float v) { p[i] = v; }
+
+// Masked loads without a branch: a lane whose element is not valid reads
+// element 0 of the same array (which exists) and discards the value.  The load
+// is then issued unconditionally and waited on at its first use; a load under
+// a divergent condition is waited on inside its own branch, right after issue.
+template <typename T>
+__device__ __forceinline__ float ldm(const T* p, int64_t i, bool v) {
+    const float r = ldf(p, v ? i : 0);
+    return v ? r : 0.f;
+}
 __device__ __forceinline__ void stf(uint16_t* p, int64_t i, float v) {
     uint32_t u = __float_as_uint(v);
     uint16_t r;
@@ -70,30 +80,37 @@ __device__ __forceinline__ float quad_sum(float v) {
     return v;
 }
 
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS operations
+// but leaves its global loads and stores in flight (a plain __syncthreads also
+// drains those, which would stall the loads issued ahead of their use).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Load 4 consecutive states (r*4 .. r*4+3) of row `row` of a [rows][N] tensor.
 template <typename TI, bool N16>
 __device__ __forceinline__ void ld4(const TI* p, int64_t row, int r, int64_t N, bool valid,
                                     float v[4]) {
     if constexpr (N16) {
-        if (!valid) {
-            v[0] = v[1] = v[2] = v[3] = 0.f;
-            return;
-        }
+        const int64_t o = valid ? row * 16 + r * 4 : 0;  // no branch around the load
         if constexpr (sizeof(TI) == 2) {
-            const uint2 u = *reinterpret_cast<const uint2*>(p + row * 16 + r * 4);
-            v[0] = __uint_as_float(u.x << 16);
-            v[1] = __uint_as_float(u.x & 0xffff0000u);
-            v[2] = __uint_as_float(u.y << 16);
-            v[3] = __uint_as_float(u.y & 0xffff0000u);
+            const uint2 u = *reinterpret_cast<const uint2*>(p + o);
+            v[0] = valid ? __uint_as_float(u.x << 16) : 0.f;
+            v[1] = valid ? __uint_as_float(u.x & 0xffff0000u) : 0.f;
+            v[2] = valid ? __uint_as_float(u.y << 16) : 0.f;
+            v[3] = valid ? __uint_as_float(u.y & 0xffff0000u) : 0.f;
         } else {
-            const float4 f = *reinterpret_cast<const float4*>(p + row * 16 + r * 4);
-            v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+            const float4 f = *reinterpret_cast<const float4*>(p + o);
+            v[0] = valid ? f.x : 0.f; v[1] = valid ? f.y : 0.f;
+            v[2] = valid ? f.z : 0.f; v[3] = valid ? f.w : 0.f;
         }
     } else {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int n = r * 4 + k;
-            v[k] = (valid && n < N) ? ldf(p, row * N + n) : 0.f;
+            v[k] = ldm(p, row * N + n, valid && n < N);
         }
     }
 }
@@ -105,7 +122,9 @@ __device__ __forceinline__ void lane_consts(const float* A_log, int64_t d, int r
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int n = r * 4 + k;
-        const float e = (dv && n < N) ? __expf(A_log[d * N + n]) : 0.f;
+        const bool v = dv && n < N;
+        const float al = ldm(A_log, d * N + n, v);
+        const float e = v ? __expf(al) : 0.f;
         wn[k] = -e;
         cn[k] = -e * kLog2e;
     }
@@ -131,14 +150,26 @@ __device__ __forceinline__ float quad_bcast(float v, int src) {
     }
 }
 
-// Raw per-(step, channel) inputs of the steps a lane prepares for its quad.
+// Raw per-(step, channel) inputs of the steps a lane prepares for its quad, as
+// element bits: they are loaded a group or segment ahead and converted at their
+// first use, so that nothing waits for the loads before then.
 template <int SPL>
 struct RawIn {
-    float x[SPL], p[SPL], dy[SPL], z[SPL];
+    uint32_t x[SPL], p[SPL], dy[SPL], z[SPL];
 };
 
-// Load the raw inputs of the steps j = r + 4*jj of segment [ts, ts+S) (zero where
-// t >= T or the channel is padding).  `full` also loads dy and z.
+__device__ __forceinline__ uint32_t ldbits(const float* p, int64_t i) { return __float_as_uint(p[i]); }
+__device__ __forceinline__ uint32_t ldbits(const uint16_t* p, int64_t i) { return p[i]; }
+// Value of element bits loaded by ldbits; 0 where the element is padding.
+template <typename TI>
+__device__ __forceinline__ float fin(uint32_t b, bool v) {
+    const float f = sizeof(TI) == 2 ? __uint_as_float(b << 16) : __uint_as_float(b);
+    return v ? f : 0.f;
+}
+
+// Load the raw inputs of the steps j = r + 4*jj of segment [ts, ts+S); lanes whose
+// step (t >= T) or channel is padding load element 0 instead.  `full` also loads
+// dy and z.
 template <typename TI, bool GATE, int SPL>
 __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64_t ts, int64_t d,
                                          bool dv, int r, bool full, RawIn<SPL>& o) {
@@ -150,12 +181,12 @@ __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64
     for (int jj = 0; jj < SPL; ++jj) {
         const int64_t t = ts + r + 4 * jj;
         const bool v = dv && t < p.T;
-        const int64_t td = (bb * p.T + t) * p.D + d;
-        o.x[jj] = v ? ldf(X, td) : 0.f;
-        o.p[jj] = v ? ldf(DL, td) : 0.f;
+        const int64_t td = v ? (bb * p.T + t) * p.D + d : 0;
+        o.x[jj] = ldbits(X, td);
+        o.p[jj] = ldbits(DL, td);
         if (full) {
-            o.dy[jj] = v ? ldf(DY, td) : 0.f;
-            o.z[jj] = (GATE && v) ? ldf(Z, td) : 0.f;
+            o.dy[jj] = ldbits(DY, td);
+            o.z[jj] = GATE ? ldbits(Z, td) : 0u;
         }
     }
 }
@@ -174,7 +205,7 @@ __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64
 template <typename TI, bool SP, bool GATE, bool WANT_M, bool N16>
 __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
     constexpr int SB = 64;  // steps per staged block
-    __shared__ float bcs[SB][32];
+    __shared__ __attribute__((aligned(16))) float bcs[SB][32];
     const int tid = threadIdx.x;
     const int r = tid & 3;
     const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);
@@ -191,33 +222,37 @@ __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
     RawIn<1> nxt;
     load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, WANT_M, nxt);
     for (int64_t sb = t0; sb < t1; sb += SB) {
-        __syncthreads();  // the previous block has been consumed
+        lds_barrier();  // the previous block has been consumed
         for (int i = tid; i < SB * 32; i += 256) {
             const int t = i >> 5, cc = i & 31, n = cc & 15;
             const int64_t tg = sb + t;
             const bool want = cc < 16 || WANT_M;
-            bcs[t][cc] = (want && tg < t1 && n < p.N) ? ldf(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n) : 0.f;
+            bcs[t][cc] = ldm(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, want && tg < t1 && n < p.N);
         }
-        __syncthreads();
+        lds_barrier();
         const int64_t se = min(sb + SB, t1);
         for (int64_t s0 = sb; s0 < se; s0 += 4) {
             const RawIn<1> cur = nxt;
             if (s0 + 4 < t1) load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, WANT_M, nxt);
             const bool v = dv && s0 + r < t1;
-            const float dlr = (SP && v) ? softplus_f(cur.p[0]) : cur.p[0];
+            const float pr = fin<TI>(cur.p[0], v), xr = fin<TI>(cur.x[0], v);
+            const float dlr = (SP && v) ? softplus_f(pr) : pr;
             float gr = 0.f;
             if constexpr (WANT_M) {
-                if constexpr (GATE)
-                    gr = cur.dy[0] * cur.z[0] * sigmoid_f(cur.z[0]);
-                else
-                    gr = cur.dy[0];
+                const float dyr = fin<TI>(cur.dy[0], v);
+                if constexpr (GATE) {
+                    const float zr = fin<TI>(cur.z[0], v);
+                    gr = dyr * zr * sigmoid_f(zr);
+                } else {
+                    gr = dyr;
+                }
             }
             sd += static_cast<double>(dlr);
             const int tb = static_cast<int>(s0 - sb);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 // steps past the end have zero B, C, Delta and x: a = 1 and no input
-                const float xv = quad_bcast(cur.x[0], j);
+                const float xv = quad_bcast(xr, j);
                 const float dl = quad_bcast(dlr, j);
                 const float4 b4 = *reinterpret_cast<const float4*>(&bcs[tb + j][4 * r]);
                 const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
@@ -353,7 +388,7 @@ __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
 #pragma unroll
     for (int n = 0; n < 16; ++n) {
         cn[n] = n < p.N ? -__expf(p.A_log[d * p.N + n]) * kLog2e : 0.f;
-        h[n] = n < p.N ? p.hbuf[cb + n * p.D] : 0.f;
+        h[n] = ldm(p.hbuf, cb + n * p.D, n < p.N);
     }
     const int64_t t0 = c * p.L;
     const int64_t t1 = min(t0 + p.L, p.T);
@@ -385,7 +420,7 @@ __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
 // by all of its waves.  Row t holds B (states 0..15) then C; padding is zero.
 // ---------------------------------------------------------------------------
 template <typename TI, int L>
-struct BCStage {
+struct __attribute__((aligned(16))) BCStage {
     float w[L][32];
 
     __device__ __forceinline__ void load(const ScanProblem& p, int64_t bb, int64_t t0, int tid,
@@ -396,7 +431,7 @@ struct BCStage {
             const int t = i >> 5, c = i & 31, n = c & 15;
             const int64_t tg = t0 + t;
             const TI* src = c < 16 ? Bp : Cp;
-            w[t][c] = (tg < p.T && n < p.N) ? ldf(src, (bb * p.T + tg) * p.N + n) : 0.f;
+            w[t][c] = ldm(src, (bb * p.T + tg) * p.N + n, tg < p.T && n < p.N);
         }
     }
     // States 4r..4r+3 of B and C at in-chunk step t.
@@ -429,8 +464,8 @@ struct ChunkPtrs {
     }
 };
 
-// Raw inputs of the steps tl = tq + r + 4*jj (in-chunk index) that lane r prepares,
-// zero where the step or the channel is padding (steps tl >= lim are padding).
+// Raw inputs of the steps tl = tq + r + 4*jj (in-chunk index) that lane r prepares;
+// lanes whose step (tl >= lim) or channel is padding load element 0 instead.
 template <typename TI, bool GATE, int SPL>
 __device__ __forceinline__ void load_raw2(const ChunkPtrs<TI>& c, uint32_t D, uint32_t d, int tq,
                                           int r, int64_t lim, bool dv, bool full, RawIn<SPL>& o) {
@@ -438,12 +473,12 @@ __device__ __forceinline__ void load_raw2(const ChunkPtrs<TI>& c, uint32_t D, ui
     for (int jj = 0; jj < SPL; ++jj) {
         const int tl = tq + r + 4 * jj;
         const bool v = dv && tl < lim;
-        const uint32_t off = static_cast<uint32_t>(tl) * D + d;
-        o.x[jj] = v ? ldf(c.x, off) : 0.f;
-        o.p[jj] = v ? ldf(c.p, off) : 0.f;
+        const uint32_t off = v ? static_cast<uint32_t>(tl) * D + d : 0u;
+        o.x[jj] = ldbits(c.x, off);
+        o.p[jj] = ldbits(c.p, off);
         if (full) {
-            o.dy[jj] = v ? ldf(c.dy, off) : 0.f;
-            o.z[jj] = (GATE && v) ? ldf(c.z, off) : 0.f;
+            o.dy[jj] = ldbits(c.dy, off);
+            o.z[jj] = GATE ? ldbits(c.z, off) : 0u;
         }
     }
 }
@@ -480,7 +515,7 @@ __device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMI
 // in LDS, and the workgroup writes the accumulator once at the end (into dB/dC,
 // or into its split's partial when nsplit > 1).  All orders are fixed.
 // ---------------------------------------------------------------------------
-template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK>
+template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK, bool OUT16>
 __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_grad(const ScanProblem p) {
     constexpr int NW = kGradWaves;
     constexpr int NTH = 64 * NW;
@@ -489,9 +524,9 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     constexpr int NP = S * 16;  // (step, state) pairs of a segment
     static_assert(NP % 64 == 0 && NP <= NTH, "pair layout");
     __shared__ BCStage<TI, L> bc;
-    __shared__ float red[NW][S][16][20];  // per wave [step][state][channel], 16-byte aligned rows
-    __shared__ float wsum[2][NW][NP];     // per-wave channel sums, alternating buffers
-    __shared__ float acc[L][32];          // chunk totals: dB in columns 0..15, dC in 16..31
+    __shared__ __attribute__((aligned(16))) float red[NW][S][16][20];  // per wave [step][state][channel]
+    __shared__ float wsum[2][NW][NP];  // per-wave channel sums, alternating buffers
+    __shared__ float acc[L][32];       // chunk totals: dB in columns 0..15, dC in 16..31
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     const int r = lane & 3, chl = lane >> 2;
@@ -505,14 +540,29 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     float* dxo = p.dx + (bb * p.T + t0) * p.D;
     float* ddo = p.ddelta + (bb * p.T + t0) * p.D;
     float* dzo = GATE ? p.dz + (bb * p.T + t0) * p.D : nullptr;
-    uint16_t* dd16o = p.dd16 ? p.dd16 + (bb * p.T + t0) * p.ld_dd16 : nullptr;
-    uint16_t* dz16o = (GATE && p.dz16) ? p.dz16 + (bb * p.T + t0) * p.ld_dz16 : nullptr;
+    // OUT16: also write the bf16 copies of ddelta and dz
+    uint16_t* dd16o = OUT16 ? p.dd16 + (bb * p.T + t0) * p.ld_dd16 : nullptr;
+    uint16_t* dz16o = OUT16 ? p.dz16 + (bb * p.T + t0) * p.ld_dz16 : nullptr;
     const uint32_t ldd16 = static_cast<uint32_t>(p.ld_dd16), ldz16 = static_cast<uint32_t>(p.ld_dz16);
+    // Lanes whose step or channel is padding store into the sink instead, so
+    // that every store is issued without a branch and the waits for loads issued
+    // before them stay exact (a skipped store would make them wait for all
+    // outstanding stores).
+    float* const sinkf = p.sink + lane;
+    uint16_t* const sink16 = reinterpret_cast<uint16_t*>(p.sink) + lane;
 
     const int64_t ntile = (p.D + 15) / 16;
     const int64_t tile_lo = static_cast<int64_t>(split) * p.tps;
     const int64_t tile_hi = min(ntile, tile_lo + p.tps);
     const int64_t nit = (tile_hi - tile_lo + NW - 1) / NW;  // the same for every wave
+
+    // truncated mode: the chunk's steps shifted by tbar
+    ChunkPtrs<TI> cps;
+    int64_t lims = 0;
+    if constexpr (TRUNC) {
+        cps.set(p, bb * p.T + min(t0 + p.tbar, p.T - 1));
+        lims = p.T - (t0 + p.tbar);
+    }
 
     for (int i = tid; i < L * 32; i += NTH) (&acc[0][0])[i] = 0.f;
     bc.load(p, bb, t0, tid, NTH);
@@ -534,7 +584,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             wsum[fb][wave][o] = (((a0.x + a0.y) + (a0.z + a0.w)) + ((a1.x + a1.y) + (a1.z + a1.w))) +
                                 (((a2.x + a2.y) + (a2.z + a2.w)) + ((a3.x + a3.y) + (a3.z + a3.w)));
         }
-        __syncthreads();
+        lds_barrier();
         if (tid < NP) {
             float s = wsum[fb][0][tid];
 #pragma unroll
@@ -556,53 +606,70 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
         const int64_t cb = ((bb * p.nc + c) * p.N + r * 4) * p.D + d;
         const uint32_t d32 = dv ? static_cast<uint32_t>(d) : 0u;
 
+        // inputs of the last segment, for the reverse sweep
+        RawIn<SPL> nxt;
+        RawIn<SPL> nxs;  // raw inputs at the shifted positions (truncated mode)
+        load_raw2<TI, GATE, SPL>(cp, D32, d32, (NCK - 1) * S, r, lim, dv, true, nxt);
+        if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (NCK - 1) * S, r, lims, dv, true, nxs);
+
         // 1. checkpoint sweep
         float h[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) h[k] = nv[k] ? p.hbuf[cb + k * p.D] : 0.f;
+        for (int k = 0; k < 4; ++k) h[k] = ldm(p.hbuf, cb + k * p.D, nv[k]);
         // segment-start states, in private memory (indexed by the segment)
         float4 ck[NCK];
-        RawIn<SPL> nxt;
-        load_raw2<TI, GATE, SPL>(cp, D32, d32, 0, r, lim, dv, false, nxt);
+        // inputs are loaded one block of CB segments ahead
+        constexpr int CB = NCK < 4 ? NCK : 4;
+        constexpr int BPL = CB * SPL;
+        RawIn<BPL> nxb;
+        load_raw2<TI, GATE, BPL>(cp, D32, d32, 0, r, lim, dv, false, nxb);
 #pragma unroll 1
-        for (int q = 0; q < NCK; ++q) {
-            ck[q] = make_float4(h[0], h[1], h[2], h[3]);
-            const RawIn<SPL> cur = nxt;
-            if (q + 1 < NCK) load_raw2<TI, GATE, SPL>(cp, D32, d32, (q + 1) * S, r, lim, dv, false, nxt);
-            float dls[SPL];
+        for (int qb = 0; qb < NCK; qb += CB) {
+            const RawIn<BPL> cur = nxb;
+            // the next block (the last block reloads itself: every path issues the
+            // same loads, so later waits count exactly)
+            load_raw2<TI, GATE, BPL>(cp, D32, d32, (qb + CB < NCK ? qb + CB : qb) * S, r, lim, dv, false, nxb);
+            float dls[BPL], xs[BPL];
 #pragma unroll
-            for (int jj = 0; jj < SPL; ++jj) {
+            for (int jj = 0; jj < BPL; ++jj) {
                 // padding steps and channels keep Delta = 0, i.e. a = 1
-                const bool v = dv && q * S + r + 4 * jj < lim;
-                dls[jj] = (SP && v) ? softplus_f(cur.p[jj]) : cur.p[jj];
+                const bool v = dv && qb * S + r + 4 * jj < lim;
+                const float pr = fin<TI>(cur.p[jj], v);
+                xs[jj] = fin<TI>(cur.x[jj], v);
+                dls[jj] = (SP && v) ? softplus_f(pr) : pr;
             }
 #pragma unroll
-            for (int j = 0; j < S; ++j) {
-                const float xv = quad_bcast(cur.x[j >> 2], j & 3);
-                const float dl = quad_bcast(dls[j >> 2], j & 3);
-                float Bv[4];
-                bc.getB(q * S + j, r, Bv);
+            for (int qi = 0; qi < CB; ++qi) {
+                const int q = qb + qi;
+                ck[q] = make_float4(h[0], h[1], h[2], h[3]);
+                float Bn[4];
+                bc.getB(q * S, r, Bn);
 #pragma unroll
-                for (int k = 0; k < 4; ++k) h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
+                for (int j = 0; j < S; ++j) {
+                    const float xv = quad_bcast(xs[qi * SPL + (j >> 2)], j & 3);
+                    const float dl = quad_bcast(dls[qi * SPL + (j >> 2)], j & 3);
+                    float Bv[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) Bv[k] = Bn[k];
+                    if (j + 1 < S) bc.getB(q * S + j + 1, r, Bn);
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
+                }
             }
         }
 
         // 2. reverse over segments
         float Mp[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) Mp[k] = nv[k] ? p.mbuf[cb + k * p.D] : 0.f;
+        for (int k = 0; k < 4; ++k) Mp[k] = ldm(p.mbuf, cb + k * p.D, nv[k]);
         float dA[4] = {0.f, 0.f, 0.f, 0.f};
 
         // truncated-mode state: shifted adjoint carry and the window sum
         float Msh[4] = {0.f, 0.f, 0.f, 0.f};
         double W = 0.0;
-        ChunkPtrs<TI> cps;
-        int64_t lims = 0;
         if constexpr (TRUNC) {
             const TI* Cp = static_cast<const TI*>(p.C);
             const int64_t tb = p.tbar;
-            cps.set(p, bb * p.T + min(t0 + tb, p.T - 1));
-            lims = p.T - (t0 + tb);
             const int64_t pstart = t0 + L - 1 + tb;
             const int64_t pb = bb * (p.nc + 1) * p.D + d;
             if (pstart < p.T) {
@@ -610,7 +677,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 const int64_t cpend = (cpk + 1) * L - 1;
                 const int64_t mb = ((bb * p.nc + cpk) * p.N + r * 4) * p.D + d;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) Msh[k] = nv[k] ? p.mbuf[mb + k * p.D] : 0.f;
+                for (int k = 0; k < 4; ++k) Msh[k] = ldm(p.mbuf, mb + k * p.D, nv[k]);
                 double pre = 0.0;
                 for (int64_t ps = cpend; ps > pstart; --ps) {
                     const bool pv = ps < p.T;
@@ -645,43 +712,48 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             }
         }
 
-        RawIn<SPL> nxs;  // raw inputs at the shifted positions (truncated mode)
-        load_raw2<TI, GATE, SPL>(cp, D32, d32, (NCK - 1) * S, r, lim, dv, true, nxt);
-        if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (NCK - 1) * S, r, lims, dv, true, nxs);
         float4 hq = ck[NCK - 1];
 #pragma unroll 1
         for (int q = NCK - 1; q >= 0; --q) {
             h[0] = hq.x; h[1] = hq.y; h[2] = hq.z; h[3] = hq.w;
-            if (q > 0) hq = ck[q - 1];
+            hq = ck[q > 0 ? q - 1 : 0];  // next segment's start state (no branch around the load)
             const RawIn<SPL> cur = nxt;
             RawIn<SPL> cus;
             if constexpr (TRUNC) cus = nxs;
-            if (q > 0) {
-                load_raw2<TI, GATE, SPL>(cp, D32, d32, (q - 1) * S, r, lim, dv, true, nxt);
-                if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (q - 1) * S, r, lims, dv, true, nxs);
+            {
+                // the next segment (segment 0 reloads itself; see the checkpoint sweep)
+                const int qn = q > 0 ? q - 1 : 0;
+                load_raw2<TI, GATE, SPL>(cp, D32, d32, qn * S, r, lim, dv, true, nxt);
+                if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, qn * S, r, lims, dv, true, nxs);
             }
             // per-channel quantities of the steps this lane prepares
-            float dls[SPL], gs[SPL], gfs[SPL], dlps[SPL], gps[SPL];
+            float dls[SPL], xs[SPL], gs[SPL], gfs[SPL], dlps[SPL], gps[SPL];
             bool sv[SPL];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) {
                 sv[jj] = dv && q * S + r + 4 * jj < lim;
-                dls[jj] = (SP && sv[jj]) ? softplus_f(cur.p[jj]) : cur.p[jj];
+                const float pr = fin<TI>(cur.p[jj], sv[jj]), dyr = fin<TI>(cur.dy[jj], sv[jj]);
+                xs[jj] = fin<TI>(cur.x[jj], sv[jj]);
+                dls[jj] = (SP && sv[jj]) ? softplus_f(pr) : pr;
                 if constexpr (GATE) {
-                    const float sg = sigmoid_f(cur.z[jj]);
-                    gs[jj] = cur.dy[jj] * cur.z[jj] * sg;
-                    gfs[jj] = cur.dy[jj] * sg * (1.f + cur.z[jj] * (1.f - sg));
+                    const float zr = fin<TI>(cur.z[jj], sv[jj]);
+                    const float sg = sigmoid_f(zr);
+                    gs[jj] = dyr * zr * sg;
+                    gfs[jj] = dyr * sg * (1.f + zr * (1.f - sg));
                 } else {
-                    gs[jj] = cur.dy[jj];
+                    gs[jj] = dyr;
                     gfs[jj] = 0.f;
                 }
                 if constexpr (TRUNC) {
                     const bool vs = dv && q * S + r + 4 * jj < lims;
-                    dlps[jj] = (SP && vs) ? softplus_f(cus.p[jj]) : cus.p[jj];
-                    if constexpr (GATE)
-                        gps[jj] = cus.dy[jj] * cus.z[jj] * sigmoid_f(cus.z[jj]);
-                    else
-                        gps[jj] = cus.dy[jj];
+                    const float psr = fin<TI>(cus.p[jj], vs), dysr = fin<TI>(cus.dy[jj], vs);
+                    dlps[jj] = (SP && vs) ? softplus_f(psr) : psr;
+                    if constexpr (GATE) {
+                        const float zsr = fin<TI>(cus.z[jj], vs);
+                        gps[jj] = dysr * zsr * sigmoid_f(zsr);
+                    } else {
+                        gps[jj] = dysr;
+                    }
                 }
             }
 
@@ -689,14 +761,22 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             float yk[SPL];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) yk[jj] = 0.f;
+            // B and C are read from LDS one step ahead of their use
+            float Bn[4], Cn[4];
+            bc.get(q * S, r, Bn, Cn);
 #pragma unroll
             for (int j = 0; j < S; ++j) {
                 const int tl = q * S + j;
-                const float xv = quad_bcast(cur.x[j >> 2], j & 3);
+                const float xv = quad_bcast(xs[j >> 2], j & 3);
                 const float dl = quad_bcast(dls[j >> 2], j & 3);
                 const float g = quad_bcast(gs[j >> 2], j & 3);
                 float Bv[4], Cv[4];
-                bc.get(tl, r, Bv, Cv);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    Bv[k] = Bn[k];
+                    Cv[k] = Cn[k];
+                }
+                if (j + 1 < S) bc.get(tl + 1, r, Bn, Cn);
                 float yp = 0.f;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
@@ -718,12 +798,10 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             if constexpr (GATE) {
 #pragma unroll
                 for (int jj = 0; jj < SPL; ++jj) {
-                    if (sv[jj]) {
-                        const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
-                        const float v = gfs[jj] * yk[jj];
-                        dzo[tl * D32 + d32] = v;
-                        if (dz16o) stf(dz16o, tl * ldz16 + d32, v);
-                    }
+                    const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
+                    const float v = gfs[jj] * yk[jj];
+                    *(sv[jj] ? dzo + (tl * D32 + d32) : sinkf) = v;
+                    if constexpr (OUT16) stf(sv[jj] ? dz16o + (tl * ldz16 + d32) : sink16, 0, v);
                 }
             }
             flush(q, 16);
@@ -731,11 +809,17 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             float dxk[SPL], ddk[SPL];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) dxk[jj] = ddk[jj] = 0.f;
+            bc.get(q * S + S - 1, r, Bn, Cn);
 #pragma unroll
             for (int j = S - 1; j >= 0; --j) {
                 const int tl = q * S + j;
                 float Bv[4], Cv[4];
-                bc.get(tl, r, Bv, Cv);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    Bv[k] = Bn[k];
+                    Cv[k] = Cn[k];
+                }
+                if (j > 0) bc.get(tl - 1, r, Bn, Cn);
                 float mu[4], mb[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
@@ -777,23 +861,20 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             }
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) {
-                if (sv[jj]) {
-                    const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
-                    const uint32_t off = tl * D32 + d32;
-                    const float ddv = SP ? ddk[jj] * (1.f - __expf(-dls[jj])) : ddk[jj];  // d softplus / d Delta_pre
-                    dxo[off] = dxk[jj];
-                    ddo[off] = ddv;
-                    if (dd16o) stf(dd16o, tl * ldd16 + d32, ddv);
-                }
+                const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
+                const uint32_t off = tl * D32 + d32;
+                const float ddv = SP ? ddk[jj] * (1.f - __expf(-dls[jj])) : ddk[jj];  // d softplus / d Delta_pre
+                *(sv[jj] ? dxo + off : sinkf) = dxk[jj];
+                *(sv[jj] ? ddo + off : sinkf) = ddv;
+                if constexpr (OUT16) stf(sv[jj] ? dd16o + (tl * ldd16 + d32) : sink16, 0, ddv);
             }
             flush(q, 0);
         }
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-            if (nv[k]) p.hbuf[cb + k * p.D] = dA[k] * wn[k];
+        for (int k = 0; k < 4; ++k) *(nv[k] ? p.hbuf + (cb + k * p.D) : sinkf) = dA[k] * wn[k];
     }
 
-    __syncthreads();
+    lds_barrier();
     const int64_t btn = p.nb * p.T * p.N;
     float* dBo = p.nsplit == 1 ? p.dB : p.pB + static_cast<int64_t>(split) * btn;
     float* dCo = p.nsplit == 1 ? p.dC : p.pC + static_cast<int64_t>(split) * btn;
@@ -875,11 +956,20 @@ void grad_main(const ScanProblem& p, hipStream_t s) {
     dim3 g(static_cast<unsigned>(p.nsplit), static_cast<unsigned>(p.nc),
            static_cast<unsigned>(p.nb));
     SSMK_TIMED("grad_fused", s);
-    hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK>), g, dim3(64 * kGradWaves), 0, s, p);
+    // the bf16 copies exist for the whole-layer path (bf16 inputs, softplus, gate)
+    if constexpr (sizeof(TI) == 2 && SP && GATE) {
+        if (p.dd16) {
+            hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK, true>), g, dim3(64 * kGradWaves), 0, s, p);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK, false>), g, dim3(64 * kGradWaves), 0, s, p);
 }
 
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16>
 hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
+    if ((p.dd16 || p.dz16 || p.bc16) && !(sizeof(TI) == 2 && SP && GATE)) return hipErrorInvalidValue;
+    if (p.dd16 && !(p.dz16 && p.bc16)) return hipErrorInvalidValue;
     dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
