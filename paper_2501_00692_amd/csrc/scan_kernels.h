@@ -52,18 +52,25 @@ __device__ __forceinline__ void stf(uint16_t* p, int64_t i, float v) {
     p[i] = r;
 }
 
-// log(1 + e) for e in [0, 1] from the hardware logarithm; the factor
-// e / ((1 + e) - 1) cancels the rounding of 1 + e (Goldberg's log1p).
+constexpr float kLn2 = 0.6931471805599453f;
+
+// e^x from the hardware base-2 exponential (no denormal results: arguments
+// below about -87 give 0, which none of the uses below can tell apart).
+__device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
+
+// log(1 + e) for e in [0, 1] from the hardware base-2 logarithm (1 + e is in
+// [1, 2], a normal number); the factor e / ((1 + e) - 1) cancels the rounding
+// of 1 + e (Goldberg's log1p).
 __device__ __forceinline__ float log1p_small(float e) {
     const float u = 1.f + e;
     const float d = u - 1.f;
-    return d == 0.f ? e : __logf(u) * (e * __builtin_amdgcn_rcpf(d));
+    return d == 0.f ? e : (__builtin_amdgcn_logf(u) * kLn2) * (e * __builtin_amdgcn_rcpf(d));
 }
 __device__ __forceinline__ float softplus_f(float p) {
-    return fmaxf(p, 0.f) + log1p_small(__expf(-fabsf(p)));
+    return fmaxf(p, 0.f) + log1p_small(fexp(-fabsf(p)));
 }
 __device__ __forceinline__ float sigmoid_f(float z) {
-    return __builtin_amdgcn_rcpf(1.f + __expf(-z));
+    return __builtin_amdgcn_rcpf(1.f + fexp(-z));
 }
 
 // DPP quad permutations: [1,0,3,2] and [2,3,0,1].
@@ -200,7 +207,8 @@ __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64
 //   sdel = sum_{t in c} Delta_t (fp64).
 // B and C are staged in LDS as fp32, 64 steps at a time, for the whole
 // workgroup.  Lane r prepares the per-channel quantities of steps s+r, s+r+4,
-// ... and broadcasts them to its quad; its raw inputs are loaded one group ahead.
+// ... and broadcasts them to its quad; its raw inputs are loaded one 16-step
+// group ahead.
 // ---------------------------------------------------------------------------
 template <typename TI, bool SP, bool GATE, bool WANT_M, bool N16>
 __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
@@ -219,41 +227,62 @@ __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
     double sd = 0.0;
     const int64_t t0 = c * p.L;
     const int64_t t1 = min(t0 + p.L, p.T);
-    RawIn<1> nxt;
-    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, WANT_M, nxt);
+    // raw inputs are loaded one 16-step group ahead (lane r: steps r, r+4, r+8, r+12)
+    constexpr int G = 1;
+    RawIn<G> nxt;
+    load_raw<TI, GATE, G>(p, bb, t0, d, dv, r, WANT_M, nxt);
     for (int64_t sb = t0; sb < t1; sb += SB) {
-        lds_barrier();  // the previous block has been consumed
-        for (int i = tid; i < SB * 32; i += 256) {
-            const int t = i >> 5, cc = i & 31, n = cc & 15;
-            const int64_t tg = sb + t;
-            const bool want = cc < 16 || WANT_M;
-            bcs[t][cc] = ldm(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, want && tg < t1 && n < p.N);
-        }
-        lds_barrier();
-        const int64_t se = min(sb + SB, t1);
-        for (int64_t s0 = sb; s0 < se; s0 += 4) {
-            const RawIn<1> cur = nxt;
-            if (s0 + 4 < t1) load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, WANT_M, nxt);
-            const bool v = dv && s0 + r < t1;
-            const float pr = fin<TI>(cur.p[0], v), xr = fin<TI>(cur.x[0], v);
-            const float dlr = (SP && v) ? softplus_f(pr) : pr;
-            float gr = 0.f;
-            if constexpr (WANT_M) {
-                const float dyr = fin<TI>(cur.dy[0], v);
-                if constexpr (GATE) {
-                    const float zr = fin<TI>(cur.z[0], v);
-                    gr = dyr * zr * sigmoid_f(zr);
-                } else {
-                    gr = dyr;
-                }
+        {
+            // all of this thread's loads are issued before any is used
+            constexpr int PT = SB * 32 / 256;
+            float v[PT];
+#pragma unroll
+            for (int e = 0; e < PT; ++e) {
+                const int i = tid + 256 * e;
+                const int t = i >> 5, cc = i & 31, n = cc & 15;
+                const int64_t tg = sb + t;
+                const bool want = cc < 16 || WANT_M;
+                v[e] = ldm(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, want && tg < t1 && n < p.N);
             }
-            sd += static_cast<double>(dlr);
+            lds_barrier();  // the previous block has been consumed
+#pragma unroll
+            for (int e = 0; e < PT; ++e) {
+                const int i = tid + 256 * e;
+                bcs[i >> 5][i & 31] = v[e];
+            }
+            lds_barrier();
+        }
+        const int64_t se = min(sb + SB, t1);
+        for (int64_t s0 = sb; s0 < se; s0 += 4 * G) {
+            const RawIn<G> cur = nxt;
+            // issued on every path (past the end it reloads valid data that is not
+            // used), so that later waits count exactly
+            load_raw<TI, GATE, G>(p, bb, s0 + 4 * G, d, dv, r, WANT_M, nxt);
+            float xs[G], dls[G], gs[G];
+#pragma unroll
+            for (int jj = 0; jj < G; ++jj) {
+                const bool v = dv && s0 + r + 4 * jj < t1;
+                const float pr = fin<TI>(cur.p[jj], v);
+                xs[jj] = fin<TI>(cur.x[jj], v);
+                dls[jj] = (SP && v) ? softplus_f(pr) : pr;
+                gs[jj] = 0.f;
+                if constexpr (WANT_M) {
+                    const float dyr = fin<TI>(cur.dy[jj], v);
+                    if constexpr (GATE) {
+                        const float zr = fin<TI>(cur.z[jj], v);
+                        gs[jj] = dyr * zr * sigmoid_f(zr);
+                    } else {
+                        gs[jj] = dyr;
+                    }
+                }
+                sd += static_cast<double>(dls[jj]);
+            }
             const int tb = static_cast<int>(s0 - sb);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < 4 * G; ++j) {
                 // steps past the end have zero B, C, Delta and x: a = 1 and no input
-                const float xv = quad_bcast(xr, j);
-                const float dl = quad_bcast(dlr, j);
+                const float xv = quad_bcast(xs[j >> 2], j & 3);
+                const float dl = quad_bcast(dls[j >> 2], j & 3);
                 const float4 b4 = *reinterpret_cast<const float4*>(&bcs[tb + j][4 * r]);
                 const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
                 float Cv[4] = {0.f, 0.f, 0.f, 0.f};
@@ -261,7 +290,7 @@ __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
                     const float4 c4 = *reinterpret_cast<const float4*>(&bcs[tb + j][16 + 4 * r]);
                     Cv[0] = c4.x; Cv[1] = c4.y; Cv[2] = c4.z; Cv[3] = c4.w;
                 }
-                const float g = WANT_M ? quad_bcast(gr, j) : 0.f;
+                const float g = WANT_M ? quad_bcast(gs[j >> 2], j & 3) : 0.f;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const float av = fexp2(cn[k] * dl);
@@ -423,15 +452,25 @@ template <typename TI, int L>
 struct __attribute__((aligned(16))) BCStage {
     float w[L][32];
 
-    __device__ __forceinline__ void load(const ScanProblem& p, int64_t bb, int64_t t0, int tid,
-                                         int nthr) {
+    // NTH threads; each issues all of its loads before it writes any to LDS.
+    template <int NTH>
+    __device__ __forceinline__ void load(const ScanProblem& p, int64_t bb, int64_t t0, int tid) {
+        static_assert((L * 32) % NTH == 0, "whole rows per pass");
+        constexpr int PT = L * 32 / NTH;
         const TI* Bp = static_cast<const TI*>(p.B);
         const TI* Cp = static_cast<const TI*>(p.C);
-        for (int i = tid; i < L * 32; i += nthr) {
+        float v[PT];
+#pragma unroll
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + NTH * e;
             const int t = i >> 5, c = i & 31, n = c & 15;
             const int64_t tg = t0 + t;
-            const TI* src = c < 16 ? Bp : Cp;
-            w[t][c] = ldm(src, (bb * p.T + tg) * p.N + n, tg < p.T && n < p.N);
+            v[e] = ldm(c < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, tg < p.T && n < p.N);
+        }
+#pragma unroll
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + NTH * e;
+            w[i >> 5][i & 31] = v[e];
         }
     }
     // States 4r..4r+3 of B and C at in-chunk step t.
@@ -565,7 +604,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     }
 
     for (int i = tid; i < L * 32; i += NTH) (&acc[0][0])[i] = 0.f;
-    bc.load(p, bb, t0, tid, NTH);
+    bc.template load<NTH>(p, bb, t0, tid);
     __syncthreads();
 
     int fb = 0;
@@ -863,7 +902,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             for (int jj = 0; jj < SPL; ++jj) {
                 const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
                 const uint32_t off = tl * D32 + d32;
-                const float ddv = SP ? ddk[jj] * (1.f - __expf(-dls[jj])) : ddk[jj];  // d softplus / d Delta_pre
+                const float ddv = SP ? ddk[jj] * (1.f - fexp(-dls[jj])) : ddk[jj];  // d softplus / d Delta_pre
                 *(sv[jj] ? dxo + off : sinkf) = dxk[jj];
                 *(sv[jj] ? ddo + off : sinkf) = ddv;
                 if constexpr (OUT16) stf(sv[jj] ? dd16o + (tl * ldd16 + d32) : sink16, 0, ddv);
