@@ -73,6 +73,10 @@ struct ScanProblem {
     int64_t ld_bc16;
     // workspace regions
     float* hbuf;    // [b][nc][N][D]
+    float* hseg;    // [b][nc][L/seg][Dp][16]: state at each segment start from a zero chunk carry-in
+    float* cseg;    // [b][nc][L/seg][Dp]: sum of Delta from the chunk start to each segment start
+    int64_t Dp;     // channels rounded up to a multiple of 64
+    int seg;        // segment length of the fused gradient kernel
     float* mbuf;    // [b][nc][N][D]
     double* sdel;   // [b][nc][D]
     double* psum;   // [b][nc+1][D]
@@ -84,10 +88,14 @@ struct ScanProblem {
 
 // Workspace layout shared by the size query and the launch.
 struct ScanWorkspace {
-    size_t off_hbuf, off_mbuf, off_sdel, off_psum, off_pB, off_pC, off_dAtmp, off_sink, total;
+    size_t off_hbuf, off_mbuf, off_hseg, off_cseg, off_sdel, off_psum, off_pB, off_pC, off_dAtmp, off_sink,
+        total;
 };
 
 int64_t default_chunk();
+// Segment length of the fused gradient kernel for chunk length L.
+inline int grad_segment(int64_t L) { return L >= 256 ? 16 : 8; }
+inline int64_t padded_channels(int64_t D) { return (D + 63) / 64 * 64; }
 bool chunk_supported(int64_t L);
 void choose_split(int64_t nb, int64_t D, int64_t nc, int* nsplit, int* tiles_per_split);
 int choose_nslice(int64_t nb, int64_t nc);

@@ -60,6 +60,13 @@ ScanWorkspace scan_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_
     off = align_up(off + carry);
     w.off_mbuf = off;
     if (grad) off = align_up(off + carry);
+    // segment-start states of every chunk (gradient only)
+    const int64_t nseg = grad ? L / grad_segment(L) : 0;
+    const int64_t Dp = padded_channels(D);
+    w.off_hseg = off;
+    off = align_up(off + static_cast<size_t>(nb * nc * nseg * Dp * 16) * sizeof(float));
+    w.off_cseg = off;
+    off = align_up(off + static_cast<size_t>(nb * nc * nseg * Dp) * sizeof(float));
     w.off_sdel = off;
     off = align_up(off + static_cast<size_t>(nb * nc * D) * sizeof(double));
     w.off_psum = off;
@@ -87,7 +94,11 @@ ScanWorkspace scan_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_
 void bind_workspace(ScanProblem& p, void* ws, const ScanWorkspace& w) {
     char* b = static_cast<char*>(ws);
     p.hbuf = reinterpret_cast<float*>(b + w.off_hbuf);
-    p.mbuf = w.off_mbuf != w.off_sdel ? reinterpret_cast<float*>(b + w.off_mbuf) : nullptr;
+    p.mbuf = w.off_mbuf != w.off_hseg ? reinterpret_cast<float*>(b + w.off_mbuf) : nullptr;
+    p.hseg = w.off_hseg != w.off_cseg ? reinterpret_cast<float*>(b + w.off_hseg) : nullptr;
+    p.cseg = w.off_cseg != w.off_sdel ? reinterpret_cast<float*>(b + w.off_cseg) : nullptr;
+    p.Dp = padded_channels(p.D);
+    p.seg = grad_segment(p.L);
     p.sdel = reinterpret_cast<double*>(b + w.off_sdel);
     p.psum = w.off_psum != w.off_pB ? reinterpret_cast<double*>(b + w.off_psum) : nullptr;
     p.pB = w.off_pB != w.off_pC ? reinterpret_cast<float*>(b + w.off_pB) : nullptr;

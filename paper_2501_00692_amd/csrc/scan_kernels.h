@@ -157,6 +157,15 @@ __device__ __forceinline__ float quad_bcast(float v, int src) {
     }
 }
 
+// Value of lane `src` of each quad, for a double.
+__device__ __forceinline__ double quad_bcast_d(double v, int src) {
+    const uint64_t u = __double_as_longlong(v);
+    const float lo = quad_bcast(__uint_as_float(static_cast<uint32_t>(u)), src);
+    const float hi = quad_bcast(__uint_as_float(static_cast<uint32_t>(u >> 32)), src);
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(__float_as_uint(hi)) << 32) |
+                                                       __float_as_uint(lo)));
+}
+
 // Raw per-(step, channel) inputs of the steps a lane prepares for its quad, as
 // element bits: they are loaded a group or segment ahead and converted at their
 // first use, so that nothing waits for the loads before then.
@@ -204,19 +213,24 @@ __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64
 //   hloc = state at e from a zero carry-in,
 //   mloc = sum_{t in c} g_t C_t prod_{j=s}^{t} a_j  (the adjoint that the chunk
 //          hands to h_{s-1} from a zero carry at its end),
-//   sdel = sum_{t in c} Delta_t (fp64).
+//   sdel = sum_{t in c} Delta_t (fp64);
+// with WANT_M (the gradient) also, for each segment of p.seg steps of the
+// chunk, the state at the segment start from a zero carry-in (hseg) and the sum
+// of Delta from the chunk start to the segment start (cseg): the fused gradient
+// kernel rebuilds its segment-start states from them and the chunk carry.
 // B and C are staged in LDS as fp32, 64 steps at a time, for the whole
 // workgroup.  Lane r prepares the per-channel quantities of steps s+r, s+r+4,
 // ... and broadcasts them to its quad; its raw inputs are loaded one 16-step
 // group ahead.
 // ---------------------------------------------------------------------------
-template <typename TI, bool SP, bool GATE, bool WANT_M, bool N16>
-__global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
+template <typename TI, bool SP, bool GATE, bool WANT_M, int SEG>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) void k_chunk_aggr(const ScanProblem p) {
     constexpr int SB = 64;  // steps per staged block
+    static_assert(SB % SEG == 0 && SEG % 4 == 0, "segments tile the staged blocks");
     __shared__ __attribute__((aligned(16))) float bcs[SB][32];
     const int tid = threadIdx.x;
     const int r = tid & 3;
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);  // < Dp
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const bool dv = d < p.D;
     const TI* Bp = static_cast<const TI*>(p.B);
@@ -227,10 +241,19 @@ __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
     double sd = 0.0;
     const int64_t t0 = c * p.L;
     const int64_t t1 = min(t0 + p.L, p.T);
-    // raw inputs are loaded one 16-step group ahead (lane r: steps r, r+4, r+8, r+12)
-    constexpr int G = 1;
-    RawIn<G> nxt;
-    load_raw<TI, GATE, G>(p, bb, t0, d, dv, r, WANT_M, nxt);
+    // segment records (WANT_M): slot q holds the record of segment q
+    const uint32_t nseg = WANT_M ? static_cast<uint32_t>(p.L / SEG) : 0u;
+    const int64_t sgb = (bb * p.nc + c) * nseg * p.Dp + d;
+    auto put_seg = [&](uint32_t q, float cum) {
+        *reinterpret_cast<float4*>(p.hseg + (sgb + q * p.Dp) * 16 + 4 * r) = make_float4(h[0], h[1], h[2], h[3]);
+        p.cseg[sgb + q * p.Dp] = cum;
+    };
+    // the quad's Delta sum so far, added in lane order
+    auto quad_total = [&]() {
+        return ((quad_bcast_d(sd, 0) + quad_bcast_d(sd, 1)) + quad_bcast_d(sd, 2)) + quad_bcast_d(sd, 3);
+    };
+    RawIn<1> nxt;  // raw inputs, loaded one group of 4 steps ahead
+    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, WANT_M, nxt);
     for (int64_t sb = t0; sb < t1; sb += SB) {
         {
             // all of this thread's loads are issued before any is used
@@ -253,55 +276,60 @@ __global__ __launch_bounds__(256) void k_chunk_aggr(const ScanProblem p) {
             lds_barrier();
         }
         const int64_t se = min(sb + SB, t1);
-        for (int64_t s0 = sb; s0 < se; s0 += 4 * G) {
-            const RawIn<G> cur = nxt;
-            // issued on every path (past the end it reloads valid data that is not
-            // used), so that later waits count exactly
-            load_raw<TI, GATE, G>(p, bb, s0 + 4 * G, d, dv, r, WANT_M, nxt);
-            float xs[G], dls[G], gs[G];
-#pragma unroll
-            for (int jj = 0; jj < G; ++jj) {
-                const bool v = dv && s0 + r + 4 * jj < t1;
-                const float pr = fin<TI>(cur.p[jj], v);
-                xs[jj] = fin<TI>(cur.x[jj], v);
-                dls[jj] = (SP && v) ? softplus_f(pr) : pr;
-                gs[jj] = 0.f;
+        for (int64_t s0 = sb; s0 < se; s0 += 4) {
+            if constexpr (WANT_M) {
+                const uint32_t tl = static_cast<uint32_t>(s0 - t0);
+                if (tl % SEG == 0) put_seg(tl / SEG, static_cast<float>(quad_total()));  // uniform
+            }
+            {
+                const RawIn<1> cur = nxt;
+                // issued on every path (past the end it reloads valid data that is
+                // not used), so that later waits count exactly
+                load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, WANT_M, nxt);
+                const bool v = dv && s0 + r < t1;
+                const float pr = fin<TI>(cur.p[0], v), xr = fin<TI>(cur.x[0], v);
+                const float dlr = (SP && v) ? softplus_f(pr) : pr;
+                float gr = 0.f;
                 if constexpr (WANT_M) {
-                    const float dyr = fin<TI>(cur.dy[jj], v);
+                    const float dyr = fin<TI>(cur.dy[0], v);
                     if constexpr (GATE) {
-                        const float zr = fin<TI>(cur.z[jj], v);
-                        gs[jj] = dyr * zr * sigmoid_f(zr);
+                        const float zr = fin<TI>(cur.z[0], v);
+                        gr = dyr * zr * sigmoid_f(zr);
                     } else {
-                        gs[jj] = dyr;
+                        gr = dyr;
                     }
                 }
-                sd += static_cast<double>(dls[jj]);
-            }
-            const int tb = static_cast<int>(s0 - sb);
+                sd += static_cast<double>(dlr);
+                const int tb = static_cast<int>(s0 - sb);
 #pragma unroll
-            for (int j = 0; j < 4 * G; ++j) {
-                // steps past the end have zero B, C, Delta and x: a = 1 and no input
-                const float xv = quad_bcast(xs[j >> 2], j & 3);
-                const float dl = quad_bcast(dls[j >> 2], j & 3);
-                const float4 b4 = *reinterpret_cast<const float4*>(&bcs[tb + j][4 * r]);
-                const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
-                float Cv[4] = {0.f, 0.f, 0.f, 0.f};
-                if constexpr (WANT_M) {
-                    const float4 c4 = *reinterpret_cast<const float4*>(&bcs[tb + j][16 + 4 * r]);
-                    Cv[0] = c4.x; Cv[1] = c4.y; Cv[2] = c4.z; Cv[3] = c4.w;
-                }
-                const float g = WANT_M ? quad_bcast(gs[j >> 2], j & 3) : 0.f;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const float av = fexp2(cn[k] * dl);
-                    h[k] = fmaf(av, h[k], Bv[k] * xv);
+                for (int j = 0; j < 4; ++j) {
+                    const float xv = quad_bcast(xr, j);
+                    const float dl = quad_bcast(dlr, j);
+                    const float4 b4 = *reinterpret_cast<const float4*>(&bcs[tb + j][4 * r]);
+                    const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
+                    float Cv[4] = {0.f, 0.f, 0.f, 0.f};
                     if constexpr (WANT_M) {
-                        P[k] *= av;
-                        m[k] = fmaf(g * Cv[k], P[k], m[k]);
+                        const float4 c4 = *reinterpret_cast<const float4*>(&bcs[tb + j][16 + 4 * r]);
+                        Cv[0] = c4.x; Cv[1] = c4.y; Cv[2] = c4.z; Cv[3] = c4.w;
+                    }
+                    const float g = WANT_M ? quad_bcast(gr, j) : 0.f;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const float av = fexp2(cn[k] * dl);
+                        h[k] = fmaf(av, h[k], Bv[k] * xv);
+                        if constexpr (WANT_M) {
+                            P[k] *= av;
+                            m[k] = fmaf(g * Cv[k], P[k], m[k]);
+                        }
                     }
                 }
             }
         }
+    }
+    if constexpr (WANT_M) {
+        // segments that start at or after the end of the sequence hold the final state
+        const float cum = static_cast<float>(quad_total());
+        for (uint32_t q = static_cast<uint32_t>((t1 - t0 + SEG - 1) / SEG); q < nseg; ++q) put_seg(q, cum);
     }
     // sum of Delta over the quad's prepared steps, in a fixed order
     const double s1 = __shfl_xor(sd, 1);
@@ -533,8 +561,9 @@ __device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMI
 // wave w takes tiles tile_lo + w, tile_lo + w + kGradWaves, ..., so the waves
 // read adjacent channels together.  Lanes of a quad share a channel and hold 4
 // of its states.  B and C of the chunk are staged in LDS once.  Per tile:
-//   1. checkpoint sweep: from the carry-in state H_c, the state at the start of
-//      each S-step segment;
+//   1. the state at the start of each S-step segment is the chunk-local one
+//      from the chunk-aggregate pass (hseg) plus the carry-in H_c decayed over
+//      the steps before the segment (2^{cn cseg});
 //   2. segments in reverse order: recompute the segment's states forward
 //      (keeping a_t and a_t h_{t-1}), form dz, sum g_t h_t over the channels
 //      (dC); then run the adjoint backwards, mu_t = g_t C_t + a_{t+1} mu_{t+1},
@@ -651,51 +680,15 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
         load_raw2<TI, GATE, SPL>(cp, D32, d32, (NCK - 1) * S, r, lim, dv, true, nxt);
         if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (NCK - 1) * S, r, lims, dv, true, nxs);
 
-        // 1. checkpoint sweep
+        // segment-start states: hseg[q] + (prod of a from the chunk start) H_c, the
+        // product being 2^{cn cseg[q]}; loaded one segment ahead
+        float Hc[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) Hc[k] = ldm(p.hbuf, cb + k * p.D, nv[k]);
+        const int64_t sgb = (bb * p.nc + c) * NCK * p.Dp + (dv ? d : 0);
+        float4 hq = *reinterpret_cast<const float4*>(p.hseg + (sgb + (NCK - 1) * p.Dp) * 16 + 4 * r);
+        float cq = p.cseg[sgb + (NCK - 1) * p.Dp];
         float h[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) h[k] = ldm(p.hbuf, cb + k * p.D, nv[k]);
-        // segment-start states, in private memory (indexed by the segment)
-        float4 ck[NCK];
-        // inputs are loaded one block of CB segments ahead
-        constexpr int CB = NCK < 4 ? NCK : 4;
-        constexpr int BPL = CB * SPL;
-        RawIn<BPL> nxb;
-        load_raw2<TI, GATE, BPL>(cp, D32, d32, 0, r, lim, dv, false, nxb);
-#pragma unroll 1
-        for (int qb = 0; qb < NCK; qb += CB) {
-            const RawIn<BPL> cur = nxb;
-            // the next block (the last block reloads itself: every path issues the
-            // same loads, so later waits count exactly)
-            load_raw2<TI, GATE, BPL>(cp, D32, d32, (qb + CB < NCK ? qb + CB : qb) * S, r, lim, dv, false, nxb);
-            float dls[BPL], xs[BPL];
-#pragma unroll
-            for (int jj = 0; jj < BPL; ++jj) {
-                // padding steps and channels keep Delta = 0, i.e. a = 1
-                const bool v = dv && qb * S + r + 4 * jj < lim;
-                const float pr = fin<TI>(cur.p[jj], v);
-                xs[jj] = fin<TI>(cur.x[jj], v);
-                dls[jj] = (SP && v) ? softplus_f(pr) : pr;
-            }
-#pragma unroll
-            for (int qi = 0; qi < CB; ++qi) {
-                const int q = qb + qi;
-                ck[q] = make_float4(h[0], h[1], h[2], h[3]);
-                float Bn[4];
-                bc.getB(q * S, r, Bn);
-#pragma unroll
-                for (int j = 0; j < S; ++j) {
-                    const float xv = quad_bcast(xs[qi * SPL + (j >> 2)], j & 3);
-                    const float dl = quad_bcast(dls[qi * SPL + (j >> 2)], j & 3);
-                    float Bv[4];
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) Bv[k] = Bn[k];
-                    if (j + 1 < S) bc.getB(q * S + j + 1, r, Bn);
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
-                }
-            }
-        }
 
         // 2. reverse over segments
         float Mp[4];
@@ -751,11 +744,17 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             }
         }
 
-        float4 hq = ck[NCK - 1];
 #pragma unroll 1
         for (int q = NCK - 1; q >= 0; --q) {
-            h[0] = hq.x; h[1] = hq.y; h[2] = hq.z; h[3] = hq.w;
-            hq = ck[q > 0 ? q - 1 : 0];  // next segment's start state (no branch around the load)
+            {
+                const float hl[4] = {hq.x, hq.y, hq.z, hq.w};
+#pragma unroll
+                for (int k = 0; k < 4; ++k) h[k] = fmaf(fexp2(cn[k] * cq), Hc[k], hl[k]);
+                // the next segment's record (segment 0 reloads its own: no branch around the loads)
+                const int64_t qn = q > 0 ? q - 1 : 0;
+                hq = *reinterpret_cast<const float4*>(p.hseg + (sgb + qn * p.Dp) * 16 + 4 * r);
+                cq = p.cseg[sgb + qn * p.Dp];
+            }
             const RawIn<SPL> cur = nxt;
             RawIn<SPL> cus;
             if constexpr (TRUNC) cus = nxs;
@@ -979,7 +978,7 @@ hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
     dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
-        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, N16>), g4, dim3(256), 0, s, p);
+        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, 8>), g4, dim3(256), 0, s, p);
     }
     SSMK_TIMED("carry", s);
     hipLaunchKernelGGL(k_carry, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N),
@@ -1012,7 +1011,10 @@ hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
     dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
-        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16>), g4, dim3(256), 0, s, p);
+        if (p.seg == 16)
+            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, 16>), g4, dim3(256), 0, s, p);
+        else
+            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, 8>), g4, dim3(256), 0, s, p);
     }
     {
         SSMK_TIMED("carry", s);
