@@ -39,7 +39,9 @@ Readings of the paper used here (where it is silent or garbled):
   only the parameters);
 * dh0 exists for the full gradient only;
 * the discretisation is a = exp(-Delta e^{A_log}) and h = a h + B x, with no
-  Delta factor on B.
+  Delta factor on B; two variants are selectable: ``a_scalar`` (the "scalar
+  SSM" row of Table 1: one decay per channel, ``A_log`` of shape [D]) and
+  ``b_delta`` (the input term scaled by the step size, ``h = a h + Delta B x``).
 """
 from __future__ import annotations
 
@@ -102,32 +104,45 @@ def _ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
-def forward(x, delta, A_log, B, C, h0=None, z=None, delta_softplus=False, nthreads=0):
+# variant bits of the C oracle's `flags` argument
+_SOFTPLUS, _A_SCALAR, _B_DELTA = 1, 2, 4
+
+
+def _flags(delta_softplus, a_scalar, b_delta):
+    return (_SOFTPLUS if delta_softplus else 0) | (_A_SCALAR if a_scalar else 0) | (_B_DELTA if b_delta else 0)
+
+
+def forward(x, delta, A_log, B, C, h0=None, z=None, delta_softplus=False, nthreads=0, a_scalar=False,
+            b_delta=False):
     """Sec. 3.1 forward.  Returns ``(out, h_last)``; ``out = y`` or ``y*silu(z)``."""
     x, delta, A_log, B, C, h0, z = map(_f64, (x, delta, A_log, B, C, h0, z))
     nb, T, D = x.shape
-    N = A_log.shape[1]
+    N = B.shape[-1]
+    assert A_log.shape == ((D,) if a_scalar else (D, N))
     out = np.empty((nb, T, D))
     h_last = np.empty((nb, D, N))
-    rc = _load().oracle_forward(nb, T, D, N, _ptr(x), _ptr(delta), int(delta_softplus), _ptr(A_log),
+    rc = _load().oracle_forward(nb, T, D, N, _ptr(x), _ptr(delta), _flags(delta_softplus, a_scalar, b_delta), _ptr(A_log),
                                 _ptr(B), _ptr(C), _ptr(h0), _ptr(z), _ptr(out), _ptr(h_last), nthreads)
     if rc:
         raise ValueError(f"oracle_forward failed ({rc})")
     return out, h_last
 
 
-def _grad(fn, with_tbar, tbar, x, delta, A_log, B, C, dy, h0, z, delta_softplus, want_dh0, nthreads):
+def _grad(fn, with_tbar, tbar, x, delta, A_log, B, C, dy, h0, z, delta_softplus, want_dh0, nthreads,
+          a_scalar=False, b_delta=False):
     x, delta, A_log, B, C, h0, z, dy = map(_f64, (x, delta, A_log, B, C, h0, z, dy))
     nb, T, D = x.shape
-    N = A_log.shape[1]
+    N = B.shape[-1]
+    assert A_log.shape == ((D,) if a_scalar else (D, N))
     out = {
-        "dx": np.empty((nb, T, D)), "ddelta": np.empty((nb, T, D)), "dA_log": np.empty((D, N)),
+        "dx": np.empty((nb, T, D)), "ddelta": np.empty((nb, T, D)), "dA_log": np.empty(A_log.shape),
         "dB": np.empty((nb, T, N)), "dC": np.empty((nb, T, N)),
     }
     out["dz"] = np.empty((nb, T, D)) if z is not None else None
     out["dh0"] = np.empty((nb, D, N)) if want_dh0 else None
     head = (nb, T, D, N, int(tbar)) if with_tbar else (nb, T, D, N)
-    rc = fn(*head, _ptr(x), _ptr(delta), int(delta_softplus), _ptr(A_log), _ptr(B), _ptr(C), _ptr(h0),
+    rc = fn(*head, _ptr(x), _ptr(delta), _flags(delta_softplus, a_scalar, b_delta), _ptr(A_log), _ptr(B),
+            _ptr(C), _ptr(h0),
             _ptr(z), _ptr(dy), _ptr(out["dx"]), _ptr(out["ddelta"]), _ptr(out["dA_log"]), _ptr(out["dB"]),
             _ptr(out["dC"]), _ptr(out["dz"]), _ptr(out["dh0"]), nthreads)
     if rc:
@@ -135,32 +150,33 @@ def _grad(fn, with_tbar, tbar, x, delta, A_log, B, C, dy, h0, z, delta_softplus,
     return out
 
 
-def bptt(x, delta, A_log, B, C, dy, h0=None, z=None, delta_softplus=False, want_dh0=True, nthreads=0):
+def bptt(x, delta, A_log, B, C, dy, h0=None, z=None, delta_softplus=False, want_dh0=True, nthreads=0,
+         a_scalar=False, b_delta=False):
     """Exact full gradient by backpropagation through time (dict of arrays)."""
     return _grad(_load().oracle_bptt, False, 0, x, delta, A_log, B, C, dy, h0, z, delta_softplus,
-                 want_dh0, nthreads)
+                 want_dh0, nthreads, a_scalar, b_delta)
 
 
 def adjoint_sum(x, delta, A_log, B, C, dy, tbar=0, h0=None, z=None, delta_softplus=False,
-                want_dh0=None, nthreads=0):
+                want_dh0=None, nthreads=0, a_scalar=False, b_delta=False):
     """Prop. 2 (``tbar<=0`` or ``tbar>=T``) / Eq. "capped" double sum, literally."""
     T = np.shape(x)[1]
     full = tbar <= 0 or tbar >= T
     if want_dh0 is None:
         want_dh0 = full
     return _grad(_load().oracle_adjoint_sum, True, tbar, x, delta, A_log, B, C, dy, h0, z,
-                 delta_softplus, want_dh0, nthreads)
+                 delta_softplus, want_dh0, nthreads, a_scalar, b_delta)
 
 
 def trunc_tail(x, delta, A_log, B, C, dy, tbar=0, h0=None, z=None, delta_softplus=False,
-               want_dh0=None, nthreads=0):
+               want_dh0=None, nthreads=0, a_scalar=False, b_delta=False):
     """Truncated estimator via the tail identity (O(T) per channel)."""
     T = np.shape(x)[1]
     full = tbar <= 0 or tbar >= T
     if want_dh0 is None:
         want_dh0 = full
     return _grad(_load().oracle_trunc_tail, True, tbar, x, delta, A_log, B, C, dy, h0, z,
-                 delta_softplus, want_dh0, nthreads)
+                 delta_softplus, want_dh0, nthreads, a_scalar, b_delta)
 
 
 def silu(z):

@@ -17,9 +17,17 @@
  * out_t = y_t * silu(z_t).  The loss is L = sum_{b,t,d} dy_t[d] * out_t[d],
  * so dy is the upstream gradient dL/dout.
  *
+ * The `flags` argument selects (bits):
+ *   OR_SOFTPLUS  the delta input is Delta_pre and Delta = softplus(Delta_pre);
+ *   OR_A_SCALAR  the "scalar SSM" row of Table 1: one decay per channel,
+ *                A^t = a_t[d] I with a_t[d] = exp(-Delta_t[d] exp(A_log[d]));
+ *                A_log and dA_log are [D];
+ *   OR_B_DELTA   the input term scaled by the step size, B^t x^t -> Delta_t B_t x_t
+ *                (the step-size-scaled input of selective SSM discretisations).
+ *
  * Layouts (row-major, fp64): x, delta, z, dy, out, dx, ddelta, dz : [b][T][D];
- * B, C, dB, dC : [b][T][N]; A_log, dA_log : [D][N]; h0, h_last, dh0 : [b][D][N].
- * All gradient outputs are overwritten.
+ * B, C, dB, dC : [b][T][N]; A_log, dA_log : [D][N] (or [D]); h0, h_last, dh0 :
+ * [b][D][N].  All gradient outputs are overwritten.
  *
  * Functions and the passages they follow:
  *   oracle_forward      Sec. 3.1 five steps (sequential loop over t).
@@ -53,6 +61,13 @@
  * of threads. */
 #define ORACLE_NBLK 16
 
+enum { OR_SOFTPLUS = 1, OR_A_SCALAR = 2, OR_B_DELTA = 4 };
+
+/* log of the decay rate of (channel d, state n). */
+static double alog_at(const double* A_log, int flags, int64_t d, int64_t N, int64_t n) {
+    return (flags & OR_A_SCALAR) ? A_log[d] : A_log[d * N + n];
+}
+
 static double softplus(double p) { return p > 0.0 ? p + log1p(exp(-p)) : log1p(exp(p)); }
 static double sigmoid(double p) {
     if (p >= 0.0) return 1.0 / (1.0 + exp(-p));
@@ -80,7 +95,7 @@ int oracle_max_threads(void) {
 /* Forward: Sec. 3.1 steps 1-5, one channel at a time, sequential in t.      */
 /* ------------------------------------------------------------------------ */
 int oracle_forward(int64_t nb, int64_t T, int64_t D, int64_t N,
-                   const double* x, const double* delta, int delta_softplus,
+                   const double* x, const double* delta, int flags,
                    const double* A_log, const double* B, const double* C,
                    const double* h0, const double* z,
                    double* out, double* h_last, int nthreads) {
@@ -93,11 +108,12 @@ int oracle_forward(int64_t nb, int64_t T, int64_t D, int64_t N,
             for (int64_t n = 0; n < N; ++n) h[n] = h0 ? h0[(bb * D + d) * N + n] : 0.0;
             for (int64_t t = 0; t < T; ++t) {
                 int64_t td = (bb * T + t) * D + d;
-                double dl = delta_softplus ? softplus(delta[td]) : delta[td];
+                double dl = (flags & OR_SOFTPLUS) ? softplus(delta[td]) : delta[td];
+                double u = (flags & OR_B_DELTA) ? dl * x[td] : x[td];
                 double y = 0.0;
                 for (int64_t n = 0; n < N; ++n) {
-                    double a = exp(-dl * exp(A_log[d * N + n]));
-                    h[n] = a * h[n] + B[(bb * T + t) * N + n] * x[td];
+                    double a = exp(-dl * exp(alog_at(A_log, flags, d, N, n)));
+                    h[n] = a * h[n] + B[(bb * T + t) * N + n] * u;
                     y += C[(bb * T + t) * N + n] * h[n];
                 }
                 out[td] = z ? y * z[td] * sigmoid(z[td]) : y;
@@ -121,19 +137,20 @@ typedef struct {
 } chan_fwd;
 
 static void chan_forward(int64_t bb, int64_t d, int64_t T, int64_t D, int64_t N,
-                         const double* x, const double* delta, int delta_softplus,
+                         const double* x, const double* delta, int flags,
                          const double* A_log, const double* B, const double* C,
                          const double* h0, const double* z, const double* dy,
                          chan_fwd* f, double* dz) {
     for (int64_t n = 0; n < N; ++n) f->hs[n] = h0 ? h0[(bb * D + d) * N + n] : 0.0;
     for (int64_t t = 0; t < T; ++t) {
         int64_t td = (bb * T + t) * D + d;
-        f->dl[t] = delta_softplus ? softplus(delta[td]) : delta[td];
+        f->dl[t] = (flags & OR_SOFTPLUS) ? softplus(delta[td]) : delta[td];
+        double u = (flags & OR_B_DELTA) ? f->dl[t] * x[td] : x[td];
         double y = 0.0;
         for (int64_t n = 0; n < N; ++n) {
-            double a = exp(-f->dl[t] * exp(A_log[d * N + n]));
+            double a = exp(-f->dl[t] * exp(alog_at(A_log, flags, d, N, n)));
             f->a[t * N + n] = a;
-            f->hs[(t + 1) * N + n] = a * f->hs[t * N + n] + B[(bb * T + t) * N + n] * x[td];
+            f->hs[(t + 1) * N + n] = a * f->hs[t * N + n] + B[(bb * T + t) * N + n] * u;
             y += C[(bb * T + t) * N + n] * f->hs[(t + 1) * N + n];
         }
         if (z) {
@@ -146,27 +163,29 @@ static void chan_forward(int64_t bb, int64_t d, int64_t T, int64_t D, int64_t N,
     }
 }
 
-/* VJP of step i with respect to (a_i, b_i = B_i x_i), given the state
+/* VJP of step i with respect to (a_i, b_i = B_i u_i), given the state
  * cotangent w[n] = dL/dh_i (or the part of it that is being accumulated):
  *   vjp_A: dL/da_i = w * h_{i-1}, chained through a = exp(-Delta e^{A_log});
- *   vjp_B: dL/db_i = w, chained through b = B_i x_i.  */
-static void step_vjp(int64_t bb, int64_t i, int64_t d, int64_t T, int64_t D, int64_t N,
+ *   vjp_B: dL/db_i = w, chained through b = B_i u_i with u_i = x_i (or
+ *          Delta_i x_i with OR_B_DELTA, which also reaches Delta).  */
+static void step_vjp(int64_t bb, int64_t i, int64_t d, int64_t T, int64_t D, int64_t N, int flags,
                      const double* w, const chan_fwd* f, const double* x,
                      const double* A_log, const double* B,
                      double* dx, double* ddelta_raw, double* dA_log_row, double* dB_acc) {
     int64_t td = (bb * T + i) * D + d;
+    double sc = (flags & OR_B_DELTA) ? f->dl[i] : 1.0;  /* d u / d x */
     double sdx = 0.0, sdd = 0.0;
     for (int64_t n = 0; n < N; ++n) {
-        double ea = exp(A_log[d * N + n]);
+        double ea = exp(alog_at(A_log, flags, d, N, n));
         double da = w[n] * f->hs[i * N + n];            /* h_{i-1} is hs[i] */
         double ai = f->a[i * N + n];
         sdd += da * ai * (-ea);                           /* d a / d Delta */
-        dA_log_row[n] += da * ai * (-f->dl[i] * ea);     /* d a / d A_log */
+        dA_log_row[(flags & OR_A_SCALAR) ? 0 : n] += da * ai * (-f->dl[i] * ea); /* d a / d A_log */
         sdx += w[n] * B[(bb * T + i) * N + n];
-        dB_acc[(bb * T + i) * N + n] += w[n] * x[td];
+        dB_acc[(bb * T + i) * N + n] += w[n] * x[td] * sc;
     }
-    dx[td] += sdx;
-    ddelta_raw[td] += sdd;
+    dx[td] += sdx * sc;
+    ddelta_raw[td] += sdd + ((flags & OR_B_DELTA) ? sdx * x[td] : 0.0);  /* d u / d Delta = x */
 }
 
 static int grad_common_checks(int64_t nb, int64_t T, int64_t D, int64_t N) {
@@ -176,8 +195,8 @@ static int grad_common_checks(int64_t nb, int64_t T, int64_t D, int64_t N) {
 /* Apply dDelta_pre = dDelta * sigmoid(Delta_pre) when the step size is a
  * softplus of the stored input. */
 static void finish_softplus(int64_t nb, int64_t T, int64_t D, const double* delta,
-                            int delta_softplus, double* ddelta) {
-    if (!delta_softplus) return;
+                            int flags, double* ddelta) {
+    if (!(flags & OR_SOFTPLUS)) return;
     for (int64_t k = 0; k < nb * T * D; ++k) ddelta[k] *= sigmoid(delta[k]);
 }
 
@@ -194,7 +213,7 @@ static void reduce_blocks(double* out, double* const* blk, int64_t len) {
 enum { MODE_BPTT = 0, MODE_DOUBLESUM = 1, MODE_TAIL = 2 };
 
 static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, int64_t tbar,
-                       const double* x, const double* delta, int delta_softplus,
+                       const double* x, const double* delta, int flags,
                        const double* A_log, const double* B, const double* C,
                        const double* h0, const double* z, const double* dy,
                        double* dx, double* ddelta, double* dA_log, double* dB, double* dC,
@@ -207,7 +226,8 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
 
     memset(dx, 0, (size_t)(nb * T * D) * sizeof(double));
     memset(ddelta, 0, (size_t)(nb * T * D) * sizeof(double));
-    memset(dA_log, 0, (size_t)(D * N) * sizeof(double));
+    const int64_t NA = (flags & OR_A_SCALAR) ? 1 : N;  /* decay rates per channel */
+    memset(dA_log, 0, (size_t)(D * NA) * sizeof(double));
     if (dz) memset(dz, 0, (size_t)(nb * T * D) * sizeof(double));
     if (dh0) memset(dh0, 0, (size_t)(nb * D * N) * sizeof(double));
 
@@ -234,9 +254,9 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
         double* wsum = (mode == MODE_TAIL) ? (double*)malloc((size_t)(T + 1) * sizeof(double)) : NULL;
         int64_t d_lo = q * per, d_hi = (q + 1) * per < D ? (q + 1) * per : D;
         for (int64_t d = d_lo; d < d_hi; ++d) {
-            double* dA_row = dA_log + d * N; /* one writer per channel */
+            double* dA_row = dA_log + d * NA; /* one writer per channel */
             for (int64_t bb = 0; bb < nb; ++bb) {
-                chan_forward(bb, d, T, D, N, x, delta, delta_softplus, A_log, B, C, h0, z, dy, &f, dz);
+                chan_forward(bb, d, T, D, N, x, delta, flags, A_log, B, C, h0, z, dy, &f, dz);
                 /* vjp_C (never truncated): dL/dC_t[n] += g_t h_t[n]. */
                 for (int64_t t = 0; t < T; ++t)
                     for (int64_t n = 0; n < N; ++n)
@@ -250,7 +270,7 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
                     for (int64_t t = T - 1; t >= 0; --t) {
                         for (int64_t n = 0; n < N; ++n)
                             w[n] = f.g[t] * C[(bb * T + t) * N + n] + lam[n];
-                        step_vjp(bb, t, d, T, D, N, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q]);
+                        step_vjp(bb, t, d, T, D, N, flags, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q]);
                         for (int64_t n = 0; n < N; ++n) lam[n] = f.a[t * N + n] * w[n];
                     }
                     if (dh0)
@@ -264,7 +284,7 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
                         for (int64_t n = 0; n < N; ++n) lam[n] = C[(bb * T + t) * N + n];
                         for (int64_t i = t; i >= i_lo; --i) {
                             for (int64_t n = 0; n < N; ++n) w[n] = f.g[t] * lam[n];
-                            step_vjp(bb, i, d, T, D, N, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q]);
+                            step_vjp(bb, i, d, T, D, N, flags, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q]);
                             for (int64_t n = 0; n < N; ++n) lam[n] *= f.a[i * N + n];
                         }
                         /* Prop. 1's lambda^0 term: only the full gradient
@@ -293,11 +313,11 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
                         if (!full && i + tbar < T) {
                             double win = wsum[i + tbar + 1] - wsum[i + 1];
                             for (int64_t n = 0; n < N; ++n) {
-                                double P = exp(-exp(A_log[d * N + n]) * win);
+                                double P = exp(-exp(alog_at(A_log, flags, d, N, n)) * win);
                                 w[n] -= P * mu[(i + tbar) * N + n];
                             }
                         }
-                        step_vjp(bb, i, d, T, D, N, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q]);
+                        step_vjp(bb, i, d, T, D, N, flags, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q]);
                     }
                     if (full && dh0)
                         for (int64_t n = 0; n < N; ++n)
@@ -311,37 +331,37 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
     reduce_blocks(dB, blkB, btn);
     reduce_blocks(dC, blkC, btn);
     for (int q = 0; q < ORACLE_NBLK; ++q) { free(blkB[q]); free(blkC[q]); }
-    finish_softplus(nb, T, D, delta, delta_softplus, ddelta);
+    finish_softplus(nb, T, D, delta, flags, ddelta);
     return 0;
 }
 
 int oracle_bptt(int64_t nb, int64_t T, int64_t D, int64_t N,
-                const double* x, const double* delta, int delta_softplus,
+                const double* x, const double* delta, int flags,
                 const double* A_log, const double* B, const double* C,
                 const double* h0, const double* z, const double* dy,
                 double* dx, double* ddelta, double* dA_log, double* dB, double* dC,
                 double* dz, double* dh0, int nthreads) {
-    return grad_driver(MODE_BPTT, nb, T, D, N, 0, x, delta, delta_softplus, A_log, B, C, h0, z,
+    return grad_driver(MODE_BPTT, nb, T, D, N, 0, x, delta, flags, A_log, B, C, h0, z,
                        dy, dx, ddelta, dA_log, dB, dC, dz, dh0, nthreads);
 }
 
 int oracle_adjoint_sum(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t tbar,
-                       const double* x, const double* delta, int delta_softplus,
+                       const double* x, const double* delta, int flags,
                        const double* A_log, const double* B, const double* C,
                        const double* h0, const double* z, const double* dy,
                        double* dx, double* ddelta, double* dA_log, double* dB, double* dC,
                        double* dz, double* dh0, int nthreads) {
-    return grad_driver(MODE_DOUBLESUM, nb, T, D, N, tbar, x, delta, delta_softplus, A_log, B, C,
+    return grad_driver(MODE_DOUBLESUM, nb, T, D, N, tbar, x, delta, flags, A_log, B, C,
                        h0, z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0, nthreads);
 }
 
 int oracle_trunc_tail(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t tbar,
-                      const double* x, const double* delta, int delta_softplus,
+                      const double* x, const double* delta, int flags,
                       const double* A_log, const double* B, const double* C,
                       const double* h0, const double* z, const double* dy,
                       double* dx, double* ddelta, double* dA_log, double* dB, double* dC,
                       double* dz, double* dh0, int nthreads) {
-    return grad_driver(MODE_TAIL, nb, T, D, N, tbar, x, delta, delta_softplus, A_log, B, C, h0,
+    return grad_driver(MODE_TAIL, nb, T, D, N, tbar, x, delta, flags, A_log, B, C, h0,
                        z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0, nthreads);
 }
 

@@ -17,23 +17,29 @@ import oracle
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
-def tiny(rng, nb=2, T=10, D=3, N=4, gate=True, softplus=True, h0=True, slow=False):
+def tiny(rng, nb=2, T=10, D=3, N=4, gate=True, softplus=True, h0=True, slow=False, a_scalar=False,
+         b_delta=False):
     x = rng.standard_normal((nb, T, D))
     dpre = rng.standard_normal((nb, T, D)) - (3.0 if slow else 0.0)
     if not softplus:
         dpre = np.log1p(np.exp(dpre))
-    A_log = rng.uniform(0.0, math.log(16.0), (D, N))
+    A_log = rng.uniform(0.0, math.log(16.0), (D,) if a_scalar else (D, N))
     B = rng.standard_normal((nb, T, N)) * 0.5
     C = rng.standard_normal((nb, T, N)) * 0.5
     z = rng.standard_normal((nb, T, D)) if gate else None
     hz = rng.standard_normal((nb, D, N)) if h0 else None
     dy = rng.standard_normal((nb, T, D))
-    return dict(x=x, delta=dpre, A_log=A_log, B=B, C=C, z=z, h0=hz, dy=dy, delta_softplus=softplus)
+    return dict(x=x, delta=dpre, A_log=A_log, B=B, C=C, z=z, h0=hz, dy=dy, delta_softplus=softplus,
+                a_scalar=a_scalar, b_delta=b_delta)
+
+
+def variant(inp):
+    return dict(a_scalar=inp.get("a_scalar", False), b_delta=inp.get("b_delta", False))
 
 
 def loss(inp):
     out, _ = oracle.forward(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], h0=inp["h0"],
-                            z=inp["z"], delta_softplus=inp["delta_softplus"])
+                            z=inp["z"], delta_softplus=inp["delta_softplus"], **variant(inp))
     return float(np.sum(inp["dy"] * out))
 
 
@@ -44,7 +50,7 @@ def relerr(a, b):
 
 def bptt_of(inp, **kw):
     return oracle.bptt(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], h0=inp["h0"],
-                       z=inp["z"], delta_softplus=inp["delta_softplus"], **kw)
+                       z=inp["z"], delta_softplus=inp["delta_softplus"], **variant(inp), **kw)
 
 
 # --------------------------------------------------------------------------
@@ -368,3 +374,97 @@ def test_layer_gradient_matches_central_differences(rng):
             fd[idx] = (lp - lm) / (2 * eps)
         got = g[key].reshape(fd.shape)
         assert relerr(got, fd) < 1e-6, key
+
+
+# --------------------------------------------------------------------------
+# Variants: the scalar-decay SSM of Table 1 and the step-size-scaled input
+# --------------------------------------------------------------------------
+VARIANTS = [(True, False), (False, True), (True, True)]
+
+
+@pytest.mark.parametrize("a_scalar,b_delta", VARIANTS)
+def test_variant_bptt_matches_central_differences(rng, a_scalar, b_delta):
+    inp = tiny(rng, nb=2, T=8, D=3, N=4, gate=True, softplus=True, h0=True, a_scalar=a_scalar, b_delta=b_delta)
+    g = bptt_of(inp)
+    eps = 1e-6
+    for src, dst in [("x", "dx"), ("delta", "ddelta"), ("A_log", "dA_log"), ("B", "dB"), ("C", "dC"),
+                     ("h0", "dh0"), ("z", "dz")]:
+        arr = inp[src]
+        fd = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            keep = arr[idx]
+            arr[idx] = keep + eps
+            lp = loss(inp)
+            arr[idx] = keep - eps
+            lm = loss(inp)
+            arr[idx] = keep
+            fd[idx] = (lp - lm) / (2 * eps)
+        assert relerr(g[dst], fd) < 1e-6, (src, relerr(g[dst], fd))
+
+
+@pytest.mark.parametrize("a_scalar,b_delta", VARIANTS)
+def test_variant_bptt_matches_torch_autograd(rng, a_scalar, b_delta):
+    inp = tiny(rng, nb=2, T=11, D=3, N=4, gate=True, softplus=True, h0=True, a_scalar=a_scalar, b_delta=b_delta)
+    ts = {k: torch.tensor(inp[k], dtype=torch.float64, requires_grad=True)
+          for k in ("x", "delta", "A_log", "B", "C", "z", "h0")}
+    delta = torch.nn.functional.softplus(ts["delta"])
+    rate = torch.exp(ts["A_log"])
+    rate = rate[:, None].expand(-1, 4) if a_scalar else rate
+    h = ts["h0"].clone()
+    L = 0.0
+    for t in range(ts["x"].shape[1]):
+        a = torch.exp(-delta[:, t, :, None] * rate[None])
+        u = ts["x"][:, t] * (delta[:, t] if b_delta else 1.0)
+        h = a * h + ts["B"][:, t, None, :] * u[:, :, None]
+        y = (ts["C"][:, t, None, :] * h).sum(-1)
+        L = L + (torch.tensor(inp["dy"][:, t]) * y * torch.nn.functional.silu(ts["z"][:, t])).sum()
+    L.backward()
+    g = bptt_of(inp)
+    for src, dst in [("x", "dx"), ("delta", "ddelta"), ("A_log", "dA_log"), ("B", "dB"), ("C", "dC"),
+                     ("z", "dz"), ("h0", "dh0")]:
+        assert relerr(g[dst], ts[src].grad.numpy()) < 1e-12, src
+
+
+def test_scalar_decay_equals_diagonal_with_shared_rates(rng):
+    """A scalar decay per channel is the diagonal decay with A_log[d, n] = A_log[d]
+    for every n: same outputs and gradients, and dA_log is the row sum."""
+    inp = tiny(rng, nb=2, T=15, D=3, N=5, gate=True, softplus=True, h0=True, a_scalar=True)
+    g = bptt_of(inp)
+    diag = dict(inp, A_log=np.repeat(inp["A_log"][:, None], 5, axis=1), a_scalar=False)
+    gd = bptt_of(diag)
+    assert abs(loss(inp) - loss(diag)) < 1e-12 * max(1.0, abs(loss(diag)))
+    for k in ("dx", "ddelta", "dB", "dC", "dz", "dh0"):
+        assert relerr(g[k], gd[k]) < 1e-13, k
+    assert relerr(g["dA_log"], gd["dA_log"].sum(axis=1)) < 1e-13
+
+
+def test_step_scaled_input_equals_rescaled_x(rng):
+    """h = a h + Delta B x is the plain layer run on x' = Delta x: same outputs,
+    dx = Delta dx', and the input path adds dx' x to dDelta."""
+    inp = tiny(rng, nb=2, T=14, D=3, N=4, gate=True, softplus=False, h0=True, b_delta=True)
+    g = bptt_of(inp)
+    plain = dict(inp, x=inp["x"] * inp["delta"], b_delta=False)
+    gp = bptt_of(plain)
+    assert abs(loss(inp) - loss(plain)) < 1e-12 * max(1.0, abs(loss(plain)))
+    assert relerr(g["dx"], gp["dx"] * inp["delta"]) < 1e-13
+    assert relerr(g["ddelta"], gp["ddelta"] + gp["dx"] * inp["x"]) < 1e-13
+    for k in ("dA_log", "dB", "dC", "dz", "dh0"):
+        assert relerr(g[k], gp[k]) < 1e-13, k
+
+
+@pytest.mark.parametrize("a_scalar,b_delta", VARIANTS)
+def test_variant_doublesum_and_tail_agree(rng, a_scalar, b_delta):
+    """Prop. 2 and the tail identity hold for the variants too."""
+    inp = tiny(rng, nb=2, T=24, D=3, N=4, gate=True, softplus=True, h0=True, slow=True, a_scalar=a_scalar,
+               b_delta=b_delta)
+    args = (inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"])
+    kw = dict(h0=inp["h0"], z=inp["z"], delta_softplus=True, a_scalar=a_scalar, b_delta=b_delta)
+    ref = bptt_of(inp)
+    full = oracle.adjoint_sum(*args, tbar=0, **kw)
+    for k in ("dx", "ddelta", "dA_log", "dB", "dC", "dz", "dh0"):
+        assert relerr(full[k], ref[k]) < 1e-12, k
+    for tbar in (1, 5, 13):
+        ds = oracle.adjoint_sum(*args, tbar=tbar, **kw)
+        tl = oracle.trunc_tail(*args, tbar=tbar, **kw)
+        for k in ("dx", "ddelta", "dA_log", "dB", "dC", "dz"):
+            assert relerr(tl[k], ds[k]) < 1e-11, (tbar, k)
