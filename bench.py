@@ -89,34 +89,37 @@ def _kernel_times(fn, steps, ssm, torch):
     return out
 
 
-def layer_step(w, inp, ssm, torch, tbar=0):
+def layer_step(w, inp, ssm, torch, tbar=0, b_delta=False):
+    """One whole-layer gradient; ``inp["A_log"]`` of shape [D] selects the scalar-decay variant."""
     b, T, D, N, dm = w.b, w.T, w.D, w.N, w.d_model
     f32 = dict(dtype=torch.float32, device="cuda")
     out = {"dW_in": torch.empty(dm, 2 * D, **f32), "dW_x": torch.empty(D, D + 2 * N, **f32),
-           "dA_log": torch.empty(D, N, **f32)}
-    desc = ssm.make_desc(inp["x"], N, True, True, 0)
+           "dA_log": torch.empty(*inp["A_log"].shape, **f32)}
+    desc = ssm.make_desc(inp["x"], N, True, True, 0, inp["A_log"].dim() == 1, b_delta)
     ws = torch.empty(ssm.layer_workspace_size(desc, tbar, dm), dtype=torch.uint8, device="cuda")
 
     def step():
         ssm.ssm_layer_grad(inp["u"], inp["x"], inp["z"], inp["delta"], inp["B"], inp["C"], inp["W_x"],
-                           inp["W_in"], inp["A_log"], inp["dy"], tbar=tbar, out=out, workspace=ws)
+                           inp["W_in"], inp["A_log"], inp["dy"], tbar=tbar, out=out, workspace=ws, b_delta=b_delta)
     return step
 
 
-def scan_step(w, inp, ssm, torch, tbar=0):
+def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False):
+    """One scan gradient; ``inp["A_log"]`` of shape [D] selects the scalar-decay variant."""
     b, T, D, N = w.b, w.T, w.D, w.N
     f32 = dict(dtype=torch.float32, device="cuda")
     out = {"dx": torch.empty(b, T, D, **f32), "ddelta": torch.empty(b, T, D, **f32),
-           "dA_log": torch.empty(D, N, **f32), "dB": torch.empty(b, T, N, **f32), "dC": torch.empty(b, T, N, **f32)}
+           "dA_log": torch.empty(*inp["A_log"].shape, **f32), "dB": torch.empty(b, T, N, **f32),
+           "dC": torch.empty(b, T, N, **f32)}
     z = inp.get("z") if w.proj else None
     if z is not None:
         out["dz"] = torch.empty(b, T, D, **f32)
-    desc = ssm.make_desc(inp["x"], N, w.proj, z is not None, 0)
+    desc = ssm.make_desc(inp["x"], N, w.proj, z is not None, 0, inp["A_log"].dim() == 1, b_delta)
     ws = torch.empty(ssm.grad_workspace_size(desc, tbar), dtype=torch.uint8, device="cuda")
 
     def step():
         ssm.ssm_adjoint_grad(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], z=z,
-                             softplus=w.proj, tbar=tbar, out=out, workspace=ws)
+                             softplus=w.proj, tbar=tbar, out=out, workspace=ws, b_delta=b_delta)
     return step
 
 
@@ -249,20 +252,26 @@ def main():
     torch.cuda.empty_cache()
 
     if not args.no_extra:
-        runs = [("small", "scan", 0), ("small", "scan", 32), ("long", "layer", 2048), ("long", "scan", 2048),
-                ("long_slow", "scan", 2048), ("slice", "layer", 0), ("slice", "layer", 4096),
-                ("vlong", "scan", 8192)]
+        # (workload, kind, tbar, variant); variant "scalarA+deltaB" is the scalar-decay SSM of
+        # Table 1 with the step-size-scaled input
+        runs = [("small", "scan", 0, ""), ("small", "scan", 32, ""), ("long", "layer", 2048, ""),
+                ("long", "scan", 2048, ""), ("long_slow", "scan", 2048, ""), ("slice", "layer", 0, ""),
+                ("slice", "layer", 4096, ""), ("vlong", "scan", 8192, ""),
+                ("layer", "layer", 0, "scalarA+deltaB"), ("long", "scan", 2048, "scalarA+deltaB")]
         res = {}
-        for name, kind, tbar in runs:
+        for name, kind, tbar, variant in runs:
             wl = WORKLOADS[name]
             x = make_inputs(wl, device="cuda")
-            st = (layer_step if kind == "layer" else scan_step)(wl, x, ssm, torch, tbar=tbar)
+            if variant:
+                x["A_log"] = x["A_log"][:, 0].contiguous()
+            st = (layer_step if kind == "layer" else scan_step)(wl, x, ssm, torch, tbar=tbar,
+                                                                b_delta=bool(variant))
             steps = 5 if wl.M >= 262144 else 10
             m = _timed(st, steps, 2, torch)
             kt = _kernel_times(st, 2, ssm, torch)
             entry = {"ms_per_step": m, "tokens_per_s": wl.M / (m * 1e-3), "tbar": tbar,
                      "grad_fused_avg_ms": kt.get("grad_fused", {}).get("avg_ms")}
-            r = roofline_for("grad_fused", kt, wl, (kind, tbar))
+            r = None if variant else roofline_for("grad_fused", kt, wl, (kind, tbar))
             if r:
                 entry["grad_fused_TFLOPs"] = r["achieved"]
                 entry["grad_fused_alu_frac"] = r["frac"]
@@ -272,7 +281,7 @@ def main():
                 if g in kt:
                     rg = roofline_for(g, kt, wl, kind)
                     entry[f"{g}_TFLOPs"] = rg["achieved"]
-            res[f"{name}/{kind}/tbar={tbar}"] = entry
+            res[f"{name}/{kind}/tbar={tbar}" + (f"/{variant}" if variant else "")] = entry
             del x, st
             torch.cuda.empty_cache()
         extra["workloads"] = res

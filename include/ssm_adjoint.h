@@ -11,6 +11,12 @@
  *     y_t[d]   = sum_n C_t[n] * h_t[d,n]
  *   optional: Delta = softplus(Delta_pre) (SSM_DELTA_SOFTPLUS) and a SiLU output
  *   gate out_t = y_t * silu(z_t) (SSM_GATE_SILU).
+ *   Variants (Table 1 and the input discretisation):
+ *     SSM_A_SCALAR : the scalar-decay SSM, one decay per channel shared by its
+ *                    states, a_t[d,n] = exp(-Delta_t[d] * exp(A_log[d]));
+ *                    A_log and dA_log are [channels];
+ *     SSM_B_DELTA  : the input term scaled by the step size,
+ *                    h_t = a_t * h_{t-1} + Delta_t[d] * B_t[n] * x_t[d].
  *   Prop. 2 (one layer): the gradient of L = sum_{b,t,d} dy_t[d] * out_t[d]
  *   splits into vector-Jacobian products of the A, B and C maps weighted by the
  *   adjoint states lambda^{t,i} = C^t A^t ... A^{i+1}; summed over the loss terms
@@ -65,6 +71,8 @@ typedef enum { SSM_FULL = 0, SSM_TRUNCATED = 1 } ssm_mode;
 #define SSM_DELTA_SOFTPLUS 1u /* `delta` holds Delta_pre; Delta = softplus(Delta_pre),
                                  and `ddelta` is the gradient w.r.t. Delta_pre          */
 #define SSM_GATE_SILU 2u      /* `z` present: out = y * silu(z); `dy` is dL/dout        */
+#define SSM_A_SCALAR 4u       /* one decay rate per channel: A_log, dA_log are [D]      */
+#define SSM_B_DELTA 8u        /* input term Delta * B * x (dDelta includes its path)    */
 
 /* ssm_proj_grad flags */
 #define SSM_ACCUM_DW 1u       /* dW += X^T dZ instead of dW = X^T dZ                   */
@@ -79,7 +87,7 @@ typedef struct {
                          16, 32, 64, 128, 256.  Results do not depend on it beyond
                          rounding.                                                  */
     int32_t in_dtype; /* ssm_dtype of x, delta, B, C, z, dy (and of y)              */
-    uint32_t flags;   /* SSM_DELTA_SOFTPLUS | SSM_GATE_SILU                         */
+    uint32_t flags;   /* SSM_DELTA_SOFTPLUS | SSM_GATE_SILU | SSM_A_SCALAR | SSM_B_DELTA */
 } ssm_desc;
 
 /* Workspace bytes needed by ssm_adjoint_forward / ssm_adjoint_grad for `desc`
@@ -90,7 +98,7 @@ ssm_status ssm_adjoint_grad_workspace_size(const ssm_desc* desc, int32_t mode, i
 
 /* Forward pass (Sec. 3.1 steps 4-5, with the state recomputed chunk by chunk and
  * never stored per step).
- *   x, delta, B, C : in_dtype inputs;  A_log : fp32 [D][N];
+ *   x, delta, B, C : in_dtype inputs;  A_log : fp32 [D][N] ([D] with SSM_A_SCALAR);
  *   h0     : fp32 [b][D][N] initial state, or NULL for zero;
  *   z      : in_dtype gate input, required iff SSM_GATE_SILU;
  *   y      : in_dtype output [b][T][D] (y, or y * silu(z) with the gate);
@@ -106,7 +114,7 @@ ssm_status ssm_adjoint_forward(const ssm_desc* desc, const void* x, const void* 
  * Outputs (fp32, overwritten):
  *   dx     [b][T][D]  B-path cotangent summed over the state, sum_n mubar B_t[n]
  *   ddelta [b][T][D]  dL/dDelta, or dL/dDelta_pre with SSM_DELTA_SOFTPLUS
- *   dA_log [D][N]
+ *   dA_log [D][N] ([D] with SSM_A_SCALAR)
  *   dB, dC [b][T][N]  (dC is never truncated)
  *   dz     [b][T][D]  required iff SSM_GATE_SILU, else must be NULL
  *   dh0    [b][D][N]  dL/dh0, full mode only (must be NULL when truncating), or NULL.
@@ -139,7 +147,8 @@ ssm_status ssm_proj_grad(int64_t M, int64_t K, int64_t Nout, const void* X, int6
  * Given the stored activations u [M][d_model], x, z, delta_pre [M][D], B, C [M][N]
  * (M = b*T rows), the weights W_x [D][D+2N] and W_in [d_model][2D] (bf16), A_log and
  * the upstream dy = dL/dout, it computes the scan gradient (as ssm_adjoint_grad with
- * SSM_DELTA_SOFTPLUS | SSM_GATE_SILU; desc->flags is ignored), then
+ * SSM_DELTA_SOFTPLUS | SSM_GATE_SILU; of desc->flags only SSM_A_SCALAR and
+ * SSM_B_DELTA are used), then
  *   dZx = [dDelta_pre | dB | dC]            (bf16, internal)
  *   dW_x = x^T dZx                           fp32 [D][D+2N]
  *   dx_total = dx + dZx W_x^T                fp32 [M][D] (optional output)

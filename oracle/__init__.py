@@ -196,7 +196,8 @@ def layer_forward(u, W_in, W_x, A_log, N, h0=None):
     return out, dict(x=x, z=z, dpre=dpre, B=B, C=C, h_last=h_last)
 
 
-def layer_grad(u, x, z, dpre, B, C, W_x, A_log, dy, W_in=None, tbar=0, scan=None):
+def layer_grad(u, x, z, dpre, B, C, W_x, A_log, dy, W_in=None, tbar=0, scan=None, a_scalar=False,
+               b_delta=False):
     """Gradient of ``L = sum dy * out`` for the layer with input projections.
 
     ``scan`` selects the scan gradient: ``bptt`` (default, full), ``trunc_tail`` or
@@ -205,10 +206,11 @@ def layer_grad(u, x, z, dpre, B, C, W_x, A_log, dy, W_in=None, tbar=0, scan=None
     ``dW_in = u^T [dx_total | dz]``, ``du = [dx_total | dz] W_in^T``.
     """
     u, x, z, dpre, B, C, W_x, dy = map(_f64, (u, x, z, dpre, B, C, W_x, dy))
+    v = dict(a_scalar=a_scalar, b_delta=b_delta)
     if scan is None:
-        g = bptt(x, dpre, A_log, B, C, dy, z=z, delta_softplus=True, want_dh0=False)
+        g = bptt(x, dpre, A_log, B, C, dy, z=z, delta_softplus=True, want_dh0=False, **v)
     else:
-        g = scan(x, dpre, A_log, B, C, dy, tbar=tbar, z=z, delta_softplus=True, want_dh0=False)
+        g = scan(x, dpre, A_log, B, C, dy, tbar=tbar, z=z, delta_softplus=True, want_dh0=False, **v)
     nb, T, D = x.shape
     M = nb * T
     dZx = np.concatenate([g["ddelta"], g["dB"], g["dC"]], axis=-1).reshape(M, -1)

@@ -23,7 +23,7 @@ LIB_PATH = _PKG / "libssm_adjoint.so"
 
 SSM_F32, SSM_BF16 = 0, 1
 SSM_FULL, SSM_TRUNCATED = 0, 1
-SSM_DELTA_SOFTPLUS, SSM_GATE_SILU = 1, 2
+SSM_DELTA_SOFTPLUS, SSM_GATE_SILU, SSM_A_SCALAR, SSM_B_DELTA = 1, 2, 4, 8
 SSM_ACCUM_DW, SSM_ACCUM_DX = 1, 2
 
 STATUS = {0: "SSM_OK", 1: "SSM_ERR_NULL", 2: "SSM_ERR_SHAPE", 3: "SSM_ERR_DTYPE",
@@ -148,10 +148,17 @@ def _need(t, name, dtype=None, shape=None):
     return t
 
 
-def make_desc(x: torch.Tensor, N: int, softplus=False, gate=False, chunk=0) -> SsmDesc:
+def make_desc(x: torch.Tensor, N: int, softplus=False, gate=False, chunk=0, a_scalar=False,
+              b_delta=False) -> SsmDesc:
     b, T, D = x.shape
-    flags = (SSM_DELTA_SOFTPLUS if softplus else 0) | (SSM_GATE_SILU if gate else 0)
+    flags = ((SSM_DELTA_SOFTPLUS if softplus else 0) | (SSM_GATE_SILU if gate else 0) |
+             (SSM_A_SCALAR if a_scalar else 0) | (SSM_B_DELTA if b_delta else 0))
     return SsmDesc(b, T, D, N, chunk, _dtype_code(x), flags)
+
+
+def _alog_shape(A_log, D, N):
+    """A_log is [D, N], or [D] for one decay rate per channel (the scalar variant)."""
+    return (D,) if A_log.dim() == 1 else (D, N)
 
 
 def _workspace(nbytes: int, device) -> torch.Tensor:
@@ -168,20 +175,22 @@ def grad_workspace_size(desc: SsmDesc, tbar: int = 0) -> int:
 
 
 def ssm_adjoint_forward(x, delta, A_log, B, C, h0=None, z=None, softplus=False, chunk=0, want_h_last=False,
-                        workspace=None):
-    """Forward pass; returns ``y`` (and ``h_last`` if asked).  ``y`` has x's dtype."""
+                        workspace=None, b_delta=False):
+    """Forward pass; returns ``y`` (and ``h_last`` if asked).  ``y`` has x's dtype.
+    ``A_log`` of shape [D] selects one decay rate per channel; ``b_delta`` the
+    input term Delta B x."""
     lib = load_library()
     dt = x.dtype
     b, T, D = x.shape
-    N = A_log.shape[1]
+    N = B.shape[-1]
     _need(x, "x", dt)
     _need(delta, "delta", dt, (b, T, D))
-    _need(A_log, "A_log", torch.float32, (D, N))
+    _need(A_log, "A_log", torch.float32, _alog_shape(A_log, D, N))
     _need(B, "B", dt, (b, T, N))
     _need(C, "C", dt, (b, T, N))
     _need(h0, "h0", torch.float32, (b, D, N))
     _need(z, "z", dt, (b, T, D))
-    desc = make_desc(x, N, softplus, z is not None, chunk)
+    desc = make_desc(x, N, softplus, z is not None, chunk, A_log.dim() == 1, b_delta)
     n = ctypes.c_size_t()
     _check(lib.ssm_adjoint_forward_workspace_size(ctypes.byref(desc), ctypes.byref(n)),
            "ssm_adjoint_forward_workspace_size")
@@ -194,31 +203,33 @@ def ssm_adjoint_forward(x, delta, A_log, B, C, h0=None, z=None, softplus=False, 
 
 
 def ssm_adjoint_grad(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False, tbar=0, chunk=0,
-                     want_dh0=False, out=None, workspace=None):
+                     want_dh0=False, out=None, workspace=None, b_delta=False):
     """Per-layer adjoint gradient.  ``tbar > 0`` selects the truncated form.
+    ``A_log`` of shape [D] selects one decay rate per channel (and dA_log is [D]);
+    ``b_delta`` the input term Delta B x.
 
     Returns a dict with fp32 ``dx, ddelta, dA_log, dB, dC`` (+ ``dz`` with a gate,
     ``dh0`` if asked).  ``out`` may hold preallocated outputs under the same keys."""
     lib = load_library()
     dt = x.dtype
     b, T, D = x.shape
-    N = A_log.shape[1]
+    N = B.shape[-1]
     _need(x, "x", dt)
     _need(delta, "delta", dt, (b, T, D))
-    _need(A_log, "A_log", torch.float32, (D, N))
+    _need(A_log, "A_log", torch.float32, _alog_shape(A_log, D, N))
     _need(B, "B", dt, (b, T, N))
     _need(C, "C", dt, (b, T, N))
     _need(dy, "dy", dt, (b, T, D))
     _need(h0, "h0", torch.float32, (b, D, N))
     _need(z, "z", dt, (b, T, D))
-    desc = make_desc(x, N, softplus, z is not None, chunk)
+    desc = make_desc(x, N, softplus, z is not None, chunk, A_log.dim() == 1, b_delta)
     mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
     dev = x.device
     f32 = dict(dtype=torch.float32, device=dev)
     o = dict(out) if out else {}
     o.setdefault("dx", torch.empty(b, T, D, **f32))
     o.setdefault("ddelta", torch.empty(b, T, D, **f32))
-    o.setdefault("dA_log", torch.empty(D, N, **f32))
+    o.setdefault("dA_log", torch.empty(*A_log.shape, **f32))
     o.setdefault("dB", torch.empty(b, T, N, **f32))
     o.setdefault("dC", torch.empty(b, T, N, **f32))
     if z is not None:
@@ -265,14 +276,14 @@ def layer_workspace_size(desc: SsmDesc, tbar: int, d_model: int) -> int:
 
 
 def ssm_layer_grad(u, x, z, delta_pre, B, C, W_x, W_in, A_log, dy, tbar=0, chunk=0, want_du=False,
-                   want_scan=False, out=None, workspace=None):
+                   want_scan=False, out=None, workspace=None, b_delta=False):
     """Whole-layer gradient with input projections (bf16 activations).
 
     Returns a dict with fp32 ``dW_in, dW_x, dA_log`` (+ ``du`` if asked; + the scan
     gradients ``dx, ddelta, dB, dC, dz`` and ``dx_total`` if ``want_scan``)."""
     lib = load_library()
     b, T, D = x.shape
-    N = A_log.shape[1]
+    N = B.shape[-1]
     dm = u.shape[-1]
     bf = torch.bfloat16
     _need(u, "u", bf, (b, T, dm))
@@ -283,16 +294,16 @@ def ssm_layer_grad(u, x, z, delta_pre, B, C, W_x, W_in, A_log, dy, tbar=0, chunk
     _need(C, "C", bf, (b, T, N))
     _need(W_x, "W_x", bf, (D, D + 2 * N))
     _need(W_in, "W_in", bf, (dm, 2 * D))
-    _need(A_log, "A_log", torch.float32, (D, N))
+    _need(A_log, "A_log", torch.float32, _alog_shape(A_log, D, N))
     _need(dy, "dy", bf, (b, T, D))
-    desc = make_desc(x, N, True, True, chunk)
+    desc = make_desc(x, N, True, True, chunk, A_log.dim() == 1, b_delta)
     mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
     dev = x.device
     f32 = dict(dtype=torch.float32, device=dev)
     o = dict(out) if out else {}
     o.setdefault("dW_in", torch.empty(dm, 2 * D, **f32))
     o.setdefault("dW_x", torch.empty(D, D + 2 * N, **f32))
-    o.setdefault("dA_log", torch.empty(D, N, **f32))
+    o.setdefault("dA_log", torch.empty(*A_log.shape, **f32))
     if want_du:
         o.setdefault("du", torch.empty(b, T, dm, **f32))
     if want_scan:

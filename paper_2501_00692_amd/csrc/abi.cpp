@@ -44,7 +44,7 @@ ssm_status check_desc(const ssm_desc* d, int64_t* L, int64_t* nc) {
     if (d->dstate > 16) return fail(SSM_ERR_UNSUPPORTED, "dstate %lld > 16", (long long)d->dstate);
     if (d->in_dtype != SSM_F32 && d->in_dtype != SSM_BF16)
         return fail(SSM_ERR_DTYPE, "unknown in_dtype %d", (int)d->in_dtype);
-    if (d->flags & ~(SSM_DELTA_SOFTPLUS | SSM_GATE_SILU))
+    if (d->flags & ~(SSM_DELTA_SOFTPLUS | SSM_GATE_SILU | SSM_A_SCALAR | SSM_B_DELTA))
         return fail(SSM_ERR_SHAPE, "unknown flag bits 0x%x", (unsigned)d->flags);
     const int64_t l = d->chunk == 0 ? ssmk::default_chunk() : d->chunk;
     if (!ssmk::chunk_supported(l))
@@ -101,6 +101,8 @@ ssmk::ScanProblem make_problem(const ssm_desc* d, int64_t L, int64_t nc) {
     p.bf16 = d->in_dtype == SSM_BF16;
     p.softplus = (d->flags & SSM_DELTA_SOFTPLUS) != 0;
     p.gate = (d->flags & SSM_GATE_SILU) != 0;
+    p.ascalar = (d->flags & SSM_A_SCALAR) != 0;
+    p.bdelta = (d->flags & SSM_B_DELTA) != 0;
     return p;
 }
 
@@ -403,7 +405,7 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     float* dC_ = dC ? dC : f32 + 4 * M * D + M * N;
 
     ssm_desc sd = *desc;
-    sd.flags = SSM_DELTA_SOFTPLUS | SSM_GATE_SILU;
+    sd.flags = SSM_DELTA_SOFTPLUS | SSM_GATE_SILU | (desc->flags & (SSM_A_SCALAR | SSM_B_DELTA));
     bool trunc2;
     st = grad_validate(&sd, mode, tbar, x, delta_pre, A_log, B, C, nullptr, z, dy, dx_, dd_, dA_log,
                        dB_, dC_, dz_, nullptr, &L, &nc, &trunc2);

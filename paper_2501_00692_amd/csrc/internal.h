@@ -39,6 +39,8 @@ struct ScanProblem {
     bool softplus;   // delta holds Delta_pre
     bool gate;       // SiLU output gate with z
     bool trunc;      // truncated estimator with window tbar (< T)
+    bool ascalar;    // one decay rate per channel: A_log, dA_log are [D]
+    bool bdelta;     // input term Delta * B * x
     int64_t tbar;
     int nsplit;      // channel splits of the fused kernel (dB/dC partials when > 1)
     int tps;         // 16-channel tiles per split (a multiple of kGradWaves unless one split)

@@ -123,14 +123,15 @@ __device__ __forceinline__ void ld4(const TI* p, int64_t row, int r, int64_t N, 
 }
 
 // Per-lane decay constants: cn = -e^{A_log} log2(e) (a = 2^{cn Delta}) and
-// wn = -e^{A_log} (da/dDelta = a wn).  Padding states get cn = wn = 0.
+// wn = -e^{A_log} (da/dDelta = a wn), with A_log per (channel, state) or, for the
+// scalar-decay variant, per channel.  Padding states get cn = wn = 0.
 __device__ __forceinline__ void lane_consts(const float* A_log, int64_t d, int r, int64_t N,
-                                            bool dv, float cn[4], float wn[4]) {
+                                            bool dv, bool ascalar, float cn[4], float wn[4]) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int n = r * 4 + k;
         const bool v = dv && n < N;
-        const float al = ldm(A_log, d * N + n, v);
+        const float al = ldm(A_log, ascalar ? d : d * N + n, v);  // one rate per channel, or per state
         const float e = v ? __expf(al) : 0.f;
         wn[k] = -e;
         cn[k] = -e * kLog2e;
@@ -236,7 +237,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
     const TI* Bp = static_cast<const TI*>(p.B);
     const TI* Cp = static_cast<const TI*>(p.C);
     float cn[4], wn[4];
-    lane_consts(p.A_log, d, r, p.N, dv, cn, wn);
+    lane_consts(p.A_log, d, r, p.N, dv, p.ascalar, cn, wn);
     float h[4] = {0.f, 0.f, 0.f, 0.f}, m[4] = {0.f, 0.f, 0.f, 0.f}, P[4] = {1.f, 1.f, 1.f, 1.f};
     double sd = 0.0;
     const int64_t t0 = c * p.L;
@@ -287,8 +288,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
                 // not used), so that later waits count exactly
                 load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, WANT_M, nxt);
                 const bool v = dv && s0 + r < t1;
-                const float pr = fin<TI>(cur.p[0], v), xr = fin<TI>(cur.x[0], v);
+                const float pr = fin<TI>(cur.p[0], v);
                 const float dlr = (SP && v) ? softplus_f(pr) : pr;
+                float xr = fin<TI>(cur.x[0], v);
+                if (p.bdelta) xr *= dlr;  // input term Delta B x
                 float gr = 0.f;
                 if constexpr (WANT_M) {
                     const float dyr = fin<TI>(cur.dy[0], v);
@@ -361,7 +364,7 @@ __global__ __launch_bounds__(256) void k_carry(const ScanProblem p) {
     const int64_t n = blockIdx.y;
     const int64_t bb = blockIdx.z >> 1;
     const int dir = blockIdx.z & 1;
-    const float cn = -__expf(p.A_log[d * p.N + n]) * kLog2e;
+    const float cn = -__expf(p.A_log[p.ascalar ? d : d * p.N + n]) * kLog2e;
     const int64_t st = p.N * p.D;
     const int64_t base = (bb * p.nc * p.N + n) * p.D + d;
     const int64_t sbase = bb * p.nc * p.D + d;
@@ -444,7 +447,7 @@ __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
     float cn[16], h[16];
 #pragma unroll
     for (int n = 0; n < 16; ++n) {
-        cn[n] = n < p.N ? -__expf(p.A_log[d * p.N + n]) * kLog2e : 0.f;
+        cn[n] = n < p.N ? -__expf(p.A_log[p.ascalar ? d : d * p.N + n]) * kLog2e : 0.f;
         h[n] = ldm(p.hbuf, cb + n * p.D, n < p.N);
     }
     const int64_t t0 = c * p.L;
@@ -452,9 +455,9 @@ __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
 #pragma unroll 2
     for (int64_t t = t0; t < t1; ++t) {
         const int64_t td = (bb * p.T + t) * p.D + d;
-        const float xv = ldf(X, td);
         const float pv = ldf(DL, td);
         const float dl = SP ? softplus_f(pv) : pv;
+        const float xv = p.bdelta ? ldf(X, td) * dl : ldf(X, td);  // input term (Delta) B x
         float Bv[16], Cv[16];
         ld_row16(Bp, bb * p.T + t, p.N, Bv);
         ld_row16(Cp, bb * p.T + t, p.N, Cv);
@@ -667,7 +670,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
         const int64_t d = tile * 16 + chl;
         const bool dv = tile < tile_hi && d < p.D;
         float cn[4], wn[4];
-        lane_consts(p.A_log, d, r, p.N, dv, cn, wn);
+        lane_consts(p.A_log, d, r, p.N, dv, p.ascalar, cn, wn);
         bool nv[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) nv[k] = dv && (r * 4 + k < p.N);
@@ -765,14 +768,15 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, qn * S, r, lims, dv, true, nxs);
             }
             // per-channel quantities of the steps this lane prepares
-            float dls[SPL], xs[SPL], gs[SPL], gfs[SPL], dlps[SPL], gps[SPL];
+            float dls[SPL], xs[SPL], xr[SPL], gs[SPL], gfs[SPL], dlps[SPL], gps[SPL];
             bool sv[SPL];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) {
                 sv[jj] = dv && q * S + r + 4 * jj < lim;
                 const float pr = fin<TI>(cur.p[jj], sv[jj]), dyr = fin<TI>(cur.dy[jj], sv[jj]);
-                xs[jj] = fin<TI>(cur.x[jj], sv[jj]);
                 dls[jj] = (SP && sv[jj]) ? softplus_f(pr) : pr;
+                xr[jj] = fin<TI>(cur.x[jj], sv[jj]);
+                xs[jj] = p.bdelta ? xr[jj] * dls[jj] : xr[jj];  // the input term is (Delta) B x
                 if constexpr (GATE) {
                     const float zr = fin<TI>(cur.z[jj], sv[jj]);
                     const float sg = sigmoid_f(zr);
@@ -901,8 +905,11 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             for (int jj = 0; jj < SPL; ++jj) {
                 const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
                 const uint32_t off = tl * D32 + d32;
-                const float ddv = SP ? ddk[jj] * (1.f - fexp(-dls[jj])) : ddk[jj];  // d softplus / d Delta_pre
-                *(sv[jj] ? dxo + off : sinkf) = dxk[jj];
+                // with the Delta-scaled input, dx' = sum_n mubar B gives dx = dx' Delta and
+                // adds dx' x to dDelta
+                const float dd0 = p.bdelta ? fmaf(dxk[jj], xr[jj], ddk[jj]) : ddk[jj];
+                const float ddv = SP ? dd0 * (1.f - fexp(-dls[jj])) : dd0;  // d softplus / d Delta_pre
+                *(sv[jj] ? dxo + off : sinkf) = p.bdelta ? dxk[jj] * dls[jj] : dxk[jj];
                 *(sv[jj] ? ddo + off : sinkf) = ddv;
                 if constexpr (OUT16) stf(sv[jj] ? dd16o + (tl * ldd16 + d32) : sink16, 0, ddv);
             }
@@ -960,9 +967,18 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     p.dAtmp[(s * p.N + n) * p.D + d] = acc;
 }
 
-// dA_log, stage 2: sum of the slices, transposed to [D][N].
+// dA_log, stage 2: sum of the slices, transposed to [D][N]; with one rate per
+// channel also summed over the states (in slice, then state order) into [D].
 [[maybe_unused]] __global__ __launch_bounds__(256) void k_reduce_da2(const ScanProblem p) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (p.ascalar) {
+        if (i >= p.D) return;
+        float acc = 0.f;
+        for (int s = 0; s < p.nslice; ++s)
+            for (int64_t n = 0; n < p.N; ++n) acc += p.dAtmp[(s * p.N + n) * p.D + i];
+        p.dA_log[i] = acc;
+        return;
+    }
     if (i >= p.D * p.N) return;
     const int64_t d = i / p.N, n = i % p.N;
     float acc = 0.f;

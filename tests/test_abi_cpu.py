@@ -59,7 +59,7 @@ def test_null_and_shape_errors(lib):
     assert grad_call(lib, desc(dstate=17)) == 4
     assert grad_call(lib, desc(in_dtype=7)) == 3
     assert grad_call(lib, desc(chunk=100)) == 4
-    assert grad_call(lib, desc(flags=8)) == 2
+    assert grad_call(lib, desc(flags=16)) == 2
     assert grad_call(lib, desc(), x=None) == 1
     assert "x is NULL" in ssm.last_error()
     assert grad_call(lib, desc(), x=MISALIGNED) == 6
