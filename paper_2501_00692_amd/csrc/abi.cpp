@@ -128,8 +128,8 @@ LayerWs layer_ws(const ssm_desc* d, int64_t L, bool trunc, int64_t d_model) {
     off = up256(off + size_t(M) * (D + 2 * N) * 2);
     w.dxz_off = off;  // bf16 [M][2D]
     off = up256(off + size_t(M) * 2 * D * 2);
-    w.f32_off = off;  // fp32 dx, ddelta, dz [M][D] and dB, dC [M][N], dx_total [M][D]
-    off = up256(off + size_t(M) * (4 * D + 2 * N) * 4);
+    w.f32_off = off;  // fp32 dx, ddelta, dz [M][D] and dB, dC [M][N]
+    off = up256(off + size_t(M) * (3 * D + 2 * N) * 4);
     w.gemm_off = off;
     size_t g1 = ssmk::gemm_dw_workspace(M, D, D + 2 * N);
     size_t g2 = ssmk::gemm_dw_workspace(M, d_model, 2 * D);
@@ -400,9 +400,8 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     float* dx_ = dx ? dx : f32;
     float* dd_ = ddelta ? ddelta : f32 + M * D;
     float* dz_ = dz ? dz : f32 + 2 * M * D;
-    float* dxt_ = dx_total ? dx_total : f32 + 3 * M * D;
-    float* dB_ = dB ? dB : f32 + 4 * M * D;
-    float* dC_ = dC ? dC : f32 + 4 * M * D + M * N;
+    float* dB_ = dB ? dB : f32 + 3 * M * D;
+    float* dC_ = dC ? dC : f32 + 3 * M * D + M * N;
 
     ssm_desc sd = *desc;
     sd.flags = SSM_DELTA_SOFTPLUS | SSM_GATE_SILU | (desc->flags & (SSM_A_SCALAR | SSM_B_DELTA));
@@ -431,6 +430,8 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     p.ld_bc16 = nx;
     p.dz16 = dxz + D;
     p.ld_dz16 = 2 * D;
+    // fp32 dDelta_pre and dz are written only when the caller asks for one of them
+    p.only16 = !ddelta && !dz;
     hipError_t e = ssmk::launch_grad(p, s);
     if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad scan launch");
     void* gws = ws + w.gemm_off;
@@ -438,7 +439,8 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     e = ssmk::launch_gemm_dw(M, D, nx, static_cast<const uint16_t*>(x), D, dzx, nx, dW_x, false, gws, s);
     if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_x launch");
     // dx_total = dx + dZx W_x^T, also packed into [dx_total | dz]
-    e = ssmk::launch_gemm_dx(M, D, nx, dzx, nx, static_cast<const uint16_t*>(W_x), nx, dxt_, false,
+    // (the fp32 dx_total only when the caller asks for it)
+    e = ssmk::launch_gemm_dx(M, D, nx, dzx, nx, static_cast<const uint16_t*>(W_x), nx, dx_total, false,
                              dx_, dxz, 2 * D, s);
     if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dx_total launch");
     // dW_in = u^T [dx_total | dz]

@@ -7,11 +7,18 @@
 //   dX[M][K] = dZ W^T  (dZ [M][N], W [K][N]): both operands are contiguous along
 //       the reduction and are staged as they are; the epilogue adds an optional
 //       fp32 addend, accumulates, and can write a bf16 copy into a strided buffer.
-// Workgroup: 512 threads = 4x2 waves (two per SIMD); tile BM x BN with BM = 256
-// and BN in {128, 192, 256}; each wave owns a (BM/4) x (BN/2) block of 32x32 MFMA
-// tiles.  Interior tiles run a loop without bounds checks.
+// Workgroup: 512 threads = 4x2 waves, two per SIMD (one wave's MFMAs run while
+// the other waits for its loads or the barrier); a wave owns a 64 x (BN/2) block
+// of 32x32 MFMA tiles.  Tile BM x BN with BM = 256 and BN in {128, 192, 256};
+// interior tiles with whole reduction steps run a loop without bounds checks,
+// other loads read a clamped in-range address and select zero (no branches).
 // LDS is double-buffered over 64-deep reduction steps (one barrier per step);
-// the next step's global loads are in flight while the MFMAs run.
+// the next step's global loads are in flight while the MFMAs run, and below
+// 256 columns the next 16-deep sub-step's fragments are read from LDS while the
+// current sub-step's MFMAs run.
+// Output tiles are assigned so that the tiles of one row block run on the same
+// XCD (consecutive workgroups go to different XCDs), which keeps a row block of
+// the first operand in one L2.
 #include "internal.h"
 
 namespace ssmk {
@@ -77,43 +84,51 @@ struct GemmArgs {
     int64_t ld16;
 };
 
-constexpr int NT = 512;  // threads per workgroup (8 waves: 4 rows x 2 cols)
+constexpr int kXcds = 8;
 
 // Staging of both operand tiles (BM and BN rows x BK reduction) into LDS rows of
-// LDK bf16.  TR (reduction-major sources): 8x8 blocks, threads [0, BM) take the A
-// blocks and [BM, BM+BN) the B blocks, one each, transposed in registers.
-// Otherwise: 16-byte pieces spread over all threads.  FULL: the tiles and the
-// reduction step are entirely in bounds (no checks).
-template <bool TR, int BM, int BN>
+// LDK bf16.  TR (reduction-major sources): 8x8 blocks, numbered A blocks first
+// (BM of them) then B blocks (BN); thread tid takes blocks tid and tid + NT,
+// transposed in registers.  Otherwise: 16-byte pieces spread over all threads.
+// FULL: the tile's rows and columns are in bounds; KF: so is the whole
+// reduction step (no checks at all when both hold).  Reduction ranges end on a multiple of 8 except in the row-wise (TR)
+// case, where each of the 8 rows of a block is checked.
+template <bool TR, int BM, int BN, int NT>
 struct Stager {
     static constexpr int PA = TR ? BM : BM * 8;
     static constexpr int PB = TR ? BN : BN * 8;
-    static constexpr int PER = TR ? 1 : (PA + PB) / NT;
+    static constexpr int PER = TR ? (PA + PB + NT - 1) / NT : (PA + PB) / NT;
     static constexpr int REGS = TR ? 8 : 1;
-    static_assert(!TR || BM + BN <= NT, "one block per thread");
     static_assert(TR || (PA % NT == 0 && PB % NT == 0), "pieces divide evenly");
     uint4 v[PER][REGS];
 
-    template <bool FULL>
+    template <bool FULL, bool KF>
     __device__ __forceinline__ void load(const GemmArgs& g, int64_t r0, int64_t c0, int64_t k,
                                          int64_t k_hi, int tid) {
         if constexpr (TR) {
-            const bool isA = tid < BM;
-            const int pc = isA ? tid : tid - BM;
-            if (!isA && pc >= BN) return;
-            const int rows8 = (isA ? BM : BN) / 8;
-            const int rb = pc / rows8, cb = pc % rows8;  // reduction block, row block
-            const uint16_t* src = isA ? g.A : g.B;
-            const int64_t ld = isA ? g.lda : g.ldb;
-            const int64_t col = (isA ? r0 : c0) + cb * 8;
-            const int64_t ncol = isA ? g.R : g.Cc;
-            const uint16_t* p0 = src + (k + rb * 8) * ld + col;
 #pragma unroll
-            for (int r = 0; r < 8; ++r) {
-                if (FULL || (col < ncol && k + rb * 8 + r < k_hi))
-                    v[0][r] = *reinterpret_cast<const uint4*>(p0 + r * ld);
-                else
-                    v[0][r] = make_uint4(0u, 0u, 0u, 0u);
+            for (int e = 0; e < PER; ++e) {
+                const int q = tid + NT * e;
+                if (q >= PA + PB) break;  // uniform per wave (PA + PB is a multiple of 64)
+                const bool isA = q < PA;
+                const int pc = isA ? q : q - PA;
+                const int rows8 = (isA ? BM : BN) / 8;
+                const int rb = pc / rows8, cb = pc % rows8;  // reduction block, row block
+                const uint16_t* src = isA ? g.A : g.B;
+                const int64_t ld = isA ? g.lda : g.ldb;
+                const int64_t col = (isA ? r0 : c0) + cb * 8;
+                const int64_t ncol = isA ? g.R : g.Cc;
+                // out-of-range pieces load an in-range one (clamped row and column)
+                // and select zero, so that every load is issued without a branch
+                const bool cok = FULL || col < ncol;
+                const int64_t cs = cok ? col : ncol - 8;
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    const int64_t kr = k + rb * 8 + r;
+                    const bool ok = cok && (KF || kr < k_hi);
+                    const uint4 t = *reinterpret_cast<const uint4*>(src + (ok ? kr : k_hi - 1) * ld + cs);
+                    v[e][r] = ok ? t : make_uint4(0u, 0u, 0u, 0u);
+                }
             }
         } else {
 #pragma unroll
@@ -125,27 +140,32 @@ struct Stager {
                 const int64_t gr = (isA ? r0 : c0) + row, kk = k + seg * 8;
                 const uint16_t* src = isA ? g.A : g.B;
                 const int64_t ld = isA ? g.lda : g.ldb;
-                if (FULL || (gr < (isA ? g.R : g.Cc) && kk < k_hi))
-                    v[e][0] = *reinterpret_cast<const uint4*>(src + gr * ld + kk);
-                else
-                    v[e][0] = make_uint4(0u, 0u, 0u, 0u);
+                const int64_t nrow = isA ? g.R : g.Cc;
+                const bool ok = (FULL || gr < nrow) && (KF || kk < k_hi);
+                const uint4 t = *reinterpret_cast<const uint4*>(src + (FULL || gr < nrow ? gr : nrow - 1) * ld +
+                                                                (KF || kk < k_hi ? kk : k_hi - 8));
+                v[e][0] = ok ? t : make_uint4(0u, 0u, 0u, 0u);
             }
         }
     }
     __device__ __forceinline__ void store(uint16_t (*As)[LDK], uint16_t (*Bs)[LDK], int tid) const {
         if constexpr (TR) {
-            const bool isA = tid < BM;
-            const int pc = isA ? tid : tid - BM;
-            if (!isA && pc >= BN) return;
-            const int rows8 = (isA ? BM : BN) / 8;
-            const int rb = pc / rows8, cb = pc % rows8;
-            uint16_t(*dst)[LDK] = isA ? As : Bs;
-            uint4 tr[8];
-            transpose8x8(v[0], tr);
 #pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                const int row = cb * 8 + c;
-                *reinterpret_cast<uint4*>(&dst[row][swz(row, rb) * 8]) = tr[c];
+            for (int e = 0; e < PER; ++e) {
+                const int q = tid + NT * e;
+                if (q >= PA + PB) break;
+                const bool isA = q < PA;
+                const int pc = isA ? q : q - PA;
+                const int rows8 = (isA ? BM : BN) / 8;
+                const int rb = pc / rows8, cb = pc % rows8;
+                uint16_t(*dst)[LDK] = isA ? As : Bs;
+                uint4 tr[8];
+                transpose8x8(v[e], tr);
+#pragma unroll
+                for (int c = 0; c < 8; ++c) {
+                    const int row = cb * 8 + c;
+                    *reinterpret_cast<uint4*>(&dst[row][swz(row, rb) * 8]) = tr[c];
+                }
             }
         } else {
 #pragma unroll
@@ -161,8 +181,9 @@ struct Stager {
     }
 };
 
-// Main loop over the workgroup's reduction range; FULL drops every bounds check.
-template <bool TR, int BM, int BN, bool FULL, int MI, int NJ>
+// Main loop over the workgroup's reduction range; FULL drops the row and column
+// bounds checks.
+template <bool TR, int BM, int BN, int NT, bool FULL, bool KF, int MI, int NJ>
 __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, uint16_t (*As)[BM][LDK],
                                               uint16_t (*Bs)[BN][LDK], int64_t r0, int64_t c0,
                                               int64_t k_lo, int64_t k_hi, int tid, int wr, int wc,
@@ -170,53 +191,94 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, uint16_t (*As)[
     const int lane = tid & 63;
     const int li = lane & 31;
     const int lk = (lane >> 5) * 8;
-    Stager<TR, BM, BN> st;
+    Stager<TR, BM, BN, NT> st;
     if (k_lo < k_hi) {
-        st.template load<FULL>(g, r0, c0, k_lo, k_hi, tid);
+        st.template load<FULL, KF>(g, r0, c0, k_lo, k_hi, tid);
         st.store(As[0], Bs[0], tid);
     }
     __syncthreads();
+    // fragments of one 16-deep sub-step, double-buffered in registers: the next
+    // sub-step's LDS reads are issued before the current sub-step's MFMAs, and the
+    // scheduling barriers keep them there, so that one wave per SIMD does not wait
+    // for LDS between MFMAs
+    auto frags = [&](int buf, int ks, bf16x8 (&a)[MI], bf16x8 (&b)[NJ]) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const int row = wr + i * 32 + li;
+            a[i] = lds_frag(&As[buf][row][swz(row, (ks + lk) >> 3) * 8]);
+        }
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int row = wc + j * 32 + li;
+            b[j] = lds_frag(&Bs[buf][row][swz(row, (ks + lk) >> 3) * 8]);
+        }
+    };
+    auto mfmas = [&](const bf16x8 (&a)[MI], const bf16x8 (&b)[NJ]) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    // 256-wide tiles have no registers to spare for a second fragment set: they
+    // read each sub-step's fragments right before its MFMAs
+    constexpr bool DB = BN < 256;
+    bf16x8 a0[MI], b0[NJ], a1[MI], b1[NJ];
     int cur = 0;
+    if (DB) frags(0, 0, a0, b0);
     for (int64_t k = k_lo; k < k_hi; k += BK) {
         const bool more = k + BK < k_hi;
-        if (more) st.template load<FULL>(g, r0, c0, k + BK, k_hi, tid);
+        if (more) st.template load<FULL, KF>(g, r0, c0, k + BK, k_hi, tid);
+        static_assert(BK == 64, "four sub-steps per step");
+        if constexpr (DB) {
+            frags(cur, 16, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            frags(cur, 32, a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            frags(cur, 48, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (more) st.store(As[cur ^ 1], Bs[cur ^ 1], tid);
+            mfmas(a1, b1);
+        } else {
 #pragma unroll
-        for (int ks = 0; ks < BK; ks += 16) {
-            bf16x8 a[MI], b[NJ];
-#pragma unroll
-            for (int i = 0; i < MI; ++i) {
-                const int row = wr + i * 32 + li;
-                a[i] = lds_frag(&As[cur][row][swz(row, (ks + lk) >> 3) * 8]);
+            for (int ks = 0; ks < BK; ks += 16) {
+                frags(cur, ks, a0, b0);
+                mfmas(a0, b0);
             }
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                const int row = wc + j * 32 + li;
-                b[j] = lds_frag(&Bs[cur][row][swz(row, (ks + lk) >> 3) * 8]);
-            }
-#pragma unroll
-            for (int i = 0; i < MI; ++i)
-#pragma unroll
-                for (int j = 0; j < NJ; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+            if (more) st.store(As[cur ^ 1], Bs[cur ^ 1], tid);
         }
-        if (more) st.store(As[cur ^ 1], Bs[cur ^ 1], tid);
         __syncthreads();
         cur ^= 1;
+        if (DB && more) frags(cur, 0, a0, b0);
     }
 }
 
-template <bool TR, int BM, int BN>
-__global__ __launch_bounds__(NT) void k_gemm(const GemmArgs g) {
-    constexpr int MI = BM / 128, NJ = BN / 64;  // 32x32 MFMA tiles per wave (4x2 waves)
+template <bool TR, int BM, int BN, int WM>
+__global__ __launch_bounds__(128 * WM) void k_gemm(const GemmArgs g) {
+    constexpr int NT = 128 * WM;  // WM x 2 waves
+    constexpr int MI = BM / (32 * WM), NJ = BN / 64;  // 32x32 MFMA tiles per wave
     __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDK];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][LDK];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * BN;
-    const int64_t r0 = static_cast<int64_t>(blockIdx.y) * BM;
+    // output tile: workgroups are dispatched to the XCDs in turn, so workgroup i
+    // takes tile (i % 8) * (tiles / 8) + i / 8 when the tile count allows it:
+    // the tiles of one XCD are consecutive in row-major order
+    const int ncb = static_cast<int>(gridDim.x);
+    const int ntl = ncb * static_cast<int>(gridDim.y);
+    const int lin = static_cast<int>(blockIdx.x) + ncb * static_cast<int>(blockIdx.y);
+    const int tile = (ntl % kXcds == 0) ? (lin % kXcds) * (ntl / kXcds) + lin / kXcds : lin;
+    const int64_t c0 = static_cast<int64_t>(tile % ncb) * BN;
+    const int64_t r0 = static_cast<int64_t>(tile / ncb) * BM;
     const int64_t k_lo = static_cast<int64_t>(blockIdx.z) * g.kper;
     const int64_t k_hi = min(g.Kr, k_lo + g.kper);
-    const int wr = (wave >> 1) * (BM / 4);
+    const int wr = (wave >> 1) * (BM / WM);
     const int wc = (wave & 1) * (BN / 2);
 
     f32x16 acc[MI][NJ];
@@ -227,14 +289,17 @@ __global__ __launch_bounds__(NT) void k_gemm(const GemmArgs g) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    const bool full = r0 + BM <= g.R && c0 + BN <= g.Cc && (k_hi - k_lo) % BK == 0;
-    if (full)
-        gemm_mainloop<TR, BM, BN, true, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
+    const bool full = r0 + BM <= g.R && c0 + BN <= g.Cc;
+    const bool kfull = (k_hi - k_lo) % BK == 0;
+    if (full && kfull)
+        gemm_mainloop<TR, BM, BN, NT, true, true, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
+    else if (full)
+        gemm_mainloop<TR, BM, BN, NT, true, false, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
     else
-        gemm_mainloop<TR, BM, BN, false, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
+        gemm_mainloop<TR, BM, BN, NT, false, false, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
 
     // acc element v of lane l is row 8*(v/4) + 4*(l/32) + v%4, col l%32 of its tile
-    float* __restrict__ dst = g.C + (g.direct ? 0 : static_cast<int64_t>(blockIdx.z) * g.R * g.Cc);
+    float* __restrict__ dst = g.C ? g.C + (g.direct ? 0 : static_cast<int64_t>(blockIdx.z) * g.R * g.Cc) : nullptr;
     const float* __restrict__ addp = g.direct ? g.add : nullptr;
     const bool accum = g.direct && g.accum;
     uint16_t* __restrict__ o16 = g.direct ? g.out16 : nullptr;
@@ -253,7 +318,7 @@ __global__ __launch_bounds__(NT) void k_gemm(const GemmArgs g) {
                 const int64_t o = row * g.Cc + col;
                 float e = 0.f;
                 if (addp && in) e = addp[o];
-                if (accum && in) e += dst[o];
+                if (accum && dst && in) e += dst[o];
                 extra[v] = e;
             }
 #pragma unroll
@@ -261,7 +326,7 @@ __global__ __launch_bounds__(NT) void k_gemm(const GemmArgs g) {
                 const int64_t row = rb + 8 * (v >> 2) + (v & 3);
                 if (row < g.R && col < g.Cc) {
                     const float val = acc[i][j][v] + extra[v];
-                    dst[row * g.Cc + col] = val;
+                    if (dst) dst[row * g.Cc + col] = val;
                     if (o16) o16[row * g.ld16 + col] = f2bf(val);
                 }
             }
@@ -292,7 +357,7 @@ struct Plan {
 };
 
 Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split) {
-    Plan best{256, 1};
+    Plan best{192, 1};
     double best_us = 1e300;
     const int bns[3] = {256, 192, 128};
     for (int bn : bns) {
@@ -315,8 +380,9 @@ Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split) {
 
 template <bool TR, int BN>
 void launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
+    constexpr int WM = 4;  // 4 x 2 waves, two per SIMD
     dim3 grid(cdiv(g.Cc, BN), cdiv(g.R, 256), static_cast<unsigned>(splits));
-    hipLaunchKernelGGL((k_gemm<TR, 256, BN>), grid, dim3(NT), 0, s, g);
+    hipLaunchKernelGGL((k_gemm<TR, 256, BN, WM>), grid, dim3(128 * WM), 0, s, g);
 }
 
 template <bool TR>

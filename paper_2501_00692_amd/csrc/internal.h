@@ -73,6 +73,7 @@ struct ScanProblem {
     int64_t ld_dz16;
     uint16_t* bc16;
     int64_t ld_bc16;
+    bool only16;    // with the copies: skip the fp32 ddelta and dz (not wanted by the caller)
     // workspace regions
     float* hbuf;    // [b][nc][N][D]
     float* hseg;    // [b][nc][L/seg][Dp][16]: state at each segment start from a zero chunk carry-in
@@ -115,7 +116,8 @@ hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, in
                           const uint16_t* dZ, int64_t lddz, float* dW, bool accum, void* ws,
                           hipStream_t s);
 // dX[M][K] (+)= dZ W^T with dZ [M][N] (lddz), W [K][N] (ldw); optional fp32 addend
-// add[M][K] (ld = K) and optional bf16 copy of the result into out16 (ld16).
+// add[M][K] (ld = K) and optional bf16 copy of the result into out16 (ld16); dX may
+// be NULL when out16 is given (only the copy is written).
 hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, int64_t lddz,
                           const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
                           uint16_t* out16, int64_t ld16, hipStream_t s);

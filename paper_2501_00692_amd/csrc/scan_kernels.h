@@ -16,6 +16,8 @@
 // dimension; B_t and C_t are the same for every channel.
 #pragma once
 
+#include <type_traits>
+
 #include "internal.h"
 
 namespace ssmk {
@@ -68,6 +70,12 @@ __device__ __forceinline__ float log1p_small(float e) {
 }
 __device__ __forceinline__ float softplus_f(float p) {
     return fmaxf(p, 0.f) + log1p_small(fexp(-fabsf(p)));
+}
+// softplus(p) where `on`, else p: evaluated on every lane and then selected, so
+// that no divergent branch splits the surrounding code into basic blocks
+__device__ __forceinline__ float softplus_sel(float p, bool on) {
+    const float sp = softplus_f(p);
+    return on ? sp : p;
 }
 __device__ __forceinline__ float sigmoid_f(float z) {
     return __builtin_amdgcn_rcpf(1.f + fexp(-z));
@@ -170,13 +178,16 @@ __device__ __forceinline__ double quad_bcast_d(double v, int src) {
 // Raw per-(step, channel) inputs of the steps a lane prepares for its quad, as
 // element bits: they are loaded a group or segment ahead and converted at their
 // first use, so that nothing waits for the loads before then.
-template <int SPL>
+template <typename TI, int SPL>
 struct RawIn {
-    uint32_t x[SPL], p[SPL], dy[SPL], z[SPL];
+    // element bits at their own width (16 for bf16: the conversion's shift then
+    // needs no zero-extension of a loaded register)
+    using Bits = typename std::conditional<sizeof(TI) == 2, uint16_t, uint32_t>::type;
+    Bits x[SPL], p[SPL], dy[SPL], z[SPL];
 };
 
 __device__ __forceinline__ uint32_t ldbits(const float* p, int64_t i) { return __float_as_uint(p[i]); }
-__device__ __forceinline__ uint32_t ldbits(const uint16_t* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ uint16_t ldbits(const uint16_t* p, int64_t i) { return p[i]; }
 // Value of element bits loaded by ldbits; 0 where the element is padding.
 template <typename TI>
 __device__ __forceinline__ float fin(uint32_t b, bool v) {
@@ -189,7 +200,7 @@ __device__ __forceinline__ float fin(uint32_t b, bool v) {
 // dy and z.
 template <typename TI, bool GATE, int SPL>
 __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64_t ts, int64_t d,
-                                         bool dv, int r, bool full, RawIn<SPL>& o) {
+                                         bool dv, int r, bool full, RawIn<TI, SPL>& o) {
     const TI* X = static_cast<const TI*>(p.x);
     const TI* DL = static_cast<const TI*>(p.delta);
     const TI* DY = static_cast<const TI*>(p.dy);
@@ -203,7 +214,7 @@ __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64
         o.p[jj] = ldbits(DL, td);
         if (full) {
             o.dy[jj] = ldbits(DY, td);
-            o.z[jj] = GATE ? ldbits(Z, td) : 0u;
+            o.z[jj] = GATE ? ldbits(Z, td) : 0;
         }
     }
 }
@@ -220,15 +231,18 @@ __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64
 // of Delta from the chunk start to the segment start (cseg): the fused gradient
 // kernel rebuilds its segment-start states from them and the chunk carry.
 // B and C are staged in LDS as fp32, 64 steps at a time, for the whole
-// workgroup.  Lane r prepares the per-channel quantities of steps s+r, s+r+4,
-// ... and broadcasts them to its quad; its raw inputs are loaded one 16-step
-// group ahead.
+// workgroup, double-buffered: the next block's loads are in flight while the
+// current block is processed, and one barrier per block publishes it.  Lane r
+// prepares the per-channel quantities of steps s+r, s+r+4, ... and broadcasts
+// them to its quad; its raw inputs are loaded two 4-step groups ahead, so a
+// whole group of arithmetic lies between the issue of a load and its use.
 // ---------------------------------------------------------------------------
 template <typename TI, bool SP, bool GATE, bool WANT_M, int SEG>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) void k_chunk_aggr(const ScanProblem p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_chunk_aggr(const ScanProblem p) {
     constexpr int SB = 64;  // steps per staged block
+    constexpr int PT = SB * 32 / 256;  // staged values per thread
     static_assert(SB % SEG == 0 && SEG % 4 == 0, "segments tile the staged blocks");
-    __shared__ __attribute__((aligned(16))) float bcs[SB][32];
+    __shared__ __attribute__((aligned(16))) float bcs[2][SB][32];
     const int tid = threadIdx.x;
     const int r = tid & 3;
     const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);  // < Dp
@@ -253,86 +267,106 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6, 8))) voi
     auto quad_total = [&]() {
         return ((quad_bcast_d(sd, 0) + quad_bcast_d(sd, 1)) + quad_bcast_d(sd, 2)) + quad_bcast_d(sd, 3);
     };
-    RawIn<1> nxt;  // raw inputs, loaded one group of 4 steps ahead
-    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, WANT_M, nxt);
-    for (int64_t sb = t0; sb < t1; sb += SB) {
-        {
-            // all of this thread's loads are issued before any is used
-            constexpr int PT = SB * 32 / 256;
-            float v[PT];
+    // B/C values of the staged block starting at step sb (padding and steps past
+    // the chunk read as 0)
+    float bcv[PT];
+    auto load_bc = [&](int64_t sb) {
 #pragma unroll
-            for (int e = 0; e < PT; ++e) {
-                const int i = tid + 256 * e;
-                const int t = i >> 5, cc = i & 31, n = cc & 15;
-                const int64_t tg = sb + t;
-                const bool want = cc < 16 || WANT_M;
-                v[e] = ldm(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, want && tg < t1 && n < p.N);
-            }
-            lds_barrier();  // the previous block has been consumed
-#pragma unroll
-            for (int e = 0; e < PT; ++e) {
-                const int i = tid + 256 * e;
-                bcs[i >> 5][i & 31] = v[e];
-            }
-            lds_barrier();
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + 256 * e;
+            const int t = i >> 5, cc = i & 31, n = cc & 15;
+            const int64_t tg = sb + t;
+            const bool want = cc < 16 || WANT_M;
+            bcv[e] = ldm(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, want && tg < t1 && n < p.N);
         }
-        const int64_t se = min(sb + SB, t1);
-        for (int64_t s0 = sb; s0 < se; s0 += 4) {
+    };
+    auto store_bc = [&](int buf) {
+#pragma unroll
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + 256 * e;
+            bcs[buf][i >> 5][i & 31] = bcv[e];
+        }
+    };
+    load_bc(t0);
+    store_bc(0);
+    load_bc(t0 + SB);  // block 1 (all padding when the chunk has one block)
+    // raw inputs of the next two groups of 4 steps, in two buffers used
+    // alternately (no copies of data still in flight)
+    RawIn<TI, 1> n1, n2;
+    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, WANT_M, n1);
+    load_raw<TI, GATE, 1>(p, bb, t0 + 4, d, dv, r, WANT_M, n2);
+    lds_barrier();
+    int buf = 0;
+    // One group of 4 steps from s0, its raw inputs in `nb`, which is then
+    // refilled with the group two ahead.  Steps past the end of the sequence have
+    // Delta = x = g = 0 and B = C = 0, so they leave h, P, m and the Delta sum
+    // unchanged; every group of the chunk runs (no tail branch).
+    auto group = [&](int64_t s0, int64_t sb, RawIn<TI, 1>& nb) {
+        if constexpr (WANT_M) {
+            const uint32_t tl = static_cast<uint32_t>(s0 - t0);
+            if (tl % SEG == 0) put_seg(tl / SEG, static_cast<float>(quad_total()));  // uniform
+        }
+        // this group's raw inputs are converted first, then `nb` is refilled: a
+        // register is only reloaded once its value has been used, so the
+        // compiler never copies a load that is still in flight
+        const bool v = dv && s0 + r < t1;
+        const float pr = fin<TI>(nb.p[0], v);
+        float xr = fin<TI>(nb.x[0], v);
+        const float dyr = WANT_M ? fin<TI>(nb.dy[0], v) : 0.f;
+        const float zr = (WANT_M && GATE) ? fin<TI>(nb.z[0], v) : 0.f;
+        // issued on every path (past the end it reloads valid data that is not
+        // used), so that later waits count exactly; the scheduling barrier keeps
+        // the loads ahead of this group's arithmetic
+        load_raw<TI, GATE, 1>(p, bb, s0 + 8, d, dv, r, WANT_M, nb);
+        __builtin_amdgcn_sched_barrier(0);
+        const float dlr = SP ? softplus_sel(pr, v) : pr;
+        if (p.bdelta) xr *= dlr;  // input term Delta B x
+        float gr = 0.f;
+        if constexpr (WANT_M) gr = GATE ? dyr * zr * sigmoid_f(zr) : dyr;
+        sd += static_cast<double>(dlr);
+        const int tb = static_cast<int>(s0 - sb);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float xv = quad_bcast(xr, j);
+            const float dl = quad_bcast(dlr, j);
+            const float4 b4 = *reinterpret_cast<const float4*>(&bcs[buf][tb + j][4 * r]);
+            const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
+            float Cv[4] = {0.f, 0.f, 0.f, 0.f};
             if constexpr (WANT_M) {
-                const uint32_t tl = static_cast<uint32_t>(s0 - t0);
-                if (tl % SEG == 0) put_seg(tl / SEG, static_cast<float>(quad_total()));  // uniform
+                const float4 c4 = *reinterpret_cast<const float4*>(&bcs[buf][tb + j][16 + 4 * r]);
+                Cv[0] = c4.x; Cv[1] = c4.y; Cv[2] = c4.z; Cv[3] = c4.w;
             }
-            {
-                const RawIn<1> cur = nxt;
-                // issued on every path (past the end it reloads valid data that is
-                // not used), so that later waits count exactly
-                load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, WANT_M, nxt);
-                const bool v = dv && s0 + r < t1;
-                const float pr = fin<TI>(cur.p[0], v);
-                const float dlr = (SP && v) ? softplus_f(pr) : pr;
-                float xr = fin<TI>(cur.x[0], v);
-                if (p.bdelta) xr *= dlr;  // input term Delta B x
-                float gr = 0.f;
+            const float g = WANT_M ? quad_bcast(gr, j) : 0.f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float av = fexp2(cn[k] * dl);
+                h[k] = fmaf(av, h[k], Bv[k] * xv);
                 if constexpr (WANT_M) {
-                    const float dyr = fin<TI>(cur.dy[0], v);
-                    if constexpr (GATE) {
-                        const float zr = fin<TI>(cur.z[0], v);
-                        gr = dyr * zr * sigmoid_f(zr);
-                    } else {
-                        gr = dyr;
-                    }
-                }
-                sd += static_cast<double>(dlr);
-                const int tb = static_cast<int>(s0 - sb);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const float xv = quad_bcast(xr, j);
-                    const float dl = quad_bcast(dlr, j);
-                    const float4 b4 = *reinterpret_cast<const float4*>(&bcs[tb + j][4 * r]);
-                    const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
-                    float Cv[4] = {0.f, 0.f, 0.f, 0.f};
-                    if constexpr (WANT_M) {
-                        const float4 c4 = *reinterpret_cast<const float4*>(&bcs[tb + j][16 + 4 * r]);
-                        Cv[0] = c4.x; Cv[1] = c4.y; Cv[2] = c4.z; Cv[3] = c4.w;
-                    }
-                    const float g = WANT_M ? quad_bcast(gr, j) : 0.f;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        const float av = fexp2(cn[k] * dl);
-                        h[k] = fmaf(av, h[k], Bv[k] * xv);
-                        if constexpr (WANT_M) {
-                            P[k] *= av;
-                            m[k] = fmaf(g * Cv[k], P[k], m[k]);
-                        }
-                    }
+                    P[k] *= av;
+                    m[k] = fmaf(g * Cv[k], P[k], m[k]);
                 }
             }
         }
+    };
+    for (int64_t sb = t0; sb < t1; sb += SB) {
+        // the block's groups, up to the chunk edge (L and SB are multiples of 8)
+        const int64_t se = min(sb + SB, t0 + p.L);
+        for (int64_t s0 = sb; s0 < se; s0 += 8) {
+            group(s0, sb, n1);
+            group(s0 + 4, sb, n2);
+        }
+        // publish the next block (its buffer was last read before the previous
+        // barrier) and start loading the one after it
+        store_bc(buf ^ 1);
+        load_bc(sb + 2 * SB);
+        lds_barrier();
+        buf ^= 1;
     }
     if constexpr (WANT_M) {
-        // segments that start at or after the end of the sequence hold the final state
+        // segments that start in a block past the end of the sequence hold the final state
         const float cum = static_cast<float>(quad_total());
-        for (uint32_t q = static_cast<uint32_t>((t1 - t0 + SEG - 1) / SEG); q < nseg; ++q) put_seg(q, cum);
+        const uint32_t done = static_cast<uint32_t>((t1 - t0 + SB - 1) / SB * SB / SEG);
+        for (uint32_t q = done; q < nseg; ++q) put_seg(q, cum);
     }
     // sum of Delta over the quad's prepared steps, in a fixed order
     const double s1 = __shfl_xor(sd, 1);
@@ -538,7 +572,7 @@ struct ChunkPtrs {
 // lanes whose step (tl >= lim) or channel is padding load element 0 instead.
 template <typename TI, bool GATE, int SPL>
 __device__ __forceinline__ void load_raw2(const ChunkPtrs<TI>& c, uint32_t D, uint32_t d, int tq,
-                                          int r, int64_t lim, bool dv, bool full, RawIn<SPL>& o) {
+                                          int r, int64_t lim, bool dv, bool full, RawIn<TI, SPL>& o) {
 #pragma unroll
     for (int jj = 0; jj < SPL; ++jj) {
         const int tl = tq + r + 4 * jj;
@@ -548,7 +582,7 @@ __device__ __forceinline__ void load_raw2(const ChunkPtrs<TI>& c, uint32_t D, ui
         o.p[jj] = ldbits(c.p, off);
         if (full) {
             o.dy[jj] = ldbits(c.dy, off);
-            o.z[jj] = GATE ? ldbits(c.z, off) : 0u;
+            o.z[jj] = GATE ? ldbits(c.z, off) : 0;
         }
     }
 }
@@ -586,7 +620,7 @@ __device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMI
 // in LDS, and the workgroup writes the accumulator once at the end (into dB/dC,
 // or into its split's partial when nsplit > 1).  All orders are fixed.
 // ---------------------------------------------------------------------------
-template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK, bool OUT16>
+template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK, int OUT>
 __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_grad(const ScanProblem p) {
     constexpr int NW = kGradWaves;
     constexpr int NTH = 64 * NW;
@@ -611,7 +645,9 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     float* dxo = p.dx + (bb * p.T + t0) * p.D;
     float* ddo = p.ddelta + (bb * p.T + t0) * p.D;
     float* dzo = GATE ? p.dz + (bb * p.T + t0) * p.D : nullptr;
-    // OUT16: also write the bf16 copies of ddelta and dz
+    // OUT 1: also write the bf16 copies of ddelta and dz; OUT 2: write only those
+    // copies (no fp32 ddelta and dz), for callers that do not want them
+    constexpr bool OUT16 = OUT > 0;
     uint16_t* dd16o = OUT16 ? p.dd16 + (bb * p.T + t0) * p.ld_dd16 : nullptr;
     uint16_t* dz16o = OUT16 ? p.dz16 + (bb * p.T + t0) * p.ld_dz16 : nullptr;
     const uint32_t ldd16 = static_cast<uint32_t>(p.ld_dd16), ldz16 = static_cast<uint32_t>(p.ld_dz16);
@@ -678,8 +714,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
         const uint32_t d32 = dv ? static_cast<uint32_t>(d) : 0u;
 
         // inputs of the last segment, for the reverse sweep
-        RawIn<SPL> nxt;
-        RawIn<SPL> nxs;  // raw inputs at the shifted positions (truncated mode)
+        RawIn<TI, SPL> nxt;
+        RawIn<TI, SPL> nxs;  // raw inputs at the shifted positions (truncated mode)
         load_raw2<TI, GATE, SPL>(cp, D32, d32, (NCK - 1) * S, r, lim, dv, true, nxt);
         if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (NCK - 1) * S, r, lims, dv, true, nxs);
 
@@ -758,8 +794,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 hq = *reinterpret_cast<const float4*>(p.hseg + (sgb + qn * p.Dp) * 16 + 4 * r);
                 cq = p.cseg[sgb + qn * p.Dp];
             }
-            const RawIn<SPL> cur = nxt;
-            RawIn<SPL> cus;
+            const RawIn<TI, SPL> cur = nxt;
+            RawIn<TI, SPL> cus;
             if constexpr (TRUNC) cus = nxs;
             {
                 // the next segment (segment 0 reloads itself; see the checkpoint sweep)
@@ -774,7 +810,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             for (int jj = 0; jj < SPL; ++jj) {
                 sv[jj] = dv && q * S + r + 4 * jj < lim;
                 const float pr = fin<TI>(cur.p[jj], sv[jj]), dyr = fin<TI>(cur.dy[jj], sv[jj]);
-                dls[jj] = (SP && sv[jj]) ? softplus_f(pr) : pr;
+                dls[jj] = SP ? softplus_sel(pr, sv[jj]) : pr;
                 xr[jj] = fin<TI>(cur.x[jj], sv[jj]);
                 xs[jj] = p.bdelta ? xr[jj] * dls[jj] : xr[jj];  // the input term is (Delta) B x
                 if constexpr (GATE) {
@@ -789,7 +825,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 if constexpr (TRUNC) {
                     const bool vs = dv && q * S + r + 4 * jj < lims;
                     const float psr = fin<TI>(cus.p[jj], vs), dysr = fin<TI>(cus.dy[jj], vs);
-                    dlps[jj] = (SP && vs) ? softplus_f(psr) : psr;
+                    dlps[jj] = SP ? softplus_sel(psr, vs) : psr;
                     if constexpr (GATE) {
                         const float zsr = fin<TI>(cus.z[jj], vs);
                         gps[jj] = dysr * zsr * sigmoid_f(zsr);
@@ -842,7 +878,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 for (int jj = 0; jj < SPL; ++jj) {
                     const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
                     const float v = gfs[jj] * yk[jj];
-                    *(sv[jj] ? dzo + (tl * D32 + d32) : sinkf) = v;
+                    if constexpr (OUT != 2) *(sv[jj] ? dzo + (tl * D32 + d32) : sinkf) = v;
                     if constexpr (OUT16) stf(sv[jj] ? dz16o + (tl * ldz16 + d32) : sink16, 0, v);
                 }
             }
@@ -910,7 +946,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 const float dd0 = p.bdelta ? fmaf(dxk[jj], xr[jj], ddk[jj]) : ddk[jj];
                 const float ddv = SP ? dd0 * (1.f - fexp(-dls[jj])) : dd0;  // d softplus / d Delta_pre
                 *(sv[jj] ? dxo + off : sinkf) = p.bdelta ? dxk[jj] * dls[jj] : dxk[jj];
-                *(sv[jj] ? ddo + off : sinkf) = ddv;
+                if constexpr (OUT != 2) *(sv[jj] ? ddo + off : sinkf) = ddv;
                 if constexpr (OUT16) stf(sv[jj] ? dd16o + (tl * ldd16 + d32) : sink16, 0, ddv);
             }
             flush(q, 0);
@@ -1012,12 +1048,16 @@ void grad_main(const ScanProblem& p, hipStream_t s) {
     SSMK_TIMED("grad_fused", s);
     // the bf16 copies exist for the whole-layer path (bf16 inputs, softplus, gate)
     if constexpr (sizeof(TI) == 2 && SP && GATE) {
+        if (p.dd16 && p.only16) {
+            hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK, 2>), g, dim3(64 * kGradWaves), 0, s, p);
+            return;
+        }
         if (p.dd16) {
-            hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK, true>), g, dim3(64 * kGradWaves), 0, s, p);
+            hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK, 1>), g, dim3(64 * kGradWaves), 0, s, p);
             return;
         }
     }
-    hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK, false>), g, dim3(64 * kGradWaves), 0, s, p);
+    hipLaunchKernelGGL((k_grad<TI, SP, GATE, TRUNC, N16, S, NCK, 0>), g, dim3(64 * kGradWaves), 0, s, p);
 }
 
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16>

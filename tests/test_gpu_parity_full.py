@@ -224,6 +224,9 @@ def test_proj_grad_slice_shapes_sampled():
     bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)
     Xb, Zb, Wb = bits(X), bits(dZ), bits(W)
     rep = {}
-    check("dW[sampled]", to_np(dW)[kk, jj], oracle.proj_dw(Xb, Zb, kk, jj), TOL_BF16, rep)
-    check("dX[rows]", to_np(dX[torch.as_tensor(rows, device="cuda")]), oracle.proj_dx(Zb, Wb, rows), TOL_BF16, rep)
+    # exact bf16 inputs on both sides: only fp32 accumulation differs, of relative
+    # order 2^-24 sqrt(n) for a reduction of n = 262,144 terms (about 3e-5 at worst)
+    tol = 1e-4
+    check("dW[sampled]", to_np(dW)[kk, jj], oracle.proj_dw(Xb, Zb, kk, jj), tol, rep)
+    check("dX[rows]", to_np(dX[torch.as_tensor(rows, device="cuda")]), oracle.proj_dx(Zb, Wb, rows), tol, rep)
     say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
