@@ -23,11 +23,11 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA
-# MI355X fp32 vector arithmetic: 256 CUs x 4 SIMDs x 16 lanes x 2 (FMA) x 2.4 GHz
-# = 78.6 TFLOP/s for ordinary VALU instructions.  The published 157.3 counts the
-# packed two-wide FMA, which this library's kernels are built without.
-FP32_VECTOR_PEAK_TFS = 78.6
-FP32_VECTOR_PACKED_PEAK_TFS = 157.3
+# MI355X fp32 vector arithmetic: 256 CUs x 4 SIMDs x 32 lanes per cycle x 2 (FMA)
+# x 2.4 GHz = 157.3 TFLOP/s.  On gfx950 an ordinary (non-packed) wave64 fp32
+# add, mul or FMA issues every 2 cycles per SIMD, so this peak needs no packed
+# instructions (which this library's kernels are built without).
+FP32_VECTOR_PEAK_TFS = 157.3
 
 
 def scan_flops_per_state_step(trunc):
@@ -40,9 +40,14 @@ def scan_flops_per_state_step(trunc):
     return 22 + (10 if trunc else 0)
 
 
-def scan_bytes_per_token(D, N, s, gate):
+def scan_bytes_per_token(D, N, s, gate, layer=False):
     """Compulsory HBM bytes per token of the scan gradient: every input read once
-    and every output written once at the ABI's dtypes (outputs fp32)."""
+    and every output written once at the ABI's dtypes (outputs fp32).  Inside the
+    whole-layer call with no scan outputs requested (``layer``), the kernel writes
+    dx in fp32 (the projection GEMM's addend) and dDelta_pre, dz, dB, dC as the
+    bf16 operands of the projection GEMMs, plus fp32 dB, dC."""
+    if layer:  # reads x, Delta_pre, dy, z; writes dx (fp32), dDelta_pre, dz (bf16)
+        return D * (4 * s + 4 + 2 + 2) + N * (2 * s + 8 + 4)
     if gate:  # reads x, Delta_pre, dy, z; writes dx, dDelta_pre, dz
         per_ch = 4 * s + 12
     else:     # reads x, Delta, dy; writes dx, dDelta
@@ -154,13 +159,13 @@ def roofline_for(kern, ktimes, w, kind):
     kt = ktimes[kern]
     s = 2 if w.bf16 else 4
     if kern == "grad_fused":
-        per_launch = scan_bytes_per_token(w.D, w.N, s, w.proj) * w.M  # bytes
+        layer = (kind[0] if isinstance(kind, tuple) else kind) == "layer"
+        per_launch = scan_bytes_per_token(w.D, w.N, s, w.proj, layer) * w.M  # bytes
         gbs = per_launch / (kt["avg_ms"] * 1e-3) / 1e9
         flops = scan_flops_per_state_step(0 < tbar_of(kind) < w.T) * w.M * w.D * w.N
         tfs = flops / (kt["avg_ms"] * 1e-3) / 1e12
         return {"kernel": kern, "bound": "alu", "achieved": tfs, "peak": FP32_VECTOR_PEAK_TFS, "unit": "TFLOP/s",
                 "frac": tfs / FP32_VECTOR_PEAK_TFS, "traffic": None, "avg_ms": kt["avg_ms"],
-                "frac_of_packed_peak": tfs / FP32_VECTOR_PACKED_PEAK_TFS,
                 "algorithmic_flops_per_launch": flops, "algorithmic_bytes_per_launch": per_launch,
                 "hbm_GBps_algorithmic": gbs, "hbm_frac_algorithmic": gbs / HBM_PEAK_GBS}
     if kern in ("gemm_dw", "gemm_dx"):
@@ -244,9 +249,12 @@ def main():
         roof["traffic"] = measured_traffic(dom, "layer-b2-T4096-D1536")
     value = w.M / (ms * 1e-3)
 
+    other = {k: roofline_for(k, ktimes, w, "layer") for k in ("grad_fused", "gemm_dw", "gemm_dx")
+             if k in ktimes and k != dom}
+    for k, r in other.items():
+        r["traffic"] = measured_traffic(k, "layer-b2-T4096-D1536")
     extra = {"kernels_layer": ktimes,
-             "roofline_other": {k: roofline_for(k, ktimes, w, "layer") for k in ("grad_fused", "gemm_dw", "gemm_dx")
-                                if k in ktimes and k != dom},
+             "roofline_other": other,
              "gemm_tflops_layer": layer_gemm_flops(w.M, w.D, w.N, w.d_model) / 1e12}
     del inp, step
     torch.cuda.empty_cache()
