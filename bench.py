@@ -109,8 +109,17 @@ def layer_step(w, inp, ssm, torch, tbar=0, b_delta=False):
     return step
 
 
-def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False):
-    """One scan gradient; ``inp["A_log"]`` of shape [D] selects the scalar-decay variant."""
+def vjp_pairs(T, tbar):
+    """(t, i) adjoint-state pairs of one sequence: T(T+1)/2 in full mode, else
+    tbar T - tbar (tbar - 1) / 2 (the paper's VJP counts, Sec. 4.3)."""
+    if tbar <= 0 or tbar >= T:
+        return T * (T + 1) // 2
+    return tbar * T - tbar * (tbar - 1) // 2
+
+
+def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False, pairs=False):
+    """One scan gradient; ``inp["A_log"]`` of shape [D] selects the scalar-decay variant;
+    ``pairs`` evaluates it by the explicit pair formulation instead of the adjoint scan."""
     b, T, D, N = w.b, w.T, w.D, w.N
     f32 = dict(dtype=torch.float32, device="cuda")
     out = {"dx": torch.empty(b, T, D, **f32), "ddelta": torch.empty(b, T, D, **f32),
@@ -120,11 +129,12 @@ def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False):
     if z is not None:
         out["dz"] = torch.empty(b, T, D, **f32)
     desc = ssm.make_desc(inp["x"], N, w.proj, z is not None, 0, inp["A_log"].dim() == 1, b_delta)
-    ws = torch.empty(ssm.grad_workspace_size(desc, tbar), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(ssm.grad_workspace_size(desc, tbar, pairs), dtype=torch.uint8, device="cuda")
+    fn = ssm.ssm_adjoint_grad_pairs if pairs else ssm.ssm_adjoint_grad
 
     def step():
-        ssm.ssm_adjoint_grad(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], z=z,
-                             softplus=w.proj, tbar=tbar, out=out, workspace=ws, b_delta=b_delta)
+        fn(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], z=z, softplus=w.proj, tbar=tbar,
+           out=out, workspace=ws, b_delta=b_delta)
     return step
 
 
@@ -265,21 +275,29 @@ def main():
         runs = [("small", "scan", 0, ""), ("small", "scan", 32, ""), ("long", "layer", 2048, ""),
                 ("long", "scan", 2048, ""), ("long_slow", "scan", 2048, ""), ("slice", "layer", 0, ""),
                 ("slice", "layer", 4096, ""), ("vlong", "scan", 8192, ""),
-                ("layer", "layer", 0, "scalarA+deltaB"), ("long", "scan", 2048, "scalarA+deltaB")]
+                ("layer", "layer", 0, "scalarA+deltaB"), ("long", "scan", 2048, "scalarA+deltaB"),
+                ("small", "pairs", 0, ""), ("small", "pairs", 32, ""), ("pairs", "pairs", 256, ""),
+                ("pairs", "scan", 256, "")]
         res = {}
         for name, kind, tbar, variant in runs:
             wl = WORKLOADS[name]
             x = make_inputs(wl, device="cuda")
             if variant:
                 x["A_log"] = x["A_log"][:, 0].contiguous()
-            st = (layer_step if kind == "layer" else scan_step)(wl, x, ssm, torch, tbar=tbar,
-                                                                b_delta=bool(variant))
+            if kind == "layer":
+                st = layer_step(wl, x, ssm, torch, tbar=tbar, b_delta=bool(variant))
+            else:
+                st = scan_step(wl, x, ssm, torch, tbar=tbar, b_delta=bool(variant), pairs=kind == "pairs")
             steps = 5 if wl.M >= 262144 else 10
             m = _timed(st, steps, 2, torch)
             kt = _kernel_times(st, 2, ssm, torch)
             entry = {"ms_per_step": m, "tokens_per_s": wl.M / (m * 1e-3), "tbar": tbar,
                      "grad_fused_avg_ms": kt.get("grad_fused", {}).get("avg_ms")}
-            r = None if variant else roofline_for("grad_fused", kt, wl, (kind, tbar))
+            if kind == "pairs":
+                # the paper's unit of work: one (t, i) adjoint state over all D x N states
+                entry["vjp_pairs_per_s"] = wl.b * vjp_pairs(wl.T, tbar) / (m * 1e-3)
+                entry["pairs_kernel_avg_ms"] = kt.get("pairs", {}).get("avg_ms")
+            r = None if (variant or kind == "pairs") else roofline_for("grad_fused", kt, wl, (kind, tbar))
             if r:
                 entry["grad_fused_TFLOPs"] = r["achieved"]
                 entry["grad_fused_alu_frac"] = r["frac"]

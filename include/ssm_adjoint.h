@@ -126,6 +126,24 @@ ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, co
                             float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
                             float* dh0, void* workspace, size_t workspace_bytes, void* stream);
 
+/* The same gradient as ssm_adjoint_grad (identical arguments, layouts, outputs
+ * and error behaviour), evaluated by the explicit pair formulation of Prop. 2 and
+ * Eq. "capped": for every step i and every loss term t in its window
+ * (i <= t < i + tbar, all t >= i in full mode) the adjoint state
+ * lambda^{t,i} = g_t C_t prod_{j=i+1}^{t} a_j is built as a running product (the
+ * zeta products of Alg. 2) and its vector-Jacobian products are accumulated, as
+ * in the paper's count of independent VJPs (Sec. 4.3): the work grows as
+ * b (tbar T - tbar (tbar-1)/2) D N, or b T (T+1)/2 D N in full mode, instead of
+ * b T D N for ssm_adjoint_grad.  dh0 (full mode) is the sum over the pairs
+ * (t, -1).  Results agree with ssm_adjoint_grad up to fp32 rounding. */
+ssm_status ssm_adjoint_grad_pairs_workspace_size(const ssm_desc* desc, int32_t mode, int64_t tbar,
+                                                 size_t* bytes);
+ssm_status ssm_adjoint_grad_pairs(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
+                                  const void* delta, const float* A_log, const void* B, const void* C,
+                                  const float* h0, const void* z, const void* dy, float* dx,
+                                  float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
+                                  float* dh0, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Projection gradients of a linear map Z = X W (Sec. 4.5: the A, B, C networks
  * are single-layer maps; the per-step vjps summed over t give these products):
  *   dW [K][Nout] (fp32)  = X^T dZ      (skipped if dW == NULL)

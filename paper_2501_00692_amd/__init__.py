@@ -9,7 +9,8 @@ other implementation behind this module, and it raises if the library is not
 built.
 
 Entry points (names as in the C ABI): :func:`ssm_adjoint_forward`,
-:func:`ssm_adjoint_grad`, :func:`ssm_proj_grad`, :func:`ssm_layer_grad`.
+:func:`ssm_adjoint_grad`, :func:`ssm_adjoint_grad_pairs`, :func:`ssm_proj_grad`,
+:func:`ssm_layer_grad`.
 """
 from __future__ import annotations
 
@@ -31,7 +32,8 @@ STATUS = {0: "SSM_OK", 1: "SSM_ERR_NULL", 2: "SSM_ERR_SHAPE", 3: "SSM_ERR_DTYPE"
 
 EXPORTED = (
     "ssm_adjoint_forward_workspace_size", "ssm_adjoint_grad_workspace_size", "ssm_adjoint_forward",
-    "ssm_adjoint_grad", "ssm_proj_grad_workspace_size", "ssm_proj_grad",
+    "ssm_adjoint_grad", "ssm_adjoint_grad_pairs_workspace_size", "ssm_adjoint_grad_pairs",
+    "ssm_proj_grad_workspace_size", "ssm_proj_grad",
     "ssm_layer_grad_workspace_size", "ssm_layer_grad", "ssm_timing_enable", "ssm_timing_summary",
     "ssm_last_error",
 )
@@ -69,6 +71,8 @@ def load_library():
         "ssm_adjoint_grad_workspace_size": [dp, i32, i64, szp],
         "ssm_adjoint_forward": [dp] + [vp] * 9 + [vp, sz, vp],
         "ssm_adjoint_grad": [dp, i32, i64] + [vp] * 15 + [vp, sz, vp],
+        "ssm_adjoint_grad_pairs_workspace_size": [dp, i32, i64, szp],
+        "ssm_adjoint_grad_pairs": [dp, i32, i64] + [vp] * 15 + [vp, sz, vp],
         "ssm_proj_grad_workspace_size": [i64, i64, i64, u32, szp],
         "ssm_proj_grad": [i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, vp, u32, vp, sz, vp],
         "ssm_layer_grad_workspace_size": [dp, i32, i64, i64, szp],
@@ -166,11 +170,11 @@ def _workspace(nbytes: int, device) -> torch.Tensor:
     return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
 
 
-def grad_workspace_size(desc: SsmDesc, tbar: int = 0) -> int:
+def grad_workspace_size(desc: SsmDesc, tbar: int = 0, pairs: bool = False) -> int:
     n = ctypes.c_size_t()
     mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
-    _check(load_library().ssm_adjoint_grad_workspace_size(ctypes.byref(desc), mode, int(tbar), ctypes.byref(n)),
-           "ssm_adjoint_grad_workspace_size")
+    name = "ssm_adjoint_grad_pairs_workspace_size" if pairs else "ssm_adjoint_grad_workspace_size"
+    _check(getattr(load_library(), name)(ctypes.byref(desc), mode, int(tbar), ctypes.byref(n)), name)
     return n.value
 
 
@@ -210,6 +214,21 @@ def ssm_adjoint_grad(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False,
 
     Returns a dict with fp32 ``dx, ddelta, dA_log, dB, dC`` (+ ``dz`` with a gate,
     ``dh0`` if asked).  ``out`` may hold preallocated outputs under the same keys."""
+    return _adjoint_grad(False, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk, want_dh0, out, workspace,
+                         b_delta)
+
+
+def ssm_adjoint_grad_pairs(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False, tbar=0, chunk=0,
+                           want_dh0=False, out=None, workspace=None, b_delta=False):
+    """The same gradient as :func:`ssm_adjoint_grad`, evaluated by the explicit
+    pair formulation (every adjoint state of the window formed and its VJPs
+    accumulated); arguments and results as there."""
+    return _adjoint_grad(True, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk, want_dh0, out, workspace,
+                         b_delta)
+
+
+def _adjoint_grad(pairs, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk, want_dh0, out, workspace,
+                  b_delta):
     lib = load_library()
     dt = x.dtype
     b, T, D = x.shape
@@ -236,11 +255,11 @@ def ssm_adjoint_grad(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False,
         o.setdefault("dz", torch.empty(b, T, D, **f32))
     if want_dh0:
         o.setdefault("dh0", torch.empty(b, D, N, **f32))
-    ws = workspace if workspace is not None else _workspace(grad_workspace_size(desc, tbar), dev)
-    _check(lib.ssm_adjoint_grad(ctypes.byref(desc), mode, int(tbar), _p(x), _p(delta), _p(A_log), _p(B), _p(C),
-                                _p(h0), _p(z), _p(dy), _p(o["dx"]), _p(o["ddelta"]), _p(o["dA_log"]), _p(o["dB"]),
-                                _p(o["dC"]), _p(o.get("dz")), _p(o.get("dh0")), _p(ws), ws.numel(), _stream()),
-           "ssm_adjoint_grad")
+    ws = workspace if workspace is not None else _workspace(grad_workspace_size(desc, tbar, pairs), dev)
+    name = "ssm_adjoint_grad_pairs" if pairs else "ssm_adjoint_grad"
+    _check(getattr(lib, name)(ctypes.byref(desc), mode, int(tbar), _p(x), _p(delta), _p(A_log), _p(B), _p(C),
+                              _p(h0), _p(z), _p(dy), _p(o["dx"]), _p(o["ddelta"]), _p(o["dA_log"]), _p(o["dB"]),
+                              _p(o["dC"]), _p(o.get("dz")), _p(o.get("dh0")), _p(ws), ws.numel(), _stream()), name)
     return o
 
 

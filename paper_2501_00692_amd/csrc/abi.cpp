@@ -290,6 +290,58 @@ ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, co
     return SSM_OK;
 }
 
+// Limits of the pair formulation: its channel blocks form a grid dimension, and
+// its workspace holds the summed adjoint states of every (step, channel).
+static ssm_status check_pairs(const ssm_desc* d) {
+    if ((d->channels + 63) / 64 > kMaxGridYZ)
+        return fail(SSM_ERR_UNSUPPORTED, "channels (%lld) exceed the pair kernel's launch grid",
+                    (long long)d->channels);
+    if (d->batch * d->seqlen * d->channels > (int64_t(1) << 40))
+        return fail(SSM_ERR_UNSUPPORTED, "batch * seqlen * channels too large for the pair workspace");
+    return SSM_OK;
+}
+
+ssm_status ssm_adjoint_grad_pairs_workspace_size(const ssm_desc* desc, int32_t mode, int64_t tbar,
+                                                 size_t* bytes) {
+    int64_t L, nc;
+    ssm_status st = check_desc(desc, &L, &nc);
+    if (st) return st;
+    st = check_pairs(desc);
+    if (st) return st;
+    bool trunc;
+    st = check_mode(desc, mode, tbar, &trunc);
+    if (st) return st;
+    if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");
+    *bytes = ssmk::pairs_workspace(desc->batch, desc->seqlen, desc->channels, desc->dstate, L).total;
+    return SSM_OK;
+}
+
+ssm_status ssm_adjoint_grad_pairs(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
+                                  const void* delta, const float* A_log, const void* B, const void* C,
+                                  const float* h0, const void* z, const void* dy, float* dx,
+                                  float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
+                                  float* dh0, void* workspace, size_t workspace_bytes, void* stream) {
+    int64_t L, nc;
+    bool trunc;
+    ssm_status st = grad_validate(desc, mode, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta,
+                                  dA_log, dB, dC, dz, dh0, &L, &nc, &trunc);
+    if (st) return st;
+    st = check_pairs(desc);
+    if (st) return st;
+    ssmk::PairsWorkspace w = ssmk::pairs_workspace(desc->batch, desc->seqlen, desc->channels,
+                                                   desc->dstate, L);
+    st = check_workspace(workspace, workspace_bytes, w.total);
+    if (st) return st;
+    ssmk::ScanProblem p = make_problem(desc, L, nc);
+    p.trunc = trunc;
+    p.tbar = trunc ? tbar : 0;
+    grad_bind(p, x, delta, A_log, B, C, h0, z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0);
+    hipError_t e = ssmk::launch_grad_pairs(p, workspace, w, trunc ? tbar : desc->seqlen,
+                                           static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "ssm_adjoint_grad_pairs launch");
+    return SSM_OK;
+}
+
 ssm_status ssm_proj_grad_workspace_size(int64_t M, int64_t K, int64_t Nout, uint32_t flags,
                                         size_t* bytes) {
     if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");

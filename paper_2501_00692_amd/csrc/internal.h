@@ -109,6 +109,14 @@ void bind_workspace(ScanProblem& p, void* ws, const ScanWorkspace& w);
 hipError_t launch_forward(const ScanProblem& p, hipStream_t s);
 hipError_t launch_grad(const ScanProblem& p, hipStream_t s);
 
+// The gradient by the explicit pair formulation (pairs.hip): workspace layout and
+// launch; W is the window (tbar, or T for the full gradient).
+struct PairsWorkspace {
+    size_t off_hbuf, off_sdel, off_dl, off_g, off_mu, off_pB, off_pC, off_dAtmp, total;
+};
+PairsWorkspace pairs_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t L);
+hipError_t launch_grad_pairs(ScanProblem& p, void* ws, const PairsWorkspace& w, int64_t W, hipStream_t s);
+
 // bf16 MFMA GEMMs (gemm.hip).
 // dW[K][N] (+)= X^T dZ with X [M][K] (ldx), dZ [M][N] (lddz).
 size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N);

@@ -1,0 +1,295 @@
+// pairs.hip -- the per-layer adjoint gradient by the explicit pair formulation of
+// Prop. 2 and Eq. "capped": every adjoint state
+//     lambda^{t,i}[d,n] = g_t[d] C_t[n] prod_{j=i+1}^{t} a_j[d,n]
+// for the pairs (t, i) of the window (i <= t < i + tbar, or every t >= i in full
+// mode) is formed as a running product over t (the zeta products of Alg. 2) and
+// its vector-Jacobian products are accumulated into step i.  No reverse
+// recurrence and no tail identity are used, so the work is
+// O(b * (tbar T - tbar (tbar - 1) / 2) * D * N) -- the paper's count of
+// independent VJPs -- against O(b T D N) for the adjoint scan of the fused
+// gradient kernel.  The results equal those of ssm_adjoint_grad up to rounding.
+//
+// Kernels:
+//   k_pairs_pre : Delta (softplus of Delta_pre when asked) and g (the upstream
+//                 gradient through the SiLU gate) per (step, channel), fp32;
+//   k_chunk_aggr, k_carry (scan_kernels.h): the state carried into every chunk;
+//   k_pairs     : one lane per (step i, channel), all pairs (t, i) of the window:
+//                 the sum over t of lambda^{t,i} for the channel's states, into
+//                 a [b][T][D][16] buffer (pairs of different i are independent);
+//   k_pairs_epi : one lane per channel with its states in registers, the steps
+//                 of one chunk in order: the forward state from the chunk's
+//                 carry, the vjp epilogue with the summed lambda, per-block
+//                 channel sums of dB, dC, and dL/dh0 from the pairs (t, -1);
+//   k_reduce_bc, k_reduce_da1, k_reduce_da2 (scan_kernels.h): fixed-order sums.
+#include "scan_kernels.h"
+
+namespace ssmk {
+namespace {
+
+constexpr int kPairLanes = 64;  // channels per block (one wave)
+
+// Delta and g per (step, channel) into dl / g ([b][T][D] fp32).
+template <typename TI, bool SP, bool GATE>
+__global__ __launch_bounds__(256) void k_pairs_pre(const ScanProblem p, float* dl, float* g) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= p.nb * p.T * p.D) return;
+    const float pr = ldf(static_cast<const TI*>(p.delta), i);
+    dl[i] = SP ? softplus_f(pr) : pr;
+    const float dy = ldf(static_cast<const TI*>(p.dy), i);
+    if constexpr (GATE) {
+        const float zv = ldf(static_cast<const TI*>(p.z), i);
+        g[i] = dy * zv * sigmoid_f(zv);
+    } else {
+        g[i] = dy;
+    }
+}
+
+// grid (T, ceil(D/64), b), 64 threads: lane = channel d of step i = blockIdx.x.
+// mu[((b T + i) D + d) 16 + n] = sum_{t=i}^{min(T, i+W)-1} g_t C_t[n] P(i, t) with
+// P(i, i) = 1 and P(i, t) = P(i, t-1) a_t, built as the running product.
+template <typename TI>
+__global__ __launch_bounds__(kPairLanes) void k_pairs(const ScanProblem p, const float* dlv,
+                                                       const float* gv, float* mu, int64_t W) {
+    const int lane = threadIdx.x;
+    const int64_t d = static_cast<int64_t>(blockIdx.y) * kPairLanes + lane;
+    const int64_t i = blockIdx.x, bb = blockIdx.z;
+    if (d >= p.D) return;
+    const TI* Cp = static_cast<const TI*>(p.C);
+    float cn[16], P[16], m[16];
+#pragma unroll
+    for (int n = 0; n < 16; ++n) {
+        const bool nv = n < p.N;
+        const float al = nv ? p.A_log[p.ascalar ? d : d * p.N + n] : 0.f;
+        cn[n] = nv ? -__expf(al) * kLog2e : 0.f;
+        P[n] = 1.f;
+        m[n] = 0.f;
+    }
+    const int64_t rowb = bb * p.T;
+    const int64_t te = min(p.T, i + W);
+    for (int64_t t = i; t < te; ++t) {
+        const int64_t td = (rowb + t) * p.D + d;
+        const float gt = gv[td];
+        float Ct[16];
+        ld_row16(Cp, rowb + t, p.N, Ct);
+        if (t > i) {
+            const float dlt = dlv[td];
+#pragma unroll
+            for (int n = 0; n < 16; ++n) P[n] *= fexp2(cn[n] * dlt);
+        }
+#pragma unroll
+        for (int n = 0; n < 16; ++n) m[n] = fmaf(gt * Ct[n], P[n], m[n]);
+    }
+    float4* o = reinterpret_cast<float4*>(mu + ((rowb + i) * p.D + d) * 16);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = make_float4(m[4 * q], m[4 * q + 1], m[4 * q + 2], m[4 * q + 3]);
+}
+
+// grid (ceil(D/64), nc, b), 64 threads.  hbuf holds the state carried into each
+// chunk on entry and receives the chunk's dA_log partial (dA * wn) on exit, at
+// the same index.
+template <typename TI, bool SP, bool GATE>
+__global__ __launch_bounds__(kPairLanes) void k_pairs_epi(const ScanProblem p, const float* dlv,
+                                                           const float* gv, const float* mu) {
+    __shared__ float red[kPairLanes][33];
+    const int lane = threadIdx.x;
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * kPairLanes + lane;
+    const int64_t c = blockIdx.y, bb = blockIdx.z;
+    const bool dv = d < p.D;
+    const int64_t dd = dv ? d : 0;  // padding lanes read channel 0 and write nothing
+    const TI* X = static_cast<const TI*>(p.x);
+    const TI* DY = static_cast<const TI*>(p.dy);
+    const TI* Z = static_cast<const TI*>(p.z);
+    const TI* Bp = static_cast<const TI*>(p.B);
+    const TI* Cp = static_cast<const TI*>(p.C);
+    float cn[16], wn[16], h[16], dA[16];
+    const int64_t cb = ((bb * p.nc + c) * p.N) * p.D + dd;
+#pragma unroll
+    for (int n = 0; n < 16; ++n) {
+        const bool nv = n < p.N;
+        const float al = nv ? p.A_log[p.ascalar ? dd : dd * p.N + n] : 0.f;
+        const float e = nv ? __expf(al) : 0.f;
+        wn[n] = -e;
+        cn[n] = -e * kLog2e;
+        h[n] = nv ? p.hbuf[cb + n * p.D] : 0.f;
+        dA[n] = 0.f;
+    }
+    const int64_t rowb = bb * p.T;  // first row of this batch entry
+    // dL/dh0 (full gradient): the pairs (t, -1), P(-1, t) = prod_{j=0}^{t} a_j
+    if (p.dh0 && c == 0) {
+        float P[16], m[16];
+#pragma unroll
+        for (int n = 0; n < 16; ++n) {
+            P[n] = 1.f;
+            m[n] = 0.f;
+        }
+        for (int64_t t = 0; t < p.T; ++t) {
+            const int64_t td = (rowb + t) * p.D + dd;
+            const float gt = gv[td], dlt = dlv[td];
+            float Ct[16];
+            ld_row16(Cp, rowb + t, p.N, Ct);
+#pragma unroll
+            for (int n = 0; n < 16; ++n) {
+                P[n] *= fexp2(cn[n] * dlt);
+                m[n] = fmaf(gt * Ct[n], P[n], m[n]);
+            }
+        }
+        if (dv)
+            for (int n = 0; n < p.N; ++n) p.dh0[(bb * p.D + d) * p.N + n] = m[n];
+    }
+    const int64_t t0 = c * p.L, t1 = min(t0 + p.L, p.T);
+    const int64_t bsz = p.nb * p.T * p.N;
+    float* pB = p.pB + static_cast<int64_t>(blockIdx.x) * bsz;
+    float* pC = p.pC + static_cast<int64_t>(blockIdx.x) * bsz;
+    for (int64_t i = t0; i < t1; ++i) {
+        const int64_t td = (rowb + i) * p.D + dd;
+        const float dl = dlv[td], g = gv[td];
+        const float xr = ldf(X, td);
+        const float xs = p.bdelta ? xr * dl : xr;  // the input term is (Delta) B x
+        float Bi[16], Ci[16], lam[16];
+        ld_row16(Bp, rowb + i, p.N, Bi);
+        ld_row16(Cp, rowb + i, p.N, Ci);
+        const float4* mi = reinterpret_cast<const float4*>(mu + td * 16);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 v = mi[q];
+            lam[4 * q] = v.x; lam[4 * q + 1] = v.y; lam[4 * q + 2] = v.z; lam[4 * q + 3] = v.w;
+        }
+        float ah[16], y = 0.f;
+#pragma unroll
+        for (int n = 0; n < 16; ++n) {
+            ah[n] = fexp2(cn[n] * dl) * h[n];  // a_i h_{i-1}
+            h[n] = fmaf(Bi[n], xs, ah[n]);
+            y = fmaf(Ci[n], h[n], y);
+        }
+        float dxp = 0.f, ddp = 0.f;
+#pragma unroll
+        for (int n = 0; n < 16; ++n) {
+            dxp = fmaf(lam[n], Bi[n], dxp);
+            const float s = lam[n] * ah[n];
+            ddp = fmaf(s, wn[n], ddp);
+            dA[n] = fmaf(s, dl, dA[n]);
+            red[lane][n] = dv ? lam[n] * xs : 0.f;      // dB_i[n] over channels
+            red[lane][16 + n] = dv ? g * h[n] : 0.f;    // dC_i[n] over channels
+        }
+        // with the Delta-scaled input, dx' = sum_n lambda B gives dx = dx' Delta and
+        // adds dx' x to dDelta
+        const float dd0 = p.bdelta ? fmaf(dxp, xr, ddp) : ddp;
+        if (dv) {
+            p.dx[td] = p.bdelta ? dxp * dl : dxp;
+            p.ddelta[td] = SP ? dd0 * (1.f - fexp(-dl)) : dd0;  // d softplus / d Delta_pre
+            if constexpr (GATE) {
+                const float zv = ldf(Z, td);
+                const float sg = sigmoid_f(zv);
+                p.dz[td] = ldf(DY, td) * sg * (1.f + zv * (1.f - sg)) * y;
+            }
+        }
+        __syncthreads();
+        if (lane < 32 && (lane & 15) < p.N) {
+            float sum = 0.f;
+            for (int l = 0; l < kPairLanes; ++l) sum += red[l][lane];
+            (lane < 16 ? pB : pC)[(rowb + i) * p.N + (lane & 15)] = sum;
+        }
+        __syncthreads();
+    }
+    if (dv)
+        for (int n = 0; n < p.N; ++n) p.hbuf[cb + n * p.D] = dA[n] * wn[n];
+}
+
+template <typename TI, bool SP, bool GATE>
+hipError_t pairs_impl(const ScanProblem& p, float* dl, float* g, float* mu, int64_t W, hipStream_t s) {
+    const int64_t MD = p.nb * p.T * p.D;
+    {
+        SSMK_TIMED("pairs_pre", s);
+        hipLaunchKernelGGL((k_pairs_pre<TI, SP, GATE>), dim3(cdiv(MD, 256)), dim3(256), 0, s, p, dl, g);
+    }
+    {
+        SSMK_TIMED("chunk_aggr", s);
+        dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
+        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, 8>), g4, dim3(256), 0, s, p);
+    }
+    {
+        SSMK_TIMED("carry", s);
+        hipLaunchKernelGGL(k_carry, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N), static_cast<unsigned>(2 * p.nb)),
+                           dim3(256), 0, s, p);
+    }
+    {
+        SSMK_TIMED("pairs", s);
+        dim3 gp(static_cast<unsigned>(p.T), cdiv(p.D, kPairLanes), static_cast<unsigned>(p.nb));
+        hipLaunchKernelGGL((k_pairs<TI>), gp, dim3(kPairLanes), 0, s, p, dl, g, mu, W);
+    }
+    {
+        SSMK_TIMED("pairs_epilogue", s);
+        dim3 ge(cdiv(p.D, kPairLanes), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
+        hipLaunchKernelGGL((k_pairs_epi<TI, SP, GATE>), ge, dim3(kPairLanes), 0, s, p, dl, g, mu);
+    }
+    SSMK_TIMED("reduce", s);
+    hipLaunchKernelGGL(k_reduce_bc, dim3(cdiv(p.nb * p.T * p.N, 256)), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_reduce_da1, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N), static_cast<unsigned>(p.nslice)),
+                       dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_reduce_da2, dim3(cdiv(p.D * p.N, 256)), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+template <typename TI>
+hipError_t pairs_sel(const ScanProblem& p, float* dl, float* g, float* mu, int64_t W, hipStream_t s) {
+    if (p.softplus) {
+        if (p.gate) return pairs_impl<TI, true, true>(p, dl, g, mu, W, s);
+        return pairs_impl<TI, true, false>(p, dl, g, mu, W, s);
+    }
+    if (p.gate) return pairs_impl<TI, false, true>(p, dl, g, mu, W, s);
+    return pairs_impl<TI, false, false>(p, dl, g, mu, W, s);
+}
+
+size_t up256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+}  // namespace
+
+PairsWorkspace pairs_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t L) {
+    PairsWorkspace w{};
+    const int64_t nc = (T + L - 1) / L;
+    const int64_t nblk = (D + kPairLanes - 1) / kPairLanes;
+    size_t off = 0;
+    w.off_hbuf = off;
+    off = up256(off + static_cast<size_t>(nb * nc * N * D) * sizeof(float));
+    w.off_sdel = off;
+    off = up256(off + static_cast<size_t>(nb * nc * D) * sizeof(double));
+    w.off_dl = off;
+    off = up256(off + static_cast<size_t>(nb * T * D) * sizeof(float));
+    w.off_g = off;
+    off = up256(off + static_cast<size_t>(nb * T * D) * sizeof(float));
+    w.off_mu = off;
+    off = up256(off + static_cast<size_t>(nb * T * D * 16) * sizeof(float));
+    w.off_pB = off;
+    off = up256(off + static_cast<size_t>(nblk * nb * T * N) * sizeof(float));
+    w.off_pC = off;
+    off = up256(off + static_cast<size_t>(nblk * nb * T * N) * sizeof(float));
+    w.off_dAtmp = off;
+    off = up256(off + static_cast<size_t>(choose_nslice(nb, nc)) * N * D * sizeof(float));
+    w.total = off;
+    return w;
+}
+
+hipError_t launch_grad_pairs(ScanProblem& p, void* ws, const PairsWorkspace& w, int64_t W, hipStream_t s) {
+    char* b = static_cast<char*>(ws);
+    p.hbuf = reinterpret_cast<float*>(b + w.off_hbuf);
+    p.mbuf = nullptr;
+    p.hseg = nullptr;
+    p.cseg = nullptr;
+    p.sdel = reinterpret_cast<double*>(b + w.off_sdel);
+    p.psum = nullptr;
+    p.pB = reinterpret_cast<float*>(b + w.off_pB);
+    p.pC = reinterpret_cast<float*>(b + w.off_pC);
+    p.dAtmp = reinterpret_cast<float*>(b + w.off_dAtmp);
+    p.sink = nullptr;
+    p.nsplit = static_cast<int>((p.D + kPairLanes - 1) / kPairLanes);
+    p.nslice = choose_nslice(p.nb, p.nc);
+    p.Dp = padded_channels(p.D);
+    p.seg = grad_segment(p.L);
+    p.dd16 = p.dz16 = p.bc16 = nullptr;
+    float* dl = reinterpret_cast<float*>(b + w.off_dl);
+    float* g = reinterpret_cast<float*>(b + w.off_g);
+    float* mu = reinterpret_cast<float*>(b + w.off_mu);
+    return p.bf16 ? pairs_sel<uint16_t>(p, dl, g, mu, W, s) : pairs_sel<float>(p, dl, g, mu, W, s);
+}
+
+}  // namespace ssmk

@@ -15,6 +15,7 @@ layer    2     4,096      1536   16  768      --     yes    bf16
 long     2     65,536     1536   16  768      2048   yes    bf16
 slice    1     262,144    4096   16  2048     4096   yes    bf16
 vlong    1     1,048,576  3072   16  --       8192   no     bf16
+pairs    2     4,096      1536   16  --       256    no     bf16
 =======  ====  =========  =====  ==  =======  =====  =====  ========
 
 Distributions: x ~ N(0,1); Delta = softplus(N(0,1)) (drawn as Delta_pre ~ N(0,1)
@@ -63,6 +64,8 @@ WORKLOADS = {
     "slice": Workload("slice", 1, 262144, 4096, 16, 2048, 4096, True, True, 692003),
     "vlong": Workload("vlong", 1, 1048576, 3072, 16, 1536, 8192, False, True, 692004),
 }
+# the explicit pair formulation's workload: the layer's scan shape with a 256-step window
+WORKLOADS["pairs"] = Workload("pairs", 2, 4096, 1536, 16, 768, 256, False, True, 692005)
 WORKLOADS["small_slow"] = WORKLOADS["small"].with_(name="small_slow", delta_scale=1.0 / 32)
 WORKLOADS["long_slow"] = WORKLOADS["long"].with_(name="long_slow", proj=False, delta_scale=1.0 / 2048)
 

@@ -35,6 +35,12 @@ def test_library_exports_every_declared_symbol(lib):
         assert hasattr(lib, name), name
 
 
+def test_binding_declares_every_signature(lib):
+    # without argtypes ctypes would pass 64-bit sizes as C ints
+    for name in ssm.EXPORTED:
+        assert getattr(lib, name).argtypes is not None, name
+
+
 def desc(**kw):
     d = dict(batch=1, seqlen=256, channels=64, dstate=16, chunk=0, in_dtype=ssm.SSM_F32, flags=0)
     d.update(kw)
@@ -46,40 +52,48 @@ MISALIGNED = ctypes.c_void_p(0x100004)
 
 
 def grad_call(lib, dsc, mode=ssm.SSM_FULL, tbar=0, x=FAKE, dh0=None, z=None, dz=None, ws=FAKE,
-              ws_bytes=1 << 40):
-    return lib.ssm_adjoint_grad(ctypes.byref(dsc) if dsc is not None else None, mode, tbar, x, FAKE, FAKE, FAKE,
-                                FAKE, None, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, dz, dh0, ws, ws_bytes, None)
+              ws_bytes=1 << 40, entry="ssm_adjoint_grad"):
+    return getattr(lib, entry)(ctypes.byref(dsc) if dsc is not None else None, mode, tbar, x, FAKE, FAKE, FAKE,
+                               FAKE, None, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, dz, dh0, ws, ws_bytes, None)
 
 
-def test_null_and_shape_errors(lib):
-    assert grad_call(lib, None) == 1
+GRAD_ENTRIES = ["ssm_adjoint_grad", "ssm_adjoint_grad_pairs"]
+
+
+@pytest.mark.parametrize("entry", GRAD_ENTRIES)
+def test_null_and_shape_errors(lib, entry):
+    call = lambda *a, **k: grad_call(*a, entry=entry, **k)
+    assert call(lib, None) == 1
     assert "desc" in ssm.last_error()
-    assert grad_call(lib, desc(batch=0)) == 2
-    assert grad_call(lib, desc(seqlen=0)) == 2
-    assert grad_call(lib, desc(dstate=17)) == 4
-    assert grad_call(lib, desc(in_dtype=7)) == 3
-    assert grad_call(lib, desc(chunk=100)) == 4
-    assert grad_call(lib, desc(flags=16)) == 2
-    assert grad_call(lib, desc(), x=None) == 1
+    assert call(lib, desc(batch=0)) == 2
+    assert call(lib, desc(seqlen=0)) == 2
+    assert call(lib, desc(dstate=17)) == 4
+    assert call(lib, desc(in_dtype=7)) == 3
+    assert call(lib, desc(chunk=100)) == 4
+    assert call(lib, desc(flags=16)) == 2
+    assert call(lib, desc(), x=None) == 1
     assert "x is NULL" in ssm.last_error()
-    assert grad_call(lib, desc(), x=MISALIGNED) == 6
+    assert call(lib, desc(), x=MISALIGNED) == 6
 
 
-def test_mode_errors(lib):
-    assert grad_call(lib, desc(), mode=5) == 2
-    assert grad_call(lib, desc(), mode=ssm.SSM_TRUNCATED, tbar=0) == 2
+@pytest.mark.parametrize("entry", GRAD_ENTRIES)
+def test_mode_errors(lib, entry):
+    call = lambda *a, **k: grad_call(*a, entry=entry, **k)
+    assert call(lib, desc(), mode=5) == 2
+    assert call(lib, desc(), mode=ssm.SSM_TRUNCATED, tbar=0) == 2
     # dh0 exists for the full gradient only
-    assert grad_call(lib, desc(), mode=ssm.SSM_TRUNCATED, tbar=32, dh0=FAKE) == 4
+    assert call(lib, desc(), mode=ssm.SSM_TRUNCATED, tbar=32, dh0=FAKE) == 4
     # gate flag and z must agree
-    assert grad_call(lib, desc(flags=ssm.SSM_GATE_SILU)) == 1
-    assert grad_call(lib, desc(), z=FAKE, dz=FAKE) == 2
+    assert call(lib, desc(flags=ssm.SSM_GATE_SILU)) == 1
+    assert call(lib, desc(), z=FAKE, dz=FAKE) == 2
 
 
-def test_workspace_errors(lib):
+@pytest.mark.parametrize("entry", GRAD_ENTRIES)
+def test_workspace_errors(lib, entry):
     d = desc()
-    assert grad_call(lib, d, ws=None) == 5
-    assert grad_call(lib, d, ws_bytes=16) == 5
-    assert grad_call(lib, d, ws=ctypes.c_void_p(0x100010)) == 6
+    assert grad_call(lib, d, ws=None, entry=entry) == 5
+    assert grad_call(lib, d, ws_bytes=16, entry=entry) == 5
+    assert grad_call(lib, d, ws=ctypes.c_void_p(0x100010), entry=entry) == 6
 
 
 def test_workspace_queries(lib):
@@ -95,6 +109,9 @@ def test_workspace_queries(lib):
     assert n.value == full
     assert lib.ssm_adjoint_forward_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
     assert 0 < n.value <= full
+    assert lib.ssm_adjoint_grad_pairs_workspace_size(ctypes.byref(d), ssm.SSM_TRUNCATED, 32, ctypes.byref(n)) == 0
+    assert n.value > 0
+    assert lib.ssm_adjoint_grad_pairs_workspace_size(ctypes.byref(d), ssm.SSM_TRUNCATED, 0, ctypes.byref(n)) == 2
     assert lib.ssm_proj_grad_workspace_size(8192, 1536, 1568, 0, ctypes.byref(n)) == 0
     assert lib.ssm_proj_grad_workspace_size(0, 1, 1, 0, ctypes.byref(n)) == 2
     ld = desc(batch=2, seqlen=4096, channels=1536, in_dtype=ssm.SSM_BF16)
