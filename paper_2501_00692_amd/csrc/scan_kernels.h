@@ -520,8 +520,7 @@ struct __attribute__((aligned(16))) BCStage {
     // NTH threads; each issues all of its loads before it writes any to LDS.
     template <int NTH>
     __device__ __forceinline__ void load(const ScanProblem& p, int64_t bb, int64_t t0, int tid) {
-        static_assert((L * 32) % NTH == 0, "whole rows per pass");
-        constexpr int PT = L * 32 / NTH;
+        constexpr int PT = (L * 32 + NTH - 1) / NTH;
         const TI* Bp = static_cast<const TI*>(p.B);
         const TI* Cp = static_cast<const TI*>(p.C);
         float v[PT];
@@ -530,12 +529,12 @@ struct __attribute__((aligned(16))) BCStage {
             const int i = tid + NTH * e;
             const int t = i >> 5, c = i & 31, n = c & 15;
             const int64_t tg = t0 + t;
-            v[e] = ldm(c < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, tg < p.T && n < p.N);
+            v[e] = ldm(c < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, i < L * 32 && tg < p.T && n < p.N);
         }
 #pragma unroll
         for (int e = 0; e < PT; ++e) {
             const int i = tid + NTH * e;
-            w[i >> 5][i & 31] = v[e];
+            if ((L * 32) % NTH == 0 || i < L * 32) w[i >> 5][i & 31] = v[e];
         }
     }
     // States 4r..4r+3 of B and C at in-chunk step t.
