@@ -138,6 +138,25 @@ def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False, pairs=False):
     return step
 
 
+def stack_step(K, b, T, D, N, ssm, torch, exact):
+    """One whole K-layer step: the forward of every layer, then every layer's
+    parameter gradient (Prop. 3 or backpropagation)."""
+    from paper_2501_00692_amd.synth import make_stack_inputs
+    inp = make_stack_inputs(K, b, T, D, N, 692500, device="cuda")
+    f32 = dict(dtype=torch.float32, device="cuda")
+    out = {"dW_in": [torch.empty(D, 2 * D, **f32) for _ in range(K)],
+           "dW_x": [torch.empty(D, D + 2 * N, **f32) for _ in range(K)],
+           "dA_log": [torch.empty(D, N, **f32) for _ in range(K)]}
+    desc = ssm.SsmDesc(b, T, D, N, 0, ssm.SSM_BF16, 0)
+    grad = ssm.SSM_STACK_EXACT if exact else ssm.SSM_STACK_ADJOINT
+    ws = torch.empty(ssm.stack_workspace_size(desc, K, grad), dtype=torch.uint8, device="cuda")
+
+    def step():
+        ssm.ssm_stack_grad(inp["y0"], inp["W_in"], inp["W_x"], inp["A_log"], inp["gK"], N, exact=exact, out=out,
+                           workspace=ws)
+    return step, inp, out
+
+
 def measured_traffic(kern, workload):
     """HBM-side bytes per launch from the committed rocprofv3 counter summary, if it
     was taken on the current kernel source (else None)."""
@@ -310,6 +329,22 @@ def main():
             res[f"{name}/{kind}/tbar={tbar}" + (f"/{variant}" if variant else "")] = entry
             del x, st
             torch.cuda.empty_cache()
+        # the K-layer residual stack (forward + gradients of every layer), Prop. 3 and
+        # backpropagation, and how far apart their parameter gradients are
+        K, b, T, D, N = 4, 2, 4096, 1536, 16
+        st_res = {}
+        grads = {}
+        for exact in (False, True):
+            st, sinp, sout = stack_step(K, b, T, D, N, ssm, torch, exact)
+            m = _timed(st, 5, 2, torch)
+            st_res["exact" if exact else "adjoint"] = {"ms_per_step": m, "tokens_per_s": b * T / (m * 1e-3)}
+            grads[exact] = [x.clone() for x in sout["dW_in"]]
+            del st, sinp, sout
+            torch.cuda.empty_cache()
+        st_res["dW_in_rel_diff_per_layer"] = [
+            float((grads[False][k] - grads[True][k]).norm() / grads[True][k].norm()) for k in range(K)]
+        st_res["config"] = f"K={K} layers, b={b}, T={T}, D={D} (residual width = channels), N={N}, bf16, full"
+        res["stack"] = st_res
         extra["workloads"] = res
 
     line = {

@@ -74,6 +74,10 @@ typedef enum { SSM_FULL = 0, SSM_TRUNCATED = 1 } ssm_mode;
 #define SSM_A_SCALAR 4u       /* one decay rate per channel: A_log, dA_log are [D]      */
 #define SSM_B_DELTA 8u        /* input term Delta * B * x (dDelta includes its path)    */
 
+/* ssm_stack_grad gradient kinds */
+#define SSM_STACK_ADJOINT 0   /* Prop. 3: every layer's vjps under dL/dy_K                 */
+#define SSM_STACK_EXACT 1     /* backpropagation through the whole stack                   */
+
 /* ssm_proj_grad flags */
 #define SSM_ACCUM_DW 1u       /* dW += X^T dZ instead of dW = X^T dZ                   */
 #define SSM_ACCUM_DX 2u       /* dX += dZ W^T instead of dX = dZ W^T                   */
@@ -197,6 +201,41 @@ ssm_status ssm_timing_summary(char* buf, size_t len);
 /* Thread-local, NUL-terminated description of the last non-OK status returned on
  * the calling thread ("" if none).  Owned by the library. */
 const char* ssm_last_error(void);
+
+/* Parameter gradients of a stack of K residual SSM layers (Sec. 3.2 and Alg. 1:
+ * y_0 given; for k = 1..K:  u_k = Norm(y_{k-1}),  y_k = y_{k-1} + SSM_k(u_k)),
+ * with L = sum g_K * y_K for a given upstream g_K = dL/dy_K (the language head
+ * and the loss stay with the caller, as Alg. 1 computes them once and hands
+ * dL/dy_K to every device).  Norm is the root-mean-square normalisation over
+ * the channels, u = y / sqrt(mean(y^2) + 1e-6), without a learned scale.  SSM_k is
+ * the selective layer of ssm_layer_grad with its projections
+ * ([x | z] = u W_in, [Delta_pre | B | C] = x W_x, out = scan(...) * silu(z)),
+ * channel count D equal to the residual width (the paper's SSM maps P to P).
+ *   desc   : batch b, seqlen T, channels D (= residual width), dstate N, chunk;
+ *            in_dtype must be SSM_BF16 (the stored activations u, x, z,
+ *            Delta_pre, B, C and each layer's output are bf16, round to
+ *            nearest even); flags must be 0.
+ *   K      : number of layers, 1..4096;  grad : SSM_STACK_ADJOINT (Prop. 3: each
+ *            layer's gradient taken with the upstream g_K and the layer's own
+ *            input, independently of the other layers) or SSM_STACK_EXACT
+ *            (backpropagation: layer k's upstream is dL/dy_k, including the paths
+ *            through later layers);  mode/tbar : as for ssm_adjoint_grad.
+ *   y0     : fp32 [b][T][D];  gK : fp32 [b][T][D] (passed to the layers in bf16);
+ *   W_in, W_x, A_log : host arrays of K device pointers (bf16 [D][2D], bf16
+ *            [D][D+2N], fp32 [D][N]);  dW_in, dW_x, dA_log : host arrays of K device
+ *            pointers to the fp32 outputs (overwritten);
+ *   yK     : fp32 [b][T][D] output of the forward, or NULL.
+ * The forward runs first and keeps every layer's activations in the workspace
+ * (about 12 b T D bytes per layer plus the transposed projections); the layer
+ * gradients then reuse the ssm_layer_grad path.  Everything is validated before
+ * anything is enqueued. */
+ssm_status ssm_stack_grad_workspace_size(const ssm_desc* desc, int64_t K, int32_t grad, int32_t mode,
+                                         int64_t tbar, size_t* bytes);
+ssm_status ssm_stack_grad(const ssm_desc* desc, int64_t K, int32_t grad, int32_t mode, int64_t tbar,
+                          const float* y0, const void* const* W_in, const void* const* W_x,
+                          const float* const* A_log, const float* gK, float* const* dW_in,
+                          float* const* dW_x, float* const* dA_log, float* yK, void* workspace,
+                          size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

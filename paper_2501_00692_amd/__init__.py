@@ -10,7 +10,7 @@ built.
 
 Entry points (names as in the C ABI): :func:`ssm_adjoint_forward`,
 :func:`ssm_adjoint_grad`, :func:`ssm_adjoint_grad_pairs`, :func:`ssm_proj_grad`,
-:func:`ssm_layer_grad`.
+:func:`ssm_layer_grad`, :func:`ssm_stack_grad`.
 """
 from __future__ import annotations
 
@@ -26,6 +26,7 @@ SSM_F32, SSM_BF16 = 0, 1
 SSM_FULL, SSM_TRUNCATED = 0, 1
 SSM_DELTA_SOFTPLUS, SSM_GATE_SILU, SSM_A_SCALAR, SSM_B_DELTA = 1, 2, 4, 8
 SSM_ACCUM_DW, SSM_ACCUM_DX = 1, 2
+SSM_STACK_ADJOINT, SSM_STACK_EXACT = 0, 1
 
 STATUS = {0: "SSM_OK", 1: "SSM_ERR_NULL", 2: "SSM_ERR_SHAPE", 3: "SSM_ERR_DTYPE",
           4: "SSM_ERR_UNSUPPORTED", 5: "SSM_ERR_WORKSPACE", 6: "SSM_ERR_ALIGN", 7: "SSM_ERR_HIP"}
@@ -34,7 +35,8 @@ EXPORTED = (
     "ssm_adjoint_forward_workspace_size", "ssm_adjoint_grad_workspace_size", "ssm_adjoint_forward",
     "ssm_adjoint_grad", "ssm_adjoint_grad_pairs_workspace_size", "ssm_adjoint_grad_pairs",
     "ssm_proj_grad_workspace_size", "ssm_proj_grad",
-    "ssm_layer_grad_workspace_size", "ssm_layer_grad", "ssm_timing_enable", "ssm_timing_summary",
+    "ssm_layer_grad_workspace_size", "ssm_layer_grad", "ssm_stack_grad_workspace_size", "ssm_stack_grad",
+    "ssm_timing_enable", "ssm_timing_summary",
     "ssm_last_error",
 )
 
@@ -77,6 +79,8 @@ def load_library():
         "ssm_proj_grad": [i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, vp, u32, vp, sz, vp],
         "ssm_layer_grad_workspace_size": [dp, i32, i64, i64, szp],
         "ssm_layer_grad": [dp, i32, i64, i64] + [vp] * 20 + [vp, sz, vp],
+        "ssm_stack_grad_workspace_size": [dp, i64, i32, i32, i64, szp],
+        "ssm_stack_grad": [dp, i64, i32, i32, i64] + [vp] * 9 + [vp, sz, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -335,4 +339,54 @@ def ssm_layer_grad(u, x, z, delta_pre, B, C, W_x, W_in, A_log, dy, tbar=0, chunk
                               _p(o["dA_log"]), _p(o.get("du")), _p(o.get("dx")), _p(o.get("ddelta")), _p(o.get("dB")),
                               _p(o.get("dC")), _p(o.get("dz")), _p(o.get("dx_total")), _p(ws), ws.numel(),
                               _stream()), "ssm_layer_grad")
+    return o
+
+
+def _ptr_array(ts):
+    return (ctypes.c_void_p * len(ts))(*[t.data_ptr() for t in ts])
+
+
+def stack_workspace_size(desc: SsmDesc, K: int, grad: int, tbar: int = 0) -> int:
+    n = ctypes.c_size_t()
+    mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
+    _check(load_library().ssm_stack_grad_workspace_size(ctypes.byref(desc), int(K), int(grad), mode, int(tbar),
+                                                        ctypes.byref(n)), "ssm_stack_grad_workspace_size")
+    return n.value
+
+
+def ssm_stack_grad(y0, W_in, W_x, A_log, gK, N, exact=False, tbar=0, chunk=0, want_yK=False, out=None,
+                   workspace=None):
+    """Parameter gradients of a K-layer residual stack (lists ``W_in``, ``W_x``,
+    ``A_log`` of K tensors) for the upstream ``gK = dL/dy_K``: Prop. 3 (each layer
+    under gK, ``exact=False``) or backpropagation (``exact=True``).  ``y0`` and
+    ``gK`` are fp32 [b, T, D]; the projections bf16.  Returns a dict with lists
+    ``dW_in, dW_x, dA_log`` (+ ``yK`` if asked)."""
+    lib = load_library()
+    b, T, D = y0.shape
+    K = len(W_in)
+    assert len(W_x) == K and len(A_log) == K
+    _need(y0, "y0", torch.float32)
+    _need(gK, "gK", torch.float32, (b, T, D))
+    for k in range(K):
+        _need(W_in[k], "W_in[k]", torch.bfloat16, (D, 2 * D))
+        _need(W_x[k], "W_x[k]", torch.bfloat16, (D, D + 2 * N))
+        _need(A_log[k], "A_log[k]", torch.float32, (D, N))
+    desc = SsmDesc(b, T, D, N, chunk, SSM_BF16, 0)
+    grad = SSM_STACK_EXACT if exact else SSM_STACK_ADJOINT
+    mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
+    dev = y0.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    o = dict(out) if out else {}
+    o.setdefault("dW_in", [torch.empty(D, 2 * D, **f32) for _ in range(K)])
+    o.setdefault("dW_x", [torch.empty(D, D + 2 * N, **f32) for _ in range(K)])
+    o.setdefault("dA_log", [torch.empty(D, N, **f32) for _ in range(K)])
+    if want_yK:
+        o.setdefault("yK", torch.empty(b, T, D, **f32))
+    ws = workspace if workspace is not None else _workspace(stack_workspace_size(desc, K, grad, tbar), dev)
+    keep = [_ptr_array(W_in), _ptr_array(W_x), _ptr_array(A_log), _ptr_array(o["dW_in"]), _ptr_array(o["dW_x"]),
+            _ptr_array(o["dA_log"])]
+    _check(lib.ssm_stack_grad(ctypes.byref(desc), K, grad, mode, int(tbar), _p(y0), *[ctypes.cast(a, ctypes.c_void_p)
+                                                                                    for a in keep[:3]],
+                              _p(gK), *[ctypes.cast(a, ctypes.c_void_p) for a in keep[3:]], _p(o.get("yK")), _p(ws),
+                              ws.numel(), _stream()), "ssm_stack_grad")
     return o

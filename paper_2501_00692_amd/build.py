@@ -13,7 +13,7 @@ PKG = Path(__file__).resolve().parent
 ROOT = PKG.parent
 CSRC = PKG / "csrc"
 SRC = [CSRC / "scan.hip", CSRC / "scan_grad_f32_full.hip", CSRC / "scan_grad_f32_trunc.hip",
-       CSRC / "scan_grad_bf16_full.hip", CSRC / "scan_grad_bf16_trunc.hip", CSRC / "gemm.hip", CSRC / "pairs.hip",
+       CSRC / "scan_grad_bf16_full.hip", CSRC / "scan_grad_bf16_trunc.hip", CSRC / "gemm.hip", CSRC / "pairs.hip", CSRC / "stack.hip",
        CSRC / "abi.cpp", CSRC / "timing.cpp"]
 OBJ = PKG / "_build"
 LIB = PKG / "libssm_adjoint.so"

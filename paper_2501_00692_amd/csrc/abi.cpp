@@ -508,3 +508,194 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// K-layer residual stack (Sec. 3.2, Prop. 3, Alg. 1).
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr int64_t kMaxStackLayers = 4096;
+
+// Workspace of the stack: per layer the activations the forward stores (u, x,
+// z, Delta_pre as bf16 [M][D], B, C as bf16 [M][N], 1/rms [M], the layer's
+// fp32 input y for layers after the first, the transposed projections), then
+// the shared buffers (the layer output, the running upstream and its bf16 copy,
+// du, y_K when the caller does not take it, the scan and layer workspaces).
+struct StackWs {
+    size_t per_layer, off_u, off_x, off_z, off_dp, off_B, off_C, off_r, off_y, off_wi, off_wx;
+    size_t off_ytil, off_g, off_g16, off_du, off_yk, off_fws, off_lws, total;
+    size_t fws_bytes, lws_bytes;
+};
+
+StackWs stack_ws(const ssm_desc* d, int64_t K, int64_t L, bool trunc) {
+    StackWs w{};
+    const int64_t M = d->batch * d->seqlen, D = d->channels, N = d->dstate;
+    const size_t a16 = size_t(M) * D * 2, n16 = size_t(M) * N * 2, f32 = size_t(M) * D * 4;
+    size_t o = 0;
+    w.off_u = o; o = up256(o + a16);
+    w.off_x = o; o = up256(o + a16);
+    w.off_z = o; o = up256(o + a16);
+    w.off_dp = o; o = up256(o + a16);
+    w.off_B = o; o = up256(o + n16);
+    w.off_C = o; o = up256(o + n16);
+    w.off_r = o; o = up256(o + size_t(M) * 4);
+    w.off_y = o; o = up256(o + f32);
+    w.off_wi = o; o = up256(o + size_t(2 * D) * D * 2);
+    w.off_wx = o; o = up256(o + size_t(D + 2 * N) * D * 2);
+    w.per_layer = o;
+    o = w.per_layer * size_t(K);
+    w.off_ytil = o; o = up256(o + a16);
+    w.off_g = o; o = up256(o + f32);
+    w.off_g16 = o; o = up256(o + a16);
+    w.off_du = o; o = up256(o + f32);
+    w.off_yk = o; o = up256(o + f32);
+    ssm_desc ld = *d;
+    ld.flags = SSM_DELTA_SOFTPLUS | SSM_GATE_SILU;
+    w.fws_bytes = ssmk::scan_workspace(ld.batch, ld.seqlen, D, N, L, false, false).total;
+    w.off_fws = o; o = up256(o + w.fws_bytes);
+    w.lws_bytes = layer_ws(&ld, L, trunc, D).total;
+    w.off_lws = o; o = up256(o + w.lws_bytes);
+    w.total = o;
+    return w;
+}
+
+ssm_status check_stack(const ssm_desc* desc, int64_t K, int32_t grad, int32_t mode, int64_t tbar, int64_t* L,
+                       bool* trunc) {
+    int64_t nc;
+    ssm_status st = check_desc(desc, L, &nc);
+    if (st) return st;
+    if (desc->in_dtype != SSM_BF16) return fail(SSM_ERR_UNSUPPORTED, "the stack takes bf16 activations");
+    if (desc->flags != 0) return fail(SSM_ERR_UNSUPPORTED, "the stack's layers take no variant flags");
+    if (K < 1 || K > kMaxStackLayers) return fail(SSM_ERR_SHAPE, "K must be in [1, %lld]", (long long)kMaxStackLayers);
+    if (grad != SSM_STACK_ADJOINT && grad != SSM_STACK_EXACT) return fail(SSM_ERR_SHAPE, "unknown gradient kind %d", grad);
+    st = check_mode(desc, mode, tbar, trunc);
+    if (st) return st;
+    const int64_t M = desc->batch * desc->seqlen, D = desc->channels, N = desc->dstate;
+    if (M >= (int64_t(1) << 31)) return fail(SSM_ERR_UNSUPPORTED, "batch * seqlen too large for the stack");
+    if ((D + 31) / 32 > kMaxGridYZ) return fail(SSM_ERR_UNSUPPORTED, "channels too large for the stack");
+    st = check_gemm_shape(M, D, D + 2 * N, D, D + 2 * N, D + 2 * N, true);
+    if (st) return st;
+    return check_gemm_shape(M, D, 2 * D, D, 2 * D, 2 * D, true);
+}
+
+}  // namespace
+
+extern "C" {
+
+ssm_status ssm_stack_grad_workspace_size(const ssm_desc* desc, int64_t K, int32_t grad, int32_t mode,
+                                         int64_t tbar, size_t* bytes) {
+    int64_t L;
+    bool trunc;
+    ssm_status st = check_stack(desc, K, grad, mode, tbar, &L, &trunc);
+    if (st) return st;
+    if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");
+    *bytes = stack_ws(desc, K, L, trunc).total;
+    return SSM_OK;
+}
+
+ssm_status ssm_stack_grad(const ssm_desc* desc, int64_t K, int32_t grad, int32_t mode, int64_t tbar,
+                          const float* y0, const void* const* W_in, const void* const* W_x,
+                          const float* const* A_log, const float* gK, float* const* dW_in,
+                          float* const* dW_x, float* const* dA_log, float* yK, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    int64_t L;
+    bool trunc;
+    ssm_status st = check_stack(desc, K, grad, mode, tbar, &L, &trunc);
+    if (st) return st;
+    REQUIRE_PTR(y0, "y0");
+    REQUIRE_PTR(gK, "gK");
+    OPTIONAL_PTR(yK, "yK");
+    if (!W_in || !W_x || !A_log || !dW_in || !dW_x || !dA_log)
+        return fail(SSM_ERR_NULL, "a per-layer pointer array is NULL");
+    for (int64_t k = 0; k < K; ++k) {
+        REQUIRE_PTR(W_in[k], "W_in[k]");
+        REQUIRE_PTR(W_x[k], "W_x[k]");
+        REQUIRE_PTR(A_log[k], "A_log[k]");
+        REQUIRE_PTR(dW_in[k], "dW_in[k]");
+        REQUIRE_PTR(dW_x[k], "dW_x[k]");
+        REQUIRE_PTR(dA_log[k], "dA_log[k]");
+    }
+    const StackWs w = stack_ws(desc, K, L, trunc);
+    st = check_workspace(workspace, workspace_bytes, w.total);
+    if (st) return st;
+
+    const int64_t M = desc->batch * desc->seqlen, D = desc->channels, N = desc->dstate;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    auto lay = [&](int64_t k, size_t off) { return ws + w.per_layer * size_t(k) + off; };
+    auto u16 = [](char* p) { return reinterpret_cast<uint16_t*>(p); };
+    auto f32 = [](char* p) { return reinterpret_cast<float*>(p); };
+    uint16_t* ytil = u16(ws + w.off_ytil);
+    float* g = f32(ws + w.off_g);
+    uint16_t* g16 = u16(ws + w.off_g16);
+    float* du = f32(ws + w.off_du);
+    float* yout = yK ? yK : f32(ws + w.off_yk);
+    ssm_desc ld = *desc;
+    ld.flags = SSM_DELTA_SOFTPLUS | SSM_GATE_SILU;
+    hipError_t e = hipSuccess;
+#define STACK_HIP(call, what)                           \
+    do {                                                \
+        e = (call);                                     \
+        if (e != hipSuccess) return hip_fail(e, what);  \
+    } while (0)
+#define STACK_SSM(call)            \
+    do {                           \
+        ssm_status r_ = (call);    \
+        if (r_ != SSM_OK) return r_; \
+    } while (0)
+
+    // forward (Alg. 1): u = Norm(y), [x | z] = u W_in, [Delta_pre | B | C] = x W_x,
+    // y += scan(...) * silu(z); every layer keeps its activations
+    const float* ycur = y0;
+    for (int64_t k = 0; k < K; ++k) {
+        uint16_t* u = u16(lay(k, w.off_u));
+        uint16_t* x = u16(lay(k, w.off_x));
+        uint16_t* z = u16(lay(k, w.off_z));
+        uint16_t* dp = u16(lay(k, w.off_dp));
+        uint16_t* Bm = u16(lay(k, w.off_B));
+        uint16_t* Cm = u16(lay(k, w.off_C));
+        uint16_t* wi = u16(lay(k, w.off_wi));
+        uint16_t* wx = u16(lay(k, w.off_wx));
+        float* rinv = f32(lay(k, w.off_r));
+        STACK_HIP(ssmk::launch_rms_fwd(ycur, u, rinv, M, D, s), "ssm_stack_grad norm");
+        STACK_HIP(ssmk::launch_transpose16(static_cast<const uint16_t*>(W_in[k]), wi, D, 2 * D, s),
+                  "ssm_stack_grad transpose");
+        STACK_HIP(ssmk::launch_transpose16(static_cast<const uint16_t*>(W_x[k]), wx, D, D + 2 * N, s),
+                  "ssm_stack_grad transpose");
+        // out[M][c] = sum_j a[M][j] W^T[c][j]: the dX form of the projection GEMM
+        STACK_HIP(ssmk::launch_gemm_dx(M, D, D, u, D, wi, D, nullptr, false, nullptr, x, D, s), "ssm_stack_grad x");
+        STACK_HIP(ssmk::launch_gemm_dx(M, D, D, u, D, wi + D * D, D, nullptr, false, nullptr, z, D, s),
+                  "ssm_stack_grad z");
+        STACK_HIP(ssmk::launch_gemm_dx(M, D, D, x, D, wx, D, nullptr, false, nullptr, dp, D, s),
+                  "ssm_stack_grad Delta_pre");
+        STACK_HIP(ssmk::launch_gemm_dx(M, N, D, x, D, wx + D * D, D, nullptr, false, nullptr, Bm, N, s),
+                  "ssm_stack_grad B");
+        STACK_HIP(ssmk::launch_gemm_dx(M, N, D, x, D, wx + (D + N) * D, D, nullptr, false, nullptr, Cm, N, s),
+                  "ssm_stack_grad C");
+        STACK_SSM(ssm_adjoint_forward(&ld, x, dp, A_log[k], Bm, Cm, nullptr, z, ytil, nullptr, ws + w.off_fws,
+                                      w.fws_bytes, stream));
+        float* ynext = k + 1 < K ? f32(lay(k + 1, w.off_y)) : yout;
+        STACK_HIP(ssmk::launch_residual(ycur, ytil, ynext, M * D, s), "ssm_stack_grad residual");
+        ycur = ynext;
+    }
+
+    // gradients: Prop. 3 (every layer under dL/dy_K) or backpropagation
+    if (grad == SSM_STACK_EXACT)
+        STACK_HIP(hipMemcpyAsync(g, gK, size_t(M) * D * 4, hipMemcpyDeviceToDevice, s), "ssm_stack_grad copy");
+    STACK_HIP(ssmk::launch_to_bf16(gK, g16, M * D, s), "ssm_stack_grad upstream");
+    for (int64_t k = K - 1; k >= 0; --k) {
+        const bool back = grad == SSM_STACK_EXACT && k > 0;
+        STACK_SSM(ssm_layer_grad(&ld, mode, tbar, D, lay(k, w.off_u), lay(k, w.off_x), lay(k, w.off_z),
+                                 lay(k, w.off_dp), lay(k, w.off_B), lay(k, w.off_C), W_x[k], W_in[k], A_log[k], g16,
+                                 dW_in[k], dW_x[k], dA_log[k], back ? du : nullptr, nullptr, nullptr, nullptr,
+                                 nullptr, nullptr, nullptr, ws + w.off_lws, w.lws_bytes, stream));
+        if (back)  // dL/dy_{k-1} = dL/dy_k + Norm'(y_{k-1})^T du_k
+            STACK_HIP(ssmk::launch_rms_bwd(f32(lay(k, w.off_y)), f32(lay(k, w.off_r)), du, g, g16, M, D, s),
+                      "ssm_stack_grad norm backward");
+    }
+#undef STACK_HIP
+#undef STACK_SSM
+    return SSM_OK;
+}
+
+}  // extern "C"

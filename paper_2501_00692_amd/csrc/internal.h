@@ -109,6 +109,14 @@ void bind_workspace(ScanProblem& p, void* ws, const ScanWorkspace& w);
 hipError_t launch_forward(const ScanProblem& p, hipStream_t s);
 hipError_t launch_grad(const ScanProblem& p, hipStream_t s);
 
+// Kernels of the K-layer residual stack (stack.hip).
+hipError_t launch_rms_fwd(const float* y, uint16_t* u, float* rinv, int64_t M, int64_t D, hipStream_t s);
+hipError_t launch_rms_bwd(const float* y, const float* rinv, const float* du, float* g, uint16_t* g16, int64_t M,
+                          int64_t D, hipStream_t s);
+hipError_t launch_residual(const float* yin, const uint16_t* ytil, float* yout, int64_t n, hipStream_t s);
+hipError_t launch_to_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s);
+hipError_t launch_transpose16(const uint16_t* in, uint16_t* out, int64_t R, int64_t C, hipStream_t s);
+
 // The gradient by the explicit pair formulation (pairs.hip): workspace layout and
 // launch; W is the window (tbar, or T for the full gradient).
 struct PairsWorkspace {

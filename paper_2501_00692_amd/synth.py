@@ -113,3 +113,18 @@ def make_inputs(w: Workload, device="cpu", seed: int | None = None, h0: bool = F
     if h0:
         out["h0"] = randn(b, D, N)
     return out
+
+
+def make_stack_inputs(K: int, b: int, T: int, D: int, N: int, seed: int, device="cpu"):
+    """Inputs of a K-layer residual stack: y0 ~ N(0,1) [b, T, D] (fp32); per layer
+    W_in ~ N(0, 1/D) [D, 2D], W_x ~ N(0, 1/D) [D, D+2N] (bf16, round to nearest
+    even) and A_log ~ U(log 1, log 16) [D, N] (fp32); the upstream gK ~ N(0,1)."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    f32 = dict(dtype=torch.float32, device=device)
+    y0 = torch.randn(b, T, D, generator=g, **f32)
+    W_in = [(torch.randn(D, 2 * D, generator=g, **f32) / math.sqrt(D)).to(torch.bfloat16) for _ in range(K)]
+    W_x = [(torch.randn(D, D + 2 * N, generator=g, **f32) / math.sqrt(D)).to(torch.bfloat16) for _ in range(K)]
+    A_log = [torch.rand(D, N, generator=g, **f32) * math.log(16.0) for _ in range(K)]
+    gK = torch.randn(b, T, D, generator=g, **f32)
+    return dict(y0=y0, W_in=W_in, W_x=W_x, A_log=A_log, gK=gK)

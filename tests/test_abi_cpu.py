@@ -133,3 +133,28 @@ def test_layer_rejects_fp32(lib):
     d = desc()
     rc = lib.ssm_layer_grad(ctypes.byref(d), 0, 0, 64, *([FAKE] * 13), *([None] * 7), FAKE, 1 << 40, None)
     assert rc == 4
+
+
+def test_stack_errors(lib):
+    d = desc(in_dtype=ssm.SSM_BF16)
+    arr = (ctypes.c_void_p * 2)(FAKE.value, FAKE.value)
+
+    def call(dsc=d, K=2, grad=ssm.SSM_STACK_ADJOINT, mode=ssm.SSM_FULL, tbar=0, y0=FAKE, ws_bytes=1 << 40, W=arr):
+        return lib.ssm_stack_grad(ctypes.byref(dsc), K, grad, mode, tbar, y0, W, arr, arr, FAKE, arr, arr, arr,
+                                  None, FAKE, ws_bytes, None)
+    assert call(K=0) == 2
+    assert call(grad=5) == 2
+    assert call(dsc=desc()) == 4                                     # fp32 activations
+    assert call(dsc=desc(in_dtype=ssm.SSM_BF16, flags=ssm.SSM_A_SCALAR)) == 4
+    assert call(dsc=desc(in_dtype=ssm.SSM_BF16, dstate=3)) == 4      # D + 2N not a multiple of 8
+    assert call(mode=ssm.SSM_TRUNCATED, tbar=0) == 2
+    assert call(y0=None) == 1
+    assert call(W=None) == 1
+    assert call(ws_bytes=16) == 5
+    n = ctypes.c_size_t()
+    assert lib.ssm_stack_grad_workspace_size(ctypes.byref(d), 3, ssm.SSM_STACK_EXACT, ssm.SSM_FULL, 0,
+                                             ctypes.byref(n)) == 0
+    three = n.value
+    assert lib.ssm_stack_grad_workspace_size(ctypes.byref(d), 1, ssm.SSM_STACK_EXACT, ssm.SSM_FULL, 0,
+                                             ctypes.byref(n)) == 0
+    assert 0 < n.value < three
