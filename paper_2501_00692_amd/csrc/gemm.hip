@@ -16,9 +16,10 @@
 // the next step's global loads are in flight while the MFMAs run, and below
 // 256 columns the next 16-deep sub-step's fragments are read from LDS while the
 // current sub-step's MFMAs run.
-// Output tiles are assigned so that the tiles of one row block run on the same
-// XCD (consecutive workgroups go to different XCDs), which keeps a row block of
-// the first operand in one L2.
+// Output tiles and reduction splits are assigned so that each XCD runs one
+// contiguous run of (split, row block, column block) (consecutive workgroups go
+// to different XCDs), which keeps a row block of the first operand and its
+// reduction range in one L2.
 #include "internal.h"
 
 namespace ssmk {
@@ -77,7 +78,7 @@ struct GemmArgs {
     int64_t ldb;
     float* C;             // output [R][Cc] (ldc = Cc), or split partials
     int64_t kper;         // reduction range per split (multiple of BK)
-    int direct;           // write C (else the partial of split blockIdx.z)
+    int direct;           // write C (else the partial of the workgroup's split)
     int accum;            // C += result
     const float* add;     // optional fp32 addend [R][Cc]
     uint16_t* out16;      // optional bf16 copy of the result
@@ -183,7 +184,7 @@ struct Stager {
 
 // Main loop over the workgroup's reduction range; FULL drops the row and column
 // bounds checks.
-template <bool TR, int BM, int BN, int NT, bool FULL, bool KF, int MI, int NJ>
+template <bool TR, int BM, int BN, int NT, bool FULL, bool KF, int MI, int NJ, bool PF2>
 __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, uint16_t (*As)[BM][LDK],
                                               uint16_t (*Bs)[BN][LDK], int64_t r0, int64_t c0,
                                               int64_t k_lo, int64_t k_hi, int tid, int wr, int wc,
@@ -196,7 +197,6 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, uint16_t (*As)[
         st.template load<FULL, KF>(g, r0, c0, k_lo, k_hi, tid);
         st.store(As[0], Bs[0], tid);
     }
-    __syncthreads();
     // fragments of one 16-deep sub-step, double-buffered in registers: the next
     // sub-step's LDS reads are issued before the current sub-step's MFMAs, and the
     // scheduling barriers keep them there, so that one wave per SIMD does not wait
@@ -222,13 +222,11 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, uint16_t (*As)[
     };
     // 256-wide tiles have no registers to spare for a second fragment set: they
     // read each sub-step's fragments right before its MFMAs
-    constexpr bool DB = BN < 256;
+    constexpr bool DB = BN < 256 && !(TR && PF2);
     bf16x8 a0[MI], b0[NJ], a1[MI], b1[NJ];
-    int cur = 0;
-    if (DB) frags(0, 0, a0, b0);
-    for (int64_t k = k_lo; k < k_hi; k += BK) {
-        const bool more = k + BK < k_hi;
-        if (more) st.template load<FULL, KF>(g, r0, c0, k + BK, k_hi, tid);
+    // the MFMAs of one 64-deep step on LDS buffer `cur`, with `between` (the
+    // staging store for the next step) issued before the last sub-step
+    auto step = [&](int cur, auto&& between) {
         static_assert(BK == 64, "four sub-steps per step");
         if constexpr (DB) {
             frags(cur, 16, a1, b1);
@@ -243,7 +241,7 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, uint16_t (*As)[
             __builtin_amdgcn_sched_barrier(0);
             mfmas(a0, b0);
             __builtin_amdgcn_sched_barrier(0);
-            if (more) st.store(As[cur ^ 1], Bs[cur ^ 1], tid);
+            between();
             mfmas(a1, b1);
         } else {
 #pragma unroll
@@ -251,8 +249,42 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, uint16_t (*As)[
                 frags(cur, ks, a0, b0);
                 mfmas(a0, b0);
             }
-            if (more) st.store(As[cur ^ 1], Bs[cur ^ 1], tid);
+            between();
         }
+    };
+    const int64_t nsteps = (k_hi - k_lo + BK - 1) / BK;
+    if constexpr (PF2) {
+        // global loads two steps ahead in two staging sets used alternately: at
+        // the top of step j the set of step j+1 is in flight and the other one,
+        // stored to LDS at the end of step j-1, takes the loads of step j+2
+        Stager<TR, BM, BN, NT> st1;
+        if (nsteps > 1) st1.template load<FULL, KF>(g, r0, c0, k_lo + BK, k_hi, tid);
+        __syncthreads();
+        if (DB) frags(0, 0, a0, b0);
+        auto pair_step = [&](int64_t j, Stager<TR, BM, BN, NT>& mine, Stager<TR, BM, BN, NT>& other) {
+            const int cur = static_cast<int>(j & 1);
+            if (j + 2 < nsteps) mine.template load<FULL, KF>(g, r0, c0, k_lo + (j + 2) * BK, k_hi, tid);
+            step(cur, [&]() {
+                if (j + 1 < nsteps) other.store(As[cur ^ 1], Bs[cur ^ 1], tid);
+            });
+            __syncthreads();
+            if (DB && j + 1 < nsteps) frags(cur ^ 1, 0, a0, b0);
+        };
+        for (int64_t j = 0; j < nsteps; j += 2) {
+            pair_step(j, st, st1);
+            if (j + 1 < nsteps) pair_step(j + 1, st1, st);
+        }
+        return;
+    }
+    __syncthreads();
+    int cur = 0;
+    if (DB) frags(0, 0, a0, b0);
+    for (int64_t j = 0; j < nsteps; ++j) {
+        const bool more = j + 1 < nsteps;
+        if (more) st.template load<FULL, KF>(g, r0, c0, k_lo + (j + 1) * BK, k_hi, tid);
+        step(cur, [&]() {
+            if (more) st.store(As[cur ^ 1], Bs[cur ^ 1], tid);
+        });
         __syncthreads();
         cur ^= 1;
         if (DB && more) frags(cur, 0, a0, b0);
@@ -263,20 +295,30 @@ template <bool TR, int BM, int BN, int WM>
 __global__ __launch_bounds__(128 * WM) void k_gemm(const GemmArgs g) {
     constexpr int NT = 128 * WM;  // WM x 2 waves
     constexpr int MI = BM / (32 * WM), NJ = BN / 64;  // 32x32 MFMA tiles per wave
+#ifndef SSMK_GEMM_PF2
+#define SSMK_GEMM_PF2 1
+#endif
+    constexpr bool PF2 = SSMK_GEMM_PF2 && BN == 128;  // registers for a second staging set
     __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDK];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][LDK];
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    // output tile: workgroups are dispatched to the XCDs in turn, so workgroup i
-    // takes tile (i % 8) * (tiles / 8) + i / 8 when the tile count allows it:
-    // the tiles of one XCD are consecutive in row-major order
+    // output tile and reduction split: workgroups are dispatched to the XCDs in
+    // turn (workgroup i to XCD i % 8), so the linear id is mapped to a logical
+    // index that gives every XCD one contiguous run of (split, row block, column
+    // block) -- the workgroups of one XCD share the first operand's row block and
+    // reduction range in its L2.  The map is a bijection for any count.
     const int ncb = static_cast<int>(gridDim.x);
     const int ntl = ncb * static_cast<int>(gridDim.y);
-    const int lin = static_cast<int>(blockIdx.x) + ncb * static_cast<int>(blockIdx.y);
-    const int tile = (ntl % kXcds == 0) ? (lin % kXcds) * (ntl / kXcds) + lin / kXcds : lin;
+    const int nwg = ntl * static_cast<int>(gridDim.z);
+    const int lin = static_cast<int>(blockIdx.x) + ncb * (static_cast<int>(blockIdx.y) +
+                                                          static_cast<int>(gridDim.y) * static_cast<int>(blockIdx.z));
+    const int xq = nwg / kXcds, xr = nwg % kXcds, xcd = lin % kXcds;
+    const int logical = (xcd < xr ? xcd * (xq + 1) : xr * (xq + 1) + (xcd - xr) * xq) + lin / kXcds;
+    const int tile = logical % ntl, split = logical / ntl;
     const int64_t c0 = static_cast<int64_t>(tile % ncb) * BN;
     const int64_t r0 = static_cast<int64_t>(tile / ncb) * BM;
-    const int64_t k_lo = static_cast<int64_t>(blockIdx.z) * g.kper;
+    const int64_t k_lo = static_cast<int64_t>(split) * g.kper;
     const int64_t k_hi = min(g.Kr, k_lo + g.kper);
     const int wr = (wave >> 1) * (BM / WM);
     const int wc = (wave & 1) * (BN / 2);
@@ -292,14 +334,14 @@ __global__ __launch_bounds__(128 * WM) void k_gemm(const GemmArgs g) {
     const bool full = r0 + BM <= g.R && c0 + BN <= g.Cc;
     const bool kfull = (k_hi - k_lo) % BK == 0;
     if (full && kfull)
-        gemm_mainloop<TR, BM, BN, NT, true, true, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
+        gemm_mainloop<TR, BM, BN, NT, true, true, MI, NJ, PF2>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
     else if (full)
-        gemm_mainloop<TR, BM, BN, NT, true, false, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
+        gemm_mainloop<TR, BM, BN, NT, true, false, MI, NJ, PF2>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
     else
-        gemm_mainloop<TR, BM, BN, NT, false, false, MI, NJ>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
+        gemm_mainloop<TR, BM, BN, NT, false, false, MI, NJ, PF2>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
 
     // acc element v of lane l is row 8*(v/4) + 4*(l/32) + v%4, col l%32 of its tile
-    float* __restrict__ dst = g.C ? g.C + (g.direct ? 0 : static_cast<int64_t>(blockIdx.z) * g.R * g.Cc) : nullptr;
+    float* __restrict__ dst = g.C ? g.C + (g.direct ? 0 : static_cast<int64_t>(split) * g.R * g.Cc) : nullptr;
     const float* __restrict__ addp = g.direct ? g.add : nullptr;
     const bool accum = g.direct && g.accum;
     uint16_t* __restrict__ o16 = g.direct ? g.out16 : nullptr;
