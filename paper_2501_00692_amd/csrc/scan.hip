@@ -44,6 +44,7 @@ void choose_split(int64_t nb, int64_t D, int64_t nc, int* nsplit, int* tiles_per
 
 int choose_nslice(int64_t nb, int64_t nc) {
     int64_t nq = nb * nc;
+    if (nq <= 256) return 1;  // one pass, in the same launch as the dB/dC sums
     int64_t s = nq / 16;
     if (s < 1) s = 1;
     if (s > 64) s = 64;

@@ -1021,6 +1021,80 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     p.dA_log[i] = acc;
 }
 
+// The tail reductions of the gradient in one launch: blocks [0, nbc) sum the
+// dB/dC split partials (as k_reduce_bc); the rest reduce the dA_log partials --
+// with one slice straight to the final [D][N] (or [D]) values, each thread
+// summing the (b, chunk) partials of one output in order (and, with one rate per
+// channel, over the states in order), else stage 1 of the sliced sum
+// (k_reduce_da1, with k_reduce_da2 launched after).
+[[maybe_unused]] __global__ __launch_bounds__(256) void k_reduce_tail(const ScanProblem p, int nbc) {
+    const int tid = threadIdx.x;
+    if (static_cast<int>(blockIdx.x) < nbc) {
+        const int64_t total = p.nb * p.T * p.N;
+        const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + tid;
+        if (i >= total) return;
+        float sb = 0.f, sc = 0.f;
+        for (int s0 = 0; s0 < p.nsplit; s0 += 8) {  // loads of a batch issued before the adds
+            float vb[8], vc[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const bool in = s0 + j < p.nsplit;
+                vb[j] = in ? p.pB[(s0 + j) * total + i] : 0.f;
+                vc[j] = in ? p.pC[(s0 + j) * total + i] : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                sb += vb[j];
+                sc += vc[j];
+            }
+        }
+        p.dB[i] = sb;
+        p.dC[i] = sc;
+        if (p.bc16) {
+            const int64_t row = i / p.N, n = i % p.N;
+            stf(p.bc16, row * p.ld_bc16 + n, sb);
+            stf(p.bc16, row * p.ld_bc16 + p.N + n, sc);
+        }
+        return;
+    }
+    const int64_t i = static_cast<int64_t>(static_cast<int>(blockIdx.x) - nbc) * 256 + tid;
+    const int64_t nq = p.nb * p.nc;
+    // acc += hbuf[(q N + n) D + d] for q = 0..nq-1 in order; the loads of a batch
+    // of 8 are issued before any of them is added
+    auto sum_q = [&](int64_t n, int64_t d, float acc) {
+        const int64_t stride = p.N * p.D;
+        const float* src = p.hbuf + n * p.D + d;
+        for (int64_t q0 = 0; q0 < nq; q0 += 8) {
+            float v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = q0 + j < nq ? src[(q0 + j) * stride] : 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc += v[j];
+        }
+        return acc;
+    };
+    if (p.nslice == 1) {
+        if (p.ascalar) {
+            if (i >= p.D) return;
+            float acc = 0.f;
+            for (int64_t n = 0; n < p.N; ++n) acc = sum_q(n, i, acc);
+            p.dA_log[i] = acc;
+            return;
+        }
+        if (i >= p.D * p.N) return;
+        const int64_t n = i / p.D, d = i % p.D;  // consecutive threads read consecutive channels
+        p.dA_log[d * p.N + n] = sum_q(n, d, 0.f);
+        return;
+    }
+    if (i >= static_cast<int64_t>(p.nslice) * p.N * p.D) return;
+    const int64_t d = i % p.D, n = (i / p.D) % p.N, sl = i / (p.D * p.N);
+    const int64_t per = (nq + p.nslice - 1) / p.nslice;
+    const int64_t q0 = sl * per, q1 = min(nq, q0 + per);
+    float acc = 0.f;
+    for (int64_t q = q0; q < q1; ++q) acc += p.hbuf[(q * p.N + n) * p.D + d];
+    p.dAtmp[(sl * p.N + n) * p.D + d] = acc;
+}
+
 inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b - 1) / b); }
 
 template <typename TI, bool SP, bool GATE, bool N16>
@@ -1085,12 +1159,10 @@ hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
         default: grad_main<TI, SP, GATE, TRUNC, N16, 16, 16>(p, s); break;  // 256
     }
     SSMK_TIMED("reduce", s);
-    if (p.nsplit > 1)
-        hipLaunchKernelGGL(k_reduce_bc, dim3(cdiv(p.nb * p.T * p.N, 256)), dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_reduce_da1, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N),
-                                          static_cast<unsigned>(p.nslice)),
-                       dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_reduce_da2, dim3(cdiv(p.D * p.N, 256)), dim3(256), 0, s, p);
+    const int nbc = p.nsplit > 1 ? static_cast<int>(cdiv(p.nb * p.T * p.N, 256)) : 0;
+    const int64_t nda = p.nslice == 1 ? (p.ascalar ? p.D : p.D * p.N) : static_cast<int64_t>(p.nslice) * p.N * p.D;
+    hipLaunchKernelGGL(k_reduce_tail, dim3(static_cast<unsigned>(nbc) + cdiv(nda, 256)), dim3(256), 0, s, p, nbc);
+    if (p.nslice > 1) hipLaunchKernelGGL(k_reduce_da2, dim3(cdiv(p.D * p.N, 256)), dim3(256), 0, s, p);
     return hipGetLastError();
 }
 
