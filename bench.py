@@ -78,6 +78,31 @@ def _timed(fn, steps, warmup, torch):
     return start.elapsed_time(stop) / steps
 
 
+def _timed_graph(fn, steps, warmup, torch):
+    """Per-step time of `fn` captured once in a HIP graph and replayed `steps`
+    times (launch overheads between the step's kernels removed)."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        fn()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        graph.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) / steps
+
+
 def _kernel_times(fn, steps, ssm, torch):
     """Per-kernel average launch duration (ms) from hipEvents recorded on the
     launch stream around every kernel of `steps` calls."""
@@ -271,6 +296,9 @@ def main():
     inp = make_inputs(w, device="cuda")
     step = layer_step(w, inp, ssm, torch, tbar=0)
     ms = _timed(step, args.steps, args.warmup, torch)
+    # the same step captured in a HIP graph and replayed, reported beside it (the
+    # gaps between dependent kernels are on the GPU side: replay gains nothing)
+    ms_graph = _timed_graph(step, args.steps, args.warmup, torch)
     ktimes = _kernel_times(step, args.steps, ssm, torch)
     dom = max(ktimes, key=lambda k: ktimes[k]["total_ms"])
     roof = roofline_for(dom, ktimes, w, "layer")
@@ -282,7 +310,7 @@ def main():
              if k in ktimes and k != dom}
     for k, r in other.items():
         r["traffic"] = measured_traffic(k, "layer-b2-T4096-D1536")
-    extra = {"kernels_layer": ktimes,
+    extra = {"ms_per_step_graph_replay": ms_graph, "kernels_layer": ktimes,
              "roofline_other": other,
              "gemm_tflops_layer": layer_gemm_flops(w.M, w.D, w.N, w.d_model) / 1e12}
     del inp, step
@@ -361,7 +389,8 @@ def main():
         "dtype": "fp32",
         "data": "synthetic",
         "config": {"workload": "layer: one selective diagonal SSM layer with input projections and SiLU gate, "
-                               "b=2, T=4096, d_model=768, D=1536, N=16, full adjoint gradient",
+                               "b=2, T=4096, d_model=768, D=1536, N=16, full adjoint gradient; each step one "
+                               "ssm_layer_grad call",
                    "batch": w.b, "seq_len": w.T, "d_model": w.d_model, "channels": w.D, "dstate": w.N,
                    "inputs": "bf16", "accumulate": "fp32", "chunk": 128},
         "roofline": roof,
