@@ -634,6 +634,11 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     const int r = lane & 3, chl = lane >> 2;
+    // Column of this lane's channel in red[]: rows of states 8..15 hold the two
+    // 8-channel halves swapped, so that the lanes of a quad (rows 20 floats
+    // apart) write distinct banks; the 16-channel sum tree in flush adds the two
+    // halves last, so the swap leaves every sum unchanged.
+    const int chs = chl ^ ((r & 2) << 2);
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const int split = blockIdx.x;
     const int64_t t0 = c * L;
@@ -862,7 +867,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     ahp[j][k] = av * h[k];
                     h[k] = fmaf(Bv[k], xv, ahp[j][k]);
                     if constexpr (GATE) yp = fmaf(Cv[k], h[k], yp);
-                    red[wave][j][r * 4 + k][chl] = g * h[k];
+                    red[wave][j][r * 4 + k][chs] = g * h[k];
                 }
                 if constexpr (GATE) {
                     const float y = quad_sum(yp);
@@ -926,7 +931,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     const float s = mb[k] * ahp[j][k];
                     ddp = fmaf(s, wn[k], ddp);
                     dA[k] = fmaf(s, dlh[j], dA[k]);
-                    red[wave][j][r * 4 + k][chl] = mb[k] * xh[j];
+                    red[wave][j][r * 4 + k][chs] = mb[k] * xh[j];
                     Mp[k] = ah[j][k] * mu[k];
                 }
                 const float dxv = quad_sum(dxp);
