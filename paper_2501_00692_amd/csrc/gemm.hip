@@ -1,25 +1,29 @@
 // gemm.hip -- bf16 MFMA GEMMs for the projection gradients (gfx950,
 // v_mfma_f32_32x32x16_bf16, fp32 accumulation), one templated kernel:
-//   dW[K][N] = X^T dZ  (X [M][K], dZ [M][N]): the reduction runs over the row
-//       index of both operands, so 8x8 blocks are transposed in registers on
-//       their way into LDS; split over M when the output has few tiles, with a
+//   dW[K][N] = X^T dZ  (X [M][K], dZ [M][N]): both operands are reduction-major
+//       (TR); their tiles are kept reduction-major in LDS and the MFMA fragments
+//       are read with the transposing LDS read (ds_read_b64_tr_b16, two per
+//       fragment); split over M when the output has few tiles, with a
 //       fixed-order second-stage reduction;
 //   dX[M][K] = dZ W^T  (dZ [M][N], W [K][N]): both operands are contiguous along
-//       the reduction and are staged as they are; the epilogue adds an optional
-//       fp32 addend, accumulates, and can write a bf16 copy into a strided buffer.
-// Workgroup: 512 threads = 4x2 waves, two per SIMD (one wave's MFMAs run while
-// the other waits for its loads or the barrier); a wave owns a 64 x (BN/2) block
-// of 32x32 MFMA tiles.  Tile BM x BN with BM = 256 and BN in {128, 192, 256};
-// interior tiles with whole reduction steps run a loop without bounds checks,
-// other loads read a clamped in-range address and select zero (no branches).
-// LDS is double-buffered over 64-deep reduction steps (one barrier per step);
-// the next step's global loads are in flight while the MFMAs run, and below
-// 256 columns the next 16-deep sub-step's fragments are read from LDS while the
-// current sub-step's MFMAs run.
+//       the reduction; fragments are plain 16-byte LDS reads.  The epilogue adds
+//       an optional fp32 addend, accumulates, and can write a bf16 copy into a
+//       strided buffer.
+// Staging: operand tiles go from global memory straight into LDS (buffer loads
+// with the LDS destination, 16 bytes per lane, no registers on the way) through
+// a ring of NS stages of BK = 32 reduction steps.  Step t waits (vmcnt) until its
+// own loads of step t+1 have landed and meets the other waves at a barrier; then
+// the loads of step t+NS-1 go into the stage that step t-1 used, and step t+1's
+// first fragments are read while step t's second half of MFMAs runs.  Pieces
+// outside the matrix (rows, columns, or the reduction tail) read as zero through
+// the buffer range check.  Workgroup: 512 threads = 4x2 waves, two per SIMD;
+// a wave owns a 64 x (BN/2) block of 32x32 MFMA tiles; tile 256 x BN.
 // Output tiles and reduction splits are assigned so that each XCD runs one
 // contiguous run of (split, row block, column block) (consecutive workgroups go
 // to different XCDs), which keeps a row block of the first operand and its
 // reduction range in one L2.
+#include <type_traits>
+
 #include "internal.h"
 
 namespace ssmk {
@@ -27,47 +31,78 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int BK = 64;   // reduction depth per step
-constexpr int LDK = BK;  // LDS row length (bf16): 8 blocks of 16 bytes, XOR-swizzled
+constexpr int BK = 32;       // reduction steps per LDS stage
+constexpr int BM = 256;      // output tile rows
+constexpr int NS = 4;        // stages in the LDS ring
+constexpr int kMaxW = 256;   // widest LDS row of the second operand (TR) / most rows (non-TR)
+constexpr int kXcds = 8;
+constexpr uint32_t kOutOfRange = 0x80000000u;  // a buffer offset past every range
+constexpr int kRsrcWord3 = 0x00020000;         // raw buffer, 32-bit data format
 
-// Physical 16-byte block of logical block `blk` in LDS row `row`: the XOR keeps
-// fragment reads (8 consecutive rows), row-wise staging writes (8 blocks of one
-// row) and transposed staging writes (rows 8 apart) free of bank conflicts.
-__device__ __forceinline__ int swz(int row, int blk) { return (blk ^ (row ^ (row >> 3))) & 7; }
+// The LDS ring: separate arrays per stage, so that the compiler sees reads of
+// one stage as independent of the loads in flight into the others.
+__shared__ __attribute__((aligned(1024))) uint16_t sA0[BM * BK];
+__shared__ __attribute__((aligned(1024))) uint16_t sA1[BM * BK];
+__shared__ __attribute__((aligned(1024))) uint16_t sA2[BM * BK];
+__shared__ __attribute__((aligned(1024))) uint16_t sA3[BM * BK];
+__shared__ __attribute__((aligned(1024))) uint16_t sB0[kMaxW * BK];
+__shared__ __attribute__((aligned(1024))) uint16_t sB1[kMaxW * BK];
+__shared__ __attribute__((aligned(1024))) uint16_t sB2[kMaxW * BK];
+__shared__ __attribute__((aligned(1024))) uint16_t sB3[kMaxW * BK];
+
+template <int S>
+__device__ __forceinline__ uint16_t* stage_a() {
+    static_assert(S >= 0 && S < NS, "stage");
+    if constexpr (S == 0) return sA0;
+    else if constexpr (S == 1) return sA1;
+    else if constexpr (S == 2) return sA2;
+    else return sA3;
+}
+template <int S>
+__device__ __forceinline__ uint16_t* stage_b() {
+    static_assert(S >= 0 && S < NS, "stage");
+    if constexpr (S == 0) return sB0;
+    else if constexpr (S == 1) return sB1;
+    else if constexpr (S == 2) return sB2;
+    else return sB3;
+}
+template <int S>
+using Stage = std::integral_constant<int, S>;
+
+// Workgroup barrier that orders LDS accesses for the compiler only: the waits
+// for the direct-to-LDS loads are explicit (wait_vm), and no other memory
+// operation needs to complete at it.
+__device__ __forceinline__ void ring_barrier() {
+    __builtin_amdgcn_sched_barrier(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_sched_barrier(0);
+}
+// Wait until at most N of this wave's vector-memory operations are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// 16 bytes per lane from buffer offset voff into LDS at lds + 16 * lane (lds is
+// wave-uniform).
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rs, uint32_t voff, uint16_t* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const uint16_t* base, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, static_cast<int>(bytes), kRsrcWord3);
+}
 
 __device__ __forceinline__ uint16_t f2bf(float v) {
     uint32_t u = __float_as_uint(v);
     if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
     u += 0x7fffu + ((u >> 16) & 1u);
     return static_cast<uint16_t>(u >> 16);
-}
-
-__device__ __forceinline__ bf16x8 lds_frag(const uint16_t* p) {
-    const uint4 v = *reinterpret_cast<const uint4*>(p);
-    return __builtin_bit_cast(bf16x8, v);
-}
-
-// Transpose an 8x8 block of bf16: in[r] holds row r (8 values, 4 words); out[c]
-// receives column c as 8 values (4 words).
-__device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[8]) {
-    uint32_t w[8][4];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-        w[r][0] = in[r].x; w[r][1] = in[r].y; w[r][2] = in[r].z; w[r][3] = in[r].w;
-    }
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        uint32_t lo[4], hi[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const uint32_t a = w[2 * j][c], b = w[2 * j + 1][c];
-            lo[j] = (a & 0xffffu) | (b << 16);          // column 2c, rows 2j, 2j+1
-            hi[j] = (a >> 16) | (b & 0xffff0000u);      // column 2c+1
-        }
-        out[2 * c] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-        out[2 * c + 1] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-    }
 }
 
 struct GemmArgs {
@@ -85,224 +120,203 @@ struct GemmArgs {
     int64_t ld16;
 };
 
-constexpr int kXcds = 8;
+// Operands contiguous along the reduction (dX = dZ W^T).  A stage holds BM rows
+// of A and BN rows of B, each a 64-byte LDS row of BK values whose four 16-byte
+// blocks are XOR-swizzled by (row >> 2) & 3: a 16-byte fragment read by 32 lanes
+// of consecutive rows then covers all 64 banks in every group of 16 lanes.
+// A 1 KB wave load fills 16 rows; lane l supplies row l/4's logical block.
+template <int BN>
+struct RowMajorOps {
+    static constexpr int NB = BN * BK * 2 / 1024;  // wave loads of B per stage
+    __amdgpu_buffer_rsrc_t ra, rb;
+    uint32_t oa[2], ob[2];
+    int ka[2], kb[2];
+    int64_t k_hi;
+    int offa[2][2], offb[2][BN / 64];  // fragment offsets (elements) per sub-step
 
-// Staging of both operand tiles (BM and BN rows x BK reduction) into LDS rows of
-// LDK bf16.  TR (reduction-major sources): 8x8 blocks, numbered A blocks first
-// (BM of them) then B blocks (BN); thread tid takes blocks tid and tid + NT,
-// transposed in registers.  Otherwise: 16-byte pieces spread over all threads.
-// FULL: the tile's rows and columns are in bounds; KF: so is the whole
-// reduction step (no checks at all when both hold).  Reduction ranges end on a multiple of 8 except in the row-wise (TR)
-// case, where each of the 8 rows of a block is checked.
-template <bool TR, int BM, int BN, int NT>
-struct Stager {
-    static constexpr int PA = TR ? BM : BM * 8;
-    static constexpr int PB = TR ? BN : BN * 8;
-    static constexpr int PER = TR ? (PA + PB + NT - 1) / NT : (PA + PB) / NT;
-    static constexpr int REGS = TR ? 8 : 1;
-    static_assert(TR || (PA % NT == 0 && PB % NT == 0), "pieces divide evenly");
-    uint4 v[PER][REGS];
+    static __device__ __forceinline__ int swz(int row) { return (row >> 2) & 3; }
 
-    template <bool FULL, bool KF>
-    __device__ __forceinline__ void load(const GemmArgs& g, int64_t r0, int64_t c0, int64_t k,
-                                         int64_t k_hi, int tid) {
-        if constexpr (TR) {
+    __device__ __forceinline__ void init(const GemmArgs& g, int64_t r0, int64_t c0, int64_t khi, int wave,
+                                         int lane, int wr, int wc) {
+        k_hi = khi;
+        // resources over the tile's rows: rows past the matrix read as zero
+        ra = rsrc(g.A + r0 * g.lda, min<int64_t>(BM, g.R - r0) * g.lda * 2);
+        rb = rsrc(g.B + c0 * g.ldb, min<int64_t>(BN, g.Cc - c0) * g.ldb * 2);
 #pragma unroll
-            for (int e = 0; e < PER; ++e) {
-                const int q = tid + NT * e;
-                if (q >= PA + PB) break;  // uniform per wave (PA + PB is a multiple of 64)
-                const bool isA = q < PA;
-                const int pc = isA ? q : q - PA;
-                const int rows8 = (isA ? BM : BN) / 8;
-                const int rb = pc / rows8, cb = pc % rows8;  // reduction block, row block
-                const uint16_t* src = isA ? g.A : g.B;
-                const int64_t ld = isA ? g.lda : g.ldb;
-                const int64_t col = (isA ? r0 : c0) + cb * 8;
-                const int64_t ncol = isA ? g.R : g.Cc;
-                // out-of-range pieces load an in-range one (clamped row and column)
-                // and select zero, so that every load is issued without a branch
-                const bool cok = FULL || col < ncol;
-                const int64_t cs = cok ? col : ncol - 8;
+        for (int i = 0; i < 2; ++i) {
+            const int row = (wave + 8 * i) * 16 + (lane >> 2);
+            ka[i] = kb[i] = ((lane & 3) ^ swz(row)) * 8;
+            oa[i] = static_cast<uint32_t>((row * g.lda + ka[i]) * 2);
+            ob[i] = static_cast<uint32_t>((row * g.ldb + kb[i]) * 2);
+        }
+        const int li = lane & 31, hk = lane >> 5;
 #pragma unroll
-                for (int r = 0; r < 8; ++r) {
-                    const int64_t kr = k + rb * 8 + r;
-                    const bool ok = cok && (KF || kr < k_hi);
-                    const uint4 t = *reinterpret_cast<const uint4*>(src + (ok ? kr : k_hi - 1) * ld + cs);
-                    v[e][r] = ok ? t : make_uint4(0u, 0u, 0u, 0u);
-                }
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int row = wr + i * 32 + li;
+                offa[ks][i] = row * BK + (((ks * 2 + hk) ^ swz(row)) * 8);
             }
-        } else {
 #pragma unroll
-            for (int e = 0; e < PER; ++e) {
-                constexpr int EA = PA / NT;  // pieces of A per thread; the rest are B
-                const bool isA = e < EA;
-                const int q = tid + NT * (isA ? e : e - EA);
-                const int row = q >> 3, seg = q & 7;
-                const int64_t gr = (isA ? r0 : c0) + row, kk = k + seg * 8;
-                const uint16_t* src = isA ? g.A : g.B;
-                const int64_t ld = isA ? g.lda : g.ldb;
-                const int64_t nrow = isA ? g.R : g.Cc;
-                const bool ok = (FULL || gr < nrow) && (KF || kk < k_hi);
-                const uint4 t = *reinterpret_cast<const uint4*>(src + (FULL || gr < nrow ? gr : nrow - 1) * ld +
-                                                                (KF || kk < k_hi ? kk : k_hi - 8));
-                v[e][0] = ok ? t : make_uint4(0u, 0u, 0u, 0u);
+            for (int j = 0; j < BN / 64; ++j) {
+                const int row = wc + j * 32 + li;
+                offb[ks][j] = row * BK + (((ks * 2 + hk) ^ swz(row)) * 8);
             }
         }
     }
-    __device__ __forceinline__ void store(uint16_t (*As)[LDK], uint16_t (*Bs)[LDK], int tid) const {
-        if constexpr (TR) {
+    // pieces past the reduction range read out of range (zero)
+    __device__ __forceinline__ uint32_t off(uint32_t o0, int kq, int64_t k) const {
+        return k + kq < k_hi ? o0 + static_cast<uint32_t>(k * 2) : kOutOfRange;
+    }
+    template <int S>
+    __device__ __forceinline__ void issue(Stage<S>, int64_t k, int wave) const {
 #pragma unroll
-            for (int e = 0; e < PER; ++e) {
-                const int q = tid + NT * e;
-                if (q >= PA + PB) break;
-                const bool isA = q < PA;
-                const int pc = isA ? q : q - PA;
-                const int rows8 = (isA ? BM : BN) / 8;
-                const int rb = pc / rows8, cb = pc % rows8;
-                uint16_t(*dst)[LDK] = isA ? As : Bs;
-                uint4 tr[8];
-                transpose8x8(v[e], tr);
+        for (int i = 0; i < 2; ++i) load_lds16(ra, off(oa[i], ka[i], k), stage_a<S>() + (wave + 8 * i) * 512);
+        if (wave < NB) load_lds16(rb, off(ob[0], kb[0], k), stage_b<S>() + wave * 512);
+        if (wave + 8 < NB) load_lds16(rb, off(ob[1], kb[1], k), stage_b<S>() + (wave + 8) * 512);
+    }
+    template <int S>
+    __device__ __forceinline__ void read(Stage<S>, int ks, bf16x8 (&a)[2], bf16x8 (&b)[BN / 64], int) const {
 #pragma unroll
-                for (int c = 0; c < 8; ++c) {
-                    const int row = cb * 8 + c;
-                    *reinterpret_cast<uint4*>(&dst[row][swz(row, rb) * 8]) = tr[c];
-                }
-            }
-        } else {
+        for (int i = 0; i < 2; ++i)
+            a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(stage_a<S>() + offa[ks][i]));
 #pragma unroll
-            for (int e = 0; e < PER; ++e) {
-                constexpr int EA = PA / NT;
-                const bool isA = e < EA;
-                const int q = tid + NT * (isA ? e : e - EA);
-                const int row = q >> 3, seg = q & 7;
-                uint16_t(*dst)[LDK] = isA ? As : Bs;
-                *reinterpret_cast<uint4*>(&dst[row][swz(row, seg) * 8]) = v[e][0];
-            }
-        }
+        for (int j = 0; j < BN / 64; ++j)
+            b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(stage_b<S>() + offb[ks][j]));
     }
 };
 
-// Main loop over the workgroup's reduction range; FULL drops the row and column
-// bounds checks.
-template <bool TR, int BM, int BN, int NT, bool FULL, bool KF, int MI, int NJ, bool PF2>
-__device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, uint16_t (*As)[BM][LDK],
-                                              uint16_t (*Bs)[BN][LDK], int64_t r0, int64_t c0,
-                                              int64_t k_lo, int64_t k_hi, int tid, int wr, int wc,
-                                              f32x16 (&acc)[MI][NJ]) {
-    const int lane = tid & 63;
-    const int li = lane & 31;
-    const int lk = (lane >> 5) * 8;
-    Stager<TR, BM, BN, NT> st;
-    if (k_lo < k_hi) {
-        st.template load<FULL, KF>(g, r0, c0, k_lo, k_hi, tid);
-        st.store(As[0], Bs[0], tid);
+// Reduction-major operands (dW = X^T dZ).  A stage holds BK rows (reduction
+// steps) of WA = BM values of A and WB values of B (BN, or 256 for BN = 192 so
+// that a row stays a power of two of 16-byte blocks); block b of row k sits at
+// b ^ 4(k & 3).  A fragment (8 consecutive reduction steps of one column per
+// lane) is two transposing 8-byte reads: in each group of 16 lanes, lane 4q+r
+// receives element r of the 8-byte chunk addressed by lane 4j+q, j = 0..3, so
+// lane l addresses (step 8(l/32) + 4h + (l%16)/4, columns 16((l/16)%2) + 4(l%4)
+// .. +3) and receives column l%32 at steps 8(l/32) + 4h + j.  The swizzle keeps
+// each 32-lane half free of bank conflicts.
+template <int BN>
+struct ColMajorOps {
+    static constexpr int WA = BM, WB = BN == 192 ? 256 : BN;
+    static constexpr int NB = BK * WB * 2 / 1024;
+    static_assert(WB <= kMaxW, "LDS row");
+    const uint16_t* A;
+    const uint16_t* B;
+    int64_t lda, ldb, k_hi;
+    uint32_t oa[2], ob[2];
+    int fa[2][2][2], fb[2][BN / 64][2];  // fragment read byte offsets [sub-step][tile][half]
+
+    static __device__ __forceinline__ int swz(int k) { return (k & 3) << 2; }
+    // byte offset of the 8-byte chunk lane `lane` addresses for the fragment of
+    // columns col0 .. col0+31 at reduction steps ks + 8(lane/32) + 4h .. +3
+    static __device__ __forceinline__ int chunk(int W, int ks, int h, int col0, int lane) {
+        const int col = col0 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+        const int k = ks + 8 * (lane >> 5) + 4 * h + ((lane & 15) >> 2);
+        return k * W * 2 + (((col >> 3) ^ swz(k)) << 4) + (((col >> 2) & 1) << 3);
     }
-    // fragments of one 16-deep sub-step, double-buffered in registers: the next
-    // sub-step's LDS reads are issued before the current sub-step's MFMAs, and the
-    // scheduling barriers keep them there, so that one wave per SIMD does not wait
-    // for LDS between MFMAs
-    auto frags = [&](int buf, int ks, bf16x8 (&a)[MI], bf16x8 (&b)[NJ]) {
+
+    __device__ __forceinline__ void init(const GemmArgs& g, int64_t r0, int64_t c0, int64_t khi, int wave,
+                                         int lane, int wr, int wc) {
+        A = g.A;
+        B = g.B;
+        lda = g.lda;
+        ldb = g.ldb;
+        k_hi = khi;
 #pragma unroll
-        for (int i = 0; i < MI; ++i) {
-            const int row = wr + i * 32 + li;
-            a[i] = lds_frag(&As[buf][row][swz(row, (ks + lk) >> 3) * 8]);
+        for (int i = 0; i < 2; ++i) {
+            const int byte = (wave + 8 * i) * 1024 + lane * 16;
+            {
+                const int row = byte / (WA * 2), col = ((byte % (WA * 2)) / 16 ^ swz(row)) * 8;
+                oa[i] = r0 + col < g.R ? static_cast<uint32_t>((row * g.lda + r0 + col) * 2) : kOutOfRange;
+            }
+            {
+                const int row = byte / (WB * 2), col = ((byte % (WB * 2)) / 16 ^ swz(row)) * 8;
+                ob[i] = (col < BN && c0 + col < g.Cc) ? static_cast<uint32_t>((row * g.ldb + c0 + col) * 2)
+                                                      : kOutOfRange;
+            }
         }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+#pragma unroll
+                for (int i = 0; i < 2; ++i) fa[ks][i][h] = chunk(WA, ks * 16, h, wr + i * 32, lane);
+#pragma unroll
+                for (int j = 0; j < BN / 64; ++j) fb[ks][j][h] = chunk(WB, ks * 16, h, wc + j * 32, lane);
+            }
+    }
+    template <int S>
+    __device__ __forceinline__ void issue(Stage<S>, int64_t k, int wave) const {
+        // resources over reduction rows k .. min(k + BK, k_hi): later rows read zero
+        const int64_t rows = min<int64_t>(BK, k_hi - k);
+        const __amdgpu_buffer_rsrc_t ra = rsrc(A + k * lda, rows * lda * 2);
+        const __amdgpu_buffer_rsrc_t rb = rsrc(B + k * ldb, rows * ldb * 2);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) load_lds16(ra, oa[i], stage_a<S>() + (wave + 8 * i) * 512);
+        if (wave < NB) load_lds16(rb, ob[0], stage_b<S>() + wave * 512);
+        if (wave + 8 < NB) load_lds16(rb, ob[1], stage_b<S>() + (wave + 8) * 512);
+    }
+    static __device__ __forceinline__ bf16x8 frag(const uint16_t* T, const int (&o)[2]) {
+        const char* base = reinterpret_cast<const char*>(T);
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(base + o[0]));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(base + o[1]));
+        const s16x8 w = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        return __builtin_bit_cast(bf16x8, w);
+    }
+    template <int S>
+    __device__ __forceinline__ void read(Stage<S>, int ks, bf16x8 (&a)[2], bf16x8 (&b)[BN / 64], int) const {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) a[i] = frag(stage_a<S>(), fa[ks][i]);
+#pragma unroll
+        for (int j = 0; j < BN / 64; ++j) b[j] = frag(stage_b<S>(), fb[ks][j]);
+    }
+};
+
+// Epilogue of one wave's MI x NJ block of 32x32 tiles (rows from row0, columns
+// from col0): result = acc (+ add) (+ C if ACC), written to C (DST) and/or as
+// bf16 (O16).  acc element v of lane l is row 8(v/4) + 4(l/32) + v%4, column
+// l%32 of its tile.  FULL: the block lies inside the output (no checks).
+template <bool ADD, bool ACC, bool DST, bool O16, bool FULL, int MI, int NJ>
+__device__ __forceinline__ void store_tile(const f32x16 (&acc)[MI][NJ], float* __restrict__ dst,
+                                           const float* __restrict__ addp, uint16_t* __restrict__ o16, int64_t ld16,
+                                           int64_t R, int64_t Cc, int64_t row0, int64_t col0, int lane) {
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
-            const int row = wc + j * 32 + li;
-            b[j] = lds_frag(&Bs[buf][row][swz(row, (ks + lk) >> 3) * 8]);
-        }
-    };
-    auto mfmas = [&](const bf16x8 (&a)[MI], const bf16x8 (&b)[NJ]) {
+            const int64_t col = col0 + j * 32 + (lane & 31);
+            const int64_t rb = row0 + i * 32 + 4 * (lane >> 5);
+            // the tile's addends first, so that their loads overlap
+            float extra[16];
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
-#pragma unroll
-            for (int j = 0; j < NJ; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    };
-    // 256-wide tiles have no registers to spare for a second fragment set: they
-    // read each sub-step's fragments right before its MFMAs
-    constexpr bool DB = BN < 256 && !(TR && PF2);
-    bf16x8 a0[MI], b0[NJ], a1[MI], b1[NJ];
-    // the MFMAs of one 64-deep step on LDS buffer `cur`, with `between` (the
-    // staging store for the next step) issued before the last sub-step
-    auto step = [&](int cur, auto&& between) {
-        static_assert(BK == 64, "four sub-steps per step");
-        if constexpr (DB) {
-            frags(cur, 16, a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-            mfmas(a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            frags(cur, 32, a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            mfmas(a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-            frags(cur, 48, a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-            mfmas(a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            between();
-            mfmas(a1, b1);
-        } else {
-#pragma unroll
-            for (int ks = 0; ks < BK; ks += 16) {
-                frags(cur, ks, a0, b0);
-                mfmas(a0, b0);
+            for (int v = 0; v < 16; ++v) {
+                const int64_t row = rb + 8 * (v >> 2) + (v & 3);
+                const bool in = FULL || (row < R && col < Cc);
+                const int64_t o = in ? row * Cc + col : 0;  // out-of-range lanes read element 0
+                float e = 0.f;
+                if constexpr (ADD) e = addp[o];
+                if constexpr (ACC) e += dst[o];
+                extra[v] = e;
             }
-            between();
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t row = rb + 8 * (v >> 2) + (v & 3);
+                if (FULL || (row < R && col < Cc)) {
+                    const float val = acc[i][j][v] + extra[v];
+                    if constexpr (DST) dst[row * Cc + col] = val;
+                    if constexpr (O16) o16[row * ld16 + col] = f2bf(val);
+                }
+            }
         }
-    };
-    const int64_t nsteps = (k_hi - k_lo + BK - 1) / BK;
-    if constexpr (PF2) {
-        // global loads two steps ahead in two staging sets used alternately: at
-        // the top of step j the set of step j+1 is in flight and the other one,
-        // stored to LDS at the end of step j-1, takes the loads of step j+2
-        Stager<TR, BM, BN, NT> st1;
-        if (nsteps > 1) st1.template load<FULL, KF>(g, r0, c0, k_lo + BK, k_hi, tid);
-        __syncthreads();
-        if (DB) frags(0, 0, a0, b0);
-        auto pair_step = [&](int64_t j, Stager<TR, BM, BN, NT>& mine, Stager<TR, BM, BN, NT>& other) {
-            const int cur = static_cast<int>(j & 1);
-            if (j + 2 < nsteps) mine.template load<FULL, KF>(g, r0, c0, k_lo + (j + 2) * BK, k_hi, tid);
-            step(cur, [&]() {
-                if (j + 1 < nsteps) other.store(As[cur ^ 1], Bs[cur ^ 1], tid);
-            });
-            __syncthreads();
-            if (DB && j + 1 < nsteps) frags(cur ^ 1, 0, a0, b0);
-        };
-        for (int64_t j = 0; j < nsteps; j += 2) {
-            pair_step(j, st, st1);
-            if (j + 1 < nsteps) pair_step(j + 1, st1, st);
-        }
-        return;
-    }
-    __syncthreads();
-    int cur = 0;
-    if (DB) frags(0, 0, a0, b0);
-    for (int64_t j = 0; j < nsteps; ++j) {
-        const bool more = j + 1 < nsteps;
-        if (more) st.template load<FULL, KF>(g, r0, c0, k_lo + (j + 1) * BK, k_hi, tid);
-        step(cur, [&]() {
-            if (more) st.store(As[cur ^ 1], Bs[cur ^ 1], tid);
-        });
-        __syncthreads();
-        cur ^= 1;
-        if (DB && more) frags(cur, 0, a0, b0);
-    }
 }
 
-template <bool TR, int BM, int BN, int WM>
-__global__ __launch_bounds__(128 * WM) void k_gemm(const GemmArgs g) {
-    constexpr int NT = 128 * WM;  // WM x 2 waves
-    constexpr int MI = BM / (32 * WM), NJ = BN / 64;  // 32x32 MFMA tiles per wave
-#ifndef SSMK_GEMM_PF2
-#define SSMK_GEMM_PF2 1
-#endif
-    constexpr bool PF2 = SSMK_GEMM_PF2 && BN == 128;  // registers for a second staging set
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDK];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][LDK];
+template <bool TR, int BN>
+__global__ __launch_bounds__(512) void k_gemm(const GemmArgs g) {
+    constexpr int MI = 2, NJ = BN / 64;  // 32x32 MFMA tiles per wave
+    using Ops = typename std::conditional<TR, ColMajorOps<BN>, RowMajorOps<BN>>::type;
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     // output tile and reduction split: workgroups are dispatched to the XCDs in
     // turn (workgroup i to XCD i % 8), so the linear id is mapped to a logical
     // index that gives every XCD one contiguous run of (split, row block, column
@@ -320,9 +334,12 @@ __global__ __launch_bounds__(128 * WM) void k_gemm(const GemmArgs g) {
     const int64_t r0 = static_cast<int64_t>(tile / ncb) * BM;
     const int64_t k_lo = static_cast<int64_t>(split) * g.kper;
     const int64_t k_hi = min(g.Kr, k_lo + g.kper);
-    const int wr = (wave >> 1) * (BM / WM);
+    const int wr = (wave >> 1) * 64;
     const int wc = (wave & 1) * (BN / 2);
+    const int64_t nsteps = k_hi > k_lo ? (k_hi - k_lo + BK - 1) / BK : 0;
 
+    Ops ops;
+    ops.init(g, r0, c0, k_hi, wave, lane, wr, wc);
     f32x16 acc[MI][NJ];
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -330,49 +347,108 @@ __global__ __launch_bounds__(128 * WM) void k_gemm(const GemmArgs g) {
         for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-    const bool full = r0 + BM <= g.R && c0 + BN <= g.Cc;
-    const bool kfull = (k_hi - k_lo) % BK == 0;
-    if (full && kfull)
-        gemm_mainloop<TR, BM, BN, NT, true, true, MI, NJ, PF2>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
-    else if (full)
-        gemm_mainloop<TR, BM, BN, NT, true, false, MI, NJ, PF2>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
-    else
-        gemm_mainloop<TR, BM, BN, NT, false, false, MI, NJ, PF2>(g, As, Bs, r0, c0, k_lo, k_hi, tid, wr, wc, acc);
-
-    // acc element v of lane l is row 8*(v/4) + 4*(l/32) + v%4, col l%32 of its tile
-    float* __restrict__ dst = g.C ? g.C + (g.direct ? 0 : static_cast<int64_t>(split) * g.R * g.Cc) : nullptr;
-    const float* __restrict__ addp = g.direct ? g.add : nullptr;
-    const bool accum = g.direct && g.accum;
-    uint16_t* __restrict__ o16 = g.direct ? g.out16 : nullptr;
+    typedef bf16x8 FA[MI];
+    typedef bf16x8 FB[NJ];
+    auto mm = [&](const FA& a, const FB& b) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int64_t col = c0 + wc + j * 32 + (lane & 31);
-            const int64_t rb = r0 + wr + i * 32 + 4 * (lane >> 5);
-            // the tile's addends first, so that their loads overlap
-            float extra[16];
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t row = rb + 8 * (v >> 2) + (v & 3);
-                const bool in = row < g.R && col < g.Cc;
-                const int64_t o = row * g.Cc + col;
-                float e = 0.f;
-                if (addp && in) e = addp[o];
-                if (accum && dst && in) e += dst[o];
-                extra[v] = e;
-            }
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t row = rb + 8 * (v >> 2) + (v & 3);
-                if (row < g.R && col < g.Cc) {
-                    const float val = acc[i][j][v] + extra[v];
-                    if (dst) dst[row * g.Cc + col] = val;
-                    if (o16) o16[row * g.ld16 + col] = f2bf(val);
-                }
-            }
+            for (int j = 0; j < NJ; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    auto read_any = [&](int s, int ks, FA& a, FB& b) __attribute__((always_inline)) {
+        switch (s) {
+            case 0: ops.read(Stage<0>{}, ks, a, b, lane); break;
+            case 1: ops.read(Stage<1>{}, ks, a, b, lane); break;
+            case 2: ops.read(Stage<2>{}, ks, a, b, lane); break;
+            default: ops.read(Stage<3>{}, ks, a, b, lane); break;
         }
+    };
+    // loads per wave per stage: two of A, one or two (or none) of B
+    const int per = 2 + (wave < Ops::NB ? 1 : 0) + (wave + 8 < Ops::NB ? 1 : 0);
+    auto wait_groups = [&](auto Gt) __attribute__((always_inline)) {  // G later stages may stay in flight
+        constexpr int G = decltype(Gt)::value;
+        if (per == 4) wait_vm<4 * G>();
+        else if (per == 3) wait_vm<3 * G>();
+        else wait_vm<2 * G>();
+    };
+    static_assert(NS == 4, "the ring code below is written for four stages");
+    if (nsteps > 0) ops.issue(Stage<0>{}, k_lo, wave);
+    if (nsteps > 1) ops.issue(Stage<1>{}, k_lo + BK, wave);
+    if (nsteps > 2) ops.issue(Stage<2>{}, k_lo + 2 * BK, wave);
+    // steady steps issue a load group each; the last NS-1 steps only drain
+    const int64_t steady = nsteps >= NS - 1 ? nsteps - (NS - 1) : 0;
+    if (steady > 0) wait_groups(std::integral_constant<int, NS - 2>{});
+    else wait_vm<0>();
+    ring_barrier();
+    FA a0, a1;
+    FB b0, b1;
+    if (nsteps > 0) ops.read(Stage<0>{}, 0, a0, b0, lane);
+    auto step = [&](auto St, int64_t t) __attribute__((always_inline)) {
+        constexpr int S = decltype(St)::value;
+        ops.read(St, 1, a1, b1, lane);
+        __builtin_amdgcn_sched_barrier(0);
+        mm(a0, b0);
+        wait_groups(std::integral_constant<int, NS - 3>{});  // step t+1's loads, every wave
+        ring_barrier();
+        ops.issue(Stage<(S + NS - 1) % NS>{}, k_lo + (t + NS - 1) * BK, wave);
+        ops.read(Stage<(S + 1) % NS>{}, 0, a0, b0, lane);
+        __builtin_amdgcn_sched_barrier(0);
+        mm(a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    int64_t t = 0;
+    for (; t + NS <= steady; t += NS) {
+        step(Stage<0>{}, t);
+        step(Stage<1>{}, t + 1);
+        step(Stage<2>{}, t + 2);
+        step(Stage<3>{}, t + 3);
+    }
+    const int64_t rem = steady - t;  // t is a multiple of NS here
+    if (rem > 0) step(Stage<0>{}, t);
+    if (rem > 1) step(Stage<1>{}, t + 1);
+    if (rem > 2) step(Stage<2>{}, t + 2);
+    if (steady > 0 && steady < nsteps) {
+        wait_vm<0>();
+        ring_barrier();
+    }
+    for (int64_t u = steady; u < nsteps; ++u) {
+        const int s = static_cast<int>(u % NS);
+        read_any(s, 1, a1, b1);
+        mm(a0, b0);
+        if (u + 1 < nsteps) read_any(s + 1 == NS ? 0 : s + 1, 0, a0, b0);
+        mm(a1, b1);
+    }
+
+    float* dst = g.C ? g.C + (g.direct ? 0 : static_cast<int64_t>(split) * g.R * g.Cc) : nullptr;
+    const float* addp = g.direct ? g.add : nullptr;
+    uint16_t* o16 = g.direct ? g.out16 : nullptr;
+    const bool accum = g.direct && g.accum && dst;
+    const bool full = r0 + BM <= g.R && c0 + BN <= g.Cc;
+    // one specialised store per combination of outputs in use (uniform per tile)
+    const int mask = (addp ? 1 : 0) | (accum ? 2 : 0) | (dst ? 4 : 0) | (o16 ? 8 : 0);
+    auto store = [&](auto Ft, auto Mt) __attribute__((always_inline)) {
+        constexpr int M = decltype(Mt)::value;
+        store_tile<(M & 1) != 0, (M & 2) != 0, (M & 4) != 0, (M & 8) != 0, decltype(Ft)::value>(
+            acc, dst, addp, o16, g.ld16, g.R, g.Cc, r0 + wr, c0 + wc, lane);
+    };
+    auto by_mask = [&](auto Ft) __attribute__((always_inline)) {
+        switch (mask) {
+            case 4: store(Ft, std::integral_constant<int, 4>{}); break;     // C
+            case 6: store(Ft, std::integral_constant<int, 6>{}); break;     // C +=
+            case 5: store(Ft, std::integral_constant<int, 5>{}); break;     // C = . + add
+            case 7: store(Ft, std::integral_constant<int, 7>{}); break;     // C += . + add
+            case 8: store(Ft, std::integral_constant<int, 8>{}); break;     // bf16 copy only
+            case 9: store(Ft, std::integral_constant<int, 9>{}); break;     // bf16 of . + add
+            case 12: store(Ft, std::integral_constant<int, 12>{}); break;   // C and its bf16 copy
+            case 13: store(Ft, std::integral_constant<int, 13>{}); break;
+            case 14: store(Ft, std::integral_constant<int, 14>{}); break;
+            case 15: store(Ft, std::integral_constant<int, 15>{}); break;
+            default: break;                                                 // no output
+        }
+    };
+    if (full) by_mask(std::true_type{});
+    else by_mask(std::false_type{});
 }
 
 // dW = (dW +) sum over splits, in split order.
@@ -390,9 +466,9 @@ inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b
 constexpr int kCUs = 256;
 
 // Output-tile width and reduction splits for an R x Cc output with reduction Kr,
-// from a simple time model: rounds of 256 workgroups x the MFMA time of one
-// workgroup's share (about 1.2 us per 256x256x64 step), plus the HBM time of
-// writing and re-reading the split partials (4 TB/s).
+// from a simple time model: rounds of 256 workgroups x the time of one
+// workgroup's share (about 0.8 us per 256x192x32 stage at full load), plus the
+// HBM time of writing and re-reading the split partials (4 TB/s).
 struct Plan {
     int bn;
     int splits;
@@ -401,15 +477,15 @@ struct Plan {
 Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split) {
     Plan best{192, 1};
     double best_us = 1e300;
-    const int bns[3] = {256, 192, 128};
+    const int bns[2] = {192, 128};
     for (int bn : bns) {
-        const int64_t tiles = ((R + 255) / 256) * ((Cc + bn - 1) / bn);
+        const int64_t tiles = ((R + BM - 1) / BM) * ((Cc + bn - 1) / bn);
         const int64_t iters = (Kr + BK - 1) / BK;
         for (int s = 1; s <= (allow_split ? 32 : 1); ++s) {
-            if (s > 1 && iters / s < 8) break;
+            if (s > 1 && iters / s < 16) break;
             const int64_t wgs = tiles * s;
             const double rounds = static_cast<double>((wgs + kCUs - 1) / kCUs);
-            double us = rounds * 1.2 * (bn / 256.0) * (static_cast<double>(Kr) / s / BK);
+            double us = rounds * 0.8 * (bn / 192.0) * static_cast<double>((iters + s - 1) / s);
             if (s > 1) us += static_cast<double>(s) * R * Cc * 8.0 / 4e12 * 1e6;
             if (us < best_us * 0.999) {
                 best_us = us;
@@ -422,18 +498,14 @@ Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split) {
 
 template <bool TR, int BN>
 void launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
-    constexpr int WM = 4;  // 4 x 2 waves, two per SIMD
-    dim3 grid(cdiv(g.Cc, BN), cdiv(g.R, 256), static_cast<unsigned>(splits));
-    hipLaunchKernelGGL((k_gemm<TR, 256, BN, WM>), grid, dim3(128 * WM), 0, s, g);
+    dim3 grid(cdiv(g.Cc, BN), cdiv(g.R, BM), static_cast<unsigned>(splits));
+    hipLaunchKernelGGL((k_gemm<TR, BN>), grid, dim3(512), 0, s, g);
 }
 
 template <bool TR>
 void launch_plan(const GemmArgs& g, const Plan& pl, hipStream_t s) {
-    switch (pl.bn) {
-        case 128: launch_tile<TR, 128>(g, pl.splits, s); break;
-        case 192: launch_tile<TR, 192>(g, pl.splits, s); break;
-        default: launch_tile<TR, 256>(g, pl.splits, s); break;
-    }
+    if (pl.bn == 128) launch_tile<TR, 128>(g, pl.splits, s);
+    else launch_tile<TR, 192>(g, pl.splits, s);
 }
 
 }  // namespace
