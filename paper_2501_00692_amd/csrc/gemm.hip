@@ -451,14 +451,36 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs g) {
     else by_mask(std::false_type{});
 }
 
-// dW = (dW +) sum over splits, in split order.
+// dW = (dW +) sum over splits, in split order; four consecutive elements per
+// thread (KN is a multiple of 4: the output width is), the loads of up to eight
+// splits issued before their in-order adds.
 __global__ __launch_bounds__(256) void k_splitk_reduce(int64_t KN, int splits, const float* part,
                                                        float* dW, int accum) {
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
     if (i >= KN) return;
-    float s = 0.f;
-    for (int q = 0; q < splits; ++q) s += part[q * KN + i];
-    dW[i] = accum ? dW[i] + s : s;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int q0 = 0; q0 < splits; q0 += 8) {
+        float4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            v[u] = q0 + u < splits ? *reinterpret_cast<const float4*>(part + (q0 + u) * KN + i)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            if (q0 + u < splits) {
+                s.x += v[u].x;
+                s.y += v[u].y;
+                s.z += v[u].z;
+                s.w += v[u].w;
+            }
+        }
+    }
+    float4* o = reinterpret_cast<float4*>(dW + i);
+    if (accum) {
+        const float4 d = *o;
+        s = make_float4(d.x + s.x, d.y + s.y, d.z + s.z, d.w + s.w);
+    }
+    *o = s;
 }
 
 inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b - 1) / b); }
@@ -530,7 +552,7 @@ hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, in
     }
     if (!direct) {
         SSMK_TIMED("splitk_reduce", s);
-        hipLaunchKernelGGL(k_splitk_reduce, dim3(cdiv(K * N, 256)), dim3(256), 0, s, K * N, pl.splits,
+        hipLaunchKernelGGL(k_splitk_reduce, dim3(cdiv(K * N, 1024)), dim3(256), 0, s, K * N, pl.splits,
                            static_cast<const float*>(ws), dW, accum ? 1 : 0);
     }
     return hipGetLastError();
