@@ -78,6 +78,29 @@ def _timed(fn, steps, warmup, torch):
     return start.elapsed_time(stop) / steps
 
 
+def _timed_each(fn, reps, warmup, torch, flush=None):
+    """Median, p10 and p90 of per-rep times (ms), each rep bracketed by its own
+    events; with `flush`, a 512 MB write runs before every rep (outside the
+    events) so that the rep starts with cold L2 and MALL caches."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        if flush is not None:
+            flush()
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        start.record()
+        fn()
+        stop.record()
+        stop.synchronize()
+        times.append(start.elapsed_time(stop))
+    times.sort()
+    pick = lambda q: times[min(len(times) - 1, int(q * (len(times) - 1) + 0.5))]
+    return {"median": pick(0.5), "p10": pick(0.1), "p90": pick(0.9), "reps": reps}
+
+
 def _timed_graph(fn, steps, warmup, torch):
     """Per-step time of `fn` captured once in a HIP graph and replayed `steps`
     times (launch overheads between the step's kernels removed)."""
@@ -299,6 +322,11 @@ def main():
     # the same step captured in a HIP graph and replayed, reported beside it (the
     # gaps between dependent kernels are on the GPU side: replay gains nothing)
     ms_graph = _timed_graph(step, args.steps, args.warmup, torch)
+    # per-rep spread, warm and with the L2 and MALL flushed before every rep
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    spread_warm = _timed_each(step, 20, 3, torch)
+    spread_cold = _timed_each(step, 20, 3, torch, flush=lambda: scratch.fill_(1))
+    del scratch
     ktimes = _kernel_times(step, args.steps, ssm, torch)
     dom = max(ktimes, key=lambda k: ktimes[k]["total_ms"])
     roof = roofline_for(dom, ktimes, w, "layer")
@@ -310,7 +338,8 @@ def main():
              if k in ktimes and k != dom}
     for k, r in other.items():
         r["traffic"] = measured_traffic(k, "layer-b2-T4096-D1536")
-    extra = {"ms_per_step_graph_replay": ms_graph, "kernels_layer": ktimes,
+    extra = {"ms_per_step_graph_replay": ms_graph, "ms_per_step_warm": spread_warm,
+             "ms_per_step_cold": spread_cold, "kernels_layer": ktimes,
              "roofline_other": other,
              "gemm_tflops_layer": layer_gemm_flops(w.M, w.D, w.N, w.d_model) / 1e12}
     del inp, step

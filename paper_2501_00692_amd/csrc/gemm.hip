@@ -19,9 +19,10 @@
 // the buffer range check.  Workgroup: 512 threads = 4x2 waves, two per SIMD;
 // a wave owns a 64 x (BN/2) block of 32x32 MFMA tiles; tile 256 x BN.
 // Output tiles and reduction splits are assigned so that each XCD runs one
-// contiguous run of (split, row block, column block) (consecutive workgroups go
-// to different XCDs), which keeps a row block of the first operand and its
-// reduction range in one L2.
+// contiguous run of (split, tile) (consecutive workgroups go to different XCDs),
+// tiles ordered in groups of four row blocks, so that the tiles one XCD runs at
+// a time share row blocks of the first operand and column blocks of the second
+// in its L2.
 #include <type_traits>
 
 #include "internal.h"
@@ -39,6 +40,7 @@ constexpr int BM = 256;      // output tile rows
 constexpr int NS = 4;        // stages in the LDS ring
 constexpr int kMaxW = 256;   // widest LDS row of the second operand (TR) / most rows (non-TR)
 constexpr int kXcds = 8;
+constexpr int kGroupRows = 4;  // row blocks per group of the tile order
 constexpr uint32_t kOutOfRange = 0x80000000u;  // a buffer offset past every range
 constexpr int kRsrcWord3 = 0x00020000;         // raw buffer, 32-bit data format
 
@@ -330,8 +332,14 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs g) {
     const int xq = nwg / kXcds, xr = nwg % kXcds, xcd = lin % kXcds;
     const int logical = (xcd < xr ? xcd * (xq + 1) : xr * (xq + 1) + (xcd - xr) * xq) + lin / kXcds;
     const int tile = logical % ntl, split = logical / ntl;
-    const int64_t c0 = static_cast<int64_t>(tile % ncb) * BN;
-    const int64_t r0 = static_cast<int64_t>(tile / ncb) * BM;
+    // tiles in groups of kGroupRows row blocks, column-major inside a group, so
+    // that the 32 consecutive tiles one XCD runs at a time form a block of about
+    // 4 row blocks x 8 column blocks (both operands reused from its L2)
+    const int nrb = static_cast<int>(gridDim.y);
+    const int grp = tile / (kGroupRows * ncb), first = grp * kGroupRows;
+    const int gh = min(kGroupRows, nrb - first), within = tile - grp * kGroupRows * ncb;
+    const int64_t r0 = static_cast<int64_t>(first + within % gh) * BM;
+    const int64_t c0 = static_cast<int64_t>(within / gh) * BN;
     const int64_t k_lo = static_cast<int64_t>(split) * g.kper;
     const int64_t k_hi = min(g.Kr, k_lo + g.kper);
     const int wr = (wave >> 1) * 64;
