@@ -138,7 +138,4 @@ hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, i
                           const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
                           uint16_t* out16, int64_t ld16, hipStream_t s);
 
-// fp32 -> bf16 (round to nearest even) copy of a [rows][cols] block into a strided
-// destination: dst[r*ldd + col0 + c] = bf16(src[r*lds + c]).
-
 }  // namespace ssmk
