@@ -186,6 +186,24 @@ def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False, pairs=False):
     return step
 
 
+def forward_bytes_per_token(D, N, s, gate):
+    """Compulsory HBM bytes per token of the forward: reads x, Delta (and z), B, C;
+    writes y (input dtype)."""
+    return D * (3 * s + (s if gate else 0)) + 2 * N * s
+
+
+def forward_step(w, inp, ssm, torch):
+    """One forward (y only) of the scan with the workload's options."""
+    z = inp.get("z") if w.proj else None
+    desc = ssm.make_desc(inp["x"], w.N, w.proj, z is not None, 0, False, False)
+    ws = torch.empty(ssm.forward_workspace_size(desc), dtype=torch.uint8, device="cuda")
+
+    def step():
+        ssm.ssm_adjoint_forward(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], z=z, softplus=w.proj,
+                                workspace=ws)
+    return step
+
+
 def stack_step(K, b, T, D, N, ssm, torch, exact):
     """One whole K-layer step: the forward of every layer, then every layer's
     parameter gradient (Prop. 3 or backpropagation)."""
@@ -386,6 +404,19 @@ def main():
             res[f"{name}/{kind}/tbar={tbar}" + (f"/{variant}" if variant else "")] = entry
             del x, st
             torch.cuda.empty_cache()
+        # the forward alone (y only), reported beside the gradients
+        fwd = {}
+        for name in ("layer", "long"):
+            wl = WORKLOADS[name]
+            x = make_inputs(wl, device="cuda")
+            st = forward_step(wl, x, ssm, torch)
+            m = _timed(st, 10, 2, torch)
+            bpt = forward_bytes_per_token(wl.D, wl.N, 2 if wl.bf16 else 4, wl.proj)
+            fwd[name] = {"ms": m, "tokens_per_s": wl.M / (m * 1e-3), "bytes_per_token": bpt,
+                         "hbm_frac_algorithmic": bpt * wl.M / (m * 1e-3) / (HBM_PEAK_GBS * 1e9)}
+            del x, st
+            torch.cuda.empty_cache()
+        res["forward"] = fwd
         # the K-layer residual stack (forward + gradients of every layer), Prop. 3 and
         # backpropagation, and how far apart their parameter gradients are
         K, b, T, D, N = 4, 2, 4096, 1536, 16

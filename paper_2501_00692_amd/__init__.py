@@ -182,6 +182,13 @@ def grad_workspace_size(desc: SsmDesc, tbar: int = 0, pairs: bool = False) -> in
     return n.value
 
 
+def forward_workspace_size(desc: SsmDesc) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().ssm_adjoint_forward_workspace_size(ctypes.byref(desc), ctypes.byref(n)),
+           "ssm_adjoint_forward_workspace_size")
+    return n.value
+
+
 def ssm_adjoint_forward(x, delta, A_log, B, C, h0=None, z=None, softplus=False, chunk=0, want_h_last=False,
                         workspace=None, b_delta=False):
     """Forward pass; returns ``y`` (and ``h_last`` if asked).  ``y`` has x's dtype.

@@ -462,50 +462,94 @@ __global__ __launch_bounds__(256) void k_carry(const ScanProblem p) {
 }
 
 // ---------------------------------------------------------------------------
-// k_forward: grid (ceil(D/256), nc, b), 256 threads, one lane per channel.
-// y_t = sum_n C_t h_t (times silu(z_t) with the gate), the state recomputed from
-// the chunk carry-in.
+// k_forward: grid (ceil(D/64), nc, b), 256 threads; as in k_chunk_aggr the 4
+// lanes of a quad share a channel and hold 4 of its states.  y_t = sum_n C_t h_t
+// (times silu(z_t) with the gate), the state recomputed from the chunk carry-in
+// H_c.  B and C are staged in LDS 64 steps at a time for the workgroup; lane r
+// prepares the per-channel quantities of step s0+r of each group of 4 steps and
+// broadcasts them to its quad (its raw inputs loaded one group ahead); the
+// quad's sum over its states gives y_t, which the lane that prepared step t
+// finishes and stores.  Steps past the end of the chunk have Delta = x = 0 and
+// B = C = 0, so every group runs (no tail branch around the arithmetic).
 // ---------------------------------------------------------------------------
 template <typename TI, bool SP, bool GATE>
 __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    constexpr int SB = 64;             // steps per staged block
+    constexpr int PT = SB * 32 / 256;  // staged values per thread
+    __shared__ __attribute__((aligned(16))) float bcs[SB][32];
+    const int tid = threadIdx.x;
+    const int r = tid & 3;
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);
     const int64_t c = blockIdx.y, bb = blockIdx.z;
-    if (d >= p.D) return;
-    const TI* X = static_cast<const TI*>(p.x);
-    const TI* DL = static_cast<const TI*>(p.delta);
+    const bool dv = d < p.D;
     const TI* Bp = static_cast<const TI*>(p.B);
     const TI* Cp = static_cast<const TI*>(p.C);
-    const TI* Z = static_cast<const TI*>(p.z);
     TI* Y = static_cast<TI*>(p.y);
-    const int64_t cb = ((bb * p.nc + c) * p.N) * p.D + d;
-    float cn[16], h[16];
+    float cn[4], wn[4];
+    lane_consts(p.A_log, d, r, p.N, dv, p.ascalar, cn, wn);
+    const int64_t cb = ((bb * p.nc + c) * p.N + r * 4) * p.D + d;
+    float h[4];
 #pragma unroll
-    for (int n = 0; n < 16; ++n) {
-        cn[n] = n < p.N ? -__expf(p.A_log[p.ascalar ? d : d * p.N + n]) * kLog2e : 0.f;
-        h[n] = ldm(p.hbuf, cb + n * p.D, n < p.N);
-    }
+    for (int k = 0; k < 4; ++k) h[k] = ldm(p.hbuf, cb + k * p.D, dv && r * 4 + k < p.N);
     const int64_t t0 = c * p.L;
     const int64_t t1 = min(t0 + p.L, p.T);
-#pragma unroll 2
-    for (int64_t t = t0; t < t1; ++t) {
-        const int64_t td = (bb * p.T + t) * p.D + d;
-        const float pv = ldf(DL, td);
-        const float dl = SP ? softplus_f(pv) : pv;
-        const float xv = p.bdelta ? ldf(X, td) * dl : ldf(X, td);  // input term (Delta) B x
-        float Bv[16], Cv[16];
-        ld_row16(Bp, bb * p.T + t, p.N, Bv);
-        ld_row16(Cp, bb * p.T + t, p.N, Cv);
-        float y = 0.f;
+    RawIn<TI, 1> nb;
+    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, false, nb);
+    uint32_t zb = 0;
+    if constexpr (GATE) zb = ldbits(static_cast<const TI*>(p.z), dv && t0 + r < p.T ? (bb * p.T + t0 + r) * p.D + d : 0);
+    for (int64_t sb = t0; sb < t1; sb += SB) {
+        float bcv[PT];
 #pragma unroll
-        for (int n = 0; n < 16; ++n) {
-            h[n] = fmaf(fexp2(cn[n] * dl), h[n], Bv[n] * xv);
-            y = fmaf(Cv[n], h[n], y);
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + 256 * e;
+            const int t = i >> 5, cc = i & 31, n = cc & 15;
+            const int64_t tg = sb + t;
+            bcv[e] = ldm(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, tg < t1 && n < p.N);
         }
-        if constexpr (GATE) {
-            const float zv = ldf(Z, td);
-            y *= zv * sigmoid_f(zv);
+        lds_barrier();  // the previous block's reads are done
+#pragma unroll
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + 256 * e;
+            bcs[i >> 5][i & 31] = bcv[e];
         }
-        stf(Y, td, y);
+        lds_barrier();
+        const int64_t se = min(sb + SB, t1);
+        for (int64_t s0 = sb; s0 < se; s0 += 4) {
+            // this group's inputs, then the next group's loads
+            const bool v = dv && s0 + r < t1;
+            const float pr = fin<TI>(nb.p[0], v);
+            float xr = fin<TI>(nb.x[0], v);
+            float zr = 0.f;
+            if constexpr (GATE) zr = fin<TI>(zb, v);
+            load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, false, nb);
+            if constexpr (GATE) {
+                const int64_t tz = s0 + 4 + r;
+                zb = ldbits(static_cast<const TI*>(p.z), dv && tz < p.T ? (bb * p.T + tz) * p.D + d : 0);
+            }
+            const float dlr = SP ? softplus_sel(pr, v) : pr;
+            if (p.bdelta) xr *= dlr;  // input term Delta B x
+            float yk = 0.f;
+            const int tb = static_cast<int>(s0 - sb);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float xv = quad_bcast(xr, j);
+                const float dl = quad_bcast(dlr, j);
+                const float4 b4 = *reinterpret_cast<const float4*>(&bcs[tb + j][4 * r]);
+                const float4 c4 = *reinterpret_cast<const float4*>(&bcs[tb + j][16 + 4 * r]);
+                const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
+                const float Cv[4] = {c4.x, c4.y, c4.z, c4.w};
+                float yp = 0.f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
+                    yp = fmaf(Cv[k], h[k], yp);
+                }
+                const float y = quad_sum(yp);
+                if (j == r) yk = y;
+            }
+            if constexpr (GATE) yk *= zr * sigmoid_f(zr);
+            if (v) stf(Y, (bb * p.T + s0 + r) * p.D + d, yk);
+        }
     }
 }
 
@@ -1104,7 +1148,6 @@ inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b
 
 template <typename TI, bool SP, bool GATE, bool N16>
 hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
-    dim3 g1(cdiv(p.D, 256), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
@@ -1115,7 +1158,7 @@ hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
                                      static_cast<unsigned>(2 * p.nb)),
                        dim3(256), 0, s, p);
     SSMK_TIMED("forward", s);
-    hipLaunchKernelGGL((k_forward<TI, SP, GATE>), g1, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((k_forward<TI, SP, GATE>), g4, dim3(256), 0, s, p);
     return hipGetLastError();
 }
 

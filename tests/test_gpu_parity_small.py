@@ -64,6 +64,26 @@ def test_forward_small(chunk):
     check("h_last", to_np(hl), rh, TOL_F32)
 
 
+# the layer's forward configuration (bf16 inputs, softplus, gate) with ragged
+# length and channel count (T = 300 ends inside a chunk, 72 channels end inside a
+# 64-channel workgroup); y is bf16, the state fp32
+GATE_BF16 = Workload("fwd_gate_bf16", 2, 300, 72, 16, 32, 0, True, True, 692151)
+
+
+@pytest.mark.parametrize("chunk", [16, 128])
+def test_forward_gate_bf16(chunk):
+    w = GATE_BF16
+    say(f"[forward gate bf16] T={w.T} D={w.D} chunk={chunk}")
+    inp = _inputs(w, h0=True)
+    y, hl = ssm.ssm_adjoint_forward(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], h0=inp["h0"],
+                                    z=inp["z"], softplus=True, chunk=chunk, want_h_last=True)
+    torch.cuda.synchronize()
+    ry, rh = oracle.forward(*(to_np(inp[k]) for k in ("x", "delta", "A_log", "B", "C")), h0=to_np(inp["h0"]),
+                            z=to_np(inp["z"]), delta_softplus=True)
+    check("y", to_np(y), ry, TOL_BF16)
+    check("h_last", to_np(hl), rh, TOL_F32)
+
+
 @pytest.mark.parametrize("chunk", [16, 64, 128, 256])
 def test_grad_small_full(chunk):
     w = SMALL
