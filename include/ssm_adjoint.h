@@ -154,8 +154,9 @@ ssm_status ssm_adjoint_grad_pairs(const ssm_desc* desc, int32_t mode, int64_t tb
  *   dX [M][K]    (fp32)  = dZ W^T      (skipped if dX == NULL; needs W)
  * X: bf16 [M][K] with row stride ldx >= K; dZ: bf16 [M][Nout], stride lddz >= Nout;
  * W: bf16 [K][Nout], stride ldw >= Nout.  flags: SSM_ACCUM_DW / SSM_ACCUM_DX.
- * bf16 operands, fp32 accumulation (MFMA).  Strides are in elements and must be
- * multiples of 8; pointers 16-byte aligned. */
+ * bf16 operands, fp32 accumulation (MFMA).  Strides are in elements, multiples of
+ * 8 and at most 2^21; K and Nout multiples of 8 and at most 2^20; pointers 16-byte
+ * aligned (SSM_ERR_SHAPE / SSM_ERR_UNSUPPORTED / SSM_ERR_ALIGN otherwise). */
 ssm_status ssm_proj_grad_workspace_size(int64_t M, int64_t K, int64_t Nout, uint32_t flags,
                                         size_t* bytes);
 ssm_status ssm_proj_grad(int64_t M, int64_t K, int64_t Nout, const void* X, int64_t ldx,

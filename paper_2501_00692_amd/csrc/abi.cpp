@@ -351,6 +351,8 @@ ssm_status ssm_proj_grad_workspace_size(int64_t M, int64_t K, int64_t Nout, uint
     return SSM_OK;
 }
 
+constexpr int64_t kMaxLd = int64_t(1) << 21;
+
 static ssm_status check_gemm_shape(int64_t M, int64_t K, int64_t Nout, int64_t ldx, int64_t lddz,
                                    int64_t ldw, bool need_w) {
     if (M < 1 || K < 1 || Nout < 1)
@@ -365,6 +367,9 @@ static ssm_status check_gemm_shape(int64_t M, int64_t K, int64_t Nout, int64_t l
         return fail(SSM_ERR_ALIGN, "leading dimensions must be multiples of 8 elements");
     if (M > (int64_t(1) << 31) || K > (int64_t(1) << 20) || Nout > (int64_t(1) << 20))
         return fail(SSM_ERR_SHAPE, "GEMM too large");
+    // the kernels address an operand tile (at most 256 rows) with 32-bit byte offsets
+    if (ldx > kMaxLd || lddz > kMaxLd || (need_w && ldw > kMaxLd))
+        return fail(SSM_ERR_SHAPE, "leading dimensions must be at most %lld elements", (long long)kMaxLd);
     return SSM_OK;
 }
 

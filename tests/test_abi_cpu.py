@@ -127,6 +127,7 @@ def test_proj_errors(lib):
     assert call(16, 8, 8, dZ=None) == 1
     assert call(16, 8, 8, dX=FAKE) == 1  # dX needs W
     assert call(16, 8, 8, ldx=4) == 2
+    assert call(16, 8, 8, ldx=(1 << 21) + 8) == 2  # strides past the 32-bit tile offsets
 
 
 def test_layer_rejects_fp32(lib):
