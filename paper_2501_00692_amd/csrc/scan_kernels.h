@@ -673,7 +673,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     static_assert(NP % 64 == 0 && NP <= NTH, "pair layout");
     __shared__ BCStage<TI, L> bc;
     __shared__ __attribute__((aligned(16))) float red[NW][S][16][20];  // per wave [step][state][channel]
-    __shared__ float wsum[2][NW][NP];  // per-wave channel sums, alternating buffers
+    __shared__ float wsum[4][NW][NP];  // per-wave channel sums: (dC, dB) of a segment, two segments alternating
     __shared__ float acc[L][32];       // chunk totals: dB in columns 0..15, dC in 16..31
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
@@ -723,10 +723,10 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     bc.template load<NTH>(p, bb, t0, tid);
     __syncthreads();
 
-    int fb = 0;
-    // Channel sums of red[wave] for the pairs of segment q, added over the waves
-    // (in wave order) into acc columns col..col+15.  Every wave calls it.
-    auto flush = [&](int q, int col) {
+    int pair = 0;
+    // Channel sums of red[wave] (16 channels per (step, state) pair of the
+    // segment) into this wave's slot of wsum; every wave calls it.
+    auto wave_sums = [&](int slot) {
         wave_lds_sync();
 #pragma unroll
         for (int i = 0; i < NP / 64; ++i) {
@@ -736,17 +736,25 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             const float4 a1 = *reinterpret_cast<const float4*>(&red[wave][j][n][4]);
             const float4 a2 = *reinterpret_cast<const float4*>(&red[wave][j][n][8]);
             const float4 a3 = *reinterpret_cast<const float4*>(&red[wave][j][n][12]);
-            wsum[fb][wave][o] = (((a0.x + a0.y) + (a0.z + a0.w)) + ((a1.x + a1.y) + (a1.z + a1.w))) +
-                                (((a2.x + a2.y) + (a2.z + a2.w)) + ((a3.x + a3.y) + (a3.z + a3.w)));
+            wsum[slot][wave][o] = (((a0.x + a0.y) + (a0.z + a0.w)) + ((a1.x + a1.y) + (a1.z + a1.w))) +
+                                  (((a2.x + a2.y) + (a2.z + a2.w)) + ((a3.x + a3.y) + (a3.z + a3.w)));
         }
+    };
+    // After both halves of segment q: one barrier, then the wave sums of dC
+    // (slot 2 pair) and dB (slot 2 pair + 1) are added in wave order into acc.
+    // The two pairs of slots alternate between segments, so a fast wave writing
+    // the next segment's sums never meets a slow wave still reading these.
+    auto flush = [&](int q) {
         lds_barrier();
-        if (tid < NP) {
-            float s = wsum[fb][0][tid];
+        for (int o2 = tid; o2 < 2 * NP; o2 += NTH) {
+            const int half = o2 >= NP ? 1 : 0, o = o2 - half * NP;
+            const int slot = 2 * pair + half;
+            float sum = wsum[slot][0][o];
 #pragma unroll
-            for (int w = 1; w < NW; ++w) s += wsum[fb][w][tid];
-            acc[q * S + (tid >> 4)][col + (tid & 15)] += s;
+            for (int w = 1; w < NW; ++w) sum += wsum[slot][w][o];
+            acc[q * S + (o >> 4)][(half ? 0 : 16) + (o & 15)] += sum;
         }
-        fb ^= 1;
+        pair ^= 1;
     };
 
     for (int64_t it = 0; it < nit; ++it) {
@@ -930,7 +938,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     if constexpr (OUT16) stf(sv[jj] ? dz16o + (tl * ldz16 + d32) : sink16, 0, v);
                 }
             }
-            flush(q, 16);
+            wave_sums(2 * pair);  // dC
 
             float dxk[SPL], ddk[SPL];
 #pragma unroll
@@ -997,7 +1005,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 if constexpr (OUT != 2) *(sv[jj] ? ddo + off : sinkf) = ddv;
                 if constexpr (OUT16) stf(sv[jj] ? dd16o + (tl * ldd16 + d32) : sink16, 0, ddv);
             }
-            flush(q, 0);
+            wave_sums(2 * pair + 1);  // dB
+            flush(q);
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k) *(nv[k] ? p.hbuf + (cb + k * p.D) : sinkf) = dA[k] * wn[k];
