@@ -124,6 +124,22 @@ def test_layer_workload_every_entry(tbar):
     say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
 
 
+def test_layer_workload_deterministic():
+    """Two calls at the layer workload (channel splits of the scan, a split
+    reduction in both dW GEMMs, the multi-slice dA_log sum) give bit-identical
+    outputs: every reduction runs in a fixed order."""
+    w = WORKLOADS["layer"]
+    say(f"[layer determinism] {w}")
+    inp = make_inputs(w, device="cuda")
+    args = (inp["u"], inp["x"], inp["z"], inp["delta"], inp["B"], inp["C"], inp["W_x"], inp["W_in"], inp["A_log"],
+            inp["dy"])
+    a = ssm.ssm_layer_grad(*args, want_du=True, want_scan=True)
+    b = ssm.ssm_layer_grad(*args, want_du=True, want_scan=True)
+    torch.cuda.synchronize()
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+
+
 def _layer_sampled(name, tbar):
     w = WORKLOADS[name]
     say(f"[layer sampled] {w} tbar={tbar}")
