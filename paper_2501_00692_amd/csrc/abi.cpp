@@ -131,9 +131,12 @@ LayerWs layer_ws(const ssm_desc* d, int64_t L, bool trunc, int64_t d_model) {
     w.f32_off = off;  // fp32 dx, ddelta, dz [M][D] and dB, dC [M][N]
     off = up256(off + size_t(M) * (3 * D + 2 * N) * 4);
     w.gemm_off = off;
-    size_t g1 = ssmk::gemm_dw_workspace(M, D, D + 2 * N);
-    size_t g2 = ssmk::gemm_dw_workspace(M, d_model, 2 * D);
-    off = up256(off + (g1 > g2 ? g1 : g2));
+    // the layer's four products run one after the other and share the region
+    size_t g = ssmk::gemm_dw_workspace(M, D, D + 2 * N);
+    for (size_t gi : {ssmk::gemm_dw_workspace(M, d_model, 2 * D), ssmk::gemm_dx_workspace(M, D, D + 2 * N),
+                      ssmk::gemm_dx_workspace(M, d_model, 2 * D)})
+        g = gi > g ? gi : g;
+    off = up256(off + g);
     w.total = off;
     return w;
 }
@@ -347,7 +350,8 @@ ssm_status ssm_proj_grad_workspace_size(int64_t M, int64_t K, int64_t Nout, uint
     if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");
     if (M < 1 || K < 1 || Nout < 1) return fail(SSM_ERR_SHAPE, "M, K, Nout must be >= 1");
     if (flags & ~(SSM_ACCUM_DW | SSM_ACCUM_DX)) return fail(SSM_ERR_SHAPE, "unknown flag bits");
-    *bytes = ssmk::gemm_dw_workspace(M, K, Nout);
+    const size_t dw = ssmk::gemm_dw_workspace(M, K, Nout), dx = ssmk::gemm_dx_workspace(M, K, Nout);
+    *bytes = dw > dx ? dw : dx;  // the two products run one after the other
     return SSM_OK;
 }
 
@@ -385,8 +389,10 @@ ssm_status ssm_proj_grad(int64_t M, int64_t K, int64_t Nout, const void* X, int6
     if (dX) REQUIRE_PTR(W, "W");
     OPTIONAL_PTR(dW, "dW");
     OPTIONAL_PTR(dX, "dX");
-    if (dW) {
-        st = check_workspace(workspace, workspace_bytes, ssmk::gemm_dw_workspace(M, K, Nout));
+    {
+        const size_t dw = dW ? ssmk::gemm_dw_workspace(M, K, Nout) : 0;
+        const size_t dx = dX ? ssmk::gemm_dx_workspace(M, K, Nout) : 0;
+        st = check_workspace(workspace, workspace_bytes, dw > dx ? dw : dx);
         if (st) return st;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -399,7 +405,7 @@ ssm_status ssm_proj_grad(int64_t M, int64_t K, int64_t Nout, const void* X, int6
     if (dX) {
         hipError_t e = ssmk::launch_gemm_dx(M, K, Nout, static_cast<const uint16_t*>(dZ), lddz,
                                             static_cast<const uint16_t*>(W), ldw, dX,
-                                            (flags & SSM_ACCUM_DX) != 0, nullptr, nullptr, 0, s);
+                                            (flags & SSM_ACCUM_DX) != 0, nullptr, nullptr, 0, workspace, s);
         if (e != hipSuccess) return hip_fail(e, "ssm_proj_grad dX launch");
     }
     return SSM_OK;
@@ -498,7 +504,7 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     // dx_total = dx + dZx W_x^T, also packed into [dx_total | dz]
     // (the fp32 dx_total only when the caller asks for it)
     e = ssmk::launch_gemm_dx(M, D, nx, dzx, nx, static_cast<const uint16_t*>(W_x), nx, dx_total, false,
-                             dx_, dxz, 2 * D, s);
+                             dx_, dxz, 2 * D, gws, s);
     if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dx_total launch");
     // dW_in = u^T [dx_total | dz]
     e = ssmk::launch_gemm_dw(M, d_model, 2 * D, static_cast<const uint16_t*>(u), d_model, dxz, 2 * D,
@@ -506,7 +512,7 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_in launch");
     if (du) {
         e = ssmk::launch_gemm_dx(M, d_model, 2 * D, dxz, 2 * D, static_cast<const uint16_t*>(W_in),
-                                 2 * D, du, false, nullptr, nullptr, 0, s);
+                                 2 * D, du, false, nullptr, nullptr, 0, gws, s);
         if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad du launch");
     }
     return SSM_OK;
@@ -528,7 +534,7 @@ constexpr int64_t kMaxStackLayers = 4096;
 // du, y_K when the caller does not take it, the scan and layer workspaces).
 struct StackWs {
     size_t per_layer, off_u, off_x, off_z, off_dp, off_B, off_C, off_r, off_y, off_wi, off_wx;
-    size_t off_ytil, off_g, off_g16, off_du, off_yk, off_fws, off_lws, total;
+    size_t off_ytil, off_g, off_g16, off_du, off_yk, off_fws, off_lws, off_gws, total;
     size_t fws_bytes, lws_bytes;
 };
 
@@ -560,6 +566,9 @@ StackWs stack_ws(const ssm_desc* d, int64_t K, int64_t L, bool trunc) {
     w.off_fws = o; o = up256(o + w.fws_bytes);
     w.lws_bytes = layer_ws(&ld, L, trunc, D).total;
     w.off_lws = o; o = up256(o + w.lws_bytes);
+    // split partials of the forward projections (the narrow B and C products)
+    const size_t gx = ssmk::gemm_dx_workspace(M, D, D), gn = ssmk::gemm_dx_workspace(M, N, D);
+    w.off_gws = o; o = up256(o + (gx > gn ? gx : gn));
     w.total = o;
     return w;
 }
@@ -668,14 +677,17 @@ ssm_status ssm_stack_grad(const ssm_desc* desc, int64_t K, int32_t grad, int32_t
         STACK_HIP(ssmk::launch_transpose16(static_cast<const uint16_t*>(W_x[k]), wx, D, D + 2 * N, s),
                   "ssm_stack_grad transpose");
         // out[M][c] = sum_j a[M][j] W^T[c][j]: the dX form of the projection GEMM
-        STACK_HIP(ssmk::launch_gemm_dx(M, D, D, u, D, wi, D, nullptr, false, nullptr, x, D, s), "ssm_stack_grad x");
-        STACK_HIP(ssmk::launch_gemm_dx(M, D, D, u, D, wi + D * D, D, nullptr, false, nullptr, z, D, s),
+        void* gws = ws + w.off_gws;
+        STACK_HIP(ssmk::launch_gemm_dx(M, D, D, u, D, wi, D, nullptr, false, nullptr, x, D, gws, s),
+                  "ssm_stack_grad x");
+        STACK_HIP(ssmk::launch_gemm_dx(M, D, D, u, D, wi + D * D, D, nullptr, false, nullptr, z, D, gws, s),
                   "ssm_stack_grad z");
-        STACK_HIP(ssmk::launch_gemm_dx(M, D, D, x, D, wx, D, nullptr, false, nullptr, dp, D, s),
+        STACK_HIP(ssmk::launch_gemm_dx(M, D, D, x, D, wx, D, nullptr, false, nullptr, dp, D, gws, s),
                   "ssm_stack_grad Delta_pre");
-        STACK_HIP(ssmk::launch_gemm_dx(M, N, D, x, D, wx + D * D, D, nullptr, false, nullptr, Bm, N, s),
+        STACK_HIP(ssmk::launch_gemm_dx(M, N, D, x, D, wx + D * D, D, nullptr, false, nullptr, Bm, N, gws, s),
                   "ssm_stack_grad B");
-        STACK_HIP(ssmk::launch_gemm_dx(M, N, D, x, D, wx + (D + N) * D, D, nullptr, false, nullptr, Cm, N, s),
+        STACK_HIP(ssmk::launch_gemm_dx(M, N, D, x, D, wx + (D + N) * D, D, nullptr, false, nullptr, Cm, N, gws,
+                                       s),
                   "ssm_stack_grad C");
         STACK_SSM(ssm_adjoint_forward(&ld, x, dp, A_log[k], Bm, Cm, nullptr, z, ytil, nullptr, ws + w.off_fws,
                                       w.fws_bytes, stream));

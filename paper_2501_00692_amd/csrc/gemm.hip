@@ -459,19 +459,23 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs g) {
     else by_mask(std::false_type{});
 }
 
-// dW = (dW +) sum over splits, in split order; four consecutive elements per
-// thread (KN is a multiple of 4: the output width is), the loads of up to eight
-// splits issued before their in-order adds.
-__global__ __launch_bounds__(256) void k_splitk_reduce(int64_t KN, int splits, const float* part,
-                                                       float* dW, int accum) {
+// Second stage of a split GEMM: result = sum over splits (in split order) +
+// (add) (+ the existing C if accum), the same combination as the single-pass
+// epilogue, written to C (if given) and/or as bf16 into out16 (row stride ld16).
+// Four consecutive elements of a row per thread (the output width is a multiple
+// of 8); the loads of up to eight splits are issued ahead of the in-order adds.
+__global__ __launch_bounds__(256) void k_splitk_reduce(int64_t R, int64_t Cc, int splits, const float* part,
+                                                       float* dst, int accum, const float* add, uint16_t* out16,
+                                                       int64_t ld16) {
+    const int64_t RC = R * Cc;
     const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
-    if (i >= KN) return;
+    if (i >= RC) return;
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int q0 = 0; q0 < splits; q0 += 8) {
         float4 v[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-            v[u] = q0 + u < splits ? *reinterpret_cast<const float4*>(part + (q0 + u) * KN + i)
+            v[u] = q0 + u < splits ? *reinterpret_cast<const float4*>(part + (q0 + u) * RC + i)
                                    : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
@@ -483,12 +487,21 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(int64_t KN, int splits, c
             }
         }
     }
-    float4* o = reinterpret_cast<float4*>(dW + i);
+    float4 e = add ? *reinterpret_cast<const float4*>(add + i) : make_float4(0.f, 0.f, 0.f, 0.f);
     if (accum) {
-        const float4 d = *o;
-        s = make_float4(d.x + s.x, d.y + s.y, d.z + s.z, d.w + s.w);
+        const float4 d = *reinterpret_cast<const float4*>(dst + i);
+        e = make_float4(e.x + d.x, e.y + d.y, e.z + d.z, e.w + d.w);
     }
-    *o = s;
+    const float4 val = make_float4(s.x + e.x, s.y + e.y, s.z + e.z, s.w + e.w);
+    if (dst) *reinterpret_cast<float4*>(dst + i) = val;
+    if (out16) {
+        const int64_t row = i / Cc, col = i - row * Cc;
+        uint16_t* o = out16 + row * ld16 + col;
+        o[0] = f2bf(val.x);
+        o[1] = f2bf(val.y);
+        o[2] = f2bf(val.z);
+        o[3] = f2bf(val.w);
+    }
 }
 
 inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b - 1) / b); }
@@ -512,7 +525,7 @@ Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split) {
         const int64_t tiles = ((R + BM - 1) / BM) * ((Cc + bn - 1) / bn);
         const int64_t iters = (Kr + BK - 1) / BK;
         for (int s = 1; s <= (allow_split ? 32 : 1); ++s) {
-            if (s > 1 && iters / s < 16) break;
+            if (s > 1 && iters / s < 8) break;
             const int64_t wgs = tiles * s;
             const double rounds = static_cast<double>((wgs + kCUs - 1) / kCUs);
             double us = rounds * 0.8 * (bn / 192.0) * static_cast<double>((iters + s - 1) / s);
@@ -538,21 +551,32 @@ void launch_plan(const GemmArgs& g, const Plan& pl, hipStream_t s) {
     else launch_tile<TR, 192>(g, pl.splits, s);
 }
 
+// Split partials of a product whose plan splits the reduction (else none).
+size_t split_workspace(const Plan& pl, int64_t R, int64_t Cc) {
+    return pl.splits > 1 ? static_cast<size_t>(pl.splits) * R * Cc * sizeof(float) : 0;
+}
+int64_t split_range(int64_t Kr, int splits) {
+    const int64_t per = (Kr + splits - 1) / splits;
+    return (per + BK - 1) / BK * BK;
+}
+void launch_reduce(const GemmArgs& g, int splits, float* dst, bool accum, const float* add, uint16_t* out16,
+                   int64_t ld16, hipStream_t s) {
+    hipLaunchKernelGGL(k_splitk_reduce, dim3(cdiv(g.R * g.Cc, 1024)), dim3(256), 0, s, g.R, g.Cc, splits,
+                       static_cast<const float*>(g.C), dst, accum ? 1 : 0, add, out16, ld16);
+}
+
 }  // namespace
 
-size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N) {
-    const Plan pl = plan_gemm(K, N, M, true);
-    return pl.splits > 1 ? static_cast<size_t>(pl.splits) * K * N * sizeof(float) : 0;
-}
+size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N) { return split_workspace(plan_gemm(K, N, M, true), K, N); }
+
+size_t gemm_dx_workspace(int64_t M, int64_t K, int64_t N) { return split_workspace(plan_gemm(M, K, N, true), M, K); }
 
 hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, int64_t ldx,
                           const uint16_t* dZ, int64_t lddz, float* dW, bool accum, void* ws,
                           hipStream_t s) {
     const Plan pl = plan_gemm(K, N, M, true);
-    int64_t per = (M + pl.splits - 1) / pl.splits;
-    per = (per + BK - 1) / BK * BK;
     const bool direct = pl.splits == 1;
-    GemmArgs g{K, N, M, X, ldx, dZ, lddz, direct ? dW : static_cast<float*>(ws), per,
+    GemmArgs g{K, N, M, X, ldx, dZ, lddz, direct ? dW : static_cast<float*>(ws), split_range(M, pl.splits),
                direct ? 1 : 0, accum ? 1 : 0, nullptr, nullptr, 0};
     {
         SSMK_TIMED("gemm_dw", s);
@@ -560,19 +584,27 @@ hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, in
     }
     if (!direct) {
         SSMK_TIMED("splitk_reduce", s);
-        hipLaunchKernelGGL(k_splitk_reduce, dim3(cdiv(K * N, 1024)), dim3(256), 0, s, K * N, pl.splits,
-                           static_cast<const float*>(ws), dW, accum ? 1 : 0);
+        launch_reduce(g, pl.splits, dW, accum, nullptr, nullptr, 0, s);
     }
     return hipGetLastError();
 }
 
 hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, int64_t lddz,
                           const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
-                          uint16_t* out16, int64_t ld16, hipStream_t s) {
-    const Plan pl = plan_gemm(M, K, N, false);
-    GemmArgs g{M, K, N, dZ, lddz, W, ldw, dX, (N + BK - 1) / BK * BK, 1, accum ? 1 : 0, add, out16, ld16};
-    SSMK_TIMED("gemm_dx", s);
-    launch_plan<false>(g, pl, s);
+                          uint16_t* out16, int64_t ld16, void* ws, hipStream_t s) {
+    // outputs with few tiles (narrow projections) split the reduction as dW does
+    const Plan pl = plan_gemm(M, K, N, true);
+    const bool direct = pl.splits == 1;
+    GemmArgs g{M, K, N, dZ, lddz, W, ldw, direct ? dX : static_cast<float*>(ws), split_range(N, pl.splits),
+               direct ? 1 : 0, accum ? 1 : 0, add, out16, ld16};
+    {
+        SSMK_TIMED("gemm_dx", s);
+        launch_plan<false>(g, pl, s);
+    }
+    if (!direct) {
+        SSMK_TIMED("splitk_reduce", s);
+        launch_reduce(g, pl.splits, dX, accum, add, out16, ld16, s);
+    }
     return hipGetLastError();
 }
 

@@ -133,9 +133,11 @@ hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, in
                           hipStream_t s);
 // dX[M][K] (+)= dZ W^T with dZ [M][N] (lddz), W [K][N] (ldw); optional fp32 addend
 // add[M][K] (ld = K) and optional bf16 copy of the result into out16 (ld16); dX may
-// be NULL when out16 is given (only the copy is written).
+// be NULL when out16 is given (only the copy is written).  Narrow outputs split the
+// reduction: ws holds gemm_dx_workspace(M, K, N) bytes (none otherwise).
+size_t gemm_dx_workspace(int64_t M, int64_t K, int64_t N);
 hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, int64_t lddz,
                           const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
-                          uint16_t* out16, int64_t ld16, hipStream_t s);
+                          uint16_t* out16, int64_t ld16, void* ws, hipStream_t s);
 
 }  // namespace ssmk

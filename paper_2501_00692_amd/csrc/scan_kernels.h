@@ -1162,10 +1162,12 @@ hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
         SSMK_TIMED("chunk_aggr", s);
         hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, 8>), g4, dim3(256), 0, s, p);
     }
-    SSMK_TIMED("carry", s);
-    hipLaunchKernelGGL(k_carry, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N),
-                                     static_cast<unsigned>(2 * p.nb)),
-                       dim3(256), 0, s, p);
+    {
+        SSMK_TIMED("carry", s);
+        hipLaunchKernelGGL(k_carry, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N),
+                                         static_cast<unsigned>(2 * p.nb)),
+                           dim3(256), 0, s, p);
+    }
     SSMK_TIMED("forward", s);
     hipLaunchKernelGGL((k_forward<TI, SP, GATE>), g4, dim3(256), 0, s, p);
     return hipGetLastError();

@@ -189,9 +189,10 @@ TOL_GEMM = 1e-5
 # shapes: ragged rows and columns, reductions that are not a multiple of the
 # 32-deep LDS stage (200, 24, 8, 1000, 700, 333), a reduction split over workgroups
 # (8192 rows onto a 256 x 256 output; 5000 rows, whose last split is short and
-# ends inside a stage), and the smallest legal sizes
+# ends inside a stage; a 16-column dX over a 1536-long reduction, split too), and
+# the smallest legal sizes
 @pytest.mark.parametrize("M,K,N", [(1000, 136, 200), (100, 64, 24), (4096, 256, 384), (333, 8, 8),
-                                   (700, 264, 1568), (8192, 256, 256), (5000, 264, 136)])
+                                   (700, 264, 1568), (8192, 256, 256), (5000, 264, 136), (4096, 16, 1536)])
 def test_proj_grad_matches_oracle(M, K, N):
     say(f"[proj] M={M} K={K} N={N}")
     X = _bf16((M, K), 11)

@@ -47,6 +47,23 @@ def test_stack_small(exact, tbar):
     say("   rel-L2 max:", f"{max(rep.values()):.2e}")
 
 
+def test_stack_split_projections():
+    """T = 512, D = 512: the forward projections (x, z, Delta_pre and the
+    16-column B and C) split their reductions and finish in the second-stage
+    reduction with the bf16 copy."""
+    K, b, T, D, N = 2, 1, 512, 512, 16
+    say(f"[stack split projections] K={K} b={b} T={T} D={D}")
+    inp = make_stack_inputs(K, b, T, D, N, 692402, device="cuda")
+    o = _gpu(inp, N, False, 0)
+    yK, ref = _oracle(inp, N, False, 0)
+    rep = {}
+    check("yK", to_np(o["yK"]), yK, TOL_BF16, rep)
+    for k in range(K):
+        for n in ("dW_in", "dW_x", "dA_log"):
+            check(f"{n}[{k}]", to_np(o[n][k]), ref[k][n], TOL_BF16, rep)
+    say("   rel-L2 max:", f"{max(rep.values()):.2e}")
+
+
 def test_stack_modes_differ_as_in_the_oracle():
     """The last layer's gradient is the same under both gradients (bit for bit on
     the GPU); below it, the GPU's difference between Prop. 3 and backpropagation
