@@ -35,9 +35,9 @@ def scan_flops_per_state_step(trunc):
     counts 2, exp counts 1): forward recompute a = exp(Delta c) (2), h = a h + B x (3),
     y += C h (2), dC contribution and channel sum (2); reverse mu = g C + a mu (3),
     dx += mu B (2), s = mu (a h) (2), ddelta += s w (2), dA += s Delta (2), dB
-    contribution and sum (2) -> 22.  The truncated window adds the shifted adjoint
-    (g C + a mu, its decay: 6), the window product (2) and mubar = mu - P mu' (2)."""
-    return 22 + (10 if trunc else 0)
+    contribution and sum (2) -> 22.  The truncated window adds the window product
+    P = exp(W c) (2), the tail nu = P g' C' + a nu (4) and mubar = mu - nu (1)."""
+    return 22 + (7 if trunc else 0)
 
 
 def scan_bytes_per_token(D, N, s, gate, layer=False):

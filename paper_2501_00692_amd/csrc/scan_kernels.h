@@ -650,10 +650,12 @@ __device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMI
 //      from the chunk's reverse carry M_c, and apply the vjp epilogue:
 //        s = mubar a_t h_{t-1};  ddelta = sum_n s wn;  dA_log += s Delta wn;
 //        dx = sum_n mubar B_t;  dB_t[n] += mubar x_t (over channels).
-//      Truncated mode: mubar_t = mu_t - P(t, t+tbar) mu_{t+tbar}; mu at the
-//      shifted position comes from a second reverse sweep run in lockstep from
-//      the carry of its own chunk, and P(t, t+tbar) = 2^{cn W_t} with the window
-//      sum W_t = sum_{j=t+1}^{t+tbar} Delta_j kept in fp64.
+//      Truncated mode: mubar_t = mu_t - nu_t with the tail nu_t = P(t, t+tbar)
+//      mu_{t+tbar}, which obeys nu_t = a_{t+1} nu_{t+1} + P(t, t+tbar) g_{t+tbar}
+//      C_{t+tbar} (the same decay as mu, so no second exponential per step); it
+//      starts at the chunk's last step from the adjoint carry of the chunk holding
+//      the shifted position, swept back to it; P(t, t+tbar) = 2^{cn W_t} with the
+//      window sum W_t = sum_{j=t+1}^{t+tbar} Delta_j kept in fp64.
 // Per-channel quantities (softplus, the gate) are computed once per step: lane
 // r of a quad prepares steps r, r+4, ... of the segment, DPP-broadcasts them,
 // keeps that step's per-channel outputs and stores them after the segment; the
@@ -791,7 +793,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
         for (int k = 0; k < 4; ++k) Mp[k] = ldm(p.mbuf, cb + k * p.D, nv[k]);
         float dA[4] = {0.f, 0.f, 0.f, 0.f};
 
-        // truncated-mode state: shifted adjoint carry and the window sum
+        // truncated-mode state: the adjoint carry at the shifted position (the start
+        // of the tail below) and the window sum
         float Msh[4] = {0.f, 0.f, 0.f, 0.f};
         double W = 0.0;
         if constexpr (TRUNC) {
@@ -837,6 +840,14 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             } else if (dv) {
                 W = p.psum[pb + p.nc * p.D] - p.psum[pb + (c + 1) * p.D];
             }
+        }
+        // the subtracted tail nu_t = P(t, t+tbar) mu_{t+tbar}, carried as a_{t+1} nu_{t+1};
+        // at the chunk's last step e: P(e, e+tbar) (a_{e+tbar+1} mu_{e+tbar+1})
+        float Np[4] = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (TRUNC) {
+            const float wf0 = static_cast<float>(W);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) Np[k] = fexp2(cn[k] * wf0) * Msh[k];
         }
 
 #pragma unroll 1
@@ -970,9 +981,10 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     const float wf = static_cast<float>(W);
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
-                        const float musp = fmaf(gp, Cs[k], Msh[k]);
-                        mb[k] = fmaf(-fexp2(cn[k] * wf), musp, mu[k]);
-                        Msh[k] = fexp2(cn[k] * dlp) * musp;
+                        // nu_t = a_{t+1} nu_{t+1} + P(t, t+tbar) g_{t+tbar} C_{t+tbar}
+                        const float nu = fmaf(fexp2(cn[k] * wf), gp * Cs[k], Np[k]);
+                        mb[k] = mu[k] - nu;
+                        Np[k] = ah[j][k] * nu;
                     }
                     W += static_cast<double>(dlh[j]) - static_cast<double>(dlp);
                 }
