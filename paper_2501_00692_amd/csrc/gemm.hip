@@ -441,6 +441,11 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs g) {
             acc, dst, addp, o16, g.ld16, g.R, g.Cc, r0 + wr, c0 + wc, lane);
     };
     auto by_mask = [&](auto Ft) __attribute__((always_inline)) {
+        if constexpr (TR) {  // dW: C or C += (split partials are C)
+            if (mask == 6) store(Ft, std::integral_constant<int, 6>{});
+            else store(Ft, std::integral_constant<int, 4>{});
+            return;
+        }
         switch (mask) {
             case 4: store(Ft, std::integral_constant<int, 4>{}); break;     // C
             case 6: store(Ft, std::integral_constant<int, 6>{}); break;     // C +=
@@ -510,25 +515,30 @@ constexpr int kCUs = 256;
 
 // Output-tile width and reduction splits for an R x Cc output with reduction Kr,
 // from a simple time model: rounds of 256 workgroups x the time of one
-// workgroup's share (about 0.8 us per 256x192x32 stage at full load), plus the
-// HBM time of writing and re-reading the split partials (4 TB/s).
+// workgroup's share (per 32-step stage at full load, measured: 0.57 us for 128
+// columns, 0.80 for 192, 0.92 for 256), plus the HBM time of writing and
+// re-reading the split partials (4 TB/s).  256-column tiles only for dW (the dX
+// form's epilogue needs the registers).
 struct Plan {
     int bn;
     int splits;
 };
 
-Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split) {
+Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split, bool tr) {
     Plan best{192, 1};
     double best_us = 1e300;
-    const int bns[2] = {192, 128};
-    for (int bn : bns) {
+    const int bns[3] = {192, 128, 256};
+    const double step_us[3] = {0.80, 0.57, 0.92};
+    for (int b = 0; b < 3; ++b) {
+        const int bn = bns[b];
+        if (bn == 256 && !tr) continue;
         const int64_t tiles = ((R + BM - 1) / BM) * ((Cc + bn - 1) / bn);
         const int64_t iters = (Kr + BK - 1) / BK;
         for (int s = 1; s <= (allow_split ? 32 : 1); ++s) {
             if (s > 1 && iters / s < 8) break;
             const int64_t wgs = tiles * s;
             const double rounds = static_cast<double>((wgs + kCUs - 1) / kCUs);
-            double us = rounds * 0.8 * (bn / 192.0) * static_cast<double>((iters + s - 1) / s);
+            double us = rounds * step_us[b] * static_cast<double>((iters + s - 1) / s);
             if (s > 1) us += static_cast<double>(s) * R * Cc * 8.0 / 4e12 * 1e6;
             if (us < best_us * 0.999) {
                 best_us = us;
@@ -548,7 +558,12 @@ void launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
 template <bool TR>
 void launch_plan(const GemmArgs& g, const Plan& pl, hipStream_t s) {
     if (pl.bn == 128) launch_tile<TR, 128>(g, pl.splits, s);
-    else launch_tile<TR, 192>(g, pl.splits, s);
+    else if constexpr (TR) {
+        if (pl.bn == 256) launch_tile<TR, 256>(g, pl.splits, s);
+        else launch_tile<TR, 192>(g, pl.splits, s);
+    } else {
+        launch_tile<TR, 192>(g, pl.splits, s);
+    }
 }
 
 // Split partials of a product whose plan splits the reduction (else none).
@@ -567,14 +582,18 @@ void launch_reduce(const GemmArgs& g, int splits, float* dst, bool accum, const 
 
 }  // namespace
 
-size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N) { return split_workspace(plan_gemm(K, N, M, true), K, N); }
+size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N) {
+    return split_workspace(plan_gemm(K, N, M, true, true), K, N);
+}
 
-size_t gemm_dx_workspace(int64_t M, int64_t K, int64_t N) { return split_workspace(plan_gemm(M, K, N, true), M, K); }
+size_t gemm_dx_workspace(int64_t M, int64_t K, int64_t N) {
+    return split_workspace(plan_gemm(M, K, N, true, false), M, K);
+}
 
 hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, int64_t ldx,
                           const uint16_t* dZ, int64_t lddz, float* dW, bool accum, void* ws,
                           hipStream_t s) {
-    const Plan pl = plan_gemm(K, N, M, true);
+    const Plan pl = plan_gemm(K, N, M, true, true);
     const bool direct = pl.splits == 1;
     GemmArgs g{K, N, M, X, ldx, dZ, lddz, direct ? dW : static_cast<float*>(ws), split_range(M, pl.splits),
                direct ? 1 : 0, accum ? 1 : 0, nullptr, nullptr, 0};
@@ -593,7 +612,7 @@ hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, i
                           const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
                           uint16_t* out16, int64_t ld16, void* ws, hipStream_t s) {
     // outputs with few tiles (narrow projections) split the reduction as dW does
-    const Plan pl = plan_gemm(M, K, N, true);
+    const Plan pl = plan_gemm(M, K, N, true, false);
     const bool direct = pl.splits == 1;
     GemmArgs g{M, K, N, dZ, lddz, W, ldw, direct ? dX : static_cast<float*>(ws), split_range(N, pl.splits),
                direct ? 1 : 0, accum ? 1 : 0, add, out16, ld16};

@@ -246,3 +246,24 @@ def test_proj_grad_slice_shapes_sampled():
     check("dW[sampled]", to_np(dW)[kk, jj], oracle.proj_dw(Xb, Zb, kk, jj), tol, rep)
     check("dX[rows]", to_np(dX[torch.as_tensor(rows, device="cuda")]), oracle.proj_dx(Zb, Wb, rows), tol, rep)
     say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+def test_proj_grad_wide_dw_tiles_sampled():
+    """dW with an output of 2040 x 8184 over a 4096-long reduction: about 256
+    output tiles, so the planner takes the 256-column tiles of the dW product; the
+    last row block and column block are ragged.  Sampled entries, including the
+    output's last row and column, against the oracle's plain loops."""
+    M, K, N = 4096, 2040, 8184
+    say(f"[proj wide dW] M={M} K={K} N={N}")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4243)
+    X = torch.randn(M, K, generator=g, device="cuda").to(torch.bfloat16)
+    dZ = torch.randn(M, N, generator=g, device="cuda").to(torch.bfloat16)
+    dW, _ = ssm.ssm_proj_grad(X, dZ, None, want_dW=True, want_dX=False)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(4)
+    kk = np.concatenate([rng.integers(0, K, 4096), [K - 1, K - 1, 0]])
+    jj = np.concatenate([rng.integers(0, N, 4096), [N - 1, 0, N - 1]])
+    bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)
+    rep = {}
+    check("dW[sampled]", to_np(dW)[kk, jj], oracle.proj_dw(bits(X), bits(dZ), kk, jj), 1e-5, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
