@@ -8,7 +8,8 @@
 //   dX[M][K] = dZ W^T  (dZ [M][N], W [K][N]): both operands are contiguous along
 //       the reduction; fragments are plain 16-byte LDS reads.  The epilogue adds
 //       an optional fp32 addend, accumulates, and can write a bf16 copy into a
-//       strided buffer.
+//       strided buffer; narrow outputs split the reduction like dW, and the
+//       second stage applies the same epilogue.
 // Staging: operand tiles go from global memory straight into LDS (buffer loads
 // with the LDS destination, 16 bytes per lane, no registers on the way) through
 // a ring of NS stages of BK = 32 reduction steps.  Step t waits (vmcnt) until its
@@ -17,7 +18,8 @@
 // first fragments are read while step t's second half of MFMAs runs.  Pieces
 // outside the matrix (rows, columns, or the reduction tail) read as zero through
 // the buffer range check.  Workgroup: 512 threads = 4x2 waves, two per SIMD;
-// a wave owns a 64 x (BN/2) block of 32x32 MFMA tiles; tile 256 x BN.
+// a wave owns a 64 x (BN/2) block of 32x32 MFMA tiles; tile 256 x BN with BN 128
+// or 192 (and 256 for dW, whose epilogue leaves the registers for it).
 // Output tiles and reduction splits are assigned so that each XCD runs one
 // contiguous run of (split, tile) (consecutive workgroups go to different XCDs),
 // tiles ordered in groups of four row blocks, so that the tiles one XCD runs at
