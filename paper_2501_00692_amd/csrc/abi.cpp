@@ -131,10 +131,12 @@ LayerWs layer_ws(const ssm_desc* d, int64_t L, bool trunc, int64_t d_model) {
     w.f32_off = off;  // fp32 dx, ddelta, dz [M][D] and dB, dC [M][N]
     off = up256(off + size_t(M) * (3 * D + 2 * N) * 4);
     w.gemm_off = off;
-    // the layer's four products run one after the other and share the region
-    size_t g = ssmk::gemm_dw_workspace(M, D, D + 2 * N);
-    for (size_t gi : {ssmk::gemm_dw_workspace(M, d_model, 2 * D), ssmk::gemm_dx_workspace(M, D, D + 2 * N),
-                      ssmk::gemm_dx_workspace(M, d_model, 2 * D)})
+    // the layer's GEMM launches (dx_total, both weight gradients together, du) run
+    // one after the other and share the region
+    const ssmk::DwProduct dwx{D, D + 2 * N, nullptr, 0, nullptr, 0, nullptr, false};
+    const ssmk::DwProduct dwin{d_model, 2 * D, nullptr, 0, nullptr, 0, nullptr, false};
+    size_t g = ssmk::gemm_dw2_workspace(M, dwx, dwin);
+    for (size_t gi : {ssmk::gemm_dx_workspace(M, D, D + 2 * N), ssmk::gemm_dx_workspace(M, d_model, 2 * D)})
         g = gi > g ? gi : g;
     off = up256(off + g);
     w.total = off;
@@ -498,18 +500,16 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     hipError_t e = ssmk::launch_grad(p, s);
     if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad scan launch");
     void* gws = ws + w.gemm_off;
-    // dW_x = x^T dZx
-    e = ssmk::launch_gemm_dw(M, D, nx, static_cast<const uint16_t*>(x), D, dzx, nx, dW_x, false, gws, s);
-    if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_x launch");
     // dx_total = dx + dZx W_x^T, also packed into [dx_total | dz]
     // (the fp32 dx_total only when the caller asks for it)
     e = ssmk::launch_gemm_dx(M, D, nx, dzx, nx, static_cast<const uint16_t*>(W_x), nx, dx_total, false,
                              dx_, dxz, 2 * D, gws, s);
     if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dx_total launch");
-    // dW_in = u^T [dx_total | dz]
-    e = ssmk::launch_gemm_dw(M, d_model, 2 * D, static_cast<const uint16_t*>(u), d_model, dxz, 2 * D,
-                             dW_in, false, gws, s);
-    if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_in launch");
+    // dW_x = x^T dZx and dW_in = u^T [dx_total | dz], in one launch
+    const ssmk::DwProduct px{D, nx, static_cast<const uint16_t*>(x), D, dzx, nx, dW_x, false};
+    const ssmk::DwProduct pin{d_model, 2 * D, static_cast<const uint16_t*>(u), d_model, dxz, 2 * D, dW_in, false};
+    e = ssmk::launch_gemm_dw2(M, px, pin, gws, s);
+    if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_x / dW_in launch");
     if (du) {
         e = ssmk::launch_gemm_dx(M, d_model, 2 * D, dxz, 2 * D, static_cast<const uint16_t*>(W_in),
                                  2 * D, du, false, nullptr, nullptr, 0, gws, s);

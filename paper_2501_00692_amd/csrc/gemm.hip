@@ -124,6 +124,16 @@ struct GemmArgs {
     int64_t ld16;
 };
 
+// One launch covers the output tiles of one product, or of two products with the
+// same reduction length and split (the layer's two weight gradients): in every
+// split, tiles [0, tiles0) belong to product 0 and [tiles0, tiles) to product 1.
+struct GemmLaunch {
+    GemmArgs p[2];
+    int tiles0;  // output tiles of product 0
+    int tiles;   // output tiles of all products
+    int cb[2];   // column blocks of each product
+};
+
 // Operands contiguous along the reduction (dX = dZ W^T).  A stage holds BM rows
 // of A and BN rows of B, each a 64-byte LDS row of BK values whose four 16-byte
 // blocks are XOR-swizzled by (row >> 2) & 3: a 16-byte fragment read by 32 lanes
@@ -315,7 +325,7 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[MI][NJ], float* _
 }
 
 template <bool TR, int BN>
-__global__ __launch_bounds__(512) void k_gemm(const GemmArgs g) {
+__global__ __launch_bounds__(512) void k_gemm(const GemmLaunch gl) {
     constexpr int MI = 2, NJ = BN / 64;  // 32x32 MFMA tiles per wave
     using Ops = typename std::conditional<TR, ColMajorOps<BN>, RowMajorOps<BN>>::type;
     const int tid = threadIdx.x;
@@ -323,21 +333,24 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs g) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     // output tile and reduction split: workgroups are dispatched to the XCDs in
     // turn (workgroup i to XCD i % 8), so the linear id is mapped to a logical
-    // index that gives every XCD one contiguous run of (split, row block, column
-    // block) -- the workgroups of one XCD share the first operand's row block and
-    // reduction range in its L2.  The map is a bijection for any count.
-    const int ncb = static_cast<int>(gridDim.x);
-    const int ntl = ncb * static_cast<int>(gridDim.y);
-    const int nwg = ntl * static_cast<int>(gridDim.z);
-    const int lin = static_cast<int>(blockIdx.x) + ncb * (static_cast<int>(blockIdx.y) +
-                                                          static_cast<int>(gridDim.y) * static_cast<int>(blockIdx.z));
+    // index that gives every XCD one contiguous run of (split, product, row block,
+    // column block) -- the workgroups of one XCD share the first operand's row
+    // block and reduction range in its L2.  The map is a bijection for any count.
+    const int nwg = static_cast<int>(gridDim.x);
+    const int lin = static_cast<int>(blockIdx.x);
     const int xq = nwg / kXcds, xr = nwg % kXcds, xcd = lin % kXcds;
     const int logical = (xcd < xr ? xcd * (xq + 1) : xr * (xq + 1) + (xcd - xr) * xq) + lin / kXcds;
-    const int tile = logical % ntl, split = logical / ntl;
+    const int tile_all = logical % gl.tiles, split = logical / gl.tiles;
+    // the product (wave-uniform; taken from the first lane so that the compiler
+    // keeps its pointers and the buffer resources built from them in SGPRs)
+    const int q = __builtin_amdgcn_readfirstlane(tile_all >= gl.tiles0 ? 1 : 0);
+    const GemmArgs g = q ? gl.p[1] : gl.p[0];
+    const int tile = tile_all - (q ? gl.tiles0 : 0);
+    const int ncb = gl.cb[q];
+    const int nrb = (q ? gl.tiles - gl.tiles0 : gl.tiles0) / ncb;
     // tiles in groups of kGroupRows row blocks, column-major inside a group, so
     // that the 32 consecutive tiles one XCD runs at a time form a block of about
     // 4 row blocks x 8 column blocks (both operands reused from its L2)
-    const int nrb = static_cast<int>(gridDim.y);
     const int grp = tile / (kGroupRows * ncb), first = grp * kGroupRows;
     const int gh = min(kGroupRows, nrb - first), within = tile - grp * kGroupRows * ncb;
     const int64_t r0 = static_cast<int64_t>(first + within % gh) * BM;
@@ -471,18 +484,37 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs g) {
 // epilogue, written to C (if given) and/or as bf16 into out16 (row stride ld16).
 // Four consecutive elements of a row per thread (the output width is a multiple
 // of 8); the loads of up to eight splits are issued ahead of the in-order adds.
-__global__ __launch_bounds__(256) void k_splitk_reduce(int64_t R, int64_t Cc, int splits, const float* part,
-                                                       float* dst, int accum, const float* add, uint16_t* out16,
-                                                       int64_t ld16) {
-    const int64_t RC = R * Cc;
-    const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+// One launch serves the products of one GEMM launch: workgroups [0, blocks0)
+// reduce product 0, the rest product 1.
+struct ReduceArgs {
+    int64_t R, Cc;
+    const float* part;  // [splits][R][Cc]
+    float* dst;
+    int accum;
+    const float* add;
+    uint16_t* out16;
+    int64_t ld16;
+};
+struct ReduceLaunch {
+    ReduceArgs p[2];
+    unsigned blocks0;
+    int splits;
+};
+
+__global__ __launch_bounds__(256) void k_splitk_reduce(const ReduceLaunch rl) {
+    const int q = blockIdx.x >= rl.blocks0 ? 1 : 0;
+    const ReduceArgs& a = rl.p[q];
+    const int64_t blk = static_cast<int64_t>(blockIdx.x) - (q ? rl.blocks0 : 0);
+    const int64_t RC = a.R * a.Cc;
+    const int64_t i = (blk * 256 + threadIdx.x) * 4;
     if (i >= RC) return;
+    const int splits = rl.splits;
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int q0 = 0; q0 < splits; q0 += 8) {
         float4 v[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-            v[u] = q0 + u < splits ? *reinterpret_cast<const float4*>(part + (q0 + u) * RC + i)
+            v[u] = q0 + u < splits ? *reinterpret_cast<const float4*>(a.part + (q0 + u) * RC + i)
                                    : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
@@ -494,16 +526,16 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(int64_t R, int64_t Cc, in
             }
         }
     }
-    float4 e = add ? *reinterpret_cast<const float4*>(add + i) : make_float4(0.f, 0.f, 0.f, 0.f);
-    if (accum) {
-        const float4 d = *reinterpret_cast<const float4*>(dst + i);
+    float4 e = a.add ? *reinterpret_cast<const float4*>(a.add + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    if (a.accum) {
+        const float4 d = *reinterpret_cast<const float4*>(a.dst + i);
         e = make_float4(e.x + d.x, e.y + d.y, e.z + d.z, e.w + d.w);
     }
     const float4 val = make_float4(s.x + e.x, s.y + e.y, s.z + e.z, s.w + e.w);
-    if (dst) *reinterpret_cast<float4*>(dst + i) = val;
-    if (out16) {
-        const int64_t row = i / Cc, col = i - row * Cc;
-        uint16_t* o = out16 + row * ld16 + col;
+    if (a.dst) *reinterpret_cast<float4*>(a.dst + i) = val;
+    if (a.out16) {
+        const int64_t row = i / a.Cc, col = i - row * a.Cc;
+        uint16_t* o = a.out16 + row * a.ld16 + col;
         o[0] = f2bf(val.x);
         o[1] = f2bf(val.y);
         o[2] = f2bf(val.z);
@@ -511,37 +543,43 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(int64_t R, int64_t Cc, in
     }
 }
 
-inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b - 1) / b); }
+inline int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 constexpr int kCUs = 256;
+// Most workgroups of one launch (the grid is one-dimensional and its thread count
+// must fit 32 bits).
+constexpr int64_t kMaxWgs = (int64_t(1) << 23) - 1;
 
-// Output-tile width and reduction splits for an R x Cc output with reduction Kr,
-// from a simple time model: rounds of 256 workgroups x the time of one
-// workgroup's share (per 32-step stage at full load, measured: 0.57 us for 128
-// columns, 0.80 for 192, 0.92 for 256), plus the HBM time of writing and
-// re-reading the split partials (4 TB/s).  256-column tiles only for dW (the dX
-// form's epilogue needs the registers).
+// Output-tile width and reduction splits for the outputs R_q x Cc_q of one launch
+// (one or two products) with reduction Kr, from a simple time model: rounds of 256
+// workgroups x the time of one workgroup's share (per 32-step stage at full
+// load, measured: 0.57 us for 128 columns, 0.80 for 192, 0.92 for 256), plus the
+// HBM time of writing and re-reading the split partials (4 TB/s).  256-column
+// tiles only for dW (the dX form's epilogue needs the registers).
 struct Plan {
     int bn;
     int splits;
 };
 
-Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split, bool tr) {
+Plan plan_gemm(int np, const int64_t* R, const int64_t* Cc, int64_t Kr, bool allow_split, bool tr) {
     Plan best{192, 1};
     double best_us = 1e300;
     const int bns[3] = {192, 128, 256};
     const double step_us[3] = {0.80, 0.57, 0.92};
+    double out = 0.0;  // output elements of all products
+    for (int q = 0; q < np; ++q) out += static_cast<double>(R[q]) * static_cast<double>(Cc[q]);
     for (int b = 0; b < 3; ++b) {
         const int bn = bns[b];
         if (bn == 256 && !tr) continue;
-        const int64_t tiles = ((R + BM - 1) / BM) * ((Cc + bn - 1) / bn);
+        int64_t tiles = 0;
+        for (int q = 0; q < np; ++q) tiles += cdiv64(R[q], BM) * cdiv64(Cc[q], bn);
         const int64_t iters = (Kr + BK - 1) / BK;
         for (int s = 1; s <= (allow_split ? 32 : 1); ++s) {
             if (s > 1 && iters / s < 8) break;
             const int64_t wgs = tiles * s;
             const double rounds = static_cast<double>((wgs + kCUs - 1) / kCUs);
             double us = rounds * step_us[b] * static_cast<double>((iters + s - 1) / s);
-            if (s > 1) us += static_cast<double>(s) * R * Cc * 8.0 / 4e12 * 1e6;
+            if (s > 1) us += static_cast<double>(s) * out * 8.0 / 4e12 * 1e6;
             if (us < best_us * 0.999) {
                 best_us = us;
                 best = Plan{bn, s};
@@ -550,64 +588,138 @@ Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split, bool tr) {
     }
     return best;
 }
+Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split, bool tr) {
+    return plan_gemm(1, &R, &Cc, Kr, allow_split, tr);
+}
 
 template <bool TR, int BN>
-void launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
-    dim3 grid(cdiv(g.Cc, BN), cdiv(g.R, BM), static_cast<unsigned>(splits));
-    hipLaunchKernelGGL((k_gemm<TR, BN>), grid, dim3(512), 0, s, g);
+void launch_tile(const GemmLaunch& gl, int splits, hipStream_t s) {
+    hipLaunchKernelGGL((k_gemm<TR, BN>), dim3(static_cast<unsigned>(gl.tiles * splits)), dim3(512), 0, s, gl);
 }
 
+// One launch over the np products g[0..np) (same reduction split) with the
+// plan's tile width; false if the grid is too large.
 template <bool TR>
-void launch_plan(const GemmArgs& g, const Plan& pl, hipStream_t s) {
-    if (pl.bn == 128) launch_tile<TR, 128>(g, pl.splits, s);
-    else if constexpr (TR) {
-        if (pl.bn == 256) launch_tile<TR, 256>(g, pl.splits, s);
-        else launch_tile<TR, 192>(g, pl.splits, s);
-    } else {
-        launch_tile<TR, 192>(g, pl.splits, s);
+bool launch_plan(const GemmArgs* g, int np, const Plan& pl, hipStream_t s) {
+    GemmLaunch gl{};
+    int64_t t[2] = {0, 0};
+    for (int q = 0; q < np; ++q) {
+        gl.p[q] = g[q];
+        gl.cb[q] = static_cast<int>(cdiv64(g[q].Cc, pl.bn));
+        t[q] = cdiv64(g[q].R, BM) * gl.cb[q];
     }
+    if (np == 1) {
+        gl.p[1] = g[0];
+        gl.cb[1] = gl.cb[0];
+    }
+    if ((t[0] + t[1]) * pl.splits > kMaxWgs) return false;
+    gl.tiles0 = static_cast<int>(t[0]);
+    gl.tiles = static_cast<int>(t[0] + t[1]);
+    if (pl.bn == 128) launch_tile<TR, 128>(gl, pl.splits, s);
+    else if constexpr (TR) {
+        if (pl.bn == 256) launch_tile<TR, 256>(gl, pl.splits, s);
+        else launch_tile<TR, 192>(gl, pl.splits, s);
+    } else {
+        launch_tile<TR, 192>(gl, pl.splits, s);
+    }
+    return true;
 }
 
-// Split partials of a product whose plan splits the reduction (else none).
-size_t split_workspace(const Plan& pl, int64_t R, int64_t Cc) {
-    return pl.splits > 1 ? static_cast<size_t>(pl.splits) * R * Cc * sizeof(float) : 0;
+// Split partials of the products of one plan (else none): product q's partials
+// follow those of the products before it.
+size_t split_workspace(const Plan& pl, int np, const int64_t* R, const int64_t* Cc) {
+    if (pl.splits == 1) return 0;
+    size_t total = 0;
+    for (int q = 0; q < np; ++q) total += static_cast<size_t>(pl.splits) * R[q] * Cc[q] * sizeof(float);
+    return total;
 }
 int64_t split_range(int64_t Kr, int splits) {
     const int64_t per = (Kr + splits - 1) / splits;
     return (per + BK - 1) / BK * BK;
 }
-void launch_reduce(const GemmArgs& g, int splits, float* dst, bool accum, const float* add, uint16_t* out16,
-                   int64_t ld16, hipStream_t s) {
-    hipLaunchKernelGGL(k_splitk_reduce, dim3(cdiv(g.R * g.Cc, 1024)), dim3(256), 0, s, g.R, g.Cc, splits,
-                       static_cast<const float*>(g.C), dst, accum ? 1 : 0, add, out16, ld16);
+// Second stage over the products g[0..np) (their C is the partials); fin[q] is
+// product q's final epilogue.
+void launch_reduce(const GemmArgs* g, const ReduceArgs* fin, int np, int splits, hipStream_t s) {
+    ReduceLaunch rl{};
+    unsigned nb[2] = {0, 0};
+    for (int q = 0; q < np; ++q) {
+        rl.p[q] = fin[q];
+        rl.p[q].R = g[q].R;
+        rl.p[q].Cc = g[q].Cc;
+        rl.p[q].part = g[q].C;
+        nb[q] = static_cast<unsigned>(cdiv64(g[q].R * g[q].Cc, 1024));
+    }
+    if (np == 1) rl.p[1] = rl.p[0];
+    rl.blocks0 = nb[0];
+    rl.splits = splits;
+    hipLaunchKernelGGL(k_splitk_reduce, dim3(nb[0] + nb[1]), dim3(256), 0, s, rl);
+}
+
+// dW_q = X_q^T dZ_q for np products with the same reduction length M.
+size_t dw_workspace(int np, const DwProduct* d, int64_t M) {
+    int64_t R[2], Cc[2];
+    for (int q = 0; q < np; ++q) {
+        R[q] = d[q].K;
+        Cc[q] = d[q].N;
+    }
+    return split_workspace(plan_gemm(np, R, Cc, M, true, true), np, R, Cc);
+}
+
+hipError_t launch_dw(int np, const DwProduct* d, int64_t M, void* ws, hipStream_t s) {
+    int64_t R[2], Cc[2];
+    for (int q = 0; q < np; ++q) {
+        R[q] = d[q].K;
+        Cc[q] = d[q].N;
+    }
+    const Plan pl = plan_gemm(np, R, Cc, M, true, true);
+    const bool direct = pl.splits == 1;
+    GemmArgs g[2];
+    ReduceArgs fin[2];
+    float* part = static_cast<float*>(ws);
+    for (int q = 0; q < np; ++q) {
+        g[q] = GemmArgs{d[q].K, d[q].N, M, d[q].X, d[q].ldx, d[q].dZ, d[q].lddz, direct ? d[q].dW : part,
+                        split_range(M, pl.splits), direct ? 1 : 0, d[q].accum ? 1 : 0, nullptr, nullptr, 0};
+        fin[q] = ReduceArgs{0, 0, nullptr, d[q].dW, d[q].accum ? 1 : 0, nullptr, nullptr, 0};
+        if (!direct) part += static_cast<int64_t>(pl.splits) * d[q].K * d[q].N;
+    }
+    {
+        SSMK_TIMED("gemm_dw", s);
+        if (!launch_plan<true>(g, np, pl, s)) return hipErrorInvalidConfiguration;
+    }
+    if (!direct) {
+        SSMK_TIMED("splitk_reduce", s);
+        launch_reduce(g, fin, np, pl.splits, s);
+    }
+    return hipGetLastError();
 }
 
 }  // namespace
 
 size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N) {
-    return split_workspace(plan_gemm(K, N, M, true, true), K, N);
+    const DwProduct d{K, N, nullptr, 0, nullptr, 0, nullptr, false};
+    return dw_workspace(1, &d, M);
+}
+
+size_t gemm_dw2_workspace(int64_t M, const DwProduct& a, const DwProduct& b) {
+    const DwProduct d[2] = {a, b};
+    return dw_workspace(2, d, M);
 }
 
 size_t gemm_dx_workspace(int64_t M, int64_t K, int64_t N) {
-    return split_workspace(plan_gemm(M, K, N, true, false), M, K);
+    const Plan pl = plan_gemm(M, K, N, true, false);
+    return split_workspace(pl, 1, &M, &K);
 }
 
 hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, int64_t ldx,
                           const uint16_t* dZ, int64_t lddz, float* dW, bool accum, void* ws,
                           hipStream_t s) {
-    const Plan pl = plan_gemm(K, N, M, true, true);
-    const bool direct = pl.splits == 1;
-    GemmArgs g{K, N, M, X, ldx, dZ, lddz, direct ? dW : static_cast<float*>(ws), split_range(M, pl.splits),
-               direct ? 1 : 0, accum ? 1 : 0, nullptr, nullptr, 0};
-    {
-        SSMK_TIMED("gemm_dw", s);
-        launch_plan<true>(g, pl, s);
-    }
-    if (!direct) {
-        SSMK_TIMED("splitk_reduce", s);
-        launch_reduce(g, pl.splits, dW, accum, nullptr, nullptr, 0, s);
-    }
-    return hipGetLastError();
+    const DwProduct d{K, N, X, ldx, dZ, lddz, dW, accum};
+    return launch_dw(1, &d, M, ws, s);
+}
+
+hipError_t launch_gemm_dw2(int64_t M, const DwProduct& a, const DwProduct& b, void* ws, hipStream_t s) {
+    const DwProduct d[2] = {a, b};
+    return launch_dw(2, d, M, ws, s);
 }
 
 hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, int64_t lddz,
@@ -616,15 +728,16 @@ hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, i
     // outputs with few tiles (narrow projections) split the reduction as dW does
     const Plan pl = plan_gemm(M, K, N, true, false);
     const bool direct = pl.splits == 1;
-    GemmArgs g{M, K, N, dZ, lddz, W, ldw, direct ? dX : static_cast<float*>(ws), split_range(N, pl.splits),
-               direct ? 1 : 0, accum ? 1 : 0, add, out16, ld16};
+    const GemmArgs g{M, K, N, dZ, lddz, W, ldw, direct ? dX : static_cast<float*>(ws), split_range(N, pl.splits),
+                     direct ? 1 : 0, accum ? 1 : 0, add, out16, ld16};
     {
         SSMK_TIMED("gemm_dx", s);
-        launch_plan<false>(g, pl, s);
+        if (!launch_plan<false>(&g, 1, pl, s)) return hipErrorInvalidConfiguration;
     }
     if (!direct) {
         SSMK_TIMED("splitk_reduce", s);
-        launch_reduce(g, pl.splits, dX, accum, add, out16, ld16, s);
+        const ReduceArgs fin{0, 0, nullptr, dX, accum ? 1 : 0, add, out16, ld16};
+        launch_reduce(&g, &fin, 1, pl.splits, s);
     }
     return hipGetLastError();
 }

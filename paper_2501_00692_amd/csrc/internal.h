@@ -131,6 +131,20 @@ size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N);
 hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, int64_t ldx,
                           const uint16_t* dZ, int64_t lddz, float* dW, bool accum, void* ws,
                           hipStream_t s);
+// Two weight gradients dW_q[K_q][N_q] (+)= X_q^T dZ_q over the same M rows in one
+// launch (and one second-stage launch when the reduction is split): the tiles of
+// both fill the GPU together.  ws holds gemm_dw2_workspace bytes.
+struct DwProduct {
+    int64_t K, N;
+    const uint16_t* X;
+    int64_t ldx;
+    const uint16_t* dZ;
+    int64_t lddz;
+    float* dW;
+    bool accum;
+};
+size_t gemm_dw2_workspace(int64_t M, const DwProduct& a, const DwProduct& b);
+hipError_t launch_gemm_dw2(int64_t M, const DwProduct& a, const DwProduct& b, void* ws, hipStream_t s);
 // dX[M][K] (+)= dZ W^T with dZ [M][N] (lddz), W [K][N] (ldw); optional fp32 addend
 // add[M][K] (ld = K) and optional bf16 copy of the result into out16 (ld16); dX may
 // be NULL when out16 is given (only the copy is written).  Narrow outputs split the

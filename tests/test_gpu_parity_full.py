@@ -267,3 +267,32 @@ def test_proj_grad_wide_dw_tiles_sampled():
     rep = {}
     check("dW[sampled]", to_np(dW)[kk, jj], oracle.proj_dw(bits(X), bits(dZ), kk, jj), 1e-5, rep)
     say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
+def test_layer_workload_weight_grads_exact_sampled():
+    """Both weight gradients of the layer workload come from one GEMM launch
+    over their tiles together (a split reduction over the M = 8192 rows).  Each
+    is the product of bf16 operands the layer hands over: dW_x = x^T dZx with dZx
+    the bf16 rounding of [dDelta_pre | dB | dC], dW_in = u^T [dx_total | dz] in
+    bf16.  The layer's own fp32 outputs, rounded to bf16, rebuild those operands
+    exactly, so sampled entries (with every row's and column's last one) are
+    checked against the oracle's plain loops at the GEMM tolerance."""
+    w = WORKLOADS["layer"]
+    say(f"[layer weight gradients] {w}")
+    inp = make_inputs(w, device="cuda")
+    o = ssm.ssm_layer_grad(inp["u"], inp["x"], inp["z"], inp["delta"], inp["B"], inp["C"], inp["W_x"],
+                           inp["W_in"], inp["A_log"], inp["dy"], want_scan=True)
+    torch.cuda.synchronize()
+    M = w.M
+    bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    dzx = torch.cat([o["ddelta"], o["dB"], o["dC"]], dim=-1).reshape(M, -1).to(torch.bfloat16)
+    dxz = torch.cat([o["dx_total"], o["dz"]], dim=-1).reshape(M, -1).to(torch.bfloat16)
+    rng = np.random.default_rng(11)
+    rep = {}
+    for name, X, dZ in (("dW_x", inp["x"], dzx), ("dW_in", inp["u"], dxz)):
+        K, N = X.shape[-1], dZ.shape[-1]
+        kk = np.concatenate([rng.integers(0, K, 2048), [K - 1, K - 1, 0]])
+        jj = np.concatenate([rng.integers(0, N, 2048), [N - 1, 0, N - 1]])
+        ref = oracle.proj_dw(bits(X.reshape(M, K)), bits(dZ), kk, jj)
+        check(f"{name}[sampled]", to_np(o[name])[kk, jj], ref, 1e-5, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
