@@ -12,10 +12,12 @@
 //       second stage applies the same epilogue.
 // Staging: operand tiles go from global memory straight into LDS (buffer loads
 // with the LDS destination, 16 bytes per lane, no registers on the way) through
-// a ring of NS stages of BK = 32 reduction steps.  Step t waits (vmcnt) until its
-// own loads of step t+1 have landed and meets the other waves at a barrier; then
-// the loads of step t+NS-1 go into the stage that step t-1 used, and step t+1's
-// first fragments are read while step t's second half of MFMAs runs.  Pieces
+// a ring of NS stages of BK = 32 reduction steps.  dX: step t waits (vmcnt) until
+// its own loads of step t+1 have landed and meets the other waves at a barrier;
+// then the loads of step t+NS-1 go into the stage that step t-1 used, and step
+// t+1's first fragments are read while step t's second half of MFMAs runs.  dW:
+// the two waves of a SIMD alternate between reading/loading and multiplying,
+// half a step apart (ping-pong), with a barrier between phases.  Pieces
 // outside the matrix (rows, columns, or the reduction tail) read as zero through
 // the buffer range check.  Workgroup: 512 threads = 4x2 waves, two per SIMD;
 // a wave owns a 64 x (BN/2) block of 32x32 MFMA tiles; tile 256 x BN with BN 128
@@ -396,51 +398,114 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmLaunch gl) {
         else wait_vm<2 * G>();
     };
     static_assert(NS == 4, "the ring code below is written for four stages");
-    if (nsteps > 0) ops.issue(Stage<0>{}, k_lo, wave);
-    if (nsteps > 1) ops.issue(Stage<1>{}, k_lo + BK, wave);
-    if (nsteps > 2) ops.issue(Stage<2>{}, k_lo + 2 * BK, wave);
-    // steady steps issue a load group each; the last NS-1 steps only drain
-    const int64_t steady = nsteps >= NS - 1 ? nsteps - (NS - 1) : 0;
-    if (steady > 0) wait_groups(std::integral_constant<int, NS - 2>{});
-    else wait_vm<0>();
-    ring_barrier();
-    FA a0, a1;
-    FB b0, b1;
-    if (nsteps > 0) ops.read(Stage<0>{}, 0, a0, b0, lane);
-    auto step = [&](auto St, int64_t t) __attribute__((always_inline)) {
-        constexpr int S = decltype(St)::value;
-        ops.read(St, 1, a1, b1, lane);
-        __builtin_amdgcn_sched_barrier(0);
-        mm(a0, b0);
-        wait_groups(std::integral_constant<int, NS - 3>{});  // step t+1's loads, every wave
+    if constexpr (TR) {
+        // dW: ping-pong schedule.  The two waves of a SIMD (w and w + 4) take turns,
+        // half a step apart, between a memory phase -- wait for the wave's own loads
+        // of the next stages, read the step's fragments from LDS, issue the loads
+        // three stages ahead -- and an MFMA phase (the step's 2 x MI x NJ MFMAs), with
+        // a workgroup barrier between phases: while one wave of a SIMD multiplies,
+        // the other feeds (dW at the layer workload 93 -> 85 us; the dX form, whose
+        // plain fragment reads are cheaper, gained nothing from it and keeps the
+        // schedule below).
+        if (nsteps > 0) ops.issue(Stage<0>{}, k_lo, wave);
+        if (nsteps > 1) ops.issue(Stage<1>{}, k_lo + BK, wave);
+        if (nsteps > 2) ops.issue(Stage<2>{}, k_lo + 2 * BK, wave);
+        FA a0, a1;
+        FB b0, b1;
+        // memory phase of step s: this wave's loads of stages <= s + 1 have landed
+        // (stage s + 2 may stay in flight; every wave waited for its share of stage s
+        // before an earlier barrier), the fragments of stage s are read and in
+        // registers before the next barrier (the other group reloads the slot read
+        // one step before), and stage s + 3 is issued into the slot of step s - 1
+        auto mem = [&](auto St, int64_t s) __attribute__((always_inline)) {
+            constexpr int S = decltype(St)::value;
+            if (s + 2 < nsteps) wait_groups(std::integral_constant<int, 1>{});
+            else wait_vm<0>();
+            ops.read(St, 0, a0, b0, lane);
+            ops.read(St, 1, a1, b1, lane);
+            if (s + 3 < nsteps) ops.issue(Stage<(S + 3) % NS>{}, k_lo + (s + 3) * BK, wave);
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // LDS reads done (vmcnt and expcnt unchanged)
+        };
+        if (nsteps > 2) wait_groups(std::integral_constant<int, 1>{});
+        else wait_vm<0>();
         ring_barrier();
-        ops.issue(Stage<(S + NS - 1) % NS>{}, k_lo + (t + NS - 1) * BK, wave);
-        ops.read(Stage<(S + 1) % NS>{}, 0, a0, b0, lane);
-        __builtin_amdgcn_sched_barrier(0);
-        mm(a1, b1);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    int64_t t = 0;
-    for (; t + NS <= steady; t += NS) {
-        step(Stage<0>{}, t);
-        step(Stage<1>{}, t + 1);
-        step(Stage<2>{}, t + 2);
-        step(Stage<3>{}, t + 3);
-    }
-    const int64_t rem = steady - t;  // t is a multiple of NS here
-    if (rem > 0) step(Stage<0>{}, t);
-    if (rem > 1) step(Stage<1>{}, t + 1);
-    if (rem > 2) step(Stage<2>{}, t + 2);
-    if (steady > 0 && steady < nsteps) {
-        wait_vm<0>();
+        auto mfma = [&]() __attribute__((always_inline)) {
+            mm(a0, b0);
+            mm(a1, b1);
+        };
+        // one step: its memory phase, a barrier, its MFMA phase, and the barrier that
+        // ends the interval unless it is the wave's last
+        auto pp_step = [&](auto St, int64_t s, bool last_barrier) __attribute__((always_inline)) {
+            mem(St, s);
+            ring_barrier();
+            mfma();
+            if (last_barrier) ring_barrier();
+        };
+        // group 0 (waves 0-3) starts with the memory phase of step 0; group 1 (waves
+        // 4-7) one interval later and so skips the barrier after its last MFMA phase:
+        // both groups pass 2 nsteps barriers
+        const bool g1 = wave >= 4;
+        if (g1 && nsteps > 0) ring_barrier();
+        int64_t t = 0;
+        for (; t + NS <= nsteps; t += NS) {
+            pp_step(Stage<0>{}, t, !g1 || t + 1 < nsteps);
+            pp_step(Stage<1>{}, t + 1, !g1 || t + 2 < nsteps);
+            pp_step(Stage<2>{}, t + 2, !g1 || t + 3 < nsteps);
+            pp_step(Stage<3>{}, t + 3, !g1 || t + 4 < nsteps);
+        }
+        const int64_t rem = nsteps - t;
+        if (rem > 0) pp_step(Stage<0>{}, t, !g1 || t + 1 < nsteps);
+        if (rem > 1) pp_step(Stage<1>{}, t + 1, !g1 || t + 2 < nsteps);
+        if (rem > 2) pp_step(Stage<2>{}, t + 2, !g1 || t + 3 < nsteps);
+    } else {
+        // dX: every wave reads, multiplies and loads in each step, one barrier per
+        // step.
+        if (nsteps > 0) ops.issue(Stage<0>{}, k_lo, wave);
+        if (nsteps > 1) ops.issue(Stage<1>{}, k_lo + BK, wave);
+        if (nsteps > 2) ops.issue(Stage<2>{}, k_lo + 2 * BK, wave);
+        // steady steps issue a load group each; the last NS-1 steps only drain
+        const int64_t steady = nsteps >= NS - 1 ? nsteps - (NS - 1) : 0;
+        if (steady > 0) wait_groups(std::integral_constant<int, NS - 2>{});
+        else wait_vm<0>();
         ring_barrier();
-    }
-    for (int64_t u = steady; u < nsteps; ++u) {
-        const int s = static_cast<int>(u % NS);
-        read_any(s, 1, a1, b1);
-        mm(a0, b0);
-        if (u + 1 < nsteps) read_any(s + 1 == NS ? 0 : s + 1, 0, a0, b0);
-        mm(a1, b1);
+        FA a0, a1;
+        FB b0, b1;
+        if (nsteps > 0) ops.read(Stage<0>{}, 0, a0, b0, lane);
+        auto step = [&](auto St, int64_t t) __attribute__((always_inline)) {
+            constexpr int S = decltype(St)::value;
+            ops.read(St, 1, a1, b1, lane);
+            __builtin_amdgcn_sched_barrier(0);
+            mm(a0, b0);
+            wait_groups(std::integral_constant<int, NS - 3>{});  // step t+1's loads, every wave
+            ring_barrier();
+            ops.issue(Stage<(S + NS - 1) % NS>{}, k_lo + (t + NS - 1) * BK, wave);
+            ops.read(Stage<(S + 1) % NS>{}, 0, a0, b0, lane);
+            __builtin_amdgcn_sched_barrier(0);
+            mm(a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        int64_t t = 0;
+        for (; t + NS <= steady; t += NS) {
+            step(Stage<0>{}, t);
+            step(Stage<1>{}, t + 1);
+            step(Stage<2>{}, t + 2);
+            step(Stage<3>{}, t + 3);
+        }
+        const int64_t rem = steady - t;  // t is a multiple of NS here
+        if (rem > 0) step(Stage<0>{}, t);
+        if (rem > 1) step(Stage<1>{}, t + 1);
+        if (rem > 2) step(Stage<2>{}, t + 2);
+        if (steady > 0 && steady < nsteps) {
+            wait_vm<0>();
+            ring_barrier();
+        }
+        for (int64_t u = steady; u < nsteps; ++u) {
+            const int s = static_cast<int>(u % NS);
+            read_any(s, 1, a1, b1);
+            mm(a0, b0);
+            if (u + 1 < nsteps) read_any(s + 1 == NS ? 0 : s + 1, 0, a0, b0);
+            mm(a1, b1);
+        }
     }
 
     float* dst = g.C ? g.C + (g.direct ? 0 : static_cast<int64_t>(split) * g.R * g.Cc) : nullptr;
