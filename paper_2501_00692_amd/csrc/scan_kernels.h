@@ -146,6 +146,55 @@ __device__ __forceinline__ void lane_consts(const float* A_log, int64_t d, int r
     }
 }
 
+// Rows of C at the truncated window's shifted steps (16 states), staged per
+// segment: the S rows x 16 states of a segment are spread over the 64 lanes of a
+// wave, CPL = S/4 consecutive states per lane, and loaded through a raw buffer
+// resource over the rows that exist (rows past it read as zero).  Loading them
+// per step instead, next to their use, left every step waiting for a load: the
+// row's validity is wave-uniform, the compiler branched around the load, and the
+// branch's merge waited for all outstanding memory operations.
+template <typename TI, int S>
+struct ShiftedC {
+    static constexpr int CPL = S / 4;                    // states per lane
+    static constexpr int BYTES = CPL * sizeof(TI);       // 4, 8 or 16
+    using Raw = typename std::conditional<BYTES == 4, uint32_t,
+                typename std::conditional<BYTES == 8, uint32_t __attribute__((ext_vector_type(2))),
+                                          uint32_t __attribute__((ext_vector_type(4)))>::type>::type;
+    static_assert(BYTES == 4 || BYTES == 8 || BYTES == 16, "segment length");
+
+    // raw bits of the rows of segment qs (in-chunk steps qs*S ..) that lane `lane` stages
+    static __device__ __forceinline__ Raw load(__amdgpu_buffer_rsrc_t rs, int qs, int lane) {
+        const int row = qs * S + lane / (16 / CPL), n0 = (lane % (16 / CPL)) * CPL;
+        const int off = (row * 16 + n0) * static_cast<int>(sizeof(TI));
+        if constexpr (BYTES == 4) return __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+        else if constexpr (BYTES == 8) return __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0);
+        else return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+    }
+    // fp32 values of the lane's CPL states into w[j][n / 4][16 + n % 4] (the spare
+    // column of the wave's channel-sum rows): states 4r .. 4r+3 of step j end up at
+    // w[j][r][16 .. 19]
+    static __device__ __forceinline__ void stage(const Raw& u, float (&w)[S][16][20], int lane) {
+        const int j = lane / (16 / CPL), n0 = (lane % (16 / CPL)) * CPL;
+        float v[CPL];
+        if constexpr (sizeof(TI) == 2) {
+#pragma unroll
+            for (int i = 0; i < CPL / 2; ++i) {
+                uint32_t x;
+                if constexpr (BYTES == 4) x = u;
+                else x = u[i];
+                v[2 * i] = __uint_as_float(x << 16);
+                v[2 * i + 1] = __uint_as_float(x & 0xffff0000u);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < CPL; ++i) v[i] = __uint_as_float(u[i]);
+        }
+        float* dst = &w[j][n0 / 4][16 + n0 % 4];
+        if constexpr (CPL == 2) *reinterpret_cast<float2*>(dst) = make_float2(v[0], v[1]);
+        else *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+};
+
 // Uniform loads of the (up to) 16 states of row `row` of a [rows][N] tensor:
 // the same for every lane of the wave.
 template <typename TI>
@@ -713,13 +762,18 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     const int64_t tile_hi = min(ntile, tile_lo + p.tps);
     const int64_t nit = (tile_hi - tile_lo + NW - 1) / NW;  // the same for every wave
 
-    // truncated mode: the chunk's steps shifted by tbar
+    // truncated mode: the chunk's steps shifted by tbar, and (16 states) a buffer
+    // resource over the rows of C at the shifted steps that exist
     ChunkPtrs<TI> cps;
     int64_t lims = 0;
     if constexpr (TRUNC) {
         cps.set(p, bb * p.T + min(t0 + p.tbar, p.T - 1));
         lims = p.T - (t0 + p.tbar);
     }
+    const int64_t c_rows = (TRUNC && N16) ? max<int64_t>(0, min<int64_t>(L, lims)) : 0;
+    const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<TI*>(static_cast<const TI*>(p.C) + (bb * p.T + min(t0 + p.tbar, p.T)) * 16), 0,
+        static_cast<int>(c_rows * 16 * static_cast<int64_t>(sizeof(TI))), 0x00020000);
 
     for (int i = tid; i < L * 32; i += NTH) (&acc[0][0])[i] = 0.f;
     bc.template load<NTH>(p, bb, t0, tid);
@@ -776,6 +830,9 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
         RawIn<TI, SPL> nxs;  // raw inputs at the shifted positions (truncated mode)
         load_raw2<TI, GATE, SPL>(cp, D32, d32, (NCK - 1) * S, r, lim, dv, true, nxt);
         if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (NCK - 1) * S, r, lims, dv, true, nxs);
+        using SC = ShiftedC<TI, S>;
+        typename SC::Raw nxc{};  // shifted C rows of the next segment (truncated mode, 16 states)
+        if constexpr (TRUNC && N16) nxc = SC::load(rsC, NCK - 1, lane);
 
         // segment-start states: hseg[q] + (prod of a from the chunk start) H_c, the
         // product being 2^{cn cseg[q]}; loaded one segment ahead
@@ -870,6 +927,11 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 load_raw2<TI, GATE, SPL>(cp, D32, d32, qn * S, r, lim, dv, true, nxt);
                 if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, qn * S, r, lims, dv, true, nxs);
             }
+            typename SC::Raw curc{};
+            if constexpr (TRUNC && N16) {
+                curc = nxc;
+                nxc = SC::load(rsC, q > 0 ? q - 1 : 0, lane);
+            }
             // per-channel quantities of the steps this lane prepares
             float dls[SPL], xs[SPL], xr[SPL], gs[SPL], gfs[SPL], dlps[SPL], gps[SPL];
             bool sv[SPL];
@@ -950,6 +1012,10 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 }
             }
             wave_sums(2 * pair);  // dC
+            if constexpr (TRUNC && N16) {
+                SC::stage(curc, red[wave], lane);
+                wave_lds_sync();
+            }
 
             float dxk[SPL], ddk[SPL];
 #pragma unroll
@@ -977,7 +1043,12 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     const float dlp = quad_bcast(dlps[j >> 2], j & 3);
                     const float gp = quad_bcast(gps[j >> 2], j & 3);
                     float Cs[4];
-                    ld4<TI, N16>(static_cast<const TI*>(p.C), bb * p.T + ps, r, p.N, pv, Cs);
+                    if constexpr (N16) {
+                        const float4 c4 = *reinterpret_cast<const float4*>(&red[wave][j][r][16]);
+                        Cs[0] = c4.x; Cs[1] = c4.y; Cs[2] = c4.z; Cs[3] = c4.w;
+                    } else {
+                        ld4<TI, N16>(static_cast<const TI*>(p.C), bb * p.T + ps, r, p.N, pv, Cs);
+                    }
                     const float wf = static_cast<float>(W);
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
