@@ -865,31 +865,79 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 const int64_t mb = ((bb * p.nc + cpk) * p.N + r * 4) * p.D + d;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) Msh[k] = ldm(p.mbuf, mb + k * p.D, nv[k]);
+                // steps cpend down to pstart + 1, eight at a time: the loads of a batch
+                // (from clamped, always valid addresses) are issued before its
+                // arithmetic, and steps outside the sweep are masked to exact no-ops
+                // (Delta = g = C = 0 leave Msh and the Delta sum unchanged) with bit
+                // masks: selecting a loaded value instead lets the compiler turn the
+                // select into a branch around the load, whose merge then waits for it.
+                const TI* DL = static_cast<const TI*>(p.delta);
+                const TI* DY = static_cast<const TI*>(p.dy);
+                const TI* Z = static_cast<const TI*>(p.z);
+                constexpr int PB = 8;
                 double pre = 0.0;
-                for (int64_t ps = cpend; ps > pstart; --ps) {
-                    const bool pv = ps < p.T;
-                    float dlp = 0.f, gp = 0.f;
-                    if (pv && dv) {
-                        const TI* DL = static_cast<const TI*>(p.delta);
-                        const TI* DY = static_cast<const TI*>(p.dy);
-                        const TI* Z = static_cast<const TI*>(p.z);
-                        const int64_t td = (bb * p.T + ps) * p.D + d;
-                        const float pr = ldf(DL, td);
-                        dlp = SP ? softplus_f(pr) : pr;
-                        const float gy = ldf(DY, td);
-                        if constexpr (GATE) {
-                            const float zv = ldf(Z, td);
-                            gp = gy * zv * sigmoid_f(zv);
+                for (int64_t p0 = cpend; p0 > pstart; p0 -= PB) {
+                    typename RawIn<TI, PB>::Bits prb[PB], gyb[PB], zb[PB];
+                    uint32_t mk[PB];
+                    // raw C bits: 4 bf16 (two words) or 4 fp32 words per step
+                    uint32_t cw[PB][sizeof(TI) == 2 ? 2 : 4];
+                    float Cb[PB][4];
+#pragma unroll
+                    for (int u = 0; u < PB; ++u) {
+                        const int64_t ps = p0 - u;
+                        const bool ok = dv && ps > pstart && ps < p.T;
+                        mk[u] = ok ? 0xffffffffu : 0u;
+                        const int64_t row = bb * p.T + min(max<int64_t>(ps, 0), p.T - 1);
+                        const int64_t td = row * p.D + (dv ? d : 0);
+                        prb[u] = ldbits(DL, td);
+                        gyb[u] = ldbits(DY, td);
+                        zb[u] = GATE ? ldbits(Z, td) : 0;
+                        if constexpr (N16) {
+                            if constexpr (sizeof(TI) == 2) {
+                                const uint2 w = *reinterpret_cast<const uint2*>(Cp + row * 16 + r * 4);
+                                cw[u][0] = w.x;
+                                cw[u][1] = w.y;
+                            } else {
+                                const uint4 w = *reinterpret_cast<const uint4*>(Cp + row * 16 + r * 4);
+                                cw[u][0] = w.x;
+                                cw[u][1] = w.y;
+                                cw[u][2] = w.z;
+                                cw[u][3] = w.w;
+                            }
                         } else {
-                            gp = gy;
+                            ld4<TI, N16>(Cp, bb * p.T + ps, r, p.N, ok, Cb[u]);
                         }
                     }
-                    float Cv[4];
-                    ld4<TI, N16>(Cp, bb * p.T + ps, r, p.N, pv, Cv);
+                    // keep the batch's loads ahead of its arithmetic
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        Msh[k] = fexp2(cn[k] * dlp) * fmaf(gp, Cv[k], Msh[k]);
-                    pre += static_cast<double>(dlp);
+                    for (int u = 0; u < PB; ++u) {
+                        const uint32_t m = mk[u];
+                        if constexpr (N16) {
+                            if constexpr (sizeof(TI) == 2) {
+                                Cb[u][0] = __uint_as_float((cw[u][0] << 16) & m);
+                                Cb[u][1] = __uint_as_float((cw[u][0] & 0xffff0000u) & m);
+                                Cb[u][2] = __uint_as_float((cw[u][1] << 16) & m);
+                                Cb[u][3] = __uint_as_float((cw[u][1] & 0xffff0000u) & m);
+                            } else {
+#pragma unroll
+                                for (int k = 0; k < 4; ++k) Cb[u][k] = __uint_as_float(cw[u][k] & m);
+                            }
+                        }
+                        const float pr = fin<TI>(prb[u], true);
+                        const float dlp = __uint_as_float(__float_as_uint(SP ? softplus_f(pr) : pr) & m);
+                        const float gy = fin<TI>(gyb[u], true);
+                        float g0 = gy;
+                        if constexpr (GATE) {
+                            const float zv = fin<TI>(zb[u], true);
+                            g0 = gy * zv * sigmoid_f(zv);
+                        }
+                        const float gp = __uint_as_float(__float_as_uint(g0) & m);
+#pragma unroll
+                        for (int k = 0; k < 4; ++k)
+                            Msh[k] = fexp2(cn[k] * dlp) * fmaf(gp, Cb[u][k], Msh[k]);
+                        pre += static_cast<double>(dlp);
+                    }
                 }
                 if (dv)
                     W = (p.psum[pb + cpk * p.D] - p.psum[pb + (c + 1) * p.D]) +
