@@ -34,13 +34,15 @@ __device__ __forceinline__ float ldf(const uint16_t* p, int64_t i) {
 __device__ __forceinline__ void stf(float* p, int64_t i, float v) { p[i] = v; }
 
 // Masked loads without a branch: a lane whose element is not valid reads
-// element 0 of the same array (which exists) and discards the value.  The load
-// is then issued unconditionally and waited on at its first use; a load under
-// a divergent condition is waited on inside its own branch, right after issue.
+// element 0 of the same array (which exists) and clears the value with a bit
+// mask.  The load is then issued unconditionally and waited on at its first use;
+// a load under a condition is waited on inside its own branch, right after
+// issue, and a select between the loaded value and 0 is turned by the compiler
+// into exactly such a branch (hence the mask, not a select).
 template <typename T>
 __device__ __forceinline__ float ldm(const T* p, int64_t i, bool v) {
     const float r = ldf(p, v ? i : 0);
-    return v ? r : 0.f;
+    return __uint_as_float(__float_as_uint(r) & (v ? 0xffffffffu : 0u));
 }
 __device__ __forceinline__ void stf(uint16_t* p, int64_t i, float v) {
     uint32_t u = __float_as_uint(v);
@@ -610,24 +612,31 @@ template <typename TI, int L>
 struct __attribute__((aligned(16))) BCStage {
     float w[L][32];
 
-    // NTH threads; each issues all of its loads before it writes any to LDS.
+    // NTH threads; each issues all of its loads (raw element bits) before it
+    // masks and writes any to LDS (the scheduling barrier keeps the compiler from
+    // placing each load's wait and use right behind it).
     template <int NTH>
     __device__ __forceinline__ void load(const ScanProblem& p, int64_t bb, int64_t t0, int tid) {
         constexpr int PT = (L * 32 + NTH - 1) / NTH;
         const TI* Bp = static_cast<const TI*>(p.B);
         const TI* Cp = static_cast<const TI*>(p.C);
-        float v[PT];
+        typename RawIn<TI, 1>::Bits v[PT];
+        uint32_t mk[PT];
 #pragma unroll
         for (int e = 0; e < PT; ++e) {
             const int i = tid + NTH * e;
             const int t = i >> 5, c = i & 31, n = c & 15;
             const int64_t tg = t0 + t;
-            v[e] = ldm(c < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, i < L * 32 && tg < p.T && n < p.N);
+            const bool ok = i < L * 32 && tg < p.T && n < p.N;
+            mk[e] = ok ? 0xffffffffu : 0u;
+            v[e] = ldbits(c < 16 ? Bp : Cp, ok ? (bb * p.T + tg) * p.N + n : 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int e = 0; e < PT; ++e) {
             const int i = tid + NTH * e;
-            if ((L * 32) % NTH == 0 || i < L * 32) w[i >> 5][i & 31] = v[e];
+            const uint32_t b = sizeof(TI) == 2 ? static_cast<uint32_t>(v[e]) << 16 : static_cast<uint32_t>(v[e]);
+            if ((L * 32) % NTH == 0 || i < L * 32) w[i >> 5][i & 31] = __uint_as_float(b & mk[e]);
         }
     }
     // States 4r..4r+3 of B and C at in-chunk step t.
