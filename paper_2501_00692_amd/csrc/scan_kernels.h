@@ -320,22 +320,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     };
     // B/C values of the staged block starting at step sb (padding and steps past
     // the chunk read as 0)
-    float bcv[PT];
+    // raw element bits and validity masks, applied when the block is stored (a
+    // masked value right after its load would make each load wait on the spot)
+    typename RawIn<TI, 1>::Bits bcv[PT];
+    uint32_t bcm[PT];
     auto load_bc = [&](int64_t sb) {
 #pragma unroll
         for (int e = 0; e < PT; ++e) {
             const int i = tid + 256 * e;
             const int t = i >> 5, cc = i & 31, n = cc & 15;
             const int64_t tg = sb + t;
-            const bool want = cc < 16 || WANT_M;
-            bcv[e] = ldm(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, want && tg < t1 && n < p.N);
+            const bool ok = (cc < 16 || WANT_M) && tg < t1 && n < p.N;
+            bcm[e] = ok ? 0xffffffffu : 0u;
+            bcv[e] = ldbits(cc < 16 ? Bp : Cp, ok ? (bb * p.T + tg) * p.N + n : 0);
         }
     };
     auto store_bc = [&](int buf) {
 #pragma unroll
         for (int e = 0; e < PT; ++e) {
             const int i = tid + 256 * e;
-            bcs[buf][i >> 5][i & 31] = bcv[e];
+            const uint32_t b = sizeof(TI) == 2 ? static_cast<uint32_t>(bcv[e]) << 16 : static_cast<uint32_t>(bcv[e]);
+            bcs[buf][i >> 5][i & 31] = __uint_as_float(b & bcm[e]);
         }
     };
     load_bc(t0);
@@ -549,19 +554,26 @@ __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
     uint32_t zb = 0;
     if constexpr (GATE) zb = ldbits(static_cast<const TI*>(p.z), dv && t0 + r < p.T ? (bb * p.T + t0 + r) * p.D + d : 0);
     for (int64_t sb = t0; sb < t1; sb += SB) {
-        float bcv[PT];
+        // the block's loads all issued before any is used (raw bits, masks
+        // applied at the store)
+        typename RawIn<TI, 1>::Bits bcv[PT];
+        uint32_t bcm[PT];
 #pragma unroll
         for (int e = 0; e < PT; ++e) {
             const int i = tid + 256 * e;
             const int t = i >> 5, cc = i & 31, n = cc & 15;
             const int64_t tg = sb + t;
-            bcv[e] = ldm(cc < 16 ? Bp : Cp, (bb * p.T + tg) * p.N + n, tg < t1 && n < p.N);
+            const bool ok = tg < t1 && n < p.N;
+            bcm[e] = ok ? 0xffffffffu : 0u;
+            bcv[e] = ldbits(cc < 16 ? Bp : Cp, ok ? (bb * p.T + tg) * p.N + n : 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
         lds_barrier();  // the previous block's reads are done
 #pragma unroll
         for (int e = 0; e < PT; ++e) {
             const int i = tid + 256 * e;
-            bcs[i >> 5][i & 31] = bcv[e];
+            const uint32_t b = sizeof(TI) == 2 ? static_cast<uint32_t>(bcv[e]) << 16 : static_cast<uint32_t>(bcv[e]);
+            bcs[i >> 5][i & 31] = __uint_as_float(b & bcm[e]);
         }
         lds_barrier();
         const int64_t se = min(sb + SB, t1);
