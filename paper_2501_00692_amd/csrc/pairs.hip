@@ -66,18 +66,67 @@ __global__ __launch_bounds__(kPairLanes) void k_pairs(const ScanProblem p, const
     }
     const int64_t rowb = bb * p.T;
     const int64_t te = min(p.T, i + W);
-    for (int64_t t = i; t < te; ++t) {
-        const int64_t td = (rowb + t) * p.D + d;
-        const float gt = gv[td];
-        float Ct[16];
-        ld_row16(Cp, rowb + t, p.N, Ct);
-        if (t > i) {
-            const float dlt = dlv[td];
+    if (p.N == 16) {
+        // eight steps at a time: the batch's loads (from clamped, valid addresses)
+        // are all issued before its arithmetic; steps past the window and the
+        // decay of step i itself are masked to exact no-ops with bit masks
+        // (g = C = 0 leave m unchanged, Delta = 0 leaves P unchanged)
+        constexpr int PB = 8;
+        for (int64_t tb = i; tb < te; tb += PB) {
+            float gb[PB], db[PB];
+            uint32_t cw[PB][sizeof(TI) == 2 ? 8 : 16];
 #pragma unroll
-            for (int n = 0; n < 16; ++n) P[n] *= fexp2(cn[n] * dlt);
+            for (int u = 0; u < PB; ++u) {
+                const int64_t tc = min(tb + u, te - 1);
+                const int64_t td = (rowb + tc) * p.D + d;
+                gb[u] = gv[td];
+                db[u] = dlv[td];
+                const uint4* row = reinterpret_cast<const uint4*>(Cp + (rowb + tc) * 16);
+#pragma unroll
+                for (int q = 0; q < static_cast<int>(sizeof(TI)); ++q) {  // 16-byte pieces of the row
+                    const uint4 w = row[q];
+                    cw[u][4 * q] = w.x;
+                    cw[u][4 * q + 1] = w.y;
+                    cw[u][4 * q + 2] = w.z;
+                    cw[u][4 * q + 3] = w.w;
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int u = 0; u < PB; ++u) {
+                const int64_t t = tb + u;
+                const uint32_t in = t < te ? 0xffffffffu : 0u;
+                const uint32_t dec = t > i && t < te ? 0xffffffffu : 0u;
+                const float gt = __uint_as_float(__float_as_uint(gb[u]) & in);
+                const float dlt = __uint_as_float(__float_as_uint(db[u]) & dec);
+                float Ct[16];
+#pragma unroll
+                for (int n = 0; n < 16; ++n) {
+                    uint32_t b;
+                    if constexpr (sizeof(TI) == 2) b = (n & 1) ? (cw[u][n >> 1] & 0xffff0000u) : (cw[u][n >> 1] << 16);
+                    else b = cw[u][n];
+                    Ct[n] = __uint_as_float(b & in);
+                }
+#pragma unroll
+                for (int n = 0; n < 16; ++n) P[n] *= fexp2(cn[n] * dlt);
+#pragma unroll
+                for (int n = 0; n < 16; ++n) m[n] = fmaf(gt * Ct[n], P[n], m[n]);
+            }
         }
+    } else {
+        for (int64_t t = i; t < te; ++t) {
+            const int64_t td = (rowb + t) * p.D + d;
+            const float gt = gv[td];
+            float Ct[16];
+            ld_row16(Cp, rowb + t, p.N, Ct);
+            if (t > i) {
+                const float dlt = dlv[td];
 #pragma unroll
-        for (int n = 0; n < 16; ++n) m[n] = fmaf(gt * Ct[n], P[n], m[n]);
+                for (int n = 0; n < 16; ++n) P[n] *= fexp2(cn[n] * dlt);
+            }
+#pragma unroll
+            for (int n = 0; n < 16; ++n) m[n] = fmaf(gt * Ct[n], P[n], m[n]);
+        }
     }
     float4* o = reinterpret_cast<float4*>(mu + ((rowb + i) * p.D + d) * 16);
 #pragma unroll
