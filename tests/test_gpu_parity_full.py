@@ -192,10 +192,14 @@ def test_vlong_workload_truncated_sampled():
     say("   rel-L2 max:", f"{max(rep.values()):.2e}", "over", len(rep), "checks")
 
 
-def test_long_slow_decay_truncated():
-    """Slow decay (Delta / 2048) so that the 2048-step window is visible: full
-    shape on sampled channels, and every output on a reduced shape."""
-    w = WORKLOADS["long_slow"]
+@pytest.mark.parametrize("tbar", [2048, 2000])
+def test_long_slow_decay_truncated(tbar):
+    """Slow decay (Delta / 2048) so that the window is visible: full shape on
+    sampled channels, and every output on a reduced shape.  2000 is not a
+    multiple of the 128-step chunk: every tile then also sweeps the adjoint carry
+    back from the end of the chunk that holds t + tbar, up to 127 steps, and the
+    last chunks' sweeps run past the end of the sequence."""
+    w = WORKLOADS["long_slow"].with_(tbar=tbar)
     say(f"[long_slow] {w}")
     inp = make_inputs(w, device="cuda")
     g = ssm.ssm_adjoint_grad(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], tbar=w.tbar)
