@@ -1,11 +1,18 @@
 """Benchmark of the per-layer adjoint gradient on one MI355X.
 
-One step = one whole-layer gradient call (``ssm_layer_grad``): the chunked
-forward recomputation, the reverse adjoint scan with its vjp epilogue, and the
-projection-gradient GEMMs, on the "layer" workload (b=2, T=4096, d_model=768,
-D=1536, N=16, full gradient; bf16 activations, fp32 accumulation).  Inputs are
-seeded synthetic tensors already resident in HBM.  The other workloads are
-reported under "extra".
+One step = the layer's two gradients over one batch of the "slice" workload
+(a 1.27B-class layer slice: b=1, T=262,144, d_model=2,048, D=4,096, N=16, with
+input projections and the SiLU gate; bf16 activations, fp32 accumulation): one
+``ssm_layer_grad`` call in full mode (Prop. 2) and one in truncated mode
+(Eq. "capped", window 4,096).  Together they run every step of the hot path:
+the decay in registers, the chunked forward recomputation with its two-level
+carry, the reverse adjoint (full) and the windowed adjoint (truncated) with the
+vjp epilogue, the activation vjps into projection space and the projection-
+gradient GEMMs.  Inputs are seeded synthetic tensors already resident in HBM.
+``value`` is tokens of gradient computed per second, 2 b T per step (the two
+modes' rates combined harmonically); each mode's own rate is in ``modes``.
+Per-kernel times come from hipEvents recorded around every launch on its
+stream during the timed steps.  The other workloads are reported under "extra".
 
 Prints ONE JSON line.  ``--gpus`` above 1 is not supported (one GPU).
 """
@@ -24,44 +31,44 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 MFMA
 # MI355X fp32 vector arithmetic: 256 CUs x 4 SIMDs x 32 lanes per cycle x 2 (FMA)
-# x 2.4 GHz = 157.3 TFLOP/s.  On gfx950 an ordinary (non-packed) wave64 fp32
-# add, mul or FMA issues every 2 cycles per SIMD, so this peak needs no packed
-# instructions (which this library's kernels are built without).
+# x 2.4 GHz = 157.3 TFLOP/s (reported beside the HBM fraction of the scan kernels)
 FP32_VECTOR_PEAK_TFS = 157.3
+HEADLINE = "slice"
 
 
 def scan_flops_per_state_step(trunc):
-    """Algorithmic fp32 operations per (state, token) of the fused gradient (an FMA
-    counts 2, exp counts 1): forward recompute a = exp(Delta c) (2), h = a h + B x (3),
-    y += C h (2), dC contribution and channel sum (2); reverse mu = g C + a mu (3),
-    dx += mu B (2), s = mu (a h) (2), ddelta += s w (2), dA += s Delta (2), dB
-    contribution and sum (2) -> 22.  The truncated window adds the window product
-    P = exp(W c) (2), the tail nu = P g' C' + a nu (4) and mubar = mu - nu (1)."""
-    return 22 + (7 if trunc else 0)
+    """fp32 operations per (state, token) of the fused gradient (an FMA counts 2,
+    exp counts 1): forward recompute a = exp(Delta c) (2), h = a h + B x (3),
+    y += C h (2), dC contribution and channel sum (2); reverse adjoint mu = g C +
+    a mu (3), dx += mu B (2), s = mu (a h) (2), ddelta += s w (2), dA += s Delta
+    (2), dB contribution and sum (2) -> 22.  The truncated form adds the window
+    product P = exp(W c) (2) and the step leaving the window, - P g' C' (3)."""
+    return 22 + (5 if trunc else 0)
 
 
-def scan_bytes_per_token(D, N, s, gate, layer=False):
-    """Compulsory HBM bytes per token of the scan gradient: every input read once
-    and every output written once at the ABI's dtypes (outputs fp32).  Inside the
-    whole-layer call with no scan outputs requested (``layer``), the kernel writes
-    dx in fp32 (the projection GEMM's addend) and dDelta_pre, dz, dB, dC as the
-    bf16 operands of the projection GEMMs, plus fp32 dB, dC."""
-    if layer:  # reads x, Delta_pre, dy, z; writes dx (fp32), dDelta_pre, dz (bf16)
-        return D * (4 * s + 4 + 2 + 2) + N * (2 * s + 8 + 4)
-    if gate:  # reads x, Delta_pre, dy, z; writes dx, dDelta_pre, dz
-        per_ch = 4 * s + 12
-    else:     # reads x, Delta, dy; writes dx, dDelta
-        per_ch = 3 * s + 8
-    return D * per_ch + N * (2 * s + 8)  # reads B, C; writes dB, dC
+def scan_bytes_per_token(D, N, s, gate):
+    """Compulsory HBM bytes per token of the scan gradient at the C ABI's dtypes:
+    every input read once and every output written once (outputs fp32).  With the
+    gate: reads x, Delta_pre, dy, z, writes dx, dDelta_pre, dz; without: reads x,
+    Delta, dy, writes dx, dDelta; both read B, C and write dB, dC."""
+    per_ch = 4 * s + 12 if gate else 3 * s + 8
+    return D * per_ch + N * (2 * s + 8)
 
 
-def layer_gemm_flops(M, D, N, dm, with_du=False):
-    f = 2 * M * D * (D + 2 * N)        # dW_x = x^T dZx
-    f += 2 * M * (D + 2 * N) * D       # dx_total = dx + dZx W_x^T
-    f += 2 * M * dm * 2 * D            # dW_in = u^T [dx_total | dz]
-    if with_du:
-        f += 2 * M * 2 * D * dm
-    return f
+def layer_scan_bytes_per_token(D, N, s):
+    """Compulsory bytes per token of the scan kernel inside the whole-layer call,
+    which writes dx in fp32 (the projection GEMM's addend) and dDelta_pre, dz, dB,
+    dC as the GEMMs' bf16 operands (plus dB, dC in fp32): reads x, Delta_pre, dy,
+    z, B, C."""
+    return D * (4 * s + 4 + 2 + 2) + N * (2 * s + 8 + 4)
+
+
+def layer_gemm_flops(M, D, N, dm):
+    """Flops of the layer's projection products: (dW_x + dW_in, the one weight-
+    gradient launch) and dx_total = dx + dZx W_x^T (the dX launch)."""
+    dw = 2 * M * D * (D + 2 * N) + 2 * M * dm * 2 * D
+    dx = 2 * M * (D + 2 * N) * D
+    return dw, dx
 
 
 def _timed(fn, steps, warmup, torch):
@@ -76,6 +83,31 @@ def _timed(fn, steps, warmup, torch):
     stop.record()
     torch.cuda.synchronize()
     return start.elapsed_time(stop) / steps
+
+
+def _timed_kernels(fn, steps, warmup, ssm, torch):
+    """Time `steps` calls of `fn` (ms per call) with every library kernel launch
+    bracketed by hipEvents on its own stream; returns the per-call time and the
+    per-kernel launches and durations of the same calls."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ssm.timing_summary()  # clear
+    ssm.timing_enable(True)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        fn()
+    stop.record()
+    torch.cuda.synchronize()
+    ssm.timing_enable(False)
+    ms = start.elapsed_time(stop) / steps
+    kt = {}
+    for name, (n, tot) in ssm.timing_summary().items():
+        kt[name] = {"launches": n, "total_ms": tot, "avg_ms": tot / n, "launches_per_step": n / steps,
+                    "ms_per_step": tot / steps}
+    return ms, kt
 
 
 def _timed_each(fn, reps, warmup, torch, flush=None):
@@ -101,59 +133,20 @@ def _timed_each(fn, reps, warmup, torch, flush=None):
     return {"median": pick(0.5), "p10": pick(0.1), "p90": pick(0.9), "reps": reps}
 
 
-def _timed_graph(fn, steps, warmup, torch):
-    """Per-step time of `fn` captured once in a HIP graph and replayed `steps`
-    times (launch overheads between the step's kernels removed)."""
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        fn()
-    torch.cuda.current_stream().wait_stream(side)
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        fn()
-    for _ in range(warmup):
-        graph.replay()
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(steps):
-        graph.replay()
-    stop.record()
-    torch.cuda.synchronize()
-    return start.elapsed_time(stop) / steps
-
-
-def _kernel_times(fn, steps, ssm, torch):
-    """Per-kernel average launch duration (ms) from hipEvents recorded on the
-    launch stream around every kernel of `steps` calls."""
-    torch.cuda.synchronize()
-    ssm.timing_summary()
-    ssm.timing_enable(True)
-    for _ in range(steps):
-        fn()
-    ssm.timing_enable(False)
-    torch.cuda.synchronize()
-    out = {}
-    for name, (n, ms) in ssm.timing_summary().items():
-        out[name] = {"launches": n, "total_ms": ms, "avg_ms": ms / n, "launches_per_step": n / steps}
-    return out
-
-
-def layer_step(w, inp, ssm, torch, tbar=0, b_delta=False):
+def layer_step(w, inp, ssm, torch, tbar=0, b_delta=False, chunk=0, ws=None):
     """One whole-layer gradient; ``inp["A_log"]`` of shape [D] selects the scalar-decay variant."""
-    b, T, D, N, dm = w.b, w.T, w.D, w.N, w.d_model
+    D, N, dm = w.D, w.N, w.d_model
     f32 = dict(dtype=torch.float32, device="cuda")
     out = {"dW_in": torch.empty(dm, 2 * D, **f32), "dW_x": torch.empty(D, D + 2 * N, **f32),
            "dA_log": torch.empty(*inp["A_log"].shape, **f32)}
-    desc = ssm.make_desc(inp["x"], N, True, True, 0, inp["A_log"].dim() == 1, b_delta)
-    ws = torch.empty(ssm.layer_workspace_size(desc, tbar, dm), dtype=torch.uint8, device="cuda")
+    if ws is None:
+        desc = ssm.make_desc(inp["x"], N, True, True, chunk, inp["A_log"].dim() == 1, b_delta)
+        ws = torch.empty(ssm.layer_workspace_size(desc, tbar, dm), dtype=torch.uint8, device="cuda")
 
     def step():
         ssm.ssm_layer_grad(inp["u"], inp["x"], inp["z"], inp["delta"], inp["B"], inp["C"], inp["W_x"],
-                           inp["W_in"], inp["A_log"], inp["dy"], tbar=tbar, out=out, workspace=ws, b_delta=b_delta)
+                           inp["W_in"], inp["A_log"], inp["dy"], tbar=tbar, chunk=chunk, out=out, workspace=ws,
+                           b_delta=b_delta)
     return step
 
 
@@ -165,7 +158,7 @@ def vjp_pairs(T, tbar):
     return tbar * T - tbar * (tbar - 1) // 2
 
 
-def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False, pairs=False):
+def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False, pairs=False, chunk=0):
     """One scan gradient; ``inp["A_log"]`` of shape [D] selects the scalar-decay variant;
     ``pairs`` evaluates it by the explicit pair formulation instead of the adjoint scan."""
     b, T, D, N = w.b, w.T, w.D, w.N
@@ -176,13 +169,13 @@ def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False, pairs=False):
     z = inp.get("z") if w.proj else None
     if z is not None:
         out["dz"] = torch.empty(b, T, D, **f32)
-    desc = ssm.make_desc(inp["x"], N, w.proj, z is not None, 0, inp["A_log"].dim() == 1, b_delta)
+    desc = ssm.make_desc(inp["x"], N, w.proj, z is not None, chunk, inp["A_log"].dim() == 1, b_delta)
     ws = torch.empty(ssm.grad_workspace_size(desc, tbar, pairs), dtype=torch.uint8, device="cuda")
     fn = ssm.ssm_adjoint_grad_pairs if pairs else ssm.ssm_adjoint_grad
 
     def step():
         fn(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], z=z, softplus=w.proj, tbar=tbar,
-           out=out, workspace=ws, b_delta=b_delta)
+           chunk=chunk, out=out, workspace=ws, b_delta=b_delta)
     return step
 
 
@@ -243,64 +236,121 @@ def measured_traffic(kern, workload):
     return int(rec["bytes_per_launch"])
 
 
-def tbar_of(kind):
-    """`kind` is "layer"/"scan" (full) or a (kind, tbar) tuple."""
-    return kind[1] if isinstance(kind, tuple) else 0
+def workload_tag(w):
+    return f"{w.name}-b{w.b}-T{w.T}-D{w.D}"
 
 
-def roofline_for(kern, ktimes, w, kind):
-    """Roofline entry for kernel `kern` (algorithmic work per launch / average
-    launch duration)."""
-    kt = ktimes[kern]
+def rooflines(kt, w, layer, tag=None):
+    """Roofline entries of the kernels with an algorithmic work figure: the scan
+    gradient kernels against HBM (compulsory bytes per launch / average launch
+    duration), the projection GEMMs against bf16 MFMA (flops per launch / average
+    launch duration).  One launch of each per gradient call."""
     s = 2 if w.bf16 else 4
-    if kern == "grad_fused":
-        layer = (kind[0] if isinstance(kind, tuple) else kind) == "layer"
-        per_launch = scan_bytes_per_token(w.D, w.N, s, w.proj, layer) * w.M  # bytes
-        gbs = per_launch / (kt["avg_ms"] * 1e-3) / 1e9
-        flops = scan_flops_per_state_step(0 < tbar_of(kind) < w.T) * w.M * w.D * w.N
-        tfs = flops / (kt["avg_ms"] * 1e-3) / 1e12
-        return {"kernel": kern, "bound": "alu", "achieved": tfs, "peak": FP32_VECTOR_PEAK_TFS, "unit": "TFLOP/s",
-                "frac": tfs / FP32_VECTOR_PEAK_TFS, "traffic": None, "avg_ms": kt["avg_ms"],
-                "algorithmic_flops_per_launch": flops, "algorithmic_bytes_per_launch": per_launch,
-                "hbm_GBps_algorithmic": gbs, "hbm_frac_algorithmic": gbs / HBM_PEAK_GBS}
-    if kern in ("gemm_dw", "gemm_dx"):
-        M, D, N, dm = w.M, w.D, w.N, w.d_model
-        if kern == "gemm_dw":
-            flops = 2 * M * D * (D + 2 * N) + 2 * M * dm * 2 * D
-        else:
-            flops = 2 * M * (D + 2 * N) * D
-        per_launch = flops / kt["launches_per_step"]
-        ach = per_launch / (kt["avg_ms"] * 1e-3) / 1e12
-        return {"kernel": kern, "bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
-                "frac": ach / MFMA_BF16_PEAK_TFS, "traffic": None, "avg_ms": kt["avg_ms"],
-                "algorithmic_flops_per_launch": per_launch}
-    return None
+    out = {}
+    for kern in ("grad_fused", "grad_fused_trunc"):
+        if kern not in kt:
+            continue
+        avg = kt[kern]["avg_ms"] * 1e-3
+        bpt = scan_bytes_per_token(w.D, w.N, s, w.proj)
+        per_launch = bpt * w.M
+        gbs = per_launch / avg / 1e9
+        flops = scan_flops_per_state_step(kern.endswith("trunc")) * w.M * w.D * w.N
+        e = {"kernel": kern, "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+             "frac": gbs / HBM_PEAK_GBS, "traffic": measured_traffic(kern, tag) if tag else None,
+             "avg_ms": kt[kern]["avg_ms"], "bytes_per_token": bpt, "tokens_per_launch": w.M,
+             "algorithmic_bytes_per_launch": per_launch,
+             "valu_TFLOPs": flops / avg / 1e12, "valu_frac": flops / avg / 1e12 / FP32_VECTOR_PEAK_TFS}
+        if layer:
+            lb = layer_scan_bytes_per_token(w.D, w.N, s)
+            e["layer_path_bytes_per_token"] = lb
+            e["layer_path_frac"] = lb * w.M / avg / 1e9 / HBM_PEAK_GBS
+        out[kern] = e
+    if layer:
+        fdw, fdx = layer_gemm_flops(w.M, w.D, w.N, w.d_model)
+        for kern, f in (("gemm_dw", fdw), ("gemm_dx", fdx)):
+            if kern not in kt:
+                continue
+            avg = kt[kern]["avg_ms"] * 1e-3
+            ach = f / avg / 1e12
+            out[kern] = {"kernel": kern, "bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFS,
+                         "unit": "TFLOP/s", "frac": ach / MFMA_BF16_PEAK_TFS,
+                         "traffic": measured_traffic(kern, tag) if tag else None, "avg_ms": kt[kern]["avg_ms"],
+                         "algorithmic_flops_per_launch": f}
+    return out
 
 
-def cpu_baseline(w, T_sample=256):
-    """The fp64 oracle (layer gradient incl. projections) on the first T_sample
-    tokens of every batch row of the workload, all channels."""
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, T_all=8192, T_one=1024, ch_one=512):
+    """The fp64 oracle as it stands, on the host cores, on bounded samples of the
+    headline workload (the first tokens of its sequence, its layer shape):
+      * all cores: the layer's full gradient (BPTT scan + projection products)
+        and its truncated gradient (tail-form scan, window w.tbar + projections)
+        on T_all tokens, all channels; ``value`` combines the two like the GPU's;
+      * one core: the full and the truncated scan gradient (no projections) on
+        T_all tokens of ch_one channels (channels are independent in the scan;
+        the rate is scaled to all channels and labelled so), and the full layer
+        gradient on T_one tokens."""
     import numpy as np
+    from threadpoolctl import threadpool_limits
 
     import oracle
     from paper_2501_00692_amd.synth import make_inputs
 
-    ws = w.with_(T=T_sample)
+    ws = w.with_(T=T_all)
     inp = make_inputs(ws, device="cpu")
     h = {k: v.float().double().numpy() for k, v in inp.items()}
+    del inp
     nthreads = oracle.max_threads()
+    args = (h["u"], h["x"], h["z"], h["delta"], h["B"], h["C"], h["W_x"], h["A_log"], h["dy"])
     t0 = time.perf_counter()
-    if w.proj:
-        oracle.layer_grad(h["u"], h["x"], h["z"], h["delta"], h["B"], h["C"], h["W_x"], h["A_log"], h["dy"],
-                          tbar=w.tbar, scan=oracle.trunc_tail if w.tbar else None)
-    else:
-        oracle.trunc_tail(h["x"], h["delta"], h["A_log"], h["B"], h["C"], h["dy"], tbar=w.tbar)
-    dt = time.perf_counter() - t0
-    del np
-    return {"value": ws.b * T_sample / dt, "unit": "tokens/s", "cores": nthreads, "kind": "oracle",
-            "sample": f"fp64 oracle layer gradient (BPTT scan + projection chain) on b={ws.b} x T={T_sample} "
-                      f"tokens of the {w.name} workload, all {w.D} channels; {dt:.2f} s wall on {nthreads} "
-                      f"OpenMP threads (numpy BLAS for the projection products)"}
+    oracle.layer_grad(*args)
+    t1 = time.perf_counter()
+    oracle.layer_grad(*args, tbar=w.tbar, scan=oracle.trunc_tail)
+    t2 = time.perf_counter()
+    full_all, trunc_all = t1 - t0, t2 - t1
+    legs = {"layer_full_all_cores": {"tokens_per_s": T_all / full_all, "s": full_all, "tokens": T_all},
+            "layer_trunc_all_cores": {"tokens_per_s": T_all / trunc_all, "s": trunc_all, "tokens": T_all,
+                                      "tbar": w.tbar}}
+    with threadpool_limits(limits=1):
+        sl = {k: np.ascontiguousarray(h[k][..., :ch_one]) for k in ("x", "delta", "dy", "z")}
+        A = np.ascontiguousarray(h["A_log"][:ch_one])
+        kw = dict(z=sl["z"], delta_softplus=True, nthreads=1)
+        t0 = time.perf_counter()
+        oracle.bptt(sl["x"], sl["delta"], A, h["B"], h["C"], sl["dy"], want_dh0=False, **kw)
+        t1 = time.perf_counter()
+        oracle.trunc_tail(sl["x"], sl["delta"], A, h["B"], h["C"], sl["dy"], tbar=w.tbar, **kw)
+        t2 = time.perf_counter()
+        scale = ch_one / w.D
+        legs["scan_full_1core"] = {"tokens_per_s": T_all / (t1 - t0) * scale, "s": t1 - t0,
+                                   "sample": f"{T_all} tokens x {ch_one} of {w.D} channels, rate scaled to "
+                                             f"all channels (extrapolated)"}
+        legs["scan_trunc_1core"] = {"tokens_per_s": T_all / (t2 - t1) * scale, "s": t2 - t1, "tbar": w.tbar,
+                                    "sample": f"{T_all} tokens x {ch_one} of {w.D} channels, rate scaled to "
+                                              f"all channels (extrapolated)"}
+        one = {k: np.ascontiguousarray(v[:, :T_one]) if v.ndim == 3 else v for k, v in h.items()}
+        t0 = time.perf_counter()
+        oracle.layer_grad(one["u"], one["x"], one["z"], one["delta"], one["B"], one["C"], one["W_x"],
+                          one["A_log"], one["dy"])
+        t1 = time.perf_counter()
+        legs["layer_full_1core"] = {"tokens_per_s": T_one / (t1 - t0), "s": t1 - t0, "tokens": T_one}
+    oracle.max_threads()  # (the OpenMP team size is set per call; later calls pass their own)
+    value = 2 * T_all / (full_all + trunc_all)
+    return {"value": value, "unit": "tokens/s", "cores": nthreads, "kind": "oracle",
+            "sample": f"fp64 oracle, layer gradient of the {w.name} workload's shape (D={w.D}, d_model={w.d_model}) "
+                      f"on its first {T_all} tokens: one full (BPTT scan + projection products) and one "
+                      f"truncated (tail-form scan, tbar={w.tbar}) call, {full_all:.1f} s + {trunc_all:.1f} s on "
+                      f"{nthreads} OpenMP threads (numpy BLAS for the projection products); value = 2 x "
+                      f"{T_all} tokens / total",
+            "cpu_model": _cpu_model(), "nproc": os.cpu_count(), "legs": legs}
 
 
 def main():
@@ -310,7 +360,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-tokens", type=int, default=4096)
+    ap.add_argument("--workload", default=HEADLINE, help="workload of the timed step (default: slice)")
     ap.add_argument("--copy-calib", action="store_true",
                     help="first run a plain 256 MiB device copy (torch copy_) three times, as the known-size "
                          "reference for HBM traffic counters")
@@ -333,75 +383,76 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    w = WORKLOADS["layer"]
+    w = WORKLOADS[args.workload]
+    tbar = w.tbar
     inp = make_inputs(w, device="cuda")
-    step = layer_step(w, inp, ssm, torch, tbar=0)
-    ms = _timed(step, args.steps, args.warmup, torch)
-    # the same step captured in a HIP graph and replayed, reported beside it (the
-    # gaps between dependent kernels are on the GPU side: replay gains nothing)
-    ms_graph = _timed_graph(step, args.steps, args.warmup, torch)
-    # per-rep spread, warm and with the L2 and MALL flushed before every rep
-    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
-    spread_warm = _timed_each(step, 20, 3, torch)
-    spread_cold = _timed_each(step, 20, 3, torch, flush=lambda: scratch.fill_(1))
-    del scratch
-    ktimes = _kernel_times(step, args.steps, ssm, torch)
-    dom = max(ktimes, key=lambda k: ktimes[k]["total_ms"])
-    roof = roofline_for(dom, ktimes, w, "layer")
-    if roof is not None:
-        roof["traffic"] = measured_traffic(dom, "layer-b2-T4096-D1536")
-    value = w.M / (ms * 1e-3)
+    desc = ssm.make_desc(inp["x"], w.N, True, True, 0, False, False)
+    ws = torch.empty(max(ssm.layer_workspace_size(desc, 0, w.d_model), ssm.layer_workspace_size(desc, tbar, w.d_model)),
+                     dtype=torch.uint8, device="cuda")
+    full = layer_step(w, inp, ssm, torch, tbar=0, ws=ws)
+    trunc = layer_step(w, inp, ssm, torch, tbar=tbar, ws=ws)
 
-    other = {k: roofline_for(k, ktimes, w, "layer") for k in ("grad_fused", "gemm_dw", "gemm_dx")
-             if k in ktimes and k != dom}
-    for k, r in other.items():
-        r["traffic"] = measured_traffic(k, "layer-b2-T4096-D1536")
-    extra = {"ms_per_step_graph_replay": ms_graph, "ms_per_step_warm": spread_warm,
-             "ms_per_step_cold": spread_cold, "kernels_layer": ktimes,
-             "roofline_other": other,
-             "gemm_tflops_layer": layer_gemm_flops(w.M, w.D, w.N, w.d_model) / 1e12}
-    del inp, step
+    def step():
+        full()
+        trunc()
+
+    print(f"bench: {w.name} workload, warmup", file=sys.stderr, flush=True)
+    ms, ktimes = _timed_kernels(step, args.steps, args.warmup, ssm, torch)
+    print(f"bench: {w.name} timed {args.steps} steps, {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    ms_plain = _timed(step, args.steps, 1, torch)
+    ms_full = _timed(full, args.steps, 1, torch)
+    ms_trunc = _timed(trunc, args.steps, 1, torch)
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    reps = 10
+    spread_warm = _timed_each(step, reps, 1, torch)
+    spread_cold = _timed_each(step, reps, 1, torch, flush=lambda: scratch.fill_(1))
+    del scratch
+    tag = workload_tag(w)
+    roofs = rooflines(ktimes, w, True, tag)
+    dom = max(roofs, key=lambda k: ktimes[k]["ms_per_step"])
+    value = 2 * w.M / (ms * 1e-3)
+    modes = {"full": {"ms": ms_full, "tokens_per_s": w.M / (ms_full * 1e-3)},
+             "truncated": {"ms": ms_trunc, "tokens_per_s": w.M / (ms_trunc * 1e-3), "tbar": tbar}}
+    extra = {"ms_per_step_without_kernel_events": ms_plain, "ms_per_step_warm": spread_warm,
+             "ms_per_step_cold": spread_cold, "kernels": ktimes,
+             "roofline_other": {k: v for k, v in roofs.items() if k != dom}}
+    del inp, full, trunc, ws
     torch.cuda.empty_cache()
 
     if not args.no_extra:
-        # (workload, kind, tbar, variant); variant "scalarA+deltaB" is the scalar-decay SSM of
-        # Table 1 with the step-size-scaled input
-        runs = [("small", "scan", 0, ""), ("small", "scan", 32, ""), ("long", "layer", 2048, ""),
-                ("long", "scan", 2048, ""), ("long_slow", "scan", 2048, ""), ("slice", "layer", 0, ""),
-                ("slice", "layer", 4096, ""), ("vlong", "scan", 8192, ""),
-                ("layer", "layer", 0, "scalarA+deltaB"), ("long", "scan", 2048, "scalarA+deltaB"),
-                ("small", "pairs", 0, ""), ("small", "pairs", 32, ""), ("pairs", "pairs", 256, ""),
-                ("pairs", "scan", 256, "")]
+        # (workload, kind, tbar, chunk, variant); variant "scalarA+deltaB" is the scalar-decay
+        # SSM of Table 1 with the step-size-scaled input
+        runs = [("small", "scan", 0, 0, ""), ("small", "scan", 32, 0, ""), ("layer", "layer", 0, 0, ""),
+                ("long", "layer", 2048, 256, ""), ("long", "layer", 2048, 0, ""), ("long", "scan", 2048, 0, ""),
+                ("long_slow", "scan", 2048, 0, ""), ("vlong", "scan", 8192, 0, ""),
+                ("layer", "layer", 0, 0, "scalarA+deltaB"), ("long", "scan", 2048, 0, "scalarA+deltaB"),
+                ("small", "pairs", 0, 0, ""), ("small", "pairs", 32, 0, ""), ("pairs", "pairs", 256, 0, ""),
+                ("pairs", "scan", 256, 0, "")]
         res = {}
-        for name, kind, tbar, variant in runs:
+        for name, kind, tb, chunk, variant in runs:
             wl = WORKLOADS[name]
+            print(f"bench: extra {name}/{kind}/tbar={tb}/chunk={chunk} {variant}", file=sys.stderr, flush=True)
             x = make_inputs(wl, device="cuda")
             if variant:
                 x["A_log"] = x["A_log"][:, 0].contiguous()
             if kind == "layer":
-                st = layer_step(wl, x, ssm, torch, tbar=tbar, b_delta=bool(variant))
+                st = layer_step(wl, x, ssm, torch, tbar=tb, b_delta=bool(variant), chunk=chunk)
             else:
-                st = scan_step(wl, x, ssm, torch, tbar=tbar, b_delta=bool(variant), pairs=kind == "pairs")
+                st = scan_step(wl, x, ssm, torch, tbar=tb, b_delta=bool(variant), pairs=kind == "pairs",
+                               chunk=chunk)
             steps = 5 if wl.M >= 262144 else 10
-            m = _timed(st, steps, 2, torch)
-            kt = _kernel_times(st, 2, ssm, torch)
-            entry = {"ms_per_step": m, "tokens_per_s": wl.M / (m * 1e-3), "tbar": tbar,
-                     "grad_fused_avg_ms": kt.get("grad_fused", {}).get("avg_ms")}
+            m, kt = _timed_kernels(st, steps, 2, ssm, torch)
+            entry = {"ms_per_step": m, "tokens_per_s": wl.M / (m * 1e-3), "tbar": tb, "chunk": chunk or "default",
+                     "kernels_ms": {k: v["avg_ms"] for k, v in kt.items()}}
             if kind == "pairs":
                 # the paper's unit of work: one (t, i) adjoint state over all D x N states
-                entry["vjp_pairs_per_s"] = wl.b * vjp_pairs(wl.T, tbar) / (m * 1e-3)
-                entry["pairs_kernel_avg_ms"] = kt.get("pairs", {}).get("avg_ms")
-            r = None if (variant or kind == "pairs") else roofline_for("grad_fused", kt, wl, (kind, tbar))
-            if r:
-                entry["grad_fused_TFLOPs"] = r["achieved"]
-                entry["grad_fused_alu_frac"] = r["frac"]
-                entry["grad_fused_GBps"] = r["hbm_GBps_algorithmic"]
-                entry["grad_fused_hbm_frac"] = r["hbm_frac_algorithmic"]
-            for g in ("gemm_dw", "gemm_dx"):
-                if g in kt:
-                    rg = roofline_for(g, kt, wl, kind)
-                    entry[f"{g}_TFLOPs"] = rg["achieved"]
-            res[f"{name}/{kind}/tbar={tbar}" + (f"/{variant}" if variant else "")] = entry
+                entry["vjp_pairs_per_s"] = wl.b * vjp_pairs(wl.T, tb) / (m * 1e-3)
+            elif not variant:
+                for k, r in rooflines(kt, wl, kind == "layer").items():
+                    entry[f"{k}_frac"] = r["frac"]
+                    entry[f"{k}_{r['unit'].replace('/', 'per')}"] = r["achieved"]
+            res[f"{name}/{kind}/tbar={tb}" + (f"/chunk={chunk}" if chunk else "") +
+                (f"/{variant}" if variant else "")] = entry
             del x, st
             torch.cuda.empty_cache()
         # the forward alone (y only), reported beside the gradients
@@ -446,17 +497,20 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "fp32",
+        "dtype": "bf16-in/fp32-acc",
         "data": "synthetic",
-        "config": {"workload": "layer: one selective diagonal SSM layer with input projections and SiLU gate, "
-                               "b=2, T=4096, d_model=768, D=1536, N=16, full adjoint gradient; each step one "
-                               "ssm_layer_grad call",
+        "config": {"workload": f"{w.name}: one selective diagonal SSM layer with input projections and SiLU gate, "
+                               f"b={w.b}, T={w.T}, d_model={w.d_model}, D={w.D}, N={w.N}; each step one full and one "
+                               f"truncated (tbar={tbar}) ssm_layer_grad call on the same batch",
                    "batch": w.b, "seq_len": w.T, "d_model": w.d_model, "channels": w.D, "dstate": w.N,
-                   "inputs": "bf16", "accumulate": "fp32", "chunk": 128},
-        "roofline": roof,
+                   "tbar": tbar, "inputs": "bf16", "accumulate": "fp32", "chunk": "default (128)",
+                   "tokens_per_step": 2 * w.M},
+        "modes": modes,
+        "roofline": roofs[dom],
     }
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(w, args.cpu_tokens)
+        print("bench: cpu baseline", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(w)
     line["extra"] = extra
     print(json.dumps(line), flush=True)
 

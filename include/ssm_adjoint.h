@@ -122,8 +122,10 @@ ssm_status ssm_adjoint_forward(const ssm_desc* desc, const void* x, const void* 
  *   dB, dC [b][T][N]  (dC is never truncated)
  *   dz     [b][T][D]  required iff SSM_GATE_SILU, else must be NULL
  *   dh0    [b][D][N]  dL/dh0, full mode only (must be NULL when truncating), or NULL.
- * Truncation reuses the full adjoint: mubar_i = mu_i - P(i, i+tbar) mu_{i+tbar}
- * with P(i, j) = prod_{k=i+1}^{j} a_k. */
+ * The truncated A- and B-path terms use the windowed adjoint
+ * mubar_i = sum_{t=i}^{min(T-1, i+tbar-1)} g_t C_t P(i, t), P(i, j) = prod_{k=i+1}^{j} a_k,
+ * computed by its own reverse recurrence mubar_i = g_i C_i + a_{i+1} mubar_{i+1}
+ * - P(i, i+tbar) g_{i+tbar} C_{i+tbar}. */
 ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
                             const void* delta, const float* A_log, const void* B, const void* C,
                             const float* h0, const void* z, const void* dy, float* dx,

@@ -720,12 +720,17 @@ __device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMI
 //      from the chunk's reverse carry M_c, and apply the vjp epilogue:
 //        s = mubar a_t h_{t-1};  ddelta = sum_n s wn;  dA_log += s Delta wn;
 //        dx = sum_n mubar B_t;  dB_t[n] += mubar x_t (over channels).
-//      Truncated mode: mubar_t = mu_t - nu_t with the tail nu_t = P(t, t+tbar)
-//      mu_{t+tbar}, which obeys nu_t = a_{t+1} nu_{t+1} + P(t, t+tbar) g_{t+tbar}
-//      C_{t+tbar} (the same decay as mu, so no second exponential per step); it
-//      starts at the chunk's last step from the adjoint carry of the chunk holding
-//      the shifted position, swept back to it; P(t, t+tbar) = 2^{cn W_t} with the
-//      window sum W_t = sum_{j=t+1}^{t+tbar} Delta_j kept in fp64.
+//      Truncated mode: the windowed adjoint mubar_t = sum_{s=t}^{t+tbar-1} g_s C_s
+//      P(t, s) obeys its own recurrence, mubar_t = g_t C_t + a_{t+1} mubar_{t+1}
+//      - P(t, t+tbar) g_{t+tbar} C_{t+tbar} (the step that leaves the window is
+//      taken out as it leaves), so it is carried at its own magnitude and never
+//      formed as the difference of two full-horizon adjoints.  Its value entering
+//      the chunk from the right, a_{e+1} mubar_{e+1}, is summed directly over the
+//      steps (e, e+tbar] when the window is shorter than the chunk; longer windows
+//      take M_c - P(e, e+tbar) a_{e+tbar+1} mu_{e+tbar+1}, with the full adjoint
+//      carry at the shifted position (that of the chunk holding it, swept back to
+//      it); P(t, t+tbar) = 2^{cn W_t} with the window sum W_t = sum_{j=t+1}^{t+tbar}
+//      Delta_j kept in fp64.
 // Per-channel quantities (softplus, the gate) are computed once per step: lane
 // r of a quad prepares steps r, r+4, ... of the segment, DPP-broadcasts them,
 // keeps that step's per-channel outputs and stores them after the segment; the
@@ -871,22 +876,34 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
         for (int k = 0; k < 4; ++k) Mp[k] = ldm(p.mbuf, cb + k * p.D, nv[k]);
         float dA[4] = {0.f, 0.f, 0.f, 0.f};
 
-        // truncated-mode state: the adjoint carry at the shifted position (the start
-        // of the tail below) and the window sum
+        // truncated-mode state: the swept adjoint carry and the window sum
         float Msh[4] = {0.f, 0.f, 0.f, 0.f};
         double W = 0.0;
         if constexpr (TRUNC) {
             const TI* Cp = static_cast<const TI*>(p.C);
             const int64_t tb = p.tbar;
-            const int64_t pstart = t0 + L - 1 + tb;
+            const int64_t e = t0 + L - 1;  // the chunk's last step
+            const int64_t pstart = e + tb;
             const int64_t pb = bb * (p.nc + 1) * p.D + d;
-            if (pstart < p.T) {
-                const int64_t cpk = pstart / L;
-                const int64_t cpend = (cpk + 1) * L - 1;
+            // Windows shorter than the chunk: the carry a_{e+1} mubar_{e+1} = sum over
+            // s in (e, e+tbar] of g_s C_s P(e, s) is summed directly over those steps
+            // from zero (no difference of full-horizon adjoints at all).  Longer
+            // windows: the full adjoint carry of the chunk holding e+tbar, swept back
+            // to it, is subtracted from the chunk's own carry below.
+            const bool direct = tb < L;
+            int64_t cpk = 0, sw_hi = e, sw_lo = e;  // the sweep covers steps (sw_lo, sw_hi]
+            if (direct) {
+                sw_hi = pstart;
+            } else if (pstart < p.T) {
+                cpk = pstart / L;
+                sw_hi = (cpk + 1) * L - 1;
+                sw_lo = pstart;
                 const int64_t mb = ((bb * p.nc + cpk) * p.N + r * 4) * p.D + d;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) Msh[k] = ldm(p.mbuf, mb + k * p.D, nv[k]);
-                // steps cpend down to pstart + 1, eight at a time: the loads of a batch
+            }
+            {
+                // steps sw_hi down to sw_lo + 1, eight at a time: the loads of a batch
                 // (from clamped, always valid addresses) are issued before its
                 // arithmetic, and steps outside the sweep are masked to exact no-ops
                 // (Delta = g = C = 0 leave Msh and the Delta sum unchanged) with bit
@@ -897,7 +914,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 const TI* Z = static_cast<const TI*>(p.z);
                 constexpr int PB = 8;
                 double pre = 0.0;
-                for (int64_t p0 = cpend; p0 > pstart; p0 -= PB) {
+                for (int64_t p0 = sw_hi; p0 > sw_lo; p0 -= PB) {
                     typename RawIn<TI, PB>::Bits prb[PB], gyb[PB], zb[PB];
                     uint32_t mk[PB];
                     // raw C bits: 4 bf16 (two words) or 4 fp32 words per step
@@ -906,7 +923,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
 #pragma unroll
                     for (int u = 0; u < PB; ++u) {
                         const int64_t ps = p0 - u;
-                        const bool ok = dv && ps > pstart && ps < p.T;
+                        const bool ok = dv && ps > sw_lo && ps < p.T;
                         mk[u] = ok ? 0xffffffffu : 0u;
                         const int64_t row = bb * p.T + min(max<int64_t>(ps, 0), p.T - 1);
                         const int64_t td = row * p.D + (dv ? d : 0);
@@ -960,20 +977,25 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                         pre += static_cast<double>(dlp);
                     }
                 }
-                if (dv)
-                    W = (p.psum[pb + cpk * p.D] - p.psum[pb + (c + 1) * p.D]) +
-                        (p.sdel[(bb * p.nc + cpk) * p.D + d] - pre);
-            } else if (dv) {
-                W = p.psum[pb + p.nc * p.D] - p.psum[pb + (c + 1) * p.D];
+                if (direct) {
+                    W = pre;  // the window's Delta sum, steps past T counting 0
+                } else if (dv) {
+                    W = pstart < p.T ? (p.psum[pb + cpk * p.D] - p.psum[pb + (c + 1) * p.D]) +
+                                           (p.sdel[(bb * p.nc + cpk) * p.D + d] - pre)
+                                     : p.psum[pb + p.nc * p.D] - p.psum[pb + (c + 1) * p.D];
+                }
             }
-        }
-        // the subtracted tail nu_t = P(t, t+tbar) mu_{t+tbar}, carried as a_{t+1} nu_{t+1};
-        // at the chunk's last step e: P(e, e+tbar) (a_{e+tbar+1} mu_{e+tbar+1})
-        float Np[4] = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (TRUNC) {
-            const float wf0 = static_cast<float>(W);
+            if (direct) {
 #pragma unroll
-            for (int k = 0; k < 4; ++k) Np[k] = fexp2(cn[k] * wf0) * Msh[k];
+                for (int k = 0; k < 4; ++k) Mp[k] = Msh[k];
+            } else {
+                // a_{e+1} mubar_{e+1} = a_{e+1} mu_{e+1} - P(e, e+tbar) (a_{e+tbar+1} mu_{e+tbar+1}):
+                // one difference of full-horizon adjoints per tile, whose rounding then
+                // decays; with windows of a chunk or more the two are of comparable size
+                const float wf0 = static_cast<float>(W);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) Mp[k] = fmaf(-fexp2(cn[k] * wf0), Msh[k], Mp[k]);
+            }
         }
 
 #pragma unroll 1
@@ -1089,6 +1111,10 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             float dxk[SPL], ddk[SPL];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) dxk[jj] = ddk[jj] = 0.f;
+            // the segment's dA_log terms are summed on their own and then added to
+            // the tile's sum: the rounding of the sequential sum grows with S + L/S
+            // terms instead of L
+            float dAs[4] = {0.f, 0.f, 0.f, 0.f};
             bc.get(q * S + S - 1, r, Bn, Cn);
 #pragma unroll
             for (int j = S - 1; j >= 0; --j) {
@@ -1100,12 +1126,9 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     Cv[k] = Cn[k];
                 }
                 if (j > 0) bc.get(tl - 1, r, Bn, Cn);
-                float mu[4], mb[4];
+                float mb[4];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    mu[k] = fmaf(gh[j], Cv[k], Mp[k]);
-                    mb[k] = mu[k];
-                }
+                for (int k = 0; k < 4; ++k) mb[k] = fmaf(gh[j], Cv[k], Mp[k]);
                 if constexpr (TRUNC) {
                     const int64_t ps = t0 + tl + p.tbar;
                     const bool pv = ps < p.T;
@@ -1120,12 +1143,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     }
                     const float wf = static_cast<float>(W);
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        // nu_t = a_{t+1} nu_{t+1} + P(t, t+tbar) g_{t+tbar} C_{t+tbar}
-                        const float nu = fmaf(fexp2(cn[k] * wf), gp * Cs[k], Np[k]);
-                        mb[k] = mu[k] - nu;
-                        Np[k] = ah[j][k] * nu;
-                    }
+                    for (int k = 0; k < 4; ++k)  // the step t+tbar leaves the window
+                        mb[k] = fmaf(-fexp2(cn[k] * wf), gp * Cs[k], mb[k]);
                     W += static_cast<double>(dlh[j]) - static_cast<double>(dlp);
                 }
                 float dxp = 0.f, ddp = 0.f;
@@ -1134,9 +1153,9 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     dxp = fmaf(mb[k], Bv[k], dxp);
                     const float s = mb[k] * ahp[j][k];
                     ddp = fmaf(s, wn[k], ddp);
-                    dA[k] = fmaf(s, dlh[j], dA[k]);
+                    dAs[k] = fmaf(s, dlh[j], dAs[k]);
                     red[wave][j][r * 4 + k][chs] = mb[k] * xh[j];
-                    Mp[k] = ah[j][k] * mu[k];
+                    Mp[k] = ah[j][k] * mb[k];
                 }
                 const float dxv = quad_sum(dxp);
                 const float ddv = quad_sum(ddp);
@@ -1157,6 +1176,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 if constexpr (OUT != 2) *(sv[jj] ? ddo + off : sinkf) = ddv;
                 if constexpr (OUT16) stf(sv[jj] ? dd16o + (tl * ldd16 + d32) : sink16, 0, ddv);
             }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) dA[k] += dAs[k];
             wave_sums(2 * pair + 1);  // dB
             flush(q);
         }
@@ -1329,7 +1350,7 @@ template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK>
 void grad_main(const ScanProblem& p, hipStream_t s) {
     dim3 g(static_cast<unsigned>(p.nsplit), static_cast<unsigned>(p.nc),
            static_cast<unsigned>(p.nb));
-    SSMK_TIMED("grad_fused", s);
+    SSMK_TIMED(TRUNC ? "grad_fused_trunc" : "grad_fused", s);
     // the bf16 copies exist for the whole-layer path (bf16 inputs, softplus, gate)
     if constexpr (sizeof(TI) == 2 && SP && GATE) {
         if (p.dd16 && p.only16) {

@@ -16,3 +16,20 @@ def pytest_configure(config):
 def rng():
     import numpy as np
     return np.random.default_rng(20250100692)
+
+
+def pytest_sessionfinish(session, exitstatus):
+    """Write every parity check's rel-L2 (test, output, error, tolerance) as JSON
+    lines into the file named by SSM_PARITY_RECORD, if set."""
+    path = os.environ.get("SSM_PARITY_RECORD")
+    if not path:
+        return
+    try:
+        from gpu_helpers import RECORD
+    except ImportError:
+        return
+    import json
+    os.makedirs(os.path.dirname(os.path.abspath(path)), exist_ok=True)
+    with open(path, "w") as f:
+        for test, name, err, tol in RECORD:
+            f.write(json.dumps({"test": test, "output": name, "rel_l2": err, "tol": tol}) + "\n")

@@ -11,7 +11,7 @@ import oracle
 import paper_2501_00692_amd as ssm
 from paper_2501_00692_amd.synth import WORKLOADS, Workload, make_inputs
 
-from gpu_helpers import TOL_BF16, TOL_F32, check, say, to_np
+from gpu_helpers import TOL_BF16, TOL_F32, TOL_SCAN_BF16, check, say, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -80,8 +80,9 @@ def test_forward_gate_bf16(chunk):
     torch.cuda.synchronize()
     ry, rh = oracle.forward(*(to_np(inp[k]) for k in ("x", "delta", "A_log", "B", "C")), h0=to_np(inp["h0"]),
                             z=to_np(inp["z"]), delta_softplus=True)
-    check("y", to_np(y), ry, TOL_BF16)
-    check("h_last", to_np(hl), rh, TOL_F32)
+    # y is stored in bf16 (one rounding, 2^-9 relative): held to half of that
+    check("y", to_np(y), ry, 2e-3)
+    check("h_last", to_np(hl), rh, TOL_SCAN_BF16)
 
 
 @pytest.mark.parametrize("chunk", [16, 64, 128, 256])
@@ -114,6 +115,62 @@ def test_grad_slow_decay_truncated(tbar, chunk):
     if 1 < tbar <= w.T // 4:
         full = _oracle_grad(inp, w, 0)
         assert np.linalg.norm(ref["dx"] - full["dx"]) > 1e-3 * np.linalg.norm(full["dx"])  # window visible
+
+
+# Chunks of 256 steps (16-step segments) over several chunks, with windows below,
+# at and above one chunk: the shifted C rows of a segment come from the next
+# chunks, and windows that are not a multiple of the chunk sweep the adjoint
+# carry back from the end of the chunk holding t + tbar.  Slow decay (Delta / 512:
+# horizons of up to about 1,300 steps) keeps the window visible at every tbar.
+SLOW1K = Workload("slow1k", 1, 1000, 64, 16, 64, 0, False, False, 692120, delta_scale=1.0 / 512)
+
+
+@pytest.mark.parametrize("tbar", [37, 255, 256, 300, 512, 700])
+def test_grad_chunk256_truncated_multichunk(tbar):
+    w = SLOW1K
+    say(f"[grad trunc chunk 256] T={w.T} D={w.D} tbar={tbar}")
+    inp = _inputs(w)
+    g = _gpu_grad(inp, w, tbar, 256)
+    ref = _oracle_grad(inp, w, tbar, literal=True)
+    _compare(g, ref, TOL_F32, False)
+    full = _oracle_grad(inp, w, 0)
+    assert np.linalg.norm(ref["dx"] - full["dx"]) > 1e-3 * np.linalg.norm(full["dx"])  # window visible
+
+
+# the same over bf16 inputs, without and with the gate and softplus (b = 2,
+# ragged last chunk); the oracle reads the same bf16 bits
+SLOW_BF16_256 = Workload("slow_bf16_256", 2, 1800, 96, 16, 96, 0, False, True, 692121, delta_scale=1.0 / 512)
+GATE_BF16_256 = Workload("gate_bf16_256", 2, 1800, 96, 16, 96, 0, True, True, 692122)
+
+
+@pytest.mark.parametrize("tbar", [0, 200, 256, 600])
+@pytest.mark.parametrize("w", [SLOW_BF16_256, GATE_BF16_256], ids=["slow", "gate"])
+def test_grad_bf16_chunk256(w, tbar):
+    say(f"[grad bf16 chunk 256] {w.name} T={w.T} D={w.D} tbar={tbar}")
+    inp = _inputs(w)
+    g = _gpu_grad(inp, w, tbar, 256)
+    _compare(g, _oracle_grad(inp, w, tbar), TOL_SCAN_BF16, w.proj)
+
+
+# fp32, long sequence, slow decay (Delta / 2048: horizons of 150 to 2,500 steps)
+# and a short window: the full adjoint is several times larger than the windowed
+# one, so any formation of the windowed adjoint as a difference of full-horizon
+# fp32 sums would lose the tolerance.
+SLOW8K = Workload("slow8k", 1, 8192, 64, 16, 64, 32, False, False, 692123, delta_scale=1.0 / 2048)
+
+
+@pytest.mark.parametrize("chunk", [128, 256])
+def test_grad_fp32_long_slow_short_window(chunk):
+    w = SLOW8K
+    say(f"[grad trunc fp32 long slow] T={w.T} D={w.D} tbar={w.tbar} chunk={chunk}")
+    inp = _inputs(w)
+    g = _gpu_grad(inp, w, w.tbar, chunk)
+    ref = _oracle_grad(inp, w, w.tbar, literal=True)
+    _compare(g, ref, TOL_F32, False)
+    full = _oracle_grad(inp, w, 0)
+    ratio = np.linalg.norm(full["dx"]) / np.linalg.norm(ref["dx"])
+    say(f"   |full dx| / |truncated dx| = {ratio:.2f}")
+    assert ratio > 2.0
 
 
 RAGGED = Workload("ragged", 2, 250, 50, 5, 50, 0, False, False, 692100, delta_scale=0.25)
@@ -157,7 +214,7 @@ def test_grad_bf16_gate(tbar):
     say(f"[grad bf16 gate] T={w.T} D={w.D} tbar={tbar}")
     inp = _inputs(w)
     g = _gpu_grad(inp, w, tbar, 0)
-    _compare(g, _oracle_grad(inp, w, tbar), TOL_BF16, True)
+    _compare(g, _oracle_grad(inp, w, tbar), TOL_SCAN_BF16, True)
 
 
 def test_grad_deterministic():
@@ -230,7 +287,8 @@ def test_layer_grad_small(tbar):
     M = w.b * w.T
     rep = {}
     for k in ("dx", "ddelta", "dB", "dC", "dz", "dA_log"):
-        check(k, to_np(o[k]), ref[k], TOL_BF16, rep)
+        check(k, to_np(o[k]), ref[k], TOL_SCAN_BF16, rep)
+    # downstream of the bf16 rounding of the GEMM operands
     check("dx_total", to_np(o["dx_total"]).reshape(M, -1), ref["dx_total"], TOL_BF16, rep)
     check("dW_x", to_np(o["dW_x"]), ref["dW_x"], TOL_BF16, rep)
     check("dW_in", to_np(o["dW_in"]), ref["dW_in"], TOL_BF16, rep)
