@@ -132,6 +132,25 @@ ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, co
                             float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
                             float* dh0, void* workspace, size_t workspace_bytes, void* stream);
 
+/* ssm_adjoint_grad without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Arguments, outputs, results and error
+ * behaviour are those of ssm_adjoint_grad (the same kernels, bit-identical
+ * outputs); the scratch is a 64 MiB device array inside the library, one per
+ * GPU, held from the first call on that GPU until the process ends.  The call
+ * allocates nothing.  It returns SSM_ERR_WORKSPACE, before anything is
+ * enqueued, when the problem needs more scratch than that (the workspace size
+ * that ssm_adjoint_grad_workspace_size reports for the same arguments is what
+ * it needs).  Every call on one GPU uses that GPU's single array: calls that
+ * can overlap on one GPU (different streams, or host threads) race and must be
+ * serialised by the caller; calls on one stream are ordered.  No part of the
+ * scratch needs to start at zero. */
+ssm_status ssm_adjoint_grad_noalloc(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
+                                    const void* delta, const float* A_log, const void* B,
+                                    const void* C, const float* h0, const void* z, const void* dy,
+                                    float* dx, float* ddelta, float* dA_log, float* dB, float* dC,
+                                    float* dz, float* dh0, void* stream);
+
 /* The same gradient as ssm_adjoint_grad (identical arguments, layouts, outputs
  * and error behaviour), evaluated by the explicit pair formulation of Prop. 2 and
  * Eq. "capped": for every step i and every loss term t in its window

@@ -9,7 +9,8 @@ other implementation behind this module, and it raises if the library is not
 built.
 
 Entry points (names as in the C ABI): :func:`ssm_adjoint_forward`,
-:func:`ssm_adjoint_grad`, :func:`ssm_adjoint_grad_pairs`, :func:`ssm_proj_grad`,
+:func:`ssm_adjoint_grad`, :func:`ssm_adjoint_grad_noalloc`, :func:`ssm_adjoint_grad_pairs`,
+:func:`ssm_proj_grad`,
 :func:`ssm_layer_grad`, :func:`ssm_stack_grad`.
 """
 from __future__ import annotations
@@ -33,7 +34,8 @@ STATUS = {0: "SSM_OK", 1: "SSM_ERR_NULL", 2: "SSM_ERR_SHAPE", 3: "SSM_ERR_DTYPE"
 
 EXPORTED = (
     "ssm_adjoint_forward_workspace_size", "ssm_adjoint_grad_workspace_size", "ssm_adjoint_forward",
-    "ssm_adjoint_grad", "ssm_adjoint_grad_pairs_workspace_size", "ssm_adjoint_grad_pairs",
+    "ssm_adjoint_grad", "ssm_adjoint_grad_noalloc", "ssm_adjoint_grad_pairs_workspace_size",
+    "ssm_adjoint_grad_pairs",
     "ssm_proj_grad_workspace_size", "ssm_proj_grad",
     "ssm_layer_grad_workspace_size", "ssm_layer_grad", "ssm_stack_grad_workspace_size", "ssm_stack_grad",
     "ssm_timing_enable", "ssm_timing_summary",
@@ -73,6 +75,7 @@ def load_library():
         "ssm_adjoint_grad_workspace_size": [dp, i32, i64, szp],
         "ssm_adjoint_forward": [dp] + [vp] * 9 + [vp, sz, vp],
         "ssm_adjoint_grad": [dp, i32, i64] + [vp] * 15 + [vp, sz, vp],
+        "ssm_adjoint_grad_noalloc": [dp, i32, i64] + [vp] * 15 + [vp],
         "ssm_adjoint_grad_pairs_workspace_size": [dp, i32, i64, szp],
         "ssm_adjoint_grad_pairs": [dp, i32, i64] + [vp] * 15 + [vp, sz, vp],
         "ssm_proj_grad_workspace_size": [i64, i64, i64, u32, szp],
@@ -229,6 +232,16 @@ def ssm_adjoint_grad(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False,
                          b_delta)
 
 
+def ssm_adjoint_grad_noalloc(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False, tbar=0, chunk=0,
+                             want_dh0=False, out=None, b_delta=False):
+    """:func:`ssm_adjoint_grad` through the C entry point that takes no workspace
+    (its scratch is a fixed device array inside the library); arguments and
+    results as there.  Raises :class:`SsmError` with SSM_ERR_WORKSPACE when the
+    problem needs more scratch than the library holds."""
+    return _adjoint_grad(False, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk, want_dh0, out, None,
+                         b_delta, noalloc=True)
+
+
 def ssm_adjoint_grad_pairs(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False, tbar=0, chunk=0,
                            want_dh0=False, out=None, workspace=None, b_delta=False):
     """The same gradient as :func:`ssm_adjoint_grad`, evaluated by the explicit
@@ -239,7 +252,7 @@ def ssm_adjoint_grad_pairs(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=
 
 
 def _adjoint_grad(pairs, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk, want_dh0, out, workspace,
-                  b_delta):
+                  b_delta, noalloc=False):
     lib = load_library()
     dt = x.dtype
     b, T, D = x.shape
@@ -266,11 +279,15 @@ def _adjoint_grad(pairs, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk
         o.setdefault("dz", torch.empty(b, T, D, **f32))
     if want_dh0:
         o.setdefault("dh0", torch.empty(b, D, N, **f32))
+    args = (ctypes.byref(desc), mode, int(tbar), _p(x), _p(delta), _p(A_log), _p(B), _p(C), _p(h0), _p(z), _p(dy),
+            _p(o["dx"]), _p(o["ddelta"]), _p(o["dA_log"]), _p(o["dB"]), _p(o["dC"]), _p(o.get("dz")),
+            _p(o.get("dh0")))
+    if noalloc:
+        _check(lib.ssm_adjoint_grad_noalloc(*args, _stream()), "ssm_adjoint_grad_noalloc")
+        return o
     ws = workspace if workspace is not None else _workspace(grad_workspace_size(desc, tbar, pairs), dev)
     name = "ssm_adjoint_grad_pairs" if pairs else "ssm_adjoint_grad"
-    _check(getattr(lib, name)(ctypes.byref(desc), mode, int(tbar), _p(x), _p(delta), _p(A_log), _p(B), _p(C),
-                              _p(h0), _p(z), _p(dy), _p(o["dx"]), _p(o["ddelta"]), _p(o["dA_log"]), _p(o["dB"]),
-                              _p(o["dC"]), _p(o.get("dz")), _p(o.get("dh0")), _p(ws), ws.numel(), _stream()), name)
+    _check(getattr(lib, name)(*args, _p(ws), ws.numel(), _stream()), name)
     return o
 
 

@@ -269,6 +269,24 @@ static void grad_bind(ssmk::ScanProblem& p, const void* x, const void* delta, co
     p.dh0 = dh0;
 }
 
+// Launch of a validated gradient call on a workspace laid out as `w`.
+static ssm_status grad_launch(const ssm_desc* desc, int64_t L, int64_t nc, bool trunc, int64_t tbar,
+                              const void* x, const void* delta, const float* A_log, const void* B,
+                              const void* C, const float* h0, const void* z, const void* dy, float* dx,
+                              float* ddelta, float* dA_log, float* dB, float* dC, float* dz, float* dh0,
+                              void* workspace, const ssmk::ScanWorkspace& w, void* stream, const char* where) {
+    ssmk::ScanProblem p = make_problem(desc, L, nc);
+    p.trunc = trunc;
+    p.tbar = trunc ? tbar : 0;
+    ssmk::choose_split(p.nb, p.D, nc, &p.nsplit, &p.tps);
+    p.nslice = ssmk::choose_nslice(p.nb, nc);
+    grad_bind(p, x, delta, A_log, B, C, h0, z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0);
+    ssmk::bind_workspace(p, workspace, w);
+    hipError_t e = ssmk::launch_grad(p, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, where);
+    return SSM_OK;
+}
+
 ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
                             const void* delta, const float* A_log, const void* B, const void* C,
                             const float* h0, const void* z, const void* dy, float* dx,
@@ -283,16 +301,32 @@ ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, co
                                                  desc->dstate, L, true, trunc);
     st = check_workspace(workspace, workspace_bytes, w.total);
     if (st) return st;
-    ssmk::ScanProblem p = make_problem(desc, L, nc);
-    p.trunc = trunc;
-    p.tbar = trunc ? tbar : 0;
-    ssmk::choose_split(p.nb, p.D, nc, &p.nsplit, &p.tps);
-    p.nslice = ssmk::choose_nslice(p.nb, nc);
-    grad_bind(p, x, delta, A_log, B, C, h0, z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0);
-    ssmk::bind_workspace(p, workspace, w);
-    hipError_t e = ssmk::launch_grad(p, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "ssm_adjoint_grad launch");
-    return SSM_OK;
+    return grad_launch(desc, L, nc, trunc, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta, dA_log, dB,
+                       dC, dz, dh0, workspace, w, stream, "ssm_adjoint_grad launch");
+}
+
+ssm_status ssm_adjoint_grad_noalloc(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
+                                    const void* delta, const float* A_log, const void* B, const void* C,
+                                    const float* h0, const void* z, const void* dy, float* dx,
+                                    float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
+                                    float* dh0, void* stream) {
+    int64_t L, nc;
+    bool trunc;
+    ssm_status st = grad_validate(desc, mode, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta,
+                                  dA_log, dB, dC, dz, dh0, &L, &nc, &trunc);
+    if (st) return st;
+    ssmk::ScanWorkspace w = ssmk::scan_workspace(desc->batch, desc->seqlen, desc->channels,
+                                                 desc->dstate, L, true, trunc);
+    if (w.total > ssmk::kNoallocScratchBytes)
+        return fail(SSM_ERR_WORKSPACE,
+                    "this gradient needs %zu bytes of scratch; the no-allocation entry point has %zu "
+                    "(use ssm_adjoint_grad with a workspace)",
+                    w.total, ssmk::kNoallocScratchBytes);
+    void* scratch = nullptr;
+    hipError_t e = ssmk::noalloc_scratch(&scratch);
+    if (e != hipSuccess) return hip_fail(e, "ssm_adjoint_grad_noalloc scratch");
+    return grad_launch(desc, L, nc, trunc, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta, dA_log, dB,
+                       dC, dz, dh0, scratch, w, stream, "ssm_adjoint_grad_noalloc launch");
 }
 
 // Limits of the pair formulation: its channel blocks form a grid dimension, and

@@ -107,6 +107,12 @@ ScanWorkspace scan_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_
 void bind_workspace(ScanProblem& p, void* ws, const ScanWorkspace& w);
 
 hipError_t launch_forward(const ScanProblem& p, hipStream_t s);
+
+// Scratch of ssm_adjoint_grad_noalloc (noalloc.hip): a file-scope device array of
+// kNoallocScratchBytes per GPU; noalloc_scratch returns the current device's
+// address of it (looked up once per device with that device current).
+constexpr size_t kNoallocScratchBytes = size_t(64) << 20;
+hipError_t noalloc_scratch(void** ptr);
 hipError_t launch_grad(const ScanProblem& p, hipStream_t s);
 
 // Kernels of the K-layer residual stack (stack.hip).

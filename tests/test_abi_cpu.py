@@ -159,3 +159,25 @@ def test_stack_errors(lib):
     assert lib.ssm_stack_grad_workspace_size(ctypes.byref(d), 1, ssm.SSM_STACK_EXACT, ssm.SSM_FULL, 0,
                                              ctypes.byref(n)) == 0
     assert 0 < n.value < three
+
+
+def noalloc_call(lib, dsc, mode=ssm.SSM_FULL, tbar=0, x=FAKE):
+    return lib.ssm_adjoint_grad_noalloc(ctypes.byref(dsc) if dsc is not None else None, mode, tbar, x, FAKE, FAKE,
+                                        FAKE, FAKE, None, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None)
+
+
+def test_noalloc_host_errors(lib):
+    """The entry point without a workspace validates like ssm_adjoint_grad and
+    rejects problems whose scratch exceeds its fixed array, all before any HIP
+    call (these run without a GPU)."""
+    assert noalloc_call(lib, None) == 1
+    assert noalloc_call(lib, desc(batch=0)) == 2
+    assert noalloc_call(lib, desc(), x=None) == 1
+    assert noalloc_call(lib, desc(), x=MISALIGNED) == 6
+    assert noalloc_call(lib, desc(), mode=ssm.SSM_TRUNCATED, tbar=0) == 2
+    big = desc(batch=8, seqlen=65536, channels=4096, in_dtype=ssm.SSM_BF16)
+    n = ctypes.c_size_t()
+    assert lib.ssm_adjoint_grad_workspace_size(ctypes.byref(big), ssm.SSM_FULL, 0, ctypes.byref(n)) == 0
+    assert n.value > (64 << 20)
+    assert noalloc_call(lib, big) == 5
+    assert "no-allocation" in ssm.last_error()
