@@ -55,20 +55,26 @@ def scan_bytes_per_token(D, N, s, gate):
     return D * per_ch + N * (2 * s + 8)
 
 
-def layer_scan_bytes_per_token(D, N, s):
-    """Compulsory bytes per token of the scan kernel inside the whole-layer call,
-    which writes dx in fp32 (the projection GEMM's addend) and dDelta_pre, dz, dB,
-    dC as the GEMMs' bf16 operands (plus dB, dC in fp32): reads x, Delta_pre, dy,
-    z, B, C."""
-    return D * (4 * s + 4 + 2 + 2) + N * (2 * s + 8 + 4)
+def layer_scan_bytes_per_token(D, N, s, dm):
+    """Compulsory bytes per token of the scan kernel inside the whole-layer call
+    (reads x, Delta_pre, dy, z, B, C), which writes the projection GEMMs' bf16
+    operands dDelta_pre, dz, dB, dC (plus dB, dC in fp32) and dx: in bf16 when
+    d_model < D (the reassociated input-projection gradient reads it as an
+    operand), else in fp32 (the addend of dx_total)."""
+    return D * (4 * s + (2 if dm < D else 4) + 2 + 2) + N * (2 * s + 8 + 4)
 
 
 def layer_gemm_flops(M, D, N, dm):
-    """Flops of the layer's projection products: (dW_x + dW_in, the one weight-
-    gradient launch) and dx_total = dx + dZx W_x^T (the dX launch)."""
-    dw = 2 * M * D * (D + 2 * N) + 2 * M * dm * 2 * D
-    dx = 2 * M * (D + 2 * N) * D
-    return dw, dx
+    """Flops per launch of the layer's projection products, by timing name.  With
+    d_model < D the input projection's gradient is reassociated: one weight-
+    gradient launch computes dW_x = x^T dZx and G = u^T [dx | dz | dZx], and two
+    small launches add (u^T dZx) W_x^T (its bf16 hi and lo parts) into dW_in.
+    Otherwise: dx_total = dx + dZx W_x^T (the dX launch), then dW_x and dW_in =
+    u^T [dx_total | dz] in one launch."""
+    nx = D + 2 * N
+    if dm < D:
+        return {"gemm_dw": 2 * M * D * nx + 2 * M * dm * (3 * D + 2 * N), "gemm_dwin_fix": 2 * dm * nx * D}
+    return {"gemm_dw": 2 * M * D * nx + 2 * M * dm * 2 * D, "gemm_dx": 2 * M * nx * D}
 
 
 def _timed(fn, steps, warmup, torch):
@@ -261,13 +267,12 @@ def rooflines(kt, w, layer, tag=None):
              "algorithmic_bytes_per_launch": per_launch,
              "valu_TFLOPs": flops / avg / 1e12, "valu_frac": flops / avg / 1e12 / FP32_VECTOR_PEAK_TFS}
         if layer:
-            lb = layer_scan_bytes_per_token(w.D, w.N, s)
+            lb = layer_scan_bytes_per_token(w.D, w.N, s, w.d_model)
             e["layer_path_bytes_per_token"] = lb
             e["layer_path_frac"] = lb * w.M / avg / 1e9 / HBM_PEAK_GBS
         out[kern] = e
     if layer:
-        fdw, fdx = layer_gemm_flops(w.M, w.D, w.N, w.d_model)
-        for kern, f in (("gemm_dw", fdw), ("gemm_dx", fdx)):
+        for kern, f in layer_gemm_flops(w.M, w.D, w.N, w.d_model).items():
             if kern not in kt:
                 continue
             avg = kt[kern]["avg_ms"] * 1e-3

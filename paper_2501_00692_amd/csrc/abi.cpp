@@ -106,37 +106,50 @@ ssmk::ScanProblem make_problem(const ssm_desc* d, int64_t L, int64_t nc) {
     return p;
 }
 
-// Workspace of the whole-layer call: the scan workspace, then bf16 packing
-// buffers, fp32 scan outputs that the caller did not supply, and the GEMM
-// workspace.
+// Workspace of the whole-layer call: the scan workspace, then the bf16 operands
+// of the projection products, fp32 scan outputs that the caller did not supply,
+// the reassociated input-projection gradient's G and its bf16 hi/lo parts
+// (d_model < D only), and the GEMM workspace.
 struct LayerWs {
-    size_t scan_off, dzx_off, dxz_off, f32_off, gemm_off, total;
+    size_t scan_off, z_off, f32_off, g_off, hl_off, gemm_off, total;
     size_t scan_total;
 };
 
 size_t up256(size_t v) { return (v + 255) & ~size_t(255); }
 
+// The input projection's gradient is reassociated when d_model < D:
+// dW_in[:, :D] = u^T (dx + dZx W_x^T) = u^T dx + (u^T dZx) W_x^T, which replaces the
+// M x (D+2N) x D product that forms dx_total by M x d_model x (D+2N) more columns
+// of the weight-gradient launch and a d_model x (D+2N) x D product.
+bool layer_reassoc(int64_t d_model, int64_t D) { return d_model < D; }
+
 LayerWs layer_ws(const ssm_desc* d, int64_t L, bool trunc, int64_t d_model) {
     LayerWs w{};
     const int64_t M = d->batch * d->seqlen, D = d->channels, N = d->dstate;
+    const int64_t nx = D + 2 * N, nz = 3 * D + 2 * N;
+    const bool re = layer_reassoc(d_model, D);
     ssmk::ScanWorkspace sw = ssmk::scan_workspace(d->batch, d->seqlen, D, N, L, true, trunc);
     w.scan_total = sw.total;
     size_t off = 0;
     w.scan_off = off;
     off = up256(off + sw.total);
-    w.dzx_off = off;  // bf16 [M][D+2N]
-    off = up256(off + size_t(M) * (D + 2 * N) * 2);
-    w.dxz_off = off;  // bf16 [M][2D]
-    off = up256(off + size_t(M) * 2 * D * 2);
+    // bf16 [M][3D+2N]: reassociated, Z = [dx | dz | dDelta_pre | dB | dC]; otherwise
+    // dZx = [dDelta_pre | dB | dC] ([M][D+2N]) followed by [dx_total | dz] ([M][2D])
+    w.z_off = off;
+    off = up256(off + size_t(M) * nz * 2);
     w.f32_off = off;  // fp32 dx, ddelta, dz [M][D] and dB, dC [M][N]
     off = up256(off + size_t(M) * (3 * D + 2 * N) * 4);
+    w.g_off = off;  // fp32 G [d_model][3D+2N]
+    if (re) off = up256(off + size_t(d_model) * nz * 4);
+    w.hl_off = off;  // bf16 hi, lo [d_model][D+2N]
+    if (re) off = up256(off + size_t(d_model) * nx * 2 * 2);
     w.gemm_off = off;
-    // the layer's GEMM launches (dx_total, both weight gradients together, du) run
-    // one after the other and share the region
-    const ssmk::DwProduct dwx{D, D + 2 * N, nullptr, 0, nullptr, 0, nullptr, false};
-    const ssmk::DwProduct dwin{d_model, 2 * D, nullptr, 0, nullptr, 0, nullptr, false};
+    // the layer's GEMM launches run one after the other and share the region
+    const ssmk::DwProduct dwx{D, nx, nullptr, 0, nullptr, 0, nullptr, false};
+    const ssmk::DwProduct dwin{d_model, re ? nz : 2 * D, nullptr, 0, nullptr, 0, nullptr, false};
     size_t g = ssmk::gemm_dw2_workspace(M, dwx, dwin);
-    for (size_t gi : {ssmk::gemm_dx_workspace(M, D, D + 2 * N), ssmk::gemm_dx_workspace(M, d_model, 2 * D)})
+    for (size_t gi : {ssmk::gemm_dx_workspace(M, D, nx), ssmk::gemm_dx_workspace(M, d_model, 2 * D),
+                      re ? ssmk::gemm_dx_workspace(d_model, D, nx) : size_t(0)})
         g = gi > g ? gi : g;
     off = up256(off + g);
     w.total = off;
@@ -482,6 +495,10 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     if (st) return st;
     st = check_gemm_shape(M, d_model, 2 * D, d_model, 2 * D, 2 * D, du != nullptr);
     if (st) return st;
+    if (layer_reassoc(d_model, D)) {  // the shapes of G = u^T Z
+        st = check_gemm_shape(M, d_model, 3 * D + 2 * N, d_model, 3 * D + 2 * N, 0, false);
+        if (st) return st;
+    }
     REQUIRE_PTR(u, "u");
     REQUIRE_PTR(W_x, "W_x");
     REQUIRE_PTR(dW_in, "dW_in");
@@ -510,6 +527,8 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     if (st) return st;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool re = layer_reassoc(d_model, D);
+    const int64_t nx = D + 2 * N, nz = 3 * D + 2 * N;
     ssmk::ScanWorkspace sw = ssmk::scan_workspace(sd.batch, sd.seqlen, D, N, L, true, trunc);
     ssmk::ScanProblem p = make_problem(&sd, L, nc);
     p.trunc = trunc;
@@ -518,26 +537,73 @@ ssm_status ssm_layer_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, int6
     p.nslice = ssmk::choose_nslice(p.nb, nc);
     grad_bind(p, x, delta_pre, A_log, B, C, nullptr, z, dy, dx_, dd_, dA_log, dB_, dC_, dz_, nullptr);
     ssmk::bind_workspace(p, ws + w.scan_off, sw);
-    // the scan kernels also write dZx = [dDelta_pre | dB | dC] and the dz half of
-    // [dx_total | dz] in bf16
-    uint16_t* dzx = reinterpret_cast<uint16_t*>(ws + w.dzx_off);
-    uint16_t* dxz = reinterpret_cast<uint16_t*>(ws + w.dxz_off);
-    const int64_t nx = D + 2 * N;
+    uint16_t* zb = reinterpret_cast<uint16_t*>(ws + w.z_off);
+    void* gws = ws + w.gemm_off;
+    const bool need_dxt = dx_total || du;  // dx_total = dx + dZx W_x^T is formed
+    hipError_t e;
+    if (re) {
+        // the scan kernels write Z = [dx | dz | dDelta_pre | dB | dC] in bf16; fp32 dx,
+        // dDelta_pre and dz only when the caller asks for one of them or for dx_total
+        p.dx16 = zb;
+        p.ld_dx16 = nz;
+        p.dz16 = zb + D;
+        p.ld_dz16 = nz;
+        p.dd16 = zb + 2 * D;
+        p.ld_dd16 = nz;
+        p.bc16 = zb + 3 * D;
+        p.ld_bc16 = nz;
+        p.only16 = !dx && !ddelta && !dz && !need_dxt;
+        e = ssmk::launch_grad(p, s);
+        if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad scan launch");
+        // dW_x = x^T dZx and G = u^T Z in one launch
+        float* G = reinterpret_cast<float*>(ws + w.g_off);
+        const ssmk::DwProduct px{D, nx, static_cast<const uint16_t*>(x), D, zb + 2 * D, nz, dW_x, false};
+        const ssmk::DwProduct pg{d_model, nz, static_cast<const uint16_t*>(u), d_model, zb, nz, G, false};
+        e = ssmk::launch_gemm_dw2(M, px, pg, gws, s);
+        if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_x / G launch");
+        // dW_in[:, D:] = G[:, D:2D]; hi + lo = G[:, 2D:] = u^T dZx
+        uint16_t* hi = reinterpret_cast<uint16_t*>(ws + w.hl_off);
+        uint16_t* lo = hi + d_model * nx;
+        e = ssmk::launch_layer_split(G, nz, d_model, D, nx, dW_in, 2 * D, hi, lo, s);
+        if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad split launch");
+        // dW_in[:, :D] = G[:, :D] + lo W_x^T, then += hi W_x^T
+        const uint16_t* Wx = static_cast<const uint16_t*>(W_x);
+        e = ssmk::launch_gemm_dx(d_model, D, nx, lo, nx, Wx, nx, dW_in, false, G, nullptr, 0, gws, s, 2 * D, nz,
+                                 "gemm_dwin_fix");
+        if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_in launch");
+        e = ssmk::launch_gemm_dx(d_model, D, nx, hi, nx, Wx, nx, dW_in, true, nullptr, nullptr, 0, gws, s, 2 * D,
+                                 0, "gemm_dwin_fix");
+        if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dW_in launch");
+        if (need_dxt) {
+            // dx_total = dx + dZx W_x^T; its bf16 copy replaces dx in Z, so that
+            // Z[:, :2D] = [dx_total | dz] for du
+            e = ssmk::launch_gemm_dx(M, D, nx, zb + 2 * D, nz, Wx, nx, dx_total, false, dx_, zb, nz, gws, s);
+            if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dx_total launch");
+        }
+        if (du) {
+            e = ssmk::launch_gemm_dx(M, d_model, 2 * D, zb, nz, static_cast<const uint16_t*>(W_in), 2 * D, du, false,
+                                     nullptr, nullptr, 0, gws, s);
+            if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad du launch");
+        }
+        return SSM_OK;
+    }
+    // d_model >= D: dx_total first, then both weight gradients in one launch
+    // (the scan kernels write dZx and the dz half of [dx_total | dz] in bf16, and dx
+    // in fp32 as the dx_total product's addend)
+    uint16_t* dzx = zb;
+    uint16_t* dxz = zb + M * nx;
     p.dd16 = dzx;
     p.ld_dd16 = nx;
     p.bc16 = dzx + D;
     p.ld_bc16 = nx;
     p.dz16 = dxz + D;
     p.ld_dz16 = 2 * D;
-    // fp32 dDelta_pre and dz are written only when the caller asks for one of them
-    p.only16 = !ddelta && !dz;
-    hipError_t e = ssmk::launch_grad(p, s);
+    e = ssmk::launch_grad(p, s);
     if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad scan launch");
-    void* gws = ws + w.gemm_off;
     // dx_total = dx + dZx W_x^T, also packed into [dx_total | dz]
     // (the fp32 dx_total only when the caller asks for it)
-    e = ssmk::launch_gemm_dx(M, D, nx, dzx, nx, static_cast<const uint16_t*>(W_x), nx, dx_total, false,
-                             dx_, dxz, 2 * D, gws, s);
+    e = ssmk::launch_gemm_dx(M, D, nx, dzx, nx, static_cast<const uint16_t*>(W_x), nx, dx_total, false, dx_, dxz,
+                             2 * D, gws, s);
     if (e != hipSuccess) return hip_fail(e, "ssm_layer_grad dx_total launch");
     // dW_x = x^T dZx and dW_in = u^T [dx_total | dz], in one launch
     const ssmk::DwProduct px{D, nx, static_cast<const uint16_t*>(x), D, dzx, nx, dW_x, false};

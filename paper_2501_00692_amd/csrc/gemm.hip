@@ -121,9 +121,11 @@ struct GemmArgs {
     int64_t kper;         // reduction range per split (multiple of BK)
     int direct;           // write C (else the partial of the workgroup's split)
     int accum;            // C += result
-    const float* add;     // optional fp32 addend [R][Cc]
+    const float* add;     // optional fp32 addend [R][Cc] (row stride ldadd)
     uint16_t* out16;      // optional bf16 copy of the result
     int64_t ld16;
+    int64_t ldc;          // row stride of C when written directly (split partials: Cc)
+    int64_t ldadd;        // row stride of add
 };
 
 // One launch covers the output tiles of one product, or of two products with the
@@ -293,9 +295,9 @@ struct ColMajorOps {
 // bf16 (O16).  acc element v of lane l is row 8(v/4) + 4(l/32) + v%4, column
 // l%32 of its tile.  FULL: the block lies inside the output (no checks).
 template <bool ADD, bool ACC, bool DST, bool O16, bool FULL, int MI, int NJ>
-__device__ __forceinline__ void store_tile(const f32x16 (&acc)[MI][NJ], float* __restrict__ dst,
-                                           const float* __restrict__ addp, uint16_t* __restrict__ o16, int64_t ld16,
-                                           int64_t R, int64_t Cc, int64_t row0, int64_t col0, int lane) {
+__device__ __forceinline__ void store_tile(const f32x16 (&acc)[MI][NJ], float* __restrict__ dst, int64_t ldc,
+                                           const float* __restrict__ addp, int64_t ldadd, uint16_t* __restrict__ o16,
+                                           int64_t ld16, int64_t R, int64_t Cc, int64_t row0, int64_t col0, int lane) {
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -308,10 +310,10 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[MI][NJ], float* _
             for (int v = 0; v < 16; ++v) {
                 const int64_t row = rb + 8 * (v >> 2) + (v & 3);
                 const bool in = FULL || (row < R && col < Cc);
-                const int64_t o = in ? row * Cc + col : 0;  // out-of-range lanes read element 0
+                // out-of-range lanes read element 0
                 float e = 0.f;
-                if constexpr (ADD) e = addp[o];
-                if constexpr (ACC) e += dst[o];
+                if constexpr (ADD) e = addp[in ? row * ldadd + col : 0];
+                if constexpr (ACC) e += dst[in ? row * ldc + col : 0];
                 extra[v] = e;
             }
 #pragma unroll
@@ -319,7 +321,7 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[MI][NJ], float* _
                 const int64_t row = rb + 8 * (v >> 2) + (v & 3);
                 if (FULL || (row < R && col < Cc)) {
                     const float val = acc[i][j][v] + extra[v];
-                    if constexpr (DST) dst[row * Cc + col] = val;
+                    if constexpr (DST) dst[row * ldc + col] = val;
                     if constexpr (O16) o16[row * ld16 + col] = f2bf(val);
                 }
             }
@@ -518,7 +520,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmLaunch gl) {
     auto store = [&](auto Ft, auto Mt) __attribute__((always_inline)) {
         constexpr int M = decltype(Mt)::value;
         store_tile<(M & 1) != 0, (M & 2) != 0, (M & 4) != 0, (M & 8) != 0, decltype(Ft)::value>(
-            acc, dst, addp, o16, g.ld16, g.R, g.Cc, r0 + wr, c0 + wc, lane);
+            acc, dst, g.direct ? g.ldc : g.Cc, addp, g.ldadd, o16, g.ld16, g.R, g.Cc, r0 + wr, c0 + wc, lane);
     };
     auto by_mask = [&](auto Ft) __attribute__((always_inline)) {
         if constexpr (TR) {  // dW: C or C += (split partials are C)
@@ -554,11 +556,12 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmLaunch gl) {
 struct ReduceArgs {
     int64_t R, Cc;
     const float* part;  // [splits][R][Cc]
-    float* dst;
+    float* dst;         // row stride ldc
     int accum;
-    const float* add;
+    const float* add;   // row stride ldadd
     uint16_t* out16;
     int64_t ld16;
+    int64_t ldc, ldadd;
 };
 struct ReduceLaunch {
     ReduceArgs p[2];
@@ -591,15 +594,15 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const ReduceLaunch rl) {
             }
         }
     }
-    float4 e = a.add ? *reinterpret_cast<const float4*>(a.add + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    const int64_t row = i / a.Cc, col = i - row * a.Cc;
+    float4 e = a.add ? *reinterpret_cast<const float4*>(a.add + row * a.ldadd + col) : make_float4(0.f, 0.f, 0.f, 0.f);
     if (a.accum) {
-        const float4 d = *reinterpret_cast<const float4*>(a.dst + i);
+        const float4 d = *reinterpret_cast<const float4*>(a.dst + row * a.ldc + col);
         e = make_float4(e.x + d.x, e.y + d.y, e.z + d.z, e.w + d.w);
     }
     const float4 val = make_float4(s.x + e.x, s.y + e.y, s.z + e.z, s.w + e.w);
-    if (a.dst) *reinterpret_cast<float4*>(a.dst + i) = val;
+    if (a.dst) *reinterpret_cast<float4*>(a.dst + row * a.ldc + col) = val;
     if (a.out16) {
-        const int64_t row = i / a.Cc, col = i - row * a.Cc;
         uint16_t* o = a.out16 + row * a.ld16 + col;
         o[0] = f2bf(val.x);
         o[1] = f2bf(val.y);
@@ -743,8 +746,9 @@ hipError_t launch_dw(int np, const DwProduct* d, int64_t M, void* ws, hipStream_
     float* part = static_cast<float*>(ws);
     for (int q = 0; q < np; ++q) {
         g[q] = GemmArgs{d[q].K, d[q].N, M, d[q].X, d[q].ldx, d[q].dZ, d[q].lddz, direct ? d[q].dW : part,
-                        split_range(M, pl.splits), direct ? 1 : 0, d[q].accum ? 1 : 0, nullptr, nullptr, 0};
-        fin[q] = ReduceArgs{0, 0, nullptr, d[q].dW, d[q].accum ? 1 : 0, nullptr, nullptr, 0};
+                        split_range(M, pl.splits), direct ? 1 : 0, d[q].accum ? 1 : 0, nullptr, nullptr, 0,
+                        d[q].N, 0};
+        fin[q] = ReduceArgs{0, 0, nullptr, d[q].dW, d[q].accum ? 1 : 0, nullptr, nullptr, 0, d[q].N, 0};
         if (!direct) part += static_cast<int64_t>(pl.splits) * d[q].K * d[q].N;
     }
     {
@@ -789,19 +793,22 @@ hipError_t launch_gemm_dw2(int64_t M, const DwProduct& a, const DwProduct& b, vo
 
 hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, int64_t lddz,
                           const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
-                          uint16_t* out16, int64_t ld16, void* ws, hipStream_t s) {
+                          uint16_t* out16, int64_t ld16, void* ws, hipStream_t s, int64_t ldx, int64_t ldadd,
+                          const char* timer) {
+    if (ldx <= 0) ldx = K;
+    if (ldadd <= 0) ldadd = K;
     // outputs with few tiles (narrow projections) split the reduction as dW does
     const Plan pl = plan_gemm(M, K, N, true, false);
     const bool direct = pl.splits == 1;
     const GemmArgs g{M, K, N, dZ, lddz, W, ldw, direct ? dX : static_cast<float*>(ws), split_range(N, pl.splits),
-                     direct ? 1 : 0, accum ? 1 : 0, add, out16, ld16};
+                     direct ? 1 : 0, accum ? 1 : 0, add, out16, ld16, ldx, ldadd};
     {
-        SSMK_TIMED("gemm_dx", s);
+        SSMK_TIMED(timer ? timer : "gemm_dx", s);
         if (!launch_plan<false>(&g, 1, pl, s)) return hipErrorInvalidConfiguration;
     }
     if (!direct) {
         SSMK_TIMED("splitk_reduce", s);
-        const ReduceArgs fin{0, 0, nullptr, dX, accum ? 1 : 0, add, out16, ld16};
+        const ReduceArgs fin{0, 0, nullptr, dX, accum ? 1 : 0, add, out16, ld16, ldx, ldadd};
         launch_reduce(&g, &fin, 1, pl.splits, s);
     }
     return hipGetLastError();

@@ -73,7 +73,9 @@ struct ScanProblem {
     int64_t ld_dz16;
     uint16_t* bc16;
     int64_t ld_bc16;
-    bool only16;    // with the copies: skip the fp32 ddelta and dz (not wanted by the caller)
+    uint16_t* dx16;  // dx -> dx16[row * ld_dx16 + d] (with the copies; required with only16)
+    int64_t ld_dx16;
+    bool only16;    // with the copies: write no fp32 dx, ddelta and dz (only the bf16 copies)
     // workspace regions
     float* hbuf;    // [b][nc][N][D]
     float* hseg;    // [b][nc][L/seg][Dp][16]: state at each segment start from a zero chunk carry-in
@@ -114,6 +116,11 @@ hipError_t launch_forward(const ScanProblem& p, hipStream_t s);
 constexpr size_t kNoallocScratchBytes = size_t(64) << 20;
 hipError_t noalloc_scratch(void** ptr);
 hipError_t launch_grad(const ScanProblem& p, hipStream_t s);
+
+// The layer's reassociated input-projection gradient (layer.hip): dW_in[:, D:2D] =
+// G[:, D:2D] and the bf16 hi/lo split of G[:, 2D:2D+nx] into hi, lo [dm][nx].
+hipError_t launch_layer_split(const float* G, int64_t ldg, int64_t dm, int64_t D, int64_t nx, float* dW_in,
+                              int64_t ldw, uint16_t* hi, uint16_t* lo, hipStream_t s);
 
 // Kernels of the K-layer residual stack (stack.hip).
 hipError_t launch_rms_fwd(const float* y, uint16_t* u, float* rinv, int64_t M, int64_t D, hipStream_t s);
@@ -156,8 +163,11 @@ hipError_t launch_gemm_dw2(int64_t M, const DwProduct& a, const DwProduct& b, vo
 // be NULL when out16 is given (only the copy is written).  Narrow outputs split the
 // reduction: ws holds gemm_dx_workspace(M, K, N) bytes (none otherwise).
 size_t gemm_dx_workspace(int64_t M, int64_t K, int64_t N);
+// ldx and ldadd are the row strides of dX and of the addend (0: K); `timer` names
+// the launch in the per-kernel timing (default "gemm_dx").
 hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, int64_t lddz,
                           const uint16_t* W, int64_t ldw, float* dX, bool accum, const float* add,
-                          uint16_t* out16, int64_t ld16, void* ws, hipStream_t s);
+                          uint16_t* out16, int64_t ld16, void* ws, hipStream_t s, int64_t ldx = 0,
+                          int64_t ldadd = 0, const char* timer = nullptr);
 
 }  // namespace ssmk

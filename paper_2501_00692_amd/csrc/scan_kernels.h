@@ -770,12 +770,15 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     float* dxo = p.dx + (bb * p.T + t0) * p.D;
     float* ddo = p.ddelta + (bb * p.T + t0) * p.D;
     float* dzo = GATE ? p.dz + (bb * p.T + t0) * p.D : nullptr;
-    // OUT 1: also write the bf16 copies of ddelta and dz; OUT 2: write only those
-    // copies (no fp32 ddelta and dz), for callers that do not want them
+    // OUT 1: also write the bf16 copies of ddelta and dz (and of dx when dx16 is
+    // given); OUT 2: write only the bf16 copies of dx, ddelta and dz (no fp32 dx,
+    // ddelta and dz), for callers that want only the projection GEMMs' operands
     constexpr bool OUT16 = OUT > 0;
     uint16_t* dd16o = OUT16 ? p.dd16 + (bb * p.T + t0) * p.ld_dd16 : nullptr;
     uint16_t* dz16o = OUT16 ? p.dz16 + (bb * p.T + t0) * p.ld_dz16 : nullptr;
+    uint16_t* dx16o = (OUT16 && p.dx16) ? p.dx16 + (bb * p.T + t0) * p.ld_dx16 : nullptr;
     const uint32_t ldd16 = static_cast<uint32_t>(p.ld_dd16), ldz16 = static_cast<uint32_t>(p.ld_dz16);
+    const uint32_t ldx16 = static_cast<uint32_t>(p.ld_dx16);
     // Lanes whose step or channel is padding store into the sink instead, so
     // that every store is issued without a branch and the waits for loads issued
     // before them stay exact (a skipped store would make them wait for all
@@ -1172,7 +1175,12 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 // adds dx' x to dDelta
                 const float dd0 = p.bdelta ? fmaf(dxk[jj], xr[jj], ddk[jj]) : ddk[jj];
                 const float ddv = SP ? dd0 * (1.f - fexp(-dls[jj])) : dd0;  // d softplus / d Delta_pre
-                *(sv[jj] ? dxo + off : sinkf) = p.bdelta ? dxk[jj] * dls[jj] : dxk[jj];
+                const float dxv = p.bdelta ? dxk[jj] * dls[jj] : dxk[jj];
+                if constexpr (OUT != 2) *(sv[jj] ? dxo + off : sinkf) = dxv;
+                if constexpr (OUT == 2) stf(sv[jj] ? dx16o + (tl * ldx16 + d32) : sink16, 0, dxv);
+                if constexpr (OUT == 1) {
+                    if (dx16o) stf(sv[jj] ? dx16o + (tl * ldx16 + d32) : sink16, 0, dxv);
+                }
                 if constexpr (OUT != 2) *(sv[jj] ? ddo + off : sinkf) = ddv;
                 if constexpr (OUT16) stf(sv[jj] ? dd16o + (tl * ldd16 + d32) : sink16, 0, ddv);
             }
@@ -1367,8 +1375,10 @@ void grad_main(const ScanProblem& p, hipStream_t s) {
 
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16>
 hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
-    if ((p.dd16 || p.dz16 || p.bc16) && !(sizeof(TI) == 2 && SP && GATE)) return hipErrorInvalidValue;
+    if ((p.dd16 || p.dz16 || p.bc16 || p.dx16) && !(sizeof(TI) == 2 && SP && GATE)) return hipErrorInvalidValue;
     if (p.dd16 && !(p.dz16 && p.bc16)) return hipErrorInvalidValue;
+    if ((p.dx16 || p.only16) && !p.dd16) return hipErrorInvalidValue;
+    if (p.only16 && !p.dx16) return hipErrorInvalidValue;
     dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);

@@ -293,29 +293,46 @@ def test_proj_grad_wide_dw_tiles_sampled():
 
 
 def test_layer_workload_weight_grads_exact_sampled():
-    """Both weight gradients of the layer workload come from one GEMM launch
-    over their tiles together (a split reduction over the M = 8192 rows).  Each
-    is the product of bf16 operands the layer hands over: dW_x = x^T dZx with dZx
-    the bf16 rounding of [dDelta_pre | dB | dC], dW_in = u^T [dx_total | dz] in
-    bf16.  The layer's own fp32 outputs, rounded to bf16, rebuild those operands
-    exactly, so sampled entries (with every row's and column's last one) are
-    checked against the oracle's plain loops at the GEMM tolerance."""
+    """The layer's weight gradients against the products of the bf16 operands the
+    layer hands over, at the layer workload (one launch over the M = 8192 rows).
+    With d_model < D the input projection's gradient is reassociated:
+    dW_x = x^T dZx, dW_in[:, D:] = u^T dz and dW_in[:, :D] = u^T dx + (u^T dZx)
+    W_x^T, with dZx = bf16([dDelta_pre | dB | dC]), dx and dz in bf16 (round to
+    nearest even).  The layer's own fp32 outputs, rounded to bf16, rebuild those
+    operands exactly, so sampled entries (with every row's and column's last
+    one) are checked against the oracle's plain loops: the pure products at the
+    GEMM tolerance, the reassociated block (whose d_model x (D+2N) factor enters
+    the second product as two bf16 parts, about 2^-17 relative) at 1e-4."""
     w = WORKLOADS["layer"]
     say(f"[layer weight gradients] {w}")
     inp = make_inputs(w, device="cuda")
     o = ssm.ssm_layer_grad(inp["u"], inp["x"], inp["z"], inp["delta"], inp["B"], inp["C"], inp["W_x"],
                            inp["W_in"], inp["A_log"], inp["dy"], want_scan=True)
     torch.cuda.synchronize()
-    M = w.M
+    M, D, dm = w.M, w.D, w.d_model
+    assert dm < D  # the reassociated form
     bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
-    dzx = torch.cat([o["ddelta"], o["dB"], o["dC"]], dim=-1).reshape(M, -1).to(torch.bfloat16)
-    dxz = torch.cat([o["dx_total"], o["dz"]], dim=-1).reshape(M, -1).to(torch.bfloat16)
+    dzx = bits(torch.cat([o["ddelta"], o["dB"], o["dC"]], dim=-1).reshape(M, -1).to(torch.bfloat16))
+    dx16 = bits(o["dx"].reshape(M, D).to(torch.bfloat16))
+    dz16 = bits(o["dz"].reshape(M, D).to(torch.bfloat16))
+    xb, ub = bits(inp["x"].reshape(M, D)), bits(inp["u"].reshape(M, dm))
     rng = np.random.default_rng(11)
     rep = {}
-    for name, X, dZ in (("dW_x", inp["x"], dzx), ("dW_in", inp["u"], dxz)):
-        K, N = X.shape[-1], dZ.shape[-1]
-        kk = np.concatenate([rng.integers(0, K, 2048), [K - 1, K - 1, 0]])
-        jj = np.concatenate([rng.integers(0, N, 2048), [N - 1, 0, N - 1]])
-        ref = oracle.proj_dw(bits(X.reshape(M, K)), bits(dZ), kk, jj)
-        check(f"{name}[sampled]", to_np(o[name])[kk, jj], ref, 1e-5, rep)
+    nx = dzx.shape[1]
+    kk = np.concatenate([rng.integers(0, D, 2048), [D - 1, D - 1, 0]])
+    jj = np.concatenate([rng.integers(0, nx, 2048), [nx - 1, 0, nx - 1]])
+    check("dW_x[sampled]", to_np(o["dW_x"])[kk, jj], oracle.proj_dw(xb, dzx, kk, jj), 1e-5, rep)
+    kk = np.concatenate([rng.integers(0, dm, 2048), [dm - 1, dm - 1, 0]])
+    jj = np.concatenate([rng.integers(0, D, 2048), [D - 1, 0, D - 1]])
+    check("dW_in[:,D:][sampled]", to_np(o["dW_in"])[kk, D + jj], oracle.proj_dw(ub, dz16, kk, jj), 1e-5, rep)
+    # the reassociated block on 24 sampled rows of dW_in (all of each row's
+    # u^T dZx, then its product with W_x^T) and 64 sampled columns
+    rows = np.concatenate([np.sort(rng.choice(dm, 23, replace=False)), [dm - 1]])
+    cols = np.concatenate([np.sort(rng.choice(D, 63, replace=False)), [D - 1]])
+    rr, cc = np.meshgrid(rows, np.arange(nx), indexing="ij")
+    gz = oracle.proj_dw(ub, dzx, rr.ravel(), cc.ravel()).reshape(len(rows), nx)
+    wx = to_np(inp["W_x"])[cols]  # [cols][nx]
+    r2, c2 = np.meshgrid(rows, cols, indexing="ij")
+    ref = oracle.proj_dw(ub, dx16, r2.ravel(), c2.ravel()).reshape(len(rows), len(cols)) + gz @ wx.T
+    check("dW_in[:,:D][sampled]", to_np(o["dW_in"])[np.ix_(rows, cols)], ref, 1e-4, rep)
     say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
