@@ -122,6 +122,11 @@ ssm_status ssm_adjoint_forward(const ssm_desc* desc, const void* x, const void* 
  *   dB, dC [b][T][N]  (dC is never truncated)
  *   dz     [b][T][D]  required iff SSM_GATE_SILU, else must be NULL
  *   dh0    [b][D][N]  dL/dh0, full mode only (must be NULL when truncating), or NULL.
+ *   da_debug [b][T][D][N] or NULL: a debug output, the cotangent of each decay value,
+ *          da_t[d,n] = mubar_t[d,n] h_{t-1}[d,n] (Prop. 2's vjp_A term before it is
+ *          chained into Delta and A_log; mubar the full or the windowed adjoint).  It
+ *          is computed by a separate, slow kernel (one thread per batch, channel and
+ *          state walking the sequence) that runs only when the pointer is given. 
  * The truncated A- and B-path terms use the windowed adjoint
  * mubar_i = sum_{t=i}^{min(T-1, i+tbar-1)} g_t C_t P(i, t), P(i, j) = prod_{k=i+1}^{j} a_k,
  * computed by its own reverse recurrence mubar_i = g_i C_i + a_{i+1} mubar_{i+1}
@@ -130,7 +135,8 @@ ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, co
                             const void* delta, const float* A_log, const void* B, const void* C,
                             const float* h0, const void* z, const void* dy, float* dx,
                             float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
-                            float* dh0, void* workspace, size_t workspace_bytes, void* stream);
+                            float* dh0, float* da_debug, void* workspace, size_t workspace_bytes,
+                            void* stream);
 
 /* ssm_adjoint_grad without a workspace argument, for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops,
@@ -149,7 +155,7 @@ ssm_status ssm_adjoint_grad_noalloc(const ssm_desc* desc, int32_t mode, int64_t 
                                     const void* delta, const float* A_log, const void* B,
                                     const void* C, const float* h0, const void* z, const void* dy,
                                     float* dx, float* ddelta, float* dA_log, float* dB, float* dC,
-                                    float* dz, float* dh0, void* stream);
+                                    float* dz, float* dh0, float* da_debug, void* stream);
 
 /* The same gradient as ssm_adjoint_grad (identical arguments, layouts, outputs
  * and error behaviour), evaluated by the explicit pair formulation of Prop. 2 and
@@ -167,7 +173,8 @@ ssm_status ssm_adjoint_grad_pairs(const ssm_desc* desc, int32_t mode, int64_t tb
                                   const void* delta, const float* A_log, const void* B, const void* C,
                                   const float* h0, const void* z, const void* dy, float* dx,
                                   float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
-                                  float* dh0, void* workspace, size_t workspace_bytes, void* stream);
+                                  float* dh0, float* da_debug, void* workspace, size_t workspace_bytes,
+                                  void* stream);
 
 /* Projection gradients of a linear map Z = X W (Sec. 4.5: the A, B, C networks
  * are single-layer maps; the per-step vjps summed over t give these products):

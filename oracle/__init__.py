@@ -76,7 +76,7 @@ def _load():
         lib = ctypes.CDLL(str(_LIB))
         i64, dp, ip = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
         lib.oracle_forward.argtypes = [i64, i64, i64, i64, dp, dp, ip, dp, dp, dp, dp, dp, dp, dp, ip]
-        grad_args = [dp, dp, ip, dp, dp, dp, dp, dp, dp, dp, dp, dp, dp, dp, dp, dp, ip]
+        grad_args = [dp, dp, ip, dp, dp, dp, dp, dp, dp, dp, dp, dp, dp, dp, dp, dp, dp, ip]
         lib.oracle_bptt.argtypes = [i64, i64, i64, i64] + grad_args
         lib.oracle_adjoint_sum.argtypes = [i64, i64, i64, i64, i64] + grad_args
         lib.oracle_trunc_tail.argtypes = [i64, i64, i64, i64, i64] + grad_args
@@ -129,7 +129,7 @@ def forward(x, delta, A_log, B, C, h0=None, z=None, delta_softplus=False, nthrea
 
 
 def _grad(fn, with_tbar, tbar, x, delta, A_log, B, C, dy, h0, z, delta_softplus, want_dh0, nthreads,
-          a_scalar=False, b_delta=False):
+          a_scalar=False, b_delta=False, want_da=False):
     x, delta, A_log, B, C, h0, z, dy = map(_f64, (x, delta, A_log, B, C, h0, z, dy))
     nb, T, D = x.shape
     N = B.shape[-1]
@@ -140,43 +140,45 @@ def _grad(fn, with_tbar, tbar, x, delta, A_log, B, C, dy, h0, z, delta_softplus,
     }
     out["dz"] = np.empty((nb, T, D)) if z is not None else None
     out["dh0"] = np.empty((nb, D, N)) if want_dh0 else None
+    out["da"] = np.empty((nb, T, D, N)) if want_da else None
     head = (nb, T, D, N, int(tbar)) if with_tbar else (nb, T, D, N)
     rc = fn(*head, _ptr(x), _ptr(delta), _flags(delta_softplus, a_scalar, b_delta), _ptr(A_log), _ptr(B),
             _ptr(C), _ptr(h0),
             _ptr(z), _ptr(dy), _ptr(out["dx"]), _ptr(out["ddelta"]), _ptr(out["dA_log"]), _ptr(out["dB"]),
-            _ptr(out["dC"]), _ptr(out["dz"]), _ptr(out["dh0"]), nthreads)
+            _ptr(out["dC"]), _ptr(out["dz"]), _ptr(out["dh0"]), _ptr(out["da"]), nthreads)
     if rc:
         raise ValueError(f"oracle gradient failed ({rc})")
     return out
 
 
 def bptt(x, delta, A_log, B, C, dy, h0=None, z=None, delta_softplus=False, want_dh0=True, nthreads=0,
-         a_scalar=False, b_delta=False):
-    """Exact full gradient by backpropagation through time (dict of arrays)."""
+         a_scalar=False, b_delta=False, want_da=False):
+    """Exact full gradient by backpropagation through time (dict of arrays).
+    ``want_da`` adds ``da`` [b, T, D, N], the cotangent of the decay a_t itself."""
     return _grad(_load().oracle_bptt, False, 0, x, delta, A_log, B, C, dy, h0, z, delta_softplus,
-                 want_dh0, nthreads, a_scalar, b_delta)
+                 want_dh0, nthreads, a_scalar, b_delta, want_da)
 
 
 def adjoint_sum(x, delta, A_log, B, C, dy, tbar=0, h0=None, z=None, delta_softplus=False,
-                want_dh0=None, nthreads=0, a_scalar=False, b_delta=False):
+                want_dh0=None, nthreads=0, a_scalar=False, b_delta=False, want_da=False):
     """Prop. 2 (``tbar<=0`` or ``tbar>=T``) / Eq. "capped" double sum, literally."""
     T = np.shape(x)[1]
     full = tbar <= 0 or tbar >= T
     if want_dh0 is None:
         want_dh0 = full
     return _grad(_load().oracle_adjoint_sum, True, tbar, x, delta, A_log, B, C, dy, h0, z,
-                 delta_softplus, want_dh0, nthreads, a_scalar, b_delta)
+                 delta_softplus, want_dh0, nthreads, a_scalar, b_delta, want_da)
 
 
 def trunc_tail(x, delta, A_log, B, C, dy, tbar=0, h0=None, z=None, delta_softplus=False,
-               want_dh0=None, nthreads=0, a_scalar=False, b_delta=False):
+               want_dh0=None, nthreads=0, a_scalar=False, b_delta=False, want_da=False):
     """Truncated estimator via the tail identity (O(T) per channel)."""
     T = np.shape(x)[1]
     full = tbar <= 0 or tbar >= T
     if want_dh0 is None:
         want_dh0 = full
     return _grad(_load().oracle_trunc_tail, True, tbar, x, delta, A_log, B, C, dy, h0, z,
-                 delta_softplus, want_dh0, nthreads, a_scalar, b_delta)
+                 delta_softplus, want_dh0, nthreads, a_scalar, b_delta, want_da)
 
 
 def silu(z):

@@ -27,7 +27,9 @@
  *
  * Layouts (row-major, fp64): x, delta, z, dy, out, dx, ddelta, dz : [b][T][D];
  * B, C, dB, dC : [b][T][N]; A_log, dA_log : [D][N] (or [D]); h0, h_last, dh0 :
- * [b][D][N].  All gradient outputs are overwritten.
+ * [b][D][N]; da : [b][T][D][N], the cotangent of the decay a_t[d,n] itself (the
+ * diagonal of Prop. 2's vjp_A term before it is chained into Delta and A_log).
+ * All gradient outputs are overwritten.
  *
  * Functions and the passages they follow:
  *   oracle_forward      Sec. 3.1 five steps (sequential loop over t).
@@ -171,13 +173,14 @@ static void chan_forward(int64_t bb, int64_t d, int64_t T, int64_t D, int64_t N,
 static void step_vjp(int64_t bb, int64_t i, int64_t d, int64_t T, int64_t D, int64_t N, int flags,
                      const double* w, const chan_fwd* f, const double* x,
                      const double* A_log, const double* B,
-                     double* dx, double* ddelta_raw, double* dA_log_row, double* dB_acc) {
+                     double* dx, double* ddelta_raw, double* dA_log_row, double* dB_acc, double* da_out) {
     int64_t td = (bb * T + i) * D + d;
     double sc = (flags & OR_B_DELTA) ? f->dl[i] : 1.0;  /* d u / d x */
     double sdx = 0.0, sdd = 0.0;
     for (int64_t n = 0; n < N; ++n) {
         double ea = exp(alog_at(A_log, flags, d, N, n));
         double da = w[n] * f->hs[i * N + n];            /* h_{i-1} is hs[i] */
+        if (da_out) da_out[td * N + n] += da;             /* the cotangent of a_i itself */
         double ai = f->a[i * N + n];
         sdd += da * ai * (-ea);                           /* d a / d Delta */
         dA_log_row[(flags & OR_A_SCALAR) ? 0 : n] += da * ai * (-f->dl[i] * ea); /* d a / d A_log */
@@ -217,7 +220,7 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
                        const double* A_log, const double* B, const double* C,
                        const double* h0, const double* z, const double* dy,
                        double* dx, double* ddelta, double* dA_log, double* dB, double* dC,
-                       double* dz, double* dh0, int nthreads) {
+                       double* dz, double* dh0, double* da, int nthreads) {
     if (grad_common_checks(nb, T, D, N)) return -1;
     int full = (tbar <= 0 || tbar >= T);
     if (!full && dh0) return -2; /* dh0 is defined for the full gradient only */
@@ -230,6 +233,7 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
     memset(dA_log, 0, (size_t)(D * NA) * sizeof(double));
     if (dz) memset(dz, 0, (size_t)(nb * T * D) * sizeof(double));
     if (dh0) memset(dh0, 0, (size_t)(nb * D * N) * sizeof(double));
+    if (da) memset(da, 0, (size_t)(nb * T * D * N) * sizeof(double));
 
     int64_t btn = nb * T * N;
     double* blkB[ORACLE_NBLK];
@@ -270,7 +274,7 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
                     for (int64_t t = T - 1; t >= 0; --t) {
                         for (int64_t n = 0; n < N; ++n)
                             w[n] = f.g[t] * C[(bb * T + t) * N + n] + lam[n];
-                        step_vjp(bb, t, d, T, D, N, flags, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q]);
+                        step_vjp(bb, t, d, T, D, N, flags, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q], da);
                         for (int64_t n = 0; n < N; ++n) lam[n] = f.a[t * N + n] * w[n];
                     }
                     if (dh0)
@@ -284,7 +288,7 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
                         for (int64_t n = 0; n < N; ++n) lam[n] = C[(bb * T + t) * N + n];
                         for (int64_t i = t; i >= i_lo; --i) {
                             for (int64_t n = 0; n < N; ++n) w[n] = f.g[t] * lam[n];
-                            step_vjp(bb, i, d, T, D, N, flags, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q]);
+                            step_vjp(bb, i, d, T, D, N, flags, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q], da);
                             for (int64_t n = 0; n < N; ++n) lam[n] *= f.a[i * N + n];
                         }
                         /* Prop. 1's lambda^0 term: only the full gradient
@@ -317,7 +321,7 @@ static int grad_driver(int mode, int64_t nb, int64_t T, int64_t D, int64_t N, in
                                 w[n] -= P * mu[(i + tbar) * N + n];
                             }
                         }
-                        step_vjp(bb, i, d, T, D, N, flags, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q]);
+                        step_vjp(bb, i, d, T, D, N, flags, w, &f, x, A_log, B, dx, ddelta, dA_row, blkB[q], da);
                     }
                     if (full && dh0)
                         for (int64_t n = 0; n < N; ++n)
@@ -340,9 +344,9 @@ int oracle_bptt(int64_t nb, int64_t T, int64_t D, int64_t N,
                 const double* A_log, const double* B, const double* C,
                 const double* h0, const double* z, const double* dy,
                 double* dx, double* ddelta, double* dA_log, double* dB, double* dC,
-                double* dz, double* dh0, int nthreads) {
+                double* dz, double* dh0, double* da, int nthreads) {
     return grad_driver(MODE_BPTT, nb, T, D, N, 0, x, delta, flags, A_log, B, C, h0, z,
-                       dy, dx, ddelta, dA_log, dB, dC, dz, dh0, nthreads);
+                       dy, dx, ddelta, dA_log, dB, dC, dz, dh0, da, nthreads);
 }
 
 int oracle_adjoint_sum(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t tbar,
@@ -350,9 +354,9 @@ int oracle_adjoint_sum(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t tbar
                        const double* A_log, const double* B, const double* C,
                        const double* h0, const double* z, const double* dy,
                        double* dx, double* ddelta, double* dA_log, double* dB, double* dC,
-                       double* dz, double* dh0, int nthreads) {
+                       double* dz, double* dh0, double* da, int nthreads) {
     return grad_driver(MODE_DOUBLESUM, nb, T, D, N, tbar, x, delta, flags, A_log, B, C,
-                       h0, z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0, nthreads);
+                       h0, z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0, da, nthreads);
 }
 
 int oracle_trunc_tail(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t tbar,
@@ -360,9 +364,9 @@ int oracle_trunc_tail(int64_t nb, int64_t T, int64_t D, int64_t N, int64_t tbar,
                       const double* A_log, const double* B, const double* C,
                       const double* h0, const double* z, const double* dy,
                       double* dx, double* ddelta, double* dA_log, double* dB, double* dC,
-                      double* dz, double* dh0, int nthreads) {
+                      double* dz, double* dh0, double* da, int nthreads) {
     return grad_driver(MODE_TAIL, nb, T, D, N, tbar, x, delta, flags, A_log, B, C, h0,
-                       z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0, nthreads);
+                       z, dy, dx, ddelta, dA_log, dB, dC, dz, dh0, da, nthreads);
 }
 
 /* ------------------------------------------------------------------------ */

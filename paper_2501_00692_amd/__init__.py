@@ -74,10 +74,10 @@ def load_library():
         "ssm_adjoint_forward_workspace_size": [dp, szp],
         "ssm_adjoint_grad_workspace_size": [dp, i32, i64, szp],
         "ssm_adjoint_forward": [dp] + [vp] * 9 + [vp, sz, vp],
-        "ssm_adjoint_grad": [dp, i32, i64] + [vp] * 15 + [vp, sz, vp],
-        "ssm_adjoint_grad_noalloc": [dp, i32, i64] + [vp] * 15 + [vp],
+        "ssm_adjoint_grad": [dp, i32, i64] + [vp] * 16 + [vp, sz, vp],
+        "ssm_adjoint_grad_noalloc": [dp, i32, i64] + [vp] * 16 + [vp],
         "ssm_adjoint_grad_pairs_workspace_size": [dp, i32, i64, szp],
-        "ssm_adjoint_grad_pairs": [dp, i32, i64] + [vp] * 15 + [vp, sz, vp],
+        "ssm_adjoint_grad_pairs": [dp, i32, i64] + [vp] * 16 + [vp, sz, vp],
         "ssm_proj_grad_workspace_size": [i64, i64, i64, u32, szp],
         "ssm_proj_grad": [i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, vp, u32, vp, sz, vp],
         "ssm_layer_grad_workspace_size": [dp, i32, i64, i64, szp],
@@ -221,38 +221,39 @@ def ssm_adjoint_forward(x, delta, A_log, B, C, h0=None, z=None, softplus=False, 
 
 
 def ssm_adjoint_grad(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False, tbar=0, chunk=0,
-                     want_dh0=False, out=None, workspace=None, b_delta=False):
+                     want_dh0=False, out=None, workspace=None, b_delta=False, want_da=False):
     """Per-layer adjoint gradient.  ``tbar > 0`` selects the truncated form.
     ``A_log`` of shape [D] selects one decay rate per channel (and dA_log is [D]);
     ``b_delta`` the input term Delta B x.
 
     Returns a dict with fp32 ``dx, ddelta, dA_log, dB, dC`` (+ ``dz`` with a gate,
-    ``dh0`` if asked).  ``out`` may hold preallocated outputs under the same keys."""
+    ``dh0`` if asked, the debug output ``da`` [b, T, D, N] if ``want_da``).  ``out``
+    may hold preallocated outputs under the same keys."""
     return _adjoint_grad(False, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk, want_dh0, out, workspace,
-                         b_delta)
+                         b_delta, want_da=want_da)
 
 
 def ssm_adjoint_grad_noalloc(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False, tbar=0, chunk=0,
-                             want_dh0=False, out=None, b_delta=False):
+                             want_dh0=False, out=None, b_delta=False, want_da=False):
     """:func:`ssm_adjoint_grad` through the C entry point that takes no workspace
     (its scratch is a fixed device array inside the library); arguments and
     results as there.  Raises :class:`SsmError` with SSM_ERR_WORKSPACE when the
     problem needs more scratch than the library holds."""
     return _adjoint_grad(False, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk, want_dh0, out, None,
-                         b_delta, noalloc=True)
+                         b_delta, noalloc=True, want_da=want_da)
 
 
 def ssm_adjoint_grad_pairs(x, delta, A_log, B, C, dy, h0=None, z=None, softplus=False, tbar=0, chunk=0,
-                           want_dh0=False, out=None, workspace=None, b_delta=False):
+                           want_dh0=False, out=None, workspace=None, b_delta=False, want_da=False):
     """The same gradient as :func:`ssm_adjoint_grad`, evaluated by the explicit
     pair formulation (every adjoint state of the window formed and its VJPs
     accumulated); arguments and results as there."""
     return _adjoint_grad(True, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk, want_dh0, out, workspace,
-                         b_delta)
+                         b_delta, want_da=want_da)
 
 
 def _adjoint_grad(pairs, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk, want_dh0, out, workspace,
-                  b_delta, noalloc=False):
+                  b_delta, noalloc=False, want_da=False):
     lib = load_library()
     dt = x.dtype
     b, T, D = x.shape
@@ -279,9 +280,11 @@ def _adjoint_grad(pairs, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk
         o.setdefault("dz", torch.empty(b, T, D, **f32))
     if want_dh0:
         o.setdefault("dh0", torch.empty(b, D, N, **f32))
+    if want_da:
+        o.setdefault("da", torch.empty(b, T, D, N, **f32))
     args = (ctypes.byref(desc), mode, int(tbar), _p(x), _p(delta), _p(A_log), _p(B), _p(C), _p(h0), _p(z), _p(dy),
             _p(o["dx"]), _p(o["ddelta"]), _p(o["dA_log"]), _p(o["dB"]), _p(o["dC"]), _p(o.get("dz")),
-            _p(o.get("dh0")))
+            _p(o.get("dh0")), _p(o.get("da")))
     if noalloc:
         _check(lib.ssm_adjoint_grad_noalloc(*args, _stream()), "ssm_adjoint_grad_noalloc")
         return o

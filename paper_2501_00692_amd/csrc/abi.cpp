@@ -287,7 +287,8 @@ static ssm_status grad_launch(const ssm_desc* desc, int64_t L, int64_t nc, bool 
                               const void* x, const void* delta, const float* A_log, const void* B,
                               const void* C, const float* h0, const void* z, const void* dy, float* dx,
                               float* ddelta, float* dA_log, float* dB, float* dC, float* dz, float* dh0,
-                              void* workspace, const ssmk::ScanWorkspace& w, void* stream, const char* where) {
+                              float* da_debug, void* workspace, const ssmk::ScanWorkspace& w, void* stream,
+                              const char* where) {
     ssmk::ScanProblem p = make_problem(desc, L, nc);
     p.trunc = trunc;
     p.tbar = trunc ? tbar : 0;
@@ -297,6 +298,10 @@ static ssm_status grad_launch(const ssm_desc* desc, int64_t L, int64_t nc, bool 
     ssmk::bind_workspace(p, workspace, w);
     hipError_t e = ssmk::launch_grad(p, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, where);
+    if (da_debug) {
+        e = ssmk::launch_da_debug(p, da_debug, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return hip_fail(e, "da_debug launch");
+    }
     return SSM_OK;
 }
 
@@ -304,30 +309,32 @@ ssm_status ssm_adjoint_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, co
                             const void* delta, const float* A_log, const void* B, const void* C,
                             const float* h0, const void* z, const void* dy, float* dx,
                             float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
-                            float* dh0, void* workspace, size_t workspace_bytes, void* stream) {
+                            float* dh0, float* da_debug, void* workspace, size_t workspace_bytes, void* stream) {
     int64_t L, nc;
     bool trunc;
     ssm_status st = grad_validate(desc, mode, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta,
                                   dA_log, dB, dC, dz, dh0, &L, &nc, &trunc);
     if (st) return st;
+    OPTIONAL_PTR(da_debug, "da_debug");
     ssmk::ScanWorkspace w = ssmk::scan_workspace(desc->batch, desc->seqlen, desc->channels,
                                                  desc->dstate, L, true, trunc);
     st = check_workspace(workspace, workspace_bytes, w.total);
     if (st) return st;
     return grad_launch(desc, L, nc, trunc, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta, dA_log, dB,
-                       dC, dz, dh0, workspace, w, stream, "ssm_adjoint_grad launch");
+                       dC, dz, dh0, da_debug, workspace, w, stream, "ssm_adjoint_grad launch");
 }
 
 ssm_status ssm_adjoint_grad_noalloc(const ssm_desc* desc, int32_t mode, int64_t tbar, const void* x,
                                     const void* delta, const float* A_log, const void* B, const void* C,
                                     const float* h0, const void* z, const void* dy, float* dx,
                                     float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
-                                    float* dh0, void* stream) {
+                                    float* dh0, float* da_debug, void* stream) {
     int64_t L, nc;
     bool trunc;
     ssm_status st = grad_validate(desc, mode, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta,
                                   dA_log, dB, dC, dz, dh0, &L, &nc, &trunc);
     if (st) return st;
+    OPTIONAL_PTR(da_debug, "da_debug");
     ssmk::ScanWorkspace w = ssmk::scan_workspace(desc->batch, desc->seqlen, desc->channels,
                                                  desc->dstate, L, true, trunc);
     if (w.total > ssmk::kNoallocScratchBytes)
@@ -339,7 +346,7 @@ ssm_status ssm_adjoint_grad_noalloc(const ssm_desc* desc, int32_t mode, int64_t 
     hipError_t e = ssmk::noalloc_scratch(&scratch);
     if (e != hipSuccess) return hip_fail(e, "ssm_adjoint_grad_noalloc scratch");
     return grad_launch(desc, L, nc, trunc, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta, dA_log, dB,
-                       dC, dz, dh0, scratch, w, stream, "ssm_adjoint_grad_noalloc launch");
+                       dC, dz, dh0, da_debug, scratch, w, stream, "ssm_adjoint_grad_noalloc launch");
 }
 
 // Limits of the pair formulation: its channel blocks form a grid dimension, and
@@ -372,12 +379,14 @@ ssm_status ssm_adjoint_grad_pairs(const ssm_desc* desc, int32_t mode, int64_t tb
                                   const void* delta, const float* A_log, const void* B, const void* C,
                                   const float* h0, const void* z, const void* dy, float* dx,
                                   float* ddelta, float* dA_log, float* dB, float* dC, float* dz,
-                                  float* dh0, void* workspace, size_t workspace_bytes, void* stream) {
+                                  float* dh0, float* da_debug, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
     int64_t L, nc;
     bool trunc;
     ssm_status st = grad_validate(desc, mode, tbar, x, delta, A_log, B, C, h0, z, dy, dx, ddelta,
                                   dA_log, dB, dC, dz, dh0, &L, &nc, &trunc);
     if (st) return st;
+    OPTIONAL_PTR(da_debug, "da_debug");
     st = check_pairs(desc);
     if (st) return st;
     ssmk::PairsWorkspace w = ssmk::pairs_workspace(desc->batch, desc->seqlen, desc->channels,
@@ -391,6 +400,10 @@ ssm_status ssm_adjoint_grad_pairs(const ssm_desc* desc, int32_t mode, int64_t tb
     hipError_t e = ssmk::launch_grad_pairs(p, workspace, w, trunc ? tbar : desc->seqlen,
                                            static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "ssm_adjoint_grad_pairs launch");
+    if (da_debug) {
+        e = ssmk::launch_da_debug(p, da_debug, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return hip_fail(e, "da_debug launch");
+    }
     return SSM_OK;
 }
 

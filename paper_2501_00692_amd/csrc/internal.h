@@ -109,6 +109,8 @@ ScanWorkspace scan_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int64_
 void bind_workspace(ScanProblem& p, void* ws, const ScanWorkspace& w);
 
 hipError_t launch_forward(const ScanProblem& p, hipStream_t s);
+// The optional debug output da [b][T][D][N] of the gradient (da_debug.hip).
+hipError_t launch_da_debug(const ScanProblem& p, float* da, hipStream_t s);
 
 // Scratch of ssm_adjoint_grad_noalloc (noalloc.hip): a file-scope device array of
 // kNoallocScratchBytes per GPU; noalloc_scratch returns the current device's

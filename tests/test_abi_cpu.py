@@ -52,9 +52,9 @@ MISALIGNED = ctypes.c_void_p(0x100004)
 
 
 def grad_call(lib, dsc, mode=ssm.SSM_FULL, tbar=0, x=FAKE, dh0=None, z=None, dz=None, ws=FAKE,
-              ws_bytes=1 << 40, entry="ssm_adjoint_grad"):
+              ws_bytes=1 << 40, entry="ssm_adjoint_grad", da=None):
     return getattr(lib, entry)(ctypes.byref(dsc) if dsc is not None else None, mode, tbar, x, FAKE, FAKE, FAKE,
-                               FAKE, None, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, dz, dh0, ws, ws_bytes, None)
+                               FAKE, None, z, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, dz, dh0, da, ws, ws_bytes, None)
 
 
 GRAD_ENTRIES = ["ssm_adjoint_grad", "ssm_adjoint_grad_pairs"]
@@ -74,6 +74,7 @@ def test_null_and_shape_errors(lib, entry):
     assert call(lib, desc(), x=None) == 1
     assert "x is NULL" in ssm.last_error()
     assert call(lib, desc(), x=MISALIGNED) == 6
+    assert call(lib, desc(), da=MISALIGNED) == 6
 
 
 @pytest.mark.parametrize("entry", GRAD_ENTRIES)
@@ -163,7 +164,8 @@ def test_stack_errors(lib):
 
 def noalloc_call(lib, dsc, mode=ssm.SSM_FULL, tbar=0, x=FAKE):
     return lib.ssm_adjoint_grad_noalloc(ctypes.byref(dsc) if dsc is not None else None, mode, tbar, x, FAKE, FAKE,
-                                        FAKE, FAKE, None, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None)
+                                        FAKE, FAKE, None, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None,
+                                        None)
 
 
 def test_noalloc_host_errors(lib):

@@ -468,3 +468,71 @@ def test_variant_doublesum_and_tail_agree(rng, a_scalar, b_delta):
         tl = oracle.trunc_tail(*args, tbar=tbar, **kw)
         for k in ("dx", "ddelta", "dA_log", "dB", "dC", "dz"):
             assert relerr(tl[k], ds[k]) < 1e-11, (tbar, k)
+
+
+# --------------------------------------------------------------------------
+# The decay cotangent da_i = mubar_i h_{i-1} (Prop. 2's vjp_A before the chain
+# into Delta and A_log)
+# --------------------------------------------------------------------------
+def _loss_with_decays(inp, a):
+    """L = sum dy * out for the layer with the decays a [b, T, D, N] given
+    directly (a plain loop, written here independently of the oracle)."""
+    nb, T, D = inp["x"].shape
+    N = inp["B"].shape[-1]
+    h = np.array(inp["h0"]) if inp["h0"] is not None else np.zeros((nb, D, N))
+    L = 0.0
+    for t in range(T):
+        h = a[:, t] * h + inp["B"][:, t, None, :] * inp["x"][:, t, :, None]
+        y = (inp["C"][:, t, None, :] * h).sum(-1)
+        if inp["z"] is not None:
+            y = y * inp["z"][:, t] / (1.0 + np.exp(-inp["z"][:, t]))
+        L += float(np.sum(inp["dy"][:, t] * y))
+    return L
+
+
+def _decays(inp):
+    dl = np.log1p(np.exp(inp["delta"])) if inp["delta_softplus"] else inp["delta"]
+    return np.exp(-dl[..., None] * np.exp(inp["A_log"])[None, None])
+
+
+def test_decay_cotangent_matches_central_differences(rng):
+    """Full mode: da[b, i, d, n] = dL/da_i[d, n] with every decay an independent
+    input; central differences (step 1e-6) on every entry of a small layer."""
+    inp = tiny(rng, nb=2, T=7, D=2, N=3, gate=True, softplus=True, h0=True)
+    got = bptt_of(inp, want_dh0=False, want_da=True)["da"]
+    a = _decays(inp)
+    fd = np.zeros_like(a)
+    eps = 1e-6
+    for idx in np.ndindex(*a.shape):
+        ap, am = a.copy(), a.copy()
+        ap[idx] += eps
+        am[idx] -= eps
+        fd[idx] = (_loss_with_decays(inp, ap) - _loss_with_decays(inp, am)) / (2 * eps)
+    assert relerr(got, fd) < 1e-7
+    ds = oracle.adjoint_sum(inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"], h0=inp["h0"],
+                            z=inp["z"], delta_softplus=True, want_da=True)["da"]
+    assert relerr(ds, got) < 1e-12  # Prop. 2's double sum, literally
+
+
+def test_truncated_decay_cotangent_is_sum_of_per_loss_truncated_backprop(rng):
+    """Truncated mode: da is the sum over loss terms l^t of the gradient of l^t
+    with respect to the decays of its last Tbar steps only (the state entering
+    that window detached): torch autograd with the decays as leaves."""
+    nb, T, D, N, tbar = 1, 13, 2, 3, 4
+    inp = tiny(rng, nb=nb, T=T, D=D, N=N, gate=True, softplus=True, h0=True)
+    a = torch.tensor(_decays(inp), dtype=torch.float64, requires_grad=True)
+    Bt, Ct, xt = (torch.tensor(inp[k]) for k in ("B", "C", "x"))
+    zt, dyt = torch.tensor(inp["z"]), torch.tensor(inp["dy"])
+    for t in range(T):
+        h = torch.tensor(inp["h0"])
+        for i in range(t + 1):
+            if i == t - tbar + 1:
+                h = h.detach()
+            h = a[:, i] * h + Bt[:, i, None, :] * xt[:, i, :, None]
+        y = (Ct[:, t, None, :] * h).sum(-1)
+        (dyt[:, t] * y * torch.nn.functional.silu(zt[:, t])).sum().backward()
+    ref = a.grad.numpy()
+    kw = dict(tbar=tbar, h0=inp["h0"], z=inp["z"], delta_softplus=True, want_da=True)
+    args = (inp["x"], inp["delta"], inp["A_log"], inp["B"], inp["C"], inp["dy"])
+    assert relerr(oracle.adjoint_sum(*args, **kw)["da"], ref) < 1e-12
+    assert relerr(oracle.trunc_tail(*args, **kw)["da"], ref) < 1e-11
