@@ -242,8 +242,24 @@ def measured_traffic(kern, workload):
     return int(rec["bytes_per_launch"])
 
 
-def workload_tag(w):
-    return f"{w.name}-b{w.b}-T{w.T}-D{w.D}"
+# The gradient modes each workload is defined with: the timed step runs one call
+# of each on the same batch.
+MODES = {"small": ("full", "truncated"), "layer": ("full",), "long": ("truncated",),
+         "slice": ("full", "truncated"), "vlong": ("truncated",)}
+
+
+def workload_tag(w, chunk=0):
+    return f"{w.name}-b{w.b}-T{w.T}-D{w.D}" + (f"-L{chunk}" if chunk else "")
+
+
+def workload_text(w, modes):
+    kind = ("one selective diagonal SSM layer with input projections and SiLU gate" if w.proj
+            else "one selective diagonal SSM scan (per-layer gradients only, no projections)")
+    dm = f", d_model={w.d_model}" if w.proj else ""
+    call = "ssm_layer_grad" if w.proj else "ssm_adjoint_grad"
+    what = " and one ".join(f"truncated (tbar={w.tbar})" if m == "truncated" else "full" for m in modes)
+    return (f"{w.name}: {kind}, b={w.b}, T={w.T}{dm}, D={w.D}, N={w.N}; each step one {what} {call} call "
+            f"on the same batch")
 
 
 def rooflines(kt, w, layer, tag=None):
@@ -365,7 +381,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--workload", default=HEADLINE, help="workload of the timed step (default: slice)")
+    ap.add_argument("--workload", default=HEADLINE,
+                    help="workload of the timed step (default: slice); the step runs the gradient modes the "
+                         "workload is defined with (see MODES)")
+    ap.add_argument("--chunk", type=int, default=0, help="carry chunk of the timed step (0: the library default)")
+    ap.add_argument("--quick", action="store_true",
+                    help="only the warmup and the timed steps (for profiler runs): no per-mode, spread or "
+                         "graph timings")
     ap.add_argument("--copy-calib", action="store_true",
                     help="first run a plain 256 MiB device copy (torch copy_) three times, as the known-size "
                          "reference for HBM traffic counters")
@@ -391,37 +413,39 @@ def main():
     w = WORKLOADS[args.workload]
     tbar = w.tbar
     inp = make_inputs(w, device="cuda")
-    desc = ssm.make_desc(inp["x"], w.N, True, True, 0, False, False)
-    ws = torch.empty(max(ssm.layer_workspace_size(desc, 0, w.d_model), ssm.layer_workspace_size(desc, tbar, w.d_model)),
-                     dtype=torch.uint8, device="cuda")
-    full = layer_step(w, inp, ssm, torch, tbar=0, ws=ws)
-    trunc = layer_step(w, inp, ssm, torch, tbar=tbar, ws=ws)
+    calls = {}
+    for mode in MODES[w.name]:
+        tb = tbar if mode == "truncated" else 0
+        if w.proj:
+            calls[mode] = layer_step(w, inp, ssm, torch, tbar=tb, chunk=args.chunk)
+        else:
+            calls[mode] = scan_step(w, inp, ssm, torch, tbar=tb, chunk=args.chunk)
 
     def step():
-        full()
-        trunc()
+        for fn in calls.values():
+            fn()
 
-    print(f"bench: {w.name} workload, warmup", file=sys.stderr, flush=True)
+    print(f"bench: {w.name} workload ({', '.join(calls)}), warmup", file=sys.stderr, flush=True)
     ms, ktimes = _timed_kernels(step, args.steps, args.warmup, ssm, torch)
     print(f"bench: {w.name} timed {args.steps} steps, {ms:.3f} ms/step", file=sys.stderr, flush=True)
-    ms_plain = _timed(step, args.steps, 1, torch)
-    ms_full = _timed(full, args.steps, 1, torch)
-    ms_trunc = _timed(trunc, args.steps, 1, torch)
-    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
-    reps = 10
-    spread_warm = _timed_each(step, reps, 1, torch)
-    spread_cold = _timed_each(step, reps, 1, torch, flush=lambda: scratch.fill_(1))
-    del scratch
-    tag = workload_tag(w)
-    roofs = rooflines(ktimes, w, True, tag)
+    tag = workload_tag(w, args.chunk)
+    roofs = rooflines(ktimes, w, w.proj, tag)
     dom = max(roofs, key=lambda k: ktimes[k]["ms_per_step"])
-    value = 2 * w.M / (ms * 1e-3)
-    modes = {"full": {"ms": ms_full, "tokens_per_s": w.M / (ms_full * 1e-3)},
-             "truncated": {"ms": ms_trunc, "tokens_per_s": w.M / (ms_trunc * 1e-3), "tbar": tbar}}
-    extra = {"ms_per_step_without_kernel_events": ms_plain, "ms_per_step_warm": spread_warm,
-             "ms_per_step_cold": spread_cold, "kernels": ktimes,
-             "roofline_other": {k: v for k, v in roofs.items() if k != dom}}
-    del inp, full, trunc, ws
+    value = len(calls) * w.M / (ms * 1e-3)
+    extra = {"kernels": ktimes, "roofline_other": {k: v for k, v in roofs.items() if k != dom}}
+    modes = {}
+    if not args.quick:
+        extra["ms_per_step_without_kernel_events"] = _timed(step, args.steps, 1, torch)
+        for mode, fn in calls.items():
+            m = _timed(fn, args.steps, 1, torch)
+            modes[mode] = {"ms": m, "tokens_per_s": w.M / (m * 1e-3)}
+            if mode == "truncated":
+                modes[mode]["tbar"] = tbar
+        scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        extra["ms_per_step_warm"] = _timed_each(step, 10, 1, torch)
+        extra["ms_per_step_cold"] = _timed_each(step, 10, 1, torch, flush=lambda: scratch.fill_(1))
+        del scratch
+    del inp, calls
     torch.cuda.empty_cache()
 
     if not args.no_extra:
@@ -502,18 +526,16 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16-in/fp32-acc",
+        "dtype": "bf16-in/fp32-acc" if w.bf16 else "fp32",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: one selective diagonal SSM layer with input projections and SiLU gate, "
-                               f"b={w.b}, T={w.T}, d_model={w.d_model}, D={w.D}, N={w.N}; each step one full and one "
-                               f"truncated (tbar={tbar}) ssm_layer_grad call on the same batch",
-                   "batch": w.b, "seq_len": w.T, "d_model": w.d_model, "channels": w.D, "dstate": w.N,
-                   "tbar": tbar, "inputs": "bf16", "accumulate": "fp32", "chunk": "default (128)",
-                   "tokens_per_step": 2 * w.M},
+        "config": {"workload": workload_text(w, list(MODES[w.name])),
+                   "batch": w.b, "seq_len": w.T, "d_model": w.d_model if w.proj else None, "channels": w.D,
+                   "dstate": w.N, "tbar": tbar, "inputs": "bf16" if w.bf16 else "fp32", "accumulate": "fp32",
+                   "chunk": args.chunk or "default (128)", "tokens_per_step": len(MODES[w.name]) * w.M},
         "modes": modes,
         "roofline": roofs[dom],
     }
-    if not args.no_cpu:
+    if not args.no_cpu and w.proj:
         print("bench: cpu baseline", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(w)
     line["extra"] = extra
