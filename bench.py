@@ -185,6 +185,31 @@ def scan_step(w, inp, ssm, torch, tbar=0, b_delta=False, pairs=False, chunk=0):
     return step
 
 
+def un_bytes_per_token(N, P):
+    """Compulsory HBM bytes per token (sequence step) of the unstructured SSM's
+    gradient call, fp32: reads A_t, B_t, C_t, x_t, dy_t; writes dA_t, dB_t, dC_t, dx_t."""
+    return 4 * (2 * N * N + 4 * N * P + 3 * P)
+
+
+def un_step(b, T, P, tbar, ssm, torch, chunk=0):
+    """One gradient call of the unstructured SSM (Table 1, 16 states) on seeded inputs."""
+    from paper_2501_00692_amd.synth import make_unstructured_inputs
+    inp = make_unstructured_inputs(b, T, P, 692210, device="cuda")
+    out = {"dA": torch.empty_like(inp["A"]), "dB": torch.empty_like(inp["B"]), "dC": torch.empty_like(inp["C"]),
+           "dx": torch.empty_like(inp["x"])}
+    desc = ssm.SsmDesc(b, T, P, 16, chunk, ssm.SSM_F32, 0)
+    import ctypes
+    n = ctypes.c_size_t()
+    mode = ssm.SSM_TRUNCATED if tbar > 0 else ssm.SSM_FULL
+    ssm.load_library().ssm_unstructured_grad_workspace_size(ctypes.byref(desc), mode, int(tbar), ctypes.byref(n))
+    ws = torch.empty(max(n.value, 1), dtype=torch.uint8, device="cuda")
+
+    def step():
+        ssm.ssm_unstructured_grad(inp["A"], inp["B"], inp["C"], inp["x"], inp["dy"], tbar=tbar, chunk=chunk, out=out,
+                                  workspace=ws)
+    return step
+
+
 def forward_bytes_per_token(D, N, s, gate):
     """Compulsory HBM bytes per token of the forward: reads x, Delta (and z), B, C;
     writes y (input dtype)."""
@@ -374,6 +399,38 @@ def cpu_baseline(w, T_all=8192, T_one=1024, ch_one=512):
             "cpu_model": _cpu_model(), "nproc": os.cpu_count(), "legs": legs}
 
 
+def unstructured_measure(ssm, torch, steps, warmup, chunk=0):
+    """Full and truncated gradient of the unstructured SSM workload: per-call
+    time, tokens/s, per-kernel times and the whole call's HBM fraction by
+    compulsory bytes."""
+    from paper_2501_00692_amd.synth import UN_WORKLOADS
+    b, T, P, tbar = UN_WORKLOADS["unstructured"]
+    res = {"config": f"b={b}, T={T}, P={P} channels, N=16 states, fp32, tbar={tbar}"}
+    for mode, tb in (("full", 0), ("truncated", tbar)):
+        st = un_step(b, T, P, tb, ssm, torch, chunk)
+        m, kt = _timed_kernels(st, steps, warmup, ssm, torch)
+        bpt = un_bytes_per_token(16, P)
+        res[mode] = {"ms": m, "tokens_per_s": b * T / (m * 1e-3), "bytes_per_token": bpt,
+                     "hbm_frac_call": bpt * b * T / (m * 1e-3) / (HBM_PEAK_GBS * 1e9),
+                     "kernels_ms": {k: v["avg_ms"] for k, v in kt.items()}}
+        del st
+        torch.cuda.empty_cache()
+    return res
+
+
+def unstructured_line(args, ssm, torch):
+    """The JSON line of ``--workload unstructured`` (for profiling that variant)."""
+    r = unstructured_measure(ssm, torch, args.steps, args.warmup, args.chunk)
+    ms = r["full"]["ms"] + r["truncated"]["ms"]
+    return {"metric": "SSM-layer adjoint-gradient tokens/sec (full & truncated Tbar); % HBM/MFMA peak",
+            "value": 2 * 8 * 16384 / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "fp32", "data": "synthetic",
+            "config": {"workload": "unstructured SSM of Table 1 (16 states shared by 64 channels, per-step matrices), "
+                                   + r["config"] + "; each step one full and one truncated ssm_unstructured_grad call"},
+            "extra": r}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -410,6 +467,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.workload == "unstructured":
+        print(json.dumps(unstructured_line(args, ssm, torch)), flush=True)
+        return
     w = WORKLOADS[args.workload]
     tbar = w.tbar
     inp = make_inputs(w, device="cuda")
@@ -484,6 +544,9 @@ def main():
                 (f"/{variant}" if variant else "")] = entry
             del x, st
             torch.cuda.empty_cache()
+        # the unstructured SSM of Table 1
+        print("bench: extra unstructured", file=sys.stderr, flush=True)
+        res["unstructured"] = unstructured_measure(ssm, torch, 5, 2)
         # the forward alone (y only), reported beside the gradients
         fwd = {}
         for name in ("layer", "long"):

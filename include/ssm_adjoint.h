@@ -176,6 +176,28 @@ ssm_status ssm_adjoint_grad_pairs(const ssm_desc* desc, int32_t mode, int64_t tb
                                   float* dh0, float* da_debug, void* workspace, size_t workspace_bytes,
                                   void* stream);
 
+/* Adjoint gradient of the unstructured SSM of Table 1 (Sec. 4.5): the general
+ * SSM of Sec. 3.1 with a 16-dimensional state shared by the P channels and
+ * full per-step matrices (the outputs of the A, B, C networks, taken as given):
+ *   h_t = A_t h_{t-1} + B_t x_t,   y_t = C_t h_t,   L = sum_{b,t} <dy_t, y_t>,
+ *   A [b][T][16][16], B [b][T][16][P], C [b][T][P][16], x, dy [b][T][P] (fp32,
+ *   row-major), h0 [b][16] or NULL (zero).
+ * desc: batch, seqlen, channels = P (a multiple of 16, at most 4096), dstate = 16,
+ * chunk (0: 64; 16..256), in_dtype SSM_F32, flags 0 (SSM_ERR_UNSUPPORTED otherwise).
+ * Outputs (fp32, overwritten): dA_t = mu_t h_{t-1}^T [b][T][16][16], dB_t = mu_t x_t^T
+ * [b][T][16][P], dC_t = dy_t h_t^T [b][T][P][16] (never truncated), dx_t = B_t^T mu_t
+ * [b][T][P], dh0 = A_0^T mu_0 [b][16] (full mode only, or NULL); mu is the state
+ * cotangent mu_t = C_t^T dy_t + A_{t+1}^T mu_{t+1}, or with SSM_TRUNCATED the
+ * windowed adjoint of Eq. "capped", sum_{t=i}^{i+tbar-1} (A_{i+1}^T ... A_t^T) C_t^T dy_t.
+ * The chunk transition products A_e ... A_s are 16x16x16 products on fp32 MFMA.
+ * Tensor pointers 16-byte aligned; workspace from the size query. */
+ssm_status ssm_unstructured_grad_workspace_size(const ssm_desc* desc, int32_t mode, int64_t tbar,
+                                                size_t* bytes);
+ssm_status ssm_unstructured_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, const float* A,
+                                 const float* B, const float* C, const float* x, const float* h0,
+                                 const float* dy, float* dA, float* dB, float* dC, float* dx,
+                                 float* dh0, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Projection gradients of a linear map Z = X W (Sec. 4.5: the A, B, C networks
  * are single-layer maps; the per-step vjps summed over t give these products):
  *   dW [K][Nout] (fp32)  = X^T dZ      (skipped if dW == NULL)

@@ -100,4 +100,27 @@ def un_adjoint_sum(A, B, C, x, dy, tbar=0, h0=None, want_dh0=None):
     return out
 
 
-__all__ = ["un_forward", "un_bptt", "un_adjoint_sum"]
+def un_trunc_at(A, B, C, x, dy, tbar, steps, h0=None):
+    """Eq. "capped" at the given steps i only (sequence b, step i pairs): the
+    windowed adjoint mubar_i = sum_{t=i}^{i+tbar-1} lambda^{t,i}, each lambda^{t,i}
+    built from C_t^T dy_t by the transposed decays A_t^T ... A_{i+1}^T, and the
+    vjps dA_i = mubar_i h_{i-1}^T, dB_i = mubar_i x_i^T, dx_i = B_i^T mubar_i.
+    Returns dict of arrays indexed like ``steps``."""
+    A, B, C, x, dy = map(_f64, (A, B, C, x, dy))
+    nb, T, N, P = B.shape
+    _, _, hs = un_forward(A, B, C, x, h0)
+    out = dict(dA=[], dB=[], dx=[])
+    for b, i in steps:
+        mub = np.zeros(N)
+        for t in range(i, min(T, i + tbar)):
+            lam = C[b, t].T @ dy[b, t]
+            for j in range(t, i, -1):  # A_t^T ... A_{i+1}^T, innermost first
+                lam = A[b, j].T @ lam
+            mub += lam
+        out["dA"].append(np.outer(mub, hs[b, i]))
+        out["dB"].append(np.outer(mub, x[b, i]))
+        out["dx"].append(B[b, i].T @ mub)
+    return {k: np.array(v) for k, v in out.items()}
+
+
+__all__ = ["un_forward", "un_bptt", "un_adjoint_sum", "un_trunc_at"]

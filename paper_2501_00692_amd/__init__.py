@@ -10,7 +10,7 @@ built.
 
 Entry points (names as in the C ABI): :func:`ssm_adjoint_forward`,
 :func:`ssm_adjoint_grad`, :func:`ssm_adjoint_grad_noalloc`, :func:`ssm_adjoint_grad_pairs`,
-:func:`ssm_proj_grad`,
+:func:`ssm_unstructured_grad`, :func:`ssm_proj_grad`,
 :func:`ssm_layer_grad`, :func:`ssm_stack_grad`.
 """
 from __future__ import annotations
@@ -36,6 +36,7 @@ EXPORTED = (
     "ssm_adjoint_forward_workspace_size", "ssm_adjoint_grad_workspace_size", "ssm_adjoint_forward",
     "ssm_adjoint_grad", "ssm_adjoint_grad_noalloc", "ssm_adjoint_grad_pairs_workspace_size",
     "ssm_adjoint_grad_pairs",
+    "ssm_unstructured_grad_workspace_size", "ssm_unstructured_grad",
     "ssm_proj_grad_workspace_size", "ssm_proj_grad",
     "ssm_layer_grad_workspace_size", "ssm_layer_grad", "ssm_stack_grad_workspace_size", "ssm_stack_grad",
     "ssm_timing_enable", "ssm_timing_summary",
@@ -78,6 +79,8 @@ def load_library():
         "ssm_adjoint_grad_noalloc": [dp, i32, i64] + [vp] * 16 + [vp],
         "ssm_adjoint_grad_pairs_workspace_size": [dp, i32, i64, szp],
         "ssm_adjoint_grad_pairs": [dp, i32, i64] + [vp] * 16 + [vp, sz, vp],
+        "ssm_unstructured_grad_workspace_size": [dp, i32, i64, szp],
+        "ssm_unstructured_grad": [dp, i32, i64] + [vp] * 11 + [vp, sz, vp],
         "ssm_proj_grad_workspace_size": [i64, i64, i64, u32, szp],
         "ssm_proj_grad": [i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, vp, u32, vp, sz, vp],
         "ssm_layer_grad_workspace_size": [dp, i32, i64, i64, szp],
@@ -291,6 +294,36 @@ def _adjoint_grad(pairs, x, delta, A_log, B, C, dy, h0, z, softplus, tbar, chunk
     ws = workspace if workspace is not None else _workspace(grad_workspace_size(desc, tbar, pairs), dev)
     name = "ssm_adjoint_grad_pairs" if pairs else "ssm_adjoint_grad"
     _check(getattr(lib, name)(*args, _p(ws), ws.numel(), _stream()), name)
+    return o
+
+
+def ssm_unstructured_grad(A, B, C, x, dy, h0=None, tbar=0, chunk=0, want_dh0=False, out=None, workspace=None):
+    """Adjoint gradient of the unstructured SSM (16 states, per-step matrices
+    A [b,T,16,16], B [b,T,16,P], C [b,T,P,16]; x, dy [b,T,P]; fp32).  Returns a dict
+    with ``dA, dB, dC, dx`` (+ ``dh0`` if asked, full mode)."""
+    lib = load_library()
+    b, T, N, P = B.shape
+    f32 = torch.float32
+    _need(A, "A", f32, (b, T, N, N))
+    _need(B, "B", f32)
+    _need(C, "C", f32, (b, T, P, N))
+    _need(x, "x", f32, (b, T, P))
+    _need(dy, "dy", f32, (b, T, P))
+    _need(h0, "h0", f32, (b, N))
+    desc = SsmDesc(b, T, P, N, chunk, SSM_F32, 0)
+    mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
+    n = ctypes.c_size_t()
+    _check(lib.ssm_unstructured_grad_workspace_size(ctypes.byref(desc), mode, int(tbar), ctypes.byref(n)),
+           "ssm_unstructured_grad_workspace_size")
+    ws = workspace if workspace is not None else _workspace(n.value, A.device)
+    o = dict(out) if out else {}
+    for k, t in (("dA", A), ("dB", B), ("dC", C), ("dx", x)):
+        o.setdefault(k, torch.empty_like(t))
+    if want_dh0:
+        o.setdefault("dh0", torch.empty(b, N, dtype=f32, device=A.device))
+    _check(lib.ssm_unstructured_grad(ctypes.byref(desc), mode, int(tbar), _p(A), _p(B), _p(C), _p(x), _p(h0), _p(dy),
+                                     _p(o["dA"]), _p(o["dB"]), _p(o["dC"]), _p(o["dx"]), _p(o.get("dh0")), _p(ws),
+                                     ws.numel(), _stream()), "ssm_unstructured_grad")
     return o
 
 

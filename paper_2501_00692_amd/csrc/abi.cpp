@@ -407,6 +407,88 @@ ssm_status ssm_adjoint_grad_pairs(const ssm_desc* desc, int32_t mode, int64_t tb
     return SSM_OK;
 }
 
+// The unstructured SSM of Table 1: 16 states, P channels (desc->channels), fp32.
+static ssm_status check_unstructured(const ssm_desc* d, int32_t mode, int64_t tbar, int64_t* L, bool* trunc) {
+    if (!d) return fail(SSM_ERR_NULL, "desc is NULL");
+    if (d->batch < 1 || d->seqlen < 1 || d->channels < 1 || d->dstate < 1)
+        return fail(SSM_ERR_SHAPE, "batch, seqlen, channels and dstate must be >= 1");
+    if (d->dstate != 16) return fail(SSM_ERR_UNSUPPORTED, "the unstructured SSM takes dstate = 16 (got %lld)",
+                                     (long long)d->dstate);
+    if (d->channels % 16 || d->channels > 4096)
+        return fail(SSM_ERR_UNSUPPORTED, "channels must be a multiple of 16, at most 4096 (got %lld)",
+                    (long long)d->channels);
+    if (d->in_dtype != SSM_F32) return fail(SSM_ERR_UNSUPPORTED, "the unstructured SSM takes fp32 tensors");
+    if (d->flags) return fail(SSM_ERR_UNSUPPORTED, "no flags apply to the unstructured SSM");
+    const int64_t l = d->chunk == 0 ? 64 : d->chunk;
+    if (!ssmk::chunk_supported(l))
+        return fail(SSM_ERR_UNSUPPORTED, "chunk %lld not in {16, 32, 64, 128, 256}", (long long)d->chunk);
+    if (d->batch > kMaxGridYZ) return fail(SSM_ERR_UNSUPPORTED, "batch exceeds the launch grid");
+    if (d->batch * d->seqlen > (int64_t(1) << 36)) return fail(SSM_ERR_SHAPE, "problem too large");
+    if (mode != SSM_FULL && mode != SSM_TRUNCATED) return fail(SSM_ERR_SHAPE, "unknown mode %d", (int)mode);
+    *trunc = false;
+    if (mode == SSM_TRUNCATED) {
+        if (tbar < 1) return fail(SSM_ERR_SHAPE, "truncated mode needs tbar >= 1 (got %lld)", (long long)tbar);
+        *trunc = tbar < d->seqlen;
+    }
+    *L = l;
+    return SSM_OK;
+}
+
+ssm_status ssm_unstructured_grad_workspace_size(const ssm_desc* desc, int32_t mode, int64_t tbar, size_t* bytes) {
+    int64_t L;
+    bool trunc;
+    ssm_status st = check_unstructured(desc, mode, tbar, &L, &trunc);
+    if (st) return st;
+    if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");
+    *bytes = ssmk::unstructured_workspace(desc->batch, desc->seqlen, L, trunc);
+    return SSM_OK;
+}
+
+ssm_status ssm_unstructured_grad(const ssm_desc* desc, int32_t mode, int64_t tbar, const float* A, const float* B,
+                                 const float* C, const float* x, const float* h0, const float* dy, float* dA,
+                                 float* dB, float* dC, float* dx, float* dh0, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+    int64_t L;
+    bool trunc;
+    ssm_status st = check_unstructured(desc, mode, tbar, &L, &trunc);
+    if (st) return st;
+    REQUIRE_PTR(A, "A");
+    REQUIRE_PTR(B, "B");
+    REQUIRE_PTR(C, "C");
+    REQUIRE_PTR(x, "x");
+    REQUIRE_PTR(dy, "dy");
+    REQUIRE_PTR(dA, "dA");
+    REQUIRE_PTR(dB, "dB");
+    REQUIRE_PTR(dC, "dC");
+    REQUIRE_PTR(dx, "dx");
+    OPTIONAL_PTR(h0, "h0");
+    OPTIONAL_PTR(dh0, "dh0");
+    if (dh0 && trunc) return fail(SSM_ERR_UNSUPPORTED, "dh0 is defined for the full gradient only");
+    st = check_workspace(workspace, workspace_bytes, ssmk::unstructured_workspace(desc->batch, desc->seqlen, L, trunc));
+    if (st) return st;
+    ssmk::UnstructuredProblem u{};
+    u.nb = desc->batch;
+    u.T = desc->seqlen;
+    u.P = desc->channels;
+    u.L = L;
+    u.trunc = trunc;
+    u.tbar = trunc ? tbar : 0;
+    u.A = A;
+    u.B = B;
+    u.C = C;
+    u.x = x;
+    u.h0 = h0;
+    u.dy = dy;
+    u.dA = dA;
+    u.dB = dB;
+    u.dC = dC;
+    u.dx = dx;
+    u.dh0 = dh0;
+    hipError_t e = ssmk::launch_unstructured_grad(u, workspace, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "ssm_unstructured_grad launch");
+    return SSM_OK;
+}
+
 ssm_status ssm_proj_grad_workspace_size(int64_t M, int64_t K, int64_t Nout, uint32_t flags,
                                         size_t* bytes) {
     if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");

@@ -119,6 +119,19 @@ constexpr size_t kNoallocScratchBytes = size_t(64) << 20;
 hipError_t noalloc_scratch(void** ptr);
 hipError_t launch_grad(const ScanProblem& p, hipStream_t s);
 
+// The unstructured SSM of Table 1 (unstructured.hip): 16 states shared by P
+// channels, per-step matrices A [b][T][16][16], B [b][T][16][P], C [b][T][P][16],
+// fp32; chunks of L steps (16..256).
+struct UnstructuredProblem {
+    int64_t nb, T, P, L;
+    bool trunc;
+    int64_t tbar;
+    const float *A, *B, *C, *x, *h0, *dy;
+    float *dA, *dB, *dC, *dx, *dh0;
+};
+size_t unstructured_workspace(int64_t nb, int64_t T, int64_t L, bool trunc);
+hipError_t launch_unstructured_grad(const UnstructuredProblem& u, void* ws, hipStream_t s);
+
 // The layer's reassociated input-projection gradient (layer.hip): dW_in[:, D:2D] =
 // G[:, D:2D] and the bf16 hi/lo split of G[:, 2D:2D+nx] into hi, lo [dm][nx].
 hipError_t launch_layer_split(const float* G, int64_t ldg, int64_t dm, int64_t D, int64_t nx, float* dW_in,

@@ -1,0 +1,358 @@
+// unstructured.hip -- the adjoint gradient of the unstructured SSM of Table 1
+// (gfx950): an N = 16 state shared by the P channels, with per-step matrices
+//   h_t = A_t h_{t-1} + B_t x_t,   y_t = C_t h_t,
+//   A_t [N][N], B_t [N][P], C_t [P][N] (fp32, row-major), L = sum <dy_t, y_t>.
+// Outputs: dA_t = mu_t h_{t-1}^T, dB_t = mu_t x_t^T, dx_t = B_t^T mu_t,
+// dC_t = dy_t h_t^T (never truncated), dh0 = A_0^T mu_0 (full mode), where mu is
+// the state cotangent mu_t = C_t^T dy_t + A_{t+1}^T mu_{t+1} (Prop. 1, summed over
+// the loss terms as in Prop. 2), or in truncated mode the windowed adjoint of
+// Eq. "capped", mubar_i = sum_{t=i}^{i+tbar-1} (A_{i+1}^T ... A_t^T) C_t^T dy_t.
+//
+// The state is tiny (16 values per sequence), so the parallelism comes from
+// time: the sequence is cut into chunks of L steps, one wave per chunk.
+//   k_un_aggr  : per chunk, the transition product Phi_c = A_e ... A_s (16x16x16
+//                products on fp32 MFMA), the local end state from zero, the
+//                local adjoint aggregate sum_t (A_t ... A_s)^T v_t and the
+//                readout cotangents v_t = C_t^T dy_t of every step;
+//   k_un_carry : per sequence, the chunk carries H_{c+1} = Phi_c H_c + hloc_c
+//                and M_{c-1} = Phi_c^T M_c + mloc_c, in order;
+//   k_un_window: truncated mode, the windowed adjoints mubar_i by Horner's rule
+//                over each window (four windows per wave);
+//   k_un_grad  : per chunk, the states recomputed from the carry (kept in LDS),
+//                then the reverse sweep (or the windowed adjoints) and the vjps.
+// Lane layout of a wave: lane l = 16 q + i; i indexes a row of the 16 x 16
+// matrices, q one of four quarters of the reduction (matrix columns 4q..4q+3,
+// or a quarter of the P channels), summed across quarters with two xor
+// shuffles.  Vectors of 16 are kept replicated in all four quarters.
+#include "internal.h"
+
+namespace ssmk {
+namespace {
+
+constexpr int UN = 16;  // state size
+
+// Sum over the four quarters of the wave (lanes i, i+16, i+32, i+48).
+__device__ __forceinline__ float qsum(float v) {
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    return v;
+}
+
+struct UnArgs {
+    int64_t nb, T, P, L, nc, tbar;
+    int trunc;
+    const float* A;   // [b][T][16][16]
+    const float* B;   // [b][T][16][P]
+    const float* C;   // [b][T][P][16]
+    const float* x;   // [b][T][P]
+    const float* h0;  // [b][16] or null
+    const float* dy;  // [b][T][P]
+    float* dA;
+    float* dB;
+    float* dC;
+    float* dx;
+    float* dh0;       // [b][16] or null (full mode)
+    float* h_last;    // [b][16] or null
+    // workspace
+    float* phi;       // [b][nc][16][16]
+    float* hc;        // [b][nc][16]: local end state, then the carry into the chunk
+    float* mc;        // [b][nc][16]: local adjoint aggregate, then the carry from the right
+    float* v;         // [b][T][16]: C_t^T dy_t
+    float* mub;       // [b][T][16]: windowed adjoints (truncated mode)
+};
+
+// partial over lane (q, i) of row i of B_t x_t (channels [q P/4, (q+1) P/4))
+__device__ __forceinline__ float bx_part(const float* Bt, const float* xt, int64_t P, int q, int i) {
+    const int64_t p0 = q * (P / 4), n = P / 4;
+    const float* br = Bt + i * P + p0;
+    const float* xr = xt + p0;
+    float s = 0.f;
+    for (int64_t p = 0; p < n; p += 4) {
+        const float4 b4 = *reinterpret_cast<const float4*>(br + p);
+        const float4 x4 = *reinterpret_cast<const float4*>(xr + p);
+        s = fmaf(b4.x, x4.x, s);
+        s = fmaf(b4.y, x4.y, s);
+        s = fmaf(b4.z, x4.z, s);
+        s = fmaf(b4.w, x4.w, s);
+    }
+    return s;
+}
+
+// partial over lane (q, i) of (C_t^T dy_t)[i] (channels [q P/4, (q+1) P/4))
+__device__ __forceinline__ float cty_part(const float* Ct, const float* dyt, int64_t P, int q, int i) {
+    const int64_t p0 = q * (P / 4), n = P / 4;
+    float s = 0.f;
+    for (int64_t p = 0; p < n; ++p) s = fmaf(Ct[(p0 + p) * UN + i], dyt[p0 + p], s);
+    return s;
+}
+
+// grid (nc, b), 64 threads
+__global__ __launch_bounds__(64) void k_un_aggr(const UnArgs a) {
+    __shared__ float sphi[UN][UN + 1];
+    __shared__ float sh[UN];
+    __shared__ float sv[UN];
+    const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
+    const int64_t c = blockIdx.x, bb = blockIdx.y;
+    const int64_t s0 = c * a.L, s1 = min(s0 + a.L, a.T);
+    // Phi in the MFMA output layout: lane (q, i) holds Phi[4q + r][i], r = 0..3
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    f4 phi;
+    for (int r = 0; r < 4; ++r) phi[r] = (4 * q + r == i) ? 1.f : 0.f;
+    float h = 0.f, m = 0.f;  // replicated: lane (q, i) holds h[i], m[i]
+    if (q == 0) sh[i] = 0.f;
+    __syncthreads();
+    for (int64_t t = s0; t < s1; ++t) {
+        const int64_t row = bb * a.T + t;
+        const float* At = a.A + row * UN * UN;
+        // h <- A_t h + B_t x_t
+        const float4 a4 = *reinterpret_cast<const float4*>(At + i * UN + 4 * q);
+        float part = a4.x * sh[4 * q] + a4.y * sh[4 * q + 1] + a4.z * sh[4 * q + 2] + a4.w * sh[4 * q + 3];
+        part += bx_part(a.B + row * UN * a.P, a.x + row * a.P, a.P, q, i);
+        h = qsum(part);
+        // Phi <- A_t Phi: B operands from the transposed staging of Phi
+        for (int r = 0; r < 4; ++r) sphi[4 * q + r][i] = phi[r];
+        __syncthreads();
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int kb = 0; kb < 4; ++kb) {
+            const float av = At[i * UN + 4 * kb + q];  // A_t[i][4kb + q]
+            const float bv = sphi[4 * kb + q][i];      // Phi[4kb + q][i]
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
+        }
+        phi = acc;
+        // v_t = C_t^T dy_t, and the adjoint aggregate m += Phi_t^T v_t
+        const float vt = qsum(cty_part(a.C + row * a.P * UN, a.dy + row * a.P, a.P, q, i));
+        if (q == 0) a.v[row * UN + i] = vt;
+        __syncthreads();  // every read of sphi and sh of this step is done
+        if (q == 0) {
+            sh[i] = h;
+            sv[i] = vt;
+        }
+        __syncthreads();
+        if (!a.trunc) {
+            // lane (q, j): sum_r Phi[4q + r][j] v[4q + r]
+            float pm = 0.f;
+            for (int r = 0; r < 4; ++r) pm = fmaf(phi[r], sv[4 * q + r], pm);
+            m += qsum(pm);
+        }
+    }
+    const int64_t cb = bb * a.nc + c;
+    for (int r = 0; r < 4; ++r) a.phi[cb * UN * UN + (4 * q + r) * UN + i] = phi[r];
+    if (q == 0) {
+        a.hc[cb * UN + i] = h;
+        a.mc[cb * UN + i] = m;
+    }
+}
+
+// grid (b), 64 threads: lanes (q, i) as above; directions one after the other
+__global__ __launch_bounds__(64) void k_un_carry(const UnArgs a) {
+    __shared__ float sv[UN];
+    const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
+    const int64_t bb = blockIdx.x;
+    float H = a.h0 ? a.h0[bb * UN + i] : 0.f;
+    if (q == 0) sv[i] = H;
+    __syncthreads();
+    for (int64_t c = 0; c < a.nc; ++c) {
+        const int64_t cb = bb * a.nc + c;
+        const float* P = a.phi + cb * UN * UN;
+        // H_{c+1} = Phi_c H_c + hloc_c  (lane (q, i): columns 4q..4q+3 of row i)
+        float part = 0.f;
+        for (int r = 0; r < 4; ++r) part = fmaf(P[i * UN + 4 * q + r], sv[4 * q + r], part);
+        const float Hn = qsum(part) + a.hc[cb * UN + i];
+        __syncthreads();
+        if (q == 0) {
+            a.hc[cb * UN + i] = sv[i];  // the carry into chunk c
+            sv[i] = Hn;
+        }
+        __syncthreads();
+    }
+    if (a.h_last && q == 0) a.h_last[bb * UN + i] = sv[i];
+    if (a.trunc) return;
+    __syncthreads();
+    if (q == 0) sv[i] = 0.f;
+    __syncthreads();
+    for (int64_t c = a.nc - 1; c >= 0; --c) {
+        const int64_t cb = bb * a.nc + c;
+        const float* P = a.phi + cb * UN * UN;
+        // M_{c-1} = Phi_c^T M_c + mloc_c  (lane (q, j): rows 4q..4q+3 of column j)
+        float part = 0.f;
+        for (int r = 0; r < 4; ++r) part = fmaf(P[(4 * q + r) * UN + i], sv[4 * q + r], part);
+        const float Mn = qsum(part) + a.mc[cb * UN + i];
+        __syncthreads();
+        if (q == 0) {
+            a.mc[cb * UN + i] = sv[i];  // the carry from the right into chunk c
+            sv[i] = Mn;
+        }
+        __syncthreads();
+    }
+    if (a.dh0 && q == 0) a.dh0[bb * UN + i] = sv[i];
+}
+
+// grid (ceil(T / 4), b), 64 threads: lane (w, j) holds component j of window
+// i = 4 blockIdx.x + w; Horner from the window's last step back to i.
+__global__ __launch_bounds__(64) void k_un_window(const UnArgs a) {
+    __shared__ float su[4][UN];
+    const int lane = threadIdx.x, j = lane & 15, w = lane >> 4;
+    const int64_t bb = blockIdx.y;
+    const int64_t i0 = static_cast<int64_t>(blockIdx.x) * 4;
+    const int64_t iw = i0 + w;
+    const bool valid = iw < a.T;
+    const int64_t e = valid ? min(iw + a.tbar - 1, a.T - 1) : 0;
+    // the windows of a wave have different lengths near the end: every lane runs
+    // the longest one, with the steps outside its own window leaving u unchanged
+    const int64_t emax = min(i0 + 3 + a.tbar - 1, a.T - 1);
+    float u = 0.f;
+    for (int64_t t = emax; t >= i0; --t) {
+        // u <- v_t + A_{t+1}^T u inside the window (t in [iw, e]); A_{t+1}^T u is
+        // zero at the window's last step
+        su[w][j] = u;
+        __syncthreads();
+        float nu = 0.f;
+        if (t < e) {
+            const float* An = a.A + (bb * a.T + t + 1) * UN * UN;
+            for (int k = 0; k < UN; ++k) nu = fmaf(An[k * UN + j], su[w][k], nu);
+        }
+        const bool in = valid && t >= iw && t <= e;
+        if (in) u = a.v[(bb * a.T + t) * UN + j] + nu;
+        __syncthreads();
+    }
+    if (valid) a.mub[(bb * a.T + iw) * UN + j] = u;
+}
+
+// grid (nc, b), 64 threads; LDS holds the chunk's states h_{s-1} .. h_e.
+template <int L>
+__global__ __launch_bounds__(64) void k_un_grad(const UnArgs a) {
+    __shared__ float shs[L + 1][UN];
+    __shared__ float smu[UN];
+    const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
+    const int64_t c = blockIdx.x, bb = blockIdx.y;
+    const int64_t s0 = c * L, s1 = min(s0 + L, a.T);
+    const int64_t cb = bb * a.nc + c;
+    const int64_t P = a.P;
+    if (q == 0) shs[0][i] = a.hc[cb * UN + i];
+    __syncthreads();
+    for (int64_t t = s0; t < s1; ++t) {
+        const int64_t row = bb * a.T + t;
+        const float* At = a.A + row * UN * UN;
+        const int k = static_cast<int>(t - s0);
+        const float4 a4 = *reinterpret_cast<const float4*>(At + i * UN + 4 * q);
+        float part = a4.x * shs[k][4 * q] + a4.y * shs[k][4 * q + 1] + a4.z * shs[k][4 * q + 2] +
+                     a4.w * shs[k][4 * q + 3];
+        part += bx_part(a.B + row * UN * P, a.x + row * P, P, q, i);
+        const float hn = qsum(part);
+        if (q == 0) shs[k + 1][i] = hn;
+        __syncthreads();
+    }
+    float mun = a.trunc ? 0.f : a.mc[cb * UN + i];  // A_{t+1}^T mu_{t+1} (replicated)
+    for (int64_t t = s1 - 1; t >= s0; --t) {
+        const int64_t row = bb * a.T + t;
+        const int k = static_cast<int>(t - s0);
+        const float mu = a.trunc ? a.mub[row * UN + i] : a.v[row * UN + i] + mun;
+        if (q == 0) smu[i] = mu;
+        __syncthreads();
+        // dA_t[r][4(l%4) .. +3] = mu[r] h_{t-1}[..], r = l / 4
+        {
+            const int r = lane >> 2, c4 = (lane & 3) * 4;
+            const float m = smu[r];
+            const float4 hv = make_float4(shs[k][c4] * m, shs[k][c4 + 1] * m, shs[k][c4 + 2] * m,
+                                          shs[k][c4 + 3] * m);
+            *reinterpret_cast<float4*>(a.dA + row * UN * UN + r * UN + c4) = hv;
+        }
+        // dB_t[r][p] = mu[r] x_t[p]; dC_t[p][r] = dy_t[p] h_t[r]; four values per lane and pass
+        const float* xt = a.x + row * P;
+        const float* dyt = a.dy + row * P;
+        for (int64_t e = 4 * lane; e < UN * P; e += 256) {
+            const int64_t r = e / P, p = e % P;
+            const float m = smu[r];
+            const float4 x4 = *reinterpret_cast<const float4*>(xt + p);
+            *reinterpret_cast<float4*>(a.dB + row * UN * P + e) = make_float4(m * x4.x, m * x4.y, m * x4.z, m * x4.w);
+            const int64_t pc = e / UN, rc = e % UN;
+            const float g = dyt[pc];
+            *reinterpret_cast<float4*>(a.dC + row * P * UN + e) =
+                make_float4(g * shs[k + 1][rc], g * shs[k + 1][rc + 1], g * shs[k + 1][rc + 2], g * shs[k + 1][rc + 3]);
+        }
+        // dx_t[p] = sum_r B_t[r][p] mu[r]
+        const float* Bt = a.B + row * UN * P;
+        for (int64_t p = lane; p < P; p += 64) {
+            float sx = 0.f;
+            for (int r = 0; r < UN; ++r) sx = fmaf(Bt[r * P + p], smu[r], sx);
+            a.dx[row * P + p] = sx;
+        }
+        // A_t^T mu for the step before (lane (q, j): rows 4q..4q+3 of column j)
+        if (!a.trunc) {
+            const float* At = a.A + row * UN * UN;
+            float part = 0.f;
+            for (int r = 0; r < 4; ++r) part = fmaf(At[(4 * q + r) * UN + i], smu[4 * q + r], part);
+            mun = qsum(part);
+        }
+        __syncthreads();
+    }
+}
+
+}  // namespace
+
+size_t unstructured_workspace(int64_t nb, int64_t T, int64_t L, bool trunc) {
+    const int64_t nc = (T + L - 1) / L;
+    auto up = [](size_t v) { return (v + 255) & ~size_t(255); };
+    size_t s = up(size_t(nb * nc) * UN * UN * 4) + 2 * up(size_t(nb * nc) * UN * 4) + up(size_t(nb * T) * UN * 4);
+    if (trunc) s += up(size_t(nb * T) * UN * 4);
+    return s;
+}
+
+hipError_t launch_unstructured_grad(const UnstructuredProblem& u, void* ws, hipStream_t s) {
+    UnArgs a{};
+    a.nb = u.nb;
+    a.T = u.T;
+    a.P = u.P;
+    a.L = u.L;
+    a.nc = (u.T + u.L - 1) / u.L;
+    a.trunc = u.trunc ? 1 : 0;
+    a.tbar = u.tbar;
+    a.A = u.A;
+    a.B = u.B;
+    a.C = u.C;
+    a.x = u.x;
+    a.h0 = u.h0;
+    a.dy = u.dy;
+    a.dA = u.dA;
+    a.dB = u.dB;
+    a.dC = u.dC;
+    a.dx = u.dx;
+    a.dh0 = u.dh0;
+    a.h_last = nullptr;
+    auto up = [](size_t v) { return (v + 255) & ~size_t(255); };
+    char* w = static_cast<char*>(ws);
+    a.phi = reinterpret_cast<float*>(w);
+    w += up(size_t(a.nb * a.nc) * UN * UN * 4);
+    a.hc = reinterpret_cast<float*>(w);
+    w += up(size_t(a.nb * a.nc) * UN * 4);
+    a.mc = reinterpret_cast<float*>(w);
+    w += up(size_t(a.nb * a.nc) * UN * 4);
+    a.v = reinterpret_cast<float*>(w);
+    w += up(size_t(a.nb * a.T) * UN * 4);
+    a.mub = u.trunc ? reinterpret_cast<float*>(w) : nullptr;
+    const dim3 gc(static_cast<unsigned>(a.nc), static_cast<unsigned>(a.nb));
+    {
+        SSMK_TIMED("un_aggr", s);
+        hipLaunchKernelGGL(k_un_aggr, gc, dim3(64), 0, s, a);
+    }
+    {
+        SSMK_TIMED("un_carry", s);
+        hipLaunchKernelGGL(k_un_carry, dim3(static_cast<unsigned>(a.nb)), dim3(64), 0, s, a);
+    }
+    if (a.trunc) {
+        SSMK_TIMED("un_window", s);
+        hipLaunchKernelGGL(k_un_window, dim3(static_cast<unsigned>((a.T + 3) / 4), static_cast<unsigned>(a.nb)),
+                           dim3(64), 0, s, a);
+    }
+    SSMK_TIMED("un_grad", s);
+    switch (a.L) {
+        case 16: hipLaunchKernelGGL(k_un_grad<16>, gc, dim3(64), 0, s, a); break;
+        case 32: hipLaunchKernelGGL(k_un_grad<32>, gc, dim3(64), 0, s, a); break;
+        case 64: hipLaunchKernelGGL(k_un_grad<64>, gc, dim3(64), 0, s, a); break;
+        case 128: hipLaunchKernelGGL(k_un_grad<128>, gc, dim3(64), 0, s, a); break;
+        default: hipLaunchKernelGGL(k_un_grad<256>, gc, dim3(64), 0, s, a); break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace ssmk

@@ -128,3 +128,31 @@ def make_stack_inputs(K: int, b: int, T: int, D: int, N: int, seed: int, device=
     A_log = [torch.rand(D, N, generator=g, **f32) * math.log(16.0) for _ in range(K)]
     gK = torch.randn(b, T, D, generator=g, **f32)
     return dict(y0=y0, W_in=W_in, W_x=W_x, A_log=A_log, gK=gK)
+
+
+# The unstructured SSM of Table 1 (16 states shared by P channels, per-step
+# matrices): (b, T, P, tbar).  "unstructured" is the measured workload.
+UN_WORKLOADS = {
+    "un_small": (2, 300, 32, 64),
+    "unstructured": (8, 16384, 64, 256),
+}
+
+
+def make_unstructured_inputs(b: int, T: int, P: int, seed: int, N: int = 16, device="cpu", h0: bool = False):
+    """Per-step matrices and inputs of the unstructured SSM, fp32: A_t with
+    entries N(0, 0.81/N) (a random transition of spectral radius about 0.9, so
+    the state neither grows nor vanishes over long sequences), B_t ~ N(0, 1/P),
+    C_t ~ N(0, 1/N), x, dy ~ N(0, 1), and h0 ~ N(0, 1) when asked."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    f32 = dict(dtype=torch.float32, device=device)
+    out = {
+        "A": torch.randn(b, T, N, N, generator=g, **f32).mul_(0.9 / math.sqrt(N)),
+        "B": torch.randn(b, T, N, P, generator=g, **f32).mul_(1.0 / math.sqrt(P)),
+        "C": torch.randn(b, T, P, N, generator=g, **f32).mul_(1.0 / math.sqrt(N)),
+        "x": torch.randn(b, T, P, generator=g, **f32),
+        "dy": torch.randn(b, T, P, generator=g, **f32),
+    }
+    if h0:
+        out["h0"] = torch.randn(b, N, generator=g, **f32)
+    return out

@@ -1,0 +1,93 @@
+"""GPU parity of the unstructured SSM of Table 1 (ssm_unstructured_grad: 16
+states shared by P channels, per-step N x N, N x P and P x N matrices, chunk
+transition products on fp32 MFMA) against the fp64 oracle in
+oracle/unstructured.py, whose pins are in tests/test_oracle_unstructured.py."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2501_00692_amd as ssm
+from oracle.unstructured import un_adjoint_sum, un_bptt, un_trunc_at
+from paper_2501_00692_amd.synth import UN_WORKLOADS, make_unstructured_inputs
+
+from gpu_helpers import TOL_F32, check, say, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _host(inp):
+    return {k: to_np(v) for k, v in inp.items()}
+
+
+def _gpu(inp, tbar, chunk=0, want_dh0=False):
+    o = ssm.ssm_unstructured_grad(inp["A"], inp["B"], inp["C"], inp["x"], inp["dy"], h0=inp.get("h0"), tbar=tbar,
+                                  chunk=chunk, want_dh0=want_dh0)
+    torch.cuda.synchronize()
+    return o
+
+
+@pytest.mark.parametrize("chunk", [16, 64, 256])
+def test_unstructured_small_full(chunk):
+    """b = 2, T = 300 (a ragged last chunk), P = 32, with h0 and dh0."""
+    b, T, P, _ = UN_WORKLOADS["un_small"]
+    say(f"[unstructured full] b={b} T={T} P={P} chunk={chunk}")
+    inp = make_unstructured_inputs(b, T, P, 692200, device="cuda", h0=True)
+    o = _gpu(inp, 0, chunk, want_dh0=True)
+    h = _host(inp)
+    ref = un_bptt(h["A"], h["B"], h["C"], h["x"], h["dy"], h["h0"])
+    rep = {}
+    for k in ("dA", "dB", "dC", "dx", "dh0"):
+        check(k, to_np(o[k]), ref[k], TOL_F32, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
+@pytest.mark.parametrize("tbar", [1, 17, 64, 100, 299])
+def test_unstructured_small_truncated_literal(tbar):
+    """Against the literal double sum of Eq. "capped"."""
+    b, T, P, _ = UN_WORKLOADS["un_small"]
+    say(f"[unstructured truncated] tbar={tbar}")
+    inp = make_unstructured_inputs(b, T, P, 692201, device="cuda", h0=True)
+    o = _gpu(inp, tbar, 64)
+    h = _host(inp)
+    ref = un_adjoint_sum(h["A"], h["B"], h["C"], h["x"], h["dy"], tbar=tbar, h0=h["h0"])
+    rep = {}
+    for k in ("dA", "dB", "dC", "dx"):
+        check(k, to_np(o[k]), ref[k], TOL_F32, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
+def test_unstructured_workload_full_every_entry():
+    """b = 8, T = 16,384, P = 64, N = 16 (chunks of 64): every output."""
+    b, T, P, _ = UN_WORKLOADS["unstructured"]
+    say(f"[unstructured workload full] b={b} T={T} P={P}")
+    inp = make_unstructured_inputs(b, T, P, 692202, device="cuda")
+    o = _gpu(inp, 0, want_dh0=True)
+    h = _host(inp)
+    ref = un_bptt(h["A"], h["B"], h["C"], h["x"], h["dy"])
+    rep = {}
+    for k in ("dA", "dB", "dC", "dx", "dh0"):
+        check(k, to_np(o[k]), ref[k], TOL_F32, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
+def test_unstructured_workload_truncated_sampled():
+    """The same shape, truncated (tbar = 256): dC everywhere (never truncated,
+    equal to the full gradient's) and the A-, B- and x-path vjps at sampled
+    steps (sequence edges, window edges and random ones) against the literal
+    window sums."""
+    b, T, P, tbar = UN_WORKLOADS["unstructured"]
+    say(f"[unstructured workload truncated] b={b} T={T} P={P} tbar={tbar}")
+    inp = make_unstructured_inputs(b, T, P, 692203, device="cuda")
+    o = _gpu(inp, tbar)
+    h = _host(inp)
+    rep = {}
+    full = un_bptt(h["A"], h["B"], h["C"], h["x"], h["dy"], want_dh0=False)
+    check("dC", to_np(o["dC"]), full["dC"], TOL_F32, rep)
+    rng = np.random.default_rng(9)
+    steps = [(0, 0), (b - 1, T - 1), (1, T - tbar), (2, T - tbar - 1), (3, tbar)]
+    steps += [(int(rng.integers(b)), int(rng.integers(T))) for _ in range(27)]
+    ref = un_trunc_at(h["A"], h["B"], h["C"], h["x"], h["dy"], tbar, steps)
+    bi = np.array([s[0] for s in steps]), np.array([s[1] for s in steps])
+    for k in ("dA", "dB", "dx"):
+        check(f"{k}[sampled]", to_np(o[k])[bi], ref[k], TOL_F32, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))

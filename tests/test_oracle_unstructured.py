@@ -8,7 +8,7 @@ import pytest
 import torch
 
 import oracle
-from oracle.unstructured import un_adjoint_sum, un_bptt, un_forward
+from oracle.unstructured import un_adjoint_sum, un_bptt, un_forward, un_trunc_at
 
 
 def _inputs(rng, nb=2, T=6, N=3, P=2, h0=True, scale=0.6):
@@ -157,3 +157,17 @@ def test_diagonal_special_case_equals_diagonal_layer(rng, tbar):
     assert _relerr(un["dB"][..., 0], dg["dB"]) < 1e-12
     assert _relerr(un["dC"][:, :, 0, :], dg["dC"]) < 1e-12
     assert _relerr(un["dA"][:, :, idx, idx], dg["da"][:, :, 0, :]) < 1e-12
+
+
+def test_sampled_truncated_steps_equal_double_sum(rng):
+    """un_trunc_at (the window sum at chosen steps, for the long workloads) equals
+    the full double sum at those steps."""
+    inp = _inputs(rng, nb=2, T=20, N=4, P=3)
+    args = (inp["A"], inp["B"], inp["C"], inp["x"], inp["dy"])
+    for tbar in (1, 5, 30):
+        full = un_adjoint_sum(*args, tbar=tbar, h0=inp["h0"], want_dh0=False)
+        steps = [(0, 0), (1, 7), (0, 19), (1, 15)]
+        got = un_trunc_at(*args, tbar=tbar, steps=steps, h0=inp["h0"])
+        for k in ("dA", "dB", "dx"):
+            ref = np.array([full[k][b, i] for b, i in steps])
+            assert _relerr(got[k], ref) < 1e-12, (tbar, k)
