@@ -21,7 +21,10 @@
 // outside the matrix (rows, columns, or the reduction tail) read as zero through
 // the buffer range check.  Workgroup: 512 threads = 4x2 waves, two per SIMD;
 // a wave owns a 64 x (BN/2) block of 32x32 MFMA tiles; tile 256 x BN with BN 128
-// or 192 (and 256 for dW, whose epilogue leaves the registers for it).
+// or 192.  dW's 256 x 256 tiles run on a kernel of their own (k_gemm_dw4): 256
+// threads, one wave per SIMD owning a 128 x 128 block with its accumulators in
+// the AGPRs, a five-stage ring (160 KB of LDS), one barrier per step and the
+// MFMAs interleaved one by one with the fragment reads and stage loads.
 // Output tiles and reduction splits are assigned so that each XCD runs one
 // contiguous run of (split, tile) (consecutive workgroups go to different XCDs),
 // tiles ordered in groups of four row blocks, so that the tiles one XCD runs at
@@ -58,22 +61,27 @@ __shared__ __attribute__((aligned(1024))) uint16_t sB0[kMaxW * BK];
 __shared__ __attribute__((aligned(1024))) uint16_t sB1[kMaxW * BK];
 __shared__ __attribute__((aligned(1024))) uint16_t sB2[kMaxW * BK];
 __shared__ __attribute__((aligned(1024))) uint16_t sB3[kMaxW * BK];
+// a fifth stage, used by the four-wave dW kernel only (160 KB of LDS in all)
+__shared__ __attribute__((aligned(1024))) uint16_t sA4[BM * BK];
+__shared__ __attribute__((aligned(1024))) uint16_t sB4[kMaxW * BK];
 
 template <int S>
 __device__ __forceinline__ uint16_t* stage_a() {
-    static_assert(S >= 0 && S < NS, "stage");
+    static_assert(S >= 0 && S <= NS, "stage");
     if constexpr (S == 0) return sA0;
     else if constexpr (S == 1) return sA1;
     else if constexpr (S == 2) return sA2;
-    else return sA3;
+    else if constexpr (S == 3) return sA3;
+    else return sA4;
 }
 template <int S>
 __device__ __forceinline__ uint16_t* stage_b() {
-    static_assert(S >= 0 && S < NS, "stage");
+    static_assert(S >= 0 && S <= NS, "stage");
     if constexpr (S == 0) return sB0;
     else if constexpr (S == 1) return sB1;
     else if constexpr (S == 2) return sB2;
-    else return sB3;
+    else if constexpr (S == 3) return sB3;
+    else return sB4;
 }
 template <int S>
 using Stage = std::integral_constant<int, S>;
@@ -546,6 +554,203 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmLaunch gl) {
     else by_mask(std::false_type{});
 }
 
+// The dW form with four waves, one per SIMD, each owning a 128 x 128 block of
+// the 256 x 256 tile (4 x 4 MFMA tiles, 256 accumulator registers): per 32-step
+// stage the waves read 64 KB of fragments from LDS instead of the 96 KB that
+// eight 64 x 128 blocks read.  Operand staging as in ColMajorOps (four wave
+// loads of A and four of B per wave and stage).  Schedule as the dX form's: one
+// barrier per step; a step's second-half fragments are read while its first half
+// of MFMAs runs, and the next step's first-half fragments while its second half
+// runs.
+struct ColMajorOps4 {
+    static constexpr int W = 256;  // LDS row of both operands (values)
+    const uint16_t* A;
+    const uint16_t* B;
+    int64_t lda, ldb, k_hi;
+    uint32_t oa[4], ob[4];
+    int fa[2][4][2], fb[2][4][2];
+
+    __device__ __forceinline__ void init(const GemmArgs& g, int64_t r0, int64_t c0, int64_t khi, int wave,
+                                         int lane, int wr, int wc) {
+        A = g.A;
+        B = g.B;
+        lda = g.lda;
+        ldb = g.ldb;
+        k_hi = khi;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int byte = (wave + 4 * i) * 1024 + lane * 16;
+            const int row = byte / (W * 2), col = ((byte % (W * 2)) / 16 ^ ColMajorOps<256>::swz(row)) * 8;
+            oa[i] = r0 + col < g.R ? static_cast<uint32_t>((row * g.lda + r0 + col) * 2) : kOutOfRange;
+            ob[i] = c0 + col < g.Cc ? static_cast<uint32_t>((row * g.ldb + c0 + col) * 2) : kOutOfRange;
+        }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    fa[ks][i][h] = ColMajorOps<256>::chunk(W, ks * 16, h, wr + i * 32, lane);
+                    fb[ks][i][h] = ColMajorOps<256>::chunk(W, ks * 16, h, wc + i * 32, lane);
+                }
+    }
+    template <int S>
+    __device__ __forceinline__ void issue(Stage<S>, int64_t k, int wave) const {
+        const int64_t rows = min<int64_t>(BK, k_hi - k);
+        const __amdgpu_buffer_rsrc_t ra = rsrc(A + k * lda, rows * lda * 2);
+        const __amdgpu_buffer_rsrc_t rb = rsrc(B + k * ldb, rows * ldb * 2);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) load_lds16(ra, oa[i], stage_a<S>() + (wave + 4 * i) * 512);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) load_lds16(rb, ob[i], stage_b<S>() + (wave + 4 * i) * 512);
+    }
+    template <int S>
+    __device__ __forceinline__ void read(Stage<S>, int ks, bf16x8 (&a)[4], bf16x8 (&b)[4]) const {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a[i] = ColMajorOps<256>::frag(stage_a<S>(), fa[ks][i]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) b[j] = ColMajorOps<256>::frag(stage_b<S>(), fb[ks][j]);
+    }
+};
+
+template <int NST>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gemm_dw4(const GemmLaunch gl) {
+    constexpr int MI = 4, NJ = 4, BN = 256;
+    static_assert(NST == 4 || NST == 5, "stages");
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // tile and split of this workgroup: the same XCD-contiguous map and grouped
+    // tile order as k_gemm
+    const int nwg = static_cast<int>(gridDim.x);
+    const int lin = static_cast<int>(blockIdx.x);
+    const int xq = nwg / kXcds, xr = nwg % kXcds, xcd = lin % kXcds;
+    const int logical = (xcd < xr ? xcd * (xq + 1) : xr * (xq + 1) + (xcd - xr) * xq) + lin / kXcds;
+    const int tile_all = logical % gl.tiles, split = logical / gl.tiles;
+    const int q = __builtin_amdgcn_readfirstlane(tile_all >= gl.tiles0 ? 1 : 0);
+    const GemmArgs g = q ? gl.p[1] : gl.p[0];
+    const int tile = tile_all - (q ? gl.tiles0 : 0);
+    const int ncb = gl.cb[q];
+    const int nrb = (q ? gl.tiles - gl.tiles0 : gl.tiles0) / ncb;
+    const int grp = tile / (kGroupRows * ncb), first = grp * kGroupRows;
+    const int gh = min(kGroupRows, nrb - first), within = tile - grp * kGroupRows * ncb;
+    const int64_t r0 = static_cast<int64_t>(first + within % gh) * BM;
+    const int64_t c0 = static_cast<int64_t>(within / gh) * BN;
+    const int64_t k_lo = static_cast<int64_t>(split) * g.kper;
+    const int64_t k_hi = min(g.Kr, k_lo + g.kper);
+    const int wr = (wave >> 1) * 128;
+    const int wc = (wave & 1) * 128;
+    const int64_t nsteps = k_hi > k_lo ? (k_hi - k_lo + BK - 1) / BK : 0;
+
+    ColMajorOps4 ops;
+    ops.init(g, r0, c0, k_hi, wave, lane, wr, wc);
+    f32x16 acc[MI][NJ];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+    typedef bf16x8 FA[MI];
+    typedef bf16x8 FB[NJ];
+    auto mm = [&](const FA& a, const FB& b) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    auto read_any = [&](int s, int ks, FA& a, FB& b) __attribute__((always_inline)) {
+        switch (s) {
+            case 0: ops.read(Stage<0>{}, ks, a, b); break;
+            case 1: ops.read(Stage<1>{}, ks, a, b); break;
+            case 2: ops.read(Stage<2>{}, ks, a, b); break;
+            case 3: ops.read(Stage<3>{}, ks, a, b); break;
+            default: ops.read(Stage<(NST > 4 ? 4 : 3)>{}, ks, a, b); break;
+        }
+    };
+    constexpr int PER = 8;  // wave loads per stage
+    // the first NST - 1 stages
+    if (nsteps > 0) ops.issue(Stage<0>{}, k_lo, wave);
+    if (nsteps > 1) ops.issue(Stage<1>{}, k_lo + BK, wave);
+    if (nsteps > 2) ops.issue(Stage<2>{}, k_lo + 2 * BK, wave);
+    if constexpr (NST == 5)
+        if (nsteps > 3) ops.issue(Stage<3>{}, k_lo + 3 * BK, wave);
+    const int64_t steady = nsteps >= NST - 1 ? nsteps - (NST - 1) : 0;
+    if (steady > 0) wait_vm<PER * (NST - 2)>();
+    else wait_vm<0>();
+    ring_barrier();
+    FA a0, a1;
+    FB b0, b1;
+    if (nsteps > 0) ops.read(Stage<0>{}, 0, a0, b0);
+    // MFMAs interleaved with the fragment reads (and the stage loads) of the
+    // other half step, one read or load between consecutive MFMAs, so that the
+    // matrix pipe is not left idle while they issue
+    auto interleave = [&](auto Loads) __attribute__((always_inline)) {
+        constexpr int NL = decltype(Loads)::value;
+#pragma unroll
+        for (int k = 0; k < MI * NJ; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // one MFMA
+            if (k < NL) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one stage load
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // one fragment read
+        }
+    };
+    auto step = [&](auto St, int64_t t) __attribute__((always_inline)) {
+        constexpr int S = decltype(St)::value;
+        ops.read(St, 1, a1, b1);
+        mm(a0, b0);
+        interleave(std::integral_constant<int, 0>{});
+        wait_vm<PER * (NST - 3)>();  // step t+1's loads, every wave
+        ring_barrier();
+        ops.issue(Stage<(S + NST - 1) % NST>{}, k_lo + (t + NST - 1) * BK, wave);
+        ops.read(Stage<(S + 1) % NST>{}, 0, a0, b0);
+        mm(a1, b1);
+        interleave(std::integral_constant<int, PER>{});
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    int64_t t = 0;
+    for (; t + NST <= steady; t += NST) {
+        step(Stage<0>{}, t);
+        step(Stage<1>{}, t + 1);
+        step(Stage<2>{}, t + 2);
+        step(Stage<3>{}, t + 3);
+        if constexpr (NST == 5) step(Stage<(NST > 4 ? 4 : 3)>{}, t + 4);
+    }
+    const int64_t rem = steady - t;
+    if (rem > 0) step(Stage<0>{}, t);
+    if (rem > 1) step(Stage<1>{}, t + 1);
+    if (rem > 2) step(Stage<2>{}, t + 2);
+    if constexpr (NST == 5)
+        if (rem > 3) step(Stage<3>{}, t + 3);
+    if (steady > 0 && steady < nsteps) {
+        wait_vm<0>();
+        ring_barrier();
+    }
+    for (int64_t u = steady; u < nsteps; ++u) {
+        const int s = static_cast<int>(u % NST);
+        read_any(s, 1, a1, b1);
+        mm(a0, b0);
+        if (u + 1 < nsteps) read_any(s + 1 == NST ? 0 : s + 1, 0, a0, b0);
+        mm(a1, b1);
+    }
+
+    float* dst = g.C + (g.direct ? 0 : static_cast<int64_t>(split) * g.R * g.Cc);
+    const bool accum = g.direct && g.accum;
+    const bool full = r0 + BM <= g.R && c0 + BN <= g.Cc;
+    const int64_t ldc = g.direct ? g.ldc : g.Cc;
+    auto store = [&](auto Ft, auto At) __attribute__((always_inline)) {
+        store_tile<false, decltype(At)::value, true, false, decltype(Ft)::value>(
+            acc, dst, ldc, nullptr, 0, nullptr, 0, g.R, g.Cc, r0 + wr, c0 + wc, lane);
+    };
+    if (full) {
+        if (accum) store(std::true_type{}, std::true_type{});
+        else store(std::true_type{}, std::false_type{});
+    } else {
+        if (accum) store(std::false_type{}, std::true_type{});
+        else store(std::false_type{}, std::false_type{});
+    }
+}
+
 // Second stage of a split GEMM: result = sum over splits (in split order) +
 // (add) (+ the existing C if accum), the same combination as the single-pass
 // epilogue, written to C (if given) and/or as bf16 into out16 (row stride ld16).
@@ -621,7 +826,8 @@ constexpr int64_t kMaxWgs = (int64_t(1) << 23) - 1;
 // Output-tile width and reduction splits for the outputs R_q x Cc_q of one launch
 // (one or two products) with reduction Kr, from a simple time model: rounds of 256
 // workgroups x the time of one workgroup's share (per 32-step stage at full
-// load, measured: 0.57 us for 128 columns, 0.80 for 192, 0.92 for 256), plus the
+// load, measured: 0.57 us for 128 columns, 0.80 for 192, 0.84 for 256 on the
+// four-wave dW kernel), plus the
 // HBM time of writing and re-reading the split partials (4 TB/s).  256-column
 // tiles only for dW (the dX form's epilogue needs the registers).
 struct Plan {
@@ -633,7 +839,7 @@ Plan plan_gemm(int np, const int64_t* R, const int64_t* Cc, int64_t Kr, bool all
     Plan best{192, 1};
     double best_us = 1e300;
     const int bns[3] = {192, 128, 256};
-    const double step_us[3] = {0.80, 0.57, 0.92};
+    const double step_us[3] = {0.80, 0.57, 0.84};
     double out = 0.0;  // output elements of all products
     for (int q = 0; q < np; ++q) out += static_cast<double>(R[q]) * static_cast<double>(Cc[q]);
     for (int b = 0; b < 3; ++b) {
@@ -660,8 +866,17 @@ Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split, bool tr) {
     return plan_gemm(1, &R, &Cc, Kr, allow_split, tr);
 }
 
+// The dW form's 256-column tiles run on the four-wave kernel with kDwStages stages.
+constexpr bool kDwFourWaves = true;
+constexpr int kDwStages = 5;
+
 template <bool TR, int BN>
 void launch_tile(const GemmLaunch& gl, int splits, hipStream_t s) {
+    if constexpr (TR && BN == 256 && kDwFourWaves) {
+        hipLaunchKernelGGL(k_gemm_dw4<kDwStages>, dim3(static_cast<unsigned>(gl.tiles * splits)), dim3(256), 0, s,
+                           gl);
+        return;
+    }
     hipLaunchKernelGGL((k_gemm<TR, BN>), dim3(static_cast<unsigned>(gl.tiles * splits)), dim3(512), 0, s, gl);
 }
 
