@@ -258,8 +258,7 @@ hipError_t pairs_impl(const ScanProblem& p, float* dl, float* g, float* mu, int6
     }
     {
         SSMK_TIMED("carry", s);
-        hipLaunchKernelGGL(k_carry, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N), static_cast<unsigned>(2 * p.nb)),
-                           dim3(256), 0, s, p);
+        hipLaunchKernelGGL(k_carry, carry_grid(p), dim3(256), 0, s, p);
     }
     {
         SSMK_TIMED("pairs", s);

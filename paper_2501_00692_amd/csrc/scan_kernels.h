@@ -441,80 +441,99 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 }
 
 // ---------------------------------------------------------------------------
-// k_carry: grid (ceil(D/256), N, 2b), 256 threads; blockIdx.z = 2*bb + dir.
+// k_carry: 256 threads (4 waves); a unit is (sequence bb, direction, block of 64
+// channels), a workgroup takes one unit and 4 of its states (wave w: state
+// 4q + w, lane: channel).  The carries are sequential over chunks:
 // dir 0: H_c = state before chunk c: H_0 = h0, H_{c+1} = Pc H_c + hloc_c, with
 //        Pc = prod over the chunk of a = 2^{cn sdel_c}; hbuf := H_c; h_last.
-//        Thread n == 0 also writes the exclusive prefix sums of sdel (psum).
+//        State 0 also writes the exclusive prefix sums of sdel (psum).
 // dir 1: M_c = a_{e_c+1} mu_{e_c+1}: M_{nc-1} = 0, M_{c-1} = mloc_c + Pc M_c;
 //        mbuf := M_c; dh0 = M_{-1}.
+// The walk is bound by memory latency: each wave keeps the loads of the next
+// kCarryU chunks in flight while it consumes the current kCarryU (two register
+// buffers used alternately).  The workgroups of one unit run on one XCD
+// (workgroups are dealt to the XCDs in turn by linear id), so the four waves of
+// a workgroup and the workgroups of the unit's other states read each chunk's
+// Delta sums through one L2.
 // ---------------------------------------------------------------------------
+constexpr int kCarryU = 16;
+
 __global__ __launch_bounds__(256) void k_carry(const ScanProblem p) {
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t nd64 = (p.D + 63) / 64;
+    const int64_t nunits = 2 * p.nb * nd64;
+    const int nq = static_cast<int>((p.N + 3) / 4);
+    const int lin = static_cast<int>(blockIdx.x);
+    const int64_t slot = lin / 8;
+    const int64_t unit = lin % 8 + 8 * (slot / nq);
+    if (unit >= nunits) return;
+    const int64_t n = 4 * (slot % nq) + (threadIdx.x >> 6);
+    if (n >= p.N) return;
+    const int64_t d = (unit % nd64) * 64 + (threadIdx.x & 63);
     if (d >= p.D) return;
-    const int64_t n = blockIdx.y;
-    const int64_t bb = blockIdx.z >> 1;
-    const int dir = blockIdx.z & 1;
+    const int dir = static_cast<int>((unit / nd64) & 1);
+    const int64_t bb = unit / nd64 / 2;
     const float cn = -__expf(p.A_log[p.ascalar ? d : d * p.N + n]) * kLog2e;
     const int64_t st = p.N * p.D;
     const int64_t base = (bb * p.nc * p.N + n) * p.D + d;
     const int64_t sbase = bb * p.nc * p.D + d;
-    constexpr int U = 8;
-    if (dir == 0) {
-        float H = p.h0 ? p.h0[(bb * p.D + d) * p.N + n] : 0.f;
-        const bool wps = (p.psum != nullptr) && n == 0;
-        const int64_t pbase = bb * (p.nc + 1) * p.D + d;
-        double ps = 0.0;
-        for (int64_t c0 = 0; c0 < p.nc; c0 += U) {
-            float hl[U];
-            double sd[U];
+    const int64_t nc = p.nc;
+    constexpr int U = kCarryU;
+    float* buf = dir == 0 ? p.hbuf : p.mbuf;
+    if (dir == 1 && !buf) return;
+    // block k covers chunks kU .. kU+U-1 in walk order (dir 1 walks backwards);
+    // positions past the end load a valid chunk and are not used
+    auto chunk = [&](int64_t k, int j) { const int64_t i = k * U + j; return dir == 0 ? i : nc - 1 - i; };
+    auto load = [&](int64_t k, float (&v)[U], double (&sd)[U]) __attribute__((always_inline)) {
 #pragma unroll
-            for (int j = 0; j < U; ++j) {
-                const int64_t c = c0 + j;
-                if (c < p.nc) {
-                    hl[j] = p.hbuf[base + c * st];
-                    sd[j] = p.sdel[sbase + c * p.D];
-                }
-            }
+        for (int j = 0; j < U; ++j) {
+            const int64_t c = min(max<int64_t>(chunk(k, j), 0), nc - 1);
+            v[j] = buf[base + c * st];
+            sd[j] = p.sdel[sbase + c * p.D];
+        }
+    };
+    float V = 0.f;  // H (dir 0) or M (dir 1)
+    if (dir == 0 && p.h0) V = p.h0[(bb * p.D + d) * p.N + n];
+    const bool wps = dir == 0 && p.psum != nullptr && n == 0;
+    const int64_t pbase = bb * (nc + 1) * p.D + d;
+    double ps = 0.0;
+    auto consume = [&](int64_t k, const float (&v)[U], const double (&sd)[U]) __attribute__((always_inline)) {
 #pragma unroll
-            for (int j = 0; j < U; ++j) {
-                const int64_t c = c0 + j;
-                if (c < p.nc) {
-                    p.hbuf[base + c * st] = H;
-                    H = fmaf(fexp2(cn * static_cast<float>(sd[j])), H, hl[j]);
-                    if (wps) {
-                        p.psum[pbase + c * p.D] = ps;
-                        ps += sd[j];
-                    }
+        for (int j = 0; j < U; ++j) {
+            const int64_t i = k * U + j;
+            if (i < nc) {
+                const int64_t c = chunk(k, j);
+                buf[base + c * st] = V;
+                V = fmaf(fexp2(cn * static_cast<float>(sd[j])), V, v[j]);
+                if (wps) {
+                    p.psum[pbase + c * p.D] = ps;
+                    ps += sd[j];
                 }
             }
         }
-        if (wps) p.psum[pbase + p.nc * p.D] = ps;
-        if (p.h_last) p.h_last[(bb * p.D + d) * p.N + n] = H;
-    } else {
-        if (!p.mbuf) return;
-        float M = 0.f;
-        for (int64_t c0 = p.nc - 1; c0 >= 0; c0 -= U) {
-            float ml[U];
-            double sd[U];
-#pragma unroll
-            for (int j = 0; j < U; ++j) {
-                const int64_t c = c0 - j;
-                if (c >= 0) {
-                    ml[j] = p.mbuf[base + c * st];
-                    sd[j] = p.sdel[sbase + c * p.D];
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < U; ++j) {
-                const int64_t c = c0 - j;
-                if (c >= 0) {
-                    p.mbuf[base + c * st] = M;
-                    M = fmaf(fexp2(cn * static_cast<float>(sd[j])), M, ml[j]);
-                }
-            }
-        }
-        if (p.dh0) p.dh0[(bb * p.D + d) * p.N + n] = M;
+    };
+    const int64_t nblk = (nc + U - 1) / U;
+    float va[U], vb[U];
+    double sa[U], sb[U];
+    load(0, va, sa);
+    for (int64_t k = 0; k < nblk; k += 2) {
+        load(k + 1, vb, sb);
+        consume(k, va, sa);
+        if (k + 1 >= nblk) break;
+        load(k + 2, va, sa);
+        consume(k + 1, vb, sb);
     }
+    if (dir == 0) {
+        if (wps) p.psum[pbase + nc * p.D] = ps;
+        if (p.h_last) p.h_last[(bb * p.D + d) * p.N + n] = V;
+    } else if (p.dh0) {
+        p.dh0[(bb * p.D + d) * p.N + n] = V;
+    }
+}
+
+// Grid of k_carry: 8 x (units per XCD) x (groups of 4 states).
+inline dim3 carry_grid(const ScanProblem& p) {
+    const int64_t nunits = 2 * p.nb * ((p.D + 63) / 64);
+    return dim3(static_cast<unsigned>(8 * ((nunits + 7) / 8) * ((p.N + 3) / 4)));
 }
 
 // ---------------------------------------------------------------------------
@@ -1345,9 +1364,7 @@ hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
     }
     {
         SSMK_TIMED("carry", s);
-        hipLaunchKernelGGL(k_carry, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N),
-                                         static_cast<unsigned>(2 * p.nb)),
-                           dim3(256), 0, s, p);
+        hipLaunchKernelGGL(k_carry, carry_grid(p), dim3(256), 0, s, p);
     }
     SSMK_TIMED("forward", s);
     hipLaunchKernelGGL((k_forward<TI, SP, GATE>), g4, dim3(256), 0, s, p);
@@ -1389,9 +1406,7 @@ hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
     }
     {
         SSMK_TIMED("carry", s);
-        hipLaunchKernelGGL(k_carry, dim3(cdiv(p.D, 256), static_cast<unsigned>(p.N),
-                                         static_cast<unsigned>(2 * p.nb)),
-                           dim3(256), 0, s, p);
+        hipLaunchKernelGGL(k_carry, carry_grid(p), dim3(256), 0, s, p);
     }
     switch (p.L) {
         case 16: grad_main<TI, SP, GATE, TRUNC, N16, 8, 2>(p, s); break;
