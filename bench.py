@@ -418,6 +418,36 @@ def unstructured_measure(ssm, torch, steps, warmup, chunk=0):
     return res
 
 
+def head_measure(ssm, torch, steps, warmup):
+    """The language head with its loss at the head workload: per-call time,
+    tokens/s, the MFMA fraction of its three products (logits, dU, dOmega:
+    3 x 2 M P V flops) and the per-kernel split."""
+    import ctypes
+
+    from paper_2501_00692_amd.synth import HEAD_WORKLOADS, make_head_inputs
+    M, P, V = HEAD_WORKLOADS["head"]
+    inp = make_head_inputs(M, P, V, 692310, device="cuda")
+    out = {"loss": torch.empty(M, dtype=torch.float32, device="cuda"),
+           "dy": torch.empty(M, P, dtype=torch.float32, device="cuda"),
+           "domega": torch.empty(V, P, dtype=torch.float32, device="cuda")}
+    n = ctypes.c_size_t()
+    ssm.load_library().ssm_lm_head_grad_workspace_size(M, P, V, ssm.SSM_HEAD_NORM, 0, ctypes.byref(n))
+    ws = torch.empty(n.value, dtype=torch.uint8, device="cuda")
+
+    def step():
+        ssm.ssm_lm_head_grad(inp["y"], inp["omega"], inp["targets"], out=out, workspace=ws)
+
+    m, kt = _timed_kernels(step, steps, warmup, ssm, torch)
+    flops = 3 * 2 * M * P * V
+    res = {"config": f"M={M} tokens, P={P}, V={V}, RMS-normalised input, bf16 products, fp32 accumulation",
+           "ms": m, "tokens_per_s": M / (m * 1e-3), "tflops": flops / (m * 1e-3) / 1e12,
+           "mfma_frac_call": flops / (m * 1e-3) / (MFMA_BF16_PEAK_TFS * 1e12),
+           "kernels_ms": {k: v["ms_per_step"] for k, v in kt.items()}}
+    del inp, out, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def unstructured_line(args, ssm, torch):
     """The JSON line of ``--workload unstructured`` (for profiling that variant)."""
     r = unstructured_measure(ssm, torch, args.steps, args.warmup, args.chunk)
@@ -547,6 +577,9 @@ def main():
         # the unstructured SSM of Table 1
         print("bench: extra unstructured", file=sys.stderr, flush=True)
         res["unstructured"] = unstructured_measure(ssm, torch, 5, 2)
+        # the language head of Sec. 3.2 with the cross-entropy loss
+        print("bench: extra head", file=sys.stderr, flush=True)
+        res["head"] = head_measure(ssm, torch, 5, 2)
         # the forward alone (y only), reported beside the gradients
         fwd = {}
         for name in ("layer", "long"):

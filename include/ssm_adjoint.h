@@ -288,6 +288,32 @@ ssm_status ssm_stack_grad(const ssm_desc* desc, int64_t K, int32_t grad, int32_t
                           float* const* dW_x, float* const* dA_log, float* yK, void* workspace,
                           size_t workspace_bytes, void* stream);
 
+/* The language head of Sec. 3.2 with its loss, the first gradient step of Alg. 1:
+ * the prediction o^t = Omega Norm(y^t) (SSM_HEAD_NORM; flags 0 gives
+ * o^t = Omega y^t, as Alg. 1 writes it), the per-token cross-entropy
+ * l^t = log sum_v exp(o^t_v) - o^t_{target_t} (the paper leaves l open), and
+ * the gradients dy = dl/dy (the upstream g_K that ssm_stack_grad takes) and
+ * dOmega.  Norm is the stack's root-mean-square normalisation.
+ *   M rows (tokens), P width, V vocabulary: P and V multiples of 8, at most 2^20;
+ *             M below 2^31.
+ *   y       : fp32 [M][P];  omega : bf16 [V][P];
+ *   targets : int32 [M]; a negative target marks a token without a loss (l = 0,
+ *             no gradient), a target >= V gives l = NaN and no gradient;
+ *   loss    : fp32 [M];  dy : fp32 [M][P];  domega : fp32 [V][P], or NULL to skip it.
+ *   block_rows : rows per block (a multiple of 256), or 0 for as many as keep the
+ *             block's fp32 logits within 1 GiB; the workspace (which also holds
+ *             Omega^T in bf16) grows with it.  Norm(y) and the logit gradients enter the
+ * products as bf16 (round to nearest even) with fp32 accumulation; the
+ * normalisation's backward recomputes Norm(y) in fp32; dOmega adds the blocks in
+ * order.  SSM_ERR_UNSUPPORTED for P or V not a multiple of 8. */
+#define SSM_HEAD_NORM 1u
+ssm_status ssm_lm_head_grad_workspace_size(int64_t M, int64_t P, int64_t V, uint32_t flags, int64_t block_rows,
+                                           size_t* bytes);
+ssm_status ssm_lm_head_grad(int64_t M, int64_t P, int64_t V, uint32_t flags, int64_t block_rows, const float* y,
+                            const void* omega,
+                            const int32_t* targets, float* loss, float* dy, float* domega, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -11,7 +11,7 @@ built.
 Entry points (names as in the C ABI): :func:`ssm_adjoint_forward`,
 :func:`ssm_adjoint_grad`, :func:`ssm_adjoint_grad_noalloc`, :func:`ssm_adjoint_grad_pairs`,
 :func:`ssm_unstructured_grad`, :func:`ssm_proj_grad`,
-:func:`ssm_layer_grad`, :func:`ssm_stack_grad`.
+:func:`ssm_layer_grad`, :func:`ssm_stack_grad`, :func:`ssm_lm_head_grad`.
 """
 from __future__ import annotations
 
@@ -28,6 +28,7 @@ SSM_FULL, SSM_TRUNCATED = 0, 1
 SSM_DELTA_SOFTPLUS, SSM_GATE_SILU, SSM_A_SCALAR, SSM_B_DELTA = 1, 2, 4, 8
 SSM_ACCUM_DW, SSM_ACCUM_DX = 1, 2
 SSM_STACK_ADJOINT, SSM_STACK_EXACT = 0, 1
+SSM_HEAD_NORM = 1
 
 STATUS = {0: "SSM_OK", 1: "SSM_ERR_NULL", 2: "SSM_ERR_SHAPE", 3: "SSM_ERR_DTYPE",
           4: "SSM_ERR_UNSUPPORTED", 5: "SSM_ERR_WORKSPACE", 6: "SSM_ERR_ALIGN", 7: "SSM_ERR_HIP"}
@@ -39,6 +40,7 @@ EXPORTED = (
     "ssm_unstructured_grad_workspace_size", "ssm_unstructured_grad",
     "ssm_proj_grad_workspace_size", "ssm_proj_grad",
     "ssm_layer_grad_workspace_size", "ssm_layer_grad", "ssm_stack_grad_workspace_size", "ssm_stack_grad",
+    "ssm_lm_head_grad_workspace_size", "ssm_lm_head_grad",
     "ssm_timing_enable", "ssm_timing_summary",
     "ssm_last_error",
 )
@@ -87,6 +89,8 @@ def load_library():
         "ssm_layer_grad": [dp, i32, i64, i64] + [vp] * 20 + [vp, sz, vp],
         "ssm_stack_grad_workspace_size": [dp, i64, i32, i32, i64, szp],
         "ssm_stack_grad": [dp, i64, i32, i32, i64] + [vp] * 9 + [vp, sz, vp],
+        "ssm_lm_head_grad_workspace_size": [i64, i64, i64, u32, i64, szp],
+        "ssm_lm_head_grad": [i64, i64, i64, u32, i64] + [vp] * 6 + [vp, sz, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -449,4 +453,29 @@ def ssm_stack_grad(y0, W_in, W_x, A_log, gK, N, exact=False, tbar=0, chunk=0, wa
                                                                                     for a in keep[:3]],
                               _p(gK), *[ctypes.cast(a, ctypes.c_void_p) for a in keep[3:]], _p(o.get("yK")), _p(ws),
                               ws.numel(), _stream()), "ssm_stack_grad")
+    return o
+
+
+def ssm_lm_head_grad(y, omega, targets, norm=True, want_domega=True, block_rows=0, out=None, workspace=None):
+    """Language head with the cross-entropy loss: y fp32 [M, P], omega bf16
+    [V, P], targets int32 [M] (negative: no loss).  Returns a dict with ``loss``
+    [M], ``dy`` [M, P] and (if asked) ``domega`` [V, P], all fp32."""
+    lib = load_library()
+    M, P = y.shape
+    V = omega.shape[0]
+    _need(y, "y", torch.float32, (M, P))
+    _need(omega, "omega", torch.bfloat16, (V, P))
+    _need(targets, "targets", torch.int32, (M,))
+    flags = SSM_HEAD_NORM if norm else 0
+    n = ctypes.c_size_t()
+    _check(lib.ssm_lm_head_grad_workspace_size(M, P, V, flags, int(block_rows), ctypes.byref(n)),
+           "ssm_lm_head_grad_workspace_size")
+    ws = workspace if workspace is not None else _workspace(n.value, y.device)
+    o = dict(out) if out else {}
+    o.setdefault("loss", torch.empty(M, dtype=torch.float32, device=y.device))
+    o.setdefault("dy", torch.empty(M, P, dtype=torch.float32, device=y.device))
+    if want_domega:
+        o.setdefault("domega", torch.empty(V, P, dtype=torch.float32, device=y.device))
+    _check(lib.ssm_lm_head_grad(M, P, V, flags, int(block_rows), _p(y), _p(omega), _p(targets), _p(o["loss"]), _p(o["dy"]),
+                                _p(o.get("domega")), _p(ws), ws.numel(), _stream()), "ssm_lm_head_grad")
     return o

@@ -14,7 +14,7 @@ ROOT = PKG.parent
 CSRC = PKG / "csrc"
 SRC = [CSRC / "scan.hip", CSRC / "scan_grad_f32_full.hip", CSRC / "scan_grad_f32_trunc.hip",
        CSRC / "scan_grad_bf16_full.hip", CSRC / "scan_grad_bf16_trunc.hip", CSRC / "gemm.hip", CSRC / "pairs.hip", CSRC / "stack.hip",
-       CSRC / "noalloc.hip", CSRC / "layer.hip", CSRC / "da_debug.hip", CSRC / "unstructured.hip", CSRC / "abi.cpp", CSRC / "timing.cpp"]
+       CSRC / "noalloc.hip", CSRC / "layer.hip", CSRC / "da_debug.hip", CSRC / "unstructured.hip", CSRC / "head.hip", CSRC / "abi.cpp", CSRC / "timing.cpp"]
 OBJ = PKG / "_build"
 LIB = PKG / "libssm_adjoint.so"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -911,3 +911,129 @@ ssm_status ssm_stack_grad(const ssm_desc* desc, int64_t K, int32_t grad, int32_t
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The language head and its loss (Sec. 3.2, Alg. 1).
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kHeadLogitBytes = size_t(1) << 30;
+
+// Workspace of the head: per row block Norm(y) (bf16) and 1/rms, Omega^T (bf16
+// [P][V]), the block's fp32 logits and bf16 logit gradients, dU (fp32), and the
+// GEMM workspace shared by the block's three products.
+struct HeadWs {
+    int64_t rows;
+    size_t off_u, off_r, off_omt, off_logit, off_g, off_du, off_gws, total;
+};
+
+HeadWs head_ws(int64_t M, int64_t P, int64_t V, int64_t block_rows) {
+    HeadWs w{};
+    int64_t rows = block_rows ? block_rows : static_cast<int64_t>(kHeadLogitBytes / (size_t(V) * 4)) / 256 * 256;
+    if (rows < 256) rows = 256;
+    if (rows > M) rows = M;
+    w.rows = rows;
+    size_t o = 0;
+    w.off_u = o; o = up256(o + size_t(rows) * P * 2);
+    w.off_r = o; o = up256(o + size_t(rows) * 4);
+    w.off_omt = o; o = up256(o + size_t(P) * V * 2);
+    w.off_logit = o; o = up256(o + size_t(rows) * V * 4);
+    w.off_g = o; o = up256(o + size_t(rows) * V * 2);
+    w.off_du = o; o = up256(o + size_t(rows) * P * 4);
+    // a whole block and the last, shorter one (whose split may differ)
+    size_t g = 0;
+    for (int64_t mb : {rows, M % rows}) {
+        if (mb == 0) continue;
+        for (size_t gi : {ssmk::gemm_dx_workspace(mb, V, P), ssmk::gemm_dx_workspace(mb, P, V),
+                          ssmk::gemm_dw_workspace(mb, V, P)})
+            g = gi > g ? gi : g;
+    }
+    w.off_gws = o; o = up256(o + g);
+    w.total = o;
+    return w;
+}
+
+ssm_status check_head(int64_t M, int64_t P, int64_t V, uint32_t flags, int64_t block_rows) {
+    if (flags & ~SSM_HEAD_NORM) return fail(SSM_ERR_SHAPE, "unknown flag bits");
+    if (M < 1 || P < 1 || V < 1) return fail(SSM_ERR_SHAPE, "M, P, V must be >= 1");
+    if (M >= (int64_t(1) << 31)) return fail(SSM_ERR_SHAPE, "M must be below 2^31");
+    if (block_rows < 0 || block_rows % 256 || block_rows >= (int64_t(1) << 31))
+        return fail(SSM_ERR_SHAPE, "block_rows must be 0 or a positive multiple of 256 below 2^31");
+    const int64_t rows = head_ws(M, P, V, block_rows).rows;
+    ssm_status st = check_gemm_shape(rows, V, P, V, P, P, true);  // logits = u Omega^T
+    if (st) return st;
+    return check_gemm_shape(rows, P, V, P, V, V, true);            // dU = G Omega, dOmega = G^T u
+}
+
+}  // namespace
+
+extern "C" {
+
+ssm_status ssm_lm_head_grad_workspace_size(int64_t M, int64_t P, int64_t V, uint32_t flags, int64_t block_rows,
+                                           size_t* bytes) {
+    ssm_status st = check_head(M, P, V, flags, block_rows);
+    if (st) return st;
+    if (!bytes) return fail(SSM_ERR_NULL, "bytes is NULL");
+    *bytes = head_ws(M, P, V, block_rows).total;
+    return SSM_OK;
+}
+
+ssm_status ssm_lm_head_grad(int64_t M, int64_t P, int64_t V, uint32_t flags, int64_t block_rows, const float* y,
+                            const void* omega, const int32_t* targets, float* loss, float* dy, float* domega,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+    ssm_status st = check_head(M, P, V, flags, block_rows);
+    if (st) return st;
+    REQUIRE_PTR(y, "y");
+    REQUIRE_PTR(omega, "omega");
+    REQUIRE_PTR(targets, "targets");
+    REQUIRE_PTR(loss, "loss");
+    REQUIRE_PTR(dy, "dy");
+    OPTIONAL_PTR(domega, "domega");
+    const HeadWs w = head_ws(M, P, V, block_rows);
+    st = check_workspace(workspace, workspace_bytes, w.total);
+    if (st) return st;
+    const bool norm = (flags & SSM_HEAD_NORM) != 0;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    uint16_t* u = reinterpret_cast<uint16_t*>(ws + w.off_u);
+    float* rinv = reinterpret_cast<float*>(ws + w.off_r);
+    uint16_t* omt = reinterpret_cast<uint16_t*>(ws + w.off_omt);
+    float* logit = reinterpret_cast<float*>(ws + w.off_logit);
+    uint16_t* G = reinterpret_cast<uint16_t*>(ws + w.off_g);
+    float* du = reinterpret_cast<float*>(ws + w.off_du);
+    void* gws = ws + w.off_gws;
+    const uint16_t* om = static_cast<const uint16_t*>(omega);
+    hipError_t e = ssmk::launch_transpose16(om, omt, V, P, s);
+    if (e != hipSuccess) return hip_fail(e, "ssm_lm_head_grad transpose");
+#define HEAD_HIP(call, what)                           \
+    do {                                               \
+        e = (call);                                    \
+        if (e != hipSuccess) return hip_fail(e, what); \
+    } while (0)
+    for (int64_t m0 = 0; m0 < M; m0 += w.rows) {
+        const int64_t mb = M - m0 < w.rows ? M - m0 : w.rows;
+        const float* yb = y + m0 * P;
+        float* dyb = dy + m0 * P;
+        if (norm)
+            HEAD_HIP(ssmk::launch_rms_fwd(yb, u, rinv, mb, P, s), "ssm_lm_head_grad norm");
+        else
+            HEAD_HIP(ssmk::launch_to_bf16(yb, u, mb * P, s), "ssm_lm_head_grad input");
+        // logits [mb][V] = u Omega^T: the dX form with the reduction over P
+        HEAD_HIP(ssmk::launch_gemm_dx(mb, V, P, u, P, om, P, logit, false, nullptr, nullptr, 0, gws, s, 0, 0,
+                                      "head_logits"),
+                 "ssm_lm_head_grad logits");
+        HEAD_HIP(ssmk::launch_head_xent(logit, V, targets + m0, loss + m0, G, V, mb, V, s),
+                 "ssm_lm_head_grad loss");
+        // dU [mb][P] = G Omega = G (Omega^T)^T: the dX form with the reduction over V
+        HEAD_HIP(ssmk::launch_gemm_dx(mb, P, V, G, V, omt, V, norm ? du : dyb, false, nullptr, nullptr, 0, gws, s,
+                                      0, 0, "head_du"),
+                 "ssm_lm_head_grad dU");
+        if (norm) HEAD_HIP(ssmk::launch_rms_bwd(yb, rinv, du, dyb, nullptr, mb, P, s, false), "ssm_lm_head_grad dy");
+        if (domega)  // dOmega [V][P] (+)= G^T u, the blocks added in order
+            HEAD_HIP(ssmk::launch_gemm_dw(mb, V, P, G, V, u, P, domega, m0 > 0, gws, s), "ssm_lm_head_grad dOmega");
+    }
+#undef HEAD_HIP
+    return SSM_OK;
+}
+
+}  // extern "C"

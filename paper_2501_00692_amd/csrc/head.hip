@@ -1,0 +1,95 @@
+// head.hip -- the language head's loss and logit gradients (Sec. 3.2: o^t =
+// Omega Norm(y_K^t); the per-token losses and dl/do^t that Alg. 1 evaluates once
+// before the layers' gradients).  The products with Omega run on the bf16 MFMA
+// GEMMs of gemm.hip; this file holds the row-wise step between them:
+//   k_head_xent : per row of fp32 logits o [V] and target t, the cross-entropy
+//                 l = log sum_v exp(o_v) - o_t and the logit gradient
+//                 G = softmax(o) - onehot(t) as bf16 (round to nearest even).
+//                 t < 0: no loss (l = 0, G = 0); t >= V: l = NaN, G = 0.
+// One workgroup of 256 threads per row: pass 1 keeps a running maximum and the
+// sum of exp(o - max) per thread over float4 pieces of the row (the sum rescaled
+// when the maximum grows), combined over the workgroup in a fixed tree; pass 2
+// reads the row again (from L2) and writes G.
+#include <cmath>
+
+#include "internal.h"
+
+namespace ssmk {
+namespace {
+
+constexpr int kXentThreads = 256;
+
+__device__ __forceinline__ uint16_t bf16_rne(float v) {
+    uint32_t u = __float_as_uint(v);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+__global__ __launch_bounds__(kXentThreads) void k_head_xent(const float* o, int64_t ldo, const int32_t* tgt,
+                                                            float* loss, uint16_t* G, int64_t ldg, int64_t V) {
+    __shared__ float smax[kXentThreads], ssum[kXentThreads];
+    const int tid = threadIdx.x;
+    const int64_t row = blockIdx.x;
+    const float4* orow = reinterpret_cast<const float4*>(o + row * ldo);
+    const int64_t nv4 = V / 4;
+    float mx = -INFINITY, s = 0.f;
+    for (int64_t i = tid; i < nv4; i += kXentThreads) {
+        const float4 x = orow[i];
+        const float m4 = fmaxf(fmaxf(x.x, x.y), fmaxf(x.z, x.w));
+        const float mn = fmaxf(mx, m4);
+        // exp(-inf) = 0 covers the first piece (mx = -inf)
+        s = s * __expf(mx - mn) + ((__expf(x.x - mn) + __expf(x.y - mn)) + (__expf(x.z - mn) + __expf(x.w - mn)));
+        mx = mn;
+    }
+    smax[tid] = mx;
+    ssum[tid] = s;
+    __syncthreads();
+#pragma unroll
+    for (int h = kXentThreads / 2; h > 0; h >>= 1) {
+        if (tid < h) {
+            const float ma = smax[tid], mb = smax[tid + h];
+            const float mn = fmaxf(ma, mb);
+            // pieces that never saw a value (-inf) contribute 0
+            const float sa = ma == -INFINITY ? 0.f : ssum[tid] * __expf(ma - mn);
+            const float sb = mb == -INFINITY ? 0.f : ssum[tid + h] * __expf(mb - mn);
+            smax[tid] = mn;
+            ssum[tid] = sa + sb;
+        }
+        __syncthreads();
+    }
+    const float m = smax[0], tot = ssum[0];
+    const int32_t t = tgt[row];
+    const bool valid = t >= 0 && t < V;
+    if (tid == 0) {
+        const float* orw = o + row * ldo;
+        loss[row] = valid ? (m + __logf(tot)) - orw[t] : (t < 0 ? 0.f : NAN);
+    }
+    const float inv = 1.f / tot;
+    const float keep = valid ? 1.f : 0.f;
+    uint2* grow = reinterpret_cast<uint2*>(G + row * ldg);
+    for (int64_t i = tid; i < nv4; i += kXentThreads) {
+        const float4 x = orow[i];
+        float g[4] = {__expf(x.x - m) * inv, __expf(x.y - m) * inv, __expf(x.z - m) * inv, __expf(x.w - m) * inv};
+        const int64_t v0 = 4 * i;
+        if (valid && t >= v0 && t < v0 + 4) g[t - v0] -= 1.f;
+        uint16_t b[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) b[k] = bf16_rne(g[k] * keep);
+        grow[i] = make_uint2(static_cast<uint32_t>(b[0]) | (static_cast<uint32_t>(b[1]) << 16),
+                             static_cast<uint32_t>(b[2]) | (static_cast<uint32_t>(b[3]) << 16));
+    }
+}
+
+}  // namespace
+
+hipError_t launch_head_xent(const float* logits, int64_t ldo, const int32_t* targets, float* loss, uint16_t* G,
+                            int64_t ldg, int64_t rows, int64_t V, hipStream_t s) {
+    if (V % 4 || ldo % 4 || ldg % 4) return hipErrorInvalidValue;
+    SSMK_TIMED("head_xent", s);
+    hipLaunchKernelGGL(k_head_xent, dim3(static_cast<unsigned>(rows)), dim3(kXentThreads), 0, s, logits, ldo,
+                       targets, loss, G, ldg, V);
+    return hipGetLastError();
+}
+
+}  // namespace ssmk

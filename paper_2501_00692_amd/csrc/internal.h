@@ -139,11 +139,19 @@ hipError_t launch_layer_split(const float* G, int64_t ldg, int64_t dm, int64_t D
 
 // Kernels of the K-layer residual stack (stack.hip).
 hipError_t launch_rms_fwd(const float* y, uint16_t* u, float* rinv, int64_t M, int64_t D, hipStream_t s);
+// g (+)= (du - u mean(du u)) / rms; accum = false overwrites g; g16 (the bf16 copy)
+// may be NULL.
 hipError_t launch_rms_bwd(const float* y, const float* rinv, const float* du, float* g, uint16_t* g16, int64_t M,
-                          int64_t D, hipStream_t s);
+                          int64_t D, hipStream_t s, bool accum = true);
 hipError_t launch_residual(const float* yin, const uint16_t* ytil, float* yout, int64_t n, hipStream_t s);
 hipError_t launch_to_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s);
 hipError_t launch_transpose16(const uint16_t* in, uint16_t* out, int64_t R, int64_t C, hipStream_t s);
+
+// The language head's row step (head.hip): per row of fp32 logits [rows][V] (ldo)
+// and int32 target, the cross-entropy loss and the bf16 logit gradient
+// softmax - onehot [rows][V] (ldg).  V, ldo and ldg must be multiples of 4.
+hipError_t launch_head_xent(const float* logits, int64_t ldo, const int32_t* targets, float* loss, uint16_t* G,
+                            int64_t ldg, int64_t rows, int64_t V, hipStream_t s);
 
 // The gradient by the explicit pair formulation (pairs.hip): workspace layout and
 // launch; W is the window (tbar, or T for the full gradient).

@@ -1,8 +1,9 @@
 // stack.hip -- kernels of the K-layer residual stack (Sec. 3.2, Alg. 1) around
 // the per-layer SSM kernels:
 //   k_rms_fwd   : u = y / sqrt(mean_d y^2 + eps) as bf16, and 1/rms per row;
-//   k_rms_bwd   : g += (du - u mean_d(du u)) / rms with u = y / rms recomputed in
-//                 fp32 (the cotangent of the normalisation), plus g's bf16 copy;
+//   k_rms_bwd   : g (+)= (du - u mean_d(du u)) / rms with u = y / rms recomputed in
+//                 fp32 (the cotangent of the normalisation), plus g's bf16 copy
+//                 when asked;
 //   k_residual  : y_out = y_in + ytil (ytil bf16);
 //   k_transpose : bf16 [R][C] -> [C][R] (the forward projections read W^T);
 //   k_to_bf16   : fp32 -> bf16 (round to nearest even).
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rms_fwd(const float* y, uint16_
 }
 
 __global__ __launch_bounds__(kRowThreads) void k_rms_bwd(const float* y, const float* rinv, const float* du,
-                                                          float* g, uint16_t* g16, int64_t D) {
+                                                          float* g, uint16_t* g16, int64_t D, bool accum) {
     __shared__ float sh[kRowThreads];
     const int64_t row = blockIdx.x;
     const float r = rinv[row];
@@ -61,9 +62,9 @@ __global__ __launch_bounds__(kRowThreads) void k_rms_bwd(const float* y, const f
     for (int64_t d = threadIdx.x; d < D; d += kRowThreads) s = fmaf(dr[d], yr[d] * r, s);
     const float m = row_sum(s, sh) / static_cast<float>(D);
     for (int64_t d = threadIdx.x; d < D; d += kRowThreads) {
-        const float v = g[row * D + d] + (dr[d] - yr[d] * r * m) * r;
+        const float v = (accum ? g[row * D + d] : 0.f) + (dr[d] - yr[d] * r * m) * r;
         g[row * D + d] = v;
-        g16[row * D + d] = to_bf16(v);
+        if (g16) g16[row * D + d] = to_bf16(v);
     }
 }
 
@@ -104,9 +105,10 @@ hipError_t launch_rms_fwd(const float* y, uint16_t* u, float* rinv, int64_t M, i
 }
 
 hipError_t launch_rms_bwd(const float* y, const float* rinv, const float* du, float* g, uint16_t* g16, int64_t M,
-                          int64_t D, hipStream_t s) {
+                          int64_t D, hipStream_t s, bool accum) {
     SSMK_TIMED("rms_bwd", s);
-    hipLaunchKernelGGL(k_rms_bwd, dim3(static_cast<unsigned>(M)), dim3(kRowThreads), 0, s, y, rinv, du, g, g16, D);
+    hipLaunchKernelGGL(k_rms_bwd, dim3(static_cast<unsigned>(M)), dim3(kRowThreads), 0, s, y, rinv, du, g, g16, D,
+                       accum);
     return hipGetLastError();
 }
 

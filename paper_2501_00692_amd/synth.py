@@ -156,3 +156,28 @@ def make_unstructured_inputs(b: int, T: int, P: int, seed: int, N: int = 16, dev
     if h0:
         out["h0"] = torch.randn(b, N, generator=g, **f32)
     return out
+
+
+# The language head of Sec. 3.2: (rows M, width P, vocabulary V).  "head" is the
+# measured workload (32,768 tokens of a 2,048-wide model, a 32,000-token
+# vocabulary); the others are parity cases.
+HEAD_WORKLOADS = {
+    "head_small": (300, 96, 1000),
+    "head_blocks": (1000, 64, 1024),
+    "head_medium": (4096, 512, 32000),
+    "head": (32768, 2048, 32000),
+}
+
+
+def make_head_inputs(M: int, P: int, V: int, seed: int, device="cpu"):
+    """Inputs of the head: y ~ N(0, 1) fp32 [M][P] (the last residual output),
+    Omega ~ N(0, 4/P) as bf16 [V][P] (logits of standard deviation about 2 on
+    the normalised input), targets uniform over the vocabulary (int32 [M])."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    f32 = dict(dtype=torch.float32, device=device)
+    return {
+        "y": torch.randn(M, P, generator=g, **f32),
+        "omega": torch.randn(V, P, generator=g, **f32).mul_(2.0 / math.sqrt(P)).to(torch.bfloat16),
+        "targets": torch.randint(0, V, (M,), generator=g, device=device, dtype=torch.int32),
+    }

@@ -183,3 +183,25 @@ def test_noalloc_host_errors(lib):
     assert n.value > (64 << 20)
     assert noalloc_call(lib, big) == 5
     assert "no-allocation" in ssm.last_error()
+
+
+def test_head_errors(lib):
+    n = ctypes.c_size_t()
+    ok = lambda M, P, V, flags=ssm.SSM_HEAD_NORM, rows=0: lib.ssm_lm_head_grad_workspace_size(
+        M, P, V, flags, rows, ctypes.byref(n))
+    assert ok(4096, 1536, 32000) == 0 and n.value > 1536 * 32000 * 2 + 4096 * 32000 * 6
+    assert ok(4096, 1536, 32000, rows=512) == 0 and n.value < 1536 * 32000 * 2 + 1024 * 32000 * 6
+    assert ok(4096, 64, 64, rows=100) == 2
+    assert ok(0, 64, 64) == 2
+    assert ok(64, 64, 64, flags=2) == 2
+    assert ok(64, 60, 64) == 4 and "multiples of 8" in ssm.last_error()
+    assert ok(64, 64, 1001) == 4
+    assert lib.ssm_lm_head_grad_workspace_size(64, 64, 64, 0, 0, None) == 1
+    call = lambda y=FAKE, om=FAKE, t=FAKE, loss=FAKE, dy=FAKE, dom=None, ws=FAKE, wsb=1 << 40: lib.ssm_lm_head_grad(
+        256, 64, 128, ssm.SSM_HEAD_NORM, 0, y, om, t, loss, dy, dom, ws, wsb, None)
+    assert call(y=None) == 1 and "y is NULL" in ssm.last_error()
+    assert call(t=None) == 1
+    assert call(dy=None) == 1
+    assert call(dom=MISALIGNED) == 6
+    assert call(ws=None) == 5
+    assert call(wsb=1024) == 5
