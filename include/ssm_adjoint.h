@@ -77,6 +77,7 @@ typedef enum { SSM_FULL = 0, SSM_TRUNCATED = 1 } ssm_mode;
 /* ssm_stack_grad gradient kinds */
 #define SSM_STACK_ADJOINT 0   /* Prop. 3: every layer's vjps under dL/dy_K                 */
 #define SSM_STACK_EXACT 1     /* backpropagation through the whole stack                   */
+#define SSM_STACK_FORWARD 2   /* the forward only: y_K for the language head                */
 
 /* ssm_proj_grad flags */
 #define SSM_ACCUM_DW 1u       /* dW += X^T dZ instead of dW = X^T dZ                   */
@@ -270,7 +271,11 @@ const char* ssm_last_error(void);
  *            layer's gradient taken with the upstream g_K and the layer's own
  *            input, independently of the other layers) or SSM_STACK_EXACT
  *            (backpropagation: layer k's upstream is dL/dy_k, including the paths
- *            through later layers);  mode/tbar : as for ssm_adjoint_grad.
+ *            through later layers) or SSM_STACK_FORWARD (the forward alone: yK is
+ *            required, gK and the gradient arrays may be NULL and are not touched;
+ *            Alg. 1 runs it, evaluates the language head on y_K with
+ *            ssm_lm_head_grad, and passes that call's dy as gK to a gradient
+ *            call);  mode/tbar : as for ssm_adjoint_grad.
  *   y0     : fp32 [b][T][D];  gK : fp32 [b][T][D] (passed to the layers in bf16);
  *   W_in, W_x, A_log : host arrays of K device pointers (bf16 [D][2D], bf16
  *            [D][D+2N], fp32 [D][N]);  dW_in, dW_x, dA_log : host arrays of K device

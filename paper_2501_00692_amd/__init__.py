@@ -27,7 +27,7 @@ SSM_F32, SSM_BF16 = 0, 1
 SSM_FULL, SSM_TRUNCATED = 0, 1
 SSM_DELTA_SOFTPLUS, SSM_GATE_SILU, SSM_A_SCALAR, SSM_B_DELTA = 1, 2, 4, 8
 SSM_ACCUM_DW, SSM_ACCUM_DX = 1, 2
-SSM_STACK_ADJOINT, SSM_STACK_EXACT = 0, 1
+SSM_STACK_ADJOINT, SSM_STACK_EXACT, SSM_STACK_FORWARD = 0, 1, 2
 SSM_HEAD_NORM = 1
 
 STATUS = {0: "SSM_OK", 1: "SSM_ERR_NULL", 2: "SSM_ERR_SHAPE", 3: "SSM_ERR_DTYPE",
@@ -419,36 +419,41 @@ def stack_workspace_size(desc: SsmDesc, K: int, grad: int, tbar: int = 0) -> int
 
 
 def ssm_stack_grad(y0, W_in, W_x, A_log, gK, N, exact=False, tbar=0, chunk=0, want_yK=False, out=None,
-                   workspace=None):
+                   workspace=None, forward_only=False):
     """Parameter gradients of a K-layer residual stack (lists ``W_in``, ``W_x``,
     ``A_log`` of K tensors) for the upstream ``gK = dL/dy_K``: Prop. 3 (each layer
     under gK, ``exact=False``) or backpropagation (``exact=True``).  ``y0`` and
     ``gK`` are fp32 [b, T, D]; the projections bf16.  Returns a dict with lists
-    ``dW_in, dW_x, dA_log`` (+ ``yK`` if asked)."""
+    ``dW_in, dW_x, dA_log`` (+ ``yK`` if asked).  ``forward_only`` runs the
+    forward alone (SSM_STACK_FORWARD; gK may be None) and returns ``yK`` only."""
     lib = load_library()
     b, T, D = y0.shape
     K = len(W_in)
     assert len(W_x) == K and len(A_log) == K
     _need(y0, "y0", torch.float32)
-    _need(gK, "gK", torch.float32, (b, T, D))
+    if not forward_only:
+        _need(gK, "gK", torch.float32, (b, T, D))
     for k in range(K):
         _need(W_in[k], "W_in[k]", torch.bfloat16, (D, 2 * D))
         _need(W_x[k], "W_x[k]", torch.bfloat16, (D, D + 2 * N))
         _need(A_log[k], "A_log[k]", torch.float32, (D, N))
     desc = SsmDesc(b, T, D, N, chunk, SSM_BF16, 0)
-    grad = SSM_STACK_EXACT if exact else SSM_STACK_ADJOINT
+    grad = SSM_STACK_FORWARD if forward_only else (SSM_STACK_EXACT if exact else SSM_STACK_ADJOINT)
     mode = SSM_TRUNCATED if tbar > 0 else SSM_FULL
     dev = y0.device
     f32 = dict(dtype=torch.float32, device=dev)
     o = dict(out) if out else {}
-    o.setdefault("dW_in", [torch.empty(D, 2 * D, **f32) for _ in range(K)])
-    o.setdefault("dW_x", [torch.empty(D, D + 2 * N, **f32) for _ in range(K)])
-    o.setdefault("dA_log", [torch.empty(D, N, **f32) for _ in range(K)])
-    if want_yK:
+    if not forward_only:
+        o.setdefault("dW_in", [torch.empty(D, 2 * D, **f32) for _ in range(K)])
+        o.setdefault("dW_x", [torch.empty(D, D + 2 * N, **f32) for _ in range(K)])
+        o.setdefault("dA_log", [torch.empty(D, N, **f32) for _ in range(K)])
+    else:
+        o = {k: v for k, v in o.items() if k == "yK"}
+    if want_yK or forward_only:
         o.setdefault("yK", torch.empty(b, T, D, **f32))
     ws = workspace if workspace is not None else _workspace(stack_workspace_size(desc, K, grad, tbar), dev)
-    keep = [_ptr_array(W_in), _ptr_array(W_x), _ptr_array(A_log), _ptr_array(o["dW_in"]), _ptr_array(o["dW_x"]),
-            _ptr_array(o["dA_log"])]
+    keep = [_ptr_array(W_in), _ptr_array(W_x), _ptr_array(A_log)]
+    keep += [None] * 3 if forward_only else [_ptr_array(o["dW_in"]), _ptr_array(o["dW_x"]), _ptr_array(o["dA_log"])]
     _check(lib.ssm_stack_grad(ctypes.byref(desc), K, grad, mode, int(tbar), _p(y0), *[ctypes.cast(a, ctypes.c_void_p)
                                                                                     for a in keep[:3]],
                               _p(gK), *[ctypes.cast(a, ctypes.c_void_p) for a in keep[3:]], _p(o.get("yK")), _p(ws),

@@ -776,7 +776,8 @@ ssm_status check_stack(const ssm_desc* desc, int64_t K, int32_t grad, int32_t mo
     if (desc->in_dtype != SSM_BF16) return fail(SSM_ERR_UNSUPPORTED, "the stack takes bf16 activations");
     if (desc->flags != 0) return fail(SSM_ERR_UNSUPPORTED, "the stack's layers take no variant flags");
     if (K < 1 || K > kMaxStackLayers) return fail(SSM_ERR_SHAPE, "K must be in [1, %lld]", (long long)kMaxStackLayers);
-    if (grad != SSM_STACK_ADJOINT && grad != SSM_STACK_EXACT) return fail(SSM_ERR_SHAPE, "unknown gradient kind %d", grad);
+    if (grad != SSM_STACK_ADJOINT && grad != SSM_STACK_EXACT && grad != SSM_STACK_FORWARD)
+        return fail(SSM_ERR_SHAPE, "unknown gradient kind %d", grad);
     st = check_mode(desc, mode, tbar, trunc);
     if (st) return st;
     const int64_t M = desc->batch * desc->seqlen, D = desc->channels, N = desc->dstate;
@@ -811,15 +812,21 @@ ssm_status ssm_stack_grad(const ssm_desc* desc, int64_t K, int32_t grad, int32_t
     bool trunc;
     ssm_status st = check_stack(desc, K, grad, mode, tbar, &L, &trunc);
     if (st) return st;
+    const bool fwd_only = grad == SSM_STACK_FORWARD;
     REQUIRE_PTR(y0, "y0");
-    REQUIRE_PTR(gK, "gK");
-    OPTIONAL_PTR(yK, "yK");
-    if (!W_in || !W_x || !A_log || !dW_in || !dW_x || !dA_log)
+    if (fwd_only) {
+        REQUIRE_PTR(yK, "yK");
+    } else {
+        REQUIRE_PTR(gK, "gK");
+        OPTIONAL_PTR(yK, "yK");
+    }
+    if (!W_in || !W_x || !A_log || (!fwd_only && (!dW_in || !dW_x || !dA_log)))
         return fail(SSM_ERR_NULL, "a per-layer pointer array is NULL");
     for (int64_t k = 0; k < K; ++k) {
         REQUIRE_PTR(W_in[k], "W_in[k]");
         REQUIRE_PTR(W_x[k], "W_x[k]");
         REQUIRE_PTR(A_log[k], "A_log[k]");
+        if (fwd_only) continue;
         REQUIRE_PTR(dW_in[k], "dW_in[k]");
         REQUIRE_PTR(dW_x[k], "dW_x[k]");
         REQUIRE_PTR(dA_log[k], "dA_log[k]");
@@ -891,6 +898,7 @@ ssm_status ssm_stack_grad(const ssm_desc* desc, int64_t K, int32_t grad, int32_t
         ycur = ynext;
     }
 
+    if (fwd_only) return SSM_OK;
     // gradients: Prop. 3 (every layer under dL/dy_K) or backpropagation
     if (grad == SSM_STACK_EXACT)
         STACK_HIP(hipMemcpyAsync(g, gK, size_t(M) * D * 4, hipMemcpyDeviceToDevice, s), "ssm_stack_grad copy");

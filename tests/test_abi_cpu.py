@@ -153,6 +153,10 @@ def test_stack_errors(lib):
     assert call(y0=None) == 1
     assert call(W=None) == 1
     assert call(ws_bytes=16) == 5
+    # the forward alone needs yK (the call above passes NULL) and nothing of the gradients
+    assert call(grad=ssm.SSM_STACK_FORWARD) == 1 and "yK" in ssm.last_error()
+    assert lib.ssm_stack_grad(ctypes.byref(d), 2, ssm.SSM_STACK_FORWARD, ssm.SSM_FULL, 0, FAKE, arr, arr, arr, None,
+                              None, None, None, FAKE, FAKE, 16, None) == 5
     n = ctypes.c_size_t()
     assert lib.ssm_stack_grad_workspace_size(ctypes.byref(d), 3, ssm.SSM_STACK_EXACT, ssm.SSM_FULL, 0,
                                              ctypes.byref(n)) == 0

@@ -108,3 +108,39 @@ def test_stack_against_unrounded_model(K, exact, tbar):
         for n in ("dW_in", "dW_x", "dA_log"):
             check(f"{n}[{k}]", to_np(o[n][k]), ref[k][n], TOL_BF16, rep)
     say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
+def test_stack_with_language_head():
+    """Alg. 1 end to end: the stack's forward (SSM_STACK_FORWARD) gives y_K, the
+    language head gives the per-token losses and dL/dy_K (Sec. 3.2's Omega with
+    the cross-entropy), and a Prop. 3 gradient call takes that as gK; against the
+    oracle chain stack_forward -> head_loss_grad -> stack_grad."""
+    from oracle.head import head_loss_grad
+    K, b, T, D, N, V = 2, 1, 256, 64, 16, 512
+    say(f"[stack + head] K={K} b={b} T={T} D={D} V={V}")
+    inp = make_stack_inputs(K, b, T, D, N, 692403, device="cuda")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(692404)
+    omega = (torch.randn(V, D, generator=g, device="cuda") * (2.0 / D ** 0.5)).to(torch.bfloat16)
+    targets = torch.randint(0, V, (b * T,), generator=g, device="cuda", dtype=torch.int32)
+    yK = ssm.ssm_stack_grad(inp["y0"], inp["W_in"], inp["W_x"], inp["A_log"], None, N, forward_only=True)["yK"]
+    head = ssm.ssm_lm_head_grad(yK.reshape(b * T, D), omega, targets)
+    gK = head["dy"].reshape(b, T, D).contiguous()
+    o = ssm.ssm_stack_grad(inp["y0"], inp["W_in"], inp["W_x"], inp["A_log"], gK, N)
+    torch.cuda.synchronize()
+
+    W_in = [to_np(w) for w in inp["W_in"]]
+    W_x = [to_np(w) for w in inp["W_x"]]
+    A_log = [to_np(a) for a in inp["A_log"]]
+    yK_ref, acts = ostack.stack_forward(to_np(inp["y0"]), W_in, W_x, A_log, N)
+    h = head_loss_grad(yK_ref.reshape(b * T, D), to_np(omega), targets.cpu().numpy(), round_bf16=True)
+    ref = ostack.stack_grad(acts, W_in, W_x, A_log, h["dy"].reshape(b, T, D), mode="adjoint")
+    rep = {}
+    check("yK", to_np(yK), yK_ref, TOL_BF16, rep)
+    check("loss", to_np(head["loss"]), h["loss"], TOL_BF16, rep)
+    check("dy_K", to_np(gK), h["dy"].reshape(b, T, D), TOL_BF16, rep)
+    check("dOmega", to_np(head["domega"]), h["domega"], TOL_BF16, rep)
+    for k in range(K):
+        for n in ("dW_in", "dW_x", "dA_log"):
+            check(f"{n}[{k}]", to_np(o[n][k]), ref[k][n], TOL_BF16, rep)
+    say("   rel-L2 max:", f"{max(rep.values()):.2e}")
