@@ -21,10 +21,11 @@
 // outside the matrix (rows, columns, or the reduction tail) read as zero through
 // the buffer range check.  Workgroup: 512 threads = 4x2 waves, two per SIMD;
 // a wave owns a 64 x (BN/2) block of 32x32 MFMA tiles; tile 256 x BN with BN 128
-// or 192.  dW's 256 x 256 tiles run on a kernel of their own (k_gemm_dw4): 256
-// threads, one wave per SIMD owning a 128 x 128 block with its accumulators in
-// the AGPRs, a five-stage ring (160 KB of LDS), one barrier per step and the
-// MFMAs interleaved one by one with the fragment reads and stage loads.
+// or 192.  256 x 256 tiles (dW, and dX with a plain epilogue) run on a kernel of
+// their own (k_gemm4): 256 threads, one wave per SIMD owning a 128 x 128 block
+// with its accumulators in the AGPRs, a five-stage ring (160 KB of LDS), one
+// barrier per step and the MFMAs interleaved one by one with the fragment reads
+// and stage loads.
 // Output tiles and reduction splits are assigned so that each XCD runs one
 // contiguous run of (split, tile) (consecutive workgroups go to different XCDs),
 // tiles ordered in groups of four row blocks, so that the tiles one XCD runs at
@@ -613,8 +614,68 @@ struct ColMajorOps4 {
     }
 };
 
-template <int NST>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gemm_dw4(const GemmLaunch gl) {
+// The dX form (operands contiguous along the reduction) on the four-wave
+// kernel: the LDS layout of RowMajorOps (64-byte rows of 32 steps, 16-byte
+// blocks XOR-swizzled by (row >> 2) & 3), 256 rows of each operand per stage,
+// four wave loads of A and four of B per wave and stage; each wave reads the
+// 16-byte fragments of its 128 rows of A and 128 rows of B.
+struct RowMajorOps4 {
+    __amdgpu_buffer_rsrc_t ra, rb;
+    uint32_t oa[4], ob[4];
+    int ka[4], kb[4];
+    int64_t k_hi;
+    int offa[2][4], offb[2][4];  // fragment offsets (elements) per sub-step
+
+    __device__ __forceinline__ void init(const GemmArgs& g, int64_t r0, int64_t c0, int64_t khi, int wave,
+                                         int lane, int wr, int wc) {
+        k_hi = khi;
+        // resources over the tile's rows: rows past the matrix read as zero
+        ra = rsrc(g.A + r0 * g.lda, min<int64_t>(BM, g.R - r0) * g.lda * 2);
+        rb = rsrc(g.B + c0 * g.ldb, min<int64_t>(256, g.Cc - c0) * g.ldb * 2);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = (wave + 4 * i) * 16 + (lane >> 2);
+            ka[i] = kb[i] = ((lane & 3) ^ RowMajorOps<128>::swz(row)) * 8;
+            oa[i] = static_cast<uint32_t>((row * g.lda + ka[i]) * 2);
+            ob[i] = static_cast<uint32_t>((row * g.ldb + kb[i]) * 2);
+        }
+        const int li = lane & 31, hk = lane >> 5;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int ra_ = wr + i * 32 + li, rb_ = wc + i * 32 + li;
+                offa[ks][i] = ra_ * BK + (((ks * 2 + hk) ^ RowMajorOps<128>::swz(ra_)) * 8);
+                offb[ks][i] = rb_ * BK + (((ks * 2 + hk) ^ RowMajorOps<128>::swz(rb_)) * 8);
+            }
+    }
+    // pieces past the reduction range read out of range (zero)
+    __device__ __forceinline__ uint32_t off(uint32_t o0, int kq, int64_t k) const {
+        return k + kq < k_hi ? o0 + static_cast<uint32_t>(k * 2) : kOutOfRange;
+    }
+    template <int S>
+    __device__ __forceinline__ void issue(Stage<S>, int64_t k, int wave) const {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) load_lds16(ra, off(oa[i], ka[i], k), stage_a<S>() + (wave + 4 * i) * 512);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) load_lds16(rb, off(ob[i], kb[i], k), stage_b<S>() + (wave + 4 * i) * 512);
+    }
+    template <int S>
+    __device__ __forceinline__ void read(Stage<S>, int ks, bf16x8 (&a)[4], bf16x8 (&b)[4]) const {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(stage_a<S>() + offa[ks][i]));
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(stage_b<S>() + offb[ks][j]));
+    }
+};
+
+// Four waves, one per SIMD, each owning a 128 x 128 block of a 256 x 256 output
+// tile: TR selects the dW form (ColMajorOps4) or the dX form (RowMajorOps4, plain
+// epilogues only: no addend, no bf16 copy).
+template <bool TR, int NST>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gemm4(const GemmLaunch gl) {
     constexpr int MI = 4, NJ = 4, BN = 256;
     static_assert(NST == 4 || NST == 5, "stages");
     const int tid = threadIdx.x;
@@ -642,7 +703,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int wc = (wave & 1) * 128;
     const int64_t nsteps = k_hi > k_lo ? (k_hi - k_lo + BK - 1) / BK : 0;
 
-    ColMajorOps4 ops;
+    std::conditional_t<TR, ColMajorOps4, RowMajorOps4> ops;
     ops.init(g, r0, c0, k_hi, wave, lane, wr, wc);
     f32x16 acc[MI][NJ];
 #pragma unroll
@@ -827,15 +888,16 @@ constexpr int64_t kMaxWgs = (int64_t(1) << 23) - 1;
 // (one or two products) with reduction Kr, from a simple time model: rounds of 256
 // workgroups x the time of one workgroup's share (per 32-step stage at full
 // load, measured: 0.57 us for 128 columns, 0.80 for 192, 0.84 for 256 on the
-// four-wave dW kernel), plus the
+// four-wave kernel), plus the
 // HBM time of writing and re-reading the split partials (4 TB/s).  256-column
-// tiles only for dW (the dX form's epilogue needs the registers).
+// tiles (`wide`) for dW, and for dX when its epilogue is plain (no addend, no
+// bf16 copy: the four-wave kernel's registers hold no more).
 struct Plan {
     int bn;
     int splits;
 };
 
-Plan plan_gemm(int np, const int64_t* R, const int64_t* Cc, int64_t Kr, bool allow_split, bool tr) {
+Plan plan_gemm(int np, const int64_t* R, const int64_t* Cc, int64_t Kr, bool allow_split, bool wide) {
     Plan best{192, 1};
     double best_us = 1e300;
     const int bns[3] = {192, 128, 256};
@@ -844,7 +906,7 @@ Plan plan_gemm(int np, const int64_t* R, const int64_t* Cc, int64_t Kr, bool all
     for (int q = 0; q < np; ++q) out += static_cast<double>(R[q]) * static_cast<double>(Cc[q]);
     for (int b = 0; b < 3; ++b) {
         const int bn = bns[b];
-        if (bn == 256 && !tr) continue;
+        if (bn == 256 && !wide) continue;
         int64_t tiles = 0;
         for (int q = 0; q < np; ++q) tiles += cdiv64(R[q], BM) * cdiv64(Cc[q], bn);
         const int64_t iters = (Kr + BK - 1) / BK;
@@ -862,22 +924,21 @@ Plan plan_gemm(int np, const int64_t* R, const int64_t* Cc, int64_t Kr, bool all
     }
     return best;
 }
-Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split, bool tr) {
-    return plan_gemm(1, &R, &Cc, Kr, allow_split, tr);
+Plan plan_gemm(int64_t R, int64_t Cc, int64_t Kr, bool allow_split, bool wide) {
+    return plan_gemm(1, &R, &Cc, Kr, allow_split, wide);
 }
 
-// The dW form's 256-column tiles run on the four-wave kernel with kDwStages stages.
-constexpr bool kDwFourWaves = true;
-constexpr int kDwStages = 5;
+// 256-column tiles run on the four-wave kernel with kStages4 stages.
+constexpr int kStages4 = 5;
 
 template <bool TR, int BN>
 void launch_tile(const GemmLaunch& gl, int splits, hipStream_t s) {
-    if constexpr (TR && BN == 256 && kDwFourWaves) {
-        hipLaunchKernelGGL(k_gemm_dw4<kDwStages>, dim3(static_cast<unsigned>(gl.tiles * splits)), dim3(256), 0, s,
+    if constexpr (BN == 256) {
+        hipLaunchKernelGGL((k_gemm4<TR, kStages4>), dim3(static_cast<unsigned>(gl.tiles * splits)), dim3(256), 0, s,
                            gl);
-        return;
+    } else {
+        hipLaunchKernelGGL((k_gemm<TR, BN>), dim3(static_cast<unsigned>(gl.tiles * splits)), dim3(512), 0, s, gl);
     }
-    hipLaunchKernelGGL((k_gemm<TR, BN>), dim3(static_cast<unsigned>(gl.tiles * splits)), dim3(512), 0, s, gl);
 }
 
 // One launch over the np products g[0..np) (same reduction split) with the
@@ -899,12 +960,8 @@ bool launch_plan(const GemmArgs* g, int np, const Plan& pl, hipStream_t s) {
     gl.tiles0 = static_cast<int>(t[0]);
     gl.tiles = static_cast<int>(t[0] + t[1]);
     if (pl.bn == 128) launch_tile<TR, 128>(gl, pl.splits, s);
-    else if constexpr (TR) {
-        if (pl.bn == 256) launch_tile<TR, 256>(gl, pl.splits, s);
-        else launch_tile<TR, 192>(gl, pl.splits, s);
-    } else {
-        launch_tile<TR, 192>(gl, pl.splits, s);
-    }
+    else if (pl.bn == 256) launch_tile<TR, 256>(gl, pl.splits, s);
+    else launch_tile<TR, 192>(gl, pl.splits, s);
     return true;
 }
 
@@ -990,8 +1047,10 @@ size_t gemm_dw2_workspace(int64_t M, const DwProduct& a, const DwProduct& b) {
 }
 
 size_t gemm_dx_workspace(int64_t M, int64_t K, int64_t N) {
-    const Plan pl = plan_gemm(M, K, N, true, false);
-    return split_workspace(pl, 1, &M, &K);
+    // either epilogue (the plan with 256-column tiles applies to plain ones)
+    const size_t a = split_workspace(plan_gemm(M, K, N, true, false), 1, &M, &K);
+    const size_t b = split_workspace(plan_gemm(M, K, N, true, true), 1, &M, &K);
+    return a > b ? a : b;
 }
 
 hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, int64_t ldx,
@@ -1013,7 +1072,7 @@ hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, i
     if (ldx <= 0) ldx = K;
     if (ldadd <= 0) ldadd = K;
     // outputs with few tiles (narrow projections) split the reduction as dW does
-    const Plan pl = plan_gemm(M, K, N, true, false);
+    const Plan pl = plan_gemm(M, K, N, true, add == nullptr && out16 == nullptr);
     const bool direct = pl.splits == 1;
     const GemmArgs g{M, K, N, dZ, lddz, W, ldw, direct ? dX : static_cast<float*>(ws), split_range(N, pl.splits),
                      direct ? 1 : 0, accum ? 1 : 0, add, out16, ld16, ldx, ldadd};

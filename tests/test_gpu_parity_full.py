@@ -292,6 +292,32 @@ def test_proj_grad_wide_dw_tiles_sampled():
     say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
 
 
+def test_proj_grad_wide_dx_tiles_sampled():
+    """dX = dZ W^T with an output of 4000 x 8184 over a 2040-long reduction (not a
+    multiple of the 32-step stage): 512 output tiles of 256 x 256, so the planner
+    takes the four-wave kernel for the plain dX epilogue; the last row block and
+    column block are ragged.  Sampled rows, the last one included, against the
+    oracle's plain loops, written and accumulated."""
+    M, K, N = 4000, 8184, 2040
+    say(f"[proj wide dX] M={M} K={K} N={N}")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4244)
+    dZ = torch.randn(M, N, generator=g, device="cuda").to(torch.bfloat16)
+    W = (torch.randn(K, N, generator=g, device="cuda") / 32).to(torch.bfloat16)
+    _, dX = ssm.ssm_proj_grad(None, dZ, W, want_dW=False, want_dX=True)
+    _, dX2 = ssm.ssm_proj_grad(None, dZ, W, want_dW=False, want_dX=True, dX=dX.clone(), accum_dX=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    rows = np.sort(np.concatenate([rng.choice(M - 1, 128, replace=False), [M - 1]]))
+    bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = oracle.proj_dx(bits(dZ), bits(W), rows)
+    idx = torch.as_tensor(rows, device="cuda")
+    rep = {}
+    check("dX[rows]", to_np(dX[idx]), ref, 1e-5, rep)
+    check("dX accum[rows]", to_np(dX2[idx]), 2 * ref, 1e-5, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
 def test_layer_workload_weight_grads_exact_sampled():
     """The layer's weight gradients against the products of the bf16 operands the
     layer hands over, at the layer workload (one launch over the M = 8192 rows).
