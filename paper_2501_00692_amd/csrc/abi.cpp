@@ -33,6 +33,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
 
 constexpr int64_t kMaxGridYZ = 65535;
+constexpr int64_t kMaxGridX = (int64_t(1) << 31) - 1;
 
 // Shape checks shared by forward and gradient.  Fills L (chunk) and nc.
 ssm_status check_desc(const ssm_desc* d, int64_t* L, int64_t* nc) {
@@ -429,6 +430,9 @@ static ssm_status check_unstructured(const ssm_desc* d, int32_t mode, int64_t tb
     if (mode == SSM_TRUNCATED) {
         if (tbar < 1) return fail(SSM_ERR_SHAPE, "truncated mode needs tbar >= 1 (got %lld)", (long long)tbar);
         *trunc = tbar < d->seqlen;
+        // one workgroup per block of tbar steps
+        if (*trunc && (d->seqlen + tbar - 1) / tbar > kMaxGridX)
+            return fail(SSM_ERR_UNSUPPORTED, "seqlen / tbar exceeds the launch grid");
     }
     *L = l;
     return SSM_OK;

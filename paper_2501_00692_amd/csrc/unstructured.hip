@@ -16,8 +16,18 @@
 //                readout cotangents v_t = C_t^T dy_t of every step;
 //   k_un_carry : per sequence, the chunk carries H_{c+1} = Phi_c H_c + hloc_c
 //                and M_{c-1} = Phi_c^T M_c + mloc_c, in order;
-//   k_un_window: truncated mode, the windowed adjoints mubar_i by Horner's rule
-//                over each window (four windows per wave);
+//   k_un_wpre, k_un_wsuf : truncated mode.  The windowed adjoint obeys
+//                mubar_i = u_i + A_{i+1}^T mubar_{i+1} with u_i = v_i - w_i and
+//                w_i = Phi(i, i+tbar)^T v_{i+tbar}, Phi(i, j) = A_j ... A_{i+1} (the
+//                step that leaves the window is taken out as it leaves), so it is
+//                the full gradient's recurrence with v replaced by u.  w_i splits
+//                at the block boundary k (blocks of tbar steps, i < k <= i + tbar):
+//                w_i = Phi(i, k)^T y_{i+tbar} with y_j = Phi(k, j)^T v_j; k_un_wpre
+//                runs the prefix products Phi(k, j) of each block and writes y,
+//                k_un_wsuf the suffix products Phi(i, k)^T and writes u = v - w
+//                over v; both keep the 16 x 16 products in MFMA registers;
+//   k_un_madj  : truncated mode, each chunk's adjoint aggregate of u (the full
+//                mode forms it inside k_un_aggr from v);
 //   k_un_grad  : per chunk, the states recomputed from the carry (kept in LDS),
 //                then the reverse sweep (or the windowed adjoints) and the vjps.
 // Lane layout of a wave: lane l = 16 q + i; i indexes a row of the 16 x 16
@@ -58,7 +68,7 @@ struct UnArgs {
     float* hc;        // [b][nc][16]: local end state, then the carry into the chunk
     float* mc;        // [b][nc][16]: local adjoint aggregate, then the carry from the right
     float* v;         // [b][T][16]: C_t^T dy_t
-    float* mub;       // [b][T][16]: windowed adjoints (truncated mode)
+    float* y;         // [b][T][16]: y_j = Phi(k, j)^T v_j (truncated mode)
 };
 
 // partial over lane (q, i) of row i of B_t x_t (channels [q P/4, (q+1) P/4))
@@ -86,18 +96,52 @@ __device__ __forceinline__ float cty_part(const float* Ct, const float* dyt, int
     return s;
 }
 
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+// M X for a 16 x 16 matrix M [row][col] in memory and X in the MFMA output
+// layout (lane 16 g + j holds X[4g + r][j] in component r): the four
+// v_mfma_f32_16x16x4_f32 of the product each take, in lane 16 q + i, M[i][4q + kb]
+// and X[4q + kb][i] (so instruction kb sums over the columns 4q + kb of M), and the
+// latter is component kb of the lane's own X: the product needs no data movement
+// and its result is again in the output layout.
+__device__ __forceinline__ f4 mul_left(const float* M, f4 X, int i, int q) {
+    const float4 m4 = *reinterpret_cast<const float4*>(M + i * UN + 4 * q);
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.x, X[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.y, X[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.z, X[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.w, X[3], acc, 0, 0, 0);
+    return acc;
+}
+// The same product from the lane's operand values m4 (M[i][4q + kb] for M X,
+// M[4q + kb][i] for M^T X), loaded ahead by the caller.
+__device__ __forceinline__ f4 mul_vals(const float4 m4, f4 X) {
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.x, X[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.y, X[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.z, X[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.w, X[3], acc, 0, 0, 0);
+    return acc;
+}
+// Lane 16 q + i's operand values of M^T X.
+__device__ __forceinline__ float4 vals_t(const float* M, int i, int q) {
+    return make_float4(M[(4 * q) * UN + i], M[(4 * q + 1) * UN + i], M[(4 * q + 2) * UN + i], M[(4 * q + 3) * UN + i]);
+}
+__device__ __forceinline__ f4 identity16(int i, int q) {
+    f4 e;
+    for (int r = 0; r < 4; ++r) e[r] = (4 * q + r == i) ? 1.f : 0.f;
+    return e;
+}
+
 // grid (nc, b), 64 threads
 __global__ __launch_bounds__(64) void k_un_aggr(const UnArgs a) {
-    __shared__ float sphi[UN][UN + 1];
     __shared__ float sh[UN];
     __shared__ float sv[UN];
     const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
     const int64_t c = blockIdx.x, bb = blockIdx.y;
     const int64_t s0 = c * a.L, s1 = min(s0 + a.L, a.T);
     // Phi in the MFMA output layout: lane (q, i) holds Phi[4q + r][i], r = 0..3
-    typedef float f4 __attribute__((ext_vector_type(4)));
-    f4 phi;
-    for (int r = 0; r < 4; ++r) phi[r] = (4 * q + r == i) ? 1.f : 0.f;
+    f4 phi = identity16(i, q);
     float h = 0.f, m = 0.f;  // replicated: lane (q, i) holds h[i], m[i]
     if (q == 0) sh[i] = 0.f;
     __syncthreads();
@@ -109,20 +153,12 @@ __global__ __launch_bounds__(64) void k_un_aggr(const UnArgs a) {
         float part = a4.x * sh[4 * q] + a4.y * sh[4 * q + 1] + a4.z * sh[4 * q + 2] + a4.w * sh[4 * q + 3];
         part += bx_part(a.B + row * UN * a.P, a.x + row * a.P, a.P, q, i);
         h = qsum(part);
-        // Phi <- A_t Phi: B operands from the transposed staging of Phi
-        for (int r = 0; r < 4; ++r) sphi[4 * q + r][i] = phi[r];
-        __syncthreads();
-        f4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int kb = 0; kb < 4; ++kb) {
-            const float av = At[i * UN + 4 * kb + q];  // A_t[i][4kb + q]
-            const float bv = sphi[4 * kb + q][i];      // Phi[4kb + q][i]
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
-        }
-        phi = acc;
+        // Phi <- A_t Phi (operands in registers, see mul_left)
+        phi = mul_left(At, phi, i, q);
         // v_t = C_t^T dy_t, and the adjoint aggregate m += Phi_t^T v_t
         const float vt = qsum(cty_part(a.C + row * a.P * UN, a.dy + row * a.P, a.P, q, i));
         if (q == 0) a.v[row * UN + i] = vt;
-        __syncthreads();  // every read of sphi and sh of this step is done
+        __syncthreads();  // every read of sh of this step is done
         if (q == 0) {
             sh[i] = h;
             sv[i] = vt;
@@ -166,7 +202,6 @@ __global__ __launch_bounds__(64) void k_un_carry(const UnArgs a) {
         __syncthreads();
     }
     if (a.h_last && q == 0) a.h_last[bb * UN + i] = sv[i];
-    if (a.trunc) return;
     __syncthreads();
     if (q == 0) sv[i] = 0.f;
     __syncthreads();
@@ -187,35 +222,98 @@ __global__ __launch_bounds__(64) void k_un_carry(const UnArgs a) {
     if (a.dh0 && q == 0) a.dh0[bb * UN + i] = sv[i];
 }
 
-// grid (ceil(T / 4), b), 64 threads: lane (w, j) holds component j of window
-// i = 4 blockIdx.x + w; Horner from the window's last step back to i.
-__global__ __launch_bounds__(64) void k_un_window(const UnArgs a) {
-    __shared__ float su[4][UN];
-    const int lane = threadIdx.x, j = lane & 15, w = lane >> 4;
+// grid (blocks - 1, b), 64 threads: block beta >= 1, steps [k, k + tbar) with
+// k = beta tbar; Pre = Phi(k, j) = A_j ... A_{k+1} in registers (output layout),
+// y_j = Pre^T v_j (lane (g, j'): sum_r Pre[4g + r][j'] v_j[4g + r], summed over g).
+__global__ __launch_bounds__(64) void k_un_wpre(const UnArgs a) {
+    const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
     const int64_t bb = blockIdx.y;
-    const int64_t i0 = static_cast<int64_t>(blockIdx.x) * 4;
-    const int64_t iw = i0 + w;
-    const bool valid = iw < a.T;
-    const int64_t e = valid ? min(iw + a.tbar - 1, a.T - 1) : 0;
-    // the windows of a wave have different lengths near the end: every lane runs
-    // the longest one, with the steps outside its own window leaving u unchanged
-    const int64_t emax = min(i0 + 3 + a.tbar - 1, a.T - 1);
-    float u = 0.f;
-    for (int64_t t = emax; t >= i0; --t) {
-        // u <- v_t + A_{t+1}^T u inside the window (t in [iw, e]); A_{t+1}^T u is
-        // zero at the window's last step
-        su[w][j] = u;
-        __syncthreads();
-        float nu = 0.f;
-        if (t < e) {
-            const float* An = a.A + (bb * a.T + t + 1) * UN * UN;
-            for (int k = 0; k < UN; ++k) nu = fmaf(An[k * UN + j], su[w][k], nu);
+    const int64_t k = (static_cast<int64_t>(blockIdx.x) + 1) * a.tbar;
+    if (k >= a.T) return;
+    const int64_t k1 = min(k + a.tbar, a.T);
+    f4 pre = identity16(i, q);
+    // A_j's operand values and v_j of step j, loaded one step ahead (the last step
+    // reloads its own; A_k is loaded and not used)
+    const int64_t r0 = bb * a.T + k;
+    float4 an = *reinterpret_cast<const float4*>(a.A + r0 * UN * UN + i * UN + 4 * q);
+    float4 vn = *reinterpret_cast<const float4*>(a.v + r0 * UN + 4 * q);
+    for (int64_t j = k; j < k1; ++j) {
+        const int64_t row = bb * a.T + j;
+        const float4 ac = an, v4 = vn;
+        const int64_t nx = j + 1 < k1 ? row + 1 : row;
+        an = *reinterpret_cast<const float4*>(a.A + nx * UN * UN + i * UN + 4 * q);
+        vn = *reinterpret_cast<const float4*>(a.v + nx * UN + 4 * q);
+        if (j > k) pre = mul_vals(ac, pre);
+        const float y = qsum(pre[0] * v4.x + pre[1] * v4.y + pre[2] * v4.z + pre[3] * v4.w);
+        if (q == 0) a.y[row * UN + i] = y;
+    }
+}
+
+// Sum over the 16 lanes of each quarter of the wave.
+__device__ __forceinline__ float sum16(float v) {
+    v += __shfl_xor(v, 1);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 4);
+    v += __shfl_xor(v, 8);
+    return v;
+}
+
+// grid (blocks, b), 64 threads: block beta, steps [beta tbar, k) with k =
+// (beta + 1) tbar < T; S = Phi(i, k)^T = A_{i+1}^T S(i + 1), S(k) = I, in registers
+// (output layout: lane (g, n) holds S[4g + r][n]); w_i = S y_{i+tbar} (lane (g, n):
+// S[4g + r][n] y[n], summed over n), and v_i -= w_i while i + tbar < T.
+__global__ __launch_bounds__(64) void k_un_wsuf(const UnArgs a) {
+    const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
+    const int64_t bb = blockIdx.y;
+    const int64_t k0 = static_cast<int64_t>(blockIdx.x) * a.tbar;
+    const int64_t k = k0 + a.tbar;
+    if (k >= a.T) return;
+    f4 sm = identity16(i, q);
+    // A_{t+1}'s operand values and y_{t+tbar} of the next step, loaded one step
+    // ahead (clamped to valid rows; a y past the end is not used)
+    const int64_t base = bb * a.T;
+    float4 an = vals_t(a.A + (base + k) * UN * UN, i, q);
+    float yv = a.y[(base + min(k - 1 + a.tbar, a.T - 1)) * UN + i];
+    for (int64_t t = k - 1; t >= k0; --t) {
+        const int64_t row = base + t;
+        const float4 ac = an;
+        const float yn = yv;
+        const int64_t tn = t > k0 ? t - 1 : t;
+        an = vals_t(a.A + (base + tn + 1) * UN * UN, i, q);
+        yv = a.y[(base + min(tn + a.tbar, a.T - 1)) * UN + i];
+        sm = mul_vals(ac, sm);
+        if (t + a.tbar >= a.T) continue;  // wave-uniform
+        float w[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) w[r] = sum16(sm[r] * yn);
+        if (i < 4) {
+            const float wr = i == 0 ? w[0] : i == 1 ? w[1] : i == 2 ? w[2] : w[3];
+            a.v[row * UN + 4 * q + i] -= wr;
         }
-        const bool in = valid && t >= iw && t <= e;
-        if (in) u = a.v[(bb * a.T + t) * UN + j] + nu;
+    }
+}
+
+// grid (nc, b), 64 threads: the chunk's adjoint aggregate of u (v after
+// k_un_wsuf), as k_un_aggr forms it from v in full mode: rho_e = u_e,
+// rho_t = u_t + A_{t+1}^T rho_{t+1}, mloc = A_s^T rho_s.
+__global__ __launch_bounds__(64) void k_un_madj(const UnArgs a) {
+    __shared__ float sr[UN];
+    const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
+    const int64_t c = blockIdx.x, bb = blockIdx.y;
+    const int64_t s0 = c * a.L, s1 = min(s0 + a.L, a.T);
+    float carry = 0.f;  // A_{t+1}^T rho_{t+1} (replicated)
+    for (int64_t t = s1 - 1; t >= s0; --t) {
+        const int64_t row = bb * a.T + t;
+        const float rho = a.v[row * UN + i] + carry;
+        if (q == 0) sr[i] = rho;
+        __syncthreads();
+        const float* At = a.A + row * UN * UN;
+        float part = 0.f;
+        for (int r = 0; r < 4; ++r) part = fmaf(At[(4 * q + r) * UN + i], sr[4 * q + r], part);
+        carry = qsum(part);
         __syncthreads();
     }
-    if (valid) a.mub[(bb * a.T + iw) * UN + j] = u;
+    if (q == 0) a.mc[(bb * a.nc + c) * UN + i] = carry;
 }
 
 // grid (nc, b), 64 threads; LDS holds the chunk's states h_{s-1} .. h_e.
@@ -242,11 +340,13 @@ __global__ __launch_bounds__(64) void k_un_grad(const UnArgs a) {
         if (q == 0) shs[k + 1][i] = hn;
         __syncthreads();
     }
-    float mun = a.trunc ? 0.f : a.mc[cb * UN + i];  // A_{t+1}^T mu_{t+1} (replicated)
+    // A_{t+1}^T mu_{t+1} (replicated); in truncated mode v holds u and the
+    // recurrence gives the windowed adjoint
+    float mun = a.mc[cb * UN + i];
     for (int64_t t = s1 - 1; t >= s0; --t) {
         const int64_t row = bb * a.T + t;
         const int k = static_cast<int>(t - s0);
-        const float mu = a.trunc ? a.mub[row * UN + i] : a.v[row * UN + i] + mun;
+        const float mu = a.v[row * UN + i] + mun;
         if (q == 0) smu[i] = mu;
         __syncthreads();
         // dA_t[r][4(l%4) .. +3] = mu[r] h_{t-1}[..], r = l / 4
@@ -278,7 +378,7 @@ __global__ __launch_bounds__(64) void k_un_grad(const UnArgs a) {
             a.dx[row * P + p] = sx;
         }
         // A_t^T mu for the step before (lane (q, j): rows 4q..4q+3 of column j)
-        if (!a.trunc) {
+        {
             const float* At = a.A + row * UN * UN;
             float part = 0.f;
             for (int r = 0; r < 4; ++r) part = fmaf(At[(4 * q + r) * UN + i], smu[4 * q + r], part);
@@ -329,20 +429,30 @@ hipError_t launch_unstructured_grad(const UnstructuredProblem& u, void* ws, hipS
     w += up(size_t(a.nb * a.nc) * UN * 4);
     a.v = reinterpret_cast<float*>(w);
     w += up(size_t(a.nb * a.T) * UN * 4);
-    a.mub = u.trunc ? reinterpret_cast<float*>(w) : nullptr;
+    a.y = u.trunc ? reinterpret_cast<float*>(w) : nullptr;
     const dim3 gc(static_cast<unsigned>(a.nc), static_cast<unsigned>(a.nb));
     {
         SSMK_TIMED("un_aggr", s);
         hipLaunchKernelGGL(k_un_aggr, gc, dim3(64), 0, s, a);
     }
+    if (a.trunc) {
+        const int64_t nblk = (a.T + a.tbar - 1) / a.tbar;  // at least 2 (tbar < T)
+        {
+            SSMK_TIMED("un_wpre", s);
+            hipLaunchKernelGGL(k_un_wpre, dim3(static_cast<unsigned>(nblk - 1), static_cast<unsigned>(a.nb)),
+                               dim3(64), 0, s, a);
+        }
+        {
+            SSMK_TIMED("un_wsuf", s);
+            hipLaunchKernelGGL(k_un_wsuf, dim3(static_cast<unsigned>(nblk), static_cast<unsigned>(a.nb)), dim3(64),
+                               0, s, a);
+        }
+        SSMK_TIMED("un_madj", s);
+        hipLaunchKernelGGL(k_un_madj, gc, dim3(64), 0, s, a);
+    }
     {
         SSMK_TIMED("un_carry", s);
         hipLaunchKernelGGL(k_un_carry, dim3(static_cast<unsigned>(a.nb)), dim3(64), 0, s, a);
-    }
-    if (a.trunc) {
-        SSMK_TIMED("un_window", s);
-        hipLaunchKernelGGL(k_un_window, dim3(static_cast<unsigned>((a.T + 3) / 4), static_cast<unsigned>(a.nb)),
-                           dim3(64), 0, s, a);
     }
     SSMK_TIMED("un_grad", s);
     switch (a.L) {
