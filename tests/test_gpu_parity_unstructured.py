@@ -91,3 +91,34 @@ def test_unstructured_workload_truncated_sampled():
     for k in ("dA", "dB", "dx"):
         check(f"{k}[sampled]", to_np(o[k])[bi], ref[k], TOL_F32, rep)
     say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
+def test_unstructured_truncated_norm_preserving_transitions():
+    """Transitions that neither grow nor shrink the state (0.999 times an
+    orthogonal matrix, spectral radius 0.999): each step's readout enters the
+    windowed adjoint and is taken out again tbar steps later at nearly its
+    original size, so a cancellation error would build up over the 40 windows of
+    the sequence.  b = 1, T = 8,000, P = 16, tbar = 200, chunks of 64 (the windows
+    straddle chunk and block edges); the A-, B- and x-path vjps at sampled steps
+    against the literal window sums, dC everywhere."""
+    b, T, P, tbar, N = 1, 8000, 16, 200, 16
+    say(f"[unstructured truncated, norm-preserving] b={b} T={T} P={P} tbar={tbar}")
+    inp = make_unstructured_inputs(b, T, P, 692204, device="cuda")
+    g = torch.Generator(device="cpu")
+    g.manual_seed(692205)
+    q, r = torch.linalg.qr(torch.randn(b * T, N, N, generator=g, dtype=torch.float64))
+    q = q * torch.sign(torch.diagonal(r, dim1=-2, dim2=-1)).unsqueeze(-2)
+    inp["A"] = (0.999 * q).reshape(b, T, N, N).to(torch.float32).contiguous().to("cuda")
+    o = _gpu(inp, tbar, 64)
+    h = _host(inp)
+    rep = {}
+    full = un_bptt(h["A"], h["B"], h["C"], h["x"], h["dy"], want_dh0=False)
+    check("dC", to_np(o["dC"]), full["dC"], TOL_F32, rep)
+    rng = np.random.default_rng(10)
+    steps = [(0, 0), (0, T - 1), (0, T - tbar), (0, T - tbar - 1), (0, tbar), (0, 2 * tbar - 1)]
+    steps += [(0, int(t)) for t in rng.integers(0, T, 18)]
+    ref = un_trunc_at(h["A"], h["B"], h["C"], h["x"], h["dy"], tbar, steps)
+    bi = np.array([s[0] for s in steps]), np.array([s[1] for s in steps])
+    for k in ("dA", "dB", "dx"):
+        check(f"{k}[sampled]", to_np(o[k])[bi], ref[k], TOL_F32, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
