@@ -418,6 +418,25 @@ def unstructured_measure(ssm, torch, steps, warmup, chunk=0):
     return res
 
 
+def copy_bandwidth(torch, nbytes=1 << 30, reps=10):
+    """Achievable HBM bandwidth as context for the HBM fractions: a plain device
+    copy of nbytes (read + write counted), timed with events over reps copies."""
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbps = 2 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbps
+
+
 def head_measure(ssm, torch, steps, warmup):
     """The language head with its loss at the head workload: per-call time,
     tokens/s, the MFMA fraction of its three products (logits, dU, dOmega:
@@ -535,6 +554,7 @@ def main():
         extra["ms_per_step_warm"] = _timed_each(step, 10, 1, torch)
         extra["ms_per_step_cold"] = _timed_each(step, 10, 1, torch, flush=lambda: scratch.fill_(1))
         del scratch
+        extra["hbm_copy_GBps"] = copy_bandwidth(torch)
     del inp, calls
     torch.cuda.empty_cache()
 

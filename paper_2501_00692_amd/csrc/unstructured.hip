@@ -30,6 +30,10 @@
 //                mode forms it inside k_un_aggr from v);
 //   k_un_grad  : per chunk, the states recomputed from the carry (kept in LDS),
 //                then the reverse sweep (or the windowed adjoints) and the vjps.
+//   k_un_proj  : per step, the two reductions over the P channels that the
+//                sequential passes need: bx_t = B_t x_t and v_t = C_t^T dy_t
+//                (fully parallel, ahead of the chunk passes, so that these walk
+//                only A_t and two 16-vectors per step, loaded a step ahead).
 // Lane layout of a wave: lane l = 16 q + i; i indexes a row of the 16 x 16
 // matrices, q one of four quarters of the reduction (matrix columns 4q..4q+3,
 // or a quarter of the P channels), summed across quarters with two xor
@@ -69,6 +73,7 @@ struct UnArgs {
     float* mc;        // [b][nc][16]: local adjoint aggregate, then the carry from the right
     float* v;         // [b][T][16]: C_t^T dy_t
     float* y;         // [b][T][16]: y_j = Phi(k, j)^T v_j (truncated mode)
+    float* bx;        // [b][T][16]: B_t x_t
 };
 
 // partial over lane (q, i) of row i of B_t x_t (channels [q P/4, (q+1) P/4))
@@ -88,33 +93,75 @@ __device__ __forceinline__ float bx_part(const float* Bt, const float* xt, int64
     return s;
 }
 
-// partial over lane (q, i) of (C_t^T dy_t)[i] (channels [q P/4, (q+1) P/4))
-__device__ __forceinline__ float cty_part(const float* Ct, const float* dyt, int64_t P, int q, int i) {
-    const int64_t p0 = q * (P / 4), n = P / 4;
-    float s = 0.f;
-    for (int64_t p = 0; p < n; ++p) s = fmaf(Ct[(p0 + p) * UN + i], dyt[p0 + p], s);
-    return s;
+// h[4q + r] from the lane that holds it (vectors of 16 are replicated in the
+// four quarters; lane 4q + r of the first quarter has component 4q + r).
+__device__ __forceinline__ float4 quarter_of(float h, int q) {
+    return make_float4(__shfl(h, 4 * q), __shfl(h, 4 * q + 1), __shfl(h, 4 * q + 2), __shfl(h, 4 * q + 3));
+}
+
+// grid (ceil(T / 4), b), 64 threads: four steps per wave, one at a time.
+// bx_t = B_t x_t: instruction j reads rows 4j..4j+3 of B_t (row 4j + g in lanes
+// 16 g .. 16 g + 15, four channels per lane, 64 channels per pass), and each
+// row's partial sums are added over its 16 lanes.  v_t = C_t^T dy_t: lane l reads
+// C_t[p][4(l%4) .. +3] for p = l/4 + 16 k (64 lanes cover 16 rows of C_t per
+// pass), weighted by dy_t[p], and the 16 lanes with the same l%4 are added.
+// Reads of B_t and C_t are contiguous across the wave.
+__global__ __launch_bounds__(64) void k_un_proj(const UnArgs a) {
+    const int lane = threadIdx.x, g = lane >> 4, sub = lane & 15, cq = lane & 3;
+    const int64_t bb = blockIdx.y, P = a.P;
+    for (int w = 0; w < 4; ++w) {
+        const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + w;
+        if (t >= a.T) return;  // wave-uniform
+        const int64_t row = bb * a.T + t;
+        const float* Bt = a.B + row * UN * P;
+        const float* xt = a.x + row * P;
+        const float* Ct = a.C + row * P * UN;
+        const float* dyt = a.dy + row * P;
+        float sb[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int64_t p = 4 * sub; p < P; p += 64) {
+            const float4 x4 = *reinterpret_cast<const float4*>(xt + p);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float4 b4 = *reinterpret_cast<const float4*>(Bt + (4 * j + g) * P + p);
+                sb[j] = fmaf(b4.x, x4.x, fmaf(b4.y, x4.y, fmaf(b4.z, x4.z, fmaf(b4.w, x4.w, sb[j]))));
+            }
+        }
+        float sc[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int64_t pr = lane >> 2; pr < P; pr += 16) {
+            const float4 c4 = *reinterpret_cast<const float4*>(Ct + pr * UN + 4 * cq);
+            const float d = dyt[pr];
+            sc[0] = fmaf(c4.x, d, sc[0]);
+            sc[1] = fmaf(c4.y, d, sc[1]);
+            sc[2] = fmaf(c4.z, d, sc[2]);
+            sc[3] = fmaf(c4.w, d, sc[3]);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            for (int m = 1; m < 16; m <<= 1) sb[j] += __shfl_xor(sb[j], m);
+            for (int m = 4; m < 64; m <<= 1) sc[j] += __shfl_xor(sc[j], m);
+        }
+        // lane 16 g + 0 holds bx rows 4j + g; lanes 0..3 hold v[4 cq + j]
+        if (sub == 0) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) a.bx[row * UN + 4 * j + g] = sb[j];
+        }
+        if (lane < 4) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) a.v[row * UN + 4 * cq + j] = sc[j];
+        }
+    }
 }
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-// M X for a 16 x 16 matrix M [row][col] in memory and X in the MFMA output
-// layout (lane 16 g + j holds X[4g + r][j] in component r): the four
-// v_mfma_f32_16x16x4_f32 of the product each take, in lane 16 q + i, M[i][4q + kb]
-// and X[4q + kb][i] (so instruction kb sums over the columns 4q + kb of M), and the
-// latter is component kb of the lane's own X: the product needs no data movement
-// and its result is again in the output layout.
-__device__ __forceinline__ f4 mul_left(const float* M, f4 X, int i, int q) {
-    const float4 m4 = *reinterpret_cast<const float4*>(M + i * UN + 4 * q);
-    f4 acc = {0.f, 0.f, 0.f, 0.f};
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.x, X[0], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.y, X[1], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.z, X[2], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.w, X[3], acc, 0, 0, 0);
-    return acc;
-}
-// The same product from the lane's operand values m4 (M[i][4q + kb] for M X,
-// M[4q + kb][i] for M^T X), loaded ahead by the caller.
+// M X for a 16 x 16 matrix M and X in the MFMA output layout (lane 16 g + j holds
+// X[4g + r][j] in component r): the four v_mfma_f32_16x16x4_f32 of the product
+// each take, in lane 16 q + i, M[i][4q + kb] and X[4q + kb][i] (so instruction kb
+// sums over the columns 4q + kb of M), and the latter is component kb of the
+// lane's own X: the product needs no data movement and its result is again in
+// the output layout.  m4 holds the lane's operand values of M (M[i][4q + kb], a
+// float4 of row i; M[4q + kb][i] for M^T X, see vals_t), loaded ahead by the
+// caller.
 __device__ __forceinline__ f4 mul_vals(const float4 m4, f4 X) {
     f4 acc = {0.f, 0.f, 0.f, 0.f};
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(m4.x, X[0], acc, 0, 0, 0);
@@ -135,40 +182,34 @@ __device__ __forceinline__ f4 identity16(int i, int q) {
 
 // grid (nc, b), 64 threads
 __global__ __launch_bounds__(64) void k_un_aggr(const UnArgs a) {
-    __shared__ float sh[UN];
-    __shared__ float sv[UN];
     const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
     const int64_t c = blockIdx.x, bb = blockIdx.y;
     const int64_t s0 = c * a.L, s1 = min(s0 + a.L, a.T);
     // Phi in the MFMA output layout: lane (q, i) holds Phi[4q + r][i], r = 0..3
     f4 phi = identity16(i, q);
     float h = 0.f, m = 0.f;  // replicated: lane (q, i) holds h[i], m[i]
-    if (q == 0) sh[i] = 0.f;
-    __syncthreads();
+    // step t's A_t[i][4q..4q+3], bx_t[i] and v_t[4q..4q+3], loaded a step ahead
+    // (the last step reloads its own)
+    const int64_t r0 = bb * a.T + s0;
+    float4 an = *reinterpret_cast<const float4*>(a.A + r0 * UN * UN + i * UN + 4 * q);
+    float bn = a.bx[r0 * UN + i];
+    float4 vn = *reinterpret_cast<const float4*>(a.v + r0 * UN + 4 * q);
     for (int64_t t = s0; t < s1; ++t) {
         const int64_t row = bb * a.T + t;
-        const float* At = a.A + row * UN * UN;
+        const float4 a4 = an, v4 = vn;
+        const float bxt = bn;
+        const int64_t nx = t + 1 < s1 ? row + 1 : row;
+        an = *reinterpret_cast<const float4*>(a.A + nx * UN * UN + i * UN + 4 * q);
+        bn = a.bx[nx * UN + i];
+        vn = *reinterpret_cast<const float4*>(a.v + nx * UN + 4 * q);
         // h <- A_t h + B_t x_t
-        const float4 a4 = *reinterpret_cast<const float4*>(At + i * UN + 4 * q);
-        float part = a4.x * sh[4 * q] + a4.y * sh[4 * q + 1] + a4.z * sh[4 * q + 2] + a4.w * sh[4 * q + 3];
-        part += bx_part(a.B + row * UN * a.P, a.x + row * a.P, a.P, q, i);
-        h = qsum(part);
-        // Phi <- A_t Phi (operands in registers, see mul_left)
-        phi = mul_left(At, phi, i, q);
-        // v_t = C_t^T dy_t, and the adjoint aggregate m += Phi_t^T v_t
-        const float vt = qsum(cty_part(a.C + row * a.P * UN, a.dy + row * a.P, a.P, q, i));
-        if (q == 0) a.v[row * UN + i] = vt;
-        __syncthreads();  // every read of sh of this step is done
-        if (q == 0) {
-            sh[i] = h;
-            sv[i] = vt;
-        }
-        __syncthreads();
+        const float4 hq = quarter_of(h, q);
+        h = qsum(a4.x * hq.x + a4.y * hq.y + a4.z * hq.z + a4.w * hq.w) + bxt;
+        // Phi <- A_t Phi (operands in registers, see mul_vals)
+        phi = mul_vals(a4, phi);
         if (!a.trunc) {
-            // lane (q, j): sum_r Phi[4q + r][j] v[4q + r]
-            float pm = 0.f;
-            for (int r = 0; r < 4; ++r) pm = fmaf(phi[r], sv[4 * q + r], pm);
-            m += qsum(pm);
+            // the adjoint aggregate m += Phi_t^T v_t; lane (q, j): sum_r Phi[4q + r][j] v[4q + r]
+            m += qsum(phi[0] * v4.x + phi[1] * v4.y + phi[2] * v4.z + phi[3] * v4.w);
         }
     }
     const int64_t cb = bb * a.nc + c;
@@ -179,47 +220,47 @@ __global__ __launch_bounds__(64) void k_un_aggr(const UnArgs a) {
     }
 }
 
-// grid (b), 64 threads: lanes (q, i) as above; directions one after the other
+// grid (b), 64 threads: lanes (q, i) as above; directions one after the other;
+// each chunk's Phi and aggregate loaded a chunk ahead.
 __global__ __launch_bounds__(64) void k_un_carry(const UnArgs a) {
-    __shared__ float sv[UN];
     const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
     const int64_t bb = blockIdx.x;
-    float H = a.h0 ? a.h0[bb * UN + i] : 0.f;
-    if (q == 0) sv[i] = H;
-    __syncthreads();
-    for (int64_t c = 0; c < a.nc; ++c) {
-        const int64_t cb = bb * a.nc + c;
-        const float* P = a.phi + cb * UN * UN;
-        // H_{c+1} = Phi_c H_c + hloc_c  (lane (q, i): columns 4q..4q+3 of row i)
-        float part = 0.f;
-        for (int r = 0; r < 4; ++r) part = fmaf(P[i * UN + 4 * q + r], sv[4 * q + r], part);
-        const float Hn = qsum(part) + a.hc[cb * UN + i];
-        __syncthreads();
-        if (q == 0) {
-            a.hc[cb * UN + i] = sv[i];  // the carry into chunk c
-            sv[i] = Hn;
-        }
-        __syncthreads();
+    const int64_t nc = a.nc, c0 = bb * nc;
+    float H = a.h0 ? a.h0[bb * UN + i] : 0.f;  // replicated
+    // H_{c+1} = Phi_c H_c + hloc_c  (lane (q, i): columns 4q..4q+3 of row i)
+    float4 pn = *reinterpret_cast<const float4*>(a.phi + c0 * UN * UN + i * UN + 4 * q);
+    float hn = a.hc[c0 * UN + i];
+    for (int64_t c = 0; c < nc; ++c) {
+        const int64_t cb = c0 + c;
+        const float4 p4 = pn;
+        const float hl = hn;
+        const int64_t nx = c + 1 < nc ? cb + 1 : cb;
+        pn = *reinterpret_cast<const float4*>(a.phi + nx * UN * UN + i * UN + 4 * q);
+        hn = a.hc[nx * UN + i];
+        const float4 hq = quarter_of(H, q);
+        const float Hn = qsum(p4.x * hq.x + p4.y * hq.y + p4.z * hq.z + p4.w * hq.w) + hl;
+        if (q == 0) a.hc[cb * UN + i] = H;  // the carry into chunk c (hloc_c was read above)
+        H = Hn;
     }
-    if (a.h_last && q == 0) a.h_last[bb * UN + i] = sv[i];
-    __syncthreads();
-    if (q == 0) sv[i] = 0.f;
-    __syncthreads();
-    for (int64_t c = a.nc - 1; c >= 0; --c) {
-        const int64_t cb = bb * a.nc + c;
-        const float* P = a.phi + cb * UN * UN;
-        // M_{c-1} = Phi_c^T M_c + mloc_c  (lane (q, j): rows 4q..4q+3 of column j)
-        float part = 0.f;
-        for (int r = 0; r < 4; ++r) part = fmaf(P[(4 * q + r) * UN + i], sv[4 * q + r], part);
-        const float Mn = qsum(part) + a.mc[cb * UN + i];
-        __syncthreads();
-        if (q == 0) {
-            a.mc[cb * UN + i] = sv[i];  // the carry from the right into chunk c
-            sv[i] = Mn;
-        }
-        __syncthreads();
+    if (a.h_last && q == 0) a.h_last[bb * UN + i] = H;
+    // M_{c-1} = Phi_c^T M_c + mloc_c  (lane (q, j): rows 4q..4q+3 of column j)
+    float M = 0.f;
+    const int64_t cl = c0 + nc - 1;
+    float4 qn = vals_t(a.phi + cl * UN * UN, i, q);
+    float mn = a.mc[cl * UN + i];
+    for (int64_t c = nc - 1; c >= 0; --c) {
+        const int64_t cb = c0 + c;
+        const float4 p4 = qn;
+        const float ml = mn;
+        const int64_t nx = c > 0 ? cb - 1 : cb;
+        qn = vals_t(a.phi + nx * UN * UN, i, q);
+        mn = a.mc[nx * UN + i];
+        const float4 mq = quarter_of(M, q);
+        const float Mn = qsum(p4.x * mq.x + p4.y * mq.y + p4.z * mq.z + p4.w * mq.w) + ml;
+        if (q == 0) a.mc[cb * UN + i] = M;  // the carry from the right into chunk c
+        M = Mn;
     }
-    if (a.dh0 && q == 0) a.dh0[bb * UN + i] = sv[i];
+    if (a.dh0 && q == 0) a.dh0[bb * UN + i] = M;
 }
 
 // grid (blocks - 1, b), 64 threads: block beta >= 1, steps [k, k + tbar) with
@@ -393,7 +434,7 @@ __global__ __launch_bounds__(64) void k_un_grad(const UnArgs a) {
 size_t unstructured_workspace(int64_t nb, int64_t T, int64_t L, bool trunc) {
     const int64_t nc = (T + L - 1) / L;
     auto up = [](size_t v) { return (v + 255) & ~size_t(255); };
-    size_t s = up(size_t(nb * nc) * UN * UN * 4) + 2 * up(size_t(nb * nc) * UN * 4) + up(size_t(nb * T) * UN * 4);
+    size_t s = up(size_t(nb * nc) * UN * UN * 4) + 2 * up(size_t(nb * nc) * UN * 4) + 2 * up(size_t(nb * T) * UN * 4);
     if (trunc) s += up(size_t(nb * T) * UN * 4);
     return s;
 }
@@ -429,8 +470,15 @@ hipError_t launch_unstructured_grad(const UnstructuredProblem& u, void* ws, hipS
     w += up(size_t(a.nb * a.nc) * UN * 4);
     a.v = reinterpret_cast<float*>(w);
     w += up(size_t(a.nb * a.T) * UN * 4);
+    a.bx = reinterpret_cast<float*>(w);
+    w += up(size_t(a.nb * a.T) * UN * 4);
     a.y = u.trunc ? reinterpret_cast<float*>(w) : nullptr;
     const dim3 gc(static_cast<unsigned>(a.nc), static_cast<unsigned>(a.nb));
+    {
+        SSMK_TIMED("un_proj", s);
+        hipLaunchKernelGGL(k_un_proj, dim3(static_cast<unsigned>((a.T + 3) / 4), static_cast<unsigned>(a.nb)),
+                           dim3(64), 0, s, a);
+    }
     {
         SSMK_TIMED("un_aggr", s);
         hipLaunchKernelGGL(k_un_aggr, gc, dim3(64), 0, s, a);
