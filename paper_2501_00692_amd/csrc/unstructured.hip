@@ -76,23 +76,6 @@ struct UnArgs {
     float* bx;        // [b][T][16]: B_t x_t
 };
 
-// partial over lane (q, i) of row i of B_t x_t (channels [q P/4, (q+1) P/4))
-__device__ __forceinline__ float bx_part(const float* Bt, const float* xt, int64_t P, int q, int i) {
-    const int64_t p0 = q * (P / 4), n = P / 4;
-    const float* br = Bt + i * P + p0;
-    const float* xr = xt + p0;
-    float s = 0.f;
-    for (int64_t p = 0; p < n; p += 4) {
-        const float4 b4 = *reinterpret_cast<const float4*>(br + p);
-        const float4 x4 = *reinterpret_cast<const float4*>(xr + p);
-        s = fmaf(b4.x, x4.x, s);
-        s = fmaf(b4.y, x4.y, s);
-        s = fmaf(b4.z, x4.z, s);
-        s = fmaf(b4.w, x4.w, s);
-    }
-    return s;
-}
-
 // h[4q + r] from the lane that holds it (vectors of 16 are replicated in the
 // four quarters; lane 4q + r of the first quarter has component 4q + r).
 __device__ __forceinline__ float4 quarter_of(float h, int q) {
@@ -220,12 +203,35 @@ __global__ __launch_bounds__(64) void k_un_aggr(const UnArgs a) {
     }
 }
 
-// grid (b), 64 threads: lanes (q, i) as above; directions one after the other;
-// each chunk's Phi and aggregate loaded a chunk ahead.
+// grid (2 b), 64 threads: lanes (q, i) as above; workgroup 2 bb + dir walks
+// sequence bb forwards (dir 0) or backwards (dir 1); each chunk's Phi and
+// aggregate loaded a chunk ahead.
 __global__ __launch_bounds__(64) void k_un_carry(const UnArgs a) {
     const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
-    const int64_t bb = blockIdx.x;
+    const int64_t bb = blockIdx.x >> 1;
+    const int dir = blockIdx.x & 1;
     const int64_t nc = a.nc, c0 = bb * nc;
+    if (dir == 1) {
+        // M_{c-1} = Phi_c^T M_c + mloc_c  (lane (q, j): rows 4q..4q+3 of column j)
+        float M = 0.f;
+        const int64_t cl = c0 + nc - 1;
+        float4 qn = vals_t(a.phi + cl * UN * UN, i, q);
+        float mn = a.mc[cl * UN + i];
+        for (int64_t c = nc - 1; c >= 0; --c) {
+            const int64_t cb = c0 + c;
+            const float4 p4 = qn;
+            const float ml = mn;
+            const int64_t nx = c > 0 ? cb - 1 : cb;
+            qn = vals_t(a.phi + nx * UN * UN, i, q);
+            mn = a.mc[nx * UN + i];
+            const float4 mq = quarter_of(M, q);
+            const float Mn = qsum(p4.x * mq.x + p4.y * mq.y + p4.z * mq.z + p4.w * mq.w) + ml;
+            if (q == 0) a.mc[cb * UN + i] = M;  // the carry from the right into chunk c
+            M = Mn;
+        }
+        if (a.dh0 && q == 0) a.dh0[bb * UN + i] = M;
+        return;
+    }
     float H = a.h0 ? a.h0[bb * UN + i] : 0.f;  // replicated
     // H_{c+1} = Phi_c H_c + hloc_c  (lane (q, i): columns 4q..4q+3 of row i)
     float4 pn = *reinterpret_cast<const float4*>(a.phi + c0 * UN * UN + i * UN + 4 * q);
@@ -243,24 +249,6 @@ __global__ __launch_bounds__(64) void k_un_carry(const UnArgs a) {
         H = Hn;
     }
     if (a.h_last && q == 0) a.h_last[bb * UN + i] = H;
-    // M_{c-1} = Phi_c^T M_c + mloc_c  (lane (q, j): rows 4q..4q+3 of column j)
-    float M = 0.f;
-    const int64_t cl = c0 + nc - 1;
-    float4 qn = vals_t(a.phi + cl * UN * UN, i, q);
-    float mn = a.mc[cl * UN + i];
-    for (int64_t c = nc - 1; c >= 0; --c) {
-        const int64_t cb = c0 + c;
-        const float4 p4 = qn;
-        const float ml = mn;
-        const int64_t nx = c > 0 ? cb - 1 : cb;
-        qn = vals_t(a.phi + nx * UN * UN, i, q);
-        mn = a.mc[nx * UN + i];
-        const float4 mq = quarter_of(M, q);
-        const float Mn = qsum(p4.x * mq.x + p4.y * mq.y + p4.z * mq.z + p4.w * mq.w) + ml;
-        if (q == 0) a.mc[cb * UN + i] = M;  // the carry from the right into chunk c
-        M = Mn;
-    }
-    if (a.dh0 && q == 0) a.dh0[bb * UN + i] = M;
 }
 
 // grid (blocks - 1, b), 64 threads: block beta >= 1, steps [k, k + tbar) with
@@ -361,39 +349,63 @@ __global__ __launch_bounds__(64) void k_un_madj(const UnArgs a) {
 template <int L>
 __global__ __launch_bounds__(64) void k_un_grad(const UnArgs a) {
     __shared__ float shs[L + 1][UN];
-    __shared__ float smu[UN];
+    __shared__ float smu[L][UN];
     const int lane = threadIdx.x, i = lane & 15, q = lane >> 4;
     const int64_t c = blockIdx.x, bb = blockIdx.y;
     const int64_t s0 = c * L, s1 = min(s0 + L, a.T);
     const int64_t cb = bb * a.nc + c;
     const int64_t P = a.P;
-    if (q == 0) shs[0][i] = a.hc[cb * UN + i];
+    // the states h_{s-1} .. h_e into LDS (h in registers, replicated), with step
+    // t's A_t[i][4q..4q+3] and bx_t[i] loaded a step ahead
+    {
+        float h = a.hc[cb * UN + i];
+        if (q == 0) shs[0][i] = h;
+        const int64_t r0 = bb * a.T + s0;
+        float4 an = *reinterpret_cast<const float4*>(a.A + r0 * UN * UN + i * UN + 4 * q);
+        float bn = a.bx[r0 * UN + i];
+        for (int64_t t = s0; t < s1; ++t) {
+            const int64_t row = bb * a.T + t;
+            const float4 a4 = an;
+            const float bxt = bn;
+            const int64_t nx = t + 1 < s1 ? row + 1 : row;
+            an = *reinterpret_cast<const float4*>(a.A + nx * UN * UN + i * UN + 4 * q);
+            bn = a.bx[nx * UN + i];
+            const float4 hq = quarter_of(h, q);
+            h = qsum(a4.x * hq.x + a4.y * hq.y + a4.z * hq.z + a4.w * hq.w) + bxt;
+            if (q == 0) shs[t - s0 + 1][i] = h;
+        }
+    }
+    // the chunk's adjoints, sequential: mu_t = v_t + A_{t+1}^T mu_{t+1} (replicated,
+    // exchanged by shuffles), into LDS; in truncated mode v holds u and the
+    // recurrence gives the windowed adjoint.  v_t and step t's operand values of
+    // A_t^T mu are loaded a step ahead.
+    {
+        float mun = a.mc[cb * UN + i];  // A_{t+1}^T mu_{t+1}
+        const int64_t re = bb * a.T + s1 - 1;
+        float vn = a.v[re * UN + i];
+        float4 an = vals_t(a.A + re * UN * UN, i, q);
+        for (int64_t t = s1 - 1; t >= s0; --t) {
+            const int64_t row = bb * a.T + t;
+            const float vt = vn;
+            const float4 a4 = an;
+            const int64_t nx = t > s0 ? row - 1 : row;
+            vn = a.v[nx * UN + i];
+            an = vals_t(a.A + nx * UN * UN, i, q);
+            const float mu = vt + mun;
+            if (q == 0) smu[t - s0][i] = mu;
+            const float4 mq = quarter_of(mu, q);
+            mun = qsum(a4.x * mq.x + a4.y * mq.y + a4.z * mq.z + a4.w * mq.w);
+        }
+    }
     __syncthreads();
+    // the vjps of every step, independent of one another
     for (int64_t t = s0; t < s1; ++t) {
         const int64_t row = bb * a.T + t;
-        const float* At = a.A + row * UN * UN;
         const int k = static_cast<int>(t - s0);
-        const float4 a4 = *reinterpret_cast<const float4*>(At + i * UN + 4 * q);
-        float part = a4.x * shs[k][4 * q] + a4.y * shs[k][4 * q + 1] + a4.z * shs[k][4 * q + 2] +
-                     a4.w * shs[k][4 * q + 3];
-        part += bx_part(a.B + row * UN * P, a.x + row * P, P, q, i);
-        const float hn = qsum(part);
-        if (q == 0) shs[k + 1][i] = hn;
-        __syncthreads();
-    }
-    // A_{t+1}^T mu_{t+1} (replicated); in truncated mode v holds u and the
-    // recurrence gives the windowed adjoint
-    float mun = a.mc[cb * UN + i];
-    for (int64_t t = s1 - 1; t >= s0; --t) {
-        const int64_t row = bb * a.T + t;
-        const int k = static_cast<int>(t - s0);
-        const float mu = a.v[row * UN + i] + mun;
-        if (q == 0) smu[i] = mu;
-        __syncthreads();
         // dA_t[r][4(l%4) .. +3] = mu[r] h_{t-1}[..], r = l / 4
         {
             const int r = lane >> 2, c4 = (lane & 3) * 4;
-            const float m = smu[r];
+            const float m = smu[k][r];
             const float4 hv = make_float4(shs[k][c4] * m, shs[k][c4 + 1] * m, shs[k][c4 + 2] * m,
                                           shs[k][c4 + 3] * m);
             *reinterpret_cast<float4*>(a.dA + row * UN * UN + r * UN + c4) = hv;
@@ -403,7 +415,7 @@ __global__ __launch_bounds__(64) void k_un_grad(const UnArgs a) {
         const float* dyt = a.dy + row * P;
         for (int64_t e = 4 * lane; e < UN * P; e += 256) {
             const int64_t r = e / P, p = e % P;
-            const float m = smu[r];
+            const float m = smu[k][r];
             const float4 x4 = *reinterpret_cast<const float4*>(xt + p);
             *reinterpret_cast<float4*>(a.dB + row * UN * P + e) = make_float4(m * x4.x, m * x4.y, m * x4.z, m * x4.w);
             const int64_t pc = e / UN, rc = e % UN;
@@ -415,17 +427,9 @@ __global__ __launch_bounds__(64) void k_un_grad(const UnArgs a) {
         const float* Bt = a.B + row * UN * P;
         for (int64_t p = lane; p < P; p += 64) {
             float sx = 0.f;
-            for (int r = 0; r < UN; ++r) sx = fmaf(Bt[r * P + p], smu[r], sx);
+            for (int r = 0; r < UN; ++r) sx = fmaf(Bt[r * P + p], smu[k][r], sx);
             a.dx[row * P + p] = sx;
         }
-        // A_t^T mu for the step before (lane (q, j): rows 4q..4q+3 of column j)
-        {
-            const float* At = a.A + row * UN * UN;
-            float part = 0.f;
-            for (int r = 0; r < 4; ++r) part = fmaf(At[(4 * q + r) * UN + i], smu[4 * q + r], part);
-            mun = qsum(part);
-        }
-        __syncthreads();
     }
 }
 
@@ -500,7 +504,7 @@ hipError_t launch_unstructured_grad(const UnstructuredProblem& u, void* ws, hipS
     }
     {
         SSMK_TIMED("un_carry", s);
-        hipLaunchKernelGGL(k_un_carry, dim3(static_cast<unsigned>(a.nb)), dim3(64), 0, s, a);
+        hipLaunchKernelGGL(k_un_carry, dim3(static_cast<unsigned>(2 * a.nb)), dim3(64), 0, s, a);
     }
     SSMK_TIMED("un_grad", s);
     switch (a.L) {
