@@ -499,7 +499,7 @@ def main():
                          "reference for HBM traffic counters")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one GPU only "
+        print(f"bench.py: --gpus {args.gpus} is not supported: this library measures one GPU only "
               f"(the multi-GPU sharding is a design, not an implementation)", file=sys.stderr)
         sys.exit(2)
 

@@ -58,7 +58,7 @@ typedef enum {
     SSM_ERR_NULL = 1,        /* a required pointer is NULL                      */
     SSM_ERR_SHAPE = 2,       /* a size is out of range or inconsistent           */
     SSM_ERR_DTYPE = 3,       /* unknown dtype code                               */
-    SSM_ERR_UNSUPPORTED = 4, /* valid request this build does not implement      */
+    SSM_ERR_UNSUPPORTED = 4, /* valid request the library does not implement      */
     SSM_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the query says    */
     SSM_ERR_ALIGN = 6,       /* a pointer is not aligned as documented           */
     SSM_ERR_HIP = 7          /* the HIP runtime reported an error at launch       */
