@@ -104,3 +104,64 @@ def test_degenerate_proj_one_row():
     kk, jj = np.meshgrid(np.arange(8), np.arange(8), indexing="ij")
     check("dW", to_np(dW), oracle.proj_dw(xb, zb, kk.ravel(), jj.ravel()).reshape(8, 8), 1e-5)
     check("dX", to_np(dX), oracle.proj_dx(zb, wb, np.arange(1)), 1e-5)
+
+
+# The language head on degenerate shapes: one token, the smallest vocabulary and
+# width (8), a ragged 257-row block, every target ignored.
+HEAD_CASES = [(1, 8, 8, True), (257, 16, 8, False), (3, 8, 16, True)]
+
+
+@pytest.mark.parametrize("M,P,V,norm", HEAD_CASES, ids=[f"M{m}-P{p}-V{v}-norm{n}" for m, p, v, n in HEAD_CASES])
+def test_degenerate_head(M, P, V, norm):
+    from oracle.head import head_loss_grad
+    from paper_2501_00692_amd.synth import make_head_inputs
+    say(f"[degenerate head] M={M} P={P} V={V} norm={norm}")
+    inp = make_head_inputs(M, P, V, 692710, device="cuda")
+    inp["targets"][0] = V - 1
+    o = ssm.ssm_lm_head_grad(inp["y"], inp["omega"], inp["targets"], norm=norm)
+    torch.cuda.synchronize()
+    ref = head_loss_grad(to_np(inp["y"]), to_np(inp["omega"]), inp["targets"].cpu().numpy(), norm=norm,
+                         round_bf16=True)
+    rep = {}
+    for k in ("loss", "dy", "domega"):
+        check(k, to_np(o[k]), ref[k], 2e-4, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
+
+
+def test_degenerate_head_all_targets_ignored():
+    """No token has a loss: every loss, dy and dOmega is exactly zero."""
+    from paper_2501_00692_amd.synth import make_head_inputs
+    inp = make_head_inputs(64, 32, 64, 692711, device="cuda")
+    inp["targets"].fill_(-1)
+    o = ssm.ssm_lm_head_grad(inp["y"], inp["omega"], inp["targets"])
+    torch.cuda.synchronize()
+    for k in ("loss", "dy", "domega"):
+        assert float(o[k].abs().max()) == 0.0, k
+
+
+# The unstructured SSM on degenerate shapes: (b, T, P, chunk, tbar); tbar 0 is the
+# full gradient (with dh0): one step, one step past a chunk, a window of one step,
+# a window one step shorter than the sequence, the smallest channel count (16).
+UN_CASES = [(1, 1, 16, 16, 0), (2, 17, 16, 16, 0), (2, 17, 16, 16, 16), (1, 33, 16, 16, 1), (3, 5, 32, 16, 4),
+            (1, 300, 16, 256, 299)]
+
+
+@pytest.mark.parametrize("b,T,P,chunk,tbar", UN_CASES, ids=[f"b{b}-T{t}-P{p}-c{c}-tbar{tb}" for b, t, p, c, tb in UN_CASES])
+def test_degenerate_unstructured(b, T, P, chunk, tbar):
+    from oracle.unstructured import un_adjoint_sum, un_bptt
+    from paper_2501_00692_amd.synth import make_unstructured_inputs
+    say(f"[degenerate unstructured] b={b} T={T} P={P} chunk={chunk} tbar={tbar}")
+    inp = make_unstructured_inputs(b, T, P, 692712, device="cuda", h0=True)
+    full = tbar == 0
+    o = ssm.ssm_unstructured_grad(inp["A"], inp["B"], inp["C"], inp["x"], inp["dy"], h0=inp["h0"], tbar=tbar,
+                                  chunk=chunk, want_dh0=full)
+    torch.cuda.synchronize()
+    h = {k: to_np(v) for k, v in inp.items()}
+    if full:
+        ref = un_bptt(h["A"], h["B"], h["C"], h["x"], h["dy"], h["h0"])
+    else:
+        ref = un_adjoint_sum(h["A"], h["B"], h["C"], h["x"], h["dy"], tbar=tbar, h0=h["h0"])
+    rep = {}
+    for k in ("dA", "dB", "dC", "dx") + (("dh0",) if full else ()):
+        check(k, to_np(o[k]), ref[k], TOL_F32, rep)
+    say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
