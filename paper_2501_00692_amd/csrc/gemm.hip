@@ -112,6 +112,18 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rs, uint32_t v
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const uint16_t* base, int64_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, static_cast<int>(bytes), kRsrcWord3);
 }
+// The same from values every lane holds alike, taken from the first lane, so that
+// the resource stays in scalar registers: a resource the compiler cannot prove
+// uniform is kept in vector registers and every buffer load through it becomes a
+// loop over its distinct values.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_uniform(const uint16_t* base, int64_t bytes) {
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32));
+    const int n = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes));
+    void* p = reinterpret_cast<void*>((static_cast<uint64_t>(hi) << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(p, 0, n, kRsrcWord3);
+}
 
 __device__ __forceinline__ uint16_t f2bf(float v) {
     uint32_t u = __float_as_uint(v);
@@ -167,8 +179,8 @@ struct RowMajorOps {
                                          int lane, int wr, int wc) {
         k_hi = khi;
         // resources over the tile's rows: rows past the matrix read as zero
-        ra = rsrc(g.A + r0 * g.lda, min<int64_t>(BM, g.R - r0) * g.lda * 2);
-        rb = rsrc(g.B + c0 * g.ldb, min<int64_t>(BN, g.Cc - c0) * g.ldb * 2);
+        ra = rsrc_uniform(g.A + r0 * g.lda, min<int64_t>(BM, g.R - r0) * g.lda * 2);
+        rb = rsrc_uniform(g.B + c0 * g.ldb, min<int64_t>(BN, g.Cc - c0) * g.ldb * 2);
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int row = (wave + 8 * i) * 16 + (lane >> 2);
@@ -359,7 +371,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmLaunch gl) {
     const int q = __builtin_amdgcn_readfirstlane(tile_all >= gl.tiles0 ? 1 : 0);
     const GemmArgs g = q ? gl.p[1] : gl.p[0];
     const int tile = tile_all - (q ? gl.tiles0 : 0);
-    const int ncb = gl.cb[q];
+    const int ncb = q ? gl.cb[1] : gl.cb[0];  // a select: an indexed kernel argument would not be uniform
     const int nrb = (q ? gl.tiles - gl.tiles0 : gl.tiles0) / ncb;
     // tiles in groups of kGroupRows row blocks, column-major inside a group, so
     // that the 32 consecutive tiles one XCD runs at a time form a block of about
@@ -630,8 +642,8 @@ struct RowMajorOps4 {
                                          int lane, int wr, int wc) {
         k_hi = khi;
         // resources over the tile's rows: rows past the matrix read as zero
-        ra = rsrc(g.A + r0 * g.lda, min<int64_t>(BM, g.R - r0) * g.lda * 2);
-        rb = rsrc(g.B + c0 * g.ldb, min<int64_t>(256, g.Cc - c0) * g.ldb * 2);
+        ra = rsrc_uniform(g.A + r0 * g.lda, min<int64_t>(BM, g.R - r0) * g.lda * 2);
+        rb = rsrc_uniform(g.B + c0 * g.ldb, min<int64_t>(256, g.Cc - c0) * g.ldb * 2);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int row = (wave + 4 * i) * 16 + (lane >> 2);
@@ -673,7 +685,7 @@ struct RowMajorOps4 {
 
 // Four waves, one per SIMD, each owning a 128 x 128 block of a 256 x 256 output
 // tile: TR selects the dW form (ColMajorOps4) or the dX form (RowMajorOps4, plain
-// epilogues only: no addend, no bf16 copy).
+// epilogues only: no addend, and the fp32 result or its bf16 copy, not both).
 template <bool TR, int NST>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gemm4(const GemmLaunch gl) {
     constexpr int MI = 4, NJ = 4, BN = 256;
@@ -691,7 +703,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int q = __builtin_amdgcn_readfirstlane(tile_all >= gl.tiles0 ? 1 : 0);
     const GemmArgs g = q ? gl.p[1] : gl.p[0];
     const int tile = tile_all - (q ? gl.tiles0 : 0);
-    const int ncb = gl.cb[q];
+    const int ncb = q ? gl.cb[1] : gl.cb[0];  // a select: an indexed kernel argument would not be uniform
     const int nrb = (q ? gl.tiles - gl.tiles0 : gl.tiles0) / ncb;
     const int grp = tile / (kGroupRows * ncb), first = grp * kGroupRows;
     const int gh = min(kGroupRows, nrb - first), within = tile - grp * kGroupRows * ncb;
@@ -803,6 +815,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         store_tile<false, decltype(At)::value, true, false, decltype(Ft)::value>(
             acc, dst, ldc, nullptr, 0, nullptr, 0, g.R, g.Cc, r0 + wr, c0 + wc, lane);
     };
+    if constexpr (!TR) {
+        // the dX form's other plain epilogue: only the bf16 copy (no fp32 result)
+        if (g.direct && g.out16) {
+            if (full)
+                store_tile<false, false, false, true, true>(acc, nullptr, 0, nullptr, 0, g.out16, g.ld16, g.R, g.Cc,
+                                                            r0 + wr, c0 + wc, lane);
+            else
+                store_tile<false, false, false, true, false>(acc, nullptr, 0, nullptr, 0, g.out16, g.ld16, g.R, g.Cc,
+                                                             r0 + wr, c0 + wc, lane);
+            return;
+        }
+    }
     if (full) {
         if (accum) store(std::true_type{}, std::true_type{});
         else store(std::true_type{}, std::false_type{});
@@ -890,8 +914,9 @@ constexpr int64_t kMaxWgs = (int64_t(1) << 23) - 1;
 // load, measured: 0.57 us for 128 columns, 0.80 for 192, 0.84 for 256 on the
 // four-wave kernel), plus the
 // HBM time of writing and re-reading the split partials (4 TB/s).  256-column
-// tiles (`wide`) for dW, and for dX when its epilogue is plain (no addend, no
-// bf16 copy: the four-wave kernel's registers hold no more).
+// tiles (`wide`) for dW, and for dX when its epilogue is plain (no addend, and
+// either the fp32 result or its bf16 copy: the four-wave kernel's registers hold
+// no more).
 struct Plan {
     int bn;
     int splits;
@@ -1072,7 +1097,7 @@ hipError_t launch_gemm_dx(int64_t M, int64_t K, int64_t N, const uint16_t* dZ, i
     if (ldx <= 0) ldx = K;
     if (ldadd <= 0) ldadd = K;
     // outputs with few tiles (narrow projections) split the reduction as dW does
-    const Plan pl = plan_gemm(M, K, N, true, add == nullptr && out16 == nullptr);
+    const Plan pl = plan_gemm(M, K, N, true, add == nullptr && (out16 == nullptr || dX == nullptr));
     const bool direct = pl.splits == 1;
     const GemmArgs g{M, K, N, dZ, lddz, W, ldw, direct ? dX : static_cast<float*>(ws), split_range(N, pl.splits),
                      direct ? 1 : 0, accum ? 1 : 0, add, out16, ld16, ldx, ldadd};
