@@ -88,3 +88,20 @@ def test_head_repeat_is_bitwise_identical():
     b = _run(inp, True)
     for k in a:
         assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("V", [6000, 12000, 50304, 80000])
+def test_head_row_kernel_paths(V):
+    """The loss kernel holds a row in registers for vocabularies up to 65,536
+    (2, 4 and 16 float4 pieces per thread here) and reads it twice above that
+    (80,000): each against the oracle with the GPU's bf16 rounding."""
+    M, P = 48, 64
+    say(f"[head row kernel] M={M} P={P} V={V}")
+    inp = make_head_inputs(M, P, V, 692304, device="cuda")
+    inp["targets"][0] = V - 1
+    inp["targets"][1] = 0
+    o = _run(inp, True)
+    y, om, t = to_np(inp["y"]), to_np(inp["omega"]), inp["targets"].cpu().numpy()
+    ref = head_loss_grad(y, om, t, norm=True, round_bf16=True)
+    for k in ("loss", "dy", "domega"):
+        check(f"{k}[rounded]", o[k], ref[k], TOL_HEAD_ROUNDED)
