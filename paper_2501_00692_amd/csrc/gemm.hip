@@ -508,12 +508,20 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmLaunch gl) {
             __builtin_amdgcn_sched_barrier(0);
         };
         int64_t t = 0;
-        for (; t + NS <= steady; t += NS) {
+        auto ring = [&](int64_t t) __attribute__((always_inline)) {
             step(Stage<0>{}, t);
             step(Stage<1>{}, t + 1);
             step(Stage<2>{}, t + 2);
             step(Stage<3>{}, t + 3);
+        };
+        // four rings per loop iteration: the compiler's own drain of the loads in
+        // flight at the loop head (see k_gemm4) comes once per 16 steps
+        constexpr int kRings = 4;
+        for (; t + kRings * NS <= steady; t += kRings * NS) {
+#pragma unroll
+            for (int u = 0; u < kRings; ++u) ring(t + u * NS);
         }
+        for (; t + NS <= steady; t += NS) ring(t);
         const int64_t rem = steady - t;  // t is a multiple of NS here
         if (rem > 0) step(Stage<0>{}, t);
         if (rem > 1) step(Stage<1>{}, t + 1);
@@ -782,13 +790,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         __builtin_amdgcn_sched_barrier(0);
     };
     int64_t t = 0;
-    for (; t + NST <= steady; t += NST) {
+    auto ring = [&](int64_t t) __attribute__((always_inline)) {
         step(Stage<0>{}, t);
         step(Stage<1>{}, t + 1);
         step(Stage<2>{}, t + 2);
         step(Stage<3>{}, t + 3);
         if constexpr (NST == 5) step(Stage<(NST > 4 ? 4 : 3)>{}, t + 4);
+    };
+    // Four passes over the ring per loop iteration: at the loop head the compiler
+    // no longer knows which stage each direct-to-LDS load in flight writes, and
+    // waits for nearly all of them before the first fragment read (vmcnt(4), then
+    // vmcnt(0)), where the explicit waits need only the next stage's; with the
+    // body four rings long that drain comes once per 20 steps instead of 5.
+    constexpr int kRings = 4;
+    for (; t + kRings * NST <= steady; t += kRings * NST) {
+#pragma unroll
+        for (int u = 0; u < kRings; ++u) ring(t + u * NST);
     }
+    for (; t + NST <= steady; t += NST) ring(t);
     const int64_t rem = steady - t;
     if (rem > 0) step(Stage<0>{}, t);
     if (rem > 1) step(Stage<1>{}, t + 1);
