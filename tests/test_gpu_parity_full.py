@@ -318,6 +318,46 @@ def test_proj_grad_wide_dx_tiles_sampled():
     say("   rel-L2:", " ".join(f"{k}={v:.2e}" for k, v in rep.items()))
 
 
+@pytest.mark.parametrize("form", ["dW", "dX"])
+def test_proj_grad_every_main_loop_residue(form):
+    """The four-wave kernel's main loop runs four passes over its five-stage LDS
+    ring per iteration (20 reduction steps of 32), then single passes, then the
+    last stages one by one.  Reductions of 32 n + 7 for n = 24..43 put every
+    residue of that schedule (and a ragged last stage) into one 256 x 256-tile
+    launch: dW of 2048 x 8192 (256 output tiles) and plain dX of 4096 x 4096 (256
+    output tiles, so both take 256-column tiles and no split; dX's reduction must
+    be a multiple of 8, so there it is 32 n + 8).  Sampled entries,
+    each output's corners included, against the oracle's plain loops."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4245 if form == "dW" else 4246)
+    rng = np.random.default_rng(6)
+    bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)
+    rep = {}
+    for n in range(24, 44):
+        red = 32 * n + (7 if form == "dW" else 8)
+        if form == "dW":
+            K, N = 2048, 8192
+            say(f"[proj residue dW] M={red} K={K} N={N}")
+            X = torch.randn(red, K, generator=g, device="cuda").to(torch.bfloat16)
+            dZ = torch.randn(red, N, generator=g, device="cuda").to(torch.bfloat16)
+            dW, _ = ssm.ssm_proj_grad(X, dZ, None, want_dW=True, want_dX=False)
+            torch.cuda.synchronize()
+            kk = np.concatenate([rng.integers(0, K, 256), [0, 0, K - 1, K - 1]])
+            jj = np.concatenate([rng.integers(0, N, 256), [0, N - 1, 0, N - 1]])
+            check(f"dW[n={n}]", to_np(dW)[kk, jj], oracle.proj_dw(bits(X), bits(dZ), kk, jj), 1e-5, rep)
+        else:
+            M, K = 4096, 4096
+            say(f"[proj residue dX] M={M} K={K} N={red}")
+            dZ = torch.randn(M, red, generator=g, device="cuda").to(torch.bfloat16)
+            W = (torch.randn(K, red, generator=g, device="cuda") / 32).to(torch.bfloat16)
+            _, dX = ssm.ssm_proj_grad(None, dZ, W, want_dW=False, want_dX=True)
+            torch.cuda.synchronize()
+            rows = np.sort(np.concatenate([rng.choice(M - 1, 6, replace=False), [0, M - 1]]))
+            ref = oracle.proj_dx(bits(dZ), bits(W), rows)
+            check(f"dX[n={n}]", to_np(dX[torch.as_tensor(rows, device="cuda")]), ref, 1e-5, rep)
+    say("   worst rel-L2: %.2e" % max(rep.values()))
+
+
 def test_layer_workload_weight_grads_exact_sampled():
     """The layer's weight gradients against the products of the bf16 operands the
     layer hands over, at the layer workload (one launch over the M = 8192 rows).
