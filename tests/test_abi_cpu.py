@@ -209,3 +209,42 @@ def test_head_errors(lib):
     assert call(dom=MISALIGNED) == 6
     assert call(ws=None) == 5
     assert call(wsb=1024) == 5
+
+
+def test_unstructured_errors(lib):
+    """The unstructured SSM (Table 1's N x N row) validates on the host: 16
+    states, channels a multiple of 16 up to 4,096, fp32 tensors, no flags, a
+    supported chunk, a known mode, tbar >= 1 when truncated, dh0 for the full
+    gradient only, required and aligned pointers and the workspace, all before any
+    HIP call (every call below fails validation, so nothing is enqueued)."""
+    n = ctypes.c_size_t()
+    ud = lambda **kw: desc(**{"channels": 64, **kw})
+    size = lambda d, mode=ssm.SSM_FULL, tbar=0: lib.ssm_unstructured_grad_workspace_size(
+        ctypes.byref(d) if d is not None else None, mode, tbar, ctypes.byref(n))
+    assert size(ud()) == 0 and n.value > 0
+    full = n.value
+    assert size(ud(), ssm.SSM_TRUNCATED, 16) == 0 and n.value >= full
+    assert size(None) == 1
+    assert size(ud(batch=0)) == 2
+    assert size(ud(dstate=8)) == 4 and "dstate = 16" in ssm.last_error()
+    assert size(ud(channels=24)) == 4
+    assert size(ud(channels=4112)) == 4
+    assert size(ud(in_dtype=ssm.SSM_BF16)) == 4 and "fp32" in ssm.last_error()
+    assert size(ud(flags=ssm.SSM_GATE_SILU)) == 4
+    assert size(ud(chunk=48)) == 4
+    assert size(ud(), mode=5) == 2
+    assert size(ud(), ssm.SSM_TRUNCATED, 0) == 2
+    assert lib.ssm_unstructured_grad_workspace_size(ctypes.byref(ud()), ssm.SSM_FULL, 0, None) == 1
+
+    def call(d=None, mode=ssm.SSM_FULL, tbar=0, A=FAKE, x=FAKE, dh0=None, ws=FAKE, wsb=1 << 40):
+        d = d if d is not None else ud()
+        return lib.ssm_unstructured_grad(ctypes.byref(d), mode, tbar, A, FAKE, FAKE, x, None, FAKE, FAKE, FAKE,
+                                         FAKE, FAKE, dh0, ws, wsb, None)
+
+    assert call(d=ud(dstate=4)) == 4
+    assert call(A=None) == 1 and "A is NULL" in ssm.last_error()
+    assert call(x=MISALIGNED) == 6
+    assert call(dh0=MISALIGNED) == 6
+    assert call(mode=ssm.SSM_TRUNCATED, tbar=16, dh0=FAKE) == 4 and "full gradient" in ssm.last_error()
+    assert call(ws=None) == 5
+    assert call(wsb=16) == 5
