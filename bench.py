@@ -480,6 +480,20 @@ def unstructured_line(args, ssm, torch):
             "extra": r}
 
 
+def head_line(args, ssm, torch):
+    """The JSON line of ``--workload head`` (for profiling the language head)."""
+    from paper_2501_00692_amd.synth import HEAD_WORKLOADS
+    r = head_measure(ssm, torch, args.steps, args.warmup)
+    M = HEAD_WORKLOADS["head"][0]
+    return {"metric": "language-head loss and gradient tokens/sec; % MFMA peak",
+            "value": M / (r["ms"] * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": r["ms"], "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16-in/fp32-acc", "data": "synthetic",
+            "config": {"workload": "language head of Sec. 3.2 with cross-entropy loss, " + r["config"]
+                                   + "; each step one ssm_lm_head_grad call"},
+            "extra": r}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -518,6 +532,9 @@ def main():
         del src, dst
     if args.workload == "unstructured":
         print(json.dumps(unstructured_line(args, ssm, torch)), flush=True)
+        return
+    if args.workload == "head":
+        print(json.dumps(head_line(args, ssm, torch)), flush=True)
         return
     w = WORKLOADS[args.workload]
     tbar = w.tbar
