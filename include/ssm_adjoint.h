@@ -306,7 +306,7 @@ ssm_status ssm_stack_grad(const ssm_desc* desc, int64_t K, int32_t grad, int32_t
  *             no gradient), a target >= V gives l = NaN and no gradient;
  *   loss    : fp32 [M];  dy : fp32 [M][P];  domega : fp32 [V][P], or NULL to skip it.
  *   block_rows : rows per block (a multiple of 256), or 0 for as many as keep the
- *             block's fp32 logits within 1 GiB; the workspace (which also holds
+ *             block's fp32 logits within 4 GiB; the workspace (which also holds
  *             Omega^T in bf16) grows with it.  Norm(y) and the logit gradients enter the
  * products as bf16 (round to nearest even) with fp32 accumulation; the
  * normalisation's backward recomputes Norm(y) in fp32; dOmega adds the blocks in

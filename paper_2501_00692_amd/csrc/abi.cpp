@@ -929,7 +929,7 @@ ssm_status ssm_stack_grad(const ssm_desc* desc, int64_t K, int32_t grad, int32_t
 // ---------------------------------------------------------------------------
 namespace {
 
-constexpr size_t kHeadLogitBytes = size_t(1) << 30;
+constexpr size_t kHeadLogitBytes = size_t(4) << 30;  // fp32 logits of one row block
 
 // Workspace of the head: per row block Norm(y) (bf16) and 1/rms, Omega^T (bf16
 // [P][V]), the block's fp32 logits and bf16 logit gradients, dU (fp32), and the
