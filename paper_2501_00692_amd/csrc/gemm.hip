@@ -1049,7 +1049,7 @@ size_t dw_workspace(int np, const DwProduct* d, int64_t M) {
     return split_workspace(plan_gemm(np, R, Cc, M, true, true), np, R, Cc);
 }
 
-hipError_t launch_dw(int np, const DwProduct* d, int64_t M, void* ws, hipStream_t s) {
+hipError_t launch_dw(int np, const DwProduct* d, int64_t M, void* ws, hipStream_t s, const char* timer = nullptr) {
     int64_t R[2], Cc[2];
     for (int q = 0; q < np; ++q) {
         R[q] = d[q].K;
@@ -1068,7 +1068,7 @@ hipError_t launch_dw(int np, const DwProduct* d, int64_t M, void* ws, hipStream_
         if (!direct) part += static_cast<int64_t>(pl.splits) * d[q].K * d[q].N;
     }
     {
-        SSMK_TIMED("gemm_dw", s);
+        SSMK_TIMED(timer ? timer : "gemm_dw", s);
         if (!launch_plan<true>(g, np, pl, s)) return hipErrorInvalidConfiguration;
     }
     if (!direct) {
@@ -1099,9 +1099,9 @@ size_t gemm_dx_workspace(int64_t M, int64_t K, int64_t N) {
 
 hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, int64_t ldx,
                           const uint16_t* dZ, int64_t lddz, float* dW, bool accum, void* ws,
-                          hipStream_t s) {
+                          hipStream_t s, const char* timer) {
     const DwProduct d{K, N, X, ldx, dZ, lddz, dW, accum};
-    return launch_dw(1, &d, M, ws, s);
+    return launch_dw(1, &d, M, ws, s, timer);
 }
 
 hipError_t launch_gemm_dw2(int64_t M, const DwProduct& a, const DwProduct& b, void* ws, hipStream_t s) {

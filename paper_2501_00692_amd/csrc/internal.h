@@ -162,11 +162,12 @@ PairsWorkspace pairs_workspace(int64_t nb, int64_t T, int64_t D, int64_t N, int6
 hipError_t launch_grad_pairs(ScanProblem& p, void* ws, const PairsWorkspace& w, int64_t W, hipStream_t s);
 
 // bf16 MFMA GEMMs (gemm.hip).
-// dW[K][N] (+)= X^T dZ with X [M][K] (ldx), dZ [M][N] (lddz).
+// dW[K][N] (+)= X^T dZ with X [M][K] (ldx), dZ [M][N] (lddz); `timer` names the
+// launch in the per-kernel timing (default "gemm_dw").
 size_t gemm_dw_workspace(int64_t M, int64_t K, int64_t N);
 hipError_t launch_gemm_dw(int64_t M, int64_t K, int64_t N, const uint16_t* X, int64_t ldx,
                           const uint16_t* dZ, int64_t lddz, float* dW, bool accum, void* ws,
-                          hipStream_t s);
+                          hipStream_t s, const char* timer = nullptr);
 // Two weight gradients dW_q[K_q][N_q] (+)= X_q^T dZ_q over the same M rows in one
 // launch (and one second-stage launch when the reduction is split): the tiles of
 // both fill the GPU together.  ws holds gemm_dw2_workspace bytes.
