@@ -125,12 +125,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_uniform(const uint16_t* b
     return __builtin_amdgcn_make_buffer_rsrc(p, 0, n, kRsrcWord3);
 }
 
-__device__ __forceinline__ uint16_t f2bf(float v) {
-    uint32_t u = __float_as_uint(v);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
-}
+// fp32 -> bf16, round to nearest even (the hardware conversion, v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint16_t f2bf(float v) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v)); }
 
 struct GemmArgs {
     int64_t R, Cc, Kr;    // output rows, output cols, reduction length

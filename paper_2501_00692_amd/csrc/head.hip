@@ -21,12 +21,8 @@ namespace {
 
 constexpr int kXentThreads = 256;
 
-__device__ __forceinline__ uint16_t bf16_rne(float v) {
-    uint32_t u = __float_as_uint(v);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
-}
+// fp32 -> bf16, round to nearest even (the hardware conversion, v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint16_t bf16_rne(float v) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v)); }
 
 __global__ __launch_bounds__(kXentThreads) void k_head_xent(const float* o, int64_t ldo, const int32_t* tgt,
                                                             float* loss, uint16_t* G, int64_t ldg, int64_t V) {

@@ -12,12 +12,8 @@
 namespace ssmk {
 namespace {
 
-__device__ __forceinline__ uint16_t rne16(float v) {
-    uint32_t u = __float_as_uint(v);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
-}
+// fp32 -> bf16, round to nearest even (the hardware conversion, v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint16_t rne16(float v) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v)); }
 
 // grid (ceil(max(D, nx) / 256), min(dm, 65535)); one thread per column of each
 // part, rows strided by the grid's height

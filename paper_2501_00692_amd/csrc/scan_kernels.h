@@ -44,16 +44,10 @@ __device__ __forceinline__ float ldm(const T* p, int64_t i, bool v) {
     const float r = ldf(p, v ? i : 0);
     return __uint_as_float(__float_as_uint(r) & (v ? 0xffffffffu : 0u));
 }
+// bf16 store, rounded to nearest even by the hardware conversion (v_cvt_pk_bf16_f32;
+// checked bit for bit against the integer rounding on every non-NaN pattern class)
 __device__ __forceinline__ void stf(uint16_t* p, int64_t i, float v) {
-    uint32_t u = __float_as_uint(v);
-    uint16_t r;
-    if ((u & 0x7fffffffu) > 0x7f800000u) {
-        r = 0x7fc0;  // NaN
-    } else {
-        u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest even
-        r = static_cast<uint16_t>(u >> 16);
-    }
-    p[i] = r;
+    p[i] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
 }
 
 constexpr float kLn2 = 0.6931471805599453f;

@@ -17,12 +17,8 @@ namespace {
 constexpr int kRowThreads = 256;
 constexpr float kRmsEps = 1e-6f;
 
-__device__ __forceinline__ uint16_t to_bf16(float v) {
-    uint32_t u = __float_as_uint(v);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
-}
+// fp32 -> bf16, round to nearest even (the hardware conversion, v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint16_t to_bf16(float v) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v)); }
 __device__ __forceinline__ float from_bf16(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
 // Sum of v over the workgroup (kRowThreads threads), the same on every thread.
