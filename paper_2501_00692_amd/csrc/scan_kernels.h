@@ -90,6 +90,18 @@ __device__ __forceinline__ float quad_sum(float v) {
     v += dpp_swap2(v);
     return v;
 }
+// Quad sums of four per-lane partials v[0..3] (of four consecutive steps): lane r
+// of the quad receives the sum of v[r] over the quad.  Two exchange rounds (lane
+// r^1, then r^2) send each lane the partials it does not keep: 9 instructions
+// where four quad_sum calls and the selection of lane r's value take 12.  The
+// additions group as quad_sum's, (v_r + v_{r^1}) + (v_{r^2} + v_{r^3}), so each
+// sum is bit-identical to quad_sum's.
+__device__ __forceinline__ float quad_sum_transposed(const float v[4], int r) {
+    const bool b0 = (r & 1) != 0, b1 = (r & 2) != 0;
+    const float s01 = (b0 ? v[1] : v[0]) + dpp_swap1(b0 ? v[0] : v[1]);
+    const float s23 = (b0 ? v[3] : v[2]) + dpp_swap1(b0 ? v[2] : v[3]);
+    return (b1 ? s23 : s01) + dpp_swap2(b1 ? s01 : s23);
+}
 
 // Workgroup barrier for LDS traffic only: waits for this wave's LDS operations
 // but leaves its global loads and stores in flight (a plain __syncthreads also
@@ -604,7 +616,7 @@ __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
             }
             const float dlr = SP ? softplus_sel(pr, v) : pr;
             if (p.bdelta) xr *= dlr;  // input term Delta B x
-            float yk = 0.f;
+            float ypart[4];
             const int tb = static_cast<int>(s0 - sb);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -620,9 +632,9 @@ __global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
                     h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
                     yp = fmaf(Cv[k], h[k], yp);
                 }
-                const float y = quad_sum(yp);
-                if (j == r) yk = y;
+                ypart[j] = yp;
             }
+            float yk = quad_sum_transposed(ypart, r);  // y of step s0 + r
             if constexpr (GATE) yk *= zr * sigmoid_f(zr);
             if (v) stf(Y, (bb * p.T + s0 + r) * p.D + d, yk);
         }
@@ -1072,7 +1084,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             }
 
             float ahp[S][4], ah[S][4], gh[S], dlh[S], xh[S];
-            float yk[SPL];
+            float yk[SPL], ypart[4];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) yk[jj] = 0.f;
             // B and C are read from LDS one step ahead of their use
@@ -1102,8 +1114,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     red[wave][j][r * 4 + k][chs] = g * h[k];
                 }
                 if constexpr (GATE) {
-                    const float y = quad_sum(yp);
-                    if ((j & 3) == r) yk[j >> 2] = y;
+                    ypart[j & 3] = yp;
+                    if ((j & 3) == 3) yk[j >> 2] = quad_sum_transposed(ypart, r);  // y of step 4(j/4) + r
                 }
                 gh[j] = g;
                 dlh[j] = dl;
@@ -1124,7 +1136,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                 wave_lds_sync();
             }
 
-            float dxk[SPL], ddk[SPL];
+            float dxk[SPL], ddk[SPL], dxpart[4], ddpart[4];
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) dxk[jj] = ddk[jj] = 0.f;
             // the segment's dA_log terms are summed on their own and then added to
@@ -1173,11 +1185,11 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     red[wave][j][r * 4 + k][chs] = mb[k] * xh[j];
                     Mp[k] = ah[j][k] * mb[k];
                 }
-                const float dxv = quad_sum(dxp);
-                const float ddv = quad_sum(ddp);
-                if ((j & 3) == r) {
-                    dxk[j >> 2] = dxv;
-                    ddk[j >> 2] = ddv;
+                dxpart[j & 3] = dxp;
+                ddpart[j & 3] = ddp;
+                if ((j & 3) == 0) {  // the group's last step in reverse order: lane r takes step 4(j/4) + r
+                    dxk[j >> 2] = quad_sum_transposed(dxpart, r);
+                    ddk[j >> 2] = quad_sum_transposed(ddpart, r);
                 }
             }
 #pragma unroll
