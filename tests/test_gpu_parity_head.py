@@ -57,9 +57,14 @@ def test_head_small(norm):
     _compare(o, y, om, t, norm, valid)
 
 
-def test_head_row_blocks():
-    """Four row blocks of 256 (the last one 232 rows): dOmega adds the blocks."""
+@pytest.mark.parametrize("extra", [0, 3])
+def test_head_row_blocks(extra):
+    """Four row blocks of 256, dOmega adding the blocks.  The last block has 232
+    rows, or 235, which is not a multiple of 8: its logits then take the dX form
+    while the full blocks' take the weight-gradient form from the transposed
+    Norm(y), so one call runs both paths."""
     M, P, V = HEAD_WORKLOADS["head_blocks"]
+    M += extra
     say(f"[head blocks] M={M} P={P} V={V} block_rows=256")
     inp = make_head_inputs(M, P, V, 692301, device="cuda")
     o = _run(inp, True, block_rows=256)
