@@ -84,9 +84,9 @@ typedef enum { SSM_FULL = 0, SSM_TRUNCATED = 1 } ssm_mode;
 #define SSM_ACCUM_DX 2u       /* dX += dZ W^T instead of dX = dZ W^T                   */
 
 typedef struct {
-    int64_t batch;    /* b >= 1                                                     */
+    int64_t batch;    /* b >= 1; b * T at most 2^40                                  */
     int64_t seqlen;   /* T >= 1                                                     */
-    int64_t channels; /* D >= 1 (the paper's P for a diagonal layer)                */
+    int64_t channels; /* D >= 1, at most 2^20 (the paper's P for a diagonal layer)   */
     int64_t dstate;   /* N, 1..16                                                   */
     int64_t chunk;    /* L, time steps per carry chunk: 0 (default 128), or one of
                          16, 32, 64, 128, 256.  Results do not depend on it beyond

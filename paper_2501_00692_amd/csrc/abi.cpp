@@ -54,8 +54,9 @@ ssm_status check_desc(const ssm_desc* d, int64_t* L, int64_t* nc) {
     if (n > kMaxGridYZ || d->batch > kMaxGridYZ / 2)
         return fail(SSM_ERR_UNSUPPORTED, "seqlen/chunk (%lld) or batch (%lld) exceeds the launch grid",
                     (long long)n, (long long)d->batch);
-    // All index arithmetic is 64-bit; element counts must fit comfortably.
-    if (d->batch * d->seqlen > (int64_t(1) << 40) || d->channels > (int64_t(1) << 22))
+    // Index arithmetic is 64-bit, except the byte offsets within one chunk of
+    // rows (L * D elements, below 2^31 bytes for D <= 2^20).
+    if (d->batch * d->seqlen > (int64_t(1) << 40) || d->channels > (int64_t(1) << 20))
         return fail(SSM_ERR_SHAPE, "problem too large");
     *L = l;
     *nc = n;

@@ -253,8 +253,10 @@ hipError_t pairs_impl(const ScanProblem& p, float* dl, float* g, float* mu, int6
     }
     {
         SSMK_TIMED("chunk_aggr", s);
-        dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
-        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, 8>), g4, dim3(256), 0, s, p);
+        if (p.N == 16)
+            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, true, 8>), aggr_grid(p), dim3(64), 0, s, p);
+        else
+            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, false, 8>), aggr_grid(p), dim3(64), 0, s, p);
     }
     {
         SSMK_TIMED("carry", s);

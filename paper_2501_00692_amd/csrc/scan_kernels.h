@@ -276,174 +276,225 @@ __device__ __forceinline__ void load_raw(const ScanProblem& p, int64_t bb, int64
     }
 }
 
+// Scalar-load views of global memory: loads through them at an address that is
+// the same for every lane of the wave become scalar loads.
+typedef const __attribute__((address_space(4))) uint32_t* ConstDw;
+
+// One row of B or C (up to 16 states) as raw bits in scalar registers: with 16
+// states the row is contiguous and read with wide scalar loads (bf16: the packed
+// pairs, fp32: the values); with fewer, each state is read on its own and held
+// as fp32 bits (states past N are 0).  Scalar loads read whole aligned dwords:
+// element e of a bf16 tensor (16-byte aligned) is half (e & 1) of dword e >> 1
+// (for a last element that starts a dword, the dword's other half lies past the
+// tensor but in the same aligned dword, so in mapped memory).
+template <typename TI, bool N16>
+struct SRow {
+    static constexpr bool PACKED = N16 && sizeof(TI) == 2;
+    static constexpr int NW = PACKED ? 8 : 16;
+    uint32_t w[NW];
+    __device__ __forceinline__ void load(const TI* base, int64_t row, int64_t N) {
+        if constexpr (N16) {
+            const ConstDw q = (ConstDw)(base + row * 16);
+#pragma unroll
+            for (int i = 0; i < NW; ++i) w[i] = q[i];  // merged into wide scalar loads
+        } else {
+            const ConstDw q = (ConstDw)(base);
+#pragma unroll
+            for (int n = 0; n < 16; ++n) {
+                const int64_t e = row * N + n;
+                if (n >= N) w[n] = 0u;
+                else if constexpr (sizeof(TI) == 4) w[n] = q[e];
+                else w[n] = (e & 1) ? (q[e >> 1] & 0xffff0000u) : (q[e >> 1] << 16);
+            }
+        }
+    }
+    __device__ __forceinline__ float at(int k) const {
+        if constexpr (PACKED) return __uint_as_float((k & 1) ? (w[k >> 1] & 0xffff0000u) : (w[k >> 1] << 16));
+        else return __uint_as_float(w[k]);
+    }
+};
+
 // ---------------------------------------------------------------------------
-// k_chunk_aggr: grid (ceil(D/64), nc, b), 256 threads; the 4 lanes of a quad
-// share a channel and hold 4 states each.  For chunk c = [s, e]:
+// k_chunk_aggr: grid (ceil(D/64), nc, b), one wave per workgroup; each lane owns
+// one channel and all 16 of its states.  For chunk c = [s, e]:
 //   hloc = state at e from a zero carry-in,
 //   mloc = sum_{t in c} g_t C_t prod_{j=s}^{t} a_j  (the adjoint that the chunk
 //          hands to h_{s-1} from a zero carry at its end),
 //   sdel = sum_{t in c} Delta_t (fp64);
-// with WANT_M (the gradient) also, for each segment of p.seg steps of the
-// chunk, the state at the segment start from a zero carry-in (hseg) and the sum
-// of Delta from the chunk start to the segment start (cseg): the fused gradient
+// with WANT_M (the gradient) also, for each segment of SEG steps of the chunk,
+// the state at the segment start from a zero carry-in (hseg) and the sum of
+// Delta from the chunk start to the segment start (cseg): the fused gradient
 // kernel rebuilds its segment-start states from them and the chunk carry.
-// B and C are staged in LDS as fp32, 64 steps at a time, for the whole
-// workgroup, double-buffered: the next block's loads are in flight while the
-// current block is processed, and one barrier per block publishes it.  Lane r
-// prepares the per-channel quantities of steps s+r, s+r+4, ... and broadcasts
-// them to its quad; its raw inputs are loaded two 4-step groups ahead, so a
-// whole group of arithmetic lies between the issue of a load and its use.
+// B_t and C_t are the same for every channel: they are read with scalar loads
+// (the rows of step t+1 while step t runs) and enter the arithmetic as scalar
+// operands, so nothing is staged in LDS or exchanged between lanes, and the
+// per-(channel, step) preparation (softplus, gate, the Delta sum) is done once
+// per step for all 16 states.  The raw inputs x, Delta, dy, z are loaded one
+// 4-step group ahead.  Steps past the end of the sequence (in the last group)
+// have Delta = x = g = 0 and leave h, P, m and the sum unchanged.
 // ---------------------------------------------------------------------------
-template <typename TI, bool SP, bool GATE, bool WANT_M, int SEG>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_chunk_aggr(const ScanProblem p) {
-    constexpr int SB = 64;  // steps per staged block
-    constexpr int PT = SB * 32 / 256;  // staged values per thread
-    static_assert(SB % SEG == 0 && SEG % 4 == 0, "segments tile the staged blocks");
-    __shared__ __attribute__((aligned(16))) float bcs[2][SB][32];
-    const int tid = threadIdx.x;
-    const int r = tid & 3;
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);  // < Dp
+template <typename TI, bool SP, bool GATE, bool WANT_M, bool N16, int SEG>
+__global__ __launch_bounds__(64) void k_chunk_aggr(const ScanProblem p) {
+    constexpr int G = 4;  // steps per group
+    static_assert(SEG % G == 0, "segments are whole groups");
+    constexpr uint32_t kEl = sizeof(TI);
+    const int lane = threadIdx.x;
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + lane;  // < Dp
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const bool dv = d < p.D;
-    const TI* Bp = static_cast<const TI*>(p.B);
-    const TI* Cp = static_cast<const TI*>(p.C);
-    float cn[4], wn[4];
-    lane_consts(p.A_log, d, r, p.N, dv, p.ascalar, cn, wn);
-    float h[4] = {0.f, 0.f, 0.f, 0.f}, m[4] = {0.f, 0.f, 0.f, 0.f}, P[4] = {1.f, 1.f, 1.f, 1.f};
+    float cn[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const bool v = dv && k < p.N;
+        const float al = ldm(p.A_log, p.ascalar ? d : d * p.N + k, v);  // one rate per channel, or per state
+        const float e = v ? __expf(al) : 0.f;
+        cn[k] = -e * kLog2e;
+    }
+    float h[16], m[16], P[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        h[k] = 0.f;
+        m[k] = 0.f;
+        P[k] = 1.f;
+    }
     double sd = 0.0;
     const int64_t t0 = c * p.L;
     const int64_t t1 = min(t0 + p.L, p.T);
-    // segment records (WANT_M): slot q holds the record of segment q
-    const uint32_t nseg = WANT_M ? static_cast<uint32_t>(p.L / SEG) : 0u;
-    const int64_t sgb = (bb * p.nc + c) * nseg * p.Dp + d;
-    auto put_seg = [&](uint32_t q, float cum) {
-        *reinterpret_cast<float4*>(p.hseg + (sgb + q * p.Dp) * 16 + 4 * r) = make_float4(h[0], h[1], h[2], h[3]);
-        p.cseg[sgb + q * p.Dp] = cum;
+    const int64_t rowb = bb * p.T;  // first row of the sequence
+    const TI* Bp = static_cast<const TI*>(p.B);
+    const TI* Cp = static_cast<const TI*>(p.C);
+    // The chunk's rows of x, Delta, dy, z through buffer resources: the lane's
+    // byte offset is fixed (padding channels read out of range, i.e. zero) and the
+    // step's row offset is a scalar.
+    const int64_t e0 = (rowb + t0) * p.D;  // the chunk's first element
+    const int nbytes = static_cast<int>((t1 - t0) * p.D * kEl);
+    auto rs = [&](const void* base) {
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<TI*>(static_cast<const TI*>(base) + e0), 0, nbytes,
+                                                 0x00020000);
     };
-    // the quad's Delta sum so far, added in lane order
-    auto quad_total = [&]() {
-        return ((quad_bcast_d(sd, 0) + quad_bcast_d(sd, 1)) + quad_bcast_d(sd, 2)) + quad_bcast_d(sd, 3);
+    const __amdgpu_buffer_rsrc_t rX = rs(p.x), rD = rs(p.delta);
+    const __amdgpu_buffer_rsrc_t rY = WANT_M ? rs(p.dy) : rX, rZ = (WANT_M && GATE) ? rs(p.z) : rX;
+    const uint32_t voff = dv ? static_cast<uint32_t>(d) * kEl : 0x80000000u;
+    const int rowbytes = static_cast<int>(p.D * kEl);
+    // step indices below are local to the chunk (32-bit: scalar compares and
+    // minima; the scalar unit has no 64-bit signed compare)
+    const int nl = static_cast<int>(t1 - t0);
+    auto ld = [&](__amdgpu_buffer_rsrc_t r, int tl) -> uint32_t {  // element bits of local step tl
+        const int so = tl * rowbytes;
+        if constexpr (kEl == 2) return __builtin_amdgcn_raw_buffer_load_b16(r, voff, so, 0);
+        else return __builtin_amdgcn_raw_buffer_load_b32(r, voff, so, 0);
     };
-    // B/C values of the staged block starting at step sb (padding and steps past
-    // the chunk read as 0)
-    // raw element bits and validity masks, applied when the block is stored (a
-    // masked value right after its load would make each load wait on the spot)
-    typename RawIn<TI, 1>::Bits bcv[PT];
-    uint32_t bcm[PT];
-    auto load_bc = [&](int64_t sb) {
-#pragma unroll
-        for (int e = 0; e < PT; ++e) {
-            const int i = tid + 256 * e;
-            const int t = i >> 5, cc = i & 31, n = cc & 15;
-            const int64_t tg = sb + t;
-            const bool ok = (cc < 16 || WANT_M) && tg < t1 && n < p.N;
-            bcm[e] = ok ? 0xffffffffu : 0u;
-            bcv[e] = ldbits(cc < 16 ? Bp : Cp, ok ? (bb * p.T + tg) * p.N + n : 0);
-        }
+    auto cvt = [](uint32_t b) { return __uint_as_float(kEl == 2 ? b << 16 : b); };
+    // segment records (WANT_M): slot q holds the record of segment q; padding
+    // channels record zero sums
+    const int64_t nseg = WANT_M ? p.L / SEG : 0;
+    const int64_t sgb = (bb * p.nc + c) * nseg * p.Dp;
+    auto put_seg = [&](int64_t q) {
+        float4* rec = reinterpret_cast<float4*>(p.hseg + (sgb + q * p.Dp) * 16) + 4 * static_cast<uint32_t>(d);
+        rec[0] = make_float4(h[0], h[1], h[2], h[3]);
+        rec[1] = make_float4(h[4], h[5], h[6], h[7]);
+        rec[2] = make_float4(h[8], h[9], h[10], h[11]);
+        rec[3] = make_float4(h[12], h[13], h[14], h[15]);
+        (p.cseg + sgb + q * p.Dp)[static_cast<uint32_t>(d)] = dv ? static_cast<float>(sd) : 0.f;
     };
-    auto store_bc = [&](int buf) {
-#pragma unroll
-        for (int e = 0; e < PT; ++e) {
-            const int i = tid + 256 * e;
-            const uint32_t b = sizeof(TI) == 2 ? static_cast<uint32_t>(bcv[e]) << 16 : static_cast<uint32_t>(bcv[e]);
-            bcs[buf][i >> 5][i & 31] = __uint_as_float(b & bcm[e]);
-        }
-    };
-    load_bc(t0);
-    store_bc(0);
-    load_bc(t0 + SB);  // block 1 (all padding when the chunk has one block)
-    // raw inputs of the next two groups of 4 steps, in two buffers used
-    // alternately (no copies of data still in flight)
-    RawIn<TI, 1> n1, n2;
-    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, WANT_M, n1);
-    load_raw<TI, GATE, 1>(p, bb, t0 + 4, d, dv, r, WANT_M, n2);
-    lds_barrier();
-    int buf = 0;
-    // One group of 4 steps from s0, its raw inputs in `nb`, which is then
-    // refilled with the group two ahead.  Steps past the end of the sequence have
-    // Delta = x = g = 0 and B = C = 0, so they leave h, P, m and the Delta sum
-    // unchanged; every group of the chunk runs (no tail branch).
-    auto group = [&](int64_t s0, int64_t sb, RawIn<TI, 1>& nb) {
+    // one step from its raw inputs and its rows of B and C
+    auto step = [&](uint32_t xb, uint32_t pb, uint32_t yb, uint32_t zb, const SRow<TI, N16>& cB,
+                    const SRow<TI, N16>& cC) __attribute__((always_inline)) {
+        float xr = cvt(xb);
+        const float dl = SP ? softplus_f(cvt(pb)) : cvt(pb);
+        if (p.bdelta) xr *= dl;  // input term Delta B x
+        float g = 0.f;
         if constexpr (WANT_M) {
-            const uint32_t tl = static_cast<uint32_t>(s0 - t0);
-            if (tl % SEG == 0) put_seg(tl / SEG, static_cast<float>(quad_total()));  // uniform
-        }
-        // this group's raw inputs are converted first, then `nb` is refilled: a
-        // register is only reloaded once its value has been used, so the
-        // compiler never copies a load that is still in flight
-        const bool v = dv && s0 + r < t1;
-        const float pr = fin<TI>(nb.p[0], v);
-        float xr = fin<TI>(nb.x[0], v);
-        const float dyr = WANT_M ? fin<TI>(nb.dy[0], v) : 0.f;
-        const float zr = (WANT_M && GATE) ? fin<TI>(nb.z[0], v) : 0.f;
-        // issued on every path (past the end it reloads valid data that is not
-        // used), so that later waits count exactly; the scheduling barrier keeps
-        // the loads ahead of this group's arithmetic
-        load_raw<TI, GATE, 1>(p, bb, s0 + 8, d, dv, r, WANT_M, nb);
-        __builtin_amdgcn_sched_barrier(0);
-        const float dlr = SP ? softplus_sel(pr, v) : pr;
-        if (p.bdelta) xr *= dlr;  // input term Delta B x
-        float gr = 0.f;
-        if constexpr (WANT_M) gr = GATE ? dyr * zr * sigmoid_f(zr) : dyr;
-        sd += static_cast<double>(dlr);
-        const int tb = static_cast<int>(s0 - sb);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const float xv = quad_bcast(xr, j);
-            const float dl = quad_bcast(dlr, j);
-            const float4 b4 = *reinterpret_cast<const float4*>(&bcs[buf][tb + j][4 * r]);
-            const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
-            float Cv[4] = {0.f, 0.f, 0.f, 0.f};
-            if constexpr (WANT_M) {
-                const float4 c4 = *reinterpret_cast<const float4*>(&bcs[buf][tb + j][16 + 4 * r]);
-                Cv[0] = c4.x; Cv[1] = c4.y; Cv[2] = c4.z; Cv[3] = c4.w;
+            const float dyr = cvt(yb);
+            if constexpr (GATE) {
+                const float zr = cvt(zb);
+                g = dyr * zr * sigmoid_f(zr);
+            } else {
+                g = dyr;
             }
-            const float g = WANT_M ? quad_bcast(gr, j) : 0.f;
+        }
+        sd += static_cast<double>(dl);
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const float av = fexp2(cn[k] * dl);
-                h[k] = fmaf(av, h[k], Bv[k] * xv);
-                if constexpr (WANT_M) {
-                    P[k] *= av;
-                    m[k] = fmaf(g * Cv[k], P[k], m[k]);
-                }
+        for (int k = 0; k < 16; ++k) {
+            const float av = fexp2(cn[k] * dl);
+            h[k] = fmaf(av, h[k], cB.at(k) * xr);
+            if constexpr (WANT_M) {
+                P[k] *= av;
+                m[k] = fmaf(g * cC.at(k), P[k], m[k]);
             }
         }
     };
-    for (int64_t sb = t0; sb < t1; sb += SB) {
-        // the block's groups, up to the chunk edge (L and SB are multiples of 8)
-        const int64_t se = min(sb + SB, t0 + p.L);
-        for (int64_t s0 = sb; s0 < se; s0 += 8) {
-            group(s0, sb, n1);
-            group(s0 + 4, sb, n2);
+    // Whole groups: the raw inputs of each step are loaded one group ahead into
+    // its slot (past the chunk: its last row again, not used), the rows of B and C
+    // one step ahead.
+    const int ngrp = nl / G;
+    RawIn<TI, G> raw;
+    auto load_slot = [&](int tl, int j) __attribute__((always_inline)) {
+        const int tc = min(tl, nl - 1);
+        raw.x[j] = ld(rX, tc);
+        raw.p[j] = ld(rD, tc);
+        if constexpr (WANT_M) {
+            raw.dy[j] = ld(rY, tc);
+            raw.z[j] = GATE ? ld(rZ, tc) : 0;
         }
-        // publish the next block (its buffer was last read before the previous
-        // barrier) and start loading the one after it
-        store_bc(buf ^ 1);
-        load_bc(sb + 2 * SB);
-        lds_barrier();
-        buf ^= 1;
+    };
+    SRow<TI, N16> nB, nC;  // B and C rows of the next step
+    if (ngrp > 0) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) load_slot(j, j);
+        nB.load(Bp, rowb + t0, p.N);
+        if constexpr (WANT_M) nC.load(Cp, rowb + t0, p.N);
+    }
+    for (int gi = 0; gi < ngrp; ++gi) {
+        const int s0 = gi * G;
+        if constexpr (WANT_M)
+            if (s0 % SEG == 0) put_seg(s0 / SEG);  // uniform
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int t = s0 + j;
+            // this step's raw inputs are taken first, then the slot is refilled (the
+            // loads are issued on every path, so that later waits count exactly)
+            const uint32_t xb = raw.x[j], pb = raw.p[j];
+            const uint32_t yb = WANT_M ? raw.dy[j] : 0u, zb = (WANT_M && GATE) ? raw.z[j] : 0u;
+            load_slot(t + G, j);
+            const SRow<TI, N16> cB = nB;
+            SRow<TI, N16> cC;
+            const int64_t rn = rowb + t0 + min(t + 1, nl - 1);
+            nB.load(Bp, rn, p.N);
+            if constexpr (WANT_M) {
+                cC = nC;
+                nC.load(Cp, rn, p.N);
+            }
+            step(xb, pb, yb, zb, cB, cC);
+        }
+    }
+    // the steps after the last whole group (fewer than G: the end of the sequence)
+    for (int t = ngrp * G; t < nl; ++t) {
+        if constexpr (WANT_M)
+            if (t % SEG == 0) put_seg(t / SEG);
+        SRow<TI, N16> cB, cC;
+        cB.load(Bp, rowb + t0 + t, p.N);
+        if constexpr (WANT_M) cC.load(Cp, rowb + t0 + t, p.N);
+        step(ld(rX, t), ld(rD, t), WANT_M ? ld(rY, t) : 0u, (WANT_M && GATE) ? ld(rZ, t) : 0u, cB, cC);
     }
     if constexpr (WANT_M) {
-        // segments that start in a block past the end of the sequence hold the final state
-        const float cum = static_cast<float>(quad_total());
-        const uint32_t done = static_cast<uint32_t>((t1 - t0 + SB - 1) / SB * SB / SEG);
-        for (uint32_t q = done; q < nseg; ++q) put_seg(q, cum);
+        // segments that start past the end of the sequence hold the final state
+        for (int64_t q = (nl + SEG - 1) / SEG; q < nseg; ++q) put_seg(q);
     }
-    // sum of Delta over the quad's prepared steps, in a fixed order
-    const double s1 = __shfl_xor(sd, 1);
-    const double s2 = __shfl_xor(sd, 2);
-    const double s3 = __shfl_xor(sd, 3);
     if (!dv) return;
-    const int64_t cb = ((bb * p.nc + c) * p.N + r * 4) * p.D + d;
+    const int64_t cb = (bb * p.nc + c) * p.N * p.D + d;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        if (r * 4 + k < p.N) {
+    for (int k = 0; k < 16; ++k) {
+        if (k < p.N) {
             p.hbuf[cb + k * p.D] = h[k];
             if constexpr (WANT_M) p.mbuf[cb + k * p.D] = m[k];
         }
     }
-    if (r == 0) p.sdel[(bb * p.nc + c) * p.D + d] = ((sd + s1) + s2) + s3;
+    p.sdel[(bb * p.nc + c) * p.D + d] = sd;
+}
+
+inline dim3 aggr_grid(const ScanProblem& p) {
+    return dim3(static_cast<unsigned>((p.D + 63) / 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
 }
 
 // ---------------------------------------------------------------------------
@@ -1366,7 +1417,7 @@ hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
     dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
-        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, 8>), g4, dim3(256), 0, s, p);
+        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, N16, 8>), aggr_grid(p), dim3(64), 0, s, p);
     }
     {
         SSMK_TIMED("carry", s);
@@ -1402,13 +1453,12 @@ hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
     if (p.dd16 && !(p.dz16 && p.bc16)) return hipErrorInvalidValue;
     if ((p.dx16 || p.only16) && !p.dd16) return hipErrorInvalidValue;
     if (p.only16 && !p.dx16) return hipErrorInvalidValue;
-    dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
         if (p.seg == 16)
-            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, 16>), g4, dim3(256), 0, s, p);
+            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16, 16>), aggr_grid(p), dim3(64), 0, s, p);
         else
-            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, 8>), g4, dim3(256), 0, s, p);
+            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16, 8>), aggr_grid(p), dim3(64), 0, s, p);
     }
     {
         SSMK_TIMED("carry", s);

@@ -115,6 +115,11 @@ def test_workspace_queries(lib):
     assert lib.ssm_adjoint_grad_pairs_workspace_size(ctypes.byref(d), ssm.SSM_TRUNCATED, 0, ctypes.byref(n)) == 2
     assert lib.ssm_proj_grad_workspace_size(8192, 1536, 1568, 0, ctypes.byref(n)) == 0
     assert lib.ssm_proj_grad_workspace_size(0, 1, 1, 0, ctypes.byref(n)) == 2
+    # the channel limit: chunk byte offsets stay 32-bit
+    assert lib.ssm_adjoint_grad_workspace_size(ctypes.byref(desc(channels=1 << 20)), ssm.SSM_FULL, 0,
+                                               ctypes.byref(n)) == 0
+    assert lib.ssm_adjoint_grad_workspace_size(ctypes.byref(desc(channels=(1 << 20) + 1)), ssm.SSM_FULL, 0,
+                                               ctypes.byref(n)) == 2
     ld = desc(batch=2, seqlen=4096, channels=1536, in_dtype=ssm.SSM_BF16)
     assert lib.ssm_layer_grad_workspace_size(ctypes.byref(ld), ssm.SSM_FULL, 0, 768, ctypes.byref(n)) == 0
     assert n.value > 0
