@@ -314,6 +314,54 @@ struct SRow {
     }
 };
 
+// Decay constants cn = -e^{A_log} log2(e) (a = 2^{cn Delta}) of the 16 states of
+// channel d (one rate per channel with the scalar-decay variant); padding
+// states and channels get 0.
+__device__ __forceinline__ void lane_rates16(const ScanProblem& p, int64_t d, bool dv, float cn[16]) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const bool v = dv && k < p.N;
+        const float al = ldm(p.A_log, p.ascalar ? d : d * p.N + k, v);
+        const float e = v ? __expf(al) : 0.f;
+        cn[k] = -e * kLog2e;
+    }
+}
+
+// The [b][T][D] inputs x, Delta, dy, z of one chunk for a wave of 64 channels
+// (one per lane): buffer resources over the chunk's rows, the lane's fixed byte
+// offset (padding channels read out of range, i.e. zero) and the step's row
+// offset as a scalar.  Step indices are local to the chunk and 32-bit, so that
+// their compares and minima stay on the scalar unit (which has no 64-bit signed
+// compare); byte offsets within a chunk fit 31 bits (L <= 256, D <= 2^20).
+template <typename TI>
+struct ChunkRows {
+    static constexpr uint32_t kEl = sizeof(TI);
+    __amdgpu_buffer_rsrc_t x, p, dy, z;
+    uint32_t voff;
+    int rowbytes;
+
+    __device__ __forceinline__ void init(const ScanProblem& q, int64_t row0, int nl, int64_t d, bool dv) {
+        const int64_t e0 = row0 * q.D;  // the chunk's first element
+        const int nbytes = static_cast<int>(nl * q.D * kEl);
+        auto rs = [&](const void* base) {
+            return __builtin_amdgcn_make_buffer_rsrc(const_cast<TI*>(static_cast<const TI*>(base) + e0), 0, nbytes,
+                                                     0x00020000);
+        };
+        x = rs(q.x);
+        p = rs(q.delta);
+        dy = q.dy ? rs(q.dy) : x;
+        z = q.z ? rs(q.z) : x;
+        voff = dv ? static_cast<uint32_t>(d) * kEl : 0x80000000u;
+        rowbytes = static_cast<int>(q.D * kEl);
+    }
+    // element bits of local step tl
+    __device__ __forceinline__ uint32_t ld(__amdgpu_buffer_rsrc_t r, int tl) const {
+        if constexpr (kEl == 2) return __builtin_amdgcn_raw_buffer_load_b16(r, voff, tl * rowbytes, 0);
+        else return __builtin_amdgcn_raw_buffer_load_b32(r, voff, tl * rowbytes, 0);
+    }
+    static __device__ __forceinline__ float cvt(uint32_t b) { return __uint_as_float(kEl == 2 ? b << 16 : b); }
+};
+
 // ---------------------------------------------------------------------------
 // k_chunk_aggr: grid (ceil(D/64), nc, b), one wave per workgroup; each lane owns
 // one channel and all 16 of its states.  For chunk c = [s, e]:
@@ -337,19 +385,12 @@ template <typename TI, bool SP, bool GATE, bool WANT_M, bool N16, int SEG>
 __global__ __launch_bounds__(64) void k_chunk_aggr(const ScanProblem p) {
     constexpr int G = 4;  // steps per group
     static_assert(SEG % G == 0, "segments are whole groups");
-    constexpr uint32_t kEl = sizeof(TI);
     const int lane = threadIdx.x;
     const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + lane;  // < Dp
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const bool dv = d < p.D;
     float cn[16];
-#pragma unroll
-    for (int k = 0; k < 16; ++k) {
-        const bool v = dv && k < p.N;
-        const float al = ldm(p.A_log, p.ascalar ? d : d * p.N + k, v);  // one rate per channel, or per state
-        const float e = v ? __expf(al) : 0.f;
-        cn[k] = -e * kLog2e;
-    }
+    lane_rates16(p, d, dv, cn);
     float h[16], m[16], P[16];
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
@@ -363,28 +404,11 @@ __global__ __launch_bounds__(64) void k_chunk_aggr(const ScanProblem p) {
     const int64_t rowb = bb * p.T;  // first row of the sequence
     const TI* Bp = static_cast<const TI*>(p.B);
     const TI* Cp = static_cast<const TI*>(p.C);
-    // The chunk's rows of x, Delta, dy, z through buffer resources: the lane's
-    // byte offset is fixed (padding channels read out of range, i.e. zero) and the
-    // step's row offset is a scalar.
-    const int64_t e0 = (rowb + t0) * p.D;  // the chunk's first element
-    const int nbytes = static_cast<int>((t1 - t0) * p.D * kEl);
-    auto rs = [&](const void* base) {
-        return __builtin_amdgcn_make_buffer_rsrc(const_cast<TI*>(static_cast<const TI*>(base) + e0), 0, nbytes,
-                                                 0x00020000);
-    };
-    const __amdgpu_buffer_rsrc_t rX = rs(p.x), rD = rs(p.delta);
-    const __amdgpu_buffer_rsrc_t rY = WANT_M ? rs(p.dy) : rX, rZ = (WANT_M && GATE) ? rs(p.z) : rX;
-    const uint32_t voff = dv ? static_cast<uint32_t>(d) * kEl : 0x80000000u;
-    const int rowbytes = static_cast<int>(p.D * kEl);
-    // step indices below are local to the chunk (32-bit: scalar compares and
-    // minima; the scalar unit has no 64-bit signed compare)
-    const int nl = static_cast<int>(t1 - t0);
-    auto ld = [&](__amdgpu_buffer_rsrc_t r, int tl) -> uint32_t {  // element bits of local step tl
-        const int so = tl * rowbytes;
-        if constexpr (kEl == 2) return __builtin_amdgcn_raw_buffer_load_b16(r, voff, so, 0);
-        else return __builtin_amdgcn_raw_buffer_load_b32(r, voff, so, 0);
-    };
-    auto cvt = [](uint32_t b) { return __uint_as_float(kEl == 2 ? b << 16 : b); };
+    const int nl = static_cast<int>(t1 - t0);  // the chunk's steps
+    ChunkRows<TI> cr;
+    cr.init(p, rowb + t0, nl, d, dv);
+    auto ld = [&](__amdgpu_buffer_rsrc_t r, int tl) { return cr.ld(r, tl); };
+    auto cvt = [](uint32_t b) { return ChunkRows<TI>::cvt(b); };
     // segment records (WANT_M): slot q holds the record of segment q; padding
     // channels record zero sums
     const int64_t nseg = WANT_M ? p.L / SEG : 0;
@@ -398,21 +422,12 @@ __global__ __launch_bounds__(64) void k_chunk_aggr(const ScanProblem p) {
         (p.cseg + sgb + q * p.Dp)[static_cast<uint32_t>(d)] = dv ? static_cast<float>(sd) : 0.f;
     };
     // one step from its raw inputs and its rows of B and C
-    auto step = [&](uint32_t xb, uint32_t pb, uint32_t yb, uint32_t zb, const SRow<TI, N16>& cB,
+    auto step = [&](float xr, float pr, float dyr, float zr, const SRow<TI, N16>& cB,
                     const SRow<TI, N16>& cC) __attribute__((always_inline)) {
-        float xr = cvt(xb);
-        const float dl = SP ? softplus_f(cvt(pb)) : cvt(pb);
+        const float dl = SP ? softplus_f(pr) : pr;
         if (p.bdelta) xr *= dl;  // input term Delta B x
         float g = 0.f;
-        if constexpr (WANT_M) {
-            const float dyr = cvt(yb);
-            if constexpr (GATE) {
-                const float zr = cvt(zb);
-                g = dyr * zr * sigmoid_f(zr);
-            } else {
-                g = dyr;
-            }
-        }
+        if constexpr (WANT_M) g = GATE ? dyr * zr * sigmoid_f(zr) : dyr;
         sd += static_cast<double>(dl);
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
@@ -431,11 +446,11 @@ __global__ __launch_bounds__(64) void k_chunk_aggr(const ScanProblem p) {
     RawIn<TI, G> raw;
     auto load_slot = [&](int tl, int j) __attribute__((always_inline)) {
         const int tc = min(tl, nl - 1);
-        raw.x[j] = ld(rX, tc);
-        raw.p[j] = ld(rD, tc);
+        raw.x[j] = ld(cr.x, tc);
+        raw.p[j] = ld(cr.p, tc);
         if constexpr (WANT_M) {
-            raw.dy[j] = ld(rY, tc);
-            raw.z[j] = GATE ? ld(rZ, tc) : 0;
+            raw.dy[j] = ld(cr.dy, tc);
+            raw.z[j] = GATE ? ld(cr.z, tc) : 0;
         }
     };
     SRow<TI, N16> nB, nC;  // B and C rows of the next step
@@ -452,10 +467,16 @@ __global__ __launch_bounds__(64) void k_chunk_aggr(const ScanProblem p) {
 #pragma unroll
         for (int j = 0; j < G; ++j) {
             const int t = s0 + j;
-            // this step's raw inputs are taken first, then the slot is refilled (the
-            // loads are issued on every path, so that later waits count exactly)
-            const uint32_t xb = raw.x[j], pb = raw.p[j];
-            const uint32_t yb = WANT_M ? raw.dy[j] : 0u, zb = (WANT_M && GATE) ? raw.z[j] : 0u;
+            // this step's raw inputs are converted first, then the slot is refilled: a
+            // register is reloaded only once its value is used, so the compiler never
+            // copies a load still in flight (it would wait for it).  The scheduler is
+            // left free here: it sinks the refills towards the end of the group and
+            // overlaps each step's per-channel chain (softplus, gate) with the previous
+            // step's state updates, which measured 4 % faster than keeping the loads
+            // a full group ahead (k_forward, with less arithmetic per step, keeps them
+            // there).
+            const float xr = cvt(raw.x[j]), pr = cvt(raw.p[j]);
+            const float dyr = WANT_M ? cvt(raw.dy[j]) : 0.f, zr = (WANT_M && GATE) ? cvt(raw.z[j]) : 0.f;
             load_slot(t + G, j);
             const SRow<TI, N16> cB = nB;
             SRow<TI, N16> cC;
@@ -465,7 +486,7 @@ __global__ __launch_bounds__(64) void k_chunk_aggr(const ScanProblem p) {
                 cC = nC;
                 nC.load(Cp, rn, p.N);
             }
-            step(xb, pb, yb, zb, cB, cC);
+            step(xr, pr, dyr, zr, cB, cC);
         }
     }
     // the steps after the last whole group (fewer than G: the end of the sequence)
@@ -475,7 +496,8 @@ __global__ __launch_bounds__(64) void k_chunk_aggr(const ScanProblem p) {
         SRow<TI, N16> cB, cC;
         cB.load(Bp, rowb + t0 + t, p.N);
         if constexpr (WANT_M) cC.load(Cp, rowb + t0 + t, p.N);
-        step(ld(rX, t), ld(rD, t), WANT_M ? ld(rY, t) : 0u, (WANT_M && GATE) ? ld(rZ, t) : 0u, cB, cC);
+        step(cvt(ld(cr.x, t)), cvt(ld(cr.p, t)), WANT_M ? cvt(ld(cr.dy, t)) : 0.f,
+             (WANT_M && GATE) ? cvt(ld(cr.z, t)) : 0.f, cB, cC);
     }
     if constexpr (WANT_M) {
         // segments that start past the end of the sequence hold the final state
@@ -594,101 +616,105 @@ inline dim3 carry_grid(const ScanProblem& p) {
 }
 
 // ---------------------------------------------------------------------------
-// k_forward: grid (ceil(D/64), nc, b), 256 threads; as in k_chunk_aggr the 4
-// lanes of a quad share a channel and hold 4 of its states.  y_t = sum_n C_t h_t
-// (times silu(z_t) with the gate), the state recomputed from the chunk carry-in
-// H_c.  B and C are staged in LDS 64 steps at a time for the workgroup; lane r
-// prepares the per-channel quantities of step s0+r of each group of 4 steps and
-// broadcasts them to its quad (its raw inputs loaded one group ahead); the
-// quad's sum over its states gives y_t, which the lane that prepared step t
-// finishes and stores.  Steps past the end of the chunk have Delta = x = 0 and
-// B = C = 0, so every group runs (no tail branch around the arithmetic).
+// k_forward: grid (ceil(D/64), nc, b), one wave per workgroup; as in
+// k_chunk_aggr each lane owns one channel and all 16 of its states, recomputed
+// from the chunk carry-in H_c, with B and C through scalar loads (one step
+// ahead) and the raw inputs through the chunk's buffer resources (one group
+// ahead; the steps after the last whole group run one by one).
+// y_t = sum_n C_t h_t (times silu(z_t) with the gate): four partial sums of four
+// states each, (S0 + S1) + (S2 + S3).
 // ---------------------------------------------------------------------------
-template <typename TI, bool SP, bool GATE>
-__global__ __launch_bounds__(256) void k_forward(const ScanProblem p) {
-    constexpr int SB = 64;             // steps per staged block
-    constexpr int PT = SB * 32 / 256;  // staged values per thread
-    __shared__ __attribute__((aligned(16))) float bcs[SB][32];
-    const int tid = threadIdx.x;
-    const int r = tid & 3;
-    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);
+template <typename TI, bool SP, bool GATE, bool N16>
+__global__ __launch_bounds__(64) void k_forward(const ScanProblem p) {
+    constexpr int G = 4;  // steps per group
+    const int lane = threadIdx.x;
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + lane;
     const int64_t c = blockIdx.y, bb = blockIdx.z;
     const bool dv = d < p.D;
-    const TI* Bp = static_cast<const TI*>(p.B);
-    const TI* Cp = static_cast<const TI*>(p.C);
-    TI* Y = static_cast<TI*>(p.y);
-    float cn[4], wn[4];
-    lane_consts(p.A_log, d, r, p.N, dv, p.ascalar, cn, wn);
-    const int64_t cb = ((bb * p.nc + c) * p.N + r * 4) * p.D + d;
-    float h[4];
+    float cn[16];
+    lane_rates16(p, d, dv, cn);
+    const int64_t cb = (bb * p.nc + c) * p.N * p.D + d;
+    float h[16];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) h[k] = ldm(p.hbuf, cb + k * p.D, dv && r * 4 + k < p.N);
+    for (int k = 0; k < 16; ++k) h[k] = ldm(p.hbuf, cb + k * p.D, dv && k < p.N);
     const int64_t t0 = c * p.L;
     const int64_t t1 = min(t0 + p.L, p.T);
-    RawIn<TI, 1> nb;
-    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, false, nb);
-    uint32_t zb = 0;
-    if constexpr (GATE) zb = ldbits(static_cast<const TI*>(p.z), dv && t0 + r < p.T ? (bb * p.T + t0 + r) * p.D + d : 0);
-    for (int64_t sb = t0; sb < t1; sb += SB) {
-        // the block's loads all issued before any is used (raw bits, masks
-        // applied at the store)
-        typename RawIn<TI, 1>::Bits bcv[PT];
-        uint32_t bcm[PT];
+    const int64_t rowb = bb * p.T;
+    const TI* Bp = static_cast<const TI*>(p.B);
+    const TI* Cp = static_cast<const TI*>(p.C);
+    const int nl = static_cast<int>(t1 - t0);
+    ChunkRows<TI> cr;
+    cr.init(p, rowb + t0, nl, d, dv);
+    // y of the chunk's rows through a buffer resource like the inputs' (padding
+    // channels store out of range, which writes nothing: no branch around the stores)
+    const __amdgpu_buffer_rsrc_t rY = __builtin_amdgcn_make_buffer_rsrc(
+        static_cast<TI*>(p.y) + (rowb + t0) * p.D, 0, static_cast<int>(nl * p.D * sizeof(TI)), 0x00020000);
+    auto step = [&](int tl, float xr, float pr, float zr, const SRow<TI, N16>& cB,
+                    const SRow<TI, N16>& cC) __attribute__((always_inline)) {
+        const float dl = SP ? softplus_f(pr) : pr;
+        if (p.bdelta) xr *= dl;  // input term Delta B x
+        float yq[4];
 #pragma unroll
-        for (int e = 0; e < PT; ++e) {
-            const int i = tid + 256 * e;
-            const int t = i >> 5, cc = i & 31, n = cc & 15;
-            const int64_t tg = sb + t;
-            const bool ok = tg < t1 && n < p.N;
-            bcm[e] = ok ? 0xffffffffu : 0u;
-            bcv[e] = ldbits(cc < 16 ? Bp : Cp, ok ? (bb * p.T + tg) * p.N + n : 0);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        lds_barrier();  // the previous block's reads are done
+        for (int i = 0; i < 4; ++i) {
+            float yp = 0.f;
 #pragma unroll
-        for (int e = 0; e < PT; ++e) {
-            const int i = tid + 256 * e;
-            const uint32_t b = sizeof(TI) == 2 ? static_cast<uint32_t>(bcv[e]) << 16 : static_cast<uint32_t>(bcv[e]);
-            bcs[i >> 5][i & 31] = __uint_as_float(b & bcm[e]);
-        }
-        lds_barrier();
-        const int64_t se = min(sb + SB, t1);
-        for (int64_t s0 = sb; s0 < se; s0 += 4) {
-            // this group's inputs, then the next group's loads
-            const bool v = dv && s0 + r < t1;
-            const float pr = fin<TI>(nb.p[0], v);
-            float xr = fin<TI>(nb.x[0], v);
-            float zr = 0.f;
-            if constexpr (GATE) zr = fin<TI>(zb, v);
-            load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, false, nb);
-            if constexpr (GATE) {
-                const int64_t tz = s0 + 4 + r;
-                zb = ldbits(static_cast<const TI*>(p.z), dv && tz < p.T ? (bb * p.T + tz) * p.D + d : 0);
+            for (int k = 4 * i; k < 4 * i + 4; ++k) {
+                h[k] = fmaf(fexp2(cn[k] * dl), h[k], cB.at(k) * xr);
+                yp = fmaf(cC.at(k), h[k], yp);
             }
-            const float dlr = SP ? softplus_sel(pr, v) : pr;
-            if (p.bdelta) xr *= dlr;  // input term Delta B x
-            float ypart[4];
-            const int tb = static_cast<int>(s0 - sb);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const float xv = quad_bcast(xr, j);
-                const float dl = quad_bcast(dlr, j);
-                const float4 b4 = *reinterpret_cast<const float4*>(&bcs[tb + j][4 * r]);
-                const float4 c4 = *reinterpret_cast<const float4*>(&bcs[tb + j][16 + 4 * r]);
-                const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
-                const float Cv[4] = {c4.x, c4.y, c4.z, c4.w};
-                float yp = 0.f;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
-                    yp = fmaf(Cv[k], h[k], yp);
-                }
-                ypart[j] = yp;
-            }
-            float yk = quad_sum_transposed(ypart, r);  // y of step s0 + r
-            if constexpr (GATE) yk *= zr * sigmoid_f(zr);
-            if (v) stf(Y, (bb * p.T + s0 + r) * p.D + d, yk);
+            yq[i] = yp;
         }
+        float y = (yq[0] + yq[1]) + (yq[2] + yq[3]);
+        if constexpr (GATE) y *= zr * sigmoid_f(zr);
+        if constexpr (sizeof(TI) == 2)
+            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, static_cast<__bf16>(y)), rY, cr.voff,
+                                                  tl * cr.rowbytes, 0);
+        else
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), rY, cr.voff, tl * cr.rowbytes, 0);
+    };
+    const int ngrp = nl / G;
+    RawIn<TI, G> raw;
+    auto load_slot = [&](int tl, int j) __attribute__((always_inline)) {
+        const int tc = min(tl, nl - 1);
+        raw.x[j] = cr.ld(cr.x, tc);
+        raw.p[j] = cr.ld(cr.p, tc);
+        raw.z[j] = GATE ? cr.ld(cr.z, tc) : 0;
+    };
+    SRow<TI, N16> nB, nC;
+    if (ngrp > 0) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            load_slot(j, j);
+            __builtin_amdgcn_sched_barrier(0);  // issued in the loop's order: the waits at its head count these
+        }
+        nB.load(Bp, rowb + t0, p.N);
+        nC.load(Cp, rowb + t0, p.N);
+    }
+    for (int gi = 0; gi < ngrp; ++gi) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int t = gi * G + j;
+            // converted before the slot is refilled (see k_chunk_aggr); the scheduling
+            // barriers keep the refills a full group ahead of their use (left free, the
+            // scheduler sinks them next to it)
+            const float xr = ChunkRows<TI>::cvt(raw.x[j]), pr = ChunkRows<TI>::cvt(raw.p[j]);
+            const float zr = GATE ? ChunkRows<TI>::cvt(raw.z[j]) : 0.f;
+            __builtin_amdgcn_sched_barrier(0);
+            load_slot(t + G, j);
+            const SRow<TI, N16> cB = nB, cC = nC;
+            const int64_t rn = rowb + t0 + min(t + 1, nl - 1);
+            nB.load(Bp, rn, p.N);
+            nC.load(Cp, rn, p.N);
+            __builtin_amdgcn_sched_barrier(0);  // the loads stay ahead of the step's arithmetic
+            step(t, xr, pr, zr, cB, cC);
+        }
+    }
+    for (int t = ngrp * G; t < nl; ++t) {
+        SRow<TI, N16> cB, cC;
+        cB.load(Bp, rowb + t0 + t, p.N);
+        cC.load(Cp, rowb + t0 + t, p.N);
+        step(t, ChunkRows<TI>::cvt(cr.ld(cr.x, t)), ChunkRows<TI>::cvt(cr.ld(cr.p, t)),
+             GATE ? ChunkRows<TI>::cvt(cr.ld(cr.z, t)) : 0.f, cB, cC);
     }
 }
 
@@ -1414,7 +1440,6 @@ inline unsigned cdiv(int64_t a, int64_t b) { return static_cast<unsigned>((a + b
 
 template <typename TI, bool SP, bool GATE, bool N16>
 hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
-    dim3 g4(cdiv(p.D, 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
     {
         SSMK_TIMED("chunk_aggr", s);
         hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, N16, 8>), aggr_grid(p), dim3(64), 0, s, p);
@@ -1424,7 +1449,7 @@ hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
         hipLaunchKernelGGL(k_carry, carry_grid(p), dim3(256), 0, s, p);
     }
     SSMK_TIMED("forward", s);
-    hipLaunchKernelGGL((k_forward<TI, SP, GATE>), g4, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((k_forward<TI, SP, GATE, N16>), aggr_grid(p), dim3(64), 0, s, p);
     return hipGetLastError();
 }
 
