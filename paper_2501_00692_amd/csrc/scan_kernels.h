@@ -766,41 +766,101 @@ struct __attribute__((aligned(16))) BCStage {
     }
 };
 
-// Wave-uniform pointers to the chunk-start row of the [b][T][D] tensors; a lane
-// addresses its element with the 32-bit offset tl*D + d.
-template <typename TI>
-struct ChunkPtrs {
-    const TI* x;
-    const TI* p;
-    const TI* dy;
-    const TI* z;
-    __device__ __forceinline__ void set(const ScanProblem& q, int64_t row) {
-        const int64_t base = row * q.D;
-        x = static_cast<const TI*>(q.x) + base;
-        p = static_cast<const TI*>(q.delta) + base;
-        dy = static_cast<const TI*>(q.dy) + base;
-        z = static_cast<const TI*>(q.z) + base;
+// One chunk's rows of a [b*T][ld] tensor for the quad layout of k_grad: a buffer
+// resource over the rows that exist; the lane of channel d at quad position r
+// reaches row tq + r + 4jj of a segment at its fixed byte offset d*el + r*rb (rb:
+// bytes per row) plus the scalar (tq + 4jj)*rb.  Padding channels, and rows past
+// the resource, take offsets with bit 31 set, past every range: loads read zero and
+// stores write nothing, with no branch and no address arithmetic per access.  Byte
+// offsets within a chunk fit 31 bits (L <= 256 rows of at most 2^20 fp32 values,
+// or of the bf16 copies' strides).
+struct QuadRows {
+    static constexpr uint32_t kOff = 0x80000000u;
+    __amdgpu_buffer_rsrc_t rs;
+    int rb;
+    __device__ __forceinline__ void init(const void* base, int64_t row0, int64_t rows, int64_t ld, int el) {
+        rb = static_cast<int>(ld * el);
+        rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(static_cast<const char*>(base)) + row0 * ld * el, 0,
+            static_cast<int>(max<int64_t>(0, rows) * rb), 0x00020000);
+    }
+    __device__ __forceinline__ uint32_t lane(uint32_t d, int r, int el, bool dv) const {
+        return dv ? d * static_cast<uint32_t>(el) + static_cast<uint32_t>(r * rb) : kOff;
+    }
+    __device__ __forceinline__ void st(uint32_t vo, int row, float v, std::true_type /*bf16*/) const {
+        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, static_cast<__bf16>(v)), rs, vo, row * rb, 0);
+    }
+    __device__ __forceinline__ void st(uint32_t vo, int row, float v, std::false_type /*fp32*/) const {
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rs, vo, row * rb, 0);
     }
 };
 
-// Raw inputs of the steps tl = tq + r + 4*jj (in-chunk index) that lane r prepares;
-// lanes whose step (tl >= lim) or channel is padding load element 0 instead.
-template <typename TI, bool GATE, int SPL>
-__device__ __forceinline__ void load_raw2(const ChunkPtrs<TI>& c, uint32_t D, uint32_t d, int tq,
-                                          int r, int64_t lim, bool dv, bool full, RawIn<TI, SPL>& o) {
+// The [b][T][D] inputs x, Delta, dy, z of one chunk (or of the chunk's steps shifted
+// by the window) in the quad layout.
+template <typename TI>
+struct QuadIn {
+    QuadRows x, p, dy, z;
+    int rows;  // rows that exist
+    __device__ __forceinline__ void init(const ScanProblem& q, int64_t row0, int64_t nrows) {
+        const int64_t n = min<int64_t>(max<int64_t>(nrows, 0), 1 << 20);
+        rows = static_cast<int>(n);
+        x.init(q.x, row0, n, q.D, sizeof(TI));
+        p.init(q.delta, row0, n, q.D, sizeof(TI));
+        dy.init(q.dy ? q.dy : q.x, row0, n, q.D, sizeof(TI));
+        z.init(q.z ? q.z : q.x, row0, n, q.D, sizeof(TI));
+    }
+    __device__ __forceinline__ uint32_t ld(const QuadRows& t, uint32_t vo, int so) const {
+        if constexpr (sizeof(TI) == 2) return __builtin_amdgcn_raw_buffer_load_b16(t.rs, vo, so, 0);
+        else return __builtin_amdgcn_raw_buffer_load_b32(t.rs, vo, so, 0);
+    }
+    // raw bits of the steps tq + r + 4jj this lane prepares (vb: its byte offset);
+    // steps past the rows that exist read zero
+    template <bool GATE, int SPL>
+    __device__ __forceinline__ void load(uint32_t vb, int tq, int r, RawIn<TI, SPL>& o) const {
 #pragma unroll
-    for (int jj = 0; jj < SPL; ++jj) {
-        const int tl = tq + r + 4 * jj;
-        const bool v = dv && tl < lim;
-        const uint32_t off = v ? static_cast<uint32_t>(tl) * D + d : 0u;
-        o.x[jj] = ldbits(c.x, off);
-        o.p[jj] = ldbits(c.p, off);
-        if (full) {
-            o.dy[jj] = ldbits(c.dy, off);
-            o.z[jj] = GATE ? ldbits(c.z, off) : 0;
+        for (int jj = 0; jj < SPL; ++jj) {
+            const uint32_t vo = tq + r + 4 * jj < rows ? vb : QuadRows::kOff;
+            const int so = (tq + 4 * jj) * x.rb;
+            o.x[jj] = ld(x, vo, so);
+            o.p[jj] = ld(p, vo, so);
+            o.dy[jj] = ld(dy, vo, so);
+            o.z[jj] = GATE ? ld(z, vo, so) : 0;
         }
     }
-}
+};
+
+// The same inputs at the window-shifted steps (truncated mode) through wave-uniform
+// base pointers and 32-bit lane offsets: a 64-bit address add per load, but two
+// scalar registers per tensor where a buffer resource takes four (the truncated
+// kernel's scalar registers are all in use, and resources it spills come back as
+// per-lane values whose loads the compiler serialises over their distinct values).
+// Lanes whose step (tl >= lim) or channel is padding load element 0 and the caller
+// masks the value.
+template <typename TI>
+struct QuadInPtr {
+    const TI* p;
+    const TI* dy;
+    const TI* z;
+    __device__ __forceinline__ void init(const ScanProblem& q, int64_t row) {
+        const int64_t base = row * q.D;
+        p = static_cast<const TI*>(q.delta) + base;
+        dy = static_cast<const TI*>(q.dy) + base;
+        z = static_cast<const TI*>(q.z ? q.z : q.delta) + base;
+    }
+    template <bool GATE, int SPL>
+    __device__ __forceinline__ void load(uint32_t D, uint32_t d, int tq, int r, int64_t lim, bool dv,
+                                         RawIn<TI, SPL>& o) const {
+#pragma unroll
+        for (int jj = 0; jj < SPL; ++jj) {
+            const int tl = tq + r + 4 * jj;
+            const uint32_t off = dv && tl < lim ? static_cast<uint32_t>(tl) * D + d : 0u;
+            o.x[jj] = 0;
+            o.p[jj] = ldbits(p, off);
+            o.dy[jj] = ldbits(dy, off);
+            o.z[jj] = GATE ? ldbits(z, off) : 0;
+        }
+    }
+};
 
 // Orders one wave's LDS writes before its own later LDS reads of other lanes'
 // data (LDS executes a wave's operations in order; this only stops the compiler
@@ -866,27 +926,29 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
     const int split = blockIdx.x;
     const int64_t t0 = c * L;
     const int64_t lim = p.T - t0;  // in-chunk steps tl < lim are real
-    const uint32_t D32 = static_cast<uint32_t>(p.D);
-    ChunkPtrs<TI> cp;
-    cp.set(p, bb * p.T + t0);
-    float* dxo = p.dx + (bb * p.T + t0) * p.D;
-    float* ddo = p.ddelta + (bb * p.T + t0) * p.D;
-    float* dzo = GATE ? p.dz + (bb * p.T + t0) * p.D : nullptr;
-    // OUT 1: also write the bf16 copies of ddelta and dz (and of dx when dx16 is
-    // given); OUT 2: write only the bf16 copies of dx, ddelta and dz (no fp32 dx,
-    // ddelta and dz), for callers that want only the projection GEMMs' operands
+    const int64_t row0 = bb * p.T + t0;
+    QuadIn<TI> qin;  // the chunk's inputs
+    qin.init(p, row0, min<int64_t>(L, lim));
+    // Per-step outputs over the same rows.  OUT 1: also write the bf16 copies of
+    // ddelta and dz (and of dx when dx16 is given); OUT 2: write only the bf16
+    // copies of dx, ddelta and dz (no fp32 dx, ddelta and dz), for callers that want
+    // only the projection GEMMs' operands.  Outputs a variant does not write get an
+    // empty resource.
     constexpr bool OUT16 = OUT > 0;
-    uint16_t* dd16o = OUT16 ? p.dd16 + (bb * p.T + t0) * p.ld_dd16 : nullptr;
-    uint16_t* dz16o = OUT16 ? p.dz16 + (bb * p.T + t0) * p.ld_dz16 : nullptr;
-    uint16_t* dx16o = (OUT16 && p.dx16) ? p.dx16 + (bb * p.T + t0) * p.ld_dx16 : nullptr;
-    const uint32_t ldd16 = static_cast<uint32_t>(p.ld_dd16), ldz16 = static_cast<uint32_t>(p.ld_dz16);
-    const uint32_t ldx16 = static_cast<uint32_t>(p.ld_dx16);
-    // Lanes whose step or channel is padding store into the sink instead, so
-    // that every store is issued without a branch and the waits for loads issued
-    // before them stay exact (a skipped store would make them wait for all
-    // outstanding stores).
+    auto out_rows = [&](const void* ptr, int64_t ld, int el) {
+        QuadRows o;
+        o.init(ptr ? ptr : p.x, row0, ptr ? qin.rows : 0, ld, el);
+        return o;
+    };
+    const QuadRows odx = out_rows(OUT != 2 ? p.dx : nullptr, p.D, 4);
+    const QuadRows odd = out_rows(OUT != 2 ? p.ddelta : nullptr, p.D, 4);
+    const QuadRows odz = out_rows(OUT != 2 && GATE ? p.dz : nullptr, p.D, 4);
+    const QuadRows o16x = out_rows(OUT16 ? p.dx16 : nullptr, p.ld_dx16, 2);
+    const QuadRows o16d = out_rows(OUT16 ? p.dd16 : nullptr, p.ld_dd16, 2);
+    const QuadRows o16z = out_rows(OUT16 ? p.dz16 : nullptr, p.ld_dz16, 2);
+    // Padding lanes of the per-tile dA_log store write into the sink instead, so
+    // that the store is issued without a branch.
     float* const sinkf = p.sink + lane;
-    uint16_t* const sink16 = reinterpret_cast<uint16_t*>(p.sink) + lane;
 
     const int64_t ntile = (p.D + 15) / 16;
     const int64_t tile_lo = static_cast<int64_t>(split) * p.tps;
@@ -895,12 +957,13 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
 
     // truncated mode: the chunk's steps shifted by tbar, and (16 states) a buffer
     // resource over the rows of C at the shifted steps that exist
-    ChunkPtrs<TI> cps;
+    QuadInPtr<TI> qis;
     int64_t lims = 0;
     if constexpr (TRUNC) {
-        cps.set(p, bb * p.T + min(t0 + p.tbar, p.T - 1));
         lims = p.T - (t0 + p.tbar);
+        qis.init(p, bb * p.T + min(t0 + p.tbar, p.T - 1));
     }
+    const uint32_t D32 = static_cast<uint32_t>(p.D);
     const int64_t c_rows = (TRUNC && N16) ? max<int64_t>(0, min<int64_t>(L, lims)) : 0;
     const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<TI*>(static_cast<const TI*>(p.C) + (bb * p.T + min(t0 + p.tbar, p.T)) * 16), 0,
@@ -955,12 +1018,18 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
         for (int k = 0; k < 4; ++k) nv[k] = dv && (r * 4 + k < p.N);
         const int64_t cb = ((bb * p.nc + c) * p.N + r * 4) * p.D + d;
         const uint32_t d32 = dv ? static_cast<uint32_t>(d) : 0u;
+        // the lane's byte offsets (row r of a quad's step group, channel d) in the
+        // inputs, the fp32 outputs and the bf16 copies
+        const uint32_t vbi = qin.x.lane(d32, r, sizeof(TI), dv);
+        const uint32_t vbo = odx.lane(d32, r, 4, dv);
+        const uint32_t vbx16 = o16x.lane(d32, r, 2, dv), vbd16 = o16d.lane(d32, r, 2, dv);
+        const uint32_t vbz16 = o16z.lane(d32, r, 2, dv);
 
         // inputs of the last segment, for the reverse sweep
         RawIn<TI, SPL> nxt;
         RawIn<TI, SPL> nxs;  // raw inputs at the shifted positions (truncated mode)
-        load_raw2<TI, GATE, SPL>(cp, D32, d32, (NCK - 1) * S, r, lim, dv, true, nxt);
-        if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, (NCK - 1) * S, r, lims, dv, true, nxs);
+        qin.template load<GATE, SPL>(vbi, (NCK - 1) * S, r, nxt);
+        if constexpr (TRUNC) qis.template load<GATE, SPL>(D32, d32, (NCK - 1) * S, r, lims, dv, nxs);
         using SC = ShiftedC<TI, S>;
         typename SC::Raw nxc{};  // shifted C rows of the next segment (truncated mode, 16 states)
         if constexpr (TRUNC && N16) nxc = SC::load(rsC, NCK - 1, lane);
@@ -1103,6 +1172,12 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             }
         }
 
+        // Everything the tile's prologue loaded is waited for here, once: the waits
+        // at the head of the segment loop are computed for the loop's entry and its
+        // back edge together, and with the prologue's loads (issued in another
+        // order) still in flight they came out as a full drain, every segment, of
+        // the next segment's inputs and the last segment's stores.
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), other counters unchanged
 #pragma unroll 1
         for (int q = NCK - 1; q >= 0; --q) {
             {
@@ -1120,8 +1195,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             {
                 // the next segment (segment 0 reloads itself; see the checkpoint sweep)
                 const int qn = q > 0 ? q - 1 : 0;
-                load_raw2<TI, GATE, SPL>(cp, D32, d32, qn * S, r, lim, dv, true, nxt);
-                if constexpr (TRUNC) load_raw2<TI, GATE, SPL>(cps, D32, d32, qn * S, r, lims, dv, true, nxs);
+                qin.template load<GATE, SPL>(vbi, qn * S, r, nxt);
+                if constexpr (TRUNC) qis.template load<GATE, SPL>(D32, d32, qn * S, r, lims, dv, nxs);
             }
             typename SC::Raw curc{};
             if constexpr (TRUNC && N16) {
@@ -1134,12 +1209,13 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) {
                 sv[jj] = dv && q * S + r + 4 * jj < lim;
-                const float pr = fin<TI>(cur.p[jj], sv[jj]), dyr = fin<TI>(cur.dy[jj], sv[jj]);
+                // (the loads read zero for padding steps and channels; softplus(0) is not 0)
+                const float pr = fin<TI>(cur.p[jj], true), dyr = fin<TI>(cur.dy[jj], true);
                 dls[jj] = SP ? softplus_sel(pr, sv[jj]) : pr;
-                xr[jj] = fin<TI>(cur.x[jj], sv[jj]);
+                xr[jj] = fin<TI>(cur.x[jj], true);
                 xs[jj] = p.bdelta ? xr[jj] * dls[jj] : xr[jj];  // the input term is (Delta) B x
                 if constexpr (GATE) {
-                    const float zr = fin<TI>(cur.z[jj], sv[jj]);
+                    const float zr = fin<TI>(cur.z[jj], true);
                     const float sg = sigmoid_f(zr);
                     gs[jj] = dyr * zr * sg;
                     gfs[jj] = dyr * sg * (1.f + zr * (1.f - sg));
@@ -1201,10 +1277,11 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             if constexpr (GATE) {
 #pragma unroll
                 for (int jj = 0; jj < SPL; ++jj) {
-                    const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
+                    const int row = q * S + 4 * jj;  // the quad's first row (the lane adds r)
+                    const uint32_t m = sv[jj] ? 0u : QuadRows::kOff;
                     const float v = gfs[jj] * yk[jj];
-                    if constexpr (OUT != 2) *(sv[jj] ? dzo + (tl * D32 + d32) : sinkf) = v;
-                    if constexpr (OUT16) stf(sv[jj] ? dz16o + (tl * ldz16 + d32) : sink16, 0, v);
+                    if constexpr (OUT != 2) odz.st(vbo | m, row, v, std::false_type{});
+                    if constexpr (OUT16) o16z.st(vbz16 | m, row, v, std::true_type{});
                 }
             }
             wave_sums(2 * pair);  // dC
@@ -1271,20 +1348,18 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             }
 #pragma unroll
             for (int jj = 0; jj < SPL; ++jj) {
-                const uint32_t tl = static_cast<uint32_t>(q * S + r + 4 * jj);
-                const uint32_t off = tl * D32 + d32;
+                const int row = q * S + 4 * jj;  // the quad's first row (the lane adds r)
+                const uint32_t m = sv[jj] ? 0u : QuadRows::kOff;
                 // with the Delta-scaled input, dx' = sum_n mubar B gives dx = dx' Delta and
                 // adds dx' x to dDelta
                 const float dd0 = p.bdelta ? fmaf(dxk[jj], xr[jj], ddk[jj]) : ddk[jj];
                 const float ddv = SP ? dd0 * (1.f - fexp(-dls[jj])) : dd0;  // d softplus / d Delta_pre
                 const float dxv = p.bdelta ? dxk[jj] * dls[jj] : dxk[jj];
-                if constexpr (OUT != 2) *(sv[jj] ? dxo + off : sinkf) = dxv;
-                if constexpr (OUT == 2) stf(sv[jj] ? dx16o + (tl * ldx16 + d32) : sink16, 0, dxv);
-                if constexpr (OUT == 1) {
-                    if (dx16o) stf(sv[jj] ? dx16o + (tl * ldx16 + d32) : sink16, 0, dxv);
-                }
-                if constexpr (OUT != 2) *(sv[jj] ? ddo + off : sinkf) = ddv;
-                if constexpr (OUT16) stf(sv[jj] ? dd16o + (tl * ldd16 + d32) : sink16, 0, ddv);
+                if constexpr (OUT != 2) odx.st(vbo | m, row, dxv, std::false_type{});
+                // the bf16 copy of dx (OUT 1: when given; without it the resource is empty)
+                if constexpr (OUT16) o16x.st(vbx16 | m, row, dxv, std::true_type{});
+                if constexpr (OUT != 2) odd.st(vbo | m, row, ddv, std::false_type{});
+                if constexpr (OUT16) o16d.st(vbd16 | m, row, ddv, std::true_type{});
             }
 #pragma unroll
             for (int k = 0; k < 4; ++k) dA[k] += dAs[k];
