@@ -253,7 +253,9 @@ hipError_t pairs_impl(const ScanProblem& p, float* dl, float* g, float* mu, int6
     }
     {
         SSMK_TIMED("chunk_aggr", s);
-        if (p.N == 16)
+        if (aggr_quad(p))
+            hipLaunchKernelGGL((k_chunk_aggr_quad<TI, SP, GATE, false, 8>), aggr_grid(p), dim3(256), 0, s, p);
+        else if (p.N == 16)
             hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, true, 8>), aggr_grid(p), dim3(64), 0, s, p);
         else
             hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, false, 8>), aggr_grid(p), dim3(64), 0, s, p);

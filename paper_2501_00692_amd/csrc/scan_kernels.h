@@ -518,6 +518,183 @@ __global__ __launch_bounds__(64) void k_chunk_aggr(const ScanProblem p) {
 inline dim3 aggr_grid(const ScanProblem& p) {
     return dim3(static_cast<unsigned>((p.D + 63) / 64), static_cast<unsigned>(p.nc), static_cast<unsigned>(p.nb));
 }
+// Grids of fewer than 2,048 waves at one lane per channel (about two per SIMD: a
+// short or narrow problem, e.g. b = 2, T = 4,096, D = 1,536) take the quad layout,
+// whose four times as many waves hide the latency that one lane per channel then
+// leaves exposed (there 78 against 98 us for the chunk aggregates, 60 against 68
+// us for the forward).
+inline bool aggr_quad(const ScanProblem& p) { return (p.D + 63) / 64 * p.nc * p.nb < 2048; }
+
+// ---------------------------------------------------------------------------
+// k_chunk_aggr_quad: the chunk aggregates of k_chunk_aggr for small grids: grid
+// (ceil(D/64), nc, b), 256 threads; the 4 lanes of a quad share a channel and
+// hold 4 states each (four times the waves of one lane per channel).  For chunk c = [s, e]:
+//   hloc = state at e from a zero carry-in,
+//   mloc = sum_{t in c} g_t C_t prod_{j=s}^{t} a_j  (the adjoint that the chunk
+//          hands to h_{s-1} from a zero carry at its end),
+//   sdel = sum_{t in c} Delta_t (fp64);
+// with WANT_M (the gradient) also, for each segment of p.seg steps of the
+// chunk, the state at the segment start from a zero carry-in (hseg) and the sum
+// of Delta from the chunk start to the segment start (cseg): the fused gradient
+// kernel rebuilds its segment-start states from them and the chunk carry.
+// B and C are staged in LDS as fp32, 64 steps at a time, for the whole
+// workgroup, double-buffered: the next block's loads are in flight while the
+// current block is processed, and one barrier per block publishes it.  Lane r
+// prepares the per-channel quantities of steps s+r, s+r+4, ... and broadcasts
+// them to its quad; its raw inputs are loaded two 4-step groups ahead, so a
+// whole group of arithmetic lies between the issue of a load and its use.
+// ---------------------------------------------------------------------------
+template <typename TI, bool SP, bool GATE, bool WANT_M, int SEG>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_chunk_aggr_quad(const ScanProblem p) {
+    constexpr int SB = 64;  // steps per staged block
+    constexpr int PT = SB * 32 / 256;  // staged values per thread
+    static_assert(SB % SEG == 0 && SEG % 4 == 0, "segments tile the staged blocks");
+    __shared__ __attribute__((aligned(16))) float bcs[2][SB][32];
+    const int tid = threadIdx.x;
+    const int r = tid & 3;
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);  // < Dp
+    const int64_t c = blockIdx.y, bb = blockIdx.z;
+    const bool dv = d < p.D;
+    const TI* Bp = static_cast<const TI*>(p.B);
+    const TI* Cp = static_cast<const TI*>(p.C);
+    float cn[4], wn[4];
+    lane_consts(p.A_log, d, r, p.N, dv, p.ascalar, cn, wn);
+    float h[4] = {0.f, 0.f, 0.f, 0.f}, m[4] = {0.f, 0.f, 0.f, 0.f}, P[4] = {1.f, 1.f, 1.f, 1.f};
+    double sd = 0.0;
+    const int64_t t0 = c * p.L;
+    const int64_t t1 = min(t0 + p.L, p.T);
+    // segment records (WANT_M): slot q holds the record of segment q
+    const uint32_t nseg = WANT_M ? static_cast<uint32_t>(p.L / SEG) : 0u;
+    const int64_t sgb = (bb * p.nc + c) * nseg * p.Dp + d;
+    auto put_seg = [&](uint32_t q, float cum) {
+        *reinterpret_cast<float4*>(p.hseg + (sgb + q * p.Dp) * 16 + 4 * r) = make_float4(h[0], h[1], h[2], h[3]);
+        p.cseg[sgb + q * p.Dp] = cum;
+    };
+    // the quad's Delta sum so far, added in lane order
+    auto quad_total = [&]() {
+        return ((quad_bcast_d(sd, 0) + quad_bcast_d(sd, 1)) + quad_bcast_d(sd, 2)) + quad_bcast_d(sd, 3);
+    };
+    // B/C values of the staged block starting at step sb (padding and steps past
+    // the chunk read as 0)
+    // raw element bits and validity masks, applied when the block is stored (a
+    // masked value right after its load would make each load wait on the spot)
+    typename RawIn<TI, 1>::Bits bcv[PT];
+    uint32_t bcm[PT];
+    auto load_bc = [&](int64_t sb) {
+#pragma unroll
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + 256 * e;
+            const int t = i >> 5, cc = i & 31, n = cc & 15;
+            const int64_t tg = sb + t;
+            const bool ok = (cc < 16 || WANT_M) && tg < t1 && n < p.N;
+            bcm[e] = ok ? 0xffffffffu : 0u;
+            bcv[e] = ldbits(cc < 16 ? Bp : Cp, ok ? (bb * p.T + tg) * p.N + n : 0);
+        }
+    };
+    auto store_bc = [&](int buf) {
+#pragma unroll
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + 256 * e;
+            const uint32_t b = sizeof(TI) == 2 ? static_cast<uint32_t>(bcv[e]) << 16 : static_cast<uint32_t>(bcv[e]);
+            bcs[buf][i >> 5][i & 31] = __uint_as_float(b & bcm[e]);
+        }
+    };
+    load_bc(t0);
+    store_bc(0);
+    load_bc(t0 + SB);  // block 1 (all padding when the chunk has one block)
+    // raw inputs of the next two groups of 4 steps, in two buffers used
+    // alternately (no copies of data still in flight)
+    RawIn<TI, 1> n1, n2;
+    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, WANT_M, n1);
+    load_raw<TI, GATE, 1>(p, bb, t0 + 4, d, dv, r, WANT_M, n2);
+    lds_barrier();
+    int buf = 0;
+    // One group of 4 steps from s0, its raw inputs in `nb`, which is then
+    // refilled with the group two ahead.  Steps past the end of the sequence have
+    // Delta = x = g = 0 and B = C = 0, so they leave h, P, m and the Delta sum
+    // unchanged; every group of the chunk runs (no tail branch).
+    auto group = [&](int64_t s0, int64_t sb, RawIn<TI, 1>& nb) {
+        if constexpr (WANT_M) {
+            const uint32_t tl = static_cast<uint32_t>(s0 - t0);
+            if (tl % SEG == 0) put_seg(tl / SEG, static_cast<float>(quad_total()));  // uniform
+        }
+        // this group's raw inputs are converted first, then `nb` is refilled: a
+        // register is only reloaded once its value has been used, so the
+        // compiler never copies a load that is still in flight
+        const bool v = dv && s0 + r < t1;
+        const float pr = fin<TI>(nb.p[0], v);
+        float xr = fin<TI>(nb.x[0], v);
+        const float dyr = WANT_M ? fin<TI>(nb.dy[0], v) : 0.f;
+        const float zr = (WANT_M && GATE) ? fin<TI>(nb.z[0], v) : 0.f;
+        // issued on every path (past the end it reloads valid data that is not
+        // used), so that later waits count exactly; the scheduling barrier keeps
+        // the loads ahead of this group's arithmetic
+        load_raw<TI, GATE, 1>(p, bb, s0 + 8, d, dv, r, WANT_M, nb);
+        __builtin_amdgcn_sched_barrier(0);
+        const float dlr = SP ? softplus_sel(pr, v) : pr;
+        if (p.bdelta) xr *= dlr;  // input term Delta B x
+        float gr = 0.f;
+        if constexpr (WANT_M) gr = GATE ? dyr * zr * sigmoid_f(zr) : dyr;
+        sd += static_cast<double>(dlr);
+        const int tb = static_cast<int>(s0 - sb);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float xv = quad_bcast(xr, j);
+            const float dl = quad_bcast(dlr, j);
+            const float4 b4 = *reinterpret_cast<const float4*>(&bcs[buf][tb + j][4 * r]);
+            const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
+            float Cv[4] = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (WANT_M) {
+                const float4 c4 = *reinterpret_cast<const float4*>(&bcs[buf][tb + j][16 + 4 * r]);
+                Cv[0] = c4.x; Cv[1] = c4.y; Cv[2] = c4.z; Cv[3] = c4.w;
+            }
+            const float g = WANT_M ? quad_bcast(gr, j) : 0.f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float av = fexp2(cn[k] * dl);
+                h[k] = fmaf(av, h[k], Bv[k] * xv);
+                if constexpr (WANT_M) {
+                    P[k] *= av;
+                    m[k] = fmaf(g * Cv[k], P[k], m[k]);
+                }
+            }
+        }
+    };
+    for (int64_t sb = t0; sb < t1; sb += SB) {
+        // the block's groups, up to the chunk edge (L and SB are multiples of 8)
+        const int64_t se = min(sb + SB, t0 + p.L);
+        for (int64_t s0 = sb; s0 < se; s0 += 8) {
+            group(s0, sb, n1);
+            group(s0 + 4, sb, n2);
+        }
+        // publish the next block (its buffer was last read before the previous
+        // barrier) and start loading the one after it
+        store_bc(buf ^ 1);
+        load_bc(sb + 2 * SB);
+        lds_barrier();
+        buf ^= 1;
+    }
+    if constexpr (WANT_M) {
+        // segments that start in a block past the end of the sequence hold the final state
+        const float cum = static_cast<float>(quad_total());
+        const uint32_t done = static_cast<uint32_t>((t1 - t0 + SB - 1) / SB * SB / SEG);
+        for (uint32_t q = done; q < nseg; ++q) put_seg(q, cum);
+    }
+    // sum of Delta over the quad's prepared steps, in a fixed order
+    const double s1 = __shfl_xor(sd, 1);
+    const double s2 = __shfl_xor(sd, 2);
+    const double s3 = __shfl_xor(sd, 3);
+    if (!dv) return;
+    const int64_t cb = ((bb * p.nc + c) * p.N + r * 4) * p.D + d;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if (r * 4 + k < p.N) {
+            p.hbuf[cb + k * p.D] = h[k];
+            if constexpr (WANT_M) p.mbuf[cb + k * p.D] = m[k];
+        }
+    }
+    if (r == 0) p.sdel[(bb * p.nc + c) * p.D + d] = ((sd + s1) + s2) + s3;
+}
 
 // ---------------------------------------------------------------------------
 // k_carry: 256 threads (4 waves); a unit is (sequence bb, direction, block of 64
@@ -715,6 +892,106 @@ __global__ __launch_bounds__(64) void k_forward(const ScanProblem p) {
         cC.load(Cp, rowb + t0 + t, p.N);
         step(t, ChunkRows<TI>::cvt(cr.ld(cr.x, t)), ChunkRows<TI>::cvt(cr.ld(cr.p, t)),
              GATE ? ChunkRows<TI>::cvt(cr.ld(cr.z, t)) : 0.f, cB, cC);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_forward_quad: the forward of k_forward for small grids (see aggr_quad): grid
+// (ceil(D/64), nc, b), 256 threads; as in k_chunk_aggr_quad the 4 lanes of a quad
+// share a channel and hold 4 of its states.  y_t = sum_n C_t h_t
+// (times silu(z_t) with the gate), the state recomputed from the chunk carry-in
+// H_c.  B and C are staged in LDS 64 steps at a time for the workgroup; lane r
+// prepares the per-channel quantities of step s0+r of each group of 4 steps and
+// broadcasts them to its quad (its raw inputs loaded one group ahead); the
+// quad's sum over its states gives y_t, which the lane that prepared step t
+// finishes and stores.  Steps past the end of the chunk have Delta = x = 0 and
+// B = C = 0, so every group runs (no tail branch around the arithmetic).
+// ---------------------------------------------------------------------------
+template <typename TI, bool SP, bool GATE>
+__global__ __launch_bounds__(256) void k_forward_quad(const ScanProblem p) {
+    constexpr int SB = 64;             // steps per staged block
+    constexpr int PT = SB * 32 / 256;  // staged values per thread
+    __shared__ __attribute__((aligned(16))) float bcs[SB][32];
+    const int tid = threadIdx.x;
+    const int r = tid & 3;
+    const int64_t d = static_cast<int64_t>(blockIdx.x) * 64 + (tid >> 2);
+    const int64_t c = blockIdx.y, bb = blockIdx.z;
+    const bool dv = d < p.D;
+    const TI* Bp = static_cast<const TI*>(p.B);
+    const TI* Cp = static_cast<const TI*>(p.C);
+    TI* Y = static_cast<TI*>(p.y);
+    float cn[4], wn[4];
+    lane_consts(p.A_log, d, r, p.N, dv, p.ascalar, cn, wn);
+    const int64_t cb = ((bb * p.nc + c) * p.N + r * 4) * p.D + d;
+    float h[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) h[k] = ldm(p.hbuf, cb + k * p.D, dv && r * 4 + k < p.N);
+    const int64_t t0 = c * p.L;
+    const int64_t t1 = min(t0 + p.L, p.T);
+    RawIn<TI, 1> nb;
+    load_raw<TI, GATE, 1>(p, bb, t0, d, dv, r, false, nb);
+    uint32_t zb = 0;
+    if constexpr (GATE) zb = ldbits(static_cast<const TI*>(p.z), dv && t0 + r < p.T ? (bb * p.T + t0 + r) * p.D + d : 0);
+    for (int64_t sb = t0; sb < t1; sb += SB) {
+        // the block's loads all issued before any is used (raw bits, masks
+        // applied at the store)
+        typename RawIn<TI, 1>::Bits bcv[PT];
+        uint32_t bcm[PT];
+#pragma unroll
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + 256 * e;
+            const int t = i >> 5, cc = i & 31, n = cc & 15;
+            const int64_t tg = sb + t;
+            const bool ok = tg < t1 && n < p.N;
+            bcm[e] = ok ? 0xffffffffu : 0u;
+            bcv[e] = ldbits(cc < 16 ? Bp : Cp, ok ? (bb * p.T + tg) * p.N + n : 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        lds_barrier();  // the previous block's reads are done
+#pragma unroll
+        for (int e = 0; e < PT; ++e) {
+            const int i = tid + 256 * e;
+            const uint32_t b = sizeof(TI) == 2 ? static_cast<uint32_t>(bcv[e]) << 16 : static_cast<uint32_t>(bcv[e]);
+            bcs[i >> 5][i & 31] = __uint_as_float(b & bcm[e]);
+        }
+        lds_barrier();
+        const int64_t se = min(sb + SB, t1);
+        for (int64_t s0 = sb; s0 < se; s0 += 4) {
+            // this group's inputs, then the next group's loads
+            const bool v = dv && s0 + r < t1;
+            const float pr = fin<TI>(nb.p[0], v);
+            float xr = fin<TI>(nb.x[0], v);
+            float zr = 0.f;
+            if constexpr (GATE) zr = fin<TI>(zb, v);
+            load_raw<TI, GATE, 1>(p, bb, s0 + 4, d, dv, r, false, nb);
+            if constexpr (GATE) {
+                const int64_t tz = s0 + 4 + r;
+                zb = ldbits(static_cast<const TI*>(p.z), dv && tz < p.T ? (bb * p.T + tz) * p.D + d : 0);
+            }
+            const float dlr = SP ? softplus_sel(pr, v) : pr;
+            if (p.bdelta) xr *= dlr;  // input term Delta B x
+            float ypart[4];
+            const int tb = static_cast<int>(s0 - sb);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float xv = quad_bcast(xr, j);
+                const float dl = quad_bcast(dlr, j);
+                const float4 b4 = *reinterpret_cast<const float4*>(&bcs[tb + j][4 * r]);
+                const float4 c4 = *reinterpret_cast<const float4*>(&bcs[tb + j][16 + 4 * r]);
+                const float Bv[4] = {b4.x, b4.y, b4.z, b4.w};
+                const float Cv[4] = {c4.x, c4.y, c4.z, c4.w};
+                float yp = 0.f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    h[k] = fmaf(fexp2(cn[k] * dl), h[k], Bv[k] * xv);
+                    yp = fmaf(Cv[k], h[k], yp);
+                }
+                ypart[j] = yp;
+            }
+            float yk = quad_sum_transposed(ypart, r);  // y of step s0 + r
+            if constexpr (GATE) yk *= zr * sigmoid_f(zr);
+            if (v) stf(Y, (bb * p.T + s0 + r) * p.D + d, yk);
+        }
     }
 }
 
@@ -1517,14 +1794,20 @@ template <typename TI, bool SP, bool GATE, bool N16>
 hipError_t forward_impl(const ScanProblem& p, hipStream_t s) {
     {
         SSMK_TIMED("chunk_aggr", s);
-        hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, N16, 8>), aggr_grid(p), dim3(64), 0, s, p);
+        if (aggr_quad(p))
+            hipLaunchKernelGGL((k_chunk_aggr_quad<TI, SP, GATE, false, 8>), aggr_grid(p), dim3(256), 0, s, p);
+        else
+            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, false, N16, 8>), aggr_grid(p), dim3(64), 0, s, p);
     }
     {
         SSMK_TIMED("carry", s);
         hipLaunchKernelGGL(k_carry, carry_grid(p), dim3(256), 0, s, p);
     }
     SSMK_TIMED("forward", s);
-    hipLaunchKernelGGL((k_forward<TI, SP, GATE, N16>), aggr_grid(p), dim3(64), 0, s, p);
+    if (aggr_quad(p))
+        hipLaunchKernelGGL((k_forward_quad<TI, SP, GATE>), aggr_grid(p), dim3(256), 0, s, p);
+    else
+        hipLaunchKernelGGL((k_forward<TI, SP, GATE, N16>), aggr_grid(p), dim3(64), 0, s, p);
     return hipGetLastError();
 }
 
@@ -1555,10 +1838,14 @@ hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
     if (p.only16 && !p.dx16) return hipErrorInvalidValue;
     {
         SSMK_TIMED("chunk_aggr", s);
-        if (p.seg == 16)
-            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16, 16>), aggr_grid(p), dim3(64), 0, s, p);
-        else
-            hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16, 8>), aggr_grid(p), dim3(64), 0, s, p);
+        const bool quad = aggr_quad(p);
+        if (p.seg == 16) {
+            if (quad) hipLaunchKernelGGL((k_chunk_aggr_quad<TI, SP, GATE, true, 16>), aggr_grid(p), dim3(256), 0, s, p);
+            else hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16, 16>), aggr_grid(p), dim3(64), 0, s, p);
+        } else {
+            if (quad) hipLaunchKernelGGL((k_chunk_aggr_quad<TI, SP, GATE, true, 8>), aggr_grid(p), dim3(256), 0, s, p);
+            else hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16, 8>), aggr_grid(p), dim3(64), 0, s, p);
+        }
     }
     {
         SSMK_TIMED("carry", s);
