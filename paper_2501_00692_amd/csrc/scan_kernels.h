@@ -1,17 +1,21 @@
 // scan_kernels.h -- gfx950 kernels for the selective diagonal SSM layer:
 //   k_chunk_aggr : per carry chunk, the local end state (from a zero carry-in),
-//                  the local adjoint aggregate and the chunk sum of Delta;
+//                  the local adjoint aggregate and the chunk sum of Delta
+//                  (k_chunk_aggr_quad for small grids);
 //   k_carry      : sequential scan of the chunk aggregates (forward state
 //                  carries, reverse adjoint carries, prefix sums of Delta);
-//   k_forward    : forward recurrence from the carries, writes y;
+//   k_forward    : forward recurrence from the carries, writes y
+//                  (k_forward_quad for small grids);
 //   k_grad       : fused reverse adjoint scan with the vjp epilogue (Prop. 2),
 //                  and the truncated window of Eq. "capped";
 //   k_reduce_*   : deterministic reductions of the dB/dC and dA_log partials.
 //
 // Thread layouts: the chunk-aggregate and forward kernels give each lane one
-// channel with all of its states in registers; the fused gradient kernel gives a
-// wave 16 channels, the 4 lanes of a quad sharing a channel and holding 4 of its
-// 16 states each, so per-channel sums over the state are two DPP quad swaps.
+// channel with all of its states in registers, B_t and C_t being scalar operands
+// (their _quad forms, for grids too small to hide latency that way, and the fused
+// gradient kernel give a wave 16 channels, the 4 lanes of a quad sharing a channel
+// and holding 4 of its 16 states each, so per-channel sums over the state are two
+// DPP quad swaps).
 // Loads of x, Delta, dy, z are coalesced along the contiguous channel
 // dimension; B_t and C_t are the same for every channel.
 #pragma once
