@@ -1184,7 +1184,8 @@ __device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMI
 // or into its split's partial when nsplit > 1).  All orders are fixed.
 // ---------------------------------------------------------------------------
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK, int OUT>
-__global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_grad(const ScanProblem p) {
+// (256-step chunks fill the CU's LDS with one workgroup: one wave per SIMD)
+__global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu(S * NCK > 128 ? 1 : 2, 8))) void k_grad(const ScanProblem p) {
     constexpr int NW = kGradWaves;
     constexpr int NTH = 64 * NW;
     constexpr int L = S * NCK;
