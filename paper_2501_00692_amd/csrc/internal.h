@@ -99,7 +99,7 @@ struct ScanWorkspace {
 
 int64_t default_chunk();
 // Segment length of the fused gradient kernel for chunk length L.
-inline int grad_segment(int64_t L) { return L >= 256 ? 16 : 8; }
+inline int grad_segment(int64_t) { return 8; }
 inline int64_t padded_channels(int64_t D) { return (D + 63) / 64 * 64; }
 bool chunk_supported(int64_t L);
 void choose_split(int64_t nb, int64_t D, int64_t nc, int* nsplit, int* tiles_per_split);

@@ -182,11 +182,18 @@ struct ShiftedC {
         else if constexpr (BYTES == 8) return __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0);
         else return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
     }
-    // fp32 values of the lane's CPL states into w[j][n / 4][16 + n % 4] (the spare
-    // column of the wave's channel-sum rows): states 4r .. 4r+3 of step j end up at
-    // w[j][r][16 .. 19]
+    // fp32 values of the lane's CPL states: into w[j][n / 4][16 + n % 4] (the spare
+    // column of the wave's padded channel-sum rows; states 4r .. 4r+3 of step j end
+    // up at w[j][r][16 .. 19]), or into w[j][n ..] of the wave's own rows of shifted C
     static __device__ __forceinline__ void stage(const Raw& u, float (&w)[S][16][20], int lane) {
         const int j = lane / (16 / CPL), n0 = (lane % (16 / CPL)) * CPL;
+        put(u, &w[j][n0 / 4][16 + n0 % 4]);
+    }
+    static __device__ __forceinline__ void stage(const Raw& u, float (&w)[S][16], int lane) {
+        const int j = lane / (16 / CPL), n0 = (lane % (16 / CPL)) * CPL;
+        put(u, &w[j][n0]);
+    }
+    static __device__ __forceinline__ void put(const Raw& u, float* dst) {
         float v[CPL];
         if constexpr (sizeof(TI) == 2) {
 #pragma unroll
@@ -201,7 +208,6 @@ struct ShiftedC {
 #pragma unroll
             for (int i = 0; i < CPL; ++i) v[i] = __uint_as_float(u[i]);
         }
-        float* dst = &w[j][n0 / 4][16 + n0 % 4];
         if constexpr (CPL == 2) *reinterpret_cast<float2*>(dst) = make_float2(v[0], v[1]);
         else *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
     }
@@ -1184,16 +1190,22 @@ __device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMI
 // or into its split's partial when nsplit > 1).  All orders are fixed.
 // ---------------------------------------------------------------------------
 template <typename TI, bool SP, bool GATE, bool TRUNC, bool N16, int S, int NCK, int OUT>
-// (256-step chunks fill the CU's LDS with one workgroup: one wave per SIMD)
-__global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu(S * NCK > 128 ? 1 : 2, 8))) void k_grad(const ScanProblem p) {
+__global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu(2, 8))) void k_grad(const ScanProblem p) {
     constexpr int NW = kGradWaves;
     constexpr int NTH = 64 * NW;
     constexpr int L = S * NCK;
     constexpr int SPL = S / 4;  // steps each lane prepares per segment
     constexpr int NP = S * 16;  // (step, state) pairs of a segment
     static_assert(NP % 64 == 0 && NP <= NTH, "pair layout");
-    __shared__ BCStage<TI, L> bc;
-    __shared__ __attribute__((aligned(16))) float red[NW][S][16][20];  // per wave [step][state][channel]
+    // LDS per workgroup, two per CU: up to 128-step chunks 80 KB: the chunk's B and C,
+    // channel-sum rows padded to 20 (free of bank conflicts; the spare column holds
+    // the window-shifted C); longer chunks (RING) 76 KB: B and C in a ring of two
+    // segments refilled one segment ahead, unpadded rows, shifted C in rows of its own
+    // (at 128 steps the ring and the unpadded rows cost 10 %)
+    constexpr bool RING = L > 128;
+    __shared__ BCStage<TI, RING ? 2 * S : L> bc;
+    __shared__ __attribute__((aligned(16))) float red[NW][S][16][RING ? 16 : 20];  // per wave [step][state][channel]
+    __shared__ __attribute__((aligned(16))) float csh[(RING && TRUNC && N16) ? NW : 1][S][16];  // per wave: shifted C
     __shared__ float wsum[4][NW][NP];  // per-wave channel sums: (dC, dB) of a segment, two segments alternating
     __shared__ float acc[L][32];       // chunk totals: dB in columns 0..15, dC in 16..31
     const int tid = threadIdx.x;
@@ -1251,8 +1263,44 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
         const_cast<TI*>(static_cast<const TI*>(p.C) + (bb * p.T + min(t0 + p.tbar, p.T)) * 16), 0,
         static_cast<int>(c_rows * 16 * static_cast<int64_t>(sizeof(TI))), 0x00020000);
 
+    // The ring's rows of segment qs (in-chunk steps qs*S ..) go to slot qs & 1: each
+    // thread fetches its raw element bits one segment ahead and writes them (masked)
+    // before the barrier that ends the segment (NCK is even, so the first segment of
+    // the next tile, NCK - 1, follows segment 0 in the other slot).
+    constexpr int BPT = (S * 32 + NTH - 1) / NTH;
+    typename RawIn<TI, 1>::Bits bcv[BPT];
+    auto bc_ok = [&](int qs, int e) {
+        const int i = tid + NTH * e, n = i & 15;
+        return i < S * 32 && t0 + qs * S + (i >> 5) < p.T && n < p.N;
+    };
+    auto bc_fetch = [&](int qs) {
+        const TI* Bp = static_cast<const TI*>(p.B);
+        const TI* Cp = static_cast<const TI*>(p.C);
+#pragma unroll
+        for (int e = 0; e < BPT; ++e) {
+            const int i = tid + NTH * e;
+            bcv[e] = ldbits((i & 31) < 16 ? Bp : Cp,
+                            bc_ok(qs, e) ? (bb * p.T + t0 + qs * S + (i >> 5)) * p.N + (i & 15) : 0);
+        }
+    };
+    auto bc_put = [&](int qs) {
+#pragma unroll
+        for (int e = 0; e < BPT; ++e) {
+            const int i = tid + NTH * e;
+            const uint32_t b = sizeof(TI) == 2 ? static_cast<uint32_t>(bcv[e]) << 16 : static_cast<uint32_t>(bcv[e]);
+            if ((S * 32) % NTH == 0 || i < S * 32)
+                bc.w[(qs & 1) * S + (i >> 5)][i & 31] = __uint_as_float(bc_ok(qs, e) ? b : 0u);
+        }
+    };
+    static_assert(!RING || NCK % 2 == 0, "the ring alternates slots across tiles");
+
     for (int i = tid; i < L * 32; i += NTH) (&acc[0][0])[i] = 0.f;
-    bc.template load<NTH>(p, bb, t0, tid);
+    if constexpr (RING) {
+        bc_fetch(NCK - 1);  // the first segment the tiles run
+        bc_put(NCK - 1);
+    } else {
+        bc.template load<NTH>(p, bb, t0, tid);
+    }
     __syncthreads();
 
     int pair = 0;
@@ -1524,7 +1572,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             for (int jj = 0; jj < SPL; ++jj) yk[jj] = 0.f;
             // B and C are read from LDS one step ahead of their use
             float Bn[4], Cn[4];
-            bc.get(q * S, r, Bn, Cn);
+            const int brow = RING ? (q & 1) * S : q * S;  // the segment's first staged row
+            bc.get(brow, r, Bn, Cn);
 #pragma unroll
             for (int j = 0; j < S; ++j) {
                 const int tl = q * S + j;
@@ -1537,7 +1586,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     Bv[k] = Bn[k];
                     Cv[k] = Cn[k];
                 }
-                if (j + 1 < S) bc.get(tl + 1, r, Bn, Cn);
+                if (j + 1 < S) bc.get(brow + j + 1, r, Bn, Cn);
                 float yp = 0.f;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
@@ -1568,7 +1617,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             }
             wave_sums(2 * pair);  // dC
             if constexpr (TRUNC && N16) {
-                SC::stage(curc, red[wave], lane);
+                if constexpr (RING) SC::stage(curc, csh[wave], lane);
+                else SC::stage(curc, red[wave], lane);
                 wave_lds_sync();
             }
 
@@ -1579,7 +1629,8 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
             // the tile's sum: the rounding of the sequential sum grows with S + L/S
             // terms instead of L
             float dAs[4] = {0.f, 0.f, 0.f, 0.f};
-            bc.get(q * S + S - 1, r, Bn, Cn);
+            if constexpr (RING) bc_fetch(q > 0 ? q - 1 : NCK - 1);  // the next segment's B and C
+            bc.get(brow + S - 1, r, Bn, Cn);
 #pragma unroll
             for (int j = S - 1; j >= 0; --j) {
                 const int tl = q * S + j;
@@ -1589,7 +1640,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     Bv[k] = Bn[k];
                     Cv[k] = Cn[k];
                 }
-                if (j > 0) bc.get(tl - 1, r, Bn, Cn);
+                if (j > 0) bc.get(brow + j - 1, r, Bn, Cn);
                 float mb[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) mb[k] = fmaf(gh[j], Cv[k], Mp[k]);
@@ -1600,7 +1651,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
                     const float gp = quad_bcast(gps[j >> 2], j & 3);
                     float Cs[4];
                     if constexpr (N16) {
-                        const float4 c4 = *reinterpret_cast<const float4*>(&red[wave][j][r][16]);
+                        const float4 c4 = *reinterpret_cast<const float4*>(RING ? &csh[wave][j][4 * r] : &red[wave][j][r][16]);
                         Cs[0] = c4.x; Cs[1] = c4.y; Cs[2] = c4.z; Cs[3] = c4.w;
                     } else {
                         ld4<TI, N16>(static_cast<const TI*>(p.C), bb * p.T + ps, r, p.N, pv, Cs);
@@ -1646,6 +1697,7 @@ __global__ __launch_bounds__(64 * kGradWaves) __attribute__((amdgpu_waves_per_eu
 #pragma unroll
             for (int k = 0; k < 4; ++k) dA[k] += dAs[k];
             wave_sums(2 * pair + 1);  // dB
+            if constexpr (RING) bc_put(q > 0 ? q - 1 : NCK - 1);
             flush(q);
         }
 #pragma unroll
@@ -1844,13 +1896,10 @@ hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
     {
         SSMK_TIMED("chunk_aggr", s);
         const bool quad = aggr_quad(p);
-        if (p.seg == 16) {
-            if (quad) hipLaunchKernelGGL((k_chunk_aggr_quad<TI, SP, GATE, true, 16>), aggr_grid(p), dim3(256), 0, s, p);
-            else hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16, 16>), aggr_grid(p), dim3(64), 0, s, p);
-        } else {
-            if (quad) hipLaunchKernelGGL((k_chunk_aggr_quad<TI, SP, GATE, true, 8>), aggr_grid(p), dim3(256), 0, s, p);
-            else hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16, 8>), aggr_grid(p), dim3(64), 0, s, p);
-        }
+        // records every 8 steps at every chunk length
+        if (p.seg != 8) return hipErrorInvalidValue;
+        if (quad) hipLaunchKernelGGL((k_chunk_aggr_quad<TI, SP, GATE, true, 8>), aggr_grid(p), dim3(256), 0, s, p);
+        else hipLaunchKernelGGL((k_chunk_aggr<TI, SP, GATE, true, N16, 8>), aggr_grid(p), dim3(64), 0, s, p);
     }
     {
         SSMK_TIMED("carry", s);
@@ -1861,7 +1910,7 @@ hipError_t grad_impl(const ScanProblem& p, hipStream_t s) {
         case 32: grad_main<TI, SP, GATE, TRUNC, N16, 8, 4>(p, s); break;
         case 64: grad_main<TI, SP, GATE, TRUNC, N16, 8, 8>(p, s); break;
         case 128: grad_main<TI, SP, GATE, TRUNC, N16, 8, 16>(p, s); break;
-        default: grad_main<TI, SP, GATE, TRUNC, N16, 16, 16>(p, s); break;  // 256
+        default: grad_main<TI, SP, GATE, TRUNC, N16, 8, 32>(p, s); break;  // 256
     }
     SSMK_TIMED("reduce", s);
     const int nbc = p.nsplit > 1 ? static_cast<int>(cdiv(p.nb * p.T * p.N, 256)) : 0;
