@@ -5,8 +5,9 @@ quad layout, which the other small-size tests cover.  Chunks of 16 steps let
 T = 32,768 steps and 64 channels reach that size at a cost the oracle finishes
 in seconds.  Cases: fp32 and bf16 inputs; 16 states (wide scalar loads of B and
 C) and fewer (per-state scalar loads, odd element offsets in bf16); gate and
-softplus; the scalar decay and the step-size-scaled input; a ragged last chunk
-with padding channels; full and truncated gradients; the forward output."""
+softplus; the scalar decay and the step-size-scaled input; ragged last chunks
+(11 steps, and 2: shorter than a group of 4) with padding channels; full and
+truncated gradients; the forward output."""
 import pytest
 import torch
 
@@ -24,7 +25,8 @@ F32 = Workload("lanes_f32", 1, 32768, 64, 16, 64, 100, False, False, 692301, del
 # ragged: T ends inside a chunk and its last group, 60 channels end inside the block
 RAGGED = Workload("lanes_ragged", 1, 32763, 60, 12, 60, 100, False, False, 692302, delta_scale=0.25)
 BF16 = Workload("lanes_bf16", 1, 32768, 64, 16, 64, 300, True, True, 692303)
-BF16_N7 = Workload("lanes_bf16_n7", 1, 32761, 64, 7, 64, 300, True, True, 692304)
+# the last chunk has 2 steps: no whole 4-step group, only the per-step tail
+BF16_N7 = Workload("lanes_bf16_n7", 1, 32754, 64, 7, 64, 300, True, True, 692304)
 
 
 def _waves(w):
